@@ -1,0 +1,265 @@
+"""CPU oracle for the HUGE embedding training step (test infrastructure only).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the benchmark's CPU
+baseline may import this module.  It loads ``liboracle.so`` built from
+``huge_oracle.c`` with gcc (no GPU code, nothing shared with the product
+library) and adds numpy glue:
+
+* :func:`step_dense`   -- one synchronous SGD step on whole float32 tables;
+* :func:`step_sparse`  -- the same step on the rows a batch touches only, with
+  every other row left at its initial value.  Tables too large for host memory
+  (up to 1e8 x 128 floats) are represented by the rows the batch reads; each
+  such row is produced by the oracle's own initialiser, so nothing here reads
+  the GPU's tables.
+
+Readings and formulas are stated in the header of ``huge_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "huge_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_u32p = ctypes.POINTER(ctypes.c_uint32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_f32p = ctypes.POINTER(ctypes.c_float)
+_f64p = ctypes.POINTER(ctypes.c_double)
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (plain -O2, no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=gnu99", "-fPIC", "-shared", "-ffp-contract=off",
+               "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        L = ctypes.CDLL(_LIB)
+        L.oracle_philox4x32_10.argtypes = [_u32p, _u32p, _u32p]
+        L.oracle_philox4x32_10.restype = None
+        L.oracle_init_value.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int64,
+                                        ctypes.c_int32, ctypes.c_float]
+        L.oracle_init_value.restype = ctypes.c_float
+        L.oracle_init_rows.argtypes = [ctypes.c_uint64, ctypes.c_int32, _i64p, ctypes.c_int64,
+                                       ctypes.c_int32, ctypes.c_float, _f32p]
+        L.oracle_build_alias.argtypes = [_f64p, ctypes.c_int64, _u32p, _i32p]
+        L.oracle_sample_negative.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32,
+                                             ctypes.c_int64, _u32p, _i32p]
+        L.oracle_sample_negative.restype = ctypes.c_int64
+        L.oracle_sample_negatives.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64,
+                                              ctypes.c_int32, ctypes.c_int64, _u32p, _i32p, _i32p]
+        grad_args = [_f64p, _f64p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                     ctypes.c_int64, ctypes.c_int32, _i32p, _i32p, _i32p, _i32p]
+        L.oracle_sgns_grad_d.argtypes = grad_args + [_f64p, _f64p, _f64p]
+        L.oracle_sgns_loss_d.argtypes = grad_args + [_f64p]
+        f_args = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                  ctypes.c_int64, ctypes.c_int32, _i32p, _i32p, _i32p, _i32p]
+        L.oracle_sgns_step.argtypes = f_args + [ctypes.c_float, _f64p]
+        L.oracle_sgns_loss.argtypes = f_args + [_f64p]
+        for name in ("oracle_init_rows", "oracle_build_alias", "oracle_sample_negatives",
+                     "oracle_sgns_grad_d", "oracle_sgns_loss_d", "oracle_sgns_step",
+                     "oracle_sgns_loss"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _ptr(a: np.ndarray, t):
+    if a is None:
+        return None
+    return a.ctypes.data_as(t)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise OracleError(f"{what} failed with code {rc}")
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _as_neg(neg, n):
+    neg = _c(neg, np.int32)
+    if neg.ndim == 2:
+        return neg
+    return neg.reshape(n, -1)
+
+
+# --------------------------------------------------------------------------- #
+# Random numbers
+# --------------------------------------------------------------------------- #
+def philox4x32_10(ctr, key) -> np.ndarray:
+    c = _c(ctr, np.uint32)
+    k = _c(key, np.uint32)
+    out = np.zeros(4, np.uint32)
+    lib().oracle_philox4x32_10(_ptr(c, _u32p), _ptr(k, _u32p), _ptr(out, _u32p))
+    return out
+
+
+def init_value(seed: int, table: int, row: int, col: int, half_width: float) -> float:
+    return float(lib().oracle_init_value(seed, table, row, col, half_width))
+
+
+def init_rows(seed: int, table: int, rows, dim: int, half_width: float) -> np.ndarray:
+    r = _c(rows, np.int64)
+    out = np.empty((r.size, dim), np.float32)
+    _check(lib().oracle_init_rows(seed, table, _ptr(r, _i64p), r.size, dim, half_width,
+                                  _ptr(out, _f32p)), "init_rows")
+    return out
+
+
+def build_alias(weights):
+    w = _c(weights, np.float64)
+    thr = np.empty(w.size, np.uint32)
+    alias = np.empty(w.size, np.int32)
+    _check(lib().oracle_build_alias(_ptr(w, _f64p), w.size, _ptr(thr, _u32p),
+                                    _ptr(alias, _i32p)), "build_alias")
+    return thr, alias
+
+
+def sample_negatives(seed: int, first_pos: int, n: int, num_neg: int, num_nodes: int,
+                     thr=None, alias=None) -> np.ndarray:
+    out = np.empty((n, num_neg), np.int32)
+    t = None if thr is None else _c(thr, np.uint32)
+    a = None if alias is None else _c(alias, np.int32)
+    _check(lib().oracle_sample_negatives(seed, first_pos, n, num_neg, num_nodes,
+                                         _ptr(t, _u32p), _ptr(a, _i32p), _ptr(out, _i32p)),
+           "sample_negatives")
+    return out
+
+
+# --------------------------------------------------------------------------- #
+# Loss, gradient and step
+# --------------------------------------------------------------------------- #
+def grad_d(S, T, src, dst, cc, neg):
+    """Loss and gradients in double on double tables (finite-difference pins)."""
+    S = _c(S, np.float64)
+    T = _c(T, np.float64)
+    src, dst, cc = _c(src, np.int32), _c(dst, np.int32), _c(cc, np.int32)
+    neg = _c(neg, np.int32)
+    n, K = neg.shape
+    gS = np.empty_like(S)
+    gT = np.empty_like(T)
+    loss = ctypes.c_double()
+    _check(lib().oracle_sgns_grad_d(_ptr(S, _f64p), _ptr(T, _f64p), S.shape[0], T.shape[0],
+                                    S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
+                                    _ptr(cc, _i32p), _ptr(neg, _i32p), _ptr(gS, _f64p),
+                                    _ptr(gT, _f64p), ctypes.byref(loss)), "sgns_grad_d")
+    return loss.value, gS, gT
+
+
+def loss_d(S, T, src, dst, cc, neg) -> float:
+    S = _c(S, np.float64)
+    T = _c(T, np.float64)
+    src, dst, cc = _c(src, np.int32), _c(dst, np.int32), _c(cc, np.int32)
+    neg = _c(neg, np.int32)
+    n, K = neg.shape
+    loss = ctypes.c_double()
+    _check(lib().oracle_sgns_loss_d(_ptr(S, _f64p), _ptr(T, _f64p), S.shape[0], T.shape[0],
+                                    S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
+                                    _ptr(cc, _i32p), _ptr(neg, _i32p), ctypes.byref(loss)),
+           "sgns_loss_d")
+    return loss.value
+
+
+def step_dense(S: np.ndarray, T: np.ndarray, src, dst, cc, neg, lr: float) -> float:
+    """One step in place on float32 tables S, T (C-contiguous); returns the loss sum."""
+    assert S.dtype == np.float32 and T.dtype == np.float32
+    assert S.flags.c_contiguous and T.flags.c_contiguous
+    src, dst, cc = _c(src, np.int32), _c(dst, np.int32), _c(cc, np.int32)
+    neg = _as_neg(neg, len(src))
+    n, K = neg.shape
+    loss = ctypes.c_double()
+    _check(lib().oracle_sgns_step(_ptr(S, _f32p), _ptr(T, _f32p), S.shape[0], T.shape[0],
+                                  S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
+                                  _ptr(cc, _i32p), _ptr(neg, _i32p), lr, ctypes.byref(loss)),
+           "sgns_step")
+    return loss.value
+
+
+def loss_dense(S: np.ndarray, T: np.ndarray, src, dst, cc, neg) -> float:
+    S = _c(S, np.float32)
+    T = _c(T, np.float32)
+    src, dst, cc = _c(src, np.int32), _c(dst, np.int32), _c(cc, np.int32)
+    neg = _as_neg(neg, len(src))
+    n, K = neg.shape
+    loss = ctypes.c_double()
+    _check(lib().oracle_sgns_loss(_ptr(S, _f32p), _ptr(T, _f32p), S.shape[0], T.shape[0],
+                                  S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
+                                  _ptr(cc, _i32p), _ptr(neg, _i32p), ctypes.byref(loss)),
+           "sgns_loss")
+    return loss.value
+
+
+@dataclass
+class SparseStep:
+    """Result of :func:`step_sparse`: post-step values of every touched row."""
+    rows_S: np.ndarray      # int64 ascending ids of touched source-table rows
+    S: np.ndarray           # float32 (len(rows_S), dim), post-step
+    rows_T: np.ndarray      # int64 ascending ids of touched context-table rows
+    T: np.ndarray           # float32 (len(rows_T), dim), post-step
+    loss: float             # loss sum over the batch, at pre-step values
+    neg: np.ndarray         # int32 (n, K) negatives used
+
+
+def step_sparse(seed: int, num_nodes: int, dim: int, num_neg: int, half_width: float,
+                src, dst, cc, first_pos: int, lr: float, thr=None, alias=None,
+                pre_S=None, pre_T=None) -> SparseStep:
+    """One step from freshly initialised tables, holding only the touched rows.
+
+    The oracle draws the negatives itself, gathers the ids the batch touches,
+    materialises those rows with its own initialiser (or takes them from
+    ``pre_S``/``pre_T``: dicts id -> float32 row produced by earlier oracle
+    steps), relabels ids to positions in that compact set and runs the dense
+    step on it.  Relabelling changes no arithmetic: the per-row accumulation
+    order is still positive index, then slot.
+    """
+    src = _c(src, np.int32)
+    dst = _c(dst, np.int32)
+    cc = _c(cc, np.int32)
+    n = src.size
+    neg = sample_negatives(seed, first_pos, n, num_neg, num_nodes, thr, alias)
+    if n and (src.min() < 0 or src.max() >= num_nodes or dst.min() < 0
+              or dst.max() >= num_nodes):
+        raise OracleError("id out of range")
+    rows_S = np.unique(src.astype(np.int64))
+    rows_T = np.unique(np.concatenate([dst.astype(np.int64), neg.reshape(-1).astype(np.int64)]))
+    S = init_rows(seed, 0, rows_S, dim, half_width)
+    T = init_rows(seed, 1, rows_T, dim, half_width)
+    if pre_S:
+        for j, r in enumerate(rows_S):
+            if int(r) in pre_S:
+                S[j] = pre_S[int(r)]
+    if pre_T:
+        for j, r in enumerate(rows_T):
+            if int(r) in pre_T:
+                T[j] = pre_T[int(r)]
+    src_c = np.searchsorted(rows_S, src).astype(np.int32)
+    dst_c = np.searchsorted(rows_T, dst).astype(np.int32)
+    neg_c = np.searchsorted(rows_T, neg.reshape(-1)).astype(np.int32).reshape(n, num_neg)
+    loss = step_dense(S, T, src_c, dst_c, cc, neg_c, lr)
+    return SparseStep(rows_S, S, rows_T, T, loss, neg)
