@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Benchmark of the HUGE training step on one MI355X.
+
+One "step" is one synchronous SGD step of skip-gram negative sampling over a
+batch of (source_id, destination_id, co_counts) triples: sampling, grouping,
+gather, loss, update.  Default workload: the 100M-node SBM (two 1e8 x 128
+fp32 tables, 102.4 GB resident; 5 uniform negatives; 262,144 positives per
+step), inputs pre-staged in HBM before the timed region.
+
+Prints one JSON line with the throughput (positives per second), the
+roofline of the dominant kernel (the fused gather/loss/update kernel, timed
+with HIP events inside the timed steps on the stream it runs on), and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "positive (src,dst) pairs/sec per train step; achieved HBM GB/s vs peak"
+HBM_PEAK_GBPS = 8000.0
+KERNEL = "k_fused_step"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "fused_step_sbm100m_counters.txt")
+KERNEL_SOURCES = ["paper_2307_14490_amd/csrc/k_step.hip", "paper_2307_14490_amd/csrc/device.hpp"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload: str, n_launch_units: float):
+    """HBM bytes per launch of the fused kernel from committed rocprofv3
+    counters, if they were taken on the current kernel source."""
+    if workload != "sbm100m" or not os.path.exists(COUNTERS_FILE):
+        return None
+    kv = {}
+    with open(COUNTERS_FILE) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, seed, budget_s=15.0, max_batches=8):
+    """The CPU oracle on a bounded sample: whole batches of the same workload
+    (negatives drawn, touched rows initialised, one step) until budget_s."""
+    import numpy as np
+    from oracle import oracle as orc
+    cfg = wl.cfg
+    thr = alias = None
+    if cfg.neg_kind == "alias":
+        thr, alias = orc.build_alias(wl.weights)
+    a = float(np.float32(cfg.init_half_width))
+    done = 0
+    t_total = 0.0
+    b = 0
+    while b < max_batches and (t_total < budget_s or b == 0):
+        src, dst, cc = wl.batch(b)
+        t0 = time.perf_counter()
+        orc.step_sparse(seed, cfg.num_nodes, cfg.dim, cfg.num_neg, a, src, dst, cc,
+                        b * cfg.batch, cfg.lr, thr, alias)
+        t_total += time.perf_counter() - t0
+        done += src.size
+        b += 1
+    return {
+        "value": done / t_total,
+        "unit": "positives/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{b} batch(es) of {cfg.batch} positives of the {cfg.name} workload, "
+                  f"one step each from initial values (negative draws, touched-row init, "
+                  f"double-precision step), {t_total:.1f} s single-threaded",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="sbm100m")
+    ap.add_argument("--scatter", default="sorted", choices=["sorted", "atomic"])
+    ap.add_argument("--batches", type=int, default=16, help="distinct pre-staged batches")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the step keeps both tables resident in one "
+              "MI355X's HBM and has no multi-GPU path; run it with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2307_14490_amd as P
+    from synth import make_workload
+
+    def log(*a):
+        print(*a, file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload, args.seed)
+    cfg = wl.cfg
+    R = max(1, min(args.batches, args.steps + args.warmup))
+    t0 = time.time()
+    host_batches = [wl.batch(b) for b in range(R)]
+    log(f"[bench] {cfg.name}: {R} batches of {cfg.batch} generated in {time.time() - t0:.1f}s")
+    dev_batches = [tuple(torch.from_numpy(x).cuda() for x in b) for b in host_batches]
+
+    tr = P.Trainer(cfg.num_nodes, cfg.dim, cfg.num_neg, cfg.batch, seed=args.seed,
+                   alias_weights=wl.weights, scatter=args.scatter)
+    torch.cuda.synchronize()
+    log(f"[bench] tables initialised: 2 x {cfg.num_nodes} x {cfg.dim} fp32")
+    n = cfg.batch
+    K = cfg.num_neg
+    D = cfg.dim
+    stream = torch.cuda.current_stream()
+
+    # Warm-up; also collects each staged batch's distinct-row counts.
+    per_batch_stats = {}
+    pos = 0
+    for w in range(args.warmup):
+        b = w % R
+        s, d, c = dev_batches[b]
+        tr.step_no_loss(s, d, c, pos, cfg.lr)
+        pos += n
+        if args.scatter == "sorted" and b not in per_batch_stats:
+            per_batch_stats[b] = tr.stats()
+    if args.scatter == "sorted":
+        for b in range(R):
+            if b not in per_batch_stats:
+                s, d, c = dev_batches[b]
+                tr.step_no_loss(s, d, c, pos, cfg.lr)
+                pos += n
+                per_batch_stats[b] = tr.stats()
+    if tr.check() != 0:
+        raise RuntimeError("device reported an error during warm-up")
+    log("[bench] warm-up done")
+
+    # Timed region: exactly K steps, phase events recorded inside the library.
+    tr.profile_begin(args.steps)
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for k in range(args.steps):
+        s, d, c = dev_batches[(args.warmup + k) % R]
+        tr.step_no_loss(s, d, c, pos, cfg.lr)
+        pos += n
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    phase_ms, prof_steps = tr.profile_end()
+    if tr.check() != 0:
+        raise RuntimeError("device reported an error in the timed steps")
+    ms_per_step = total_ms / args.steps
+    value = n * args.steps / (total_ms / 1e3)
+    log(f"[bench] {args.steps} steps in {total_ms:.2f} ms: {ms_per_step:.4f} ms/step")
+
+    # Algorithmic bytes of the fused kernel per launch: the batch (12 B per
+    # positive), each distinct row read once (4 D bytes) and each row that
+    # occurs once written once in place.  Repeated rows are written by the
+    # duplicate kernels, not counted here.
+    phases = ["setup_sample", "sort", "mark", "fused_step", "repeated_rows", "loss"]
+    phase_avg_us = {p: phase_ms[i] / max(prof_steps, 1) * 1e3 for i, p in enumerate(phases)}
+    fused_us = phase_avg_us["fused_step"] if args.scatter == "sorted" else phase_avg_us["sort"]
+    if args.scatter == "sorted":
+        seq = [(args.warmup + k) % R for k in range(args.steps)]
+        uS = np.mean([per_batch_stats[b][0] for b in seq])
+        uT = np.mean([per_batch_stats[b][1] for b in seq])
+        dup = np.mean([per_batch_stats[b][2] for b in seq])
+        occ = n * (2 + K)
+        kernel_bytes = 12.0 * n + 4.0 * D * (uS + uT) + 4.0 * D * (occ - dup)
+        step_bytes = 12.0 * n + 8.0 * D * (uS + uT)
+    else:
+        uS = uT = dup = None
+        kernel_bytes = 12.0 * n + 4.0 * D * n * (2 + K)  # gather kernel: every row read
+        step_bytes = 12.0 * n + 8.0 * D * n * (2 + K)
+    achieved = kernel_bytes / (fused_us * 1e-6) / 1e9
+    traffic = read_traffic(cfg.name, n)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "positives/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name,
+            "num_nodes": cfg.num_nodes,
+            "dim": D,
+            "num_neg_per_pos": K,
+            "batch": n,
+            "negatives": cfg.neg_kind,
+            "scatter": args.scatter,
+            "lr": cfg.lr,
+            "staged_batches": R,
+        },
+        "roofline": {
+            "kernel": KERNEL if args.scatter == "sorted" else "k_atomic_gather",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "avg_kernel_us": fused_us,
+            "alg_bytes_per_launch": kernel_bytes,
+        },
+        "step": {
+            "alg_bytes": step_bytes,
+            "alg_GBps": step_bytes / (ms_per_step * 1e-3) / 1e9,
+            "phase_avg_us": phase_avg_us,
+            "unique_src_rows": uS,
+            "unique_ctx_rows": uT,
+            "repeated_row_occurrences": dup,
+        },
+    }
+    tr.close()
+    del tr, dev_batches
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        log("[bench] timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(wl, args.seed, budget_s=args.cpu_budget)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

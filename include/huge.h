@@ -1,0 +1,183 @@
+/*
+ * huge.h -- C ABI of libhuge, the MI355X (gfx950) training step of HUGE
+ * ("HUGE: Huge Unsupervised Graph Embeddings with TPUs", KDD'23).
+ *
+ * The library trains DeepWalk-style graph embeddings by skip-gram negative
+ * sampling (Sec. 2.2) on batches of the (source_id, destination_id, co_counts)
+ * triples produced by the random-walk sampler (Sec. 3.2).  Per step it
+ * replicates each source, draws negatives (Sec. 3.3.2), gathers the rows of a
+ * source table S and a context table T, computes the co_counts-weighted
+ * sigmoid loss, aggregates the gradient of the whole batch and applies it to
+ * the tables with SGD (Sec. 3.3.2; Table 2).  Everything runs in hand-written
+ * HIP kernels on one GPU; both tables stay resident in HBM.
+ *
+ * The quantities computed (the paper names the loss parts but prints no
+ * formula; the reading used here is standard word2vec negative sampling):
+ *   x_i  = <S[u_i], T[v_i]>,  y_ik = <S[u_i], T[m_ik]>,  k < K
+ *   L    = sum_i c_i * ( softplus(-x_i) + sum_k softplus(y_ik) )
+ *   g_i  = c_i (sigmoid(x_i) - 1),  h_ik = c_i sigmoid(y_ik)
+ *   S[u] -= lr * sum_{i: u_i = u} ( g_i T[v_i] + sum_k h_ik T[m_ik] )
+ *   T[r] -= lr * ( sum_{i: v_i = r} g_i S[u_i] + sum_{(i,k): m_ik = r} h_ik S[u_i] )
+ * Every read uses pre-step values (one synchronous step); contributions to a
+ * row that appears several times in a batch are summed.
+ *
+ * Conventions
+ *   - Device pointers are HIP device memory of the current device; host
+ *     pointers are ordinary memory.  The caller owns every buffer; the
+ *     library owns only the small host-side handle.  Buffers must outlive
+ *     the handle, and batch arrays must stay valid until the step completes
+ *     on its stream.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     All calls are asynchronous on that stream except huge_check and
+ *     huge_step_stats, which synchronise it.  A handle is not thread-safe.
+ *   - Every function returns a huge_status (0 = success, negative = error)
+ *     and never aborts the process.  Argument errors are detected on the
+ *     host before any launch and leave every buffer untouched.
+ *   - Ids are int32 (N <= 2^31 - 1); row offsets are computed in 64 bits.
+ *   - Tables are fp32, row-major, N x D, contiguous.
+ */
+#ifndef HUGE_H
+#define HUGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t huge_status;
+#define HUGE_OK 0
+#define HUGE_ERR_INVALID_ARG (-1)     /* null pointer, bad size or config          */
+#define HUGE_ERR_ID_OUT_OF_RANGE (-2) /* a source/destination id outside [0, N)    */
+#define HUGE_ERR_BAD_COUNT (-3)       /* a negative co_count                       */
+#define HUGE_ERR_WORKSPACE (-4)       /* workspace smaller than huge_workspace_bytes */
+#define HUGE_ERR_HIP (-5)             /* a HIP runtime call failed                 */
+
+/* Negative distribution: uniform over the vocabulary (Sec. 3.3.2), or an
+   alias table over caller weights (e.g. degree^0.75). */
+#define HUGE_NEG_UNIFORM 0
+#define HUGE_NEG_ALIAS 1
+
+/* Gradient scatter: SORTED groups the rows of a batch by id (radix sort),
+   updates rows that occur once in place and sums repeated rows in occurrence
+   order -- bitwise reproducible run to run.  ATOMIC adds every contribution
+   with fp32 atomics into the tables after all reads -- same result up to the
+   order of summation, not reproducible bit for bit. */
+#define HUGE_SCATTER_SORTED 0
+#define HUGE_SCATTER_ATOMIC 1
+
+typedef struct huge_config {
+    int64_t num_nodes;       /* N: rows of each table, 1 .. 2^31-1                       */
+    int32_t dim;             /* D: floats per row, multiple of 4, 4 .. 1024              */
+    int32_t num_neg_per_pos; /* K: negatives per positive, 1 .. 64 (Sec. 3.3.2, Table 2) */
+    int64_t max_batch;       /* largest number of positives per call, >= 1               */
+    uint64_t seed;           /* Philox key for the initial tables and the negatives      */
+    float init_half_width;   /* a: initial values U[-a, a); 0 selects 0.5 / D            */
+    int32_t neg_kind;        /* HUGE_NEG_UNIFORM or HUGE_NEG_ALIAS                       */
+    int32_t scatter_kind;    /* HUGE_SCATTER_SORTED or HUGE_SCATTER_ATOMIC               */
+} huge_config;
+
+typedef struct huge_handle huge_handle; /* opaque, host-side */
+
+/* Bytes of device workspace a handle with this config needs (scratch for the
+   negatives, sort buffers, duplicate contributions, loss partials and
+   counters).  Returns 0 if the config is invalid. */
+size_t huge_workspace_bytes(const huge_config* cfg);
+
+/* Host-only, deterministic alias table for negative sampling (Walker; Vose)
+   in exact integer form: bucket j keeps mass W_j = trunc(w_j N 2^32 / sum w)
+   (the rounding residue goes to the largest bucket, lowest index on ties);
+   small buckets (W < 2^32) are filled from large ones in FIFO index order;
+   thr[j] is the 32-bit threshold below which a draw keeps j, alias[j] the
+   other outcome.  weights: n >= 1 finite non-negative doubles with a positive
+   sum; thr_out, alias_out: n entries, host memory.  The caller copies them
+   to device memory for huge_init_tables. */
+huge_status huge_build_alias(const double* weights, int64_t n, uint32_t* thr_out,
+                             int32_t* alias_out);
+
+/* Create a handle over caller-owned tables and fill both with the initial
+   values: element (r, c) of table t (0 = S, 1 = T) is j * (a 2^-23) with
+   j = (word >> 8) - 2^23 and word = word (c mod 4) of Philox4x32-10 on counter
+   (lo32 r, hi32 r, c div 4, 2 + t) under key (lo32 seed, hi32 seed): uniform
+   on [-a, a) (the paper does not state an initialisation).
+     d_S, d_T       : N x D fp32 device tables (written)
+     d_alias_thr,
+     d_alias        : N entries each on the device (HUGE_NEG_ALIAS), else NULL
+     d_workspace    : >= huge_workspace_bytes(cfg) bytes of device memory
+     out            : receives the handle; destroy with huge_destroy */
+huge_status huge_init_tables(const huge_config* cfg, float* d_S, float* d_T,
+                             const uint32_t* d_alias_thr, const int32_t* d_alias,
+                             void* d_workspace, size_t ws_bytes, void* stream,
+                             huge_handle** out);
+
+/* Same as huge_init_tables without writing the tables: for tables restored
+   from a checkpoint. */
+huge_status huge_attach_tables(const huge_config* cfg, float* d_S, float* d_T,
+                               const uint32_t* d_alias_thr, const int32_t* d_alias,
+                               void* d_workspace, size_t ws_bytes, huge_handle** out);
+
+/* One synchronous SGD step over n positives (Sec. 3.3.2; Table 2).
+     d_src, d_dst    : n int32 ids in [0, N) (source_id, destination_id)
+     d_cc            : n int32 co_counts >= 0, the weight of each positive
+     first_pos_index : global index p of the first positive; negative k of
+                       positive i is drawn from Philox counter
+                       (lo32 p+i, hi32 p+i, k, 1): j = floor(x N / 2^64) with
+                       x = (r1 << 32) | r0, and with an alias table the result
+                       is j if r2 < thr[j], else alias[j]
+     lr              : SGD learning rate
+     d_loss_sum      : device double receiving L at the pre-step values, or NULL
+   n = 0 is a no-op that writes 0 to *d_loss_sum.  Ids outside [0, N) or a
+   negative co_count make the whole step a no-op (no table is written, the
+   loss is NaN); huge_check then reports the error. */
+huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                            const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
+                            float lr, double* d_loss_sum, void* stream);
+
+/* L of a batch at the current tables, with the negatives huge_train_step
+   would draw for the same first_pos_index; writes nothing else. */
+huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                           const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
+                           double* d_loss_sum, void* stream);
+
+/* Copy rows of table (0 = S, 1 = T) into d_out (n x D fp32, row-major).
+   d_ids: n int64 device ids; an id outside [0, N) yields a row of NaN and
+   makes huge_check report HUGE_ERR_ID_OUT_OF_RANGE. */
+huge_status huge_get_rows(huge_handle* h, int32_t table, const int64_t* d_ids, int64_t n,
+                          float* d_out, void* stream);
+
+/* The negatives huge_train_step draws for n positives starting at
+   first_pos_index: d_neg_out receives n x K int32 (row i = positive i). */
+huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_index,
+                                  int32_t* d_neg_out, void* stream);
+
+/* Synchronise the stream; return and clear the first device-side error
+   (HUGE_ERR_ID_OUT_OF_RANGE or HUGE_ERR_BAD_COUNT) since the last check. */
+huge_status huge_check(huge_handle* h, void* stream);
+
+/* Synchronise the stream and report the last sorted step's row counts:
+   distinct source rows, distinct context rows, and occurrences that fell in
+   a repeated row (their contributions were summed before the update). */
+huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
+                            int64_t* unique_ctx, int64_t* dup_occurrences);
+
+/* Phase timing.  After huge_profile_begin(h, max_steps), each of the next
+   max_steps calls of huge_train_step records HIP events on its stream at the
+   phase boundaries.  huge_profile_end synchronises the stream, writes the
+   summed durations in milliseconds to phase_ms[HUGE_PHASES] and the number
+   of recorded steps to *steps, and releases the events.  Phases of the
+   sorted scatter: 0 set-up and negative sampling, 1 radix sort, 2 run
+   marking, 3 fused gather/loss/update kernel, 4 repeated rows, 5 loss sum.
+   Atomic scatter: 0 set-up and sampling, 1 gather and coefficients,
+   2 context-row atomics, 3 source-row atomics, 4 unused, 5 loss sum. */
+#define HUGE_PHASES 6
+huge_status huge_profile_begin(huge_handle* h, int32_t max_steps);
+huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int32_t* steps);
+
+void huge_destroy(huge_handle* h);
+const char* huge_status_string(huge_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HUGE_H */

@@ -105,12 +105,26 @@ float oracle_init_value(uint64_t seed, int32_t table, int64_t row, int32_t col,
     return v;
 }
 
+/* Whole rows: one Philox block serves the four columns 4q .. 4q+3. */
 int oracle_init_rows(uint64_t seed, int32_t table, const int64_t *rows, int64_t nrows,
                      int32_t dim, float half_width, float *out) {
     if (nrows < 0 || dim <= 0 || (nrows > 0 && (!rows || !out))) return OR_EINVAL;
-    for (int64_t r = 0; r < nrows; ++r)
-        for (int32_t c = 0; c < dim; ++c)
-            out[r * dim + c] = oracle_init_value(seed, table, rows[r], c, half_width);
+    uint32_t key[2], ctr[4], word[4];
+    seed_key(seed, key);
+    float scale = (float)ldexp((double)half_width, -23);
+    for (int64_t r = 0; r < nrows; ++r) {
+        for (int32_t q = 0; 4 * q < dim; ++q) {
+            ctr[0] = (uint32_t)((uint64_t)rows[r] & 0xFFFFFFFFu);
+            ctr[1] = (uint32_t)((uint64_t)rows[r] >> 32);
+            ctr[2] = (uint32_t)q;
+            ctr[3] = (uint32_t)(2 + table);
+            oracle_philox4x32_10(ctr, key, word);
+            for (int32_t w = 0; w < 4 && 4 * q + w < dim; ++w) {
+                int32_t j = (int32_t)(word[w] >> 8) - 8388608;
+                out[r * dim + 4 * q + w] = (float)j * scale;
+            }
+        }
+    }
     return OR_OK;
 }
 

@@ -1,0 +1,21 @@
+"""MI355X-native training step of HUGE (KDD'23): skip-gram negative sampling
+over (source_id, destination_id, co_counts) batches, in hand-written HIP
+kernels behind the C ABI of ``include/huge.h``.
+
+``binding`` is the ctypes layer; ``build`` compiles ``libhuge.so`` in-tree.
+"""
+from .binding import (  # noqa: F401
+    EXPORTED,
+    HUGE_NEG_ALIAS,
+    HUGE_NEG_UNIFORM,
+    HUGE_SCATTER_ATOMIC,
+    HUGE_SCATTER_SORTED,
+    HugeConfig,
+    HugeError,
+    Trainer,
+    build_alias,
+    load,
+    make_config,
+    status_string,
+    workspace_bytes,
+)

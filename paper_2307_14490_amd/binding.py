@@ -1,0 +1,248 @@
+"""ctypes binding of libhuge (argument marshalling only).
+
+Every call maps one-to-one onto a function of ``include/huge.h``; all work
+happens in the library's HIP kernels.  PyTorch provides device memory and the
+current HIP stream.  If ``libhuge.so`` has not been built, importing this
+module raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhuge.so")
+
+HUGE_OK = 0
+HUGE_ERR_INVALID_ARG = -1
+HUGE_ERR_ID_OUT_OF_RANGE = -2
+HUGE_ERR_BAD_COUNT = -3
+HUGE_ERR_WORKSPACE = -4
+HUGE_ERR_HIP = -5
+
+HUGE_NEG_UNIFORM = 0
+HUGE_NEG_ALIAS = 1
+HUGE_SCATTER_SORTED = 0
+HUGE_SCATTER_ATOMIC = 1
+
+EXPORTED = [
+    "huge_workspace_bytes", "huge_build_alias", "huge_init_tables", "huge_attach_tables",
+    "huge_train_step", "huge_eval_loss", "huge_get_rows", "huge_sample_negatives",
+    "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
+    "huge_destroy", "huge_status_string",
+]
+HUGE_PHASES = 6
+
+
+class HugeConfig(ctypes.Structure):
+    _fields_ = [
+        ("num_nodes", ctypes.c_int64),
+        ("dim", ctypes.c_int32),
+        ("num_neg_per_pos", ctypes.c_int32),
+        ("max_batch", ctypes.c_int64),
+        ("seed", ctypes.c_uint64),
+        ("init_half_width", ctypes.c_float),
+        ("neg_kind", ctypes.c_int32),
+        ("scatter_kind", ctypes.c_int32),
+    ]
+
+
+class HugeError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+_vp = ctypes.c_void_p
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libhuge.so; raise if it is missing (build it first)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run python -m paper_2307_14490_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    cfgp = ctypes.POINTER(HugeConfig)
+    L.huge_workspace_bytes.argtypes = [cfgp]
+    L.huge_workspace_bytes.restype = ctypes.c_size_t
+    L.huge_build_alias.argtypes = [_vp, ctypes.c_int64, _vp, _vp]
+    L.huge_init_tables.argtypes = [cfgp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp,
+                                   ctypes.POINTER(_vp)]
+    L.huge_attach_tables.argtypes = [cfgp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t,
+                                     ctypes.POINTER(_vp)]
+    L.huge_train_step.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64,
+                                  ctypes.c_float, _vp, _vp]
+    L.huge_eval_loss.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64, _vp, _vp]
+    L.huge_get_rows.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp]
+    L.huge_sample_negatives.argtypes = [_vp, ctypes.c_int64, ctypes.c_uint64, _vp, _vp]
+    L.huge_check.argtypes = [_vp, _vp]
+    L.huge_step_stats.argtypes = [_vp, _vp, ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
+    L.huge_profile_begin.argtypes = [_vp, ctypes.c_int32]
+    L.huge_profile_end.argtypes = [_vp, _vp, ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_int32)]
+    L.huge_destroy.argtypes = [_vp]
+    L.huge_destroy.restype = None
+    L.huge_status_string.argtypes = [ctypes.c_int32]
+    L.huge_status_string.restype = ctypes.c_char_p
+    for name in ("huge_build_alias", "huge_init_tables", "huge_attach_tables", "huge_train_step",
+                 "huge_eval_loss", "huge_get_rows", "huge_sample_negatives", "huge_check",
+                 "huge_step_stats", "huge_profile_begin", "huge_profile_end"):
+        getattr(L, name).restype = ctypes.c_int32
+    _lib = L
+    return L
+
+
+def status_string(st: int) -> str:
+    return load().huge_status_string(st).decode()
+
+
+def _ok(st: int, what: str):
+    if st != HUGE_OK:
+        raise HugeError(st, what)
+
+
+def make_config(num_nodes, dim, num_neg, max_batch, seed=0, init_half_width=0.0,
+                neg_kind=HUGE_NEG_UNIFORM, scatter_kind=HUGE_SCATTER_SORTED) -> HugeConfig:
+    return HugeConfig(int(num_nodes), int(dim), int(num_neg), int(max_batch), int(seed),
+                      float(init_half_width), int(neg_kind), int(scatter_kind))
+
+
+def workspace_bytes(cfg: HugeConfig) -> int:
+    return int(load().huge_workspace_bytes(ctypes.byref(cfg)))
+
+
+def build_alias(weights):
+    """Host alias table: returns (thr uint32[n], alias int32[n]) numpy arrays."""
+    w = np.ascontiguousarray(weights, dtype=np.float64)
+    thr = np.empty(w.size, np.uint32)
+    alias = np.empty(w.size, np.int32)
+    _ok(load().huge_build_alias(w.ctypes.data, w.size, thr.ctypes.data, alias.ctypes.data),
+        "huge_build_alias")
+    return thr, alias
+
+
+def _stream_ptr(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dptr(t):
+    return None if t is None else t.data_ptr()
+
+
+class Trainer:
+    """Tables, workspace and a libhuge handle on one GPU.
+
+    S and T are float32 torch tensors (N x D) on the device; the workspace is
+    a uint8 torch tensor.  Batches are int32 device tensors.
+    """
+
+    def __init__(self, num_nodes, dim, num_neg, max_batch, seed=0, init_half_width=0.0,
+                 alias_weights=None, scatter="sorted", device="cuda", tables=None,
+                 init=True):
+        import torch
+        load()
+        self.device = torch.device(device)
+        kind = HUGE_NEG_ALIAS if alias_weights is not None else HUGE_NEG_UNIFORM
+        sk = {"sorted": HUGE_SCATTER_SORTED, "atomic": HUGE_SCATTER_ATOMIC}[scatter]
+        self.cfg = make_config(num_nodes, dim, num_neg, max_batch, seed, init_half_width, kind, sk)
+        ws = workspace_bytes(self.cfg)
+        if ws == 0:
+            raise HugeError(HUGE_ERR_INVALID_ARG, "huge_workspace_bytes")
+        if tables is None:
+            self.S = torch.empty((num_nodes, dim), dtype=torch.float32, device=self.device)
+            self.T = torch.empty((num_nodes, dim), dtype=torch.float32, device=self.device)
+        else:
+            self.S, self.T = tables
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=self.device)
+        if kind == HUGE_NEG_ALIAS:
+            thr, alias = build_alias(alias_weights)
+            self.alias_thr = torch.from_numpy(thr.view(np.int32)).to(self.device)
+            self.alias = torch.from_numpy(alias).to(self.device)
+        else:
+            self.alias_thr = self.alias = None
+        self.loss_buf = torch.zeros(1, dtype=torch.float64, device=self.device)
+        h = _vp()
+        if init:
+            st = load().huge_init_tables(ctypes.byref(self.cfg), _dptr(self.S), _dptr(self.T),
+                                         _dptr(self.alias_thr), _dptr(self.alias),
+                                         _dptr(self.workspace), ws, _stream_ptr(), ctypes.byref(h))
+        else:
+            st = load().huge_attach_tables(ctypes.byref(self.cfg), _dptr(self.S), _dptr(self.T),
+                                           _dptr(self.alias_thr), _dptr(self.alias),
+                                           _dptr(self.workspace), ws, ctypes.byref(h))
+        _ok(st, "huge_init_tables" if init else "huge_attach_tables")
+        self._h = h
+
+    # -- calls ------------------------------------------------------------
+    def step(self, src, dst, cc, first_pos, lr, loss_out=None, stream=None):
+        loss = self.loss_buf if loss_out is None else loss_out
+        _ok(load().huge_train_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                   int(first_pos), float(lr), _dptr(loss), _stream_ptr(stream)),
+            "huge_train_step")
+        return loss
+
+    def step_no_loss(self, src, dst, cc, first_pos, lr, stream=None):
+        _ok(load().huge_train_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                   int(first_pos), float(lr), None, _stream_ptr(stream)),
+            "huge_train_step")
+
+    def eval_loss(self, src, dst, cc, first_pos, loss_out=None, stream=None):
+        loss = self.loss_buf if loss_out is None else loss_out
+        _ok(load().huge_eval_loss(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                  int(first_pos), _dptr(loss), _stream_ptr(stream)),
+            "huge_eval_loss")
+        return loss
+
+    def get_rows(self, table, ids, stream=None):
+        import torch
+        ids = ids.to(device=self.device, dtype=torch.int64).contiguous()
+        out = torch.empty((ids.numel(), self.cfg.dim), dtype=torch.float32, device=self.device)
+        _ok(load().huge_get_rows(self._h, int(table), _dptr(ids), ids.numel(), _dptr(out),
+                                 _stream_ptr(stream)), "huge_get_rows")
+        return out
+
+    def sample_negatives(self, n, first_pos, stream=None):
+        import torch
+        out = torch.empty((n, self.cfg.num_neg_per_pos), dtype=torch.int32, device=self.device)
+        _ok(load().huge_sample_negatives(self._h, int(n), int(first_pos), _dptr(out),
+                                         _stream_ptr(stream)), "huge_sample_negatives")
+        return out
+
+    def check(self, stream=None) -> int:
+        return int(load().huge_check(self._h, _stream_ptr(stream)))
+
+    def stats(self, stream=None):
+        a, b, c = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _ok(load().huge_step_stats(self._h, _stream_ptr(stream), ctypes.byref(a), ctypes.byref(b),
+                                   ctypes.byref(c)), "huge_step_stats")
+        return a.value, b.value, c.value
+
+    def profile_begin(self, max_steps):
+        _ok(load().huge_profile_begin(self._h, int(max_steps)), "huge_profile_begin")
+
+    def profile_end(self, stream=None):
+        """Summed phase durations (ms, list of HUGE_PHASES) and the step count."""
+        arr = (ctypes.c_double * HUGE_PHASES)()
+        n = ctypes.c_int32()
+        _ok(load().huge_profile_end(self._h, _stream_ptr(stream), arr, ctypes.byref(n)),
+            "huge_profile_end")
+        return list(arr), n.value
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load().huge_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,139 @@
+// Internal declarations shared by the kernels and the host layer of libhuge.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace huge {
+
+// ---------------------------------------------------------------------------
+// Compile-time constants
+// ---------------------------------------------------------------------------
+constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
+constexpr int kRadixBits = 8;          // digit width of the LSD radix sort
+constexpr int kRadixBins = 1 << kRadixBits;
+constexpr int kMaxPasses = 4;          // keys < 2^32
+constexpr int kSortItems = 16;         // keys per thread in a sort tile
+constexpr int kSortTile = kBlock * kSortItems;  // 4096 keys per tile
+constexpr int kChunk = 256;            // sorted positions per duplicate-sum window
+constexpr int kNegBlock = 8;           // negatives whose rows are in flight together
+constexpr int kMaxNeg = 64;
+constexpr int kMaxDim = 1024;
+
+// Status bits of a step (Control::step_bad) and the sticky error code.
+constexpr uint32_t kBadId = 1u;
+constexpr uint32_t kBadCount = 2u;
+constexpr uint32_t kBadInternal = 4u;  // a bounded wait expired or an index check failed
+
+// Device-side control block, at the start of the workspace.
+struct Control {
+    uint32_t step_bad;               // this call's input is invalid: skip all writes
+    uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
+    uint32_t tickets[kMaxPasses];    // dynamic tile ids of the radix passes
+    uint32_t n_work;                 // duplicate pieces found by the run marking
+    uint32_t n_long;                 // repeated rows spanning several windows
+    uint32_t uniq_S, uniq_T;         // distinct rows in the last sorted step
+    uint32_t dup_occ;                // occurrences that fell in a repeated row
+    uint32_t pad[5];
+};
+
+// Byte offsets of the workspace regions (all 256-byte aligned).
+struct Layout {
+    size_t ctrl = 0;
+    size_t hist = 0;     // u32 [kMaxPasses][256] global digit counts
+    size_t lossp = 0;    // double [loss_blocks]
+    size_t neg = 0;      // i32 [max_batch * K]
+    // sorted scatter
+    size_t keys0 = 0, keys1 = 0, vals0 = 0, vals1 = 0;  // u32 [M]
+    size_t info = 0;     // i32 [M]: -1 = row occurs once, else sorted position
+    size_t status = 0;   // u64 [sort_tiles * 256] look-back words
+    size_t work = 0;     // uint4 [M] duplicate pieces
+    size_t longseg = 0;  // uint2 [M / kChunk + 1]
+    size_t partA = 0, partB = 0;  // f64 [(M / kChunk + 2) * D] partial sums
+    size_t dup = 0;      // f32 [M * D] per-occurrence contributions of repeated rows
+    // atomic scatter
+    size_t gsrc = 0;     // f32 [max_batch * D] source-row gradients
+    size_t coef = 0;     // f32 [max_batch * (1 + K)]
+    size_t total = 0;
+    int64_t max_occ = 0;       // M = max_batch * (2 + K)
+    int64_t sort_tiles = 0;
+    int64_t loss_blocks = 0;
+};
+
+// Rows handled per workgroup: G lanes per row, C float4 per lane.
+struct RowShape {
+    int G;
+    int C;
+};
+
+inline RowShape row_shape(int dim) {
+    int q = dim / 4;
+    int G = 1;
+    while (G < q && G < 64) G <<= 1;
+    int C = (q + G - 1) / G;
+    return {G, C};
+}
+
+struct StepArgs {
+    const int32_t* src;
+    const int32_t* dst;
+    const int32_t* cc;
+    int64_t n;
+    uint64_t first_pos;
+    float lr;
+    double* loss_out;
+};
+
+struct TableArgs {
+    float* S;
+    float* T;
+    int64_t N;
+    int32_t D;
+    int32_t K;
+    uint64_t seed;
+    const uint32_t* thr;   // alias thresholds or nullptr (uniform)
+    const int32_t* alias;
+};
+
+// ---------------------------------------------------------------------------
+// Launchers (each defined next to its kernels).  All return hipError_t of the
+// launch.
+// ---------------------------------------------------------------------------
+hipError_t launch_init(const TableArgs& t, float half_width, hipStream_t s);
+hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, const int64_t* ids,
+                           int64_t n, float* out, hipStream_t s);
+hipError_t launch_begin(Control* ctl, uint32_t* hist, hipStream_t s);
+hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s);
+hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
+                         uint32_t* keys, uint32_t* hist, int passes, hipStream_t s);
+hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
+                             uint32_t* keys_out, uint32_t* vals_out, int64_t m, int pass,
+                             const uint32_t* hist, uint64_t* status, uint32_t tag,
+                             hipStream_t s);
+hipError_t launch_mark(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
+                       int64_t N, int32_t* info, uint4* work, uint2* longseg, hipStream_t s);
+hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
+                             const int32_t* neg, const int32_t* info, float* dup,
+                             double* lossp, int64_t* blocks_out, hipStream_t s);
+hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
+                            const float* dup, double* partA, double* partB, float lr,
+                            int64_t max_work, hipStream_t s);
+hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint2* longseg,
+                               const uint32_t* keys, int64_t m, const double* partA,
+                               const double* partB, float lr, hipStream_t s);
+hipError_t launch_loss_final(Control* ctl, const double* lossp, int64_t blocks, double* out,
+                             hipStream_t s);
+hipError_t launch_atomic_gather(const TableArgs& t, Control* ctl, const StepArgs& a,
+                                const int32_t* neg, float* gsrc, float* coef, double* lossp,
+                                int64_t* blocks_out, hipStream_t s);
+hipError_t launch_atomic_scatter_T(const TableArgs& t, Control* ctl, const StepArgs& a,
+                                   const int32_t* neg, const float* coef, hipStream_t s);
+hipError_t launch_atomic_scatter_S(const TableArgs& t, Control* ctl, const StepArgs& a,
+                                   const float* gsrc, hipStream_t s);
+hipError_t launch_eval(const TableArgs& t, Control* ctl, const StepArgs& a, double* lossp,
+                       int64_t* blocks_out, hipStream_t s);
+
+int64_t fused_step_blocks(int dim, int64_t n);
+
+}  // namespace huge

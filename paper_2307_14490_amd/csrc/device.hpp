@@ -1,0 +1,125 @@
+// Device helpers: counter-based random numbers, negative draws, row access in
+// groups of lanes, and the loss pieces.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace huge {
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of the 4x32
+// multiply-xor bijection; the key advances by the Weyl constants between
+// rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 ctr, uint32_t key_lo, uint32_t key_hi) {
+    constexpr uint32_t kMulA = 0xD2511F53u;
+    constexpr uint32_t kMulB = 0xCD9E8D57u;
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        const uint32_t ha = __umulhi(kMulA, ctr.x);
+        const uint32_t la = kMulA * ctr.x;
+        const uint32_t hb = __umulhi(kMulB, ctr.z);
+        const uint32_t lb = kMulB * ctr.z;
+        ctr = make_uint4(hb ^ ctr.y ^ key_lo, lb, ha ^ ctr.w ^ key_hi, la);
+        key_lo += 0x9E3779B9u;
+        key_hi += 0xBB67AE85u;
+    }
+    return ctr;
+}
+
+// Negative k of the positive with global index p: a uniform bucket
+// floor(x N / 2^64) from the 64-bit word x = (r1 << 32) | r0, then, with an
+// alias table, the 32-bit coin r2 keeps the bucket or takes its alias.
+__device__ __forceinline__ int32_t draw_negative(uint64_t seed, uint64_t p, uint32_t k,
+                                                 uint64_t N, const uint32_t* __restrict__ thr,
+                                                 const int32_t* __restrict__ alias) {
+    const uint4 r = philox4x32_10(make_uint4((uint32_t)p, (uint32_t)(p >> 32), k, 1u),
+                                  (uint32_t)seed, (uint32_t)(seed >> 32));
+    const uint64_t x = ((uint64_t)r.y << 32) | (uint64_t)r.x;
+    uint64_t j = __umul64hi(x, N);
+    if (thr != nullptr) {
+        // alias entries come from the caller: one outside [0, N) keeps j
+        if (r.z >= thr[j]) {
+            const uint64_t a = (uint64_t)(uint32_t)alias[j];
+            j = a < N ? a : j;
+        }
+    }
+    return (int32_t)j;
+}
+
+// Sum over the G lanes of a group (G a power of two <= 64, groups aligned).
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+    for (int off = G / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// softplus(z) = log(1 + e^z), evaluated without overflow.
+__device__ __forceinline__ float softplus_f(float z) {
+    return fmaxf(z, 0.0f) + log1pf(expf(-fabsf(z)));
+}
+
+// c (sigmoid(x) - 1) = -c / (1 + e^x) and c sigmoid(y) = c / (1 + e^-y).
+__device__ __forceinline__ float coef_pos(float c, float x) { return -c / (1.0f + expf(x)); }
+__device__ __forceinline__ float coef_neg(float c, float y) { return c / (1.0f + expf(-y)); }
+
+__device__ __forceinline__ float dot4(float4 a, float4 b) {
+    return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+}
+
+__device__ __forceinline__ float4 axpy4(float a, float4 x, float4 y) {
+    return make_float4(fmaf(a, x.x, y.x), fmaf(a, x.y, y.y), fmaf(a, x.z, y.z),
+                       fmaf(a, x.w, y.w));
+}
+
+__device__ __forceinline__ float4 scale4(float a, float4 x) {
+    return make_float4(a * x.x, a * x.y, a * x.z, a * x.w);
+}
+
+__device__ __forceinline__ float4 add4(float4 a, float4 b) {
+    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+__device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+
+// Row r of a D-float table as float4 chunks; lane l of a group owns chunks
+// l, l + G, ..., l + (C-1) G, those below D/4 are valid.
+template <int G, int C>
+struct RowIO {
+    __device__ __forceinline__ static void load(float4 (&x)[C], const float* __restrict__ base,
+                                                int64_t row, int32_t D, int lane) {
+        const float4* p = reinterpret_cast<const float4*>(base + row * (int64_t)D);
+        const int q = D >> 2;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int j = lane + c * G;
+            x[c] = (j < q) ? p[j] : zero4();
+        }
+    }
+    __device__ __forceinline__ static void store(float* __restrict__ base, int64_t row,
+                                                 int32_t D, int lane, const float4 (&x)[C]) {
+        float4* p = reinterpret_cast<float4*>(base + row * (int64_t)D);
+        const int q = D >> 2;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int j = lane + c * G;
+            if (j < q) p[j] = x[c];
+        }
+    }
+    __device__ __forceinline__ static float dot(const float4 (&a)[C], const float4 (&b)[C]) {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) s += dot4(a[c], b[c]);
+        return s;
+    }
+};
+
+// Record the first error since the last huge_check and flag this call.
+__device__ __forceinline__ void raise_error(Control* ctl, uint32_t bit) {
+    atomicOr(&ctl->step_bad, bit);
+    atomicCAS(&ctl->error, 0u, bit);
+}
+
+}  // namespace huge

@@ -1,0 +1,26 @@
+// Instantiation over the supported row shapes: G lanes per row (power of two,
+// 1..64) and C float4 chunks per lane (C > 1 only with G = 64), D <= 1024.
+#pragma once
+
+#define HUGE_ROW_CASE(GG, CC, ...)           \
+    case (GG) * 8 + (CC): {                  \
+        constexpr int G_ = (GG);             \
+        constexpr int C_ = (CC);             \
+        __VA_ARGS__;                         \
+    } break;
+
+#define HUGE_ROW_DISPATCH(rs, ...)                   \
+    switch ((rs).G * 8 + (rs).C) {                   \
+        HUGE_ROW_CASE(1, 1, __VA_ARGS__)             \
+        HUGE_ROW_CASE(2, 1, __VA_ARGS__)             \
+        HUGE_ROW_CASE(4, 1, __VA_ARGS__)             \
+        HUGE_ROW_CASE(8, 1, __VA_ARGS__)             \
+        HUGE_ROW_CASE(16, 1, __VA_ARGS__)            \
+        HUGE_ROW_CASE(32, 1, __VA_ARGS__)            \
+        HUGE_ROW_CASE(64, 1, __VA_ARGS__)            \
+        HUGE_ROW_CASE(64, 2, __VA_ARGS__)            \
+        HUGE_ROW_CASE(64, 3, __VA_ARGS__)            \
+        HUGE_ROW_CASE(64, 4, __VA_ARGS__)            \
+        default:                                     \
+            return hipErrorInvalidValue;             \
+    }

@@ -1,0 +1,357 @@
+// The training step proper: for every positive, gather its rows, take the
+// (1 + K) dot products, the loss and the coefficients, and update the rows
+// (HUGE Sec. 3.3.2: gather, forward and gradient, aggregate, update).
+//
+// Rows that occur once in the batch are rewritten in place by the thread
+// group that read them -- no other group reads them.  A row that occurs
+// several times is left untouched here: each occurrence stores its
+// contribution at its sorted position, and the duplicate kernels sum them in
+// occurrence order and update the row once, so every read sees pre-step
+// values.
+#include "common.hpp"
+#include "device.hpp"
+#include "dispatch.hpp"
+
+namespace huge {
+
+// Sum of one double per thread over the workgroup, written by thread 0.
+__device__ __forceinline__ void block_loss(float loss, double* __restrict__ out) {
+    __shared__ double s_w[kBlock / 64];
+    double v = (double)loss;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double acc = 0.0;
+#pragma unroll
+        for (int w = 0; w < kBlock / 64; ++w) acc += s_w[w];
+        out[blockIdx.x] = acc;
+    }
+}
+
+template <int G, int C>
+__global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, const Control* __restrict__ ctl,
+                                                       StepArgs a, const int32_t* __restrict__ neg,
+                                                       const int32_t* __restrict__ info,
+                                                       float* __restrict__ dup,
+                                                       double* __restrict__ lossp) {
+    using IO = RowIO<G, C>;
+    if (ctl->step_bad) return;
+    constexpr int PPB = kBlock / G;
+    const int grp = threadIdx.x / G;
+    const int lane = threadIdx.x % G;
+    const int64_t i = (int64_t)blockIdx.x * PPB + grp;
+    const int K = t.K;
+    const int32_t D = t.D;
+    const float lr = a.lr;
+    float* __restrict__ S = t.S;
+    float* __restrict__ T = t.T;
+    float loss = 0.f;
+
+    if (i < a.n) {
+        const int32_t u = a.src[i];
+        const int32_t v = a.dst[i];
+        const float c = (float)a.cc[i];
+        const int64_t o = i * (int64_t)(2 + K);
+        const int32_t info_s = info[o];
+        const int32_t info_d = info[o + 1];
+        const int32_t* negi = neg + i * (int64_t)K;
+        const int32_t* infok = info + o + 2;
+
+        float4 s[C], t0[C], dS[C];
+        float4 tk[kNegBlock][C];
+        int32_t mk[kNegBlock], ik[kNegBlock];
+        int cnt = K < kNegBlock ? K : kNegBlock;
+#pragma unroll
+        for (int j = 0; j < kNegBlock; ++j) {
+            if (j < cnt) {
+                mk[j] = negi[j];
+                ik[j] = infok[j];
+            }
+        }
+        IO::load(s, S, u, D, lane);
+        IO::load(t0, T, v, D, lane);
+#pragma unroll
+        for (int j = 0; j < kNegBlock; ++j)
+            if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
+
+        // positive pair
+        const float x = group_sum<G>(IO::dot(s, t0));
+        const float g = coef_pos(c, x);
+        float lsum = softplus_f(-x);
+#pragma unroll
+        for (int q = 0; q < C; ++q) dS[q] = scale4(g, t0[q]);
+        if (info_d < 0) {
+            float4 nv[C];
+#pragma unroll
+            for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * g), s[q], t0[q]);
+            IO::store(T, v, D, lane, nv);
+        } else {
+            float4 cv[C];
+#pragma unroll
+            for (int q = 0; q < C; ++q) cv[q] = scale4(g, s[q]);
+            IO::store(dup, info_d, D, lane, cv);
+        }
+
+        // negatives, kNegBlock rows in flight at a time
+        int kb = 0;
+        while (true) {
+            float y[kNegBlock];
+#pragma unroll
+            for (int j = 0; j < kNegBlock; ++j) y[j] = (j < cnt) ? IO::dot(s, tk[j]) : 0.f;
+#pragma unroll
+            for (int off = G / 2; off > 0; off >>= 1) {
+#pragma unroll
+                for (int j = 0; j < kNegBlock; ++j) y[j] += __shfl_xor(y[j], off, 64);
+            }
+#pragma unroll
+            for (int j = 0; j < kNegBlock; ++j) {
+                if (j < cnt) {
+                    const float h = coef_neg(c, y[j]);
+                    lsum += softplus_f(y[j]);
+#pragma unroll
+                    for (int q = 0; q < C; ++q) dS[q] = axpy4(h, tk[j][q], dS[q]);
+                    if (ik[j] < 0) {
+                        float4 nv[C];
+#pragma unroll
+                        for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * h), s[q], tk[j][q]);
+                        IO::store(T, mk[j], D, lane, nv);
+                    } else {
+                        float4 cv[C];
+#pragma unroll
+                        for (int q = 0; q < C; ++q) cv[q] = scale4(h, s[q]);
+                        IO::store(dup, ik[j], D, lane, cv);
+                    }
+                }
+            }
+            kb += kNegBlock;
+            if (kb >= K) break;
+            cnt = (K - kb) < kNegBlock ? (K - kb) : kNegBlock;
+#pragma unroll
+            for (int j = 0; j < kNegBlock; ++j) {
+                if (j < cnt) {
+                    mk[j] = negi[kb + j];
+                    ik[j] = infok[kb + j];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kNegBlock; ++j)
+                if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
+        }
+
+        // source row
+        if (info_s < 0) {
+            float4 nv[C];
+#pragma unroll
+            for (int q = 0; q < C; ++q) nv[q] = axpy4(-lr, dS[q], s[q]);
+            IO::store(S, u, D, lane, nv);
+        } else {
+            IO::store(dup, info_s, D, lane, dS);
+        }
+        if (lane == 0) loss = c * lsum;
+    }
+    block_loss(loss, lossp);
+}
+
+int64_t fused_step_blocks(int dim, int64_t n) {
+    const RowShape rs = row_shape(dim);
+    const int64_t ppb = kBlock / rs.G;
+    return (n + ppb - 1) / ppb;
+}
+
+hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
+                             const int32_t* neg, const int32_t* info, float* dup,
+                             double* lossp, int64_t* blocks_out, hipStream_t s) {
+    const RowShape rs = row_shape(t.D);
+    const int64_t blocks = fused_step_blocks(t.D, a.n);
+    *blocks_out = blocks;
+    if (blocks == 0) return hipSuccess;
+    HUGE_ROW_DISPATCH(rs, {
+        hipLaunchKernelGGL((k_fused_step<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t,
+                           ctl, a, neg, info, dup, lossp);
+    });
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Repeated rows.  Work item {start, len, key, kind}: the contributions at
+// sorted positions start .. start + len - 1 are added in that order, in
+// double (a hub row can collect tens of thousands of terms), and the row is
+// rounded to fp32 once: row = fp32(row - lr * sum).
+// ---------------------------------------------------------------------------
+struct double4_ {
+    double x, y, z, w;
+};
+
+__device__ __forceinline__ void addd(double4_& a, float4 b) {
+    a.x += (double)b.x;
+    a.y += (double)b.y;
+    a.z += (double)b.z;
+    a.w += (double)b.w;
+}
+
+template <int G, int C>
+struct PartIO {
+    // rows of D doubles, lane l owns elements 4 (l + c G) .. + 3
+    __device__ __forceinline__ static void load(double4_ (&x)[C], const double* __restrict__ base,
+                                                int64_t row, int32_t D, int lane) {
+        const double4_* p = reinterpret_cast<const double4_*>(base + row * (int64_t)D);
+        const int q = D >> 2;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int j = lane + c * G;
+            x[c] = (j < q) ? p[j] : double4_{0.0, 0.0, 0.0, 0.0};
+        }
+    }
+    __device__ __forceinline__ static void store(double* __restrict__ base, int64_t row,
+                                                 int32_t D, int lane, const double4_ (&x)[C]) {
+        double4_* p = reinterpret_cast<double4_*>(base + row * (int64_t)D);
+        const int q = D >> 2;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int j = lane + c * G;
+            if (j < q) p[j] = x[c];
+        }
+    }
+};
+
+template <int G, int C>
+__device__ __forceinline__ void sum_rows(double4_ (&acc)[C], const float* __restrict__ rows,
+                                         int64_t start, int64_t len, int32_t D, int lane) {
+    using IO = RowIO<G, C>;
+#pragma unroll
+    for (int q = 0; q < C; ++q) acc[q] = double4_{0.0, 0.0, 0.0, 0.0};
+    int64_t r = 0;
+    for (; r + 4 <= len; r += 4) {
+        float4 b0[C], b1[C], b2[C], b3[C];
+        IO::load(b0, rows, start + r, D, lane);
+        IO::load(b1, rows, start + r + 1, D, lane);
+        IO::load(b2, rows, start + r + 2, D, lane);
+        IO::load(b3, rows, start + r + 3, D, lane);
+#pragma unroll
+        for (int q = 0; q < C; ++q) {
+            addd(acc[q], b0[q]);
+            addd(acc[q], b1[q]);
+            addd(acc[q], b2[q]);
+            addd(acc[q], b3[q]);
+        }
+    }
+    for (; r < len; ++r) {
+        float4 b[C];
+        IO::load(b, rows, start + r, D, lane);
+#pragma unroll
+        for (int q = 0; q < C; ++q) addd(acc[q], b[q]);
+    }
+}
+
+template <int G, int C>
+__device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
+                                          const double4_ (&g)[C], float lr, int lane) {
+    using IO = RowIO<G, C>;
+    float* base = (int64_t)key >= t.N ? t.S : t.T;
+    const int64_t row = (int64_t)key >= t.N ? (int64_t)key - t.N : (int64_t)key;
+    const double l = (double)lr;
+    float4 r[C];
+    IO::load(r, base, row, t.D, lane);
+#pragma unroll
+    for (int q = 0; q < C; ++q) {
+        r[q].x = (float)((double)r[q].x - l * g[q].x);
+        r[q].y = (float)((double)r[q].y - l * g[q].y);
+        r[q].z = (float)((double)r[q].z - l * g[q].z);
+        r[q].w = (float)((double)r[q].w - l * g[q].w);
+    }
+    IO::store(base, row, t.D, lane, r);
+}
+
+template <int G, int C>
+__global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control* __restrict__ ctl,
+                                                      const uint4* __restrict__ work,
+                                                      const float* __restrict__ dup,
+                                                      double* __restrict__ partA,
+                                                      double* __restrict__ partB, float lr) {
+    if (ctl->step_bad) return;
+    constexpr int PPB = kBlock / G;
+    const int grp = threadIdx.x / G;
+    const int lane = threadIdx.x % G;
+    const int64_t nw = ctl->n_work;
+    for (int64_t w = (int64_t)blockIdx.x * PPB + grp; w < nw; w += (int64_t)gridDim.x * PPB) {
+        const uint4 rec = work[w];
+        double4_ acc[C];
+        sum_rows<G, C>(acc, dup, rec.x, rec.y, t.D, lane);
+        if (rec.w == 0u) {
+            apply_row<G, C>(t, rec.z, acc, lr, lane);
+        } else {
+            double* part = rec.w == 1u ? partB : partA;
+            PartIO<G, C>::store(part, (int64_t)(rec.x / kChunk), t.D, lane, acc);
+        }
+    }
+}
+
+template <int G, int C>
+__global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Control* __restrict__ ctl,
+                                                         const uint2* __restrict__ longseg,
+                                                         const uint32_t* __restrict__ keys,
+                                                         int64_t m, const double* __restrict__ partA,
+                                                         const double* __restrict__ partB,
+                                                         float lr) {
+    using IO = PartIO<G, C>;
+    if (ctl->step_bad) return;
+    constexpr int PPB = kBlock / G;
+    const int grp = threadIdx.x / G;
+    const int lane = threadIdx.x % G;
+    const int64_t nl = ctl->n_long;
+    for (int64_t l = (int64_t)blockIdx.x * PPB + grp; l < nl; l += (int64_t)gridDim.x * PPB) {
+        const uint2 rec = longseg[l];
+        const uint32_t key = rec.y;
+        int64_t win = rec.x / kChunk;
+        double4_ acc[C];
+        IO::load(acc, partB, win, t.D, lane);
+        while (true) {
+            ++win;
+            double4_ b[C];
+            IO::load(b, partA, win, t.D, lane);
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                acc[q].x += b[q].x;
+                acc[q].y += b[q].y;
+                acc[q].z += b[q].z;
+                acc[q].w += b[q].w;
+            }
+            const int64_t e = (win + 1) * kChunk;
+            if (!(e < m && keys[e] == key)) break;
+        }
+        apply_row<G, C>(t, key, acc, lr, lane);
+    }
+}
+
+hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
+                            const float* dup, double* partA, double* partB, float lr,
+                            int64_t max_work, hipStream_t s) {
+    const RowShape rs = row_shape(t.D);
+    const int64_t ppb = kBlock / rs.G;
+    int64_t blocks = (max_work / 2 + ppb - 1) / ppb + 1;
+    if (blocks > 2048) blocks = 2048;
+    HUGE_ROW_DISPATCH(rs, {
+        hipLaunchKernelGGL((k_dup_apply<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t,
+                           ctl, work, dup, partA, partB, lr);
+    });
+    return hipGetLastError();
+}
+
+hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint2* longseg,
+                               const uint32_t* keys, int64_t m, const double* partA,
+                               const double* partB, float lr, hipStream_t s) {
+    const RowShape rs = row_shape(t.D);
+    const int64_t ppb = kBlock / rs.G;
+    int64_t blocks = (m / kChunk + 1 + ppb - 1) / ppb;
+    if (blocks > 256) blocks = 256;
+    if (blocks < 1) blocks = 1;
+    HUGE_ROW_DISPATCH(rs, {
+        hipLaunchKernelGGL((k_long_combine<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
+                           t, ctl, longseg, keys, m, partA, partB, lr);
+    });
+    return hipGetLastError();
+}
+
+}  // namespace huge

@@ -1,0 +1,129 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function declared in include/huge.h, sizes its workspace, builds alias tables
+identical to the oracle's, and rejects bad arguments before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2307_14490_amd as P
+from paper_2307_14490_amd import binding as B
+from oracle import oracle as orc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "huge.h")).read()
+    decl = r"^(?:size_t|huge_status|void|const char\*)\s+(huge_[a-z_]+)\s*\("
+    return sorted(set(re.findall(decl, text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = P.load()
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(B.EXPORTED) == names
+
+
+def test_status_strings_cover_every_code():
+    seen = set()
+    for code in (0, -1, -2, -3, -4, -5):
+        s = B.status_string(code)
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 6
+    assert B.status_string(-99) == "unknown status"
+
+
+@pytest.mark.parametrize("kw", [
+    dict(num_nodes=0), dict(num_nodes=2**31), dict(dim=6), dict(dim=0), dict(dim=1028),
+    dict(num_neg=0), dict(num_neg=65), dict(max_batch=0), dict(max_batch=2**31 // 7 + 1),
+])
+def test_invalid_configs_have_no_workspace(kw):
+    base = dict(num_nodes=1000, dim=32, num_neg=5, max_batch=100)
+    base.update(kw)
+    assert P.workspace_bytes(P.make_config(**base)) == 0
+
+
+def test_bad_kind_and_width():
+    c = P.make_config(1000, 32, 5, 100)
+    c.neg_kind = 7
+    assert P.workspace_bytes(c) == 0
+    c = P.make_config(1000, 32, 5, 100)
+    c.scatter_kind = 2
+    assert P.workspace_bytes(c) == 0
+    c = P.make_config(1000, 32, 5, 100, init_half_width=-1.0)
+    assert P.workspace_bytes(c) == 0
+    c = P.make_config(1000, 32, 5, 100, init_half_width=float("inf"))
+    assert P.workspace_bytes(c) == 0
+
+
+def test_workspace_grows_with_batch_and_holds_duplicate_buffer():
+    small = P.workspace_bytes(P.make_config(10**6, 128, 5, 1000))
+    big = P.workspace_bytes(P.make_config(10**6, 128, 5, 100_000))
+    assert big > small > 0
+    # sorted scatter keeps one D-float slot per occurrence
+    M = 100_000 * 7
+    assert big >= M * 128 * 4
+    atomic = P.workspace_bytes(P.make_config(10**6, 128, 5, 100_000, scatter_kind=1))
+    assert 0 < atomic < big
+
+
+def test_host_alias_table_equals_oracle_bitwise():
+    rng = np.random.default_rng(0)
+    for w in (rng.pareto(1.2, 50_000) + 1e-3,
+              np.concatenate([np.zeros(10), rng.integers(1, 100, 1000).astype(float)]),
+              np.ones(33), np.array([0.0, 0.0, 2.5])):
+        t1, a1 = P.build_alias(w)
+        t2, a2 = orc.build_alias(w)
+        assert np.array_equal(t1, t2) and np.array_equal(a1, a2)
+
+
+def test_host_alias_rejects_bad_weights():
+    for w in (np.zeros(3), np.array([1.0, -2.0]), np.array([np.inf]), np.array([])):
+        with pytest.raises(B.HugeError) as e:
+            P.build_alias(w)
+        assert e.value.status == B.HUGE_ERR_INVALID_ARG
+
+
+def test_calls_reject_bad_arguments_before_any_launch():
+    L = P.load()
+    vp = ctypes.c_void_p
+    # null handle
+    assert L.huge_train_step(None, None, None, None, 0, 0, 0.1, None, None) == -1
+    assert L.huge_eval_loss(None, None, None, None, 0, 0, None, None) == -1
+    assert L.huge_get_rows(None, 0, None, 1, None, None) == -1
+    assert L.huge_sample_negatives(None, 1, 0, None, None) == -1
+    assert L.huge_check(None, None) == -1
+    assert L.huge_step_stats(None, None, None, None, None) == -1
+    L.huge_destroy(None)
+    # invalid config or null pointers: rejected on the host
+    h = vp()
+    cfg = P.make_config(1000, 6, 5, 10)
+    assert L.huge_init_tables(ctypes.byref(cfg), 4096, 8192, None, None, 1 << 20, 1 << 30,
+                              None, ctypes.byref(h)) == -1
+    cfg = P.make_config(1000, 32, 5, 10)
+    assert L.huge_init_tables(ctypes.byref(cfg), None, 8192, None, None, 1 << 20, 1 << 30,
+                              None, ctypes.byref(h)) == -1
+    assert L.huge_init_tables(ctypes.byref(cfg), 4096, 8192, None, None, None, 1 << 30,
+                              None, ctypes.byref(h)) == -1
+    # alias sampling without tables
+    cfg = P.make_config(1000, 32, 5, 10, neg_kind=1)
+    assert L.huge_init_tables(ctypes.byref(cfg), 4096, 8192, None, None, 1 << 20, 1 << 30,
+                              None, ctypes.byref(h)) == -1
+    # misaligned workspace
+    cfg = P.make_config(1000, 32, 5, 10)
+    assert L.huge_init_tables(ctypes.byref(cfg), 4096, 8192, None, None, (1 << 20) + 8,
+                              1 << 30, None, ctypes.byref(h)) == -1
+    # workspace too small
+    need = P.workspace_bytes(cfg)
+    assert L.huge_init_tables(ctypes.byref(cfg), 4096, 8192, None, None, 1 << 20, need - 1,
+                              None, ctypes.byref(h)) == -4
+    assert L.huge_attach_tables(ctypes.byref(cfg), 4096, 8192, None, None, 1 << 20, need - 1,
+                                ctypes.byref(h)) == -4
+    assert not h.value

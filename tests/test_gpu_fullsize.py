@@ -1,0 +1,89 @@
+"""Parity at the full sizes of the benchmark workloads (GPU).
+
+One step from freshly initialised tables on batch 0 of each workload, in the
+launch configuration the benchmark times (sorted scatter; the medium workload
+also with the atomic scatter).  The oracle holds only the rows the batch
+touches (its own sampler picks the negatives, its own initialiser the
+pre-step values), so every touched element is checked against it; a random
+sample of untouched rows must still equal the oracle's initial values bit for
+bit, and the step's row counts must equal the oracle's exactly.
+"""
+import time
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import oracle as orc  # noqa: E402
+import paper_2307_14490_amd as P  # noqa: E402
+from gpu_common import assert_close, dev, say  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+CASES = [("medium", "sorted"), ("medium", "atomic"), ("powerlaw", "sorted"),
+         ("sbm100m", "sorted"), ("hubstress", "sorted")]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name,scatter", CASES)
+def test_full_size_step(name, scatter):
+    from synth import make_workload
+    t0 = time.time()
+    wl = make_workload(name, 0)
+    cfg = wl.cfg
+    src, dst, cc = wl.batch(0)
+    say(f"[{name}/{scatter}] N={cfg.num_nodes} D={cfg.dim} K={cfg.num_neg} n={src.size} "
+        f"inputs {time.time() - t0:.1f}s")
+    seed = 2024
+    first = 3 * cfg.batch
+    a = float(np.float32(cfg.init_half_width))
+    thr = alias = None
+    if cfg.neg_kind == "alias":
+        thr, alias = orc.build_alias(wl.weights)
+    tr = P.Trainer(cfg.num_nodes, cfg.dim, cfg.num_neg, cfg.batch, seed=seed,
+                   alias_weights=wl.weights, scatter=scatter)
+    loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), first, cfg.lr).item()
+    assert tr.check() == 0
+    say(f"[{name}/{scatter}] gpu step done {time.time() - t0:.1f}s")
+
+    ref = orc.step_sparse(seed, cfg.num_nodes, cfg.dim, cfg.num_neg, a, src, dst, cc, first,
+                          cfg.lr, thr, alias)
+    say(f"[{name}/{scatter}] oracle done {time.time() - t0:.1f}s "
+        f"rows S {ref.rows_S.size} T {ref.rows_T.size}")
+    # negatives: the device sampler must give the oracle's draws
+    negs = tr.sample_negatives(src.size, first).cpu().numpy()
+    assert np.array_equal(negs, ref.neg)
+    if scatter == "sorted":
+        uS, uT, dup = tr.stats()
+        keys = np.concatenate([src.astype(np.int64) + cfg.num_nodes, dst, ref.neg.reshape(-1)])
+        _, cnt = np.unique(keys, return_counts=True)
+        assert (uS, uT) == (ref.rows_S.size, ref.rows_T.size)
+        assert dup == int(cnt[cnt > 1].sum())
+    gS = tr.get_rows(0, torch.from_numpy(ref.rows_S)).cpu().numpy()
+    assert_close(gS, ref.S, f"{name} S")
+    del gS
+    gT = tr.get_rows(1, torch.from_numpy(ref.rows_T)).cpu().numpy()
+    assert_close(gT, ref.T, f"{name} T")
+    del gT
+    assert loss == pytest.approx(ref.loss, rel=1e-5)
+    # untouched rows keep their initial values exactly
+    rng = np.random.default_rng(1)
+    for table, rows in ((0, ref.rows_S), (1, ref.rows_T)):
+        cand = rng.integers(0, cfg.num_nodes, 6000)
+        cand = np.setdiff1d(cand, rows)[:4096]
+        got = tr.get_rows(table, torch.from_numpy(cand)).cpu().numpy()
+        assert np.array_equal(got, orc.init_rows(seed, table, cand, cfg.dim, a))
+    say(f"[{name}/{scatter}] checked {time.time() - t0:.1f}s")
+    tr.close()
+    del tr

@@ -1,0 +1,309 @@
+"""GPU parity of libhuge against the CPU oracle, through the C ABI.
+
+Bit-exact: initial tables, sampled negatives, rows a step does not touch, the
+row counts of the grouping, run-to-run results of the sorted scatter.
+Within |gpu - oracle| <= 1e-6 + 1e-5 |oracle|: every touched table element
+after a step, for both scatter variants.  Loss sums within 1e-5 relative.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import oracle as orc  # noqa: E402
+import paper_2307_14490_amd as P  # noqa: E402
+from gpu_common import assert_close, dev, say  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _trainer(N, D, K, nmax, seed=0, weights=None, scatter="sorted", a=0.0):
+    tr = P.Trainer(N, D, K, nmax, seed=seed, init_half_width=a, alias_weights=weights,
+                   scatter=scatter)
+    torch.cuda.synchronize()
+    return tr
+
+
+def _half(D, a=0.0):
+    return float(np.float32(a if a else 0.5 / D))
+
+
+def _random_batch(rng, N, n, cmax=5, hub_frac=0.0):
+    src = rng.integers(0, N, n).astype(np.int32)
+    dst = rng.integers(0, N, n).astype(np.int32)
+    cc = rng.integers(0, cmax + 1, n).astype(np.int32)
+    if hub_frac > 0:
+        k = int(n * hub_frac)
+        src[:k] = 1 % N
+        dst[k // 2:k] = 0
+    return src, dst, cc
+
+
+# --------------------------------------------------------------------------- #
+# Bit-exact random streams
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("N,D,a", [(10_000, 32, 0.0), (777, 36, 0.0), (50, 1024, 0.3)])
+def test_init_tables_bit_exact(N, D, a):
+    say(f"init N={N} D={D}")
+    tr = _trainer(N, D, 5, 16, seed=1234, a=a)
+    S = tr.S.cpu().numpy()
+    T = tr.T.cpu().numpy()
+    ids = np.arange(N)
+    assert np.array_equal(S, orc.init_rows(1234, 0, ids, D, _half(D, a)))
+    assert np.array_equal(T, orc.init_rows(1234, 1, ids, D, _half(D, a)))
+
+
+@pytest.mark.parametrize("kind", ["uniform", "alias"])
+@pytest.mark.parametrize("N,n,first", [(10_000, 1024, 0), (99_991, 1037, 2**33 + 5),
+                                       (3, 513, 7), (100_000_000, 4096, 12345)])
+def test_negatives_bit_exact(kind, N, n, first):
+    say(f"negatives {kind} N={N} n={n} first={first}")
+    w = None
+    thr = alias = None
+    if kind == "alias":
+        if N > 10**7:
+            pytest.skip("alias over 1e8 weights is covered by the full-size tests")
+        rng = np.random.default_rng(N)
+        w = (rng.pareto(1.1, N) + 0.1) ** 0.75
+        w[::7] = 0.0
+        thr, alias = orc.build_alias(w)
+    tr = _trainer(N, 8, 7, max(n, 1), seed=99, weights=w)
+    got = tr.sample_negatives(n, first).cpu().numpy()
+    ref = orc.sample_negatives(99, first, n, 7, N, thr, alias)
+    assert np.array_equal(got, ref)
+
+
+# --------------------------------------------------------------------------- #
+# One step against the dense oracle
+# --------------------------------------------------------------------------- #
+STEP_CASES = [
+    # N, D, K, n, note
+    (10_000, 32, 5, 1024, "tiny shape"),
+    (1_000, 36, 3, 777, "D/4 not a power of two, ragged n"),
+    (500, 512, 2, 300, "two float4 per lane"),
+    (300, 1024, 1, 100, "widest row, K=1"),
+    (50, 4, 20, 64, "narrowest row, several negative blocks"),
+    (2, 8, 5, 50, "two nodes: every row repeats"),
+    (1_000, 128, 64, 100, "largest K"),
+    (20_000, 128, 5, 9000, "several sort tiles"),
+]
+
+
+def _one_step(N, D, K, n, scatter, seed=7, weights=None, hub=0.0, cmax=5, lr=0.025):
+    rng = np.random.default_rng(N * 31 + D * 7 + K)
+    src, dst, cc = _random_batch(rng, N, n, cmax=cmax, hub_frac=hub)
+    first = 1000
+    tr = _trainer(N, D, K, n, seed=seed, weights=weights, scatter=scatter)
+    loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), first, lr).item()
+    assert tr.check() == 0
+    S = tr.S.cpu().numpy()
+    T = tr.T.cpu().numpy()
+    ids = np.arange(N)
+    a = _half(D)
+    S0 = orc.init_rows(seed, 0, ids, D, a)
+    T0 = orc.init_rows(seed, 1, ids, D, a)
+    thr = alias = None
+    if weights is not None:
+        thr, alias = orc.build_alias(weights)
+    neg = orc.sample_negatives(seed, first, n, K, N, thr, alias)
+    Sr, Tr = S0.copy(), T0.copy()
+    ref_loss = orc.step_dense(Sr, Tr, src, dst, cc, neg, lr)
+    tS = np.zeros(N, bool)
+    tS[src] = True
+    tT = np.zeros(N, bool)
+    tT[dst] = True
+    tT[neg.reshape(-1)] = True
+    assert np.array_equal(S[~tS], S0[~tS]), "untouched source rows changed"
+    assert np.array_equal(T[~tT], T0[~tT]), "untouched context rows changed"
+    assert_close(S[tS], Sr[tS], f"S {scatter}")
+    assert_close(T[tT], Tr[tT], f"T {scatter}")
+    assert loss == pytest.approx(ref_loss, rel=1e-5, abs=1e-6)
+    return tr, (src, dst, cc, neg)
+
+
+@pytest.mark.parametrize("scatter", ["sorted", "atomic"])
+@pytest.mark.parametrize("N,D,K,n,note", STEP_CASES)
+def test_one_step_matches_oracle(scatter, N, D, K, n, note):
+    say(f"step {scatter} N={N} D={D} K={K} n={n} ({note})")
+    tr, (src, dst, cc, neg) = _one_step(N, D, K, n, scatter)
+    if scatter == "sorted":
+        uS, uT, dup = tr.stats()
+        keys = np.concatenate([src.astype(np.int64) + N, dst, neg.reshape(-1)])
+        u, cnt = np.unique(keys, return_counts=True)
+        assert uS == np.unique(src).size
+        assert uT == np.unique(np.concatenate([dst, neg.reshape(-1)])).size
+        assert dup == int(cnt[cnt > 1].sum())
+
+
+@pytest.mark.parametrize("scatter", ["sorted", "atomic"])
+def test_hub_rows_and_large_counts(scatter):
+    """Half the batch shares one source row, a quarter one destination row,
+    co_counts up to 1000: long runs split over several sum windows."""
+    say(f"hub {scatter}")
+    _one_step(5_000, 64, 4, 6000, scatter, hub=0.5, cmax=1000)
+
+
+def test_alias_negatives_step():
+    say("alias step")
+    rng = np.random.default_rng(3)
+    w = rng.integers(1, 60, 4000).astype(np.float64) ** 0.75
+    _one_step(4000, 64, 6, 3000, "sorted", weights=w)
+
+
+def test_sorted_scatter_is_bitwise_reproducible():
+    say("determinism")
+    N, D, K, n = 3000, 64, 5, 5000
+    rng = np.random.default_rng(11)
+    batches = [_random_batch(rng, N, n, hub_frac=0.3) for _ in range(3)]
+    out = []
+    for _ in range(2):
+        tr = _trainer(N, D, K, n, seed=5)
+        for b, (s, d, c) in enumerate(batches):
+            tr.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n, 0.05)
+        out.append((tr.S.cpu().numpy(), tr.T.cpu().numpy()))
+        del tr
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
+
+
+# --------------------------------------------------------------------------- #
+# Boundary behaviour
+# --------------------------------------------------------------------------- #
+@pytest.mark.parametrize("scatter", ["sorted", "atomic"])
+def test_empty_batch_is_a_no_op(scatter):
+    tr = _trainer(100, 16, 3, 10, scatter=scatter)
+    S0, T0 = tr.S.clone(), tr.T.clone()
+    e = torch.zeros(0, dtype=torch.int32, device="cuda")
+    loss = torch.full((1,), 7.0, dtype=torch.float64, device="cuda")
+    tr.step(e, e, e, 0, 0.1, loss_out=loss)
+    assert loss.item() == 0.0
+    assert torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+    assert tr.check() == 0
+
+
+@pytest.mark.parametrize("scatter", ["sorted", "atomic"])
+@pytest.mark.parametrize("bad", ["src", "dst", "neg_src", "count"])
+def test_invalid_batch_is_a_no_op_and_reported(scatter, bad):
+    N = 1000
+    tr = _trainer(N, 32, 4, 256, scatter=scatter)
+    rng = np.random.default_rng(1)
+    src, dst, cc = _random_batch(rng, N, 256)
+    if bad == "src":
+        src[100] = N
+    elif bad == "dst":
+        dst[5] = N + 7
+    elif bad == "neg_src":
+        src[0] = -1
+    else:
+        cc[17] = -2
+    S0, T0 = tr.S.clone(), tr.T.clone()
+    loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), 0, 0.1).item()
+    assert np.isnan(loss)
+    assert tr.check() == (-3 if bad == "count" else -2)
+    assert tr.check() == 0  # cleared
+    assert torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+    # the next valid batch is applied normally
+    s2, d2, c2 = _random_batch(rng, N, 256)
+    loss = tr.step(dev(s2, torch), dev(d2, torch), dev(c2, torch), 256, 0.1).item()
+    assert np.isfinite(loss) and tr.check() == 0
+    assert not torch.equal(tr.S, S0)
+
+
+def test_batch_larger_than_max_is_rejected_on_host():
+    tr = _trainer(100, 16, 3, 10)
+    x = torch.zeros(11, dtype=torch.int32, device="cuda")
+    with pytest.raises(P.HugeError):
+        tr.step(x, x, x, 0, 0.1)
+
+
+def test_get_rows_and_out_of_range_ids():
+    tr = _trainer(500, 40, 2, 8, seed=3)
+    ids = torch.tensor([0, 499, 17, 500, -1], dtype=torch.int64, device="cuda")
+    rows = tr.get_rows(1, ids).cpu().numpy()
+    ref = orc.init_rows(3, 1, [0, 499, 17], 40, _half(40))
+    assert np.array_equal(rows[:3], ref)
+    assert np.all(np.isnan(rows[3:]))
+    assert tr.check() == -2
+
+
+def test_eval_loss_matches_oracle_and_writes_nothing():
+    N, D, K, n = 2000, 48, 6, 1500
+    rng = np.random.default_rng(5)
+    src, dst, cc = _random_batch(rng, N, n)
+    tr = _trainer(N, D, K, n, seed=8)
+    S0, T0 = tr.S.clone(), tr.T.clone()
+    got = tr.eval_loss(dev(src, torch), dev(dst, torch), dev(cc, torch), 77).item()
+    assert torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+    neg = orc.sample_negatives(8, 77, n, K, N)
+    ref = orc.loss_dense(S0.cpu().numpy(), T0.cpu().numpy(), src, dst, cc, neg)
+    assert got == pytest.approx(ref, rel=1e-5)
+    # it also agrees with the step's own loss on the same batch
+    step_loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), 77, 0.1).item()
+    assert step_loss == pytest.approx(got, rel=1e-6)
+
+
+# --------------------------------------------------------------------------- #
+# Several steps: resume equals straight run; an epoch of the tiny workload
+# --------------------------------------------------------------------------- #
+def test_resume_from_saved_tables_is_bitwise_equal():
+    N, D, K, n = 4000, 32, 5, 2048
+    rng = np.random.default_rng(2)
+    batches = [_random_batch(rng, N, n, hub_frac=0.2) for _ in range(4)]
+    straight = _trainer(N, D, K, n, seed=21)
+    for b, (s, d, c) in enumerate(batches):
+        straight.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n, 0.05)
+    first = _trainer(N, D, K, n, seed=21)
+    for b, (s, d, c) in enumerate(batches[:2]):
+        first.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n, 0.05)
+    saved = (first.S.cpu().clone(), first.T.cpu().clone())
+    del first
+    resumed = P.Trainer(N, D, K, n, seed=21,
+                        tables=(saved[0].cuda().contiguous(), saved[1].cuda().contiguous()),
+                        init=False)
+    for b, (s, d, c) in enumerate(batches[2:], start=2):
+        resumed.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n, 0.05)
+    assert torch.equal(resumed.S, straight.S) and torch.equal(resumed.T, straight.T)
+
+
+@pytest.mark.parametrize("scatter", ["sorted", "atomic"])
+def test_tiny_epoch_loss_curve(scatter):
+    """The tiny SBM workload for one epoch: per-step mean loss within 1e-3."""
+    from synth import make_workload
+    wl = make_workload("tiny", 0)
+    cfg = wl.cfg
+    src, dst, cc = wl.epoch()
+    nb = (src.size + cfg.batch - 1) // cfg.batch
+    say(f"tiny epoch {scatter}: {src.size} positives, {nb} steps")
+    tr = _trainer(cfg.num_nodes, cfg.dim, cfg.num_neg, cfg.batch, seed=0, scatter=scatter)
+    losses = torch.zeros(nb, dtype=torch.float64, device="cuda")
+    ds, dd, dc = dev(src, torch), dev(dst, torch), dev(cc, torch)
+    for b in range(nb):
+        lo, hi = b * cfg.batch, min(src.size, (b + 1) * cfg.batch)
+        tr.step(ds[lo:hi], dd[lo:hi], dc[lo:hi], lo, cfg.lr, loss_out=losses[b:b + 1])
+    gl = losses.cpu().numpy()
+    a = _half(cfg.dim)
+    ids = np.arange(cfg.num_nodes)
+    S = orc.init_rows(0, 0, ids, cfg.dim, a)
+    T = orc.init_rows(0, 1, ids, cfg.dim, a)
+    ol = np.zeros(nb)
+    csum = np.zeros(nb)
+    for b in range(nb):
+        lo, hi = b * cfg.batch, min(src.size, (b + 1) * cfg.batch)
+        neg = orc.sample_negatives(0, lo, hi - lo, cfg.num_neg, cfg.num_nodes)
+        ol[b] = orc.step_dense(S, T, src[lo:hi], dst[lo:hi], cc[lo:hi], neg, cfg.lr)
+        csum[b] = cc[lo:hi].sum()
+    gm, om = gl / csum, ol / csum
+    err = np.abs(gm - om) / np.maximum(1.0, np.abs(om))
+    say(f"  mean loss first {om[0]:.5f} last {om[-1]:.5f}; max rel err {err.max():.2e}")
+    assert err.max() <= 1e-3
+    assert om[-1] < om[0]  # it learns
+    # tables after the epoch stay close to the oracle's
+    assert_close(tr.S.cpu().numpy(), S, "S after epoch", abs_tol=1e-4, rel_tol=1e-3)
+    assert_close(tr.T.cpu().numpy(), T, "T after epoch", abs_tol=1e-4, rel_tol=1e-3)

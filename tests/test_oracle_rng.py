@@ -238,3 +238,12 @@ def test_init_is_position_addressed():
     hi = orc.init_rows(9, 0, [5 + (1 << 32)], 8, a)
     lo = orc.init_rows(9, 0, [5], 8, a)
     assert not np.array_equal(hi, lo)
+
+
+def test_init_rows_agree_with_elementwise_definition():
+    rows = np.array([0, 3, 77, 2**33 + 5])
+    for dim in (4, 10, 32):
+        R = orc.init_rows(17, 1, rows, dim, np.float32(0.02))
+        for a, r in enumerate(rows):
+            for c in range(dim):
+                assert R[a, c] == np.float32(orc.init_value(17, 1, int(r), c, 0.02))
