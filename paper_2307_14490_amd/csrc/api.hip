@@ -88,8 +88,11 @@ Layout make_layout(const huge_config* c) {
         L.vals1 = take(sizeof(uint32_t) * (size_t)M);
         L.info = take(sizeof(int32_t) * (size_t)M);
         L.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kRadixBins));
-        L.work = take(sizeof(uint4) * (size_t)M);
-        L.longseg = take(sizeof(uint2) * (size_t)(M / kChunk + 2));
+        const int64_t windows = M / kChunk + 2;
+        L.work = take(sizeof(uint4) * (size_t)(windows * kChunk));
+        L.wcount = take(sizeof(uint32_t) * (size_t)windows);
+        L.longhead = take(sizeof(uint32_t) * (size_t)windows);
+        L.wstats = take(sizeof(uint32_t) * (size_t)(windows * 3));
         L.partA = take(sizeof(double) * (size_t)((M / kChunk + 2) * D));
         L.partB = take(sizeof(double) * (size_t)((M / kChunk + 2) * D));
         L.dup = take(sizeof(float) * (size_t)(M * D));
@@ -256,17 +259,20 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
         if (!mark(2)) return HUGE_ERR_HIP;
         int32_t* info = at<int32_t>(h, L.info);
         uint4* work = at<uint4>(h, L.work);
-        uint2* longseg = at<uint2>(h, L.longseg);
+        uint32_t* wcount = at<uint32_t>(h, L.wcount);
+        uint32_t* longhead = at<uint32_t>(h, L.longhead);
+        uint32_t* wstats = at<uint32_t>(h, L.wstats);
         double* partA = at<double>(h, L.partA);
         double* partB = at<double>(h, L.partB);
         float* dup = at<float>(h, L.dup);
-        HIP_TRY(launch_mark(ctl, keys[cur], vals[cur], m, t.N, info, work, longseg, s));
+        HIP_TRY(launch_mark(ctl, keys[cur], vals[cur], m, t.N, info, work, wcount, longhead,
+                            wstats, s));
         if (!mark(3)) return HUGE_ERR_HIP;
         HIP_TRY(launch_fused_step(t, ctl, a, neg, info, dup, lossp, &blocks, s));
         if (!mark(4)) return HUGE_ERR_HIP;
         if (m > 0) {
-            HIP_TRY(launch_dup_apply(t, ctl, work, dup, partA, partB, lr, m, s));
-            HIP_TRY(launch_long_combine(t, ctl, longseg, keys[cur], m, partA, partB, lr, s));
+            HIP_TRY(launch_dup_apply(t, ctl, work, wcount, dup, partA, partB, lr, m, s));
+            HIP_TRY(launch_long_combine(t, ctl, longhead, keys[cur], m, partA, partB, lr, s));
         }
         if (!mark(5)) return HUGE_ERR_HIP;
         h->last_m = m;
@@ -345,14 +351,26 @@ huge_status huge_check(huge_handle* h, void* stream) {
 huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
                             int64_t* unique_ctx, int64_t* dup_occurrences) {
     if (!h) return HUGE_ERR_INVALID_ARG;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    Control c;
-    HIP_TRY(hipMemcpyAsync(&c, h->ws + h->lay.ctrl, sizeof(Control), hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
-    if (unique_src) *unique_src = sorted ? (int64_t)c.uniq_S : -1;
-    if (unique_ctx) *unique_ctx = sorted ? (int64_t)c.uniq_T : -1;
-    if (dup_occurrences) *dup_occurrences = sorted ? (int64_t)c.dup_occ : -1;
+    int64_t a = -1, b = -1, c = -1;
+    if (sorted) {
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        const int64_t windows = (h->last_m + kChunk - 1) / kChunk;
+        std::vector<uint32_t> w((size_t)windows * 3);
+        if (windows > 0)
+            HIP_TRY(hipMemcpyAsync(w.data(), h->ws + h->lay.wstats, w.size() * sizeof(uint32_t),
+                                   hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        a = b = c = 0;
+        for (int64_t i = 0; i < windows; ++i) {
+            a += w[(size_t)i * 3];
+            b += w[(size_t)i * 3 + 1];
+            c += w[(size_t)i * 3 + 2];
+        }
+    }
+    if (unique_src) *unique_src = a;
+    if (unique_ctx) *unique_ctx = b;
+    if (dup_occurrences) *dup_occurrences = c;
     return HUGE_OK;
 }
 

@@ -14,9 +14,12 @@ constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
 constexpr int kRadixBits = 8;          // digit width of the LSD radix sort
 constexpr int kRadixBins = 1 << kRadixBits;
 constexpr int kMaxPasses = 4;          // keys < 2^32
-constexpr int kSortItems = 16;         // keys per thread in a sort tile
-constexpr int kSortTile = kBlock * kSortItems;  // 4096 keys per tile
+constexpr int kSortItems = 32;         // keys per thread in a sort tile
+constexpr int kSortTile = kBlock * kSortItems;  // 8192 keys per tile
+constexpr int kLookBatch = 8;          // look-back words read together
 constexpr int kChunk = 256;            // sorted positions per duplicate-sum window
+constexpr uint32_t kNoHead = 0xFFFFFFFFu;
+constexpr int kSamplePer = 8;          // positives per thread in the sampler
 constexpr int kNegBlock = 8;           // negatives whose rows are in flight together
 constexpr int kMaxNeg = 64;
 constexpr int kMaxDim = 1024;
@@ -31,11 +34,7 @@ struct Control {
     uint32_t step_bad;               // this call's input is invalid: skip all writes
     uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
     uint32_t tickets[kMaxPasses];    // dynamic tile ids of the radix passes
-    uint32_t n_work;                 // duplicate pieces found by the run marking
-    uint32_t n_long;                 // repeated rows spanning several windows
-    uint32_t uniq_S, uniq_T;         // distinct rows in the last sorted step
-    uint32_t dup_occ;                // occurrences that fell in a repeated row
-    uint32_t pad[5];
+    uint32_t pad[10];
 };
 
 // Byte offsets of the workspace regions (all 256-byte aligned).
@@ -48,8 +47,10 @@ struct Layout {
     size_t keys0 = 0, keys1 = 0, vals0 = 0, vals1 = 0;  // u32 [M]
     size_t info = 0;     // i32 [M]: -1 = row occurs once, else sorted position
     size_t status = 0;   // u64 [sort_tiles * 256] look-back words
-    size_t work = 0;     // uint4 [M] duplicate pieces
-    size_t longseg = 0;  // uint2 [M / kChunk + 1]
+    size_t work = 0;     // uint4 [M] duplicate pieces, kChunk slots per window
+    size_t wcount = 0;   // u32 [windows] pieces per window
+    size_t longhead = 0; // u32 [windows] start of a run continuing past the window
+    size_t wstats = 0;   // u32 [windows * 3] distinct S, distinct T, repeated occurrences
     size_t partA = 0, partB = 0;  // f64 [(M / kChunk + 2) * D] partial sums
     size_t dup = 0;      // f32 [M * D] per-occurrence contributions of repeated rows
     // atomic scatter
@@ -112,14 +113,15 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
                              const uint32_t* hist, uint64_t* status, uint32_t tag,
                              hipStream_t s);
 hipError_t launch_mark(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
-                       int64_t N, int32_t* info, uint4* work, uint2* longseg, hipStream_t s);
+                       int64_t N, int32_t* info, uint4* work, uint32_t* wcount,
+                       uint32_t* longhead, uint32_t* wstats, hipStream_t s);
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, const int32_t* info, float* dup,
                              double* lossp, int64_t* blocks_out, hipStream_t s);
 hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
-                            const float* dup, double* partA, double* partB, float lr,
-                            int64_t max_work, hipStream_t s);
-hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint2* longseg,
+                            const uint32_t* wcount, const float* dup, double* partA,
+                            double* partB, float lr, int64_t m, hipStream_t s);
+hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t* longhead,
                                const uint32_t* keys, int64_t m, const double* partA,
                                const double* partB, float lr, hipStream_t s);
 hipError_t launch_loss_final(Control* ctl, const double* lossp, int64_t blocks, double* out,

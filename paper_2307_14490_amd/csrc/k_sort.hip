@@ -29,7 +29,7 @@ __device__ __forceinline__ uint64_t lb_load(const uint64_t* p) {
 }
 
 // One pass of 8 bits at shift 8 * pass.  Tile = kSortTile consecutive items,
-// wave w of the tile owns items [w * 1024, (w + 1) * 1024) in 16 rounds of 64.
+// wave w of the tile owns a quarter of them, in kSortItems rounds of 64.
 // Within a round, lanes with the same digit are found with 8 ballots; the
 // round's count per digit is added to the wave's LDS counter by one lane,
 // whose old value orders the round after the earlier ones.
@@ -108,20 +108,37 @@ __global__ __launch_bounds__(kBlock) void k_radix_pass(
     s_wave[2][d] = c0 + c1;
     s_wave[3][d] = c0 + c1 + c2;
 
-    // Decoupled look-back over the tiles before this one, for digit d.
+    // Decoupled look-back over the tiles before this one, for digit d: the
+    // words of kLookBatch predecessors are read together, then consumed in
+    // order until an inclusive prefix is met.
     uint64_t* my = status + tile * kRadixBins + d;
     uint32_t excl = 0;
     if (tile == 0) {
         lb_store(my, lb_word(tag, kFlagPrefix, tile_count));
     } else {
         lb_store(my, lb_word(tag, kFlagAggregate, tile_count));
+        const uint32_t want = tag & 0x3FFFFFFFu;
         int64_t look = tile - 1;
         uint32_t spins = 0;
-        while (true) {
-            const uint64_t w = lb_load(status + look * kRadixBins + d);
-            const uint32_t wtag = (uint32_t)(w >> 34);
-            const uint64_t flag = (w >> 32) & 3ull;
-            if (wtag != (tag & 0x3FFFFFFFu) || flag == 0ull) {
+        bool done = false;
+        while (!done) {
+            uint64_t w[kLookBatch];
+#pragma unroll
+            for (int j = 0; j < kLookBatch; ++j)
+                w[j] = (look - j >= 0) ? lb_load(status + (look - j) * kRadixBins + d)
+                                       : lb_word(want, kFlagPrefix, 0u);
+            int used = 0;
+#pragma unroll
+            for (int j = 0; j < kLookBatch; ++j) {
+                if (done || used != j) break;
+                const uint64_t flag = (w[j] >> 32) & 3ull;
+                if ((uint32_t)(w[j] >> 34) != want || flag == 0ull) break;
+                excl += (uint32_t)w[j];
+                used = j + 1;
+                if (flag == kFlagPrefix) done = true;
+            }
+            look -= used;
+            if (!done && used < kLookBatch) {
                 // every earlier tile is resident (it holds a smaller ticket) and
                 // publishes without waiting; the bound only guards against a
                 // broken invariant, turning it into a reported error
@@ -130,11 +147,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_pass(
                     break;
                 }
                 __builtin_amdgcn_s_sleep(1);
-                continue;
             }
-            excl += (uint32_t)w;
-            if (flag == kFlagPrefix) break;
-            --look;
         }
         lb_store(my, lb_word(tag, kFlagPrefix, excl + tile_count));
     }
@@ -170,81 +183,97 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
 }
 
 // ---------------------------------------------------------------------------
-// Run marking on the sorted keys.  Position j (occurrence o = vals[j]):
+// Run marking on the sorted keys, one workgroup per window of kChunk sorted
+// positions.  Position j (occurrence o = vals[j]):
 //   info[o] = -1 if its key occurs once, else j (its slot in the duplicate
-//   buffer).  Runs of a repeated key are cut into pieces at multiples of
-//   kChunk; each piece becomes a work item {start, len, key, kind}:
+//   buffer).  Runs of a repeated key are cut into pieces at window
+//   boundaries; each piece becomes a work item {start, len, key, kind} stored
+//   in its window's slots work[w * kChunk ..]:
 //     kind 0: the whole run -> sum and update the row directly;
 //     kind 1: the run's first piece, the run continues past the window ->
-//             partial sum to partB[window];
-//     kind 2: a later piece, starting at a window boundary -> partA[window].
-//   Every run with a kind-1 piece is also listed in longseg {head, key}.
-// Distinct keys are counted per table, and occurrences in repeated rows.
+//             partial sum to partB[w]; longhead[w] = its start;
+//     kind 2: a later piece, starting at the window boundary -> partA[w].
+//   A window holds at most one kind-1 piece.  Per window: number of pieces,
+//   and {distinct source keys, distinct context keys, repeated occurrences}.
+// Everything is written without global atomics.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_mark(Control* ctl, const uint32_t* __restrict__ keys,
+__global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl,
+                                                 const uint32_t* __restrict__ keys,
                                                  const uint32_t* __restrict__ vals, int64_t m,
                                                  int64_t N, int32_t* __restrict__ info,
                                                  uint4* __restrict__ work,
-                                                 uint2* __restrict__ longseg) {
+                                                 uint32_t* __restrict__ wcount,
+                                                 uint32_t* __restrict__ longhead,
+                                                 uint32_t* __restrict__ wstats) {
+    static_assert(kChunk == kBlock, "one workgroup per window");
     __shared__ uint32_t s_cnt[3];
+    __shared__ uint32_t s_wave_emit[kBlock / 64];
+    __shared__ uint32_t s_long;
     if (ctl->step_bad) return;
-    if (threadIdx.x < 3) s_cnt[threadIdx.x] = 0u;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    if (tid < 3) s_cnt[tid] = 0u;
+    if (tid == 0) s_long = 0xFFFFFFFFu;
     __syncthreads();
-    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    const int lane = threadIdx.x & 63;
-    bool emit = false, emit_long = false;
+    const int64_t win = blockIdx.x;
+    const int64_t j = win * kChunk + tid;
+    bool emit = false, head_S = false, head_T = false, dup = false;
     uint4 rec = make_uint4(0, 0, 0, 0);
     if (j < m) {
         const uint32_t key = keys[j];
         const bool prev_same = j > 0 && keys[j - 1] == key;
         const bool next_same = j + 1 < m && keys[j + 1] == key;
-        const bool dup = prev_same || next_same;
+        dup = prev_same || next_same;
         const uint32_t o = vals[j];
         if ((int64_t)o < m) info[o] = dup ? (int32_t)j : -1;
-        if (!prev_same) atomicAdd(&s_cnt[(int64_t)key >= N ? 0 : 1], 1u);
-        if (dup) atomicAdd(&s_cnt[2], 1u);
-        if (dup && (!prev_same || (j % kChunk) == 0)) {
-            const int64_t win_end = (j / kChunk + 1) * kChunk;
+        head_S = !prev_same && (int64_t)key >= N;
+        head_T = !prev_same && (int64_t)key < N;
+        if (dup && (!prev_same || tid == 0)) {
+            const int64_t win_end = (win + 1) * kChunk;
             const int64_t lim = win_end < m ? win_end : m;
             int64_t e = j + 1;
             while (e < lim && keys[e] == key) ++e;
             const bool cont_after = (e == win_end) && (e < m) && keys[e] == key;
-            uint32_t kind;
-            if (!prev_same) kind = cont_after ? 1u : 0u;
-            else kind = 2u;
+            const uint32_t kind = !prev_same ? (cont_after ? 1u : 0u) : 2u;
             rec = make_uint4((uint32_t)j, (uint32_t)(e - j), key, kind);
             emit = true;
-            emit_long = kind == 1u;
+            if (kind == 1u) s_long = (uint32_t)j;
         }
     }
-    // one atomic per wave for the work list
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const uint64_t em = __ballot(emit);
-    if (em) {
-        const int first = __ffsll((long long)em) - 1;
-        uint32_t base = 0;
-        if (lane == first) base = atomicAdd(&ctl->n_work, (uint32_t)__popcll(em));
-        base = __shfl(base, first, 64);
-        const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        if (emit) work[base + __popcll(em & lt)] = rec;
-    }
-    if (emit_long) {
-        const uint32_t slot = atomicAdd(&ctl->n_long, 1u);
-        longseg[slot] = make_uint2(rec.x, rec.z);
+    const uint64_t bs = __ballot(head_S);
+    const uint64_t bt = __ballot(head_T);
+    const uint64_t bd = __ballot(dup);
+    if (lane == 0) {
+        s_wave_emit[wave] = (uint32_t)__popcll(em);
+        atomicAdd(&s_cnt[0], (uint32_t)__popcll(bs));
+        atomicAdd(&s_cnt[1], (uint32_t)__popcll(bt));
+        atomicAdd(&s_cnt[2], (uint32_t)__popcll(bd));
     }
     __syncthreads();
-    if (threadIdx.x < 3 && s_cnt[threadIdx.x]) {
-        uint32_t* dstc = threadIdx.x == 0 ? &ctl->uniq_S : threadIdx.x == 1 ? &ctl->uniq_T
-                                                                            : &ctl->dup_occ;
-        atomicAdd(dstc, s_cnt[threadIdx.x]);
+    uint32_t base = 0;
+    for (int w = 0; w < wave; ++w) base += s_wave_emit[w];
+    if (emit) work[win * kChunk + base + __popcll(em & lt)] = rec;
+    if (tid == 0) {
+        uint32_t total = 0;
+        for (int w = 0; w < kBlock / 64; ++w) total += s_wave_emit[w];
+        wcount[win] = total;
+        longhead[win] = s_long;
+        wstats[win * 3 + 0] = s_cnt[0];
+        wstats[win * 3 + 1] = s_cnt[1];
+        wstats[win * 3 + 2] = s_cnt[2];
     }
 }
 
 hipError_t launch_mark(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
-                       int64_t N, int32_t* info, uint4* work, uint2* longseg, hipStream_t s) {
-    const int64_t blocks = (m + kBlock - 1) / kBlock;
+                       int64_t N, int32_t* info, uint4* work, uint32_t* wcount,
+                       uint32_t* longhead, uint32_t* wstats, hipStream_t s) {
+    const int64_t blocks = (m + kChunk - 1) / kChunk;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_mark, dim3((unsigned)blocks), dim3(kBlock), 0, s, ctl, keys, vals, m, N,
-                       info, work, longseg);
+                       info, work, wcount, longhead, wstats);
     return hipGetLastError();
 }
 

@@ -267,44 +267,53 @@ __device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
 template <int G, int C>
 __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control* __restrict__ ctl,
                                                       const uint4* __restrict__ work,
+                                                      const uint32_t* __restrict__ wcount,
                                                       const float* __restrict__ dup,
                                                       double* __restrict__ partA,
-                                                      double* __restrict__ partB, float lr) {
+                                                      double* __restrict__ partB, float lr,
+                                                      int64_t windows) {
     if (ctl->step_bad) return;
     constexpr int PPB = kBlock / G;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
-    const int64_t nw = ctl->n_work;
-    for (int64_t w = (int64_t)blockIdx.x * PPB + grp; w < nw; w += (int64_t)gridDim.x * PPB) {
-        const uint4 rec = work[w];
-        double4_ acc[C];
-        sum_rows<G, C>(acc, dup, rec.x, rec.y, t.D, lane);
-        if (rec.w == 0u) {
-            apply_row<G, C>(t, rec.z, acc, lr, lane);
-        } else {
-            double* part = rec.w == 1u ? partB : partA;
-            PartIO<G, C>::store(part, (int64_t)(rec.x / kChunk), t.D, lane, acc);
+    for (int64_t w = (int64_t)blockIdx.x * PPB + grp; w < windows;
+         w += (int64_t)gridDim.x * PPB) {
+        const uint32_t cnt = wcount[w];
+        for (uint32_t p = 0; p < cnt; ++p) {
+            const uint4 rec = work[w * kChunk + p];
+            double4_ acc[C];
+            sum_rows<G, C>(acc, dup, rec.x, rec.y, t.D, lane);
+            if (rec.w == 0u) {
+                apply_row<G, C>(t, rec.z, acc, lr, lane);
+            } else {
+                double* part = rec.w == 1u ? partB : partA;
+                PartIO<G, C>::store(part, w, t.D, lane, acc);
+            }
         }
     }
 }
 
+// A run that spans windows: its first piece's partial sum (partB of the
+// head's window) plus the pieces of the following windows (partA), in
+// window order, then one update of the row.
 template <int G, int C>
 __global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Control* __restrict__ ctl,
-                                                         const uint2* __restrict__ longseg,
+                                                         const uint32_t* __restrict__ longhead,
                                                          const uint32_t* __restrict__ keys,
                                                          int64_t m, const double* __restrict__ partA,
                                                          const double* __restrict__ partB,
-                                                         float lr) {
+                                                         float lr, int64_t windows) {
     using IO = PartIO<G, C>;
     if (ctl->step_bad) return;
     constexpr int PPB = kBlock / G;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
-    const int64_t nl = ctl->n_long;
-    for (int64_t l = (int64_t)blockIdx.x * PPB + grp; l < nl; l += (int64_t)gridDim.x * PPB) {
-        const uint2 rec = longseg[l];
-        const uint32_t key = rec.y;
-        int64_t win = rec.x / kChunk;
+    for (int64_t w0 = (int64_t)blockIdx.x * PPB + grp; w0 < windows;
+         w0 += (int64_t)gridDim.x * PPB) {
+        const uint32_t head = longhead[w0];
+        if (head == kNoHead) continue;
+        const uint32_t key = keys[head];
+        int64_t win = w0;
         double4_ acc[C];
         IO::load(acc, partB, win, t.D, lane);
         while (true) {
@@ -325,31 +334,35 @@ __global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Cont
     }
 }
 
+static int64_t window_blocks(int G, int64_t windows) {
+    const int64_t ppb = kBlock / G;
+    int64_t blocks = (windows + ppb - 1) / ppb;
+    if (blocks > 4096) blocks = 4096;
+    return blocks < 1 ? 1 : blocks;
+}
+
 hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
-                            const float* dup, double* partA, double* partB, float lr,
-                            int64_t max_work, hipStream_t s) {
+                            const uint32_t* wcount, const float* dup, double* partA,
+                            double* partB, float lr, int64_t m, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
-    const int64_t ppb = kBlock / rs.G;
-    int64_t blocks = (max_work / 2 + ppb - 1) / ppb + 1;
-    if (blocks > 2048) blocks = 2048;
+    const int64_t windows = (m + kChunk - 1) / kChunk;
+    const int64_t blocks = window_blocks(rs.G, windows);
     HUGE_ROW_DISPATCH(rs, {
         hipLaunchKernelGGL((k_dup_apply<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t,
-                           ctl, work, dup, partA, partB, lr);
+                           ctl, work, wcount, dup, partA, partB, lr, windows);
     });
     return hipGetLastError();
 }
 
-hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint2* longseg,
+hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t* longhead,
                                const uint32_t* keys, int64_t m, const double* partA,
                                const double* partB, float lr, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
-    const int64_t ppb = kBlock / rs.G;
-    int64_t blocks = (m / kChunk + 1 + ppb - 1) / ppb;
-    if (blocks > 256) blocks = 256;
-    if (blocks < 1) blocks = 1;
+    const int64_t windows = (m + kChunk - 1) / kChunk;
+    const int64_t blocks = window_blocks(rs.G, windows);
     HUGE_ROW_DISPATCH(rs, {
         hipLaunchKernelGGL((k_long_combine<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
-                           t, ctl, longseg, keys, m, partA, partB, lr);
+                           t, ctl, longhead, keys, m, partA, partB, lr, windows);
     });
     return hipGetLastError();
 }

@@ -88,11 +88,6 @@ __global__ void k_begin(Control* ctl, uint32_t* hist) {
     if (t == 0) {
         ctl->step_bad = 0u;
         for (int p = 0; p < kMaxPasses; ++p) ctl->tickets[p] = 0u;
-        ctl->n_work = 0u;
-        ctl->n_long = 0u;
-        ctl->uniq_S = 0u;
-        ctl->uniq_T = 0u;
-        ctl->dup_occ = 0u;
     }
 }
 
@@ -116,7 +111,8 @@ hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Validation, negatives and sort keys.  One thread per positive i:
+// Validation, negatives and sort keys.  kSamplePer positives per thread
+// (coalesced rounds of one workgroup width); for each positive i:
 //   - checks 0 <= src, dst < N and co_count >= 0 (a failure flags the call);
 //   - draws the K negatives into neg[i K + k];
 //   - if keys != nullptr, writes the (2 + K) occurrence keys of positive i at
@@ -135,9 +131,10 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
         for (int j = threadIdx.x; j < passes * kRadixBins; j += kBlock) s_hist[j] = 0u;
         __syncthreads();
     }
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int K = t.K;
-    if (i < a.n) {
+    for (int r = 0; r < kSamplePer; ++r) {
+        const int64_t i = ((int64_t)blockIdx.x * kSamplePer + r) * kBlock + threadIdx.x;
+        if (i >= a.n) break;
         const uint64_t p = a.first_pos + (uint64_t)i;
         uint32_t key_s = 0, key_d = 0;
         if (a.src != nullptr) {
@@ -183,7 +180,8 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
 
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
                          uint32_t* keys, uint32_t* hist, int passes, hipStream_t s) {
-    const int64_t blocks = (a.n + kBlock - 1) / kBlock;
+    const int64_t per_block = (int64_t)kBlock * kSamplePer;
+    const int64_t blocks = (a.n + per_block - 1) / per_block;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
                        hist, passes);

@@ -97,7 +97,8 @@ STEP_CASES = [
 ]
 
 
-def _one_step(N, D, K, n, scatter, seed=7, weights=None, hub=0.0, cmax=5, lr=0.025):
+def _one_step(N, D, K, n, scatter, seed=7, weights=None, hub=0.0, cmax=5, lr=0.025,
+              heavy=None):
     rng = np.random.default_rng(N * 31 + D * 7 + K)
     src, dst, cc = _random_batch(rng, N, n, cmax=cmax, hub_frac=hub)
     first = 1000
@@ -123,6 +124,21 @@ def _one_step(N, D, K, n, scatter, seed=7, weights=None, hub=0.0, cmax=5, lr=0.0
     tT[neg.reshape(-1)] = True
     assert np.array_equal(S[~tS], S0[~tS]), "untouched source rows changed"
     assert np.array_equal(T[~tT], T0[~tT]), "untouched context rows changed"
+    if heavy is not None:
+        # Rows hit more than `heavy` times: fp32 atomics add thousands of
+        # cancelling terms in arbitrary order, so only the update as a whole
+        # is held to 1e-4 of its own size; every other row keeps the strict
+        # element-wise bound.
+        mS = np.bincount(src, minlength=N)
+        mT = np.bincount(np.concatenate([dst, neg.reshape(-1)]), minlength=N)
+        for name, G, R0, Rr, mult in (("S", S, S0, Sr, mS), ("T", T, T0, Tr, mT)):
+            hv = mult > heavy
+            for r in np.nonzero(hv)[0]:
+                upd = np.linalg.norm(Rr[r].astype(np.float64) - R0[r])
+                err = np.linalg.norm(G[r].astype(np.float64) - Rr[r])
+                assert err <= 1e-4 * upd + 1e-6, (name, r, err, upd)
+            tS = tS & ~hv if name == "S" else tS
+            tT = tT & ~hv if name == "T" else tT
     assert_close(S[tS], Sr[tS], f"S {scatter}")
     assert_close(T[tT], Tr[tT], f"T {scatter}")
     assert loss == pytest.approx(ref_loss, rel=1e-5, abs=1e-6)
@@ -146,9 +162,12 @@ def test_one_step_matches_oracle(scatter, N, D, K, n, note):
 @pytest.mark.parametrize("scatter", ["sorted", "atomic"])
 def test_hub_rows_and_large_counts(scatter):
     """Half the batch shares one source row, a quarter one destination row,
-    co_counts up to 1000: long runs split over several sum windows."""
+    co_counts up to 1000: long runs split over several sum windows.  The
+    sorted scatter sums repeated rows in double and meets the element-wise
+    bound everywhere; the atomic one is held to it on rows hit <= 64 times."""
     say(f"hub {scatter}")
-    _one_step(5_000, 64, 4, 6000, scatter, hub=0.5, cmax=1000)
+    _one_step(5_000, 64, 4, 6000, scatter, hub=0.5, cmax=1000,
+              heavy=None if scatter == "sorted" else 64)
 
 
 def test_alias_negatives_step():
