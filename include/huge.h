@@ -134,6 +134,24 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
                             const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                             float lr, double* d_loss_sum, void* stream);
 
+/* The same step in two halves, so that the next batch can be grouped on one
+   stream while the current one is applied on another (grouping never reads
+   or writes the tables).
+     huge_prepare_step   : validation, negative draws, de-duplication of the
+                           batch's rows, into the next of two grouping slots;
+                           at most two prepared batches may be pending
+     huge_train_prepared : the gather, loss and update of the oldest prepared
+                           batch, with the given lr and loss output
+   The library orders the halves with HIP events: an apply waits for its
+   grouping and for the previous apply; a grouping waits until the apply
+   that last used its slot is done.  The batch arrays must stay valid until
+   the batch is applied.  Results are bitwise those of huge_train_step, which
+   is the two halves on one stream and requires that no batch is pending. */
+huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                              const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
+                              void* stream);
+huge_status huge_train_prepared(huge_handle* h, float lr, double* d_loss_sum, void* stream);
+
 /* L of a batch at the current tables, with the negatives huge_train_step
    would draw for the same first_pos_index; writes nothing else. */
 huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
@@ -163,13 +181,14 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
 
 /* Phase timing.  After huge_profile_begin(h, max_steps), each of the next
    max_steps calls of huge_train_step records HIP events on its stream at the
-   phase boundaries.  huge_profile_end synchronises the stream, writes the
+   phase boundaries (groupings and applies on their own streams).
+   huge_profile_end waits for all of them on `stream`, writes the
    summed durations in milliseconds to phase_ms[HUGE_PHASES] and the number
-   of recorded steps to *steps, and releases the events.  Phases of the
-   sorted scatter: 0 set-up and negative sampling, 1 radix sort, 2 run
-   marking, 3 fused gather/loss/update kernel, 4 repeated rows, 5 loss sum.
-   Atomic scatter: 0 set-up and sampling, 1 gather and coefficients,
-   2 context-row atomics, 3 source-row atomics, 4 unused, 5 loss sum. */
+   of recorded steps to *steps, and releases the events.  Phases: 0 set-up
+   and negative sampling, 1 radix sort, 2 run marking (grouping; 1 and 2 are
+   empty for the atomic scatter), 3 the fused gather/loss/update kernel
+   (atomic scatter: gather and coefficients), 4 repeated rows (atomic
+   scatter: the atomic adds), 5 loss sum. */
 #define HUGE_PHASES 6
 huge_status huge_profile_begin(huge_handle* h, int32_t max_steps);
 huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int32_t* steps);

@@ -29,7 +29,7 @@ HUGE_SCATTER_ATOMIC = 1
 
 EXPORTED = [
     "huge_workspace_bytes", "huge_build_alias", "huge_init_tables", "huge_attach_tables",
-    "huge_train_step", "huge_eval_loss", "huge_get_rows", "huge_sample_negatives",
+    "huge_train_step", "huge_prepare_step", "huge_train_prepared", "huge_eval_loss", "huge_get_rows", "huge_sample_negatives",
     "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
     "huge_destroy", "huge_status_string",
 ]
@@ -77,6 +77,8 @@ def load() -> ctypes.CDLL:
                                      ctypes.POINTER(_vp)]
     L.huge_train_step.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64,
                                   ctypes.c_float, _vp, _vp]
+    L.huge_prepare_step.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64, _vp]
+    L.huge_train_prepared.argtypes = [_vp, ctypes.c_float, _vp, _vp]
     L.huge_eval_loss.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64, _vp, _vp]
     L.huge_get_rows.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp]
     L.huge_sample_negatives.argtypes = [_vp, ctypes.c_int64, ctypes.c_uint64, _vp, _vp]
@@ -91,6 +93,7 @@ def load() -> ctypes.CDLL:
     L.huge_status_string.argtypes = [ctypes.c_int32]
     L.huge_status_string.restype = ctypes.c_char_p
     for name in ("huge_build_alias", "huge_init_tables", "huge_attach_tables", "huge_train_step",
+                 "huge_prepare_step", "huge_train_prepared",
                  "huge_eval_loss", "huge_get_rows", "huge_sample_negatives", "huge_check",
                  "huge_step_stats", "huge_profile_begin", "huge_profile_end"):
         getattr(L, name).restype = ctypes.c_int32
@@ -193,6 +196,18 @@ class Trainer:
         _ok(load().huge_train_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
                                    int(first_pos), float(lr), None, _stream_ptr(stream)),
             "huge_train_step")
+
+    def prepare(self, src, dst, cc, first_pos, stream=None):
+        """Group a batch (validation, negatives, de-duplication) into a slot."""
+        _ok(load().huge_prepare_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                     int(first_pos), _stream_ptr(stream)), "huge_prepare_step")
+
+    def train_prepared(self, lr, loss_out=None, with_loss=True, stream=None):
+        """Apply the oldest prepared batch; returns the loss tensor (or None)."""
+        loss = (self.loss_buf if loss_out is None else loss_out) if with_loss else None
+        _ok(load().huge_train_prepared(self._h, float(lr), _dptr(loss), _stream_ptr(stream)),
+            "huge_train_prepared")
+        return loss
 
     def eval_loss(self, src, dst, cc, first_pos, loss_out=None, stream=None):
         loss = self.loss_buf if loss_out is None else loss_out

@@ -1,5 +1,13 @@
 // C-ABI host layer of libhuge: argument checks, workspace layout, and the
 // launch sequence of each call on the caller's stream.
+//
+// A step has two halves.  Grouping (k_begin, k_sample, the radix passes,
+// k_mark) reads only the batch; applying (k_fused_step, the repeated-row
+// kernels, the loss) reads and writes the tables.  Two grouping slots let
+// the caller group batch t+1 on one stream while batch t is applied on
+// another; events recorded here order the two: an apply waits until its
+// slot's grouping is complete, a grouping waits until the previous apply
+// that used its slot is complete.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
@@ -12,6 +20,22 @@
 
 using namespace huge;
 
+namespace {
+
+constexpr int kSlots = 2;
+constexpr int kPrepEvents = 4;   // begin, after sampling, after sort, after marking
+constexpr int kApplyEvents = 4;  // begin, after fused step, after repeated rows, after loss
+
+struct PendingBatch {
+    const int32_t* src = nullptr;
+    const int32_t* dst = nullptr;
+    const int32_t* cc = nullptr;
+    int64_t n = 0;
+    uint64_t first_pos = 0;
+};
+
+}  // namespace
+
 struct huge_handle {
     huge_config cfg;
     float* S;
@@ -22,12 +46,16 @@ struct huge_handle {
     size_t ws_bytes;
     Layout lay;
     int passes;
-    uint32_t epoch;   // counts calls that use the look-back words
-    int64_t last_m;   // occurrences of the last sorted step
-    // phase timing: (HUGE_PHASES + 1) events per profiled step
-    std::vector<hipEvent_t> events;
-    int32_t prof_max = 0;
-    int32_t prof_used = 0;
+    uint32_t epoch;            // tags the look-back words of each grouping
+    int64_t prepared;          // groupings issued
+    int64_t applied;           // applies issued
+    int last_applied_slot;     // -1 before the first apply
+    PendingBatch pending[kSlots];
+    hipEvent_t ready[kSlots];  // grouping of the slot complete
+    hipEvent_t done[kSlots];   // apply of the slot complete
+    // phase timing
+    std::vector<hipEvent_t> prep_ev, apply_ev;
+    int32_t prof_max = 0, prof_prep = 0, prof_apply = 0;
 };
 
 namespace {
@@ -68,33 +96,40 @@ Layout make_layout(const huge_config* c) {
     const int64_t D = c->dim;
     const int64_t nb = c->max_batch;
     const int64_t M = nb * (2 + K);
+    const bool sorted = c->scatter_kind == HUGE_SCATTER_SORTED;
     L.max_occ = M;
     L.sort_tiles = (M + kSortTile - 1) / kSortTile;
-    L.loss_blocks = (nb + 0) / 1 + 1;  // bounded by one workgroup per positive
+    L.windows = M / kChunk + 2;
+    L.loss_blocks = nb + 1;  // at most one workgroup per positive
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t at = off;
         off = align_up(off + bytes);
         return at;
     };
-    L.ctrl = take(sizeof(Control));
-    L.hist = take(sizeof(uint32_t) * kMaxPasses * kRadixBins);
+    for (int s = 0; s < kSlots; ++s) {
+        SlotLayout& S = L.slot[s];
+        S.ctrl = take(sizeof(Control));
+        S.hist = take(sizeof(uint32_t) * kMaxPasses * kRadixBins);
+        S.neg = take(sizeof(int32_t) * (size_t)(nb * K));
+        if (sorted) {
+            S.keys0 = take(sizeof(uint32_t) * (size_t)M);
+            S.keys1 = take(sizeof(uint32_t) * (size_t)M);
+            S.vals0 = take(sizeof(uint32_t) * (size_t)M);
+            S.vals1 = take(sizeof(uint32_t) * (size_t)M);
+            S.info = take(sizeof(int32_t) * (size_t)M);
+            S.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kRadixBins));
+            S.work = take(sizeof(uint4) * (size_t)(L.windows * kChunk));
+            S.wcount = take(sizeof(uint32_t) * (size_t)L.windows);
+            S.longhead = take(sizeof(uint32_t) * (size_t)L.windows);
+            S.wstats = take(sizeof(uint32_t) * (size_t)(L.windows * 3));
+        }
+    }
+    L.eval_ctrl = take(sizeof(Control));
     L.lossp = take(sizeof(double) * (size_t)L.loss_blocks);
-    L.neg = take(sizeof(int32_t) * (size_t)(nb * K));
-    if (c->scatter_kind == HUGE_SCATTER_SORTED) {
-        L.keys0 = take(sizeof(uint32_t) * (size_t)M);
-        L.keys1 = take(sizeof(uint32_t) * (size_t)M);
-        L.vals0 = take(sizeof(uint32_t) * (size_t)M);
-        L.vals1 = take(sizeof(uint32_t) * (size_t)M);
-        L.info = take(sizeof(int32_t) * (size_t)M);
-        L.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kRadixBins));
-        const int64_t windows = M / kChunk + 2;
-        L.work = take(sizeof(uint4) * (size_t)(windows * kChunk));
-        L.wcount = take(sizeof(uint32_t) * (size_t)windows);
-        L.longhead = take(sizeof(uint32_t) * (size_t)windows);
-        L.wstats = take(sizeof(uint32_t) * (size_t)(windows * 3));
-        L.partA = take(sizeof(double) * (size_t)((M / kChunk + 2) * D));
-        L.partB = take(sizeof(double) * (size_t)((M / kChunk + 2) * D));
+    if (sorted) {
+        L.partA = take(sizeof(double) * (size_t)(L.windows * D));
+        L.partB = take(sizeof(double) * (size_t)(L.windows * D));
         L.dup = take(sizeof(float) * (size_t)(M * D));
     } else {
         L.gsrc = take(sizeof(float) * (size_t)(nb * D));
@@ -127,6 +162,26 @@ TableArgs table_args(huge_handle* h) {
         if ((expr) != hipSuccess) return HUGE_ERR_HIP;  \
     } while (0)
 
+void release_profile(huge_handle* h) {
+    for (hipEvent_t e : h->prep_ev)
+        if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : h->apply_ev)
+        if (e) (void)hipEventDestroy(e);
+    h->prep_ev.clear();
+    h->apply_ev.clear();
+    h->prof_max = h->prof_prep = h->prof_apply = 0;
+}
+
+void destroy_handle(huge_handle* h) {
+    if (!h) return;
+    release_profile(h);
+    for (int s = 0; s < kSlots; ++s) {
+        if (h->ready[s]) (void)hipEventDestroy(h->ready[s]);
+        if (h->done[s]) (void)hipEventDestroy(h->done[s]);
+    }
+    delete h;
+}
+
 huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* thr,
                    const int32_t* alias, void* ws, size_t ws_bytes, huge_handle** out) {
     if (!out) return HUGE_ERR_INVALID_ARG;
@@ -150,17 +205,31 @@ huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* t
     h->lay = L;
     h->passes = (key_bits(cfg->num_nodes) + kRadixBits - 1) / kRadixBits;
     h->epoch = 0;
-    h->last_m = 0;
+    h->prepared = h->applied = 0;
+    h->last_applied_slot = -1;
+    for (int s = 0; s < kSlots; ++s) h->ready[s] = h->done[s] = nullptr;
+    for (int s = 0; s < kSlots; ++s) {
+        if (hipEventCreateWithFlags(&h->ready[s], hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&h->done[s], hipEventDisableTiming) != hipSuccess) {
+            destroy_handle(h);
+            return HUGE_ERR_HIP;
+        }
+    }
     *out = h;
     return HUGE_OK;
 }
 
-// Zero the control block, and the look-back words, on the stream.
+// Zero the control blocks and the look-back words, on the stream.
 huge_status reset_workspace(huge_handle* h, hipStream_t s) {
-    HIP_TRY(hipMemsetAsync(h->ws + h->lay.ctrl, 0, sizeof(Control), s));
-    if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED)
-        HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.status),
-                                    h->lay.sort_tiles * kRadixBins, s));
+    for (int k = 0; k < kSlots; ++k) {
+        HIP_TRY(hipMemsetAsync(h->ws + h->lay.slot[k].ctrl, 0, sizeof(Control), s));
+        if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
+            HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
+                                        h->lay.sort_tiles * kRadixBins, s));
+            HIP_TRY(launch_fill_i32(at<int32_t>(h, h->lay.slot[k].info), -1, h->lay.max_occ, s));
+        }
+    }
+    HIP_TRY(hipMemsetAsync(h->ws + h->lay.eval_ctrl, 0, sizeof(Control), s));
     return HUGE_OK;
 }
 
@@ -169,6 +238,123 @@ huge_status check_batch_args(huge_handle* h, const int32_t* src, const int32_t* 
     if (!h) return HUGE_ERR_INVALID_ARG;
     if (n < 0 || n > h->cfg.max_batch) return HUGE_ERR_INVALID_ARG;
     if (n > 0 && (!src || !dst || !cc)) return HUGE_ERR_INVALID_ARG;
+    return HUGE_OK;
+}
+
+// Grouping of one batch into the next slot (launches only; arguments checked).
+huge_status group_batch(huge_handle* h, const int32_t* src, const int32_t* dst,
+                        const int32_t* cc, int64_t n, uint64_t first_pos, hipStream_t s) {
+    const int slot = (int)(h->prepared % kSlots);
+    const SlotLayout& SL = h->lay.slot[slot];
+    Control* ctl = at<Control>(h, SL.ctrl);
+    uint32_t* hist = at<uint32_t>(h, SL.hist);
+    int32_t* neg = at<int32_t>(h, SL.neg);
+    const TableArgs t = table_args(h);
+    const StepArgs a{src, dst, cc, n, first_pos, 0.0f, nullptr};
+    const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+
+    hipEvent_t* ev = nullptr;
+    if (h->prof_prep < h->prof_max) ev = &h->prep_ev[(size_t)h->prof_prep++ * kPrepEvents];
+    auto mark = [&](int k) -> bool {
+        return ev == nullptr || hipEventRecord(ev[k], s) == hipSuccess;
+    };
+
+    // the slot's previous apply must be complete before its buffers change
+    HIP_TRY(hipStreamWaitEvent(s, h->done[slot], 0));
+    if (!mark(0)) return HUGE_ERR_HIP;
+    HIP_TRY(launch_begin(ctl, hist, s));
+    if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
+        uint32_t* keys[2] = {at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1)};
+        uint32_t* vals[2] = {at<uint32_t>(h, SL.vals0), at<uint32_t>(h, SL.vals1)};
+        uint64_t* status = at<uint64_t>(h, SL.status);
+        HIP_TRY(launch_sample(t, ctl, a, neg, keys[0], at<int32_t>(h, SL.info), hist, h->passes,
+                              s));
+        if (!mark(1)) return HUGE_ERR_HIP;
+        // look-back tags: 8 per grouping; the words are cleared when the
+        // 30-bit tag wraps
+        h->epoch += 1;
+        if ((h->epoch & 0x07FFFFFFu) == 0u) {
+            for (int k = 0; k < kSlots; ++k)
+                HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
+                                            h->lay.sort_tiles * kRadixBins, s));
+            h->epoch += 1;
+        }
+        int cur = 0;
+        for (int p = 0; p < h->passes; ++p) {
+            const uint32_t tag = (h->epoch << 3) | (uint32_t)p;
+            HIP_TRY(launch_radix_pass(ctl, keys[cur], p == 0 ? nullptr : vals[cur], keys[cur ^ 1],
+                                      vals[cur ^ 1], m, p, hist, status, tag, s));
+            cur ^= 1;
+        }
+        if (!mark(2)) return HUGE_ERR_HIP;
+        HIP_TRY(launch_mark(ctl, keys[cur], vals[cur], m, t.N, at<int32_t>(h, SL.info),
+                            at<uint4>(h, SL.work), at<uint32_t>(h, SL.wcount),
+                            at<uint32_t>(h, SL.longhead), at<uint32_t>(h, SL.wstats), s));
+        if (!mark(3)) return HUGE_ERR_HIP;
+    } else {
+        HIP_TRY(launch_sample(t, ctl, a, neg, nullptr, nullptr, hist, 0, s));
+        if (!mark(1) || !mark(2) || !mark(3)) return HUGE_ERR_HIP;
+    }
+    HIP_TRY(hipEventRecord(h->ready[slot], s));
+    h->pending[slot] = PendingBatch{src, dst, cc, n, first_pos};
+    h->prepared += 1;
+    return HUGE_OK;
+}
+
+// Apply the oldest grouped batch (launches only).
+huge_status apply_batch(huge_handle* h, float lr, double* loss_out, hipStream_t s) {
+    const int slot = (int)(h->applied % kSlots);
+    const SlotLayout& SL = h->lay.slot[slot];
+    const Layout& L = h->lay;
+    Control* ctl = at<Control>(h, SL.ctrl);
+    const PendingBatch& b = h->pending[slot];
+    const TableArgs t = table_args(h);
+    const StepArgs a{b.src, b.dst, b.cc, b.n, b.first_pos, lr, loss_out};
+    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+    int32_t* neg = at<int32_t>(h, SL.neg);
+    double* lossp = at<double>(h, L.lossp);
+
+    hipEvent_t* ev = nullptr;
+    if (h->prof_apply < h->prof_max) ev = &h->apply_ev[(size_t)h->prof_apply++ * kApplyEvents];
+    auto mark = [&](int k) -> bool {
+        return ev == nullptr || hipEventRecord(ev[k], s) == hipSuccess;
+    };
+
+    HIP_TRY(hipStreamWaitEvent(s, h->ready[slot], 0));
+    // applies write the tables and share the apply regions: one at a time
+    if (h->last_applied_slot >= 0)
+        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
+    if (!mark(0)) return HUGE_ERR_HIP;
+    int64_t blocks = 0;
+    if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
+        const uint32_t* keys_sorted = at<uint32_t>(h, (h->passes & 1) ? SL.keys1 : SL.keys0);
+        double* partA = at<double>(h, L.partA);
+        double* partB = at<double>(h, L.partB);
+        float* dup = at<float>(h, L.dup);
+        HIP_TRY(launch_fused_step(t, ctl, a, neg, at<int32_t>(h, SL.info), dup, lossp, &blocks,
+                                  s));
+        if (!mark(1)) return HUGE_ERR_HIP;
+        if (m > 0) {
+            HIP_TRY(launch_dup_apply(t, ctl, at<uint4>(h, SL.work), at<uint32_t>(h, SL.wcount),
+                                     dup, partA, partB, lr, m, s));
+            HIP_TRY(launch_long_combine(t, ctl, at<uint32_t>(h, SL.longhead), keys_sorted, m,
+                                        partA, partB, lr, s));
+        }
+        if (!mark(2)) return HUGE_ERR_HIP;
+    } else {
+        float* gsrc = at<float>(h, L.gsrc);
+        float* coef = at<float>(h, L.coef);
+        HIP_TRY(launch_atomic_gather(t, ctl, a, neg, gsrc, coef, lossp, &blocks, s));
+        if (!mark(1)) return HUGE_ERR_HIP;
+        HIP_TRY(launch_atomic_scatter_T(t, ctl, a, neg, coef, s));
+        HIP_TRY(launch_atomic_scatter_S(t, ctl, a, gsrc, s));
+        if (!mark(2)) return HUGE_ERR_HIP;
+    }
+    if (loss_out) HIP_TRY(launch_loss_final(ctl, lossp, blocks, loss_out, s));
+    if (!mark(3)) return HUGE_ERR_HIP;
+    HIP_TRY(hipEventRecord(h->done[slot], s));
+    h->last_applied_slot = slot;
+    h->applied += 1;
     return HUGE_OK;
 }
 
@@ -192,7 +378,7 @@ huge_status huge_init_tables(const huge_config* cfg, float* d_S, float* d_T,
     if (st == HUGE_OK && launch_init(table_args(h), h->cfg.init_half_width, s) != hipSuccess)
         st = HUGE_ERR_HIP;
     if (st != HUGE_OK) {
-        delete h;
+        destroy_handle(h);
         *out = nullptr;
     }
     return st;
@@ -206,7 +392,7 @@ huge_status huge_attach_tables(const huge_config* cfg, float* d_S, float* d_T,
     st = reset_workspace(*out, nullptr);
     if (st == HUGE_OK && hipStreamSynchronize(nullptr) != hipSuccess) st = HUGE_ERR_HIP;
     if (st != HUGE_OK) {
-        delete *out;
+        destroy_handle(*out);
         *out = nullptr;
     }
     return st;
@@ -218,80 +404,27 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
     huge_status st = check_batch_args(h, d_src, d_dst, d_cc, n);
     if (st != HUGE_OK) return st;
     if (!isfinite(lr)) return HUGE_ERR_INVALID_ARG;
+    if (h->prepared != h->applied) return HUGE_ERR_INVALID_ARG;  // a prepared batch is pending
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const Layout& L = h->lay;
-    Control* ctl = at<Control>(h, L.ctrl);
-    uint32_t* hist = at<uint32_t>(h, L.hist);
-    double* lossp = at<double>(h, L.lossp);
-    int32_t* neg = at<int32_t>(h, L.neg);
-    const TableArgs t = table_args(h);
-    StepArgs a{d_src, d_dst, d_cc, n, first_pos_index, lr, d_loss_sum};
-    const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+    st = group_batch(h, d_src, d_dst, d_cc, n, first_pos_index, s);
+    if (st != HUGE_OK) return st;
+    return apply_batch(h, lr, d_loss_sum, s);
+}
 
-    hipEvent_t* ev = nullptr;
-    if (h->prof_used < h->prof_max) {
-        ev = &h->events[(size_t)h->prof_used * (HUGE_PHASES + 1)];
-        h->prof_used += 1;
-    }
-    auto mark = [&](int k) -> bool { return ev == nullptr || hipEventRecord(ev[k], s) == hipSuccess; };
-    if (!mark(0)) return HUGE_ERR_HIP;
-    HIP_TRY(launch_begin(ctl, hist, s));
-    int64_t blocks = 0;
-    if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-        uint32_t* keys[2] = {at<uint32_t>(h, L.keys0), at<uint32_t>(h, L.keys1)};
-        uint32_t* vals[2] = {at<uint32_t>(h, L.vals0), at<uint32_t>(h, L.vals1)};
-        uint64_t* status = at<uint64_t>(h, L.status);
-        HIP_TRY(launch_sample(t, ctl, a, neg, keys[0], hist, h->passes, s));
-        if (!mark(1)) return HUGE_ERR_HIP;
-        // look-back tags: 8 per call; clear the words when the 30-bit tag wraps
-        h->epoch += 1;
-        if ((h->epoch & 0x07FFFFFFu) == 0u) {
-            HIP_TRY(launch_clear_status(status, L.sort_tiles * kRadixBins, s));
-            h->epoch += 1;
-        }
-        int cur = 0;
-        for (int p = 0; p < h->passes; ++p) {
-            const uint32_t tag = (h->epoch << 3) | (uint32_t)p;
-            HIP_TRY(launch_radix_pass(ctl, keys[cur], p == 0 ? nullptr : vals[cur], keys[cur ^ 1],
-                                      vals[cur ^ 1], m, p, hist, status, tag, s));
-            cur ^= 1;
-        }
-        if (!mark(2)) return HUGE_ERR_HIP;
-        int32_t* info = at<int32_t>(h, L.info);
-        uint4* work = at<uint4>(h, L.work);
-        uint32_t* wcount = at<uint32_t>(h, L.wcount);
-        uint32_t* longhead = at<uint32_t>(h, L.longhead);
-        uint32_t* wstats = at<uint32_t>(h, L.wstats);
-        double* partA = at<double>(h, L.partA);
-        double* partB = at<double>(h, L.partB);
-        float* dup = at<float>(h, L.dup);
-        HIP_TRY(launch_mark(ctl, keys[cur], vals[cur], m, t.N, info, work, wcount, longhead,
-                            wstats, s));
-        if (!mark(3)) return HUGE_ERR_HIP;
-        HIP_TRY(launch_fused_step(t, ctl, a, neg, info, dup, lossp, &blocks, s));
-        if (!mark(4)) return HUGE_ERR_HIP;
-        if (m > 0) {
-            HIP_TRY(launch_dup_apply(t, ctl, work, wcount, dup, partA, partB, lr, m, s));
-            HIP_TRY(launch_long_combine(t, ctl, longhead, keys[cur], m, partA, partB, lr, s));
-        }
-        if (!mark(5)) return HUGE_ERR_HIP;
-        h->last_m = m;
-    } else {
-        float* gsrc = at<float>(h, L.gsrc);
-        float* coef = at<float>(h, L.coef);
-        HIP_TRY(launch_sample(t, ctl, a, neg, nullptr, hist, 0, s));
-        if (!mark(1)) return HUGE_ERR_HIP;
-        HIP_TRY(launch_atomic_gather(t, ctl, a, neg, gsrc, coef, lossp, &blocks, s));
-        if (!mark(2)) return HUGE_ERR_HIP;
-        HIP_TRY(launch_atomic_scatter_T(t, ctl, a, neg, coef, s));
-        if (!mark(3)) return HUGE_ERR_HIP;
-        HIP_TRY(launch_atomic_scatter_S(t, ctl, a, gsrc, s));
-        if (!mark(4)) return HUGE_ERR_HIP;
-        if (!mark(5)) return HUGE_ERR_HIP;
-    }
-    if (d_loss_sum) HIP_TRY(launch_loss_final(ctl, lossp, blocks, d_loss_sum, s));
-    if (!mark(6)) return HUGE_ERR_HIP;
-    return HUGE_OK;
+huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                              const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
+                              void* stream) {
+    huge_status st = check_batch_args(h, d_src, d_dst, d_cc, n);
+    if (st != HUGE_OK) return st;
+    if (h->prepared - h->applied >= kSlots) return HUGE_ERR_INVALID_ARG;
+    return group_batch(h, d_src, d_dst, d_cc, n, first_pos_index,
+                       static_cast<hipStream_t>(stream));
+}
+
+huge_status huge_train_prepared(huge_handle* h, float lr, double* d_loss_sum, void* stream) {
+    if (!h || !isfinite(lr)) return HUGE_ERR_INVALID_ARG;
+    if (h->applied >= h->prepared) return HUGE_ERR_INVALID_ARG;  // nothing prepared
+    return apply_batch(h, lr, d_loss_sum, static_cast<hipStream_t>(stream));
 }
 
 huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
@@ -302,10 +435,13 @@ huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* 
     if (!d_loss_sum) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const Layout& L = h->lay;
-    Control* ctl = at<Control>(h, L.ctrl);
+    Control* ctl = at<Control>(h, L.eval_ctrl);
+    // the loss partials are shared with applies: order after the last one
+    if (h->last_applied_slot >= 0)
+        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
     double* lossp = at<double>(h, L.lossp);
     StepArgs a{d_src, d_dst, d_cc, n, first_pos_index, 0.0f, d_loss_sum};
-    HIP_TRY(launch_begin(ctl, at<uint32_t>(h, L.hist), s));
+    HIP_TRY(launch_begin(ctl, nullptr, s));
     int64_t blocks = 0;
     HIP_TRY(launch_eval(table_args(h), ctl, a, lossp, &blocks, s));
     HIP_TRY(launch_loss_final(ctl, lossp, blocks, d_loss_sum, s));
@@ -318,7 +454,8 @@ huge_status huge_get_rows(huge_handle* h, int32_t table, const int64_t* d_ids, i
     if (n == 0) return HUGE_OK;
     if (!d_ids || !d_out) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(launch_get_rows(table_args(h), at<Control>(h, h->lay.ctrl), table, d_ids, n, d_out, s));
+    HIP_TRY(launch_get_rows(table_args(h), at<Control>(h, h->lay.eval_ctrl), table, d_ids, n,
+                            d_out, s));
     return HUGE_OK;
 }
 
@@ -329,22 +466,33 @@ huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_
     if (!d_neg_out) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
     StepArgs a{nullptr, nullptr, nullptr, n, first_pos_index, 0.0f, nullptr};
-    HIP_TRY(launch_sample(table_args(h), at<Control>(h, h->lay.ctrl), a, d_neg_out, nullptr,
-                          nullptr, 0, s));
+    HIP_TRY(launch_sample(table_args(h), at<Control>(h, h->lay.eval_ctrl), a, d_neg_out, nullptr,
+                          nullptr, nullptr, 0, s));
     return HUGE_OK;
 }
 
 huge_status huge_check(huge_handle* h, void* stream) {
     if (!h) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    Control* ctl = at<Control>(h, h->lay.ctrl);
-    uint32_t err = 0;
-    HIP_TRY(hipMemcpyAsync(&err, &ctl->error, sizeof(err), hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipMemsetAsync(&ctl->error, 0, sizeof(uint32_t), s));
+    // every grouping and apply issued so far, on any stream
+    for (int k = 0; k < kSlots; ++k) {
+        HIP_TRY(hipStreamWaitEvent(s, h->ready[k], 0));
+        HIP_TRY(hipStreamWaitEvent(s, h->done[k], 0));
+    }
+    const size_t ctrls[3] = {h->lay.slot[0].ctrl, h->lay.slot[1].ctrl, h->lay.eval_ctrl};
+    uint32_t err[3] = {0, 0, 0};
+    for (int k = 0; k < 3; ++k) {
+        Control* c = at<Control>(h, ctrls[k]);
+        HIP_TRY(hipMemcpyAsync(&err[k], &c->error, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemsetAsync(&c->error, 0, sizeof(uint32_t), s));
+    }
     HIP_TRY(hipStreamSynchronize(s));
-    if (err == kBadId) return HUGE_ERR_ID_OUT_OF_RANGE;
-    if (err == kBadCount) return HUGE_ERR_BAD_COUNT;
-    if (err != 0) return HUGE_ERR_HIP;
+    uint32_t first = 0;
+    for (int k = 0; k < 3; ++k)
+        if (!first) first = err[k];
+    if (first == kBadId) return HUGE_ERR_ID_OUT_OF_RANGE;
+    if (first == kBadCount) return HUGE_ERR_BAD_COUNT;
+    if (first != 0) return HUGE_ERR_HIP;
     return HUGE_OK;
 }
 
@@ -353,13 +501,16 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
     if (!h) return HUGE_ERR_INVALID_ARG;
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
     int64_t a = -1, b = -1, c = -1;
-    if (sorted) {
+    if (sorted && h->last_applied_slot >= 0) {
+        const int slot = h->last_applied_slot;
         hipStream_t s = static_cast<hipStream_t>(stream);
-        const int64_t windows = (h->last_m + kChunk - 1) / kChunk;
+        HIP_TRY(hipStreamWaitEvent(s, h->done[slot], 0));
+        const int64_t m = h->pending[slot].n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+        const int64_t windows = (m + kChunk - 1) / kChunk;
         std::vector<uint32_t> w((size_t)windows * 3);
         if (windows > 0)
-            HIP_TRY(hipMemcpyAsync(w.data(), h->ws + h->lay.wstats, w.size() * sizeof(uint32_t),
-                                   hipMemcpyDeviceToHost, s));
+            HIP_TRY(hipMemcpyAsync(w.data(), h->ws + h->lay.slot[slot].wstats,
+                                   w.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
         a = b = c = 0;
         for (int64_t i = 0; i < windows; ++i) {
@@ -374,56 +525,56 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
     return HUGE_OK;
 }
 
-static void release_events(huge_handle* h) {
-    for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
-    h->events.clear();
-    h->prof_max = 0;
-    h->prof_used = 0;
-}
-
 huge_status huge_profile_begin(huge_handle* h, int32_t max_steps) {
     if (!h || max_steps < 1 || max_steps > 1000000) return HUGE_ERR_INVALID_ARG;
-    release_events(h);
-    h->events.resize((size_t)max_steps * (HUGE_PHASES + 1), nullptr);
-    for (auto& e : h->events) {
-        if (hipEventCreate(&e) != hipSuccess) {
-            e = nullptr;
-            release_events(h);
-            return HUGE_ERR_HIP;
+    release_profile(h);
+    h->prep_ev.assign((size_t)max_steps * kPrepEvents, nullptr);
+    h->apply_ev.assign((size_t)max_steps * kApplyEvents, nullptr);
+    for (std::vector<hipEvent_t>* v : {&h->prep_ev, &h->apply_ev}) {
+        for (hipEvent_t& e : *v) {
+            if (hipEventCreate(&e) != hipSuccess) {
+                e = nullptr;
+                release_profile(h);
+                return HUGE_ERR_HIP;
+            }
         }
     }
     h->prof_max = max_steps;
-    h->prof_used = 0;
     return HUGE_OK;
 }
 
 huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int32_t* steps) {
     if (!h || !phase_ms || !steps) return HUGE_ERR_INVALID_ARG;
-    hipStream_t s = static_cast<hipStream_t>(stream);
     huge_status st = HUGE_OK;
-    if (hipStreamSynchronize(s) != hipSuccess) st = HUGE_ERR_HIP;
-    for (int k = 0; k < HUGE_PHASES; ++k) phase_ms[k] = 0.0;
-    for (int32_t i = 0; st == HUGE_OK && i < h->prof_used; ++i) {
-        hipEvent_t* ev = &h->events[(size_t)i * (HUGE_PHASES + 1)];
-        for (int k = 0; k < HUGE_PHASES; ++k) {
-            float ms = 0.0f;
-            if (hipEventElapsedTime(&ms, ev[k], ev[k + 1]) != hipSuccess) {
-                st = HUGE_ERR_HIP;
-                break;
-            }
-            phase_ms[k] += (double)ms;
-        }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int k = 0; k < kSlots; ++k) {
+        if (hipStreamWaitEvent(s, h->ready[k], 0) != hipSuccess ||
+            hipStreamWaitEvent(s, h->done[k], 0) != hipSuccess)
+            st = HUGE_ERR_HIP;
     }
-    *steps = h->prof_used;
-    release_events(h);
+    if (st == HUGE_OK && hipStreamSynchronize(s) != hipSuccess) st = HUGE_ERR_HIP;
+    for (int k = 0; k < HUGE_PHASES; ++k) phase_ms[k] = 0.0;
+    auto sum = [&](const std::vector<hipEvent_t>& ev, int per, int used, int first_phase) {
+        for (int32_t i = 0; st == HUGE_OK && i < used; ++i) {
+            for (int k = 0; k + 1 < per; ++k) {
+                float ms = 0.0f;
+                if (hipEventElapsedTime(&ms, ev[(size_t)i * per + k],
+                                        ev[(size_t)i * per + k + 1]) != hipSuccess) {
+                    st = HUGE_ERR_HIP;
+                    break;
+                }
+                phase_ms[first_phase + k] += (double)ms;
+            }
+        }
+    };
+    sum(h->prep_ev, kPrepEvents, h->prof_prep, 0);
+    sum(h->apply_ev, kApplyEvents, h->prof_apply, 3);
+    *steps = h->prof_apply < h->prof_prep ? h->prof_apply : h->prof_prep;
+    release_profile(h);
     return st;
 }
 
-void huge_destroy(huge_handle* h) {
-    if (!h) return;
-    release_events(h);
-    delete h;
-}
+void huge_destroy(huge_handle* h) { destroy_handle(h); }
 
 const char* huge_status_string(huge_status st) {
     switch (st) {

@@ -14,12 +14,13 @@ constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
 constexpr int kRadixBits = 8;          // digit width of the LSD radix sort
 constexpr int kRadixBins = 1 << kRadixBits;
 constexpr int kMaxPasses = 4;          // keys < 2^32
-constexpr int kSortItems = 32;         // keys per thread in a sort tile
-constexpr int kSortTile = kBlock * kSortItems;  // 8192 keys per tile
-constexpr int kLookBatch = 8;          // look-back words read together
+constexpr int kSortThreads = 1024;     // threads of a sort workgroup (16 wave64)
+constexpr int kSortItems = 8;          // keys per thread in a sort tile
+constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 keys per tile
+constexpr int kLookBatch = 32;         // look-back words read together
 constexpr int kChunk = 256;            // sorted positions per duplicate-sum window
 constexpr uint32_t kNoHead = 0xFFFFFFFFu;
-constexpr int kSamplePer = 8;          // positives per thread in the sampler
+constexpr int kSamplePer = 2;          // positives per thread in the sampler
 constexpr int kNegBlock = 8;           // negatives whose rows are in flight together
 constexpr int kMaxNeg = 64;
 constexpr int kMaxDim = 1024;
@@ -38,19 +39,31 @@ struct Control {
 };
 
 // Byte offsets of the workspace regions (all 256-byte aligned).
-struct Layout {
-    size_t ctrl = 0;
+//
+// A batch is processed in two halves: grouping (validation, negatives, sort,
+// run marking) and applying (gather, loss, updates).  Grouping never touches
+// the tables, so the grouping of the next batch may run on another stream
+// while the current one is applied: each of the two grouping slots has its
+// own regions; the apply regions are shared (applies are ordered).
+struct SlotLayout {
+    size_t ctrl = 0;     // Control
     size_t hist = 0;     // u32 [kMaxPasses][256] global digit counts
-    size_t lossp = 0;    // double [loss_blocks]
     size_t neg = 0;      // i32 [max_batch * K]
     // sorted scatter
     size_t keys0 = 0, keys1 = 0, vals0 = 0, vals1 = 0;  // u32 [M]
-    size_t info = 0;     // i32 [M]: -1 = row occurs once, else sorted position
+    size_t info = 0;     // i32 [M]: -1, or the sorted position of an occurrence of a repeated row
     size_t status = 0;   // u64 [sort_tiles * 256] look-back words
     size_t work = 0;     // uint4 [M] duplicate pieces, kChunk slots per window
     size_t wcount = 0;   // u32 [windows] pieces per window
     size_t longhead = 0; // u32 [windows] start of a run continuing past the window
     size_t wstats = 0;   // u32 [windows * 3] distinct S, distinct T, repeated occurrences
+};
+
+struct Layout {
+    SlotLayout slot[2];
+    size_t eval_ctrl = 0;  // Control of huge_eval_loss
+    size_t lossp = 0;      // double [loss_blocks]
+    // sorted scatter
     size_t partA = 0, partB = 0;  // f64 [(M / kChunk + 2) * D] partial sums
     size_t dup = 0;      // f32 [M * D] per-occurrence contributions of repeated rows
     // atomic scatter
@@ -59,6 +72,7 @@ struct Layout {
     size_t total = 0;
     int64_t max_occ = 0;       // M = max_batch * (2 + K)
     int64_t sort_tiles = 0;
+    int64_t windows = 0;
     int64_t loss_blocks = 0;
 };
 
@@ -107,7 +121,8 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 hipError_t launch_begin(Control* ctl, uint32_t* hist, hipStream_t s);
 hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s);
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, uint32_t* hist, int passes, hipStream_t s);
+                         uint32_t* keys, int32_t* info, uint32_t* hist, int passes,
+                         hipStream_t s);
 hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
                              uint32_t* keys_out, uint32_t* vals_out, int64_t m, int pass,
                              const uint32_t* hist, uint64_t* status, uint32_t tag,
@@ -121,6 +136,7 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
                             const uint32_t* wcount, const float* dup, double* partA,
                             double* partB, float lr, int64_t m, hipStream_t s);
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t* longhead,
                                const uint32_t* keys, int64_t m, const double* partA,
                                const double* partB, float lr, hipStream_t s);

@@ -30,15 +30,13 @@ __device__ __forceinline__ void block_loss_a(float loss, double* __restrict__ ou
 // the (1 + K) coefficients and the source gradient.
 template <int G, int C, bool kDrawInline>
 __device__ __forceinline__ float forward_positive(const TableArgs& t, const StepArgs& a, int64_t i,
+                                                  int32_t u, int32_t v, float c,
                                                   const int32_t* __restrict__ neg, int lane,
                                                   float* __restrict__ coef,
                                                   float* __restrict__ gsrc) {
     using IO = RowIO<G, C>;
     const int K = t.K;
     const int32_t D = t.D;
-    const int32_t u = a.src[i];
-    const int32_t v = a.dst[i];
-    const float c = (float)a.cc[i];
     float4 s[C], t0[C], dS[C];
     IO::load(s, t.S, u, D, lane);
     IO::load(t0, t.T, v, D, lane);
@@ -93,7 +91,7 @@ __device__ __forceinline__ float forward_positive(const TableArgs& t, const Step
 }
 
 template <int G, int C>
-__global__ __launch_bounds__(kBlock) void k_atomic_gather(TableArgs t, const Control* __restrict__ ctl,
+__global__ __launch_bounds__(kBlock) void k_atomic_gather(TableArgs t, Control* __restrict__ ctl,
                                                           StepArgs a,
                                                           const int32_t* __restrict__ neg,
                                                           float* __restrict__ gsrc,
@@ -105,8 +103,16 @@ __global__ __launch_bounds__(kBlock) void k_atomic_gather(TableArgs t, const Con
     const int64_t i = (int64_t)blockIdx.x * PPB + threadIdx.x / G;
     float loss = 0.f;
     if (i < a.n) {
-        const float l = forward_positive<G, C, false>(t, a, i, neg, lane, coef, gsrc);
-        if (lane == 0) loss = l;
+        // validated when the batch was grouped; checked again so that a batch
+        // changed before its apply is reported instead of read out of bounds
+        const int32_t u = a.src[i], v = a.dst[i];
+        if (u >= 0 && (int64_t)u < t.N && v >= 0 && (int64_t)v < t.N) {
+            const float l = forward_positive<G, C, false>(t, a, i, u, v, (float)a.cc[i], neg, lane,
+                                                          coef, gsrc);
+            if (lane == 0) loss = l;
+        } else if (lane == 0) {
+            raise_error(ctl, kBadInternal);
+        }
     }
     block_loss_a(loss, lossp);
 }
@@ -123,13 +129,15 @@ __global__ __launch_bounds__(kBlock) void k_atomic_scatter_T(TableArgs t,
     const int lane = threadIdx.x % G;
     const int64_t i = (int64_t)blockIdx.x * PPB + threadIdx.x / G;
     if (i >= a.n) return;
+    const int32_t u = a.src[i], v = a.dst[i];
+    if (u < 0 || (int64_t)u >= t.N || v < 0 || (int64_t)v >= t.N) return;
     const int K = t.K;
     const int32_t D = t.D;
     const int q4 = D >> 2;
     float4 s[C];
-    IO::load(s, t.S, a.src[i], D, lane);
+    IO::load(s, t.S, u, D, lane);
     for (int j = 0; j <= K; ++j) {
-        const int64_t row = j == 0 ? (int64_t)a.dst[i] : (int64_t)neg[i * (int64_t)K + j - 1];
+        const int64_t row = j == 0 ? (int64_t)v : (int64_t)neg[i * (int64_t)K + j - 1];
         const float w = -a.lr * coef[i * (int64_t)(1 + K) + j];
         float* p = t.T + row * (int64_t)D;
 #pragma unroll
@@ -156,11 +164,13 @@ __global__ __launch_bounds__(kBlock) void k_atomic_scatter_S(TableArgs t,
     const int lane = threadIdx.x % G;
     const int64_t i = (int64_t)blockIdx.x * PPB + threadIdx.x / G;
     if (i >= a.n) return;
+    const int32_t u = a.src[i];
+    if (u < 0 || (int64_t)u >= t.N) return;
     const int32_t D = t.D;
     const int q4 = D >> 2;
     float4 g[C];
     IO::load(g, gsrc, i, D, lane);
-    float* p = t.S + (int64_t)a.src[i] * D;
+    float* p = t.S + (int64_t)u * D;
     const float w = -a.lr;
 #pragma unroll
     for (int q = 0; q < C; ++q) {
@@ -189,7 +199,8 @@ __global__ __launch_bounds__(kBlock) void k_eval(TableArgs t, Control* __restric
         if (!ok_id || c < 0) {
             if (lane == 0) raise_error(ctl, ok_id ? kBadCount : kBadId);
         } else {
-            const float l = forward_positive<G, C, true>(t, a, i, nullptr, lane, nullptr, nullptr);
+            const float l = forward_positive<G, C, true>(t, a, i, u, v, (float)c, nullptr, lane,
+                                                         nullptr, nullptr);
             if (lane == 0) loss = l;
         }
     }

@@ -28,20 +28,52 @@ __device__ __forceinline__ uint64_t lb_load(const uint64_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// One pass of 8 bits at shift 8 * pass.  Tile = kSortTile consecutive items,
-// wave w of the tile owns a quarter of them, in kSortItems rounds of 64.
-// Within a round, lanes with the same digit are found with 8 ballots; the
-// round's count per digit is added to the wave's LDS counter by one lane,
-// whose old value orders the round after the earlier ones.
-__global__ __launch_bounds__(kBlock) void k_radix_pass(
+// Inclusive sum over the first kRadixBins threads of the workgroup (one
+// value each): wave shuffles, then the wave totals through LDS.  Every
+// thread of the workgroup must call it (it synchronises); the others get 0.
+__device__ __forceinline__ uint32_t digit_inclusive_sum(uint32_t v, uint32_t* s_tmp) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const bool mine = threadIdx.x < kRadixBins;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = __shfl_up(v, off, 64);
+        if (lane >= off) v += t;
+    }
+    if (mine && lane == 63) s_tmp[wave] = v;
+    __syncthreads();
+    uint32_t add = 0;
+    if (mine)
+        for (int w = 0; w < wave; ++w) add += s_tmp[w];
+    return mine ? v + add : 0u;
+}
+
+// One pass of 8 bits at shift 8 * pass over a tile of kSortTile consecutive
+// items, kSortThreads threads; wave w owns items [w * 512, (w + 1) * 512) of
+// the tile in kSortItems rounds of 64.
+//   rank:    lanes of a round holding the same digit are found with 8
+//            ballots; one lane per digit adds the round's count to the wave's
+//            LDS counter, whose old value places the round after the earlier
+//            ones;
+//   publish: per digit (threads < 256), the tile's count; the items are
+//            then written to LDS in digit order (stable);
+//   look-back: the counts of earlier tiles, kLookBatch words at a time, up
+//            to the first inclusive prefix;
+//   write:   LDS position p goes to global position p + (digit's global
+//            offset - digit's tile offset): runs of equal digits are
+//            contiguous, so the writes coalesce.
+__global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     Control* __restrict__ ctl, uint32_t* __restrict__ tickets,
     const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m, int pass,
     const uint32_t* __restrict__ hist, uint64_t* __restrict__ status, uint32_t tag) {
-    __shared__ uint32_t s_wave[4][kRadixBins];
-    __shared__ uint32_t s_base[kRadixBins];
-    __shared__ uint32_t s_scan[kRadixBins];
+    constexpr int kWaves = kSortThreads / 64;
+    constexpr int kWaveItems = kSortTile / kWaves;
+    __shared__ uint32_t s_wave[kWaves][kRadixBins];
+    __shared__ int32_t s_delta[kRadixBins];
+    __shared__ uint32_t s_tmp[2][kRadixBins / 64];
     __shared__ uint32_t s_tile;
+    __shared__ uint32_t s_keys[kSortTile];
+    __shared__ uint32_t s_vals[kSortTile];
 
     if (ctl->step_bad) return;  // uniform: the call is a no-op
 
@@ -49,123 +81,159 @@ __global__ __launch_bounds__(kBlock) void k_radix_pass(
     const int wave = tid >> 6;
     const int lane = tid & 63;
     const int shift = pass * kRadixBits;
+    const bool digit_thread = tid < kRadixBins;
+    const int d = tid;  // the digit of threads < kRadixBins
 
-    for (int j = tid; j < 4 * kRadixBins; j += kBlock) (&s_wave[0][0])[j] = 0u;
+    for (int j = tid; j < kWaves * kRadixBins; j += kSortThreads) (&s_wave[0][0])[j] = 0u;
     if (tid == 0) s_tile = atomicAdd(tickets, 1u);
-    // global exclusive prefix of the digit counts (Hillis-Steele in LDS)
-    s_scan[tid] = hist[tid];
-    __syncthreads();
-    for (int off = 1; off < kRadixBins; off <<= 1) {
-        const uint32_t add = tid >= off ? s_scan[tid - off] : 0u;
-        __syncthreads();
-        s_scan[tid] += add;
-        __syncthreads();
-    }
-    const uint32_t global_excl = s_scan[tid] - hist[tid];
+    // Tiles are normally handed out in workgroup order: load that tile's
+    // items while the ticket is in flight, reload if it differs.
+    uint32_t key[kSortItems], val[kSortItems];
+    auto load_tile = [&](int64_t t) {
+        const int64_t base = t * kSortTile + (int64_t)wave * kWaveItems;
+#pragma unroll
+        for (int r = 0; r < kSortItems; ++r) {
+            const int64_t idx = base + r * 64 + lane;
+            const bool valid = idx < m;
+            key[r] = valid ? keys_in[idx] : 0u;
+            val[r] = valid ? (vals_in ? vals_in[idx] : (uint32_t)idx) : 0u;
+        }
+    };
+    load_tile(blockIdx.x);
+    const uint32_t hd = digit_thread ? hist[d] : 0u;
+    const uint32_t global_excl = digit_inclusive_sum(hd, s_tmp[0]) - hd;  // synchronises
     const int64_t tile = s_tile;
     if (tile >= (int64_t)gridDim.x) {  // tickets were not reset: refuse, never wait
         if (tid == 0) raise_error(ctl, kBadInternal);
         return;
     }
-    const int64_t base_idx = tile * kSortTile + (int64_t)wave * (kSortTile / 4);
+    if (tile != (int64_t)blockIdx.x) load_tile(tile);
+    const int64_t base_idx = tile * kSortTile + (int64_t)wave * kWaveItems;
 
-    uint32_t key[kSortItems], val[kSortItems], rank[kSortItems];
+    uint32_t rank[kSortItems];
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    {
+        uint32_t before[kSortItems], old[kSortItems];
+        int leader[kSortItems];
 #pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
-        const int64_t idx = base_idx + r * 64 + lane;
-        const bool valid = idx < m;
-        key[r] = valid ? keys_in[idx] : 0u;
-        val[r] = valid ? (vals_in ? vals_in[idx] : (uint32_t)idx) : 0u;
-    }
+        for (int r = 0; r < kSortItems; ++r) {
+            const bool valid = base_idx + r * 64 + lane < m;
+            const uint32_t dg = (key[r] >> shift) & (kRadixBins - 1);
+            uint64_t peers = __ballot(valid);
 #pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
-        const int64_t idx = base_idx + r * 64 + lane;
-        const bool valid = idx < m;
-        const uint32_t d = (key[r] >> shift) & (kRadixBins - 1);
-        uint64_t peers = __ballot(valid);
-#pragma unroll
-        for (int b = 0; b < kRadixBits; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t ones = __ballot(bit);
-            peers &= bit ? ones : ~ones;
+            for (int b = 0; b < kRadixBits; ++b) {
+                const bool bit = (dg >> b) & 1u;
+                const uint64_t ones = __ballot(bit);
+                peers &= bit ? ones : ~ones;
+            }
+            before[r] = (uint32_t)__popcll(peers & lt_mask);
+            const int ld = __ffsll((long long)peers) - 1;
+            leader[r] = ld < 0 ? 0 : ld;
+            old[r] = 0u;
+            if (valid && before[r] == 0)
+                old[r] = atomicAdd(&s_wave[wave][dg], (uint32_t)__popcll(peers));
         }
-        const uint32_t before = (uint32_t)__popcll(peers & lt_mask);
-        const int leader = __ffsll((long long)peers) - 1;
-        uint32_t old = 0;
-        if (valid && before == 0) old = atomicAdd(&s_wave[wave][d], (uint32_t)__popcll(peers));
-        old = __shfl(old, leader < 0 ? 0 : leader, 64);
-        rank[r] = old + before;
+#pragma unroll
+        for (int r = 0; r < kSortItems; ++r) rank[r] = __shfl(old[r], leader[r], 64) + before[r];
     }
     __syncthreads();
 
-    // Per digit: counts of the four waves -> exclusive offsets; tile count.
-    const int d = tid;
-    const uint32_t c0 = s_wave[0][d], c1 = s_wave[1][d], c2 = s_wave[2][d], c3 = s_wave[3][d];
-    const uint32_t tile_count = c0 + c1 + c2 + c3;
-    s_wave[0][d] = 0u;
-    s_wave[1][d] = c0;
-    s_wave[2][d] = c0 + c1;
-    s_wave[3][d] = c0 + c1 + c2;
+    // Per digit: wave offsets, tile count, publication.
+    uint32_t tile_count = 0;
+    uint32_t wcnt[kWaves];
+    if (digit_thread) {
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            wcnt[w] = s_wave[w][d];
+            tile_count += wcnt[w];
+        }
+        lb_store(status + tile * kRadixBins + d,
+                 lb_word(tag, tile == 0 ? kFlagPrefix : kFlagAggregate, tile_count));
+    }
+    const uint32_t local_excl = digit_inclusive_sum(tile_count, s_tmp[1]) - tile_count;
+    if (digit_thread) {
+        uint32_t run = local_excl;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            s_wave[w][d] = run;
+            run += wcnt[w];
+        }
+    }
+    __syncthreads();
 
-    // Decoupled look-back over the tiles before this one, for digit d: the
-    // words of kLookBatch predecessors are read together, then consumed in
-    // order until an inclusive prefix is met.
-    uint64_t* my = status + tile * kRadixBins + d;
-    uint32_t excl = 0;
-    if (tile == 0) {
-        lb_store(my, lb_word(tag, kFlagPrefix, tile_count));
-    } else {
-        lb_store(my, lb_word(tag, kFlagAggregate, tile_count));
-        const uint32_t want = tag & 0x3FFFFFFFu;
-        int64_t look = tile - 1;
-        uint32_t spins = 0;
-        bool done = false;
-        while (!done) {
-            uint64_t w[kLookBatch];
+    // Stable tile-local order in LDS.
 #pragma unroll
-            for (int j = 0; j < kLookBatch; ++j)
-                w[j] = (look - j >= 0) ? lb_load(status + (look - j) * kRadixBins + d)
-                                       : lb_word(want, kFlagPrefix, 0u);
-            int used = 0;
+    for (int r = 0; r < kSortItems; ++r) {
+        if (base_idx + r * 64 + lane < m) {
+            const uint32_t dg = (key[r] >> shift) & (kRadixBins - 1);
+            const uint32_t p = s_wave[wave][dg] + rank[r];
+            s_keys[p] = key[r];
+            s_vals[p] = val[r];
+        }
+    }
+
+    // Decoupled look-back over the tiles before this one, for digit d.
+    if (digit_thread) {
+        uint32_t excl = 0;
+        if (tile > 0) {
+            const uint32_t want = tag & 0x3FFFFFFFu;
+            int64_t look = tile - 1;
+            uint32_t spins = 0;
+            bool done = false;
+            while (!done) {
+                uint64_t w[kLookBatch];
 #pragma unroll
-            for (int j = 0; j < kLookBatch; ++j) {
-                if (done || used != j) break;
-                const uint64_t flag = (w[j] >> 32) & 3ull;
-                if ((uint32_t)(w[j] >> 34) != want || flag == 0ull) break;
-                excl += (uint32_t)w[j];
-                used = j + 1;
-                if (flag == kFlagPrefix) done = true;
-            }
-            look -= used;
-            if (!done && used < kLookBatch) {
-                // every earlier tile is resident (it holds a smaller ticket) and
-                // publishes without waiting; the bound only guards against a
-                // broken invariant, turning it into a reported error
-                if (++spins > (1u << 22)) {
-                    raise_error(ctl, kBadInternal);
-                    break;
+                for (int j = 0; j < kLookBatch; ++j)
+                    w[j] = (look - j >= 0) ? lb_load(status + (look - j) * kRadixBins + d)
+                                           : lb_word(want, kFlagPrefix, 0u);
+                int used = 0;
+                bool stop = false;
+#pragma unroll
+                for (int j = 0; j < kLookBatch; ++j) {
+                    if (!stop) {
+                        const uint64_t flag = (w[j] >> 32) & 3ull;
+                        if ((uint32_t)(w[j] >> 34) != want || flag == 0ull) {
+                            stop = true;
+                        } else {
+                            excl += (uint32_t)w[j];
+                            used = j + 1;
+                            if (flag == kFlagPrefix) {
+                                done = true;
+                                stop = true;
+                            }
+                        }
+                    }
                 }
-                __builtin_amdgcn_s_sleep(1);
+                look -= used;
+                if (!done && used < kLookBatch) {
+                    // every earlier tile is resident (it holds a smaller
+                    // ticket) and publishes without waiting; the bound only
+                    // guards against a broken invariant, turning it into a
+                    // reported error
+                    if (++spins > (1u << 22)) {
+                        raise_error(ctl, kBadInternal);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
             }
+            lb_store(status + tile * kRadixBins + d,
+                     lb_word(tag, kFlagPrefix, excl + tile_count));
         }
-        lb_store(my, lb_word(tag, kFlagPrefix, excl + tile_count));
+        s_delta[d] = (int32_t)(global_excl + excl) - (int32_t)local_excl;
     }
-    s_base[d] = global_excl + excl;
     __syncthreads();
 
-#pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
-        const int64_t idx = base_idx + r * 64 + lane;
-        if (idx < m) {
-            const uint32_t dd = (key[r] >> shift) & (kRadixBins - 1);
-            const uint32_t dest = s_base[dd] + s_wave[wave][dd] + rank[r];
-            if ((int64_t)dest < m) {
-                keys_out[dest] = key[r];
-                vals_out[dest] = val[r];
-            } else {
-                raise_error(ctl, kBadInternal);
-            }
+    const int64_t tile_base = tile * kSortTile;
+    const int64_t valid_n = (m - tile_base) < kSortTile ? (m - tile_base) : kSortTile;
+    for (int p = tid; p < valid_n; p += kSortThreads) {
+        const uint32_t k = s_keys[p];
+        const int64_t dest = (int64_t)s_delta[(k >> shift) & (kRadixBins - 1)] + p;
+        if (dest >= 0 && dest < m) {
+            keys_out[dest] = k;
+            vals_out[dest] = s_vals[p];
+        } else {
+            raise_error(ctl, kBadInternal);
         }
     }
 }
@@ -176,7 +244,7 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
                              hipStream_t s) {
     const int64_t tiles = (m + kSortTile - 1) / kSortTile;
     if (tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)tiles), dim3(kBlock), 0, s, ctl,
+    hipLaunchKernelGGL(k_radix_pass, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ctl,
                        &ctl->tickets[pass], keys_in, vals_in, keys_out, vals_out, m, pass,
                        hist + pass * kRadixBins, status, tag);
     return hipGetLastError();
@@ -185,8 +253,8 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
 // ---------------------------------------------------------------------------
 // Run marking on the sorted keys, one workgroup per window of kChunk sorted
 // positions.  Position j (occurrence o = vals[j]):
-//   info[o] = -1 if its key occurs once, else j (its slot in the duplicate
-//   buffer).  Runs of a repeated key are cut into pieces at window
+//   if its key occurs more than once, info[o] = j (its slot in the duplicate
+//   buffer); the sampler has set every entry of the batch to -1.  Runs of a repeated key are cut into pieces at window
 //   boundaries; each piece becomes a work item {start, len, key, kind} stored
 //   in its window's slots work[w * kChunk ..]:
 //     kind 0: the whole run -> sum and update the row directly;
@@ -209,14 +277,21 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
     __shared__ uint32_t s_cnt[3];
     __shared__ uint32_t s_wave_emit[kBlock / 64];
     __shared__ uint32_t s_long;
-    if (ctl->step_bad) return;
+    const int64_t win = blockIdx.x;
+    if (ctl->step_bad) {  // unsorted keys: no pieces, nothing marked
+        if (threadIdx.x == 0) {
+            wcount[win] = 0u;
+            longhead[win] = kNoHead;
+            wstats[win * 3 + 0] = wstats[win * 3 + 1] = wstats[win * 3 + 2] = 0u;
+        }
+        return;
+    }
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     if (tid < 3) s_cnt[tid] = 0u;
     if (tid == 0) s_long = 0xFFFFFFFFu;
     __syncthreads();
-    const int64_t win = blockIdx.x;
     const int64_t j = win * kChunk + tid;
     bool emit = false, head_S = false, head_T = false, dup = false;
     uint4 rec = make_uint4(0, 0, 0, 0);
@@ -225,8 +300,10 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
         const bool prev_same = j > 0 && keys[j - 1] == key;
         const bool next_same = j + 1 < m && keys[j + 1] == key;
         dup = prev_same || next_same;
-        const uint32_t o = vals[j];
-        if ((int64_t)o < m) info[o] = dup ? (int32_t)j : -1;
+        if (dup) {
+            const uint32_t o = vals[j];
+            if ((int64_t)o < m) info[o] = (int32_t)j;
+        }
         head_S = !prev_same && (int64_t)key >= N;
         head_T = !prev_same && (int64_t)key < N;
         if (dup && (!prev_same || tid == 0)) {

@@ -31,7 +31,7 @@ __device__ __forceinline__ void block_loss(float loss, double* __restrict__ out)
 }
 
 template <int G, int C>
-__global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, const Control* __restrict__ ctl,
+__global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __restrict__ ctl,
                                                        StepArgs a, const int32_t* __restrict__ neg,
                                                        const int32_t* __restrict__ info,
                                                        float* __restrict__ dup,
@@ -49,20 +49,23 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, const Contro
     float* __restrict__ T = t.T;
     float loss = 0.f;
 
-    if (i < a.n) {
-        const int32_t u = a.src[i];
-        const int32_t v = a.dst[i];
-        const float c = (float)a.cc[i];
-        const int64_t o = i * (int64_t)(2 + K);
-        const int32_t info_s = info[o];
-        const int32_t info_d = info[o + 1];
-        const int32_t* negi = neg + i * (int64_t)K;
-        const int32_t* infok = info + o + 2;
-
-        float4 s[C], t0[C], dS[C];
-        float4 tk[kNegBlock][C];
-        int32_t mk[kNegBlock], ik[kNegBlock];
-        int cnt = K < kNegBlock ? K : kNegBlock;
+    // Every index of the positive is loaded before any of them is used, so
+    // the loads overlap; ids were validated when the batch was grouped and
+    // are checked again so that a batch changed before its apply is reported
+    // instead of read out of bounds.
+    bool active = i < a.n;
+    int32_t u = 0, v = 0, cnt_i = 0, info_s = -1, info_d = -1;
+    int32_t mk[kNegBlock], ik[kNegBlock];
+    const int64_t o = i * (int64_t)(2 + K);
+    const int32_t* negi = neg + i * (int64_t)K;
+    const int32_t* infok = info + o + 2;
+    int cnt = K < kNegBlock ? K : kNegBlock;
+    if (active) {
+        u = a.src[i];
+        v = a.dst[i];
+        cnt_i = a.cc[i];
+        info_s = info[o];
+        info_d = info[o + 1];
 #pragma unroll
         for (int j = 0; j < kNegBlock; ++j) {
             if (j < cnt) {
@@ -70,6 +73,15 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, const Contro
                 ik[j] = infok[j];
             }
         }
+        if (u < 0 || (int64_t)u >= t.N || v < 0 || (int64_t)v >= t.N) {
+            if (lane == 0) raise_error(ctl, kBadInternal);
+            active = false;
+        }
+    }
+    if (active) {
+        const float c = (float)cnt_i;
+        float4 s[C], t0[C], dS[C];
+        float4 tk[kNegBlock][C];
         IO::load(s, S, u, D, lane);
         IO::load(t0, T, v, D, lane);
 #pragma unroll

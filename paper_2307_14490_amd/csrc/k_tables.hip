@@ -84,7 +84,8 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 // ---------------------------------------------------------------------------
 __global__ void k_begin(Control* ctl, uint32_t* hist) {
     const int t = threadIdx.x;
-    for (int i = t; i < kMaxPasses * kRadixBins; i += blockDim.x) hist[i] = 0u;
+    if (hist != nullptr)
+        for (int i = t; i < kMaxPasses * kRadixBins; i += blockDim.x) hist[i] = 0u;
     if (t == 0) {
         ctl->step_bad = 0u;
         for (int p = 0; p < kMaxPasses; ++p) ctl->tickets[p] = 0u;
@@ -102,6 +103,20 @@ __global__ __launch_bounds__(kBlock) void k_clear_u64(uint64_t* p, int64_t words
         p[i] = 0ull;
 }
 
+__global__ __launch_bounds__(kBlock) void k_fill_i32(int32_t* p, int32_t v, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kBlock)
+        p[i] = v;
+}
+
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s) {
+    int64_t blocks = (n + kBlock - 1) / kBlock;
+    if (blocks > 4096) blocks = 4096;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)blocks), dim3(kBlock), 0, s, p, v, n);
+    return hipGetLastError();
+}
+
 hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
     int64_t blocks = (words + kBlock - 1) / kBlock;
     if (blocks > 4096) blocks = 4096;
@@ -117,13 +132,15 @@ hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
 //   - draws the K negatives into neg[i K + k];
 //   - if keys != nullptr, writes the (2 + K) occurrence keys of positive i at
 //     o = i (2 + K) + slot: slot 0 the source row (key N + src), slot 1 the
-//     destination row (key dst), slots 2.. the negatives (key m), and counts
-//     the digits of every radix pass.
+//     destination row (key dst), slots 2.. the negatives (key m), sets their
+//     info entries to -1 (the run marking overwrites repeated ones) and
+//     counts the digits of every radix pass.
 // Without src (src == nullptr) only negatives are drawn.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, StepArgs a,
                                                    int32_t* __restrict__ neg,
                                                    uint32_t* __restrict__ keys,
+                                                   int32_t* __restrict__ info,
                                                    uint32_t* __restrict__ hist, int passes) {
     __shared__ uint32_t s_hist[kMaxPasses * kRadixBins];
     const bool with_keys = keys != nullptr;
@@ -153,6 +170,7 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
         if (with_keys) {
             keys[o] = key_s;
             keys[o + 1] = key_d;
+            for (int sl = 0; sl < 2 + K; ++sl) info[o + sl] = -1;
             for (int ps = 0; ps < passes; ++ps) {
                 atomicAdd(&s_hist[ps * kRadixBins + ((key_s >> (ps * kRadixBits)) & 255u)], 1u);
                 atomicAdd(&s_hist[ps * kRadixBins + ((key_d >> (ps * kRadixBits)) & 255u)], 1u);
@@ -179,12 +197,13 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
 }
 
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, uint32_t* hist, int passes, hipStream_t s) {
+                         uint32_t* keys, int32_t* info, uint32_t* hist, int passes,
+                         hipStream_t s) {
     const int64_t per_block = (int64_t)kBlock * kSamplePer;
     const int64_t blocks = (a.n + per_block - 1) / per_block;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
-                       hist, passes);
+                       info, hist, passes);
     return hipGetLastError();
 }
 

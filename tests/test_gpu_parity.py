@@ -326,3 +326,69 @@ def test_tiny_epoch_loss_curve(scatter):
     # tables after the epoch stay close to the oracle's
     assert_close(tr.S.cpu().numpy(), S, "S after epoch", abs_tol=1e-4, rel_tol=1e-3)
     assert_close(tr.T.cpu().numpy(), T, "T after epoch", abs_tol=1e-4, rel_tol=1e-3)
+
+
+# --------------------------------------------------------------------------- #
+# Grouping on one stream while the previous batch is applied on another
+# --------------------------------------------------------------------------- #
+def test_prepared_steps_on_two_streams_equal_train_step_bitwise():
+    N, D, K, n = 5000, 64, 5, 3000
+    rng = np.random.default_rng(17)
+    batches = [_random_batch(rng, N, n, hub_frac=0.2, cmax=50) for _ in range(5)]
+    ref = _trainer(N, D, K, n, seed=4)
+    ref_losses = []
+    for b, (s, d, c) in enumerate(batches):
+        ref_losses.append(ref.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n, 0.05).item())
+    tr = _trainer(N, D, K, n, seed=4)
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    dbs = [tuple(dev(x, torch) for x in b) for b in batches]
+    losses = torch.zeros(len(batches), dtype=torch.float64, device="cuda")
+    tr.prepare(*dbs[0], 0, stream=side)
+    for k in range(len(batches)):
+        tr.train_prepared(0.05, loss_out=losses[k:k + 1], stream=main)
+        if k + 1 < len(batches):
+            tr.prepare(*dbs[k + 1], (k + 1) * n, stream=side)
+    torch.cuda.synchronize()
+    assert tr.check() == 0
+    assert torch.equal(tr.S, ref.S) and torch.equal(tr.T, ref.T)
+    assert losses.cpu().tolist() == ref_losses
+
+
+def test_prepared_call_order_is_checked_on_host():
+    tr = _trainer(100, 16, 3, 64)
+    rng = np.random.default_rng(3)
+    s, d, c = (dev(x, torch) for x in _random_batch(rng, 100, 64))
+    with pytest.raises(P.HugeError):
+        tr.train_prepared(0.1)
+    tr.prepare(s, d, c, 0)
+    tr.prepare(s, d, c, 64)
+    with pytest.raises(P.HugeError):
+        tr.prepare(s, d, c, 128)  # both slots pending
+    with pytest.raises(P.HugeError):
+        tr.step(s, d, c, 128, 0.1)  # a prepared batch is pending
+    tr.train_prepared(0.1)
+    tr.train_prepared(0.1)
+    tr.step(s, d, c, 128, 0.1)
+    assert tr.check() == 0
+
+
+def test_invalid_prepared_batch_is_a_no_op():
+    N = 500
+    tr = _trainer(N, 16, 3, 64)
+    rng = np.random.default_rng(4)
+    s, d, c = _random_batch(rng, N, 64)
+    bad = s.copy()
+    bad[3] = N
+    S0 = tr.S.clone()
+    # the batch arrays must outlive their apply: keep them referenced
+    b1 = (dev(bad, torch), dev(d, torch), dev(c, torch))
+    b2 = (dev(s, torch), dev(d, torch), dev(c, torch))
+    tr.prepare(*b1, 0)
+    tr.prepare(*b2, 64)
+    l1 = tr.train_prepared(0.1, loss_out=torch.zeros(1, dtype=torch.float64, device="cuda"))
+    assert np.isnan(l1.item())
+    assert torch.equal(tr.S, S0)
+    l2 = tr.train_prepared(0.1, loss_out=torch.zeros(1, dtype=torch.float64, device="cuda"))
+    assert np.isfinite(l2.item())
+    assert tr.check() == -2
