@@ -20,6 +20,8 @@ constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 keys per tile
 constexpr int kLookBatch = 32;         // look-back words read together
 constexpr int kChunk = 256;            // sorted positions per duplicate-sum window
 constexpr uint32_t kNoHead = 0xFFFFFFFFu;
+constexpr uint32_t kLongPiece = 32;            // pieces longer than this are summed by a workgroup
+constexpr uint32_t kHasLong = 0x80000000u;     // window count flag: the window has such a piece
 constexpr int kSamplePer = 2;          // positives per thread in the sampler
 constexpr int kNegBlock = 8;           // negatives whose rows are in flight together
 constexpr int kMaxNeg = 64;
@@ -54,7 +56,7 @@ struct SlotLayout {
     size_t info = 0;     // i32 [M]: -1, or the sorted position of an occurrence of a repeated row
     size_t status = 0;   // u64 [sort_tiles * 256] look-back words
     size_t work = 0;     // uint4 [M] duplicate pieces, kChunk slots per window
-    size_t wcount = 0;   // u32 [windows] pieces per window
+    size_t wcount = 0;   // u32 [windows] pieces per window (| kHasLong if one is long)
     size_t longhead = 0; // u32 [windows] start of a run continuing past the window
     size_t wstats = 0;   // u32 [windows * 3] distinct S, distinct T, repeated occurrences
 };

@@ -39,11 +39,11 @@ __device__ __forceinline__ int32_t draw_negative(uint64_t seed, uint64_t p, uint
     const uint64_t x = ((uint64_t)r.y << 32) | (uint64_t)r.x;
     uint64_t j = __umul64hi(x, N);
     if (thr != nullptr) {
-        // alias entries come from the caller: one outside [0, N) keeps j
-        if (r.z >= thr[j]) {
-            const uint64_t a = (uint64_t)(uint32_t)alias[j];
-            j = a < N ? a : j;
-        }
+        // both table words are loaded before either is used (independent
+        // loads); an alias entry outside [0, N) (caller data) keeps j
+        const uint32_t th = thr[j];
+        const uint64_t a = (uint64_t)(uint32_t)alias[j];
+        if (r.z >= th && a < N) j = a;
     }
     return (int32_t)j;
 }

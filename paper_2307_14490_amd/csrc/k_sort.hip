@@ -261,8 +261,9 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
 //     kind 1: the run's first piece, the run continues past the window ->
 //             partial sum to partB[w]; longhead[w] = its start;
 //     kind 2: a later piece, starting at the window boundary -> partA[w].
-//   A window holds at most one kind-1 piece.  Per window: number of pieces,
-//   and {distinct source keys, distinct context keys, repeated occurrences}.
+//   A window holds at most one kind-1 piece.  Per window: number of pieces
+//   (with kHasLong set if one is longer than kLongPiece), and {distinct
+//   source keys, distinct context keys, repeated occurrences}.
 // Everything is written without global atomics.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl,
@@ -277,6 +278,7 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
     __shared__ uint32_t s_cnt[3];
     __shared__ uint32_t s_wave_emit[kBlock / 64];
     __shared__ uint32_t s_long;
+    __shared__ uint32_t s_long_piece;
     const int64_t win = blockIdx.x;
     if (ctl->step_bad) {  // unsorted keys: no pieces, nothing marked
         if (threadIdx.x == 0) {
@@ -286,19 +288,29 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
         }
         return;
     }
+    __shared__ uint32_t s_key[kChunk + 2];  // keys j-1 .. window end (inclusive of one past)
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     if (tid < 3) s_cnt[tid] = 0u;
-    if (tid == 0) s_long = 0xFFFFFFFFu;
-    __syncthreads();
+    if (tid == 0) {
+        s_long = 0xFFFFFFFFu;
+        s_long_piece = 0u;
+    }
     const int64_t j = win * kChunk + tid;
+    // s_key[1 + t] = keys[win * kChunk + t]; s_key[0] = the key before the
+    // window, s_key[kChunk + 1] = the key after it (a sentinel if none: it is
+    // only compared under an index check)
+    s_key[1 + tid] = j < m ? keys[j] : 0u;
+    if (tid == 0) s_key[0] = j > 0 ? keys[j - 1] : 0u;
+    if (tid == 1) s_key[kChunk + 1] = win * kChunk + kChunk < m ? keys[win * kChunk + kChunk] : 0u;
+    __syncthreads();
     bool emit = false, head_S = false, head_T = false, dup = false;
     uint4 rec = make_uint4(0, 0, 0, 0);
     if (j < m) {
-        const uint32_t key = keys[j];
-        const bool prev_same = j > 0 && keys[j - 1] == key;
-        const bool next_same = j + 1 < m && keys[j + 1] == key;
+        const uint32_t key = s_key[1 + tid];
+        const bool prev_same = j > 0 && s_key[tid] == key;
+        const bool next_same = j + 1 < m && s_key[2 + tid] == key;
         dup = prev_same || next_same;
         if (dup) {
             const uint32_t o = vals[j];
@@ -310,8 +322,8 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
             const int64_t win_end = (win + 1) * kChunk;
             const int64_t lim = win_end < m ? win_end : m;
             int64_t e = j + 1;
-            while (e < lim && keys[e] == key) ++e;
-            const bool cont_after = (e == win_end) && (e < m) && keys[e] == key;
+            while (e < lim && s_key[1 + (e - win * kChunk)] == key) ++e;
+            const bool cont_after = (e == win_end) && (e < m) && s_key[kChunk + 1] == key;
             const uint32_t kind = !prev_same ? (cont_after ? 1u : 0u) : 2u;
             rec = make_uint4((uint32_t)j, (uint32_t)(e - j), key, kind);
             emit = true;
@@ -320,6 +332,8 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
     }
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const uint64_t em = __ballot(emit);
+    const uint64_t lg = __ballot(emit && rec.y > kLongPiece);
+    if (lane == 0 && lg) s_long_piece = 1u;
     const uint64_t bs = __ballot(head_S);
     const uint64_t bt = __ballot(head_T);
     const uint64_t bd = __ballot(dup);
@@ -336,7 +350,7 @@ __global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl
     if (tid == 0) {
         uint32_t total = 0;
         for (int w = 0; w < kBlock / 64; ++w) total += s_wave_emit[w];
-        wcount[win] = total;
+        wcount[win] = total | (s_long_piece ? kHasLong : 0u);
         longhead[win] = s_long;
         wstats[win * 3 + 0] = s_cnt[0];
         wstats[win * 3 + 1] = s_cnt[1];

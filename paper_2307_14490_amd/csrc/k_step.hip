@@ -276,6 +276,44 @@ __device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
     IO::store(base, row, t.D, lane, r);
 }
 
+// Partial sums of the groups of a workgroup, combined in group order.
+template <int G, int C>
+__device__ __forceinline__ void coop_store(double* s_part, int grp, int lane, int32_t D,
+                                           const double4_ (&acc)[C]) {
+    const int q = D >> 2;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int j = lane + c * G;
+        if (j < q) reinterpret_cast<double4_*>(s_part + (size_t)grp * D)[j] = acc[c];
+    }
+}
+
+template <int G, int C>
+__device__ __forceinline__ void coop_total(double4_ (&acc)[C], const double* s_part, int lane,
+                                           int32_t D) {
+    constexpr int PPB = kBlock / G;
+    const int q = D >> 2;
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] = double4_{0.0, 0.0, 0.0, 0.0};
+    for (int g = 0; g < PPB; ++g) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int j = lane + c * G;
+            if (j < q) {
+                const double4_ b = reinterpret_cast<const double4_*>(s_part + (size_t)g * D)[j];
+                acc[c].x += b.x;
+                acc[c].y += b.y;
+                acc[c].z += b.z;
+                acc[c].w += b.w;
+            }
+        }
+    }
+}
+
+// Repeated rows, one workgroup per window of sorted positions.  A piece of
+// at most kLongPiece rows is summed by one group; a longer one by all PPB
+// groups of the workgroup, each over a fixed contiguous part, combined in
+// group order (the result does not depend on scheduling).
 template <int G, int C>
 __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control* __restrict__ ctl,
                                                       const uint4* __restrict__ work,
@@ -284,30 +322,59 @@ __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control
                                                       double* __restrict__ partA,
                                                       double* __restrict__ partB, float lr,
                                                       int64_t windows) {
-    if (ctl->step_bad) return;
     constexpr int PPB = kBlock / G;
+    __shared__ double s_part[1024 * C];  // PPB x D doubles: D <= 4 G C
+    if (ctl->step_bad) return;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
-    for (int64_t w = (int64_t)blockIdx.x * PPB + grp; w < windows;
-         w += (int64_t)gridDim.x * PPB) {
-        const uint32_t cnt = wcount[w];
-        for (uint32_t p = 0; p < cnt; ++p) {
+    const int32_t D = t.D;
+    for (int64_t w = blockIdx.x; w < windows; w += gridDim.x) {
+        const uint32_t wc = wcount[w];
+        const uint32_t cnt = wc & ~kHasLong;
+        // short pieces: one group each
+        for (uint32_t p = grp; p < cnt; p += PPB) {
             const uint4 rec = work[w * kChunk + p];
+            if (rec.y > kLongPiece) continue;
             double4_ acc[C];
-            sum_rows<G, C>(acc, dup, rec.x, rec.y, t.D, lane);
+            sum_rows<G, C>(acc, dup, rec.x, rec.y, D, lane);
             if (rec.w == 0u) {
                 apply_row<G, C>(t, rec.z, acc, lr, lane);
             } else {
                 double* part = rec.w == 1u ? partB : partA;
-                PartIO<G, C>::store(part, w, t.D, lane, acc);
+                PartIO<G, C>::store(part, w, D, lane, acc);
             }
+        }
+        if (!(wc & kHasLong)) continue;
+        // long pieces: the whole workgroup (rec is the same for every thread)
+        for (uint32_t p = 0; p < cnt; ++p) {
+            const uint4 rec = work[w * kChunk + p];
+            if (rec.y <= kLongPiece) continue;
+            const uint32_t part_len = (rec.y + PPB - 1) / PPB;
+            const uint32_t b0 = grp * part_len;
+            const uint32_t b1 = b0 + part_len < rec.y ? b0 + part_len : rec.y;
+            double4_ acc[C];
+            sum_rows<G, C>(acc, dup, (int64_t)rec.x + b0, b1 > b0 ? (int64_t)(b1 - b0) : 0, D,
+                           lane);
+            coop_store<G, C>(s_part, grp, lane, D, acc);
+            __syncthreads();
+            if (grp == 0) {
+                coop_total<G, C>(acc, s_part, lane, D);
+                if (rec.w == 0u) {
+                    apply_row<G, C>(t, rec.z, acc, lr, lane);
+                } else {
+                    double* part = rec.w == 1u ? partB : partA;
+                    PartIO<G, C>::store(part, w, D, lane, acc);
+                }
+            }
+            __syncthreads();
         }
     }
 }
 
-// A run that spans windows: its first piece's partial sum (partB of the
-// head's window) plus the pieces of the following windows (partA), in
-// window order, then one update of the row.
+// A run that spans windows w0 .. wl: its first piece's partial sum (partB of
+// w0) plus the pieces of windows w0+1 .. wl (partA), then one update of the
+// row.  The windows of the run are found 256 at a time; the groups of the
+// workgroup sum fixed interleaved subsets of them, combined in group order.
 template <int G, int C>
 __global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Control* __restrict__ ctl,
                                                          const uint32_t* __restrict__ longhead,
@@ -316,22 +383,42 @@ __global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Cont
                                                          const double* __restrict__ partB,
                                                          float lr, int64_t windows) {
     using IO = PartIO<G, C>;
-    if (ctl->step_bad) return;
     constexpr int PPB = kBlock / G;
+    __shared__ double s_part[1024 * C];
+    __shared__ int64_t s_end;
+    if (ctl->step_bad) return;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
-    for (int64_t w0 = (int64_t)blockIdx.x * PPB + grp; w0 < windows;
-         w0 += (int64_t)gridDim.x * PPB) {
+    const int32_t D = t.D;
+    for (int64_t w0 = blockIdx.x; w0 < windows; w0 += gridDim.x) {
         const uint32_t head = longhead[w0];
-        if (head == kNoHead) continue;
+        if (head == kNoHead) continue;  // uniform over the workgroup
         const uint32_t key = keys[head];
-        int64_t win = w0;
-        double4_ acc[C];
-        IO::load(acc, partB, win, t.D, lane);
+        // last window of the run: the first window from w0+1 whose first key
+        // differs (or that starts past the end), minus one
+        int64_t base = w0 + 1;
         while (true) {
-            ++win;
+            if (threadIdx.x == 0) s_end = INT64_MAX;
+            __syncthreads();
+            const int64_t w = base + threadIdx.x;
+            const bool cont = w * kChunk < m && keys[w * kChunk] == key;
+            if (!cont) atomicMin((unsigned long long*)&s_end, (unsigned long long)w);
+            __syncthreads();
+            const int64_t e = s_end;
+            __syncthreads();
+            if (e != INT64_MAX) {
+                base = e;
+                break;
+            }
+            base += kBlock;
+        }
+        const int64_t wl = base - 1;  // >= w0 + 1: the head piece reached its window's end
+        double4_ acc[C];
+#pragma unroll
+        for (int q = 0; q < C; ++q) acc[q] = double4_{0.0, 0.0, 0.0, 0.0};
+        for (int64_t w = w0 + 1 + grp; w <= wl; w += PPB) {
             double4_ b[C];
-            IO::load(b, partA, win, t.D, lane);
+            IO::load(b, partA, w, D, lane);
 #pragma unroll
             for (int q = 0; q < C; ++q) {
                 acc[q].x += b[q].x;
@@ -339,18 +426,24 @@ __global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Cont
                 acc[q].z += b[q].z;
                 acc[q].w += b[q].w;
             }
-            const int64_t e = (win + 1) * kChunk;
-            if (!(e < m && keys[e] == key)) break;
         }
-        apply_row<G, C>(t, key, acc, lr, lane);
+        coop_store<G, C>(s_part, grp, lane, D, acc);
+        __syncthreads();
+        if (grp == 0) {
+            double4_ tot[C], hb[C];
+            coop_total<G, C>(tot, s_part, lane, D);
+            IO::load(hb, partB, w0, D, lane);
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                hb[q].x += tot[q].x;
+                hb[q].y += tot[q].y;
+                hb[q].z += tot[q].z;
+                hb[q].w += tot[q].w;
+            }
+            apply_row<G, C>(t, key, hb, lr, lane);
+        }
+        __syncthreads();
     }
-}
-
-static int64_t window_blocks(int G, int64_t windows) {
-    const int64_t ppb = kBlock / G;
-    int64_t blocks = (windows + ppb - 1) / ppb;
-    if (blocks > 4096) blocks = 4096;
-    return blocks < 1 ? 1 : blocks;
 }
 
 hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
@@ -358,7 +451,7 @@ hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
                             double* partB, float lr, int64_t m, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
     const int64_t windows = (m + kChunk - 1) / kChunk;
-    const int64_t blocks = window_blocks(rs.G, windows);
+    const int64_t blocks = windows < 16384 ? (windows > 0 ? windows : 1) : 16384;
     HUGE_ROW_DISPATCH(rs, {
         hipLaunchKernelGGL((k_dup_apply<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t,
                            ctl, work, wcount, dup, partA, partB, lr, windows);
@@ -371,7 +464,7 @@ hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t*
                                const double* partB, float lr, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
     const int64_t windows = (m + kChunk - 1) / kChunk;
-    const int64_t blocks = window_blocks(rs.G, windows);
+    const int64_t blocks = windows < 2048 ? (windows > 0 ? windows : 1) : 2048;
     HUGE_ROW_DISPATCH(rs, {
         hipLaunchKernelGGL((k_long_combine<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
                            t, ctl, longhead, keys, m, partA, partB, lr, windows);

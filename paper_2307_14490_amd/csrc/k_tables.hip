@@ -176,14 +176,28 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
                 atomicAdd(&s_hist[ps * kRadixBins + ((key_d >> (ps * kRadixBits)) & 255u)], 1u);
             }
         }
-        for (int k = 0; k < K; ++k) {
-            const int32_t m = draw_negative(t.seed, p, (uint32_t)k, (uint64_t)t.N, t.thr, t.alias);
-            neg[i * K + k] = m;
-            if (with_keys) {
-                keys[o + 2 + k] = (uint32_t)m;
-                for (int ps = 0; ps < passes; ++ps)
-                    atomicAdd(&s_hist[ps * kRadixBins + (((uint32_t)m >> (ps * kRadixBits)) & 255u)],
-                              1u);
+        // negatives in chunks of kNegBlock: the alias-table loads of a chunk
+        // are independent and issued together
+        for (int k0 = 0; k0 < K; k0 += kNegBlock) {
+            int32_t mm[kNegBlock];
+#pragma unroll
+            for (int q = 0; q < kNegBlock; ++q)
+                if (k0 + q < K)
+                    mm[q] = draw_negative(t.seed, p, (uint32_t)(k0 + q), (uint64_t)t.N, t.thr,
+                                          t.alias);
+#pragma unroll
+            for (int q = 0; q < kNegBlock; ++q) {
+                if (k0 + q < K) {
+                    const int32_t m = mm[q];
+                    neg[i * K + k0 + q] = m;
+                    if (with_keys) {
+                        keys[o + 2 + k0 + q] = (uint32_t)m;
+                        for (int ps = 0; ps < passes; ++ps)
+                            atomicAdd(&s_hist[ps * kRadixBins +
+                                              (((uint32_t)m >> (ps * kRadixBits)) & 255u)],
+                                      1u);
+                    }
+                }
             }
         }
     }
