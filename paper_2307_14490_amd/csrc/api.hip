@@ -45,7 +45,8 @@ struct huge_handle {
     uint8_t* ws;
     size_t ws_bytes;
     Layout lay;
-    int passes;
+    SortPlan plan;  // radix passes and digit width for keys below 2N
+    int key_bits;   // bits of 2N - 1
     uint32_t epoch;            // tags the look-back words of each grouping
     int64_t prepared;          // groupings issued
     int64_t applied;           // applies issued
@@ -110,7 +111,7 @@ Layout make_layout(const huge_config* c) {
     for (int s = 0; s < kSlots; ++s) {
         SlotLayout& S = L.slot[s];
         S.ctrl = take(sizeof(Control));
-        S.hist = take(sizeof(uint32_t) * kMaxPasses * kRadixBins);
+        S.hist = take(sizeof(uint32_t) * kMaxPasses * kMaxBins);
         S.neg = take(sizeof(int32_t) * (size_t)(nb * K));
         if (sorted) {
             S.keys0 = take(sizeof(uint32_t) * (size_t)M);
@@ -118,7 +119,9 @@ Layout make_layout(const huge_config* c) {
             S.vals0 = take(sizeof(uint32_t) * (size_t)M);
             S.vals1 = take(sizeof(uint32_t) * (size_t)M);
             S.info = take(sizeof(int32_t) * (size_t)M);
-            S.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kRadixBins));
+            S.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kMaxBins));
+            S.bstart = take(sizeof(uint32_t) * kMaxBins);
+            S.biglist = take(sizeof(uint32_t) * kMaxBins);
             S.work = take(sizeof(uint4) * (size_t)(L.windows * kChunk));
             S.wcount = take(sizeof(uint32_t) * (size_t)L.windows);
             S.longhead = take(sizeof(uint32_t) * (size_t)L.windows);
@@ -203,7 +206,8 @@ huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* t
     h->ws = static_cast<uint8_t*>(ws);
     h->ws_bytes = ws_bytes;
     h->lay = L;
-    h->passes = (key_bits(cfg->num_nodes) + kRadixBits - 1) / kRadixBits;
+    h->key_bits = key_bits(cfg->num_nodes);
+    h->plan = sort_plan(h->key_bits);
     h->epoch = 0;
     h->prepared = h->applied = 0;
     h->last_applied_slot = -1;
@@ -225,7 +229,7 @@ huge_status reset_workspace(huge_handle* h, hipStream_t s) {
         HIP_TRY(hipMemsetAsync(h->ws + h->lay.slot[k].ctrl, 0, sizeof(Control), s));
         if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
             HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
-                                        h->lay.sort_tiles * kRadixBins, s));
+                                        h->lay.sort_tiles * kMaxBins, s));
             HIP_TRY(launch_fill_i32(at<int32_t>(h, h->lay.slot[k].info), -1, h->lay.max_occ, s));
         }
     }
@@ -267,7 +271,7 @@ huge_status group_batch(huge_handle* h, const int32_t* src, const int32_t* dst,
         uint32_t* keys[2] = {at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1)};
         uint32_t* vals[2] = {at<uint32_t>(h, SL.vals0), at<uint32_t>(h, SL.vals1)};
         uint64_t* status = at<uint64_t>(h, SL.status);
-        HIP_TRY(launch_sample(t, ctl, a, neg, keys[0], at<int32_t>(h, SL.info), hist, h->passes,
+        HIP_TRY(launch_sample(t, ctl, a, neg, keys[0], at<int32_t>(h, SL.info), hist, h->plan,
                               s));
         if (!mark(1)) return HUGE_ERR_HIP;
         // look-back tags: 8 per grouping; the words are cleared when the
@@ -276,23 +280,37 @@ huge_status group_batch(huge_handle* h, const int32_t* src, const int32_t* dst,
         if ((h->epoch & 0x07FFFFFFu) == 0u) {
             for (int k = 0; k < kSlots; ++k)
                 HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
-                                            h->lay.sort_tiles * kRadixBins, s));
+                                            h->lay.sort_tiles * kMaxBins, s));
             h->epoch += 1;
         }
-        int cur = 0;
-        for (int p = 0; p < h->passes; ++p) {
-            const uint32_t tag = (h->epoch << 3) | (uint32_t)p;
-            HIP_TRY(launch_radix_pass(ctl, keys[cur], p == 0 ? nullptr : vals[cur], keys[cur ^ 1],
-                                      vals[cur ^ 1], m, p, hist, status, tag, s));
-            cur ^= 1;
+        // First pass: buckets by the lowest digit.  Then each bucket is
+        // sorted in LDS into the buffer the full sort would end in; the later
+        // passes run only if a bucket was too large for that (ctl->overflow).
+        const int fin = h->plan.passes & 1;
+        uint32_t* bstart = at<uint32_t>(h, SL.bstart);
+        HIP_TRY(launch_radix_pass(ctl, keys[0], nullptr, keys[1], vals[1], m, 0, h->plan.bits,
+                                  hist, status, h->epoch << 3, nullptr, bstart, s));
+        if (h->plan.passes > 1) {
+            HIP_TRY(launch_bucket_sort(ctl, keys[1], vals[1], keys[fin], vals[fin], m,
+                                       h->plan.bits, h->key_bits, hist, bstart,
+                                       at<uint32_t>(h, SL.biglist), s));
+            int cur = 1;
+            for (int p = 1; p < h->plan.passes; ++p) {
+                const uint32_t tag = (h->epoch << 3) | (uint32_t)p;
+                HIP_TRY(launch_radix_pass(ctl, keys[cur], vals[cur], keys[cur ^ 1], vals[cur ^ 1],
+                                          m, p, h->plan.bits, hist, status, tag, &ctl->overflow,
+                                          nullptr, s));
+                cur ^= 1;
+            }
         }
+        const int cur = fin;
         if (!mark(2)) return HUGE_ERR_HIP;
         HIP_TRY(launch_mark(ctl, keys[cur], vals[cur], m, t.N, at<int32_t>(h, SL.info),
                             at<uint4>(h, SL.work), at<uint32_t>(h, SL.wcount),
                             at<uint32_t>(h, SL.longhead), at<uint32_t>(h, SL.wstats), s));
         if (!mark(3)) return HUGE_ERR_HIP;
     } else {
-        HIP_TRY(launch_sample(t, ctl, a, neg, nullptr, nullptr, hist, 0, s));
+        HIP_TRY(launch_sample(t, ctl, a, neg, nullptr, nullptr, hist, h->plan, s));
         if (!mark(1) || !mark(2) || !mark(3)) return HUGE_ERR_HIP;
     }
     HIP_TRY(hipEventRecord(h->ready[slot], s));
@@ -327,7 +345,7 @@ huge_status apply_batch(huge_handle* h, float lr, double* loss_out, hipStream_t 
     if (!mark(0)) return HUGE_ERR_HIP;
     int64_t blocks = 0;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-        const uint32_t* keys_sorted = at<uint32_t>(h, (h->passes & 1) ? SL.keys1 : SL.keys0);
+        const uint32_t* keys_sorted = at<uint32_t>(h, (h->plan.passes & 1) ? SL.keys1 : SL.keys0);
         double* partA = at<double>(h, L.partA);
         double* partB = at<double>(h, L.partB);
         float* dup = at<float>(h, L.dup);
@@ -467,7 +485,7 @@ huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_
     hipStream_t s = static_cast<hipStream_t>(stream);
     StepArgs a{nullptr, nullptr, nullptr, n, first_pos_index, 0.0f, nullptr};
     HIP_TRY(launch_sample(table_args(h), at<Control>(h, h->lay.eval_ctrl), a, d_neg_out, nullptr,
-                          nullptr, nullptr, 0, s));
+                          nullptr, nullptr, h->plan, s));
     return HUGE_OK;
 }
 

@@ -11,13 +11,16 @@ namespace huge {
 // Compile-time constants
 // ---------------------------------------------------------------------------
 constexpr int kBlock = 256;            // threads per workgroup (4 wave64)
-constexpr int kRadixBits = 8;          // digit width of the LSD radix sort
-constexpr int kRadixBins = 1 << kRadixBits;
+constexpr int kMinDigitBits = 8;       // digit widths of the LSD radix sort: 8 to 10 bits,
+constexpr int kMaxDigitBits = 10;      // the same in every pass of a sort
+constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;          // keys < 2^32
 constexpr int kSortThreads = 1024;     // threads of a sort workgroup (16 wave64)
 constexpr int kSortItems = 8;          // keys per thread in a sort tile
 constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 keys per tile
-constexpr int kLookBatch = 32;         // look-back words read together
+constexpr int kLookBatch = 8;          // look-back words read together
+constexpr int kLocalMaxBits = 9;       // digit width limit of the in-LDS bucket sort
+constexpr int kLocalBins = 1 << kLocalMaxBits;
 constexpr int kChunk = 256;            // sorted positions per duplicate-sum window
 constexpr uint32_t kNoHead = 0xFFFFFFFFu;
 constexpr uint32_t kLongPiece = 32;            // pieces longer than this are summed by a workgroup
@@ -37,7 +40,9 @@ struct Control {
     uint32_t step_bad;               // this call's input is invalid: skip all writes
     uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
     uint32_t tickets[kMaxPasses];    // dynamic tile ids of the radix passes
-    uint32_t pad[10];
+    uint32_t overflow;               // a bucket exceeded the in-LDS sort: run the later passes
+    uint32_t big_count;              // buckets queued for the large in-LDS sort
+    uint32_t pad[8];
 };
 
 // Byte offsets of the workspace regions (all 256-byte aligned).
@@ -49,12 +54,14 @@ struct Control {
 // own regions; the apply regions are shared (applies are ordered).
 struct SlotLayout {
     size_t ctrl = 0;     // Control
-    size_t hist = 0;     // u32 [kMaxPasses][256] global digit counts
+    size_t hist = 0;     // u32 [kMaxPasses][kMaxBins] global digit counts
     size_t neg = 0;      // i32 [max_batch * K]
     // sorted scatter
     size_t keys0 = 0, keys1 = 0, vals0 = 0, vals1 = 0;  // u32 [M]
     size_t info = 0;     // i32 [M]: -1, or the sorted position of an occurrence of a repeated row
-    size_t status = 0;   // u64 [sort_tiles * 256] look-back words
+    size_t status = 0;   // u64 [sort_tiles * kMaxBins] look-back words
+    size_t bstart = 0;   // u32 [kMaxBins] first sorted position of each bucket
+    size_t biglist = 0;  // u32 [kMaxBins] buckets for the large in-LDS sort
     size_t work = 0;     // uint4 [M] duplicate pieces, kChunk slots per window
     size_t wcount = 0;   // u32 [windows] pieces per window (| kHasLong if one is long)
     size_t longhead = 0; // u32 [windows] start of a run continuing past the window
@@ -77,6 +84,21 @@ struct Layout {
     int64_t windows = 0;
     int64_t loss_blocks = 0;
 };
+
+// Radix sort of keys below 2^key_bits: the fewest passes of at most
+// kMaxDigitBits bits, at one width per sort (at least kMinDigitBits).
+struct SortPlan {
+    int passes;
+    int bits;
+};
+
+inline SortPlan sort_plan(int key_bits) {
+    if (key_bits < 1) key_bits = 1;
+    const int passes = (key_bits + kMaxDigitBits - 1) / kMaxDigitBits;
+    int bits = (key_bits + passes - 1) / passes;
+    if (bits < kMinDigitBits) bits = kMinDigitBits;
+    return {passes, bits};
+}
 
 // Rows handled per workgroup: G lanes per row, C float4 per lane.
 struct RowShape {
@@ -123,12 +145,16 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 hipError_t launch_begin(Control* ctl, uint32_t* hist, hipStream_t s);
 hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s);
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, int32_t* info, uint32_t* hist, int passes,
+                         uint32_t* keys, int32_t* info, uint32_t* hist, SortPlan plan,
                          hipStream_t s);
 hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
                              uint32_t* keys_out, uint32_t* vals_out, int64_t m, int pass,
-                             const uint32_t* hist, uint64_t* status, uint32_t tag,
-                             hipStream_t s);
+                             int bits, const uint32_t* hist, uint64_t* status, uint32_t tag,
+                             const uint32_t* gate, uint32_t* bstart, hipStream_t s);
+hipError_t launch_bucket_sort(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
+                              uint32_t* keys_out, uint32_t* vals_out, int64_t m, int bits,
+                              int key_bits, const uint32_t* hist0, const uint32_t* bstart,
+                              uint32_t* biglist, hipStream_t s);
 hipError_t launch_mark(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                        int64_t N, int32_t* info, uint4* work, uint32_t* wcount,
                        uint32_t* longhead, uint32_t* wstats, hipStream_t s);

@@ -78,17 +78,19 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 }
 
 // ---------------------------------------------------------------------------
-// Per-call set-up: clear the call's flag, the tile tickets, the digit
-// histograms and the counters (a kernel rather than a memset so that the
-// sequence stays valid inside a captured graph).
+// Per-call set-up: clear the call's flag, the tile tickets, the sort's
+// overflow flag and queue count, and the digit histograms (a kernel rather
+// than a memset so that the sequence stays valid inside a captured graph).
 // ---------------------------------------------------------------------------
 __global__ void k_begin(Control* ctl, uint32_t* hist) {
     const int t = threadIdx.x;
     if (hist != nullptr)
-        for (int i = t; i < kMaxPasses * kRadixBins; i += blockDim.x) hist[i] = 0u;
+        for (int i = t; i < kMaxPasses * kMaxBins; i += blockDim.x) hist[i] = 0u;
     if (t == 0) {
         ctl->step_bad = 0u;
         for (int p = 0; p < kMaxPasses; ++p) ctl->tickets[p] = 0u;
+        ctl->overflow = 0u;
+        ctl->big_count = 0u;
     }
 }
 
@@ -134,18 +136,21 @@ hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
 //     o = i (2 + K) + slot: slot 0 the source row (key N + src), slot 1 the
 //     destination row (key dst), slots 2.. the negatives (key m), sets their
 //     info entries to -1 (the run marking overwrites repeated ones) and
-//     counts the digits of every radix pass.
+//     counts the digits of every radix pass (digit ps = bits [ps * bits,
+//     (ps + 1) * bits) of the key, counted at hist[ps * kMaxBins + digit]).
 // Without src (src == nullptr) only negatives are drawn.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, StepArgs a,
                                                    int32_t* __restrict__ neg,
                                                    uint32_t* __restrict__ keys,
                                                    int32_t* __restrict__ info,
-                                                   uint32_t* __restrict__ hist, int passes) {
-    __shared__ uint32_t s_hist[kMaxPasses * kRadixBins];
+                                                   uint32_t* __restrict__ hist, int passes,
+                                                   int bits) {
+    __shared__ uint32_t s_hist[kMaxPasses * kMaxBins];
     const bool with_keys = keys != nullptr;
+    const uint32_t dmask = (1u << bits) - 1u;
     if (with_keys) {
-        for (int j = threadIdx.x; j < passes * kRadixBins; j += kBlock) s_hist[j] = 0u;
+        for (int j = threadIdx.x; j < passes * kMaxBins; j += kBlock) s_hist[j] = 0u;
         __syncthreads();
     }
     const int K = t.K;
@@ -172,8 +177,8 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
             keys[o + 1] = key_d;
             for (int sl = 0; sl < 2 + K; ++sl) info[o + sl] = -1;
             for (int ps = 0; ps < passes; ++ps) {
-                atomicAdd(&s_hist[ps * kRadixBins + ((key_s >> (ps * kRadixBits)) & 255u)], 1u);
-                atomicAdd(&s_hist[ps * kRadixBins + ((key_d >> (ps * kRadixBits)) & 255u)], 1u);
+                atomicAdd(&s_hist[ps * kMaxBins + ((key_s >> (ps * bits)) & dmask)], 1u);
+                atomicAdd(&s_hist[ps * kMaxBins + ((key_d >> (ps * bits)) & dmask)], 1u);
             }
         }
         // negatives in chunks of kNegBlock: the alias-table loads of a chunk
@@ -193,8 +198,7 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
                     if (with_keys) {
                         keys[o + 2 + k0 + q] = (uint32_t)m;
                         for (int ps = 0; ps < passes; ++ps)
-                            atomicAdd(&s_hist[ps * kRadixBins +
-                                              (((uint32_t)m >> (ps * kRadixBits)) & 255u)],
+                            atomicAdd(&s_hist[ps * kMaxBins + (((uint32_t)m >> (ps * bits)) & dmask)],
                                       1u);
                     }
                 }
@@ -203,7 +207,7 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
     }
     if (with_keys) {
         __syncthreads();
-        for (int j = threadIdx.x; j < passes * kRadixBins; j += kBlock) {
+        for (int j = threadIdx.x; j < passes * kMaxBins; j += kBlock) {
             const uint32_t c = s_hist[j];
             if (c) atomicAdd(&hist[j], c);
         }
@@ -211,13 +215,13 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
 }
 
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, int32_t* info, uint32_t* hist, int passes,
+                         uint32_t* keys, int32_t* info, uint32_t* hist, SortPlan plan,
                          hipStream_t s) {
     const int64_t per_block = (int64_t)kBlock * kSamplePer;
     const int64_t blocks = (a.n + per_block - 1) / per_block;
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
-                       info, hist, passes);
+                       info, hist, keys ? plan.passes : 0, plan.bits);
     return hipGetLastError();
 }
 

@@ -94,6 +94,8 @@ STEP_CASES = [
     (2, 8, 5, 50, "two nodes: every row repeats"),
     (1_000, 128, 64, 100, "largest K"),
     (20_000, 128, 5, 9000, "several sort tiles"),
+    (100_000, 16, 5, 20_000, "keys of 18 bits: two 9-bit radix passes"),
+    (300_000, 16, 4, 30_000, "keys of 20 bits: two 10-bit radix passes, 22 tiles"),
 ]
 
 
@@ -168,6 +170,26 @@ def test_hub_rows_and_large_counts(scatter):
     say(f"hub {scatter}")
     _one_step(5_000, 64, 4, 6000, scatter, hub=0.5, cmax=1000,
               heavy=None if scatter == "sorted" else 64)
+
+
+@pytest.mark.parametrize("N,n,hub,note", [
+    (5_000, 8_000, 0.75, "hub bucket of 6000: large in-LDS sort, output in the other buffer"),
+    (5_000, 16_000, 0.9, "hub bucket of 14400: overflow, later global pass"),
+    (1_100_000, 8_000, 0.75, "three passes: large in-LDS sort in place"),
+    (1_100_000, 16_000, 0.9, "three passes: overflow, two later global passes"),
+])
+def test_bucket_sort_regimes(N, n, hub, note):
+    """Grouping with buckets of every size class; tables and the distinct /
+    repeated counts must match the oracle and numpy."""
+    say(f"bucket regimes N={N} n={n} hub={hub} ({note})")
+    K = 2
+    tr, (src, dst, cc, neg) = _one_step(N, 8, K, n, "sorted", hub=hub)
+    uS, uT, dup = tr.stats()
+    keys = np.concatenate([src.astype(np.int64) + N, dst, neg.reshape(-1)])
+    u, cnt = np.unique(keys, return_counts=True)
+    assert uS == np.unique(src).size
+    assert uT == np.unique(np.concatenate([dst, neg.reshape(-1)])).size
+    assert dup == int(cnt[cnt > 1].sum())
 
 
 def test_alias_negatives_step():
