@@ -104,6 +104,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--sequential", action="store_true",
                     help="one stream, huge_train_step per step (no overlap of grouping)")
+    ap.add_argument("--pipeline", default="alternate", choices=["alternate", "side"],
+                    help="streams of the overlapped steps (see run_steps)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -150,25 +152,34 @@ def main():
             per_batch_stats[b] = tr.stats()
 
     side = torch.cuda.Stream()  # default priority, like the current stream
+    streams = [stream, side]
 
     def run_steps(count, first_batch, pos):
-        """`count` steps; pipelined: batch k+1 is grouped on `side` while
-        batch k is applied on the current stream."""
+        """`count` steps.  Pipelined: batch k is grouped and applied on
+        streams[k % 2], and batch k+1 is grouped while batch k is applied, so
+        the grouping of k+1 runs beside the apply of k and the apply of k+1
+        follows its own grouping on the same stream (the wait for the apply
+        of k crosses streams, and that apply has finished first).  With
+        --pipeline side, every grouping runs on `side` and every apply on the
+        current stream."""
         if args.sequential:
             for k in range(count):
                 s, d, c = dev_batches[(first_batch + k) % R]
                 tr.step_no_loss(s, d, c, pos, cfg.lr)
                 pos += n
             return pos
+        alt = args.pipeline == "alternate"
+        gstream = (lambda k: streams[k % 2]) if alt else (lambda k: side)
+        astream = (lambda k: streams[k % 2]) if alt else (lambda k: stream)
         s, d, c = dev_batches[first_batch % R]
-        tr.prepare(s, d, c, pos, stream=side)
+        tr.prepare(s, d, c, pos, stream=gstream(0))
         pos += n
         for k in range(count):
-            tr.train_prepared(cfg.lr, with_loss=False, stream=stream)
             if k + 1 < count:
                 s, d, c = dev_batches[(first_batch + k + 1) % R]
-                tr.prepare(s, d, c, pos, stream=side)
+                tr.prepare(s, d, c, pos, stream=gstream(k + 1))
                 pos += n
+            tr.train_prepared(cfg.lr, with_loss=False, stream=astream(k))
         return pos
 
     pos = run_steps(args.warmup, 0, pos)
@@ -184,7 +195,8 @@ def main():
     ev0.record(stream)
     side.wait_event(ev0)
     pos = run_steps(args.steps, args.warmup, pos)
-    ev1.record(stream)  # the last apply waits for every grouping before it
+    stream.wait_stream(side)  # the last apply may run on either stream
+    ev1.record(stream)
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
     phase_ms, prof_steps = tr.profile_end()
@@ -238,7 +250,8 @@ def main():
             "scatter": args.scatter,
             "lr": cfg.lr,
             "staged_batches": R,
-            "grouping": "sequential" if args.sequential else "overlapped with the previous apply",
+            "grouping": ("sequential" if args.sequential else
+                         f"overlapped with the previous apply ({args.pipeline} streams)"),
         },
         "roofline": {
             "kernel": KERNEL if args.scatter == "sorted" else "k_atomic_gather",
