@@ -206,6 +206,28 @@ def main():
     value = n * args.steps / (total_ms / 1e3)
     log(f"[bench] {args.steps} steps in {total_ms:.2f} ms: {ms_per_step:.4f} ms/step")
 
+    # Roofline probe: the rows of the same batches (sources, destinations and
+    # the negatives a step would draw) read and written back unchanged, with
+    # the fused kernel's launch shape and no arithmetic: the practical ceiling
+    # of the step's random row traffic on this device.
+    n_probe = min(args.steps, 50)
+    for k in range(3):
+        s, d, c = dev_batches[k % R]
+        tr.probe_rows(s, d, pos + k * n, stream=stream)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for k in range(n_probe):
+        s, d, c = dev_batches[k % R]
+        tr.probe_rows(s, d, pos + k * n, stream=stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    probe_us = ev0.elapsed_time(ev1) / n_probe * 1e3
+    if tr.check() != 0:
+        raise RuntimeError("device reported an error in the probe")
+    probe_bytes = 8.0 * n + 2.0 * 4.0 * D * n * (2 + K)
+    probe_gbps = probe_bytes / (probe_us * 1e-6) / 1e9
+    log(f"[bench] probe: {probe_us:.1f} us per launch, {probe_gbps:.0f} GB/s")
+
     # Algorithmic bytes of the fused kernel per launch: the batch (12 B per
     # positive), each distinct row read once (4 D bytes) and each row that
     # occurs once written once in place.  Repeated rows are written by the
@@ -263,6 +285,14 @@ def main():
             "traffic": traffic,
             "avg_kernel_us": fused_us,
             "alg_bytes_per_launch": kernel_bytes,
+            "probe": {
+                "achieved": probe_gbps,
+                "unit": "GB/s",
+                "avg_us": probe_us,
+                "bytes_per_launch": probe_bytes,
+                "what": "the same batches' rows read and written back unchanged, no arithmetic",
+            },
+            "frac_of_probe": achieved / probe_gbps,
         },
         "step": {
             "alg_bytes": step_bytes,

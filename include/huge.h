@@ -169,6 +169,18 @@ huge_status huge_get_rows(huge_handle* h, int32_t table, const int64_t* d_ids, i
 huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_index,
                                   int32_t* d_neg_out, void* stream);
 
+/* Bandwidth probe, for measurement: reads and writes back unchanged every
+   row a step over this batch would touch -- S[src_i], T[dst_i] and the K
+   rows T[m_ik] drawn for first_pos_index as in huge_train_step -- one read
+   and one write per occurrence, in the fused step's launch shape and with no
+   arithmetic.  Its rate is the practical ceiling of the step's random row
+   traffic on the device.  d_src, d_dst: n <= max_batch int32 ids in [0, N);
+   an id outside that range skips its positive and makes huge_check report
+   HUGE_ERR_ID_OUT_OF_RANGE.  The tables keep their values bit for bit; the
+   call is ordered after the last apply, and must not run beside a step. */
+huge_status huge_probe_rows(huge_handle* h, const int32_t* d_src, const int32_t* d_dst, int64_t n,
+                            uint64_t first_pos_index, void* stream);
+
 /* Synchronise the stream; return and clear the first device-side error
    (HUGE_ERR_ID_OUT_OF_RANGE or HUGE_ERR_BAD_COUNT) since the last check. */
 huge_status huge_check(huge_handle* h, void* stream);

@@ -29,8 +29,8 @@ HUGE_SCATTER_ATOMIC = 1
 
 EXPORTED = [
     "huge_workspace_bytes", "huge_build_alias", "huge_init_tables", "huge_attach_tables",
-    "huge_train_step", "huge_prepare_step", "huge_train_prepared", "huge_eval_loss", "huge_get_rows", "huge_sample_negatives",
-    "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
+    "huge_train_step", "huge_prepare_step", "huge_train_prepared", "huge_eval_loss",
+    "huge_get_rows", "huge_sample_negatives", "huge_probe_rows", "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
     "huge_destroy", "huge_status_string",
 ]
 HUGE_PHASES = 6
@@ -82,6 +82,7 @@ def load() -> ctypes.CDLL:
     L.huge_eval_loss.argtypes = [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64, _vp, _vp]
     L.huge_get_rows.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp]
     L.huge_sample_negatives.argtypes = [_vp, ctypes.c_int64, ctypes.c_uint64, _vp, _vp]
+    L.huge_probe_rows.argtypes = [_vp, _vp, _vp, ctypes.c_int64, ctypes.c_uint64, _vp]
     L.huge_check.argtypes = [_vp, _vp]
     L.huge_step_stats.argtypes = [_vp, _vp, ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
@@ -94,7 +95,8 @@ def load() -> ctypes.CDLL:
     L.huge_status_string.restype = ctypes.c_char_p
     for name in ("huge_build_alias", "huge_init_tables", "huge_attach_tables", "huge_train_step",
                  "huge_prepare_step", "huge_train_prepared",
-                 "huge_eval_loss", "huge_get_rows", "huge_sample_negatives", "huge_check",
+                 "huge_eval_loss", "huge_get_rows", "huge_sample_negatives", "huge_probe_rows",
+                 "huge_check",
                  "huge_step_stats", "huge_profile_begin", "huge_profile_end"):
         getattr(L, name).restype = ctypes.c_int32
     _lib = L
@@ -230,6 +232,15 @@ class Trainer:
         _ok(load().huge_sample_negatives(self._h, int(n), int(first_pos), _dptr(out),
                                          _stream_ptr(stream)), "huge_sample_negatives")
         return out
+
+    def probe_rows(self, src, dst, first_pos, stream=None):
+        """Read and write back, unchanged, every row a step over this batch
+        would touch (the bandwidth ceiling of the step's row traffic)."""
+        n = src.numel()
+        if dst.numel() != n:
+            raise ValueError("src and dst must have the same length")
+        _ok(load().huge_probe_rows(self._h, _dptr(src), _dptr(dst), n, int(first_pos),
+                                   _stream_ptr(stream)), "huge_probe_rows")
 
     def check(self, stream=None) -> int:
         return int(load().huge_check(self._h, _stream_ptr(stream)))

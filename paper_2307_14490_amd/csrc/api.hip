@@ -477,6 +477,20 @@ huge_status huge_get_rows(huge_handle* h, int32_t table, const int64_t* d_ids, i
     return HUGE_OK;
 }
 
+huge_status huge_probe_rows(huge_handle* h, const int32_t* d_src, const int32_t* d_dst, int64_t n,
+                            uint64_t first_pos_index, void* stream) {
+    if (!h || n < 0 || n > h->cfg.max_batch) return HUGE_ERR_INVALID_ARG;
+    if (n == 0) return HUGE_OK;
+    if (!d_src || !d_dst) return HUGE_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // the tables are shared with applies: order after the last one
+    if (h->last_applied_slot >= 0)
+        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
+    HIP_TRY(launch_probe(table_args(h), at<Control>(h, h->lay.eval_ctrl), d_src, d_dst, n,
+                         first_pos_index, s));
+    return HUGE_OK;
+}
+
 huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_index,
                                   int32_t* d_neg_out, void* stream) {
     if (!h || n < 0) return HUGE_ERR_INVALID_ARG;

@@ -180,6 +180,9 @@ hipError_t launch_atomic_scatter_S(const TableArgs& t, Control* ctl, const StepA
 hipError_t launch_eval(const TableArgs& t, Control* ctl, const StepArgs& a, double* lossp,
                        int64_t* blocks_out, hipStream_t s);
 
+hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, const int32_t* dst,
+                        int64_t n, uint64_t first_pos, hipStream_t s);
+
 int64_t fused_step_blocks(int dim, int64_t n);
 
 }  // namespace huge

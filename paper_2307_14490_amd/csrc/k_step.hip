@@ -187,6 +187,80 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 }
 
 // ---------------------------------------------------------------------------
+// Bandwidth probe: the rows one step over the batch touches -- S[u_i],
+// T[v_i] and the K negatives T[m_ik] it would draw -- each read and written
+// back unchanged, in the fused kernel's launch shape (one group of G lanes per
+// positive, kNegBlock negative rows in flight), with no arithmetic besides a
+// multiplication by a run-time 1.0f that keeps the compiler from dropping the
+// stores (x * 1.0f == x for every x).  Its rate is the practical ceiling of
+// the step's random row traffic.
+// ---------------------------------------------------------------------------
+template <int G, int C>
+__global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restrict__ ctl,
+                                                  const int32_t* __restrict__ src,
+                                                  const int32_t* __restrict__ dst, int64_t n,
+                                                  uint64_t first_pos, float one) {
+    using IO = RowIO<G, C>;
+    constexpr int PPB = kBlock / G;
+    const int lane = threadIdx.x % G;
+    const int64_t i = (int64_t)blockIdx.x * PPB + threadIdx.x / G;
+    if (i >= n) return;  // no barrier below
+    const int32_t u = src[i], v = dst[i];
+    if (u < 0 || (int64_t)u >= t.N || v < 0 || (int64_t)v >= t.N) {
+        if (lane == 0) raise_error(ctl, kBadId);
+        return;
+    }
+    const int K = t.K;
+    auto touch = [&](float4 (&x)[C]) {
+#pragma unroll
+        for (int q = 0; q < C; ++q) x[q] = scale4(one, x[q]);
+    };
+    float4 s[C], t0[C];
+    float4 tk[kNegBlock][C];
+    int32_t mk[kNegBlock];
+    for (int kb = 0; kb < K; kb += kNegBlock) {
+        const int cnt = (K - kb) < kNegBlock ? (K - kb) : kNegBlock;
+#pragma unroll
+        for (int j = 0; j < kNegBlock; ++j)
+            if (j < cnt)
+                mk[j] = draw_negative(t.seed, first_pos + (uint64_t)i, (uint32_t)(kb + j),
+                                      (uint64_t)t.N, t.thr, t.alias);
+        if (kb == 0) {
+            IO::load(s, t.S, u, t.D, lane);
+            IO::load(t0, t.T, v, t.D, lane);
+        }
+#pragma unroll
+        for (int j = 0; j < kNegBlock; ++j)
+            if (j < cnt) IO::load(tk[j], t.T, mk[j], t.D, lane);
+        if (kb == 0) {
+            touch(s);
+            touch(t0);
+            IO::store(t.S, u, t.D, lane, s);
+            IO::store(t.T, v, t.D, lane, t0);
+        }
+#pragma unroll
+        for (int j = 0; j < kNegBlock; ++j) {
+            if (j < cnt) {
+                touch(tk[j]);
+                IO::store(t.T, mk[j], t.D, lane, tk[j]);
+            }
+        }
+    }
+}
+
+hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, const int32_t* dst,
+                        int64_t n, uint64_t first_pos, hipStream_t s) {
+    const RowShape rs = row_shape(t.D);
+    const int64_t blocks = fused_step_blocks(t.D, n);
+    if (blocks == 0) return hipSuccess;
+    HUGE_ROW_DISPATCH(rs, {
+        hipLaunchKernelGGL((k_probe<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl,
+                           src, dst, n, first_pos, 1.0f);
+    });
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Repeated rows.  Work item {start, len, key, kind}: the contributions at
 // sorted positions start .. start + len - 1 are added in that order, in
 // double (a hub row can collect tens of thousands of terms), and the row is

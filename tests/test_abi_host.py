@@ -99,6 +99,7 @@ def test_calls_reject_bad_arguments_before_any_launch():
     assert L.huge_eval_loss(None, None, None, None, 0, 0, None, None) == -1
     assert L.huge_get_rows(None, 0, None, 1, None, None) == -1
     assert L.huge_sample_negatives(None, 1, 0, None, None) == -1
+    assert L.huge_probe_rows(None, None, None, 1, 0, None) == -1
     assert L.huge_check(None, None) == -1
     assert L.huge_step_stats(None, None, None, None, None) == -1
     L.huge_destroy(None)

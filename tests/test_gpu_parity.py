@@ -274,6 +274,28 @@ def test_get_rows_and_out_of_range_ids():
     assert tr.check() == -2
 
 
+@pytest.mark.parametrize("D,K", [(128, 5), (36, 11), (1024, 2)])
+def test_probe_rows_leaves_tables_bitwise_unchanged(D, K):
+    """The bandwidth probe reads and rewrites every row a step would touch
+    (hub rows included) and must leave both tables bit for bit as they were;
+    an out-of-range id is reported and skipped."""
+    N, n = 3000, 2000
+    rng = np.random.default_rng(D + K)
+    src, dst, cc = _random_batch(rng, N, n, hub_frac=0.3)
+    tr = _trainer(N, D, K, n, seed=6)
+    tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), 0, 0.05)  # non-initial values
+    S0, T0 = tr.S.clone(), tr.T.clone()
+    for rep in range(3):
+        tr.probe_rows(dev(src, torch), dev(dst, torch), n * (rep + 1))
+    assert tr.check() == 0
+    assert torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+    bad = src.copy()
+    bad[7] = N
+    tr.probe_rows(dev(bad, torch), dev(dst, torch), 0)
+    assert tr.check() == -2
+    assert torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+
+
 def test_eval_loss_matches_oracle_and_writes_nothing():
     N, D, K, n = 2000, 48, 6, 1500
     rng = np.random.default_rng(5)
