@@ -29,14 +29,20 @@ METRIC = "positive (src,dst) pairs/sec per train step; achieved HBM GB/s vs peak
 HBM_PEAK_GBPS = 8000.0
 KERNEL = "k_fused_step"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "fused_step_sbm100m_counters.txt")
-KERNEL_SOURCES = ["paper_2307_14490_amd/csrc/k_step.hip", "paper_2307_14490_amd/csrc/device.hpp"]
+KERNEL_SOURCES = ["paper_2307_14490_amd/csrc/device.hpp", "paper_2307_14490_amd/csrc/k_step.hip"]
+KERNEL_END = "int64_t fused_step_blocks("  # the fused kernel's source ends before this line
 
 
 def kernel_source_hash() -> str:
+    """Hash of the fused kernel's source: device.hpp and k_step.hip up to the
+    end of k_fused_step (the counters stay valid while neither changes)."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
         with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+            text = f.read()
+        if p.endswith("k_step.hip"):
+            text = text[:text.index(KERNEL_END.encode())]
+        h.update(text)
     return h.hexdigest()[:16]
 
 
