@@ -6,6 +6,8 @@ baseline may import this module.  It loads ``liboracle.so`` built from
 library) and adds numpy glue:
 
 * :func:`step_dense`   -- one synchronous SGD step on whole float32 tables;
+* :func:`lwsgd_lr`     -- the LWSGD learning-rate schedule (Table 2), as the
+  piecewise-linear curve through its knots;
 * :func:`step_sparse`  -- the same step on the rows a batch touches only, with
   every other row left at its initial value.  Tables too large for host memory
   (up to 1e8 x 128 floats) are represented by the rows the batch reads; each
@@ -263,3 +265,18 @@ def step_sparse(seed: int, num_nodes: int, dim: int, num_neg: int, half_width: f
     neg_c = np.searchsorted(rows_T, neg.reshape(-1)).astype(np.int32).reshape(n, num_neg)
     loss = step_dense(S, T, src_c, dst_c, cc, neg_c, lr)
     return SparseStep(rows_S, S, rows_T, T, loss, neg)
+
+
+def lwsgd_lr(t: int, warmup: int, peak: float, decay: int, final: float) -> float:
+    """LWSGD (Table 2): linear warm-up to `peak` over `warmup` steps, linear
+    decay to `final` over `decay` steps, then `final`.  Reading (the paper
+    gives only the four numbers): steps count from 0 and the curve is the
+    straight line through the knots (-1, 0), (warmup - 1, peak),
+    (warmup + decay - 1, final), held constant after the last knot."""
+    knots = [(-1.0, 0.0), (warmup - 1.0, peak), (warmup + decay - 1.0, final)]
+    if t >= knots[-1][0]:
+        return final
+    for (x0, y0), (x1, y1) in zip(knots, knots[1:]):
+        if x0 <= t <= x1 and x1 > x0:
+            return y0 + (y1 - y0) * (t - x0) / (x1 - x0)
+    return final

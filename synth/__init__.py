@@ -14,7 +14,9 @@ the paper are replaced by random graphs of the kind it uses, Sec. 4.1.1):
 * ``powerlaw``  Chung-Lu, 10M nodes, exponent 2.1, annealed walks;
 * ``sbm100m``   SBM, 100M nodes, annealed walks;
 * ``hubstress`` Chung-Lu, 50M nodes, exponent 1.9, i.i.d. endpoint pairs,
-                Zipf(1.5) co_counts capped at 1000.
+                Zipf(1.5) co_counts capped at 1000;
+* ``sbm100m_k31`` the SBM-100M graph with 31 negatives per positive (the
+                number of negatives of the paper's TPU runs, Table 2).
 """
 from .gen import (  # noqa: F401
     CONFIGS,

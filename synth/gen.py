@@ -74,6 +74,10 @@ CONFIGS = {
     "hubstress": Config("hubstress", 4, 50_000_000, 256, 20, 262_144, 0.025, "alias",
                         "chung_lu", exponent=1.9, mean_deg=50.0, pairs="endpoints",
                         cc_zipf=1.5, cc_cap=1000),
+    # the SBM-100M graph with the paper's 31 negatives per positive (Table 2)
+    "sbm100m_k31": Config("sbm100m_k31", 5, 100_000_000, 128, 31, 262_144, 0.025, "uniform",
+                          "sbm", blocks=1000, deg_in=25.0, deg_out=2.0, walks_per_node=1,
+                          walk_steps=20, window=2),
 }
 
 

@@ -32,7 +32,7 @@ def _need_gpu():
 
 
 CASES = [("medium", "sorted"), ("medium", "atomic"), ("powerlaw", "sorted"),
-         ("sbm100m", "sorted"), ("hubstress", "sorted")]
+         ("sbm100m", "sorted"), ("hubstress", "sorted"), ("sbm100m_k31", "sorted")]
 
 
 @pytest.mark.timeout(600)

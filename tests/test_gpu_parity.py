@@ -372,6 +372,39 @@ def test_tiny_epoch_loss_curve(scatter):
     assert_close(tr.T.cpu().numpy(), T, "T after epoch", abs_tol=1e-4, rel_tol=1e-3)
 
 
+def test_lwsgd_schedule_over_tiny_steps():
+    """60 steps of the tiny workload under a scaled LWSGD schedule (warm-up
+    15, peak 0.05, decay 30, final 0.01): the GPU takes each step's rate from
+    the library's helper, the oracle from its own definition of the schedule;
+    per-step losses and the final tables must agree."""
+    from paper_2307_14490_amd.schedule import lwsgd
+    from synth import make_workload
+    wl = make_workload("tiny", 0)
+    cfg = wl.cfg
+    src, dst, cc = wl.epoch()
+    steps, sched = 60, (15, 0.05, 30, 0.01)
+    tr = _trainer(cfg.num_nodes, cfg.dim, cfg.num_neg, cfg.batch, seed=3)
+    losses = torch.zeros(steps, dtype=torch.float64, device="cuda")
+    ds, dd, dc = dev(src, torch), dev(dst, torch), dev(cc, torch)
+    for b in range(steps):
+        lo, hi = b * cfg.batch, (b + 1) * cfg.batch
+        tr.step(ds[lo:hi], dd[lo:hi], dc[lo:hi], lo, lwsgd(b, *sched), loss_out=losses[b:b + 1])
+    gl = losses.cpu().numpy()
+    a = _half(cfg.dim)
+    ids = np.arange(cfg.num_nodes)
+    S = orc.init_rows(3, 0, ids, cfg.dim, a)
+    T = orc.init_rows(3, 1, ids, cfg.dim, a)
+    ol = np.zeros(steps)
+    for b in range(steps):
+        lo, hi = b * cfg.batch, (b + 1) * cfg.batch
+        neg = orc.sample_negatives(3, lo, hi - lo, cfg.num_neg, cfg.num_nodes)
+        ol[b] = orc.step_dense(S, T, src[lo:hi], dst[lo:hi], cc[lo:hi], neg,
+                               orc.lwsgd_lr(b, *sched))
+    np.testing.assert_allclose(gl, ol, rtol=1e-5)
+    assert_close(tr.S.cpu().numpy(), S, "S after LWSGD steps", abs_tol=1e-5, rel_tol=1e-4)
+    assert_close(tr.T.cpu().numpy(), T, "T after LWSGD steps", abs_tol=1e-5, rel_tol=1e-4)
+
+
 # --------------------------------------------------------------------------- #
 # Grouping on one stream while the previous batch is applied on another
 # --------------------------------------------------------------------------- #
