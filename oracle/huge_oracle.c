@@ -399,3 +399,134 @@ int oracle_sgns_loss(const float *S, const float *T, int64_t ns, int64_t nt, int
     *loss_out = loss;
     return OR_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Random-walk co-occurrence sampler (Sec. 3.2, Alg. 1).                      */
+/*                                                                           */
+/* Every seed node s is repeated walks_per_node (gamma) times; walk r of s    */
+/* takes walk_steps (k) uniform steps: w_0 = s, and w_t is neighbour          */
+/* floor(x * deg / 2^64) of w_{t-1} in CSR order, x = (r1 << 32) | r0 of      */
+/* Philox4x32-10 on counter (lo32 s, hi32 s, r, 4 + t) under the seed's key;  */
+/* a node without neighbours ends the walk.  The walks of one seed are        */
+/* grouped and their co-occurrences combined (Alg. 1, GroupByKey and          */
+/* CombineValues):                                                           */
+/*   seed_only = 1: the pairs (s, w_t), t = 1 .. window, as in the paper      */
+/*                  (the histogram is indexed by the distance t from s);      */
+/*   seed_only = 0: every ordered pair (w_a, w_b) of a walk with              */
+/*                  1 <= |a - b| <= window (DeepWalk's window), distance      */
+/*                  |a - b|.                                                  */
+/* Pairs of a node with itself are dropped.  Output: one triple per distinct  */
+/* (source, destination) of a seed, seeds in ascending order and, within a   */
+/* seed, (source, destination) ascending; cc = number of co-occurrences,      */
+/* hist[d - 1] = those at distance d (window entries per triple).             */
+/* Returns -4 with *count_out = the number needed if capacity is too small.   */
+/* ------------------------------------------------------------------------- */
+#define OR_ECAP (-4)
+
+typedef struct {
+    int32_t src, dst, dist;
+} walk_pair;
+
+static int cmp_walk_pair(const void *a, const void *b) {
+    const walk_pair *x = (const walk_pair *)a, *y = (const walk_pair *)b;
+    if (x->src != y->src) return x->src < y->src ? -1 : 1;
+    if (x->dst != y->dst) return x->dst < y->dst ? -1 : 1;
+    if (x->dist != y->dist) return x->dist < y->dist ? -1 : 1;
+    return 0;
+}
+
+/* One walk; returns its last position (0 .. walk_steps), or -1 on a bad graph. */
+static int32_t oracle_walk(const int64_t *off, const int32_t *nbr, int64_t num_nodes,
+                           int64_t num_edges, uint64_t seed, int64_t s, int32_t r,
+                           int32_t walk_steps, int32_t *w) {
+    uint32_t key[2], ctr[4], rr[4];
+    seed_key(seed, key);
+    w[0] = (int32_t)s;
+    for (int32_t t = 1; t <= walk_steps; ++t) {
+        const int64_t cur = w[t - 1];
+        const int64_t b = off[cur], e = off[cur + 1];
+        if (b < 0 || e < b || e > num_edges) return -1;
+        const uint64_t deg = (uint64_t)(e - b);
+        if (deg == 0) return t - 1;
+        ctr[0] = (uint32_t)((uint64_t)s & 0xFFFFFFFFu);
+        ctr[1] = (uint32_t)((uint64_t)s >> 32);
+        ctr[2] = (uint32_t)r;
+        ctr[3] = 4u + (uint32_t)t;
+        oracle_philox4x32_10(ctr, key, rr);
+        const uint64_t x = ((uint64_t)rr[1] << 32) | (uint64_t)rr[0];
+        const uint64_t j = (uint64_t)(((unsigned __int128)x * (unsigned __int128)deg) >> 64);
+        const int64_t next = nbr[b + (int64_t)j];
+        if (next < 0 || next >= num_nodes) return -1;
+        w[t] = (int32_t)next;
+    }
+    return walk_steps;
+}
+
+int oracle_sample_walks(const int64_t *off, const int32_t *nbr, int64_t num_nodes,
+                        int64_t num_edges, int32_t walks_per_node, int32_t walk_steps,
+                        int32_t window, int32_t seed_only, uint64_t seed, int64_t first_seed,
+                        int64_t num_seeds, int32_t *src, int32_t *dst, int32_t *cc,
+                        int32_t *hist, int64_t capacity, int64_t *count_out) {
+    if (!off || (num_edges > 0 && !nbr) || num_nodes < 1 || num_edges < 0 ||
+        walks_per_node < 1 || walk_steps < 1 || window < 1 || window > walk_steps ||
+        num_seeds < 0 || first_seed < 0 || first_seed + num_seeds > num_nodes || capacity < 0 ||
+        !count_out || (capacity > 0 && (!src || !dst || !cc)))
+        return OR_EINVAL;
+    int32_t *w = (int32_t *)malloc(sizeof(int32_t) * (size_t)(walk_steps + 1));
+    /* pairs of one seed: at most walks * (walk_steps + 1)^2 */
+    const int64_t max_pairs =
+        (int64_t)walks_per_node * (int64_t)(walk_steps + 1) * (int64_t)(walk_steps + 1);
+    walk_pair *pairs = (walk_pair *)malloc(sizeof(walk_pair) * (size_t)max_pairs);
+    if (!w || !pairs) {
+        free(w); free(pairs);
+        return OR_EINVAL;
+    }
+    int64_t out = 0;
+    int rc = OR_OK;
+    for (int64_t s = first_seed; s < first_seed + num_seeds && rc == OR_OK; ++s) {
+        int64_t np = 0;
+        for (int32_t r = 0; r < walks_per_node; ++r) {
+            const int32_t last = oracle_walk(off, nbr, num_nodes, num_edges, seed, s, r,
+                                             walk_steps, w);
+            if (last < 0) {
+                rc = OR_ERANGE;
+                break;
+            }
+            for (int32_t a = 0; a <= last; ++a) {
+                if (seed_only && a > 0) break;
+                for (int32_t b = 0; b <= last; ++b) {
+                    const int32_t d = a > b ? a - b : b - a;
+                    if (d < 1 || d > window) continue;
+                    if (seed_only && b < a) continue;
+                    if (w[a] == w[b]) continue;
+                    pairs[np].src = w[a];
+                    pairs[np].dst = w[b];
+                    pairs[np].dist = d;
+                    ++np;
+                }
+            }
+        }
+        if (rc != OR_OK) break;
+        qsort(pairs, (size_t)np, sizeof(walk_pair), cmp_walk_pair);
+        for (int64_t i = 0; i < np;) {
+            int64_t j = i;
+            while (j < np && pairs[j].src == pairs[i].src && pairs[j].dst == pairs[i].dst) ++j;
+            if (out < capacity) {
+                src[out] = pairs[i].src;
+                dst[out] = pairs[i].dst;
+                cc[out] = (int32_t)(j - i);
+                if (hist) {
+                    for (int32_t d = 0; d < window; ++d) hist[out * window + d] = 0;
+                    for (int64_t q = i; q < j; ++q) hist[out * window + pairs[q].dist - 1] += 1;
+                }
+            }
+            ++out;
+            i = j;
+        }
+    }
+    free(w);
+    free(pairs);
+    *count_out = out;
+    if (rc != OR_OK) return rc;
+    return out > capacity ? OR_ECAP : OR_OK;
+}

@@ -6,6 +6,8 @@ baseline may import this module.  It loads ``liboracle.so`` built from
 library) and adds numpy glue:
 
 * :func:`step_dense`   -- one synchronous SGD step on whole float32 tables;
+* :func:`sample_walks` -- co-occurrence triples from uniform random walks grouped
+  by seed (Sec. 3.2, Alg. 1);
 * :func:`lwsgd_lr`     -- the LWSGD learning-rate schedule (Table 2), as the
   piecewise-linear curve through its knots;
 * :func:`step_sparse`  -- the same step on the rows a batch touches only, with
@@ -77,7 +79,13 @@ def lib():
                   ctypes.c_int64, ctypes.c_int32, _i32p, _i32p, _i32p, _i32p]
         L.oracle_sgns_step.argtypes = f_args + [ctypes.c_float, _f64p]
         L.oracle_sgns_loss.argtypes = f_args + [_f64p]
+        L.oracle_sample_walks.argtypes = [_i64p, _i32p, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
+                                          ctypes.c_int64, _i32p, _i32p, _i32p, _i32p,
+                                          ctypes.c_int64, _i64p]
         for name in ("oracle_init_rows", "oracle_build_alias", "oracle_sample_negatives",
+                     "oracle_sample_walks",
                      "oracle_sgns_grad_d", "oracle_sgns_loss_d", "oracle_sgns_step",
                      "oracle_sgns_loss"):
             getattr(L, name).restype = ctypes.c_int
@@ -280,3 +288,31 @@ def lwsgd_lr(t: int, warmup: int, peak: float, decay: int, final: float) -> floa
         if x0 <= t <= x1 and x1 > x0:
             return y0 + (y1 - y0) * (t - x0) / (x1 - x0)
     return final
+
+
+def sample_walks(off, nbr, num_nodes: int, walks_per_node: int, walk_steps: int, window: int,
+                 seed_only: bool, seed: int, first_seed: int = 0, num_seeds=None):
+    """Co-occurrence triples of the walks of seeds first_seed ..
+    first_seed + num_seeds - 1 (see oracle_sample_walks in huge_oracle.c):
+    returns (src, dst, cc, hist[n x window]) as int32 arrays."""
+    L = lib()
+    off = _c(off, np.int64)
+    nbr = _c(nbr, np.int32)
+    if num_seeds is None:
+        num_seeds = num_nodes - first_seed
+    count = ctypes.c_int64(0)
+    args = (off.ctypes.data_as(_i64p), nbr.ctypes.data_as(_i32p), int(num_nodes),
+            int(nbr.size), int(walks_per_node), int(walk_steps), int(window),
+            int(bool(seed_only)), int(seed), int(first_seed), int(num_seeds))
+    rc = L.oracle_sample_walks(*args, None, None, None, None, 0, ctypes.byref(count))
+    if rc not in (0, -4):
+        _check(rc, "oracle_sample_walks")
+    n = count.value
+    src = np.zeros(n, np.int32)
+    dst = np.zeros(n, np.int32)
+    cc = np.zeros(n, np.int32)
+    hist = np.zeros((n, window), np.int32)
+    rc = L.oracle_sample_walks(*args, _ptr(src, _i32p), _ptr(dst, _i32p), _ptr(cc, _i32p),
+                               _ptr(hist, _i32p), n, ctypes.byref(count))
+    _check(rc, "oracle_sample_walks")
+    return src, dst, cc, hist
