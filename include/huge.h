@@ -205,6 +205,64 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
 huge_status huge_profile_begin(huge_handle* h, int32_t max_steps);
 huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int32_t* steps);
 
+/* ------------------------------------------------------------------------
+   Random-walk sampler: the (source_id, destination_id, co_counts) triples the
+   step consumes, produced on the GPU from a graph in device memory
+   (Sec. 3.2, Alg. 1).  Every seed node s is repeated walks_per_node times
+   (Alg. 1's gamma); walk r of s takes walk_steps uniform steps (Alg. 1's k):
+   w_0 = s, w_t = neighbour floor(x deg / 2^64) of w_{t-1} in CSR order, x the
+   64-bit word (r1 << 32) | r0 of Philox4x32-10 on counter
+   (lo32 s, hi32 s, r, 4 + t) under key (lo32 seed, hi32 seed); a node without
+   neighbours ends the walk.  The walks of a seed are grouped and their
+   co-occurrences combined (Alg. 1, GroupByKey, CombineValues) into one triple
+   per distinct (source, destination) pair:
+     seed_pairs_only = 1: the pairs (s, w_t) for t = 1 .. window -- the
+                          paper's triple, its histogram indexed by the walk
+                          distance from the seed (Sec. 3.2);
+     seed_pairs_only = 0: every ordered pair (w_a, w_b) of a walk with
+                          1 <= |a - b| <= window (DeepWalk's context window).
+   Pairs of a node with itself are dropped.  cc = the pair's co-occurrences;
+   hist[d - 1] = those at distance d.  Triples come in ascending seed order
+   and, within a seed, in ascending (source, destination) order: the output
+   is a deterministic function of the graph, the config and the seed range. */
+typedef struct huge_walk_config {
+    int64_t num_nodes;       /* N: nodes of the graph, 1 .. 2^31-1                      */
+    int32_t walks_per_node;  /* walks started from every seed, 1 .. 1024                */
+    int32_t walk_steps;      /* steps per walk, 1 .. 64                                  */
+    int32_t window;          /* largest co-occurrence distance, 1 .. min(walk_steps, 32) */
+    int32_t seed_pairs_only; /* 1: pairs (seed, w_t); 0: all pairs within the window     */
+    uint64_t seed;           /* Philox key                                               */
+} huge_walk_config;
+/* Besides these bounds, a seed's walks may hold at most 8192 nodes
+   (walks_per_node x (walk_steps + 1)) and 4096 pairs (walks_per_node x
+   window for seed pairs, walks_per_node x 2 (window (walk_steps + 1) -
+   window (window + 1) / 2) for window pairs). */
+
+/* Bytes of device workspace huge_sample_walks needs for num_seeds seeds;
+   0 if the config is invalid. */
+size_t huge_walk_workspace_bytes(const huge_walk_config* cfg, int64_t num_seeds);
+
+/* Triples of the seeds first_seed .. first_seed + num_seeds - 1.
+     d_offsets   : N + 1 int64 CSR offsets (device), non-decreasing from 0
+     d_neighbors : num_edges int32 neighbour ids in [0, N) (device)
+     d_src, d_dst, d_cc : capacity int32 each (device), the triples
+     d_hist      : capacity x window int32 (device), or NULL
+     d_count     : device int64, receives the number of triples (also when
+                   it exceeds capacity)
+     d_status    : device int32, receives 0; -2 if the graph is malformed
+                   (an offset or neighbour out of range: nothing is written);
+                   -4 if the triples exceed capacity (nothing is written)
+     d_workspace : >= huge_walk_workspace_bytes(cfg, num_seeds) bytes, 256-byte
+                   aligned
+   Asynchronous on `stream`; host-detectable argument errors return before
+   any launch. */
+huge_status huge_sample_walks(const huge_walk_config* cfg, const int64_t* d_offsets,
+                              const int32_t* d_neighbors, int64_t num_edges, int64_t first_seed,
+                              int64_t num_seeds, int32_t* d_src, int32_t* d_dst, int32_t* d_cc,
+                              int32_t* d_hist, int64_t capacity, int64_t* d_count,
+                              int32_t* d_status, void* d_workspace, size_t ws_bytes,
+                              void* stream);
+
 void huge_destroy(huge_handle* h);
 const char* huge_status_string(huge_status s);
 

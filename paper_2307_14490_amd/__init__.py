@@ -1,6 +1,7 @@
 """MI355X-native training step of HUGE (KDD'23): skip-gram negative sampling
 over (source_id, destination_id, co_counts) batches, in hand-written HIP
-kernels behind the C ABI of ``include/huge.h``.
+kernels behind the C ABI of ``include/huge.h``, and the random-walk sampler
+that produces those batches on the GPU.
 
 ``binding`` is the ctypes layer; ``build`` compiles ``libhuge.so`` in-tree.
 """
@@ -12,10 +13,13 @@ from .binding import (  # noqa: F401
     HUGE_SCATTER_SORTED,
     HugeConfig,
     HugeError,
+    HugeWalkConfig,
     Trainer,
     build_alias,
     load,
     make_config,
+    sample_walks,
     status_string,
+    walk_config,
     workspace_bytes,
 )

@@ -31,7 +31,7 @@ EXPORTED = [
     "huge_workspace_bytes", "huge_build_alias", "huge_init_tables", "huge_attach_tables",
     "huge_train_step", "huge_prepare_step", "huge_train_prepared", "huge_eval_loss",
     "huge_get_rows", "huge_sample_negatives", "huge_probe_rows", "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
-    "huge_destroy", "huge_status_string",
+    "huge_destroy", "huge_status_string", "huge_walk_workspace_bytes", "huge_sample_walks",
 ]
 HUGE_PHASES = 6
 
@@ -46,6 +46,17 @@ class HugeConfig(ctypes.Structure):
         ("init_half_width", ctypes.c_float),
         ("neg_kind", ctypes.c_int32),
         ("scatter_kind", ctypes.c_int32),
+    ]
+
+
+class HugeWalkConfig(ctypes.Structure):
+    _fields_ = [
+        ("num_nodes", ctypes.c_int64),
+        ("walks_per_node", ctypes.c_int32),
+        ("walk_steps", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("seed_pairs_only", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
     ]
 
 
@@ -89,6 +100,13 @@ def load() -> ctypes.CDLL:
     L.huge_profile_begin.argtypes = [_vp, ctypes.c_int32]
     L.huge_profile_end.argtypes = [_vp, _vp, ctypes.POINTER(ctypes.c_double),
                                    ctypes.POINTER(ctypes.c_int32)]
+    wcfgp = ctypes.POINTER(HugeWalkConfig)
+    L.huge_walk_workspace_bytes.argtypes = [wcfgp, ctypes.c_int64]
+    L.huge_walk_workspace_bytes.restype = ctypes.c_size_t
+    L.huge_sample_walks.argtypes = [wcfgp, _vp, _vp, ctypes.c_int64, ctypes.c_int64,
+                                    ctypes.c_int64, _vp, _vp, _vp, _vp, ctypes.c_int64, _vp, _vp,
+                                    _vp, ctypes.c_size_t, _vp]
+    L.huge_sample_walks.restype = ctypes.c_int32
     L.huge_destroy.argtypes = [_vp]
     L.huge_destroy.restype = None
     L.huge_status_string.argtypes = [ctypes.c_int32]
@@ -272,3 +290,58 @@ class Trainer:
             self.close()
         except Exception:
             pass
+
+
+def walk_config(num_nodes, walks_per_node, walk_steps, window, seed_pairs_only=True, seed=0):
+    return HugeWalkConfig(int(num_nodes), int(walks_per_node), int(walk_steps), int(window),
+                          int(bool(seed_pairs_only)), int(seed))
+
+
+def sample_walks(offsets, neighbors, num_nodes, walks_per_node, walk_steps, window,
+                 seed_pairs_only=True, seed=0, first_seed=0, num_seeds=None, capacity=None,
+                 with_hist=True, stream=None):
+    """Co-occurrence triples of random walks on a device CSR graph (int64
+    offsets, int32 neighbours), computed by huge_sample_walks.  With
+    capacity=None the triples are counted first (one extra pass) and the
+    outputs sized to fit.  Returns (src, dst, cc, hist or None) on the device."""
+    import torch
+    L = load()
+    cfg = walk_config(num_nodes, walks_per_node, walk_steps, window, seed_pairs_only, seed)
+    if num_seeds is None:
+        num_seeds = int(num_nodes) - int(first_seed)
+    dev = offsets.device
+    ws_bytes = L.huge_walk_workspace_bytes(ctypes.byref(cfg), int(num_seeds))
+    if ws_bytes == 0:
+        raise HugeError(HUGE_ERR_INVALID_ARG, "huge_walk_workspace_bytes")
+    ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=dev)
+    ws_off = (-ws.data_ptr()) % 256
+    count = torch.zeros(1, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    empty = torch.empty(0, dtype=torch.int32, device=dev)
+
+    def run(cap, src, dst, cc, hist):
+        _ok(L.huge_sample_walks(ctypes.byref(cfg), _dptr(offsets), _dptr(neighbors),
+                                neighbors.numel(), int(first_seed), int(num_seeds),
+                                _dptr(src) if cap else None, _dptr(dst) if cap else None,
+                                _dptr(cc) if cap else None,
+                                _dptr(hist) if (cap and hist is not None) else None, int(cap),
+                                _dptr(count), _dptr(status), ws.data_ptr() + ws_off, ws_bytes,
+                                _stream_ptr(stream)), "huge_sample_walks")
+
+    if capacity is None:
+        run(0, empty, empty, empty, None)
+        st = int(status.item())
+        if st not in (0, -4):
+            raise HugeError(st, "huge_sample_walks (device)")
+        capacity = int(count.item())
+    n = int(capacity)
+    src = torch.empty(n, dtype=torch.int32, device=dev)
+    dst = torch.empty(n, dtype=torch.int32, device=dev)
+    cc = torch.empty(n, dtype=torch.int32, device=dev)
+    hist = torch.empty((n, int(window)), dtype=torch.int32, device=dev) if with_hist else None
+    run(n, src, dst, cc, hist)
+    st = int(status.item())
+    if st != 0:
+        raise HugeError(st, "huge_sample_walks (device)")
+    got = int(count.item())
+    return src[:got], dst[:got], cc[:got], (hist[:got] if hist is not None else None)

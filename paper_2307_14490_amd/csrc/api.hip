@@ -503,6 +503,70 @@ huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_
     return HUGE_OK;
 }
 
+namespace {
+
+// Pairs one walk of steps + 1 nodes contributes at most.
+int64_t walk_pairs_per_walk(const huge_walk_config* c) {
+    if (c->seed_pairs_only) return c->window;
+    const int64_t w = c->window, L = c->walk_steps + 1;
+    return 2 * (w * L - w * (w + 1) / 2);
+}
+
+bool walk_config_ok(const huge_walk_config* c) {
+    if (!c) return false;
+    if (c->num_nodes < 1 || c->num_nodes > 2147483647LL) return false;
+    if (c->walks_per_node < 1 || c->walks_per_node > kWalkMaxWalks) return false;
+    if (c->walk_steps < 1 || c->walk_steps > kWalkMaxSteps) return false;
+    if (c->window < 1 || c->window > c->walk_steps || c->window > kWalkMaxWindow) return false;
+    if (c->seed_pairs_only != 0 && c->seed_pairs_only != 1) return false;
+    if ((int64_t)c->walks_per_node * (c->walk_steps + 1) > kWalkMaxNodes) return false;
+    if ((int64_t)c->walks_per_node * walk_pairs_per_walk(c) > kWalkMaxPairs) return false;
+    return true;
+}
+
+}  // namespace
+
+size_t huge_walk_workspace_bytes(const huge_walk_config* cfg, int64_t num_seeds) {
+    if (!walk_config_ok(cfg) || num_seeds < 0) return 0;
+    const size_t n = (size_t)(num_seeds > 0 ? num_seeds : 1);
+    return align_up(sizeof(uint64_t) * n) + align_up(sizeof(uint32_t) * n);
+}
+
+huge_status huge_sample_walks(const huge_walk_config* cfg, const int64_t* d_offsets,
+                              const int32_t* d_neighbors, int64_t num_edges, int64_t first_seed,
+                              int64_t num_seeds, int32_t* d_src, int32_t* d_dst, int32_t* d_cc,
+                              int32_t* d_hist, int64_t capacity, int64_t* d_count,
+                              int32_t* d_status, void* d_workspace, size_t ws_bytes,
+                              void* stream) {
+    if (!walk_config_ok(cfg) || !d_offsets || num_edges < 0 || (num_edges > 0 && !d_neighbors))
+        return HUGE_ERR_INVALID_ARG;
+    if (first_seed < 0 || num_seeds < 0 || first_seed + num_seeds > cfg->num_nodes)
+        return HUGE_ERR_INVALID_ARG;
+    if (capacity < 0 || !d_count || !d_status || !d_workspace) return HUGE_ERR_INVALID_ARG;
+    if (capacity > 0 && (!d_src || !d_dst || !d_cc)) return HUGE_ERR_INVALID_ARG;
+    if ((uintptr_t)d_workspace % kAlign != 0) return HUGE_ERR_INVALID_ARG;
+    if (ws_bytes < huge_walk_workspace_bytes(cfg, num_seeds)) return HUGE_ERR_WORKSPACE;
+    const size_t n = (size_t)(num_seeds > 0 ? num_seeds : 1);
+    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
+    uint64_t* offsets = reinterpret_cast<uint64_t*>(ws);
+    uint32_t* counts = reinterpret_cast<uint32_t*>(ws + align_up(sizeof(uint64_t) * n));
+    WalkArgs A;
+    A.off = d_offsets;
+    A.nbr = d_neighbors;
+    A.num_nodes = cfg->num_nodes;
+    A.num_edges = num_edges;
+    A.walks = cfg->walks_per_node;
+    A.steps = cfg->walk_steps;
+    A.window = cfg->window;
+    A.seed_only = cfg->seed_pairs_only;
+    A.seed = cfg->seed;
+    A.first_seed = first_seed;
+    A.num_seeds = num_seeds;
+    HIP_TRY(launch_walks(A, counts, offsets, d_count, capacity, d_src, d_dst, d_cc, d_hist,
+                         d_status, static_cast<hipStream_t>(stream)));
+    return HUGE_OK;
+}
+
 huge_status huge_check(huge_handle* h, void* stream) {
     if (!h) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);

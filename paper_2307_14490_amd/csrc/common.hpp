@@ -29,6 +29,12 @@ constexpr int kSamplePer = 2;          // positives per thread in the sampler
 constexpr int kNegBlock = 8;           // negatives whose rows are in flight together
 constexpr int kMaxNeg = 64;
 constexpr int kMaxDim = 1024;
+// Random-walk sampler: one workgroup holds a seed's walks and pairs in LDS.
+constexpr int kWalkMaxWalks = 1024;    // walks per seed
+constexpr int kWalkMaxNodes = 8192;    // walks x (steps + 1)
+constexpr int kWalkMaxPairs = 4096;    // co-occurrence pairs of one seed
+constexpr int kWalkMaxSteps = 64;
+constexpr int kWalkMaxWindow = 32;
 
 // Status bits of a step (Control::step_bad) and the sticky error code.
 constexpr uint32_t kBadId = 1u;
@@ -135,6 +141,20 @@ struct TableArgs {
     const int32_t* alias;
 };
 
+struct WalkArgs {
+    const int64_t* off;  // CSR offsets, num_nodes + 1
+    const int32_t* nbr;  // CSR neighbours, num_edges
+    int64_t num_nodes;
+    int64_t num_edges;
+    int32_t walks;       // walks per seed (gamma)
+    int32_t steps;       // steps per walk (k)
+    int32_t window;      // largest co-occurrence distance
+    int32_t seed_only;   // pairs (seed, w_t) only
+    uint64_t seed;       // Philox key
+    int64_t first_seed;
+    int64_t num_seeds;
+};
+
 // ---------------------------------------------------------------------------
 // Launchers (each defined next to its kernels).  All return hipError_t of the
 // launch.
@@ -168,6 +188,9 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t* longhead,
                                const uint32_t* keys, int64_t m, const double* partA,
                                const double* partB, float lr, hipStream_t s);
+hipError_t launch_walks(const WalkArgs& A, uint32_t* counts, uint64_t* offsets, int64_t* total,
+                        int64_t capacity, int32_t* src, int32_t* dst, int32_t* cc, int32_t* hist,
+                        int32_t* status, hipStream_t s);
 hipError_t launch_loss_final(Control* ctl, const double* lossp, int64_t blocks, double* out,
                              hipStream_t s);
 hipError_t launch_atomic_gather(const TableArgs& t, Control* ctl, const StepArgs& a,
