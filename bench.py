@@ -97,6 +97,118 @@ def cpu_baseline(wl, seed, budget_s=15.0, max_batches=8):
     }
 
 
+def bench_producer(args):
+    """The random-walk sampler on the exact SBM graph of a workload (default
+    the 1M-node medium one) with the paper's sampling parameters (Table 2:
+    128 walks of 3 steps per node; pairs of the seed with each visited node,
+    their distance histograms): all seeds in chunks, timed with HIP events."""
+    import numpy as np
+    import torch
+
+    import paper_2307_14490_amd as P
+    from synth import make_workload
+
+    def log(*a):
+        print(*a, file=sys.stderr, flush=True)
+
+    wl = make_workload(args.workload, args.seed)
+    if wl.csr is None:
+        raise SystemExit(f"--producer needs a workload with an exact graph (tiny, medium)")
+    off, nbr = wl.csr
+    N = wl.cfg.num_nodes
+    gamma, steps, window = 128, 3, 3
+    chunk = 65536
+    doff = torch.from_numpy(np.asarray(off, np.int64)).cuda()
+    dnbr = torch.from_numpy(np.asarray(nbr, np.int32)).cuda()
+    log(f"[bench] graph: {N} nodes, {nbr.size} directed edges")
+    cap = chunk * gamma * window
+    cfg = P.walk_config(N, gamma, steps, window, True, args.seed)
+    L = P.load()
+    import ctypes
+    ws_bytes = L.huge_walk_workspace_bytes(ctypes.byref(cfg), chunk)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    outs = [torch.empty(cap, dtype=torch.int32, device="cuda") for _ in range(3)]
+    hist = torch.empty((cap, window), dtype=torch.int32, device="cuda")
+    counts = torch.zeros(max(1, (N + chunk - 1) // chunk), dtype=torch.int64, device="cuda")
+    status = torch.zeros(counts.numel(), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def run_all():
+        for c, s0 in enumerate(range(0, N, chunk)):
+            ns = min(chunk, N - s0)
+            rc = L.huge_sample_walks(ctypes.byref(cfg), doff.data_ptr(), dnbr.data_ptr(),
+                                     dnbr.numel(), s0, ns, outs[0].data_ptr(),
+                                     outs[1].data_ptr(), outs[2].data_ptr(), hist.data_ptr(),
+                                     cap, counts[c:c + 1].data_ptr(),
+                                     status[c:c + 1].data_ptr(), ws.data_ptr(), ws_bytes,
+                                     ctypes.c_void_p(stream.cuda_stream))
+            if rc != 0:
+                raise P.HugeError(rc, "huge_sample_walks")
+
+    run_all()  # warm-up
+    torch.cuda.synchronize()
+    if int(status.abs().max().item()) != 0:
+        raise RuntimeError("the sampler reported an error")
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    reps = max(1, args.steps // 100)
+    ev0.record(stream)
+    for _ in range(reps):
+        run_all()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / reps
+    triples = int(counts.sum().item())
+    walk_steps = N * gamma * steps
+    value = triples / (ms * 1e-3)
+    log(f"[bench] {triples} triples from {N} seeds in {ms:.2f} ms")
+    # Algorithmic bytes: per walk step two offsets and one neighbour (20 B),
+    # taken twice (counting pass and writing pass), plus the triples written
+    # (src, dst, cc and a 3-entry histogram: 24 B each).
+    alg_bytes = 2 * 20.0 * walk_steps + 24.0 * triples
+    achieved = alg_bytes / (ms * 1e-3) / 1e9
+    out = {
+        "metric": "co-occurrence triples/sec (random-walk sampler)",
+        "value": value,
+        "unit": "triples/s",
+        "n_gpus": 1,
+        "steps": reps,
+        "warmup": 1,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.cfg.name} graph, sampler", "num_nodes": N,
+                   "edges": int(nbr.size), "walks_per_node": gamma, "walk_steps": steps,
+                   "window": window, "pairs": "seed", "seeds_per_call": chunk},
+        "roofline": {"kernel": "k_walk", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": None,
+                     "note": "dependent random 4-16 B reads: latency-bound, not bandwidth-bound"},
+        "walk_steps_per_s": walk_steps / (ms * 1e-3),
+    }
+    if not args.no_cpu:
+        from oracle import oracle as orc
+        t0 = time.perf_counter()
+        done = 0
+        n_seeds = 0
+        while time.perf_counter() - t0 < args.cpu_budget and n_seeds < N:
+            r = orc.sample_walks(off, nbr, N, gamma, steps, window, True, args.seed,
+                                 first_seed=n_seeds, num_seeds=min(2000, N - n_seeds))
+            done += r[0].size
+            n_seeds += min(2000, N - n_seeds)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": done / dt, "unit": "triples/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{n_seeds} seeds of the same graph and parameters, "
+                                         f"{dt:.1f} s single-threaded"}
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -112,6 +224,9 @@ def main():
                     help="one stream, huge_train_step per step (no overlap of grouping)")
     ap.add_argument("--pipeline", default="alternate", choices=["alternate", "side"],
                     help="streams of the overlapped steps (see run_steps)")
+    ap.add_argument("--producer", action="store_true",
+                    help="measure the random-walk sampler instead of the training step "
+                         "(default workload: medium)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -119,6 +234,13 @@ def main():
               "MI355X's HBM and has no multi-GPU path; run it with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.producer:
+        import torch
+        torch.cuda.set_device(0)
+        if args.workload == "sbm100m":
+            args.workload = "medium"
+        return bench_producer(args)
 
     import numpy as np
     import torch
