@@ -222,8 +222,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--sequential", action="store_true",
                     help="one stream, huge_train_step per step (no overlap of grouping)")
-    ap.add_argument("--pipeline", default="alternate", choices=["alternate", "side"],
+    ap.add_argument("--pipeline", default="side", choices=["alternate", "side"],
                     help="streams of the overlapped steps (see run_steps)")
+    ap.add_argument("--no-phases", action="store_true",
+                    help="diagnostic: no per-phase HIP events in the timed steps (no roofline)")
     ap.add_argument("--producer", action="store_true",
                     help="measure the random-walk sampler instead of the training step "
                          "(default workload: medium)")
@@ -283,13 +285,12 @@ def main():
     streams = [stream, side]
 
     def run_steps(count, first_batch, pos):
-        """`count` steps.  Pipelined: batch k is grouped and applied on
-        streams[k % 2], and batch k+1 is grouped while batch k is applied, so
-        the grouping of k+1 runs beside the apply of k and the apply of k+1
-        follows its own grouping on the same stream (the wait for the apply
-        of k crosses streams, and that apply has finished first).  With
-        --pipeline side, every grouping runs on `side` and every apply on the
-        current stream."""
+        """`count` steps.  Pipelined: batch k+1 is prepared before batch k is
+        applied.  With --pipeline side (default), every batch is prepared on
+        `side` and applied on the current stream: the library issues batch
+        k+1's radix pass on the apply stream just before batch k's update, and
+        its grouping on `side`, beside that update.  With --pipeline
+        alternate, batch k is prepared and applied on streams[k % 2]."""
         if args.sequential:
             for k in range(count):
                 s, d, c = dev_batches[(first_batch + k) % R]
@@ -316,7 +317,8 @@ def main():
     log("[bench] warm-up done")
 
     # Timed region: exactly K steps; phase events recorded inside the library.
-    tr.profile_begin(args.steps)
+    if not args.no_phases:
+        tr.profile_begin(args.steps)  # events around the fused kernel only
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -327,6 +329,11 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
+    if args.no_phases:
+        log(f"[bench] no phase events: {total_ms / args.steps:.4f} ms/step")
+        print(json.dumps({"metric": METRIC, "value": n * args.steps / (total_ms / 1e3),
+                          "ms_per_step": total_ms / args.steps, "phases": None}), flush=True)
+        return
     phase_ms, prof_steps = tr.profile_end()
     if tr.check() != 0:
         raise RuntimeError("device reported an error in the timed steps")
@@ -356,13 +363,22 @@ def main():
     probe_gbps = probe_bytes / (probe_us * 1e-6) / 1e9
     log(f"[bench] probe: {probe_us:.1f} us per launch, {probe_gbps:.0f} GB/s")
 
+    phases = ["setup_sample", "radix", "group", "fused_step", "repeated_rows", "loss"]
+    fused_us = phase_ms[3] / max(prof_steps, 1) * 1e3
+    # Phase breakdown from a separate pass of 50 steps with an event at every
+    # phase boundary (those events lengthen each step by tens of microseconds,
+    # so the timed steps above record only the two around the fused kernel).
+    n_diag = min(50, args.steps)
+    tr.profile_begin(n_diag, all_phases=True)
+    pos = run_steps(n_diag, args.warmup + args.steps, pos)
+    stream.wait_stream(side)
+    diag_ms, diag_steps = tr.profile_end()
+    phase_avg_us = {p: diag_ms[i] / max(diag_steps, 1) * 1e3 for i, p in enumerate(phases)}
+
     # Algorithmic bytes of the fused kernel per launch: the batch (12 B per
     # positive), each distinct row read once (4 D bytes) and each row that
     # occurs once written once in place.  Repeated rows are written by the
     # duplicate kernels, not counted here.
-    phases = ["setup_sample", "sort", "mark", "fused_step", "repeated_rows", "loss"]
-    phase_avg_us = {p: phase_ms[i] / max(prof_steps, 1) * 1e3 for i, p in enumerate(phases)}
-    fused_us = phase_avg_us["fused_step"]
     if args.scatter == "sorted":
         seq = [(args.warmup + k) % R for k in range(args.steps)]
         uS = np.mean([per_batch_stats[b][0] for b in seq])
@@ -426,6 +442,7 @@ def main():
             "alg_bytes": step_bytes,
             "alg_GBps": step_bytes / (ms_per_step * 1e-3) / 1e9,
             "phase_avg_us": phase_avg_us,
+            "phase_note": "from a separate 50-step pass with an event at every phase boundary",
             "unique_src_rows": uS,
             "unique_ctx_rows": uT,
             "repeated_row_occurrences": dup,

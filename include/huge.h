@@ -59,9 +59,10 @@ typedef int32_t huge_status;
 #define HUGE_NEG_UNIFORM 0
 #define HUGE_NEG_ALIAS 1
 
-/* Gradient scatter: SORTED groups the rows of a batch by id (radix sort),
-   updates rows that occur once in place and sums repeated rows in occurrence
-   order -- bitwise reproducible run to run.  ATOMIC adds every contribution
+/* Gradient scatter: SORTED groups the rows of a batch by id (one radix pass
+   on the lowest digit, then a hash table per bucket), updates rows that occur
+   once in place and sums repeated rows in occurrence order -- bitwise
+   reproducible run to run.  ATOMIC adds every contribution
    with fp32 atomics into the tables after all reads -- same result up to the
    order of summation, not reproducible bit for bit. */
 #define HUGE_SCATTER_SORTED 0
@@ -134,19 +135,25 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
                             const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                             float lr, double* d_loss_sum, void* stream);
 
-/* The same step in two halves, so that the next batch can be grouped on one
-   stream while the current one is applied on another (grouping never reads
-   or writes the tables).
-     huge_prepare_step   : validation, negative draws, de-duplication of the
-                           batch's rows, into the next of two grouping slots;
-                           at most two prepared batches may be pending
+/* The same step in two halves, so that the next batch is grouped while the
+   current one is applied (grouping never reads or writes the tables).
+     huge_prepare_step   : validation, negative draws and grouping keys of a
+                           batch, on `stream` (the grouping stream); at most
+                           two prepared batches may be pending
      huge_train_prepared : the gather, loss and update of the oldest prepared
-                           batch, with the given lr and loss output
-   The library orders the halves with HIP events: an apply waits for its
-   grouping and for the previous apply; a grouping waits until the apply
-   that last used its slot is done.  The batch arrays must stay valid until
-   the batch is applied.  Results are bitwise those of huge_train_step, which
-   is the two halves on one stream and requires that no batch is pending. */
+                           batch, with the given lr and loss output, on
+                           `stream` (the apply stream)
+   huge_train_prepared also issues the rest of the grouping: on the apply
+   stream, whatever its own batch still lacks and then the radix pass of the
+   next prepared batch (it runs alone, before the update); on the next
+   batch's grouping stream, that batch's per-bucket grouping (it runs beside
+   the update).  So the stream given to huge_prepare_step must stay valid
+   until the batch is applied.  The library orders all of this with HIP
+   events: every stage waits for the previous stage of its batch, an apply
+   for the previous apply, a new batch for the apply that last used its
+   grouping buffers.  The batch arrays must stay valid until the batch is
+   applied.  Results are bitwise those of huge_train_step, which is the two
+   halves on one stream and requires that no batch is pending. */
 huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
                               const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                               void* stream);
@@ -191,18 +198,21 @@ huge_status huge_check(huge_handle* h, void* stream);
 huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
                             int64_t* unique_ctx, int64_t* dup_occurrences);
 
-/* Phase timing.  After huge_profile_begin(h, max_steps), each of the next
-   max_steps calls of huge_train_step records HIP events on its stream at the
-   phase boundaries (groupings and applies on their own streams).
-   huge_profile_end waits for all of them on `stream`, writes the
-   summed durations in milliseconds to phase_ms[HUGE_PHASES] and the number
-   of recorded steps to *steps, and releases the events.  Phases: 0 set-up
-   and negative sampling, 1 radix sort, 2 run marking (grouping; 1 and 2 are
-   empty for the atomic scatter), 3 the fused gather/loss/update kernel
+/* Phase timing.  After huge_profile_begin(h, max_steps, all_phases), each
+   of the next max_steps batches (prepared, or stepped with huge_train_step)
+   records HIP events on the streams its stages run on: around the fused
+   kernel only (all_phases = 0), or at every phase boundary (all_phases = 1;
+   each event is one more packet in a stream, which costs a few
+   microseconds of every step).  huge_profile_end waits for all of them on
+   `stream`, writes the summed durations in milliseconds to
+   phase_ms[HUGE_PHASES] (0 for phases not recorded) and the number of
+   recorded steps to *steps, and releases the events.  Phases: 0 set-up and
+   negative sampling, 1 the radix pass, 2 the per-bucket grouping (1 and 2
+   are empty for the atomic scatter), 3 the fused gather/loss/update kernel
    (atomic scatter: gather and coefficients), 4 repeated rows (atomic
    scatter: the atomic adds), 5 loss sum. */
 #define HUGE_PHASES 6
-huge_status huge_profile_begin(huge_handle* h, int32_t max_steps);
+huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases);
 huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int32_t* steps);
 
 /* ------------------------------------------------------------------------

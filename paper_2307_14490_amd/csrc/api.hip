@@ -1,14 +1,23 @@
 // C-ABI host layer of libhuge: argument checks, workspace layout, and the
-// launch sequence of each call on the caller's stream.
+// launch sequence of each call on the caller's streams.
 //
-// A step has two halves.  Grouping (k_begin, k_sample, the radix passes,
-// k_mark) reads only the batch; applying (k_fused_step, the repeated-row
-// kernels, the loss) reads and writes the tables.  Two grouping slots let
-// the caller group batch t+1 on one stream while batch t is applied on
-// another; events recorded here order the two: an apply waits until its
-// slot's grouping is complete, a grouping waits until the previous apply
-// that used its slot is complete.
+// A batch goes through four stages: sampling (k_begin, k_sample: validation,
+// negatives, keys, digit counts), the radix pass (k_radix_pass: keys grouped
+// by their lowest digit), grouping (k_group: repeated rows and their slots)
+// and the apply (k_fused_step, the repeated-row kernels, the loss).  The
+// first three read only the batch; the apply reads and writes the tables.
+// huge_prepare_step issues the sampling on the caller's grouping stream.
+// huge_train_prepared issues, on the apply stream, whatever its own batch
+// still lacks, then the radix pass of the next prepared batch -- while
+// nothing else runs: its 1024-thread workgroups would find no free CU beside
+// an apply -- then the apply; the next batch's grouping (256-thread
+// workgroups) goes to that batch's grouping stream, where it runs beside the
+// apply.  kSlots grouping slots let two batches be prepared ahead; events
+// order the stages: a stage waits for the previous stage of its batch, an
+// apply for the previous apply, a sampling for the apply that last used its
+// slot.
 #include <math.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -22,9 +31,12 @@ using namespace huge;
 
 namespace {
 
-constexpr int kSlots = 2;
-constexpr int kPrepEvents = 4;   // begin, after sampling, after sort, after marking
-constexpr int kApplyEvents = 4;  // begin, after fused step, after repeated rows, after loss
+// Events recorded per profiled batch: sampling start and end, radix pass
+// start and end, grouping start and end, apply start, after the fused
+// kernel, after the repeated rows, after the loss.
+constexpr int kProfEvents = 10;
+constexpr int kMaxPending = 2;  // prepared batches not yet applied
+constexpr int kBesideGrid = 0;  // workgroups of a grouping beside an apply (0: one per bucket)
 
 struct PendingBatch {
     const int32_t* src = nullptr;
@@ -32,6 +44,10 @@ struct PendingBatch {
     const int32_t* cc = nullptr;
     int64_t n = 0;
     uint64_t first_pos = 0;
+    int stage = 0;               // 0 sampled, 1 radix pass issued, 2 grouped
+    hipStream_t gstream = nullptr;  // the stream of its huge_prepare_step
+    hipStream_t stage_stream = nullptr;  // the stream of its last stage
+    int prof = -1;               // index of its profile events, or -1
 };
 
 }  // namespace
@@ -45,18 +61,28 @@ struct huge_handle {
     uint8_t* ws;
     size_t ws_bytes;
     Layout lay;
-    SortPlan plan;  // radix passes and digit width for keys below 2N
+    SortPlan plan;  // digit width of the radix pass for keys below 2N
     int key_bits;   // bits of 2N - 1
-    uint32_t epoch;            // tags the look-back words of each grouping
-    int64_t prepared;          // groupings issued
+    uint32_t epoch;            // tags the look-back words of each radix pass
+    int64_t prepared;          // batches sampled
     int64_t applied;           // applies issued
     int last_applied_slot;     // -1 before the first apply
     PendingBatch pending[kSlots];
-    hipEvent_t ready[kSlots];  // grouping of the slot complete
-    hipEvent_t done[kSlots];   // apply of the slot complete
+    hipEvent_t sampled[kSlots];  // sampling of the slot's batch complete
+    hipEvent_t radixed[kSlots];  // its radix pass complete
+    hipEvent_t ready[kSlots];    // its grouping complete
+    hipEvent_t done[kSlots];     // its apply complete
     // phase timing
-    std::vector<hipEvent_t> prep_ev, apply_ev;
-    int32_t prof_max = 0, prof_prep = 0, prof_apply = 0;
+    std::vector<hipEvent_t> prof_ev;
+    std::vector<char> prof_applied;
+    int32_t prof_max = 0, prof_next = 0;
+    bool prof_all = false;     // events at every phase boundary, not only the fused kernel
+    // the stream each kind of stage last used, so that a wait on an event of
+    // the same stream is skipped (the stream orders it already)
+    hipStream_t last_apply_stream = nullptr;
+    hipStream_t slot_apply_stream[kSlots] = {};
+    int beside_grid = kBesideGrid;  // workgroups of a grouping beside an apply
+    int group_bits = 0;             // grouping table bits; 0: from the mean bucket size
 };
 
 namespace {
@@ -98,10 +124,14 @@ Layout make_layout(const huge_config* c) {
     const int64_t nb = c->max_batch;
     const int64_t M = nb * (2 + K);
     const bool sorted = c->scatter_kind == HUGE_SCATTER_SORTED;
+    const ListCaps caps = list_caps(M);
     L.max_occ = M;
     L.sort_tiles = (M + kSortTile - 1) / kSortTile;
-    L.windows = M / kChunk + 2;
     L.loss_blocks = nb + 1;  // at most one workgroup per positive
+    L.cap_short = caps.shorts;
+    L.cap_piece = caps.pieces;
+    L.cap_comb = caps.combs;
+    L.cap_part = caps.parts;
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t at = off;
@@ -116,23 +146,20 @@ Layout make_layout(const huge_config* c) {
         if (sorted) {
             S.keys0 = take(sizeof(uint32_t) * (size_t)M);
             S.keys1 = take(sizeof(uint32_t) * (size_t)M);
-            S.vals0 = take(sizeof(uint32_t) * (size_t)M);
             S.vals1 = take(sizeof(uint32_t) * (size_t)M);
             S.info = take(sizeof(int32_t) * (size_t)M);
             S.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kMaxBins));
             S.bstart = take(sizeof(uint32_t) * kMaxBins);
-            S.biglist = take(sizeof(uint32_t) * kMaxBins);
-            S.work = take(sizeof(uint4) * (size_t)(L.windows * kChunk));
-            S.wcount = take(sizeof(uint32_t) * (size_t)L.windows);
-            S.longhead = take(sizeof(uint32_t) * (size_t)L.windows);
-            S.wstats = take(sizeof(uint32_t) * (size_t)(L.windows * 3));
+            S.shorts = take(sizeof(uint4) * (size_t)caps.shorts);
+            S.pieces = take(sizeof(uint4) * (size_t)caps.pieces);
+            S.combs = take(sizeof(uint4) * (size_t)caps.combs);
+            S.wstats = take(sizeof(uint32_t) * kMaxBins * 3);
         }
     }
     L.eval_ctrl = take(sizeof(Control));
     L.lossp = take(sizeof(double) * (size_t)L.loss_blocks);
     if (sorted) {
-        L.partA = take(sizeof(double) * (size_t)(L.windows * D));
-        L.partB = take(sizeof(double) * (size_t)(L.windows * D));
+        L.part = take(sizeof(double) * (size_t)caps.parts * (size_t)D);
         L.dup = take(sizeof(float) * (size_t)(M * D));
     } else {
         L.gsrc = take(sizeof(float) * (size_t)(nb * D));
@@ -165,22 +192,26 @@ TableArgs table_args(huge_handle* h) {
         if ((expr) != hipSuccess) return HUGE_ERR_HIP;  \
     } while (0)
 
+#define HIP_TRY_ST(expr)                  \
+    do {                                  \
+        const huge_status st_ = (expr);   \
+        if (st_ != HUGE_OK) return st_;   \
+    } while (0)
+
 void release_profile(huge_handle* h) {
-    for (hipEvent_t e : h->prep_ev)
+    for (hipEvent_t e : h->prof_ev)
         if (e) (void)hipEventDestroy(e);
-    for (hipEvent_t e : h->apply_ev)
-        if (e) (void)hipEventDestroy(e);
-    h->prep_ev.clear();
-    h->apply_ev.clear();
-    h->prof_max = h->prof_prep = h->prof_apply = 0;
+    h->prof_ev.clear();
+    h->prof_applied.clear();
+    h->prof_max = h->prof_next = 0;
 }
 
 void destroy_handle(huge_handle* h) {
     if (!h) return;
     release_profile(h);
     for (int s = 0; s < kSlots; ++s) {
-        if (h->ready[s]) (void)hipEventDestroy(h->ready[s]);
-        if (h->done[s]) (void)hipEventDestroy(h->done[s]);
+        for (hipEvent_t e : {h->sampled[s], h->radixed[s], h->ready[s], h->done[s]})
+            if (e) (void)hipEventDestroy(e);
     }
     delete h;
 }
@@ -209,14 +240,25 @@ huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* t
     h->key_bits = key_bits(cfg->num_nodes);
     h->plan = sort_plan(h->key_bits);
     h->epoch = 0;
+    if (const char* e = getenv("HUGE_BESIDE_GRID")) {  // tuning experiments
+        const int g = atoi(e);
+        if (g >= 0 && g <= 65536) h->beside_grid = g;
+    }
+    if (const char* e = getenv("HUGE_GROUP_TABLE_BITS")) {  // tuning experiments
+        const int g = atoi(e);
+        if (g >= kTableBitsMin && g <= kTableBitsMax) h->group_bits = g;
+    }
     h->prepared = h->applied = 0;
     h->last_applied_slot = -1;
-    for (int s = 0; s < kSlots; ++s) h->ready[s] = h->done[s] = nullptr;
+    for (int s = 0; s < kSlots; ++s)
+        h->sampled[s] = h->radixed[s] = h->ready[s] = h->done[s] = nullptr;
     for (int s = 0; s < kSlots; ++s) {
-        if (hipEventCreateWithFlags(&h->ready[s], hipEventDisableTiming) != hipSuccess ||
-            hipEventCreateWithFlags(&h->done[s], hipEventDisableTiming) != hipSuccess) {
-            destroy_handle(h);
-            return HUGE_ERR_HIP;
+        for (hipEvent_t* e : {&h->sampled[s], &h->radixed[s], &h->ready[s], &h->done[s]}) {
+            if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) {
+                *e = nullptr;
+                destroy_handle(h);
+                return HUGE_ERR_HIP;
+            }
         }
     }
     *out = h;
@@ -245,132 +287,169 @@ huge_status check_batch_args(huge_handle* h, const int32_t* src, const int32_t* 
     return HUGE_OK;
 }
 
-// Grouping of one batch into the next slot (launches only; arguments checked).
-huge_status group_batch(huge_handle* h, const int32_t* src, const int32_t* dst,
-                        const int32_t* cc, int64_t n, uint64_t first_pos, hipStream_t s) {
+// Profile event k of a batch, recorded on s (nothing if it is not profiled).
+bool prof_mark(huge_handle* h, const PendingBatch& b, int k, hipStream_t s) {
+    if (b.prof < 0) return true;
+    if (!h->prof_all && k != 6 && k != 7) return true;  // the fused kernel only
+    return hipEventRecord(h->prof_ev[(size_t)b.prof * kProfEvents + k], s) == hipSuccess;
+}
+
+// Make s wait for event e recorded on stream `from`, unless that is s itself.
+hipError_t wait_on(hipStream_t s, hipEvent_t e, hipStream_t from) {
+    if (from == s) return hipSuccess;
+    return hipStreamWaitEvent(s, e, 0);
+}
+
+// Stage 1: validation, negatives, keys and digit counts of a batch, into the
+// next slot, on the grouping stream s (launches only; arguments checked).
+huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
+                         const int32_t* cc, int64_t n, uint64_t first_pos, hipStream_t s) {
     const int slot = (int)(h->prepared % kSlots);
     const SlotLayout& SL = h->lay.slot[slot];
     Control* ctl = at<Control>(h, SL.ctrl);
     uint32_t* hist = at<uint32_t>(h, SL.hist);
-    int32_t* neg = at<int32_t>(h, SL.neg);
     const TableArgs t = table_args(h);
     const StepArgs a{src, dst, cc, n, first_pos, 0.0f, nullptr};
-    const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-
-    hipEvent_t* ev = nullptr;
-    if (h->prof_prep < h->prof_max) ev = &h->prep_ev[(size_t)h->prof_prep++ * kPrepEvents];
-    auto mark = [&](int k) -> bool {
-        return ev == nullptr || hipEventRecord(ev[k], s) == hipSuccess;
-    };
-
+    PendingBatch b;
+    b.src = src;
+    b.dst = dst;
+    b.cc = cc;
+    b.n = n;
+    b.first_pos = first_pos;
+    b.gstream = s;
+    b.prof = h->prof_next < h->prof_max ? h->prof_next++ : -1;
     // the slot's previous apply must be complete before its buffers change
-    HIP_TRY(hipStreamWaitEvent(s, h->done[slot], 0));
-    if (!mark(0)) return HUGE_ERR_HIP;
+    HIP_TRY(wait_on(s, h->done[slot], h->slot_apply_stream[slot]));
+    if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
     HIP_TRY(launch_begin(ctl, hist, s));
-    if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-        uint32_t* keys[2] = {at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1)};
-        uint32_t* vals[2] = {at<uint32_t>(h, SL.vals0), at<uint32_t>(h, SL.vals1)};
-        uint64_t* status = at<uint64_t>(h, SL.status);
-        HIP_TRY(launch_sample(t, ctl, a, neg, keys[0], at<int32_t>(h, SL.info), hist, h->plan,
-                              s));
-        if (!mark(1)) return HUGE_ERR_HIP;
-        // look-back tags: 8 per grouping; the words are cleared when the
-        // 30-bit tag wraps
-        h->epoch += 1;
-        if ((h->epoch & 0x07FFFFFFu) == 0u) {
-            for (int k = 0; k < kSlots; ++k)
-                HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
-                                            h->lay.sort_tiles * kMaxBins, s));
-            h->epoch += 1;
-        }
-        // First pass: buckets by the lowest digit.  Then each bucket is
-        // sorted in LDS into the buffer the full sort would end in; the later
-        // passes run only if a bucket was too large for that (ctl->overflow).
-        const int fin = h->plan.passes & 1;
-        uint32_t* bstart = at<uint32_t>(h, SL.bstart);
-        HIP_TRY(launch_radix_pass(ctl, keys[0], nullptr, keys[1], vals[1], m, 0, h->plan.bits,
-                                  hist, status, h->epoch << 3, nullptr, bstart, s));
-        if (h->plan.passes > 1) {
-            HIP_TRY(launch_bucket_sort(ctl, keys[1], vals[1], keys[fin], vals[fin], m,
-                                       h->plan.bits, h->key_bits, hist, bstart,
-                                       at<uint32_t>(h, SL.biglist), s));
-            int cur = 1;
-            for (int p = 1; p < h->plan.passes; ++p) {
-                const uint32_t tag = (h->epoch << 3) | (uint32_t)p;
-                HIP_TRY(launch_radix_pass(ctl, keys[cur], vals[cur], keys[cur ^ 1], vals[cur ^ 1],
-                                          m, p, h->plan.bits, hist, status, tag, &ctl->overflow,
-                                          nullptr, s));
-                cur ^= 1;
-            }
-        }
-        const int cur = fin;
-        if (!mark(2)) return HUGE_ERR_HIP;
-        HIP_TRY(launch_mark(ctl, keys[cur], vals[cur], m, t.N, at<int32_t>(h, SL.info),
-                            at<uint4>(h, SL.work), at<uint32_t>(h, SL.wcount),
-                            at<uint32_t>(h, SL.longhead), at<uint32_t>(h, SL.wstats), s));
-        if (!mark(3)) return HUGE_ERR_HIP;
-    } else {
-        HIP_TRY(launch_sample(t, ctl, a, neg, nullptr, nullptr, hist, h->plan, s));
-        if (!mark(1) || !mark(2) || !mark(3)) return HUGE_ERR_HIP;
-    }
-    HIP_TRY(hipEventRecord(h->ready[slot], s));
-    h->pending[slot] = PendingBatch{src, dst, cc, n, first_pos};
+    const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
+    // only the digit counts of the one radix pass are needed
+    const SortPlan one{1, h->plan.bits};
+    HIP_TRY(launch_sample(t, ctl, a, at<int32_t>(h, SL.neg),
+                          sorted ? at<uint32_t>(h, SL.keys0) : nullptr,
+                          sorted ? at<int32_t>(h, SL.info) : nullptr, hist, one, s));
+    if (!prof_mark(h, b, 1, s)) return HUGE_ERR_HIP;
+    HIP_TRY(hipEventRecord(h->sampled[slot], s));
+    b.stage = sorted ? 0 : 2;  // the atomic scatter needs no grouping
+    if (!sorted) HIP_TRY(hipEventRecord(h->ready[slot], s));
+    b.stage_stream = s;
+    h->pending[slot] = b;
     h->prepared += 1;
     return HUGE_OK;
 }
 
-// Apply the oldest grouped batch (launches only).
-huge_status apply_batch(huge_handle* h, float lr, double* loss_out, hipStream_t s) {
+// Stage 2: the radix pass of the batch in `slot`, on s.
+huge_status stage_radix(huge_handle* h, int slot, hipStream_t s) {
+    PendingBatch& b = h->pending[slot];
+    const SlotLayout& SL = h->lay.slot[slot];
+    Control* ctl = at<Control>(h, SL.ctrl);
+    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+    HIP_TRY(wait_on(s, h->sampled[slot], b.stage_stream));
+    if (!prof_mark(h, b, 2, s)) return HUGE_ERR_HIP;
+    // look-back tags: 8 per radix pass; the words are cleared when the 27-bit
+    // epoch wraps
+    h->epoch += 1;
+    if ((h->epoch & 0x07FFFFFFu) == 0u) {
+        for (int k = 0; k < kSlots; ++k)
+            HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
+                                        h->lay.sort_tiles * kMaxBins, s));
+        h->epoch += 1;
+    }
+    HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), nullptr, at<uint32_t>(h, SL.keys1),
+                              at<uint32_t>(h, SL.vals1), m, 0, h->plan.bits,
+                              at<uint32_t>(h, SL.hist), at<uint64_t>(h, SL.status),
+                              h->epoch << 3, nullptr, at<uint32_t>(h, SL.bstart), s));
+    if (!prof_mark(h, b, 3, s)) return HUGE_ERR_HIP;
+    HIP_TRY(hipEventRecord(h->radixed[slot], s));
+    b.stage = 1;
+    b.stage_stream = s;
+    return HUGE_OK;
+}
+
+// Stage 3: grouping of the batch in `slot`, on s.  Beside an apply
+// (`beside`), its workgroups are few and loop over the buckets, so that they
+// hold a slot of the fused kernel on only a few CUs.
+huge_status stage_group(huge_handle* h, int slot, hipStream_t s, bool beside) {
+    PendingBatch& b = h->pending[slot];
+    const SlotLayout& SL = h->lay.slot[slot];
+    const Layout& L = h->lay;
+    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+    HIP_TRY(wait_on(s, h->radixed[slot], b.stage_stream));
+    if (!prof_mark(h, b, 4, s)) return HUGE_ERR_HIP;
+    const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
+    HIP_TRY(launch_group(at<Control>(h, SL.ctrl), at<uint32_t>(h, SL.keys1),
+                         at<uint32_t>(h, SL.vals1), m, h->cfg.num_nodes, at<uint32_t>(h, SL.hist),
+                         at<uint32_t>(h, SL.bstart), at<int32_t>(h, SL.info),
+                         at<uint4>(h, SL.shorts), at<uint4>(h, SL.pieces), at<uint4>(h, SL.combs),
+                         caps, at<uint32_t>(h, SL.wstats), 1 << h->plan.bits, h->key_bits,
+                         beside ? h->beside_grid : 0, h->group_bits, s));
+    if (!prof_mark(h, b, 5, s)) return HUGE_ERR_HIP;
+    HIP_TRY(hipEventRecord(h->ready[slot], s));
+    b.stage = 2;
+    b.stage_stream = s;
+    return HUGE_OK;
+}
+
+// The oldest prepared batch: its missing stages and the next batch's radix
+// pass on s, the next batch's grouping on its own stream, then the apply
+// (launches only).
+huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s) {
     const int slot = (int)(h->applied % kSlots);
+    PendingBatch& b = h->pending[slot];
+    if (b.stage == 0) HIP_TRY_ST(stage_radix(h, slot, s));
+    if (b.stage == 1) HIP_TRY_ST(stage_group(h, slot, s, false));
+    if (h->prepared > h->applied + 1) {
+        const int nslot = (int)((h->applied + 1) % kSlots);
+        PendingBatch& nb = h->pending[nslot];
+        if (nb.stage == 0) {
+            HIP_TRY_ST(stage_radix(h, nslot, s));
+            HIP_TRY_ST(stage_group(h, nslot, nb.gstream, true));
+        }
+    }
+
     const SlotLayout& SL = h->lay.slot[slot];
     const Layout& L = h->lay;
     Control* ctl = at<Control>(h, SL.ctrl);
-    const PendingBatch& b = h->pending[slot];
     const TableArgs t = table_args(h);
     const StepArgs a{b.src, b.dst, b.cc, b.n, b.first_pos, lr, loss_out};
     const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
     int32_t* neg = at<int32_t>(h, SL.neg);
     double* lossp = at<double>(h, L.lossp);
 
-    hipEvent_t* ev = nullptr;
-    if (h->prof_apply < h->prof_max) ev = &h->apply_ev[(size_t)h->prof_apply++ * kApplyEvents];
-    auto mark = [&](int k) -> bool {
-        return ev == nullptr || hipEventRecord(ev[k], s) == hipSuccess;
-    };
-
-    HIP_TRY(hipStreamWaitEvent(s, h->ready[slot], 0));
+    HIP_TRY(wait_on(s, h->ready[slot], b.stage_stream));
     // applies write the tables and share the apply regions: one at a time
     if (h->last_applied_slot >= 0)
-        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
-    if (!mark(0)) return HUGE_ERR_HIP;
+        HIP_TRY(wait_on(s, h->done[h->last_applied_slot], h->last_apply_stream));
+    if (!prof_mark(h, b, 6, s)) return HUGE_ERR_HIP;
     int64_t blocks = 0;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-        const uint32_t* keys_sorted = at<uint32_t>(h, (h->plan.passes & 1) ? SL.keys1 : SL.keys0);
-        double* partA = at<double>(h, L.partA);
-        double* partB = at<double>(h, L.partB);
+        double* part = at<double>(h, L.part);
         float* dup = at<float>(h, L.dup);
         HIP_TRY(launch_fused_step(t, ctl, a, neg, at<int32_t>(h, SL.info), dup, lossp, &blocks,
                                   s));
-        if (!mark(1)) return HUGE_ERR_HIP;
+        if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
         if (m > 0) {
-            HIP_TRY(launch_dup_apply(t, ctl, at<uint4>(h, SL.work), at<uint32_t>(h, SL.wcount),
-                                     dup, partA, partB, lr, m, s));
-            HIP_TRY(launch_long_combine(t, ctl, at<uint32_t>(h, SL.longhead), keys_sorted, m,
-                                        partA, partB, lr, s));
+            const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
+            HIP_TRY(launch_dup_apply(t, ctl, at<uint4>(h, SL.shorts), at<uint4>(h, SL.pieces),
+                                     dup, part, lr, caps, s));
+            HIP_TRY(launch_combine(t, ctl, at<uint4>(h, SL.combs), part, lr, caps, s));
         }
-        if (!mark(2)) return HUGE_ERR_HIP;
+        if (!prof_mark(h, b, 8, s)) return HUGE_ERR_HIP;
     } else {
         float* gsrc = at<float>(h, L.gsrc);
         float* coef = at<float>(h, L.coef);
         HIP_TRY(launch_atomic_gather(t, ctl, a, neg, gsrc, coef, lossp, &blocks, s));
-        if (!mark(1)) return HUGE_ERR_HIP;
+        if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
         HIP_TRY(launch_atomic_scatter_T(t, ctl, a, neg, coef, s));
         HIP_TRY(launch_atomic_scatter_S(t, ctl, a, gsrc, s));
-        if (!mark(2)) return HUGE_ERR_HIP;
+        if (!prof_mark(h, b, 8, s)) return HUGE_ERR_HIP;
     }
     if (loss_out) HIP_TRY(launch_loss_final(ctl, lossp, blocks, loss_out, s));
-    if (!mark(3)) return HUGE_ERR_HIP;
+    if (!prof_mark(h, b, 9, s)) return HUGE_ERR_HIP;
     HIP_TRY(hipEventRecord(h->done[slot], s));
+    if (b.prof >= 0) h->prof_applied[(size_t)b.prof] = 1;
+    h->slot_apply_stream[slot] = s;
+    h->last_apply_stream = s;
     h->last_applied_slot = slot;
     h->applied += 1;
     return HUGE_OK;
@@ -424,9 +503,9 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
     if (!isfinite(lr)) return HUGE_ERR_INVALID_ARG;
     if (h->prepared != h->applied) return HUGE_ERR_INVALID_ARG;  // a prepared batch is pending
     hipStream_t s = static_cast<hipStream_t>(stream);
-    st = group_batch(h, d_src, d_dst, d_cc, n, first_pos_index, s);
+    st = stage_sample(h, d_src, d_dst, d_cc, n, first_pos_index, s);
     if (st != HUGE_OK) return st;
-    return apply_batch(h, lr, d_loss_sum, s);
+    return apply_next(h, lr, d_loss_sum, s);
 }
 
 huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
@@ -434,15 +513,15 @@ huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_
                               void* stream) {
     huge_status st = check_batch_args(h, d_src, d_dst, d_cc, n);
     if (st != HUGE_OK) return st;
-    if (h->prepared - h->applied >= kSlots) return HUGE_ERR_INVALID_ARG;
-    return group_batch(h, d_src, d_dst, d_cc, n, first_pos_index,
-                       static_cast<hipStream_t>(stream));
+    if (h->prepared - h->applied >= kMaxPending) return HUGE_ERR_INVALID_ARG;
+    return stage_sample(h, d_src, d_dst, d_cc, n, first_pos_index,
+                        static_cast<hipStream_t>(stream));
 }
 
 huge_status huge_train_prepared(huge_handle* h, float lr, double* d_loss_sum, void* stream) {
     if (!h || !isfinite(lr)) return HUGE_ERR_INVALID_ARG;
     if (h->applied >= h->prepared) return HUGE_ERR_INVALID_ARG;  // nothing prepared
-    return apply_batch(h, lr, d_loss_sum, static_cast<hipStream_t>(stream));
+    return apply_next(h, lr, d_loss_sum, static_cast<hipStream_t>(stream));
 }
 
 huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
@@ -570,22 +649,30 @@ huge_status huge_sample_walks(const huge_walk_config* cfg, const int64_t* d_offs
 huge_status huge_check(huge_handle* h, void* stream) {
     if (!h) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // every grouping and apply issued so far, on any stream
+    // every stage issued so far, on any stream
     for (int k = 0; k < kSlots; ++k) {
-        HIP_TRY(hipStreamWaitEvent(s, h->ready[k], 0));
-        HIP_TRY(hipStreamWaitEvent(s, h->done[k], 0));
+        for (hipEvent_t e : {h->sampled[k], h->radixed[k], h->ready[k], h->done[k]})
+            HIP_TRY(hipStreamWaitEvent(s, e, 0));
     }
-    const size_t ctrls[3] = {h->lay.slot[0].ctrl, h->lay.slot[1].ctrl, h->lay.eval_ctrl};
-    uint32_t err[3] = {0, 0, 0};
-    for (int k = 0; k < 3; ++k) {
+    constexpr int kCtrls = kSlots + 1;
+    size_t ctrls[kCtrls];
+    for (int k = 0; k < kSlots; ++k) ctrls[k] = h->lay.slot[k].ctrl;
+    ctrls[kSlots] = h->lay.eval_ctrl;
+    Control got[kCtrls];
+    for (int k = 0; k < kCtrls; ++k) {
         Control* c = at<Control>(h, ctrls[k]);
-        HIP_TRY(hipMemcpyAsync(&err[k], &c->error, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(&got[k], c, sizeof(Control), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipMemsetAsync(&c->error, 0, sizeof(uint32_t), s));
+        HIP_TRY(hipMemsetAsync(&c->site, 0, sizeof(uint32_t), s));
     }
     HIP_TRY(hipStreamSynchronize(s));
-    uint32_t first = 0;
-    for (int k = 0; k < 3; ++k)
-        if (!first) first = err[k];
+    uint32_t first = 0, site = 0;
+    for (int k = 0; k < kCtrls; ++k) {
+        if (!first) first = got[k].error;
+        if (!site) site = got[k].site;
+    }
+    if (site != 0 && getenv("HUGE_DEBUG") != nullptr)
+        fprintf(stderr, "libhuge: internal check %u failed\n", site);
     if (first == kBadId) return HUGE_ERR_ID_OUT_OF_RANGE;
     if (first == kBadCount) return HUGE_ERR_BAD_COUNT;
     if (first != 0) return HUGE_ERR_HIP;
@@ -602,14 +689,15 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
         hipStream_t s = static_cast<hipStream_t>(stream);
         HIP_TRY(hipStreamWaitEvent(s, h->done[slot], 0));
         const int64_t m = h->pending[slot].n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-        const int64_t windows = (m + kChunk - 1) / kChunk;
-        std::vector<uint32_t> w((size_t)windows * 3);
-        if (windows > 0)
+        // k_group writes the counts of every bucket when the batch is not empty
+        const int64_t buckets = m > 0 ? ((int64_t)1 << h->plan.bits) : 0;
+        std::vector<uint32_t> w((size_t)buckets * 3);
+        if (buckets > 0)
             HIP_TRY(hipMemcpyAsync(w.data(), h->ws + h->lay.slot[slot].wstats,
                                    w.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
         HIP_TRY(hipStreamSynchronize(s));
         a = b = c = 0;
-        for (int64_t i = 0; i < windows; ++i) {
+        for (int64_t i = 0; i < buckets; ++i) {
             a += w[(size_t)i * 3];
             b += w[(size_t)i * 3 + 1];
             c += w[(size_t)i * 3 + 2];
@@ -621,18 +709,18 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
     return HUGE_OK;
 }
 
-huge_status huge_profile_begin(huge_handle* h, int32_t max_steps) {
+huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases) {
     if (!h || max_steps < 1 || max_steps > 1000000) return HUGE_ERR_INVALID_ARG;
+    if (all_phases != 0 && all_phases != 1) return HUGE_ERR_INVALID_ARG;
     release_profile(h);
-    h->prep_ev.assign((size_t)max_steps * kPrepEvents, nullptr);
-    h->apply_ev.assign((size_t)max_steps * kApplyEvents, nullptr);
-    for (std::vector<hipEvent_t>* v : {&h->prep_ev, &h->apply_ev}) {
-        for (hipEvent_t& e : *v) {
-            if (hipEventCreate(&e) != hipSuccess) {
-                e = nullptr;
-                release_profile(h);
-                return HUGE_ERR_HIP;
-            }
+    h->prof_all = all_phases != 0;
+    h->prof_ev.assign((size_t)max_steps * kProfEvents, nullptr);
+    h->prof_applied.assign((size_t)max_steps, 0);
+    for (hipEvent_t& e : h->prof_ev) {
+        if (hipEventCreate(&e) != hipSuccess) {
+            e = nullptr;
+            release_profile(h);
+            return HUGE_ERR_HIP;
         }
     }
     h->prof_max = max_steps;
@@ -643,29 +731,34 @@ huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int
     if (!h || !phase_ms || !steps) return HUGE_ERR_INVALID_ARG;
     huge_status st = HUGE_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    for (int k = 0; k < kSlots; ++k) {
-        if (hipStreamWaitEvent(s, h->ready[k], 0) != hipSuccess ||
-            hipStreamWaitEvent(s, h->done[k], 0) != hipSuccess)
-            st = HUGE_ERR_HIP;
+    for (int k = 0; k < kSlots && st == HUGE_OK; ++k) {
+        for (hipEvent_t e : {h->sampled[k], h->radixed[k], h->ready[k], h->done[k]})
+            if (hipStreamWaitEvent(s, e, 0) != hipSuccess) st = HUGE_ERR_HIP;
     }
     if (st == HUGE_OK && hipStreamSynchronize(s) != hipSuccess) st = HUGE_ERR_HIP;
     for (int k = 0; k < HUGE_PHASES; ++k) phase_ms[k] = 0.0;
-    auto sum = [&](const std::vector<hipEvent_t>& ev, int per, int used, int first_phase) {
-        for (int32_t i = 0; st == HUGE_OK && i < used; ++i) {
-            for (int k = 0; k + 1 < per; ++k) {
-                float ms = 0.0f;
-                if (hipEventElapsedTime(&ms, ev[(size_t)i * per + k],
-                                        ev[(size_t)i * per + k + 1]) != hipSuccess) {
-                    st = HUGE_ERR_HIP;
-                    break;
-                }
-                phase_ms[first_phase + k] += (double)ms;
+    // phase p lasts from event first[p] to event last[p] of a batch
+    static const int first[HUGE_PHASES] = {0, 2, 4, 6, 7, 8};
+    static const int last[HUGE_PHASES] = {1, 3, 5, 7, 8, 9};
+    int32_t counted = 0;
+    for (int32_t i = 0; st == HUGE_OK && i < h->prof_next; ++i) {
+        if (!h->prof_applied[(size_t)i]) continue;
+        const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
+        for (int p = 0; p < HUGE_PHASES; ++p) {
+            if (!sorted && (p == 1 || p == 2)) continue;  // no radix pass or grouping
+            if (!h->prof_all && p != 3) continue;         // only the fused kernel
+            float ms = 0.0f;
+            if (hipEventElapsedTime(&ms, h->prof_ev[(size_t)i * kProfEvents + first[p]],
+                                    h->prof_ev[(size_t)i * kProfEvents + last[p]]) !=
+                hipSuccess) {
+                st = HUGE_ERR_HIP;
+                break;
             }
+            phase_ms[p] += (double)ms;
         }
-    };
-    sum(h->prep_ev, kPrepEvents, h->prof_prep, 0);
-    sum(h->apply_ev, kApplyEvents, h->prof_apply, 3);
-    *steps = h->prof_apply < h->prof_prep ? h->prof_apply : h->prof_prep;
+        ++counted;
+    }
+    *steps = counted;
     release_profile(h);
     return st;
 }

@@ -19,13 +19,21 @@ constexpr int kSortThreads = 1024;     // threads of a sort workgroup (16 wave64
 constexpr int kSortItems = 8;          // keys per thread in a sort tile
 constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 keys per tile
 constexpr int kLookBatch = 8;          // look-back words read together
-constexpr int kLocalMaxBits = 9;       // digit width limit of the in-LDS bucket sort
-constexpr int kLocalBins = 1 << kLocalMaxBits;
-constexpr int kChunk = 256;            // sorted positions per duplicate-sum window
-constexpr uint32_t kNoHead = 0xFFFFFFFFu;
-constexpr uint32_t kLongPiece = 32;            // pieces longer than this are summed by a workgroup
-constexpr uint32_t kHasLong = 0x80000000u;     // window count flag: the window has such a piece
-constexpr int kSamplePer = 2;          // positives per thread in the sampler
+// Per-bucket grouping (k_group): chunks of kGroupChunk keys, an LDS hash
+// table of 2^bits slots (bits 12..14, from the mean bucket size); a bucket
+// range with more than 3/4 of the slots in distinct keys is split by further
+// hash bits.  Where a bucket's keys differ in at most kBitmapBits bits, an
+// LDS bitmap of them first marks the keys that occur more than once, and
+// only those enter the table (of 2^12 slots).
+constexpr int kGroupItems = 8;         // keys per thread in a grouping chunk
+constexpr int kGroupChunk = kBlock * kGroupItems;     // 2048 keys per chunk
+constexpr int kTableBitsMin = 12;      // 4096 slots: 36 KB of LDS per workgroup
+constexpr int kTableBitsMax = 14;      // 16384 slots: 144 KB of LDS per workgroup
+constexpr int kBitmapBits = 18;        // two 32 KB bitmaps (seen, repeated)
+constexpr uint32_t kShortRun = 32;     // repeated rows with at most this many occurrences are
+                                       // summed by one thread group
+constexpr uint32_t kPiece = 256;       // occurrences summed by one workgroup task
+constexpr int kSamplePos = 512;        // positives per sampler workgroup
 constexpr int kNegBlock = 8;           // negatives whose rows are in flight together
 constexpr int kMaxNeg = 64;
 constexpr int kMaxDim = 1024;
@@ -46,9 +54,27 @@ struct Control {
     uint32_t step_bad;               // this call's input is invalid: skip all writes
     uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
     uint32_t tickets[kMaxPasses];    // dynamic tile ids of the radix passes
-    uint32_t overflow;               // a bucket exceeded the in-LDS sort: run the later passes
-    uint32_t big_count;              // buckets queued for the large in-LDS sort
-    uint32_t pad[8];
+    uint32_t n_short;                // repeated rows summed by one thread group
+    uint32_t n_piece;                // pieces of up to kPiece occurrences summed by a workgroup
+    uint32_t n_comb;                 // rows whose pieces' partial sums are combined
+    uint32_t n_part;                 // partial sums allocated
+    uint32_t site;                   // first failed internal check (a kSite* code)
+    uint32_t pad[5];
+};
+
+// Internal checks (kBadInternal), recorded in Control::site.
+enum InternalSite : uint32_t {
+    kSiteRadixTicket = 1,
+    kSiteRadixWait = 2,
+    kSiteRadixDest = 3,
+    kSiteGroupBucket = 4,
+    kSiteGroupDepth = 5,
+    kSiteGroupLists = 6,
+    kSiteGroupLookup = 7,
+    kSiteGroupPlace = 8,
+    kSiteStepIds = 9,
+    kSiteAtomicIds = 10,
+    kSiteGroupBits = 11,
 };
 
 // Byte offsets of the workspace regions (all 256-byte aligned).
@@ -63,23 +89,26 @@ struct SlotLayout {
     size_t hist = 0;     // u32 [kMaxPasses][kMaxBins] global digit counts
     size_t neg = 0;      // i32 [max_batch * K]
     // sorted scatter
-    size_t keys0 = 0, keys1 = 0, vals0 = 0, vals1 = 0;  // u32 [M]
-    size_t info = 0;     // i32 [M]: -1, or the sorted position of an occurrence of a repeated row
+    size_t keys0 = 0;    // u32 [M] keys in occurrence order
+    size_t keys1 = 0;    // u32 [M] keys grouped by their lowest digit
+    size_t vals1 = 0;    // u32 [M] their occurrence indices
+    size_t info = 0;     // i32 [M]: -1, or the duplicate-buffer slot of an occurrence of a repeated row
     size_t status = 0;   // u64 [sort_tiles * kMaxBins] look-back words
-    size_t bstart = 0;   // u32 [kMaxBins] first sorted position of each bucket
-    size_t biglist = 0;  // u32 [kMaxBins] buckets for the large in-LDS sort
-    size_t work = 0;     // uint4 [M] duplicate pieces, kChunk slots per window
-    size_t wcount = 0;   // u32 [windows] pieces per window (| kHasLong if one is long)
-    size_t longhead = 0; // u32 [windows] start of a run continuing past the window
-    size_t wstats = 0;   // u32 [windows * 3] distinct S, distinct T, repeated occurrences
+    size_t bstart = 0;   // u32 [kMaxBins] first position of each bucket
+    size_t shorts = 0;   // uint4 [cap_short] {start, len, key, 0}
+    size_t pieces = 0;   // uint4 [cap_piece] {start, len, key, 0 or partial index + 1}
+    size_t combs = 0;    // uint4 [cap_comb] {key, first partial, partials, 0}
+    size_t wstats = 0;   // u32 [kMaxBins * 3] distinct S, distinct T, repeated occurrences
 };
 
+constexpr int kSlots = 3;  // groupings in flight: applied, next, and one more being sampled
+
 struct Layout {
-    SlotLayout slot[2];
+    SlotLayout slot[kSlots];
     size_t eval_ctrl = 0;  // Control of huge_eval_loss
     size_t lossp = 0;      // double [loss_blocks]
     // sorted scatter
-    size_t partA = 0, partB = 0;  // f64 [(M / kChunk + 2) * D] partial sums
+    size_t part = 0;     // f64 [cap_part * D] partial sums of the pieces of long runs
     size_t dup = 0;      // f32 [M * D] per-occurrence contributions of repeated rows
     // atomic scatter
     size_t gsrc = 0;     // f32 [max_batch * D] source-row gradients
@@ -87,23 +116,35 @@ struct Layout {
     size_t total = 0;
     int64_t max_occ = 0;       // M = max_batch * (2 + K)
     int64_t sort_tiles = 0;
-    int64_t windows = 0;
     int64_t loss_blocks = 0;
+    uint32_t cap_short = 0, cap_piece = 0, cap_comb = 0, cap_part = 0;
 };
 
-// Radix sort of keys below 2^key_bits: the fewest passes of at most
-// kMaxDigitBits bits, at one width per sort (at least kMinDigitBits).
+// List capacities for M occurrences.  A repeated row has >= 2 occurrences; a
+// piece is either a whole run of kShortRun+1 .. kPiece occurrences or one of
+// the ceil(len / kPiece) pieces of a longer run (fewer than len / (kPiece/2)
+// of them); a combined row has more than kPiece occurrences.
+struct ListCaps {
+    uint32_t shorts, pieces, combs, parts;
+};
+
+inline ListCaps list_caps(int64_t M) {
+    return {(uint32_t)(M / 2 + 2), (uint32_t)(M / (kShortRun + 1) + M / (kPiece / 2) + 2),
+            (uint32_t)(M / kPiece + 2), (uint32_t)(M / (kPiece / 2) + 2)};
+}
+
+// Bucketing of keys below 2^key_bits: one radix pass on the lowest digit, as
+// wide as the keys allow within kMinDigitBits..kMaxDigitBits; the grouping of
+// each bucket resolves the remaining key_bits - bits bits.
 struct SortPlan {
     int passes;
     int bits;
 };
 
 inline SortPlan sort_plan(int key_bits) {
-    if (key_bits < 1) key_bits = 1;
-    const int passes = (key_bits + kMaxDigitBits - 1) / kMaxDigitBits;
-    int bits = (key_bits + passes - 1) / passes;
+    int bits = key_bits < kMaxDigitBits ? key_bits : kMaxDigitBits;
     if (bits < kMinDigitBits) bits = kMinDigitBits;
-    return {passes, bits};
+    return {1, bits};
 }
 
 // Rows handled per workgroup: G lanes per row, C float4 per lane.
@@ -171,23 +212,23 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
                              uint32_t* keys_out, uint32_t* vals_out, int64_t m, int pass,
                              int bits, const uint32_t* hist, uint64_t* status, uint32_t tag,
                              const uint32_t* gate, uint32_t* bstart, hipStream_t s);
-hipError_t launch_bucket_sort(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
-                              uint32_t* keys_out, uint32_t* vals_out, int64_t m, int bits,
-                              int key_bits, const uint32_t* hist0, const uint32_t* bstart,
-                              uint32_t* biglist, hipStream_t s);
-hipError_t launch_mark(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
-                       int64_t N, int32_t* info, uint4* work, uint32_t* wcount,
-                       uint32_t* longhead, uint32_t* wstats, hipStream_t s);
+hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
+                        int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
+                        uint4* shorts, uint4* pieces, uint4* combs, ListCaps caps,
+                        uint32_t* wstats, int bins, int key_bits, int grid_cap,
+                        int table_bits, hipStream_t s);
+// Table bits for a grouping of m keys over `bins` buckets: the smallest table
+// whose 3/4 load holds a mean bucket of distinct keys.
+int group_table_bits(int64_t m, int bins);
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, const int32_t* info, float* dup,
                              double* lossp, int64_t* blocks_out, hipStream_t s);
-hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
-                            const uint32_t* wcount, const float* dup, double* partA,
-                            double* partB, float lr, int64_t m, hipStream_t s);
+hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* shorts,
+                            const uint4* pieces, const float* dup, double* part, float lr,
+                            ListCaps caps, hipStream_t s);
+hipError_t launch_combine(const TableArgs& t, Control* ctl, const uint4* combs,
+                          const double* part, float lr, ListCaps caps, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
-hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t* longhead,
-                               const uint32_t* keys, int64_t m, const double* partA,
-                               const double* partB, float lr, hipStream_t s);
 hipError_t launch_walks(const WalkArgs& A, uint32_t* counts, uint64_t* offsets, int64_t* total,
                         int64_t capacity, int32_t* src, int32_t* dst, int32_t* cc, int32_t* hist,
                         int32_t* status, hipStream_t s);

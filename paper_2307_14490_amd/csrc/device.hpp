@@ -122,4 +122,10 @@ __device__ __forceinline__ void raise_error(Control* ctl, uint32_t bit) {
     atomicCAS(&ctl->error, 0u, bit);
 }
 
+// A failed internal check: flags the call and records which check failed.
+__device__ __forceinline__ void raise_internal(Control* ctl, uint32_t site) {
+    raise_error(ctl, kBadInternal);
+    atomicCAS(&ctl->site, 0u, site);
+}
+
 }  // namespace huge

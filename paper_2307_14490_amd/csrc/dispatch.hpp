@@ -24,3 +24,31 @@
         default:                                     \
             return hipErrorInvalidValue;             \
     }
+
+// Negative rows in flight in the step kernels: the smallest supported block
+// that holds min(K, 8) rows.
+inline int neg_block(int K) {
+    const int want = K < 8 ? K : 8;
+    const int blocks[] = {2, 3, 4, 5, 6, 8};
+    for (int b : blocks)
+        if (b >= want) return b;
+    return 8;
+}
+
+#define HUGE_NEG_CASE(NN, ...)        \
+    case (NN): {                      \
+        constexpr int NB_ = (NN);     \
+        __VA_ARGS__;                  \
+    } break;
+
+#define HUGE_NEG_DISPATCH(nb, ...)           \
+    switch (nb) {                            \
+        HUGE_NEG_CASE(2, __VA_ARGS__)        \
+        HUGE_NEG_CASE(3, __VA_ARGS__)        \
+        HUGE_NEG_CASE(4, __VA_ARGS__)        \
+        HUGE_NEG_CASE(5, __VA_ARGS__)        \
+        HUGE_NEG_CASE(6, __VA_ARGS__)        \
+        HUGE_NEG_CASE(8, __VA_ARGS__)        \
+        default:                             \
+            return hipErrorInvalidValue;     \
+    }

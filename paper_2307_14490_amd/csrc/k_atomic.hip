@@ -111,7 +111,7 @@ __global__ __launch_bounds__(kBlock) void k_atomic_gather(TableArgs t, Control* 
                                                           coef, gsrc);
             if (lane == 0) loss = l;
         } else if (lane == 0) {
-            raise_error(ctl, kBadInternal);
+            raise_internal(ctl, kSiteAtomicIds);
         }
     }
     block_loss_a(loss, lossp);

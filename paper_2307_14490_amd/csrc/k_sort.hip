@@ -1,12 +1,22 @@
-// Grouping of the rows a batch touches: a stable LSD radix sort of the
-// occurrence keys (one kernel per digit of 8 to 10 bits, single pass over the
-// data with decoupled look-back between tiles), then run marking on the
-// sorted keys.
+// Grouping of the rows a batch touches (the de-duplication of HUGE Sec. 3.3.2):
+// which rows occur once -- those are updated in place by the step -- and, for
+// every row that occurs several times, the list of its occurrences in
+// occurrence order, which is the order in which its contributions are summed.
 //
 // Occurrence o = i (2 + K) + slot of positive i carries key N + src (slot 0,
-// source table) or the context row id (destination, negatives).  After the
-// sort, equal keys are adjacent and, the sort being stable, in occurrence
-// order: that is the order in which repeated rows sum their contributions.
+// source table) or the context row id (destination, negatives).
+//   1. k_radix_pass: one stable pass of an LSD radix sort on the lowest 8-10
+//      key bits (one kernel, single pass over the data with decoupled
+//      look-back between tiles) puts the occurrences of each bucket (digit)
+//      together, in occurrence order;
+//   2. k_group: one workgroup per bucket counts the bucket's keys in an LDS
+//      hash table, gives every repeated row a contiguous range of
+//      duplicate-buffer slots (inside the bucket's own range of positions),
+//      writes the slot of each of its occurrences, in occurrence order, to
+//      info[o], and lists the repeated rows for the duplicate kernels.
+// The radix pass uses 1024-thread workgroups and runs alone (it is issued just
+// before the previous batch's update); the grouping uses 256-thread
+// workgroups and runs beside that update.
 #include "common.hpp"
 #include "device.hpp"
 
@@ -111,7 +121,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     const uint32_t global_excl = digit_inclusive_sum<kBins>(hd, s_tmp[0]) - hd;  // synchronises
     const int64_t tile = s_tile;
     if (tile >= (int64_t)gridDim.x) {  // tickets were not reset: refuse, never wait
-        if (tid == 0) raise_error(ctl, kBadInternal);
+        if (tid == 0) raise_internal(ctl, kSiteRadixTicket);
         return;
     }
     if (bstart != nullptr && tile == 0 && digit_thread) bstart[d] = global_excl;
@@ -219,7 +229,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
                     // guards against a broken invariant, turning it into a
                     // reported error
                     if (++spins > (1u << 22)) {
-                        raise_error(ctl, kBadInternal);
+                        raise_internal(ctl, kSiteRadixWait);
                         break;
                     }
                     __builtin_amdgcn_s_sleep(1);
@@ -241,7 +251,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
             keys_out[dest] = k;
             vals_out[dest] = s_vals[p];
         } else {
-            raise_error(ctl, kBadInternal);
+            raise_internal(ctl, kSiteRadixDest);
         }
     }
 }
@@ -267,23 +277,10 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32
     return hipGetLastError();
 }
 
-// ---------------------------------------------------------------------------
-// Bucket stage: completion of the grouping inside the buckets of the first
-// pass.
-//
-// After the first radix pass (digit = the lowest `bits` key bits) the items
-// of bucket b (digit b) occupy positions [bstart[b], bstart[b] + hist0[b])
-// in occurrence order.  One workgroup takes one bucket and makes equal keys
-// adjacent, in occurrence order, writing the bucket to the output buffer
-// (the input buffer itself, or the other one): a small bucket by hashing its
-// keys in LDS (k_bucket_group), a larger one by a stable in-LDS LSD sort on
-// key bits [bits, key_bits) (k_bucket_sort_large).  A bucket too large for
-// both sets ctl->overflow, and the later global radix passes then sort the
-// whole array from the first pass's output.  Either way equal keys end up
-// adjacent and in occurrence order, which is all the run marking needs.
-// ---------------------------------------------------------------------------
-template <int THREADS>
-__device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t v, uint32_t* s_tmp) {
+// Exclusive sum of one value per thread over the workgroup (kBlock threads);
+// *total receives the sum.  Synchronises; s_tmp holds kBlock / 64 words and
+// may be reused after the next barrier.
+__device__ __forceinline__ uint32_t block_excl(uint32_t v, uint32_t* s_tmp, uint32_t* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     uint32_t incl = v;
 #pragma unroll
@@ -293,455 +290,481 @@ __device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t v, uint32_t* s_
     }
     if (lane == 63) s_tmp[wave] = incl;
     __syncthreads();
-    uint32_t add = 0;
-    for (int w = 0; w < wave; ++w) add += s_tmp[w];
+    uint32_t add = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kBlock / 64; ++w) {
+        const uint32_t x = s_tmp[w];
+        if (w < wave) add += x;
+        all += x;
+    }
+    *total = all;
     return add + incl - v;
 }
 
-// Sorts `size` (<= THREADS * ITEMS) items of one bucket; wave w holds items
-// [w * ITEMS * 64, (w + 1) * ITEMS * 64) in ITEMS rounds of 64 lanes.
-template <int THREADS, int ITEMS>
-__device__ __forceinline__ void bucket_sort_lds(const uint32_t* keys_in, const uint32_t* vals_in,
-                                                uint32_t* keys_out, uint32_t* vals_out,
-                                                int64_t start, int size, int lo, int rbits,
-                                                uint32_t* s_k, uint32_t* s_v,
-                                                uint32_t (*s_cnt)[kLocalBins], uint32_t* s_tmp) {
-    constexpr int kWaves = THREADS / 64;
-    constexpr int kWaveItems = ITEMS * 64;
-    constexpr int kDigitsPer = (kLocalBins + THREADS - 1) / THREADS;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    uint32_t key[ITEMS], val[ITEMS];
-#pragma unroll
-    for (int r = 0; r < ITEMS; ++r) {
-        const int e = wave * kWaveItems + r * 64 + lane;
-        key[r] = e < size ? keys_in[start + e] : 0u;
-        val[r] = e < size ? vals_in[start + e] : 0u;
+// Lanes of the wave whose `bits`-bit value equals this lane's, among the
+// lanes in `mask`.
+__device__ __forceinline__ uint64_t match_peers(uint32_t value, int bits, uint64_t mask) {
+    uint64_t peers = mask;
+    for (int b = 0; b < bits; ++b) {
+        const bool bit = (value >> b) & 1u;
+        const uint64_t ones = __ballot(bit);
+        peers &= bit ? ones : ~ones;
     }
-    const int npass = (rbits + kLocalMaxBits - 1) / kLocalMaxBits;
-    const int width = (rbits + npass - 1) / npass;
-    for (int q = 0; q < npass; ++q) {
-        const int shift = lo + q * width;
-        const int wq = (rbits - q * width) < width ? (rbits - q * width) : width;
-        const uint32_t mask = (1u << wq) - 1u;
-        const int bins = 1 << wq;
-        for (int j = tid; j < kWaves * kLocalBins; j += THREADS) (&s_cnt[0][0])[j] = 0u;
-        __syncthreads();
-        uint32_t rank[ITEMS];
-        {
-            uint32_t before[ITEMS], old[ITEMS];
-            int leader[ITEMS];
-#pragma unroll
-            for (int r = 0; r < ITEMS; ++r) {
-                const bool valid = wave * kWaveItems + r * 64 + lane < size;
-                const uint32_t dg = (key[r] >> shift) & mask;
-                uint64_t peers = __ballot(valid);
-                for (int b = 0; b < wq; ++b) {
-                    const bool bit = (dg >> b) & 1u;
-                    const uint64_t ones = __ballot(bit);
-                    peers &= bit ? ones : ~ones;
-                }
-                before[r] = (uint32_t)__popcll(peers & lt_mask);
-                const int ld = __ffsll((long long)peers) - 1;
-                leader[r] = ld < 0 ? 0 : ld;
-                old[r] = 0u;
-                if (valid && before[r] == 0)
-                    old[r] = atomicAdd(&s_cnt[wave][dg], (uint32_t)__popcll(peers));
-            }
-#pragma unroll
-            for (int r = 0; r < ITEMS; ++r) rank[r] = __shfl(old[r], leader[r], 64) + before[r];
-        }
-        __syncthreads();
-        // digit-major, wave-minor exclusive offsets
-        uint32_t tot[kDigitsPer];
-        uint32_t mine = 0;
-#pragma unroll
-        for (int j = 0; j < kDigitsPer; ++j) {
-            const int d = tid * kDigitsPer + j;
-            uint32_t t = 0;
-            if (d < bins)
-                for (int w = 0; w < kWaves; ++w) t += s_cnt[w][d];
-            tot[j] = t;
-            mine += t;
-        }
-        uint32_t run = block_exclusive_sum<THREADS>(mine, s_tmp);  // synchronises
-#pragma unroll
-        for (int j = 0; j < kDigitsPer; ++j) {
-            const int d = tid * kDigitsPer + j;
-            if (d < bins) {
-                for (int w = 0; w < kWaves; ++w) {
-                    const uint32_t c = s_cnt[w][d];
-                    s_cnt[w][d] = run;
-                    run += c;
-                }
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int r = 0; r < ITEMS; ++r) {
-            if (wave * kWaveItems + r * 64 + lane < size) {
-                const uint32_t p = s_cnt[wave][(key[r] >> shift) & mask] + rank[r];
-                s_k[p] = key[r];
-                s_v[p] = val[r];
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int r = 0; r < ITEMS; ++r) {
-            const int e = wave * kWaveItems + r * 64 + lane;
-            if (e < size) {
-                key[r] = s_k[e];
-                val[r] = s_v[e];
-            }
-        }
-        __syncthreads();  // s_cnt and s_tmp are reused by the next pass
-    }
-#pragma unroll
-    for (int r = 0; r < ITEMS; ++r) {
-        const int e = wave * kWaveItems + r * 64 + lane;
-        if (e < size) {
-            keys_out[start + e] = key[r];
-            vals_out[start + e] = val[r];
-        }
-    }
+    return peers;
 }
 
-constexpr int kBucketLargeThreads = 1024;
-constexpr int kBucketLargeItems = 12;   // up to 12288 items per bucket
-
 // ---------------------------------------------------------------------------
-// Grouping of one small bucket (at most kGroupCap items) without sorting it:
-// equal keys only have to be adjacent and in occurrence order.
-//   1. every item inserts its key into an LDS hash table (linear probing)
-//      and counts it there;
-//   2. items whose key occurs once keep their relative order and fill the
-//      front of the bucket (their position = their index minus the number of
-//      repeated items before them);
-//   3. the repeated items, listed in occurrence order, are placed by one
-//      wave: groups in the order of their first occurrence, each in
-//      occurrence order.
-// The result does not depend on where a key landed in the table.  Larger
-// buckets are queued for k_bucket_sort_large.
+// Grouping of one bucket (its items are in occurrence order).
+//
+// With BM (the bucket's keys differ in at most kBitmapBits bits above the
+// bucket digit), a first pass sets, per item, the key's bit in an LDS bitmap
+// and, where it was set already, the key's bit in a second bitmap of
+// repeated keys; it also counts the bucket's distinct source and destination
+// rows.  Only keys marked repeated take part in what follows.
+//
+// The (repeated) keys are counted in an LDS hash table of 2^TB slots (linear
+// probing).  A bucket with more than 3/4 of the slots in distinct keys is
+// split into key ranges by further hash bits, each range counted and placed
+// in turn (depth first over the binary tree of ranges); at depth 32 a range
+// holds one key value, so the split ends.  A count that overflows stops at
+// the first chunk that would load the table past 7/8, and the number of
+// distinct keys seen so far, scaled to the whole bucket, sets how many levels
+// the split descends at once (later sibling ranges start at that depth).
+// Per range:
+//   count:  every item of the range inserts its key and counts it;
+//   emit:   rows counted more than once get consecutive duplicate-buffer
+//           slots (positions of the bucket, after those of earlier ranges),
+//           and a work record: a short run, a piece, or
+//           pieces plus a combine record for a run longer than kPiece;
+//   place:  the repeated items, taken in occurrence order (chunk by chunk,
+//           compacted, then ranked by one wave 64 at a time), receive their
+//           row's next slot: info[o] = slot.
+// Where a row's range lands depends on the order of the hash insertions, the
+// order of its occurrences does not: every sum is taken in occurrence order.
+// Items that occur once keep info = -1 (set by the sampler).
 // ---------------------------------------------------------------------------
-constexpr int kGroupThreads = 256;
-constexpr int kGroupItems = 8;                              // item e = tid * 8 + r
-constexpr int kGroupCap = kGroupThreads * kGroupItems;      // 2048
-constexpr int kGroupSlotBits = 12;
-constexpr int kGroupSlots = 1 << kGroupSlotBits;            // twice the capacity
-constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;                 // keys are below 2N <= 2^32 - 2
+constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;   // keys are below 2N <= 2^32 - 2
+constexpr uint32_t kRepFlag = 0x80000000u;    // table count word: a repeated row, next slot
+constexpr int kMaxProbe = 512;                // a longer probe also splits the range
 
-// keys_in/vals_in may be the same buffers as keys_out/vals_out: every item
-// is read before the first write.
-__global__ __launch_bounds__(kGroupThreads) void k_bucket_group(
-    Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in, uint32_t* keys_out,
-    uint32_t* vals_out, int64_t m, int lo, const uint32_t* __restrict__ hist0,
-    const uint32_t* __restrict__ bstart, uint32_t* __restrict__ biglist) {
-    __shared__ uint32_t s_slot_key[kGroupSlots];     // table keys; later the group states
-    __shared__ uint32_t s_count[kGroupSlots / 2];    // two 16-bit counts per word
-    __shared__ uint32_t s_rep[kGroupCap];            // repeated items: slot << 16 | e
-    __shared__ uint16_t s_pos[kGroupCap];            // final position of repeated item e
-    __shared__ uint32_t s_tmp[kGroupThreads / 64];
-    if (ctl->step_bad) return;
-    const int b = blockIdx.x;
-    const uint32_t size = hist0[b];
-    if (size == 0u) return;
-    if (size > (uint32_t)kGroupCap) {
-        if (threadIdx.x == 0) biglist[atomicAdd(&ctl->big_count, 1u)] = (uint32_t)b;
-        return;
-    }
-    const int64_t start = bstart[b];
-    if (start + (int64_t)size > m) {
-        if (threadIdx.x == 0) raise_error(ctl, kBadInternal);
-        return;
-    }
+template <int TB>
+__device__ __forceinline__ uint32_t slot_hash(uint32_t key) {
+    return (key * 0x85EBCA6Bu) >> (32 - TB);
+}
+
+__device__ __forceinline__ bool in_range(uint32_t key, int level, uint32_t idx) {
+    return level == 0 || ((key * 0xC2B2AE35u) >> (32 - level)) == idx;
+}
+
+template <int TB, bool BM>
+__global__ __launch_bounds__(kBlock) void k_group(
+    Control* __restrict__ ctl, const uint32_t* __restrict__ keys,
+    const uint32_t* __restrict__ vals, int64_t m, int64_t N, const uint32_t* __restrict__ hist,
+    const uint32_t* __restrict__ bstart, int32_t* __restrict__ info, uint4* __restrict__ shorts,
+    uint4* __restrict__ pieces, uint4* __restrict__ combs, ListCaps caps,
+    uint32_t* __restrict__ wstats, int bins, int shift, int sub_bits) {
+    constexpr int kSlots = 1 << TB;
+    constexpr uint32_t kMax = (uint32_t)kSlots / 4u * 3u;    // distinct keys a range may hold
+    constexpr uint32_t kLoad = (uint32_t)kSlots / 8u * 7u;   // table load a count stays below
+    constexpr int kPer = kSlots / kBlock;                    // table slots per thread
+    constexpr int kBitWords = (1 << kBitmapBits) / 32;       // words of one bitmap
+    static_assert(!BM || 2 * kSlots <= kBitWords, "the table overlays the first bitmap");
+    // the table (key words, then count words); with BM it overlays the bitmap
+    // of keys seen, which the table no longer needs, and the bitmap of
+    // repeated keys follows
+    __shared__ uint32_t s_pool[BM ? 2 * kBitWords : 2 * kSlots];
+    uint32_t* const s_key = s_pool;
+    uint32_t* const s_cnt = s_pool + kSlots;  // count; after emit, kRepFlag | next slot
+    uint32_t* const s_seen = s_pool;
+    uint32_t* const s_dup = s_pool + (BM ? kBitWords : 0);
+    // repeated items of a chunk in order: their table slot, then their
+    // duplicate-buffer slot
+    __shared__ uint32_t s_rep[kGroupChunk];
+    __shared__ uint32_t s_tmp[6][kBlock / 64];
+    __shared__ uint32_t s_distinct, s_fail;
+    __shared__ uint32_t s_base[4];
+    __shared__ uint32_t s_stat[3];
+
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int n = (int)size;
-    for (int j = tid; j < kGroupSlots; j += kGroupThreads) s_slot_key[j] = kEmptyKey;
-    for (int j = tid; j < kGroupSlots / 2; j += kGroupThreads) s_count[j] = 0u;
+    for (int b = blockIdx.x; b < bins; b += gridDim.x) {
+    __syncthreads();  // LDS of the previous bucket
+    if (tid < 3) s_stat[tid] = 0u;
+    const uint32_t n = ctl->step_bad ? 0u : hist[b];
+    const int64_t s0 = n ? (int64_t)bstart[b] : 0;
+    if (n == 0u || s0 + (int64_t)n > m) {
+        if (n != 0u && tid == 0) raise_internal(ctl, kSiteGroupBucket);
+        if (tid < 3) wstats[b * 3 + tid] = 0u;
+        continue;
+    }
+    const bool single = n <= (uint32_t)kGroupChunk;
     uint32_t key[kGroupItems], val[kGroupItems], slot[kGroupItems];
-#pragma unroll
-    for (int r = 0; r < kGroupItems; ++r) {
-        const int e = tid * kGroupItems + r;
-        key[r] = e < n ? keys_in[start + e] : 0u;
-        val[r] = e < n ? vals_in[start + e] : 0u;
-    }
-    __syncthreads();
-    // 1. insert and count.  The table has more slots than the bucket has
-    //    items, so every probe sequence ends at the key or at an empty slot.
-#pragma unroll
-    for (int r = 0; r < kGroupItems; ++r) {
-        slot[r] = 0u;
-        if (tid * kGroupItems + r < n) {
-            uint32_t h = ((key[r] >> lo) * 0x9E3779B1u) >> (32 - kGroupSlotBits);
-            for (int probe = 0; probe < kGroupSlots; ++probe) {
-                const uint32_t old = atomicCAS(&s_slot_key[h], kEmptyKey, key[r]);
-                if (old == kEmptyKey || old == key[r]) break;
-                h = (h + 1u) & (uint32_t)(kGroupSlots - 1);
-            }
-            slot[r] = h;
-            atomicAdd(&s_count[h >> 1], 1u << ((h & 1u) * 16u));
-        }
-    }
-    __syncthreads();
-    // 2. repeated items before each item (block scan over threads); the
-    //    others are written now
-    uint32_t rep_mask = 0u, nrep = 0u;
-#pragma unroll
-    for (int r = 0; r < kGroupItems; ++r) {
-        if (tid * kGroupItems + r < n) {
-            const uint32_t c = (s_count[slot[r] >> 1] >> ((slot[r] & 1u) * 16u)) & 0xFFFFu;
-            if (c > 1u) {
-                rep_mask |= 1u << r;
-                ++nrep;
-            }
-        }
-    }
-    const uint32_t rep_before = block_exclusive_sum<kGroupThreads>(nrep, s_tmp);  // synchronises
-    uint32_t rep_total = 0;
-    for (int w = 0; w < kGroupThreads / 64; ++w) rep_total += s_tmp[w];
-    const uint32_t uniq_total = (uint32_t)n - rep_total;
-    {
-        uint32_t k = rep_before;
+    auto load_keys = [&](uint32_t c0) {
 #pragma unroll
         for (int r = 0; r < kGroupItems; ++r) {
-            const int e = tid * kGroupItems + r;
-            if (e < n) {
-                if (rep_mask & (1u << r)) {
-                    s_rep[k++] = (slot[r] << 16) | (uint32_t)e;
+            const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
+            key[r] = e < n ? keys[s0 + e] : 0u;
+        }
+    };
+    auto load_chunk = [&](uint32_t c0) {
+        load_keys(c0);
+#pragma unroll
+        for (int r = 0; r < kGroupItems; ++r) {
+            const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
+            val[r] = e < n ? vals[s0 + e] : 0u;
+        }
+    };
+    if (single) load_chunk(0u);
+
+    // ---- repeated keys (BM) ----
+    // the bit of key k is bit (k >> shift) of the bucket's bitmap; a key
+    // beyond the bitmap cannot occur (sub_bits <= kBitmapBits)
+    const uint32_t bit_words = sub_bits > 5 ? 1u << (sub_bits - 5) : 1u;
+    auto repeated = [&](uint32_t k) -> bool {
+        if (!BM) return true;
+        const uint32_t sub = k >> shift;
+        return sub >> 5 < bit_words && ((s_dup[sub >> 5] >> (sub & 31u)) & 1u);
+    };
+    if (BM) {
+        for (uint32_t j = tid; j < bit_words; j += kBlock) {
+            s_seen[j] = 0u;
+            s_dup[j] = 0u;
+        }
+        __syncthreads();
+        uint32_t nS = 0, nT = 0;
+        for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
+            if (!single) load_keys(c0);
+#pragma unroll
+            for (int r = 0; r < kGroupItems; ++r) {
+                const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
+                if (e >= n) continue;
+                const uint32_t sub = key[r] >> shift, w = sub >> 5, bit = 1u << (sub & 31u);
+                if (w >= bit_words) {
+                    raise_internal(ctl, kSiteGroupBits);
+                    continue;
+                }
+                const uint32_t old = atomicOr(&s_seen[w], bit);
+                if (old & bit) {
+                    atomicOr(&s_dup[w], bit);
+                } else if ((int64_t)key[r] >= N) {
+                    ++nS;
                 } else {
-                    const int64_t dst = start + (int64_t)((uint32_t)e - k);
-                    keys_out[dst] = key[r];
-                    vals_out[dst] = val[r];
+                    ++nT;
                 }
             }
         }
+        if (nS) atomicAdd(&s_stat[0], nS);
+        if (nT) atomicAdd(&s_stat[1], nT);
+        __syncthreads();
     }
-    __syncthreads();  // every item has read its count; the table keys are no longer needed
-    for (int j = tid; j < kGroupSlots; j += kGroupThreads) s_slot_key[j] = kEmptyKey;
-    __syncthreads();
-    // 3. one wave places the repeated items; s_slot_key[slot] becomes the
-    //    group state (first position << 16 | items placed so far)
-    if (wave == 0 && rep_total > 0u) {
-        const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-        uint32_t gsum = 0u;  // items of the groups started so far
-        for (uint32_t j0 = 0; j0 < rep_total; j0 += 64) {
-            const uint32_t j = j0 + (uint32_t)lane;
-            const bool act = j < rep_total;
-            const uint32_t ent = act ? s_rep[j] : 0u;
-            const uint32_t sl = ent >> 16, e = ent & 0xFFFFu;
-            uint64_t peers = __ballot(act);
-#pragma unroll
-            for (int bt = 0; bt < kGroupSlotBits; ++bt) {
-                const bool bit = (sl >> bt) & 1u;
-                const uint64_t ones = __ballot(bit);
-                peers &= bit ? ones : ~ones;
-            }
-            const uint32_t before = (uint32_t)__popcll(peers & lt_mask);
-            const int ld = __ffsll((long long)peers) - 1;
-            const int leader = ld < 0 ? 0 : ld;
-            const bool is_leader = act && before == 0u;
-            const uint32_t st = is_leader ? s_slot_key[sl] : 0u;
-            const bool starts = is_leader && st == kEmptyKey;
-            const uint32_t c = starts ? (s_count[sl >> 1] >> ((sl & 1u) * 16u)) & 0xFFFFu : 0u;
-            uint32_t incl = c;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const uint32_t t = __shfl_up(incl, off, 64);
-                if (lane >= off) incl += t;
-            }
-            uint32_t base = starts ? gsum + incl - c : (st >> 16);
-            uint32_t placed = starts ? 0u : (st & 0xFFFFu);
-            if (is_leader) s_slot_key[sl] = (base << 16) | (placed + (uint32_t)__popcll(peers));
-            base = __shfl(base, leader, 64);
-            placed = __shfl(placed, leader, 64);
-            if (act) s_pos[e] = (uint16_t)(uniq_total + base + placed + before);
-            gsum += __shfl(incl, 63, 64);
-        }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kGroupItems; ++r) {
-        if (rep_mask & (1u << r)) {
-            const int e = tid * kGroupItems + r;
-            const uint32_t pos = s_pos[e];
-            if (pos >= uniq_total && pos < (uint32_t)n) {
-                keys_out[start + (int64_t)pos] = key[r];
-                vals_out[start + (int64_t)pos] = val[r];
-            } else {
-                raise_error(ctl, kBadInternal);
-            }
-        }
-    }
-}
 
-// Buckets queued by the small kernel; a fixed grid walks the queue.
-__global__ __launch_bounds__(kBucketLargeThreads) void k_bucket_sort_large(
-    Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in, uint32_t* keys_out,
-    uint32_t* vals_out, int64_t m, int lo, int rbits, const uint32_t* __restrict__ hist0,
-    const uint32_t* __restrict__ bstart, const uint32_t* __restrict__ biglist, int bins) {
-    constexpr int kCap = kBucketLargeThreads * kBucketLargeItems;
-    __shared__ uint32_t s_k[kCap], s_v[kCap];
-    __shared__ uint32_t s_cnt[kBucketLargeThreads / 64][kLocalBins];
-    __shared__ uint32_t s_tmp[kBucketLargeThreads / 64];
-    if (ctl->step_bad) return;
-    const uint32_t count = ctl->big_count;
-    for (uint32_t q = blockIdx.x; q < count && q < (uint32_t)bins; q += gridDim.x) {
-        const uint32_t b = biglist[q];
-        if (b >= (uint32_t)bins) {
-            if (threadIdx.x == 0) raise_error(ctl, kBadInternal);
-            return;
+    uint32_t rep_base = 0;  // slots handed out to earlier ranges
+    int level = 0, depth = 0;  // depth: where the next sibling range starts
+    uint32_t ridx = 0;
+    while (true) {
+        // ---- count ----
+        for (int j = tid; j < kSlots; j += kBlock) {
+            s_key[j] = kEmptyKey;
+            s_cnt[j] = 0u;
         }
-        const uint32_t size = hist0[b];
-        if (size > (uint32_t)kCap) {  // the later global passes sort everything
-            if (threadIdx.x == 0) atomicOr(&ctl->overflow, 1u);
+        if (tid == 0) {
+            s_distinct = 0u;
+            s_fail = 0u;
+        }
+        __syncthreads();
+        uint32_t seen = 0;  // items the count went through
+        bool over = false;
+        for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
+            const uint32_t len = n - c0 < (uint32_t)kGroupChunk ? n - c0 : (uint32_t)kGroupChunk;
+            if (s_distinct + len > kLoad) {  // uniform: the table could fill up
+                over = true;
+                break;
+            }
+            if (!single) load_chunk(c0);
+            // the items of a thread probe together: one compare-and-swap per
+            // pending item and step, all issued before any result is used;
+            // the counting atomics come after the probe loop
+            uint32_t h[kGroupItems], pend = 0u, fresh = 0u;
+#pragma unroll
+            for (int r = 0; r < kGroupItems; ++r) {
+                const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
+                h[r] = slot_hash<TB>(key[r]);
+                if (e < n && in_range(key[r], level, ridx) && repeated(key[r])) pend |= 1u << r;
+            }
+            uint32_t found = 0u;
+            for (int probe = 0; pend != 0u && probe < kMaxProbe; ++probe) {
+                uint32_t old[kGroupItems];
+#pragma unroll
+                for (int r = 0; r < kGroupItems; ++r)
+                    old[r] = (pend >> r) & 1u ? atomicCAS(&s_key[h[r]], kEmptyKey, key[r])
+                                              : key[r];
+#pragma unroll
+                for (int r = 0; r < kGroupItems; ++r) {
+                    if (!((pend >> r) & 1u)) continue;
+                    if (old[r] == kEmptyKey || old[r] == key[r]) {
+                        fresh += old[r] == kEmptyKey ? 1u : 0u;
+                        found |= 1u << r;
+                    } else {
+                        h[r] = (h[r] + 1u) & (uint32_t)(kSlots - 1);
+                    }
+                }
+                pend &= ~found;
+            }
+            if (pend != 0u) s_fail = 1u;
+#pragma unroll
+            for (int r = 0; r < kGroupItems; ++r) {
+                slot[r] = (found >> r) & 1u ? h[r] : kEmptyKey;
+                if ((found >> r) & 1u) atomicAdd(&s_cnt[h[r]], 1u);
+            }
+            if (fresh) atomicAdd(&s_distinct, fresh);
+            __syncthreads();
+            seen = c0 + len;
+            if (s_fail || s_distinct > kMax) {  // uniform
+                over = true;
+                break;
+            }
+        }
+        if (over) {
+            // split the range; its first part next (uniform)
+            int add = 1;
+            if (!s_fail && seen > 0u) {
+                const uint64_t est = (uint64_t)s_distinct * n / seen;
+                while (add < 8 && est > ((uint64_t)kMax << add) / 4u * 3u) ++add;
+            }
+            __syncthreads();
+            if (level >= 32) {  // cannot happen: a depth-32 range holds one key value
+                if (tid == 0) raise_internal(ctl, kSiteGroupDepth);
+                return;
+            }
+            if (add > 32 - level) add = 32 - level;
+            level += add;
+            ridx <<= add;
+            if (depth < level) depth = level;
             continue;
         }
-        const int64_t start = bstart[b];
-        if (start + (int64_t)size > m) {
-            if (threadIdx.x == 0) raise_error(ctl, kBadInternal);
+
+        // ---- emit ----
+        // this thread's table slots (tid, tid + kBlock, ...; conflict-free
+        // LDS reads): statistics, slot counts, record counts; slots and
+        // records are handed out thread by thread
+        uint32_t nS = 0, nT = 0, nrep = 0, nshort = 0, npiece = 0, ncomb = 0, npart = 0;
+#pragma unroll 8
+        for (int j = 0; j < kPer; ++j) {
+            const int q = j * kBlock + tid;
+            const uint32_t k = s_key[q];
+            if (k == kEmptyKey) continue;
+            if (!BM) {  // with BM the first pass counted the rows
+                if ((int64_t)k >= N) ++nS; else ++nT;
+            }
+            const uint32_t c = s_cnt[q];
+            if (c > 1u) {
+                nrep += c;
+                if (c <= kShortRun) {
+                    ++nshort;
+                } else if (c <= kPiece) {
+                    ++npiece;
+                } else {
+                    const uint32_t np = (c + kPiece - 1) / kPiece;
+                    npiece += np;
+                    npart += np;
+                    ++ncomb;
+                }
+            }
+        }
+        uint32_t t_rep, t_short, t_piece, t_comb, t_part;
+        uint32_t x_rep = block_excl(nrep, s_tmp[0], &t_rep);
+        uint32_t x_short = block_excl(nshort, s_tmp[1], &t_short);
+        uint32_t x_piece = block_excl(npiece, s_tmp[2], &t_piece);
+        uint32_t x_comb = block_excl(ncomb, s_tmp[3], &t_comb);
+        uint32_t x_part = block_excl(npart, s_tmp[4], &t_part);
+        if (tid == 0) {
+            s_base[0] = t_short ? atomicAdd(&ctl->n_short, t_short) : 0u;
+            s_base[1] = t_piece ? atomicAdd(&ctl->n_piece, t_piece) : 0u;
+            s_base[2] = t_comb ? atomicAdd(&ctl->n_comb, t_comb) : 0u;
+            s_base[3] = t_part ? atomicAdd(&ctl->n_part, t_part) : 0u;
+        }
+        if (nS) atomicAdd(&s_stat[0], nS);
+        if (nT) atomicAdd(&s_stat[1], nT);
+        __syncthreads();
+        const bool fits = (uint64_t)s_base[0] + t_short <= caps.shorts &&
+                          (uint64_t)s_base[1] + t_piece <= caps.pieces &&
+                          (uint64_t)s_base[2] + t_comb <= caps.combs &&
+                          (uint64_t)s_base[3] + t_part <= caps.parts &&
+                          (uint64_t)rep_base + t_rep <= n;
+        if (!fits) {  // cannot happen: the capacities bound every batch
+            if (tid == 0) raise_internal(ctl, kSiteGroupLists);
             return;
         }
-        bucket_sort_lds<kBucketLargeThreads, kBucketLargeItems>(
-            keys_in, vals_in, keys_out, vals_out, start, (int)size, lo, rbits, s_k, s_v, s_cnt,
-            s_tmp);
-        __syncthreads();  // LDS is reused by the next bucket
-    }
-}
-
-hipError_t launch_bucket_sort(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
-                              uint32_t* keys_out, uint32_t* vals_out, int64_t m, int bits,
-                              int key_bits, const uint32_t* hist0, const uint32_t* bstart,
-                              uint32_t* biglist, hipStream_t s) {
-    const int rbits = key_bits - bits;
-    if (m == 0 || rbits <= 0) return hipSuccess;
-    if (bits < 1 || bits > kMaxDigitBits || rbits > 32 - bits) return hipErrorInvalidValue;
-    const int bins = 1 << bits;
-    hipLaunchKernelGGL(k_bucket_group, dim3((unsigned)bins), dim3(kGroupThreads), 0, s, ctl,
-                       keys_in, vals_in, keys_out, vals_out, m, bits, hist0, bstart, biglist);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int grid = bins < 256 ? bins : 256;
-    hipLaunchKernelGGL(k_bucket_sort_large, dim3((unsigned)grid), dim3(kBucketLargeThreads), 0, s,
-                       ctl, keys_in, vals_in, keys_out, vals_out, m, bits, rbits, hist0, bstart,
-                       biglist, bins);
-    return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Run marking on the sorted keys, one workgroup per window of kChunk sorted
-// positions.  Position j (occurrence o = vals[j]):
-//   if its key occurs more than once, info[o] = j (its slot in the duplicate
-//   buffer); the sampler has set every entry of the batch to -1.  Runs of a repeated key are cut into pieces at window
-//   boundaries; each piece becomes a work item {start, len, key, kind} stored
-//   in its window's slots work[w * kChunk ..]:
-//     kind 0: the whole run -> sum and update the row directly;
-//     kind 1: the run's first piece, the run continues past the window ->
-//             partial sum to partB[w]; longhead[w] = its start;
-//     kind 2: a later piece, starting at the window boundary -> partA[w].
-//   A window holds at most one kind-1 piece.  Per window: number of pieces
-//   (with kHasLong set if one is longer than kLongPiece), and {distinct
-//   source keys, distinct context keys, repeated occurrences}.
-// Everything is written without global atomics.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_mark(const Control* __restrict__ ctl,
-                                                 const uint32_t* __restrict__ keys,
-                                                 const uint32_t* __restrict__ vals, int64_t m,
-                                                 int64_t N, int32_t* __restrict__ info,
-                                                 uint4* __restrict__ work,
-                                                 uint32_t* __restrict__ wcount,
-                                                 uint32_t* __restrict__ longhead,
-                                                 uint32_t* __restrict__ wstats) {
-    static_assert(kChunk == kBlock, "one workgroup per window");
-    __shared__ uint32_t s_cnt[3];
-    __shared__ uint32_t s_wave_emit[kBlock / 64];
-    __shared__ uint32_t s_long;
-    __shared__ uint32_t s_long_piece;
-    const int64_t win = blockIdx.x;
-    if (ctl->step_bad) {  // unsorted keys: no pieces, nothing marked
-        if (threadIdx.x == 0) {
-            wcount[win] = 0u;
-            longhead[win] = kNoHead;
-            wstats[win * 3 + 0] = wstats[win * 3 + 1] = wstats[win * 3 + 2] = 0u;
+        {
+            uint32_t pos = (uint32_t)s0 + rep_base + x_rep;
+            uint32_t is = s_base[0] + x_short, ip = s_base[1] + x_piece;
+            uint32_t ic = s_base[2] + x_comb, ia = s_base[3] + x_part;
+#pragma unroll 4
+            for (int j = 0; j < kPer; ++j) {
+                const int q = j * kBlock + tid;
+                const uint32_t k = s_key[q];
+                const uint32_t c = s_cnt[q];
+                if (k == kEmptyKey || c <= 1u) continue;
+                if (c <= kShortRun) {
+                    shorts[is++] = make_uint4(pos, c, k, 0u);
+                } else if (c <= kPiece) {
+                    pieces[ip++] = make_uint4(pos, c, k, 0u);
+                } else {
+                    const uint32_t np = (c + kPiece - 1) / kPiece;
+                    for (uint32_t z = 0; z < np; ++z) {
+                        const uint32_t len = (c - z * kPiece) < kPiece ? (c - z * kPiece) : kPiece;
+                        pieces[ip++] = make_uint4(pos + z * kPiece, len, k, ia + z + 1u);
+                    }
+                    combs[ic++] = make_uint4(k, ia, np, 0u);
+                    ia += np;
+                }
+                s_cnt[q] = kRepFlag | pos;
+                pos += c;
+            }
         }
-        return;
+        if (tid == 0) s_stat[2] += t_rep;
+        __syncthreads();
+
+        // ---- place ----
+        if (t_rep > 0u) {
+            for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
+                if (!single) {
+                    load_chunk(c0);
+                    // lookups of the chunk's items, issued together as in the count
+                    uint32_t h[kGroupItems], pend = 0u, found = 0u;
+#pragma unroll
+                    for (int r = 0; r < kGroupItems; ++r) {
+                        const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
+                        h[r] = slot_hash<TB>(key[r]);
+                        if (e < n && in_range(key[r], level, ridx) && repeated(key[r]))
+                            pend |= 1u << r;
+                    }
+                    for (int probe = 0; pend != 0u && probe < kMaxProbe; ++probe) {
+                        uint32_t cur[kGroupItems];
+#pragma unroll
+                        for (int r = 0; r < kGroupItems; ++r)
+                            cur[r] = (pend >> r) & 1u ? s_key[h[r]] : key[r];
+#pragma unroll
+                        for (int r = 0; r < kGroupItems; ++r) {
+                            if (!((pend >> r) & 1u)) continue;
+                            if (cur[r] == key[r])
+                                found |= 1u << r;
+                            else
+                                h[r] = (h[r] + 1u) & (uint32_t)(kSlots - 1);
+                        }
+                        pend &= ~found;
+                    }
+                    if (pend != 0u) raise_internal(ctl, kSiteGroupLookup);
+#pragma unroll
+                    for (int r = 0; r < kGroupItems; ++r)
+                        slot[r] = (found >> r) & 1u ? h[r] : kEmptyKey;
+                }
+                uint32_t mask = 0u, cnt = 0u;
+#pragma unroll
+                for (int r = 0; r < kGroupItems; ++r) {
+                    if (slot[r] != kEmptyKey && (s_cnt[slot[r]] & kRepFlag)) {
+                        mask |= 1u << r;
+                        ++cnt;
+                    }
+                }
+                uint32_t chunk_rep;
+                const uint32_t k0 = block_excl(cnt, s_tmp[5], &chunk_rep);  // synchronises
+                {
+                    uint32_t k = k0;
+#pragma unroll
+                    for (int r = 0; r < kGroupItems; ++r)
+                        if (mask & (1u << r)) s_rep[k++] = slot[r];
+                }
+                __syncthreads();
+                if (wave == 0) {
+                    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+                    for (uint32_t j0 = 0; j0 < chunk_rep; j0 += 64) {
+                        const uint32_t j = j0 + (uint32_t)lane;
+                        const bool act = j < chunk_rep;
+                        const uint32_t sl = act ? s_rep[j] : 0u;
+                        const uint64_t peers = match_peers(sl, TB, __ballot(act));
+                        const uint32_t before = (uint32_t)__popcll(peers & lt_mask);
+                        const int ld = __ffsll((long long)peers) - 1;
+                        const int leader = ld < 0 ? 0 : ld;
+                        uint32_t st = 0u;
+                        if (act && before == 0u) {
+                            st = s_cnt[sl];
+                            s_cnt[sl] = st + (uint32_t)__popcll(peers);
+                        }
+                        st = __shfl(st, leader, 64);
+                        if (act) s_rep[j] = (st & ~kRepFlag) + before;
+                    }
+                }
+                __syncthreads();
+                uint32_t k = k0;
+#pragma unroll
+                for (int r = 0; r < kGroupItems; ++r) {
+                    if (mask & (1u << r)) {
+                        const uint32_t pos = s_rep[k++];
+                        if ((int64_t)pos >= s0 && (int64_t)pos < s0 + (int64_t)n &&
+                            (int64_t)val[r] < m)
+                            info[val[r]] = (int32_t)pos;
+                        else
+                            raise_internal(ctl, kSiteGroupPlace);
+                    }
+                }
+                __syncthreads();  // s_rep is reused by the next chunk
+            }
+        }
+        rep_base += t_rep;
+
+        // ---- next range, depth first ----
+        while (level > 0 && (ridx & 1u)) {
+            --level;
+            ridx >>= 1;
+        }
+        if (level == 0) break;
+        ridx += 1u;
+        if (level < depth) {  // the sibling is split as far as this one was
+            ridx <<= (depth - level);
+            level = depth;
+        }
+        __syncthreads();  // the table is cleared for the next range
     }
-    __shared__ uint32_t s_key[kChunk + 2];  // keys j-1 .. window end (inclusive of one past)
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    if (tid < 3) s_cnt[tid] = 0u;
-    if (tid == 0) {
-        s_long = 0xFFFFFFFFu;
-        s_long_piece = 0u;
-    }
-    const int64_t j = win * kChunk + tid;
-    // s_key[1 + t] = keys[win * kChunk + t]; s_key[0] = the key before the
-    // window, s_key[kChunk + 1] = the key after it (a sentinel if none: it is
-    // only compared under an index check)
-    s_key[1 + tid] = j < m ? keys[j] : 0u;
-    if (tid == 0) s_key[0] = j > 0 ? keys[j - 1] : 0u;
-    if (tid == 1) s_key[kChunk + 1] = win * kChunk + kChunk < m ? keys[win * kChunk + kChunk] : 0u;
     __syncthreads();
-    bool emit = false, head_S = false, head_T = false, dup = false;
-    uint4 rec = make_uint4(0, 0, 0, 0);
-    if (j < m) {
-        const uint32_t key = s_key[1 + tid];
-        const bool prev_same = j > 0 && s_key[tid] == key;
-        const bool next_same = j + 1 < m && s_key[2 + tid] == key;
-        dup = prev_same || next_same;
-        if (dup) {
-            const uint32_t o = vals[j];
-            if ((int64_t)o < m) info[o] = (int32_t)j;
-        }
-        head_S = !prev_same && (int64_t)key >= N;
-        head_T = !prev_same && (int64_t)key < N;
-        if (dup && (!prev_same || tid == 0)) {
-            const int64_t win_end = (win + 1) * kChunk;
-            const int64_t lim = win_end < m ? win_end : m;
-            int64_t e = j + 1;
-            while (e < lim && s_key[1 + (e - win * kChunk)] == key) ++e;
-            const bool cont_after = (e == win_end) && (e < m) && s_key[kChunk + 1] == key;
-            const uint32_t kind = !prev_same ? (cont_after ? 1u : 0u) : 2u;
-            rec = make_uint4((uint32_t)j, (uint32_t)(e - j), key, kind);
-            emit = true;
-            if (kind == 1u) s_long = (uint32_t)j;
-        }
-    }
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const uint64_t em = __ballot(emit);
-    const uint64_t lg = __ballot(emit && rec.y > kLongPiece);
-    if (lane == 0 && lg) s_long_piece = 1u;
-    const uint64_t bs = __ballot(head_S);
-    const uint64_t bt = __ballot(head_T);
-    const uint64_t bd = __ballot(dup);
-    if (lane == 0) {
-        s_wave_emit[wave] = (uint32_t)__popcll(em);
-        atomicAdd(&s_cnt[0], (uint32_t)__popcll(bs));
-        atomicAdd(&s_cnt[1], (uint32_t)__popcll(bt));
-        atomicAdd(&s_cnt[2], (uint32_t)__popcll(bd));
-    }
-    __syncthreads();
-    uint32_t base = 0;
-    for (int w = 0; w < wave; ++w) base += s_wave_emit[w];
-    if (emit) work[win * kChunk + base + __popcll(em & lt)] = rec;
-    if (tid == 0) {
-        uint32_t total = 0;
-        for (int w = 0; w < kBlock / 64; ++w) total += s_wave_emit[w];
-        wcount[win] = total | (s_long_piece ? kHasLong : 0u);
-        longhead[win] = s_long;
-        wstats[win * 3 + 0] = s_cnt[0];
-        wstats[win * 3 + 1] = s_cnt[1];
-        wstats[win * 3 + 2] = s_cnt[2];
+    if (tid < 3) wstats[b * 3 + tid] = s_stat[tid];
     }
 }
 
-hipError_t launch_mark(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
-                       int64_t N, int32_t* info, uint4* work, uint32_t* wcount,
-                       uint32_t* longhead, uint32_t* wstats, hipStream_t s) {
-    const int64_t blocks = (m + kChunk - 1) / kChunk;
-    if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_mark, dim3((unsigned)blocks), dim3(kBlock), 0, s, ctl, keys, vals, m, N,
-                       info, work, wcount, longhead, wstats);
+int group_table_bits(int64_t m, int bins) {
+    const int64_t mean = bins > 0 ? (m + bins - 1) / bins : m;
+    int tb = kTableBitsMin;
+    while (tb < kTableBitsMax && mean > ((int64_t)1 << tb) / 4 * 3) ++tb;
+    return tb;
+}
+
+hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
+                        int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
+                        uint4* shorts, uint4* pieces, uint4* combs, ListCaps caps,
+                        uint32_t* wstats, int bins, int key_bits, int grid_cap,
+                        int table_bits, hipStream_t s) {
+    if (m == 0) return hipSuccess;
+    if (bins < 2 || bins > kMaxBins || (bins & (bins - 1)) != 0) return hipErrorInvalidValue;
+    const int shift = __builtin_ctz((unsigned)bins);
+    const int sub_bits = key_bits > shift ? key_bits - shift : 0;
+    // the bitmap path unless a table size is asked for
+    const bool bm = table_bits == 0 && sub_bits <= kBitmapBits;
+    if (table_bits == 0) table_bits = bm ? kTableBitsMin : group_table_bits(m, bins);
+    const int grid = grid_cap > 0 && grid_cap < bins ? grid_cap : bins;
+#define HUGE_GROUP_LAUNCH(TB, BM)                                                             \
+    hipLaunchKernelGGL((k_group<TB, BM>), dim3((unsigned)grid), dim3(kBlock), 0, s, ctl, keys, \
+                       vals, m, N, hist, bstart, info, shorts, pieces, combs, caps, wstats,    \
+                       bins, shift, sub_bits)
+    if (bm) {
+        HUGE_GROUP_LAUNCH(kTableBitsMin, true);
+    } else {
+        switch (table_bits) {
+            case 12: HUGE_GROUP_LAUNCH(12, false); break;
+            case 13: HUGE_GROUP_LAUNCH(13, false); break;
+            case 14: HUGE_GROUP_LAUNCH(14, false); break;
+            default: return hipErrorInvalidValue;
+        }
+    }
+#undef HUGE_GROUP_LAUNCH
     return hipGetLastError();
 }
 

@@ -5,9 +5,9 @@
 // Rows that occur once in the batch are rewritten in place by the thread
 // group that read them -- no other group reads them.  A row that occurs
 // several times is left untouched here: each occurrence stores its
-// contribution at its sorted position, and the duplicate kernels sum them in
-// occurrence order and update the row once, so every read sees pre-step
-// values.
+// contribution in the slot the grouping gave it (a row's slots are
+// consecutive, in occurrence order), and the duplicate kernels sum them in
+// that order and update the row once, so every read sees pre-step values.
 #include "common.hpp"
 #include "device.hpp"
 #include "dispatch.hpp"
@@ -30,7 +30,10 @@ __device__ __forceinline__ void block_loss(float loss, double* __restrict__ out)
     }
 }
 
-template <int G, int C>
+// NB negative rows are in flight at a time (NB = K up to 8, rounded up to
+// a supported block): the block holds NB rows of registers, so a smaller one
+// raises the occupancy, which the kernel needs to hide its memory latency.
+template <int G, int C, int NB>
 __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __restrict__ ctl,
                                                        StepArgs a, const int32_t* __restrict__ neg,
                                                        const int32_t* __restrict__ info,
@@ -55,11 +58,11 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     // instead of read out of bounds.
     bool active = i < a.n;
     int32_t u = 0, v = 0, cnt_i = 0, info_s = -1, info_d = -1;
-    int32_t mk[kNegBlock], ik[kNegBlock];
+    int32_t mk[NB], ik[NB];
     const int64_t o = i * (int64_t)(2 + K);
     const int32_t* negi = neg + i * (int64_t)K;
     const int32_t* infok = info + o + 2;
-    int cnt = K < kNegBlock ? K : kNegBlock;
+    int cnt = K < NB ? K : NB;
     if (active) {
         u = a.src[i];
         v = a.dst[i];
@@ -67,25 +70,25 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
         info_s = info[o];
         info_d = info[o + 1];
 #pragma unroll
-        for (int j = 0; j < kNegBlock; ++j) {
+        for (int j = 0; j < NB; ++j) {
             if (j < cnt) {
                 mk[j] = negi[j];
                 ik[j] = infok[j];
             }
         }
         if (u < 0 || (int64_t)u >= t.N || v < 0 || (int64_t)v >= t.N) {
-            if (lane == 0) raise_error(ctl, kBadInternal);
+            if (lane == 0) raise_internal(ctl, kSiteStepIds);
             active = false;
         }
     }
     if (active) {
         const float c = (float)cnt_i;
         float4 s[C], t0[C], dS[C];
-        float4 tk[kNegBlock][C];
+        float4 tk[NB][C];
         IO::load(s, S, u, D, lane);
         IO::load(t0, T, v, D, lane);
 #pragma unroll
-        for (int j = 0; j < kNegBlock; ++j)
+        for (int j = 0; j < NB; ++j)
             if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
 
         // positive pair
@@ -106,19 +109,19 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
             IO::store(dup, info_d, D, lane, cv);
         }
 
-        // negatives, kNegBlock rows in flight at a time
+        // negatives, NB rows in flight at a time
         int kb = 0;
         while (true) {
-            float y[kNegBlock];
+            float y[NB];
 #pragma unroll
-            for (int j = 0; j < kNegBlock; ++j) y[j] = (j < cnt) ? IO::dot(s, tk[j]) : 0.f;
+            for (int j = 0; j < NB; ++j) y[j] = (j < cnt) ? IO::dot(s, tk[j]) : 0.f;
 #pragma unroll
             for (int off = G / 2; off > 0; off >>= 1) {
 #pragma unroll
-                for (int j = 0; j < kNegBlock; ++j) y[j] += __shfl_xor(y[j], off, 64);
+                for (int j = 0; j < NB; ++j) y[j] += __shfl_xor(y[j], off, 64);
             }
 #pragma unroll
-            for (int j = 0; j < kNegBlock; ++j) {
+            for (int j = 0; j < NB; ++j) {
                 if (j < cnt) {
                     const float h = coef_neg(c, y[j]);
                     lsum += softplus_f(y[j]);
@@ -137,18 +140,18 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
                     }
                 }
             }
-            kb += kNegBlock;
+            kb += NB;
             if (kb >= K) break;
-            cnt = (K - kb) < kNegBlock ? (K - kb) : kNegBlock;
+            cnt = (K - kb) < NB ? (K - kb) : NB;
 #pragma unroll
-            for (int j = 0; j < kNegBlock; ++j) {
+            for (int j = 0; j < NB; ++j) {
                 if (j < cnt) {
                     mk[j] = negi[kb + j];
                     ik[j] = infok[kb + j];
                 }
             }
 #pragma unroll
-            for (int j = 0; j < kNegBlock; ++j)
+            for (int j = 0; j < NB; ++j)
                 if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
         }
 
@@ -180,8 +183,10 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
     *blocks_out = blocks;
     if (blocks == 0) return hipSuccess;
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_fused_step<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t,
-                           ctl, a, neg, info, dup, lossp);
+        HUGE_NEG_DISPATCH(neg_block(t.K), {
+            hipLaunchKernelGGL((k_fused_step<G_, C_, NB_>), dim3((unsigned)blocks), dim3(kBlock),
+                               0, s, t, ctl, a, neg, info, dup, lossp);
+        });
     });
     return hipGetLastError();
 }
@@ -190,12 +195,12 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 // Bandwidth probe: the rows one step over the batch touches -- S[u_i],
 // T[v_i] and the K negatives T[m_ik] it would draw -- each read and written
 // back unchanged, in the fused kernel's launch shape (one group of G lanes per
-// positive, kNegBlock negative rows in flight), with no arithmetic besides a
+// positive, NB negative rows in flight), with no arithmetic besides a
 // multiplication by a run-time 1.0f that keeps the compiler from dropping the
 // stores (x * 1.0f == x for every x).  Its rate is the practical ceiling of
 // the step's random row traffic.
 // ---------------------------------------------------------------------------
-template <int G, int C>
+template <int G, int C, int NB>
 __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restrict__ ctl,
                                                   const int32_t* __restrict__ src,
                                                   const int32_t* __restrict__ dst, int64_t n,
@@ -216,12 +221,12 @@ __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restri
         for (int q = 0; q < C; ++q) x[q] = scale4(one, x[q]);
     };
     float4 s[C], t0[C];
-    float4 tk[kNegBlock][C];
-    int32_t mk[kNegBlock];
-    for (int kb = 0; kb < K; kb += kNegBlock) {
-        const int cnt = (K - kb) < kNegBlock ? (K - kb) : kNegBlock;
+    float4 tk[NB][C];
+    int32_t mk[NB];
+    for (int kb = 0; kb < K; kb += NB) {
+        const int cnt = (K - kb) < NB ? (K - kb) : NB;
 #pragma unroll
-        for (int j = 0; j < kNegBlock; ++j)
+        for (int j = 0; j < NB; ++j)
             if (j < cnt)
                 mk[j] = draw_negative(t.seed, first_pos + (uint64_t)i, (uint32_t)(kb + j),
                                       (uint64_t)t.N, t.thr, t.alias);
@@ -230,7 +235,7 @@ __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restri
             IO::load(t0, t.T, v, t.D, lane);
         }
 #pragma unroll
-        for (int j = 0; j < kNegBlock; ++j)
+        for (int j = 0; j < NB; ++j)
             if (j < cnt) IO::load(tk[j], t.T, mk[j], t.D, lane);
         if (kb == 0) {
             touch(s);
@@ -239,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restri
             IO::store(t.T, v, t.D, lane, t0);
         }
 #pragma unroll
-        for (int j = 0; j < kNegBlock; ++j) {
+        for (int j = 0; j < NB; ++j) {
             if (j < cnt) {
                 touch(tk[j]);
                 IO::store(t.T, mk[j], t.D, lane, tk[j]);
@@ -254,17 +259,19 @@ hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, co
     const int64_t blocks = fused_step_blocks(t.D, n);
     if (blocks == 0) return hipSuccess;
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_probe<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl,
-                           src, dst, n, first_pos, 1.0f);
+        HUGE_NEG_DISPATCH(neg_block(t.K), {
+            hipLaunchKernelGGL((k_probe<G_, C_, NB_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
+                               t, ctl, src, dst, n, first_pos, 1.0f);
+        });
     });
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Repeated rows.  Work item {start, len, key, kind}: the contributions at
-// sorted positions start .. start + len - 1 are added in that order, in
-// double (a hub row can collect tens of thousands of terms), and the row is
-// rounded to fp32 once: row = fp32(row - lr * sum).
+// Repeated rows.  The contributions of a row, at duplicate-buffer slots
+// start .. start + len - 1, are added in that order, in double (a hub row can
+// collect tens of thousands of terms), and the row is rounded to fp32 once:
+// row = fp32(row - lr * sum).
 // ---------------------------------------------------------------------------
 struct double4_ {
     double x, y, z, w;
@@ -384,164 +391,121 @@ __device__ __forceinline__ void coop_total(double4_ (&acc)[C], const double* s_p
     }
 }
 
-// Repeated rows, one workgroup per window of sorted positions.  A piece of
-// at most kLongPiece rows is summed by one group; a longer one by all PPB
-// groups of the workgroup, each over a fixed contiguous part, combined in
-// group order (the result does not depend on scheduling).
+// Cooperative sum of `len` rows starting at row `start` of `rows` (fp32
+// contributions or fp64 partials): the PPB groups of the workgroup each sum
+// a fixed contiguous part, and group 0 receives the parts' sum in group
+// order (the result does not depend on scheduling).  Every thread of the
+// workgroup calls it; it synchronises twice.
+template <int G, int C, typename Row>
+__device__ __forceinline__ void coop_sum(double4_ (&acc)[C], const Row* __restrict__ rows,
+                                         int64_t start, uint32_t len, int32_t D, int grp,
+                                         int lane, double* s_part) {
+    constexpr int PPB = kBlock / G;
+    const uint32_t part_len = (len + PPB - 1) / PPB;
+    const uint32_t b0 = (uint32_t)grp * part_len;
+    const uint32_t b1 = b0 + part_len < len ? b0 + part_len : len;
+    const int64_t cnt = b1 > b0 ? (int64_t)(b1 - b0) : 0;
+    if constexpr (sizeof(Row) == sizeof(float)) {
+        sum_rows<G, C>(acc, rows, start + b0, cnt, D, lane);
+    } else {
+#pragma unroll
+        for (int q = 0; q < C; ++q) acc[q] = double4_{0.0, 0.0, 0.0, 0.0};
+        for (int64_t r = 0; r < cnt; ++r) {
+            double4_ x[C];
+            PartIO<G, C>::load(x, rows, start + b0 + r, D, lane);
+#pragma unroll
+            for (int q = 0; q < C; ++q) {
+                acc[q].x += x[q].x;
+                acc[q].y += x[q].y;
+                acc[q].z += x[q].z;
+                acc[q].w += x[q].w;
+            }
+        }
+    }
+    coop_store<G, C>(s_part, grp, lane, D, acc);
+    __syncthreads();
+    if (grp == 0) coop_total<G, C>(acc, s_part, lane, D);
+    __syncthreads();
+}
+
+// Repeated rows.  Short runs ({start, len <= kShortRun, key}): one group each
+// sums its contributions in occurrence order and updates the row.  Pieces
+// ({start, len <= kPiece, key, part}): the whole workgroup sums them; a whole
+// run (part = 0) updates its row, a piece of a longer run stores its sum as
+// partial part - 1.  The record counts were set by the grouping of this batch.
 template <int G, int C>
 __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control* __restrict__ ctl,
-                                                      const uint4* __restrict__ work,
-                                                      const uint32_t* __restrict__ wcount,
+                                                      const uint4* __restrict__ shorts,
+                                                      const uint4* __restrict__ pieces,
                                                       const float* __restrict__ dup,
-                                                      double* __restrict__ partA,
-                                                      double* __restrict__ partB, float lr,
-                                                      int64_t windows) {
+                                                      double* __restrict__ part, float lr,
+                                                      ListCaps caps) {
     constexpr int PPB = kBlock / G;
     __shared__ double s_part[1024 * C];  // PPB x D doubles: D <= 4 G C
     if (ctl->step_bad) return;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
     const int32_t D = t.D;
-    for (int64_t w = blockIdx.x; w < windows; w += gridDim.x) {
-        const uint32_t wc = wcount[w];
-        const uint32_t cnt = wc & ~kHasLong;
-        // short pieces: one group each
-        for (uint32_t p = grp; p < cnt; p += PPB) {
-            const uint4 rec = work[w * kChunk + p];
-            if (rec.y > kLongPiece) continue;
-            double4_ acc[C];
-            sum_rows<G, C>(acc, dup, rec.x, rec.y, D, lane);
-            if (rec.w == 0u) {
+    // the grouping never lists more than the capacities (it flags the call
+    // instead); the bounds only keep a broken invariant inside the lists
+    const uint32_t ns = ctl->n_short < caps.shorts ? ctl->n_short : caps.shorts;
+    const uint32_t np = ctl->n_piece < caps.pieces ? ctl->n_piece : caps.pieces;
+    for (uint32_t r = blockIdx.x * PPB + grp; r < ns; r += gridDim.x * PPB) {
+        const uint4 rec = shorts[r];
+        double4_ acc[C];
+        sum_rows<G, C>(acc, dup, rec.x, rec.y, D, lane);
+        apply_row<G, C>(t, rec.z, acc, lr, lane);
+    }
+    for (uint32_t r = blockIdx.x; r < np; r += gridDim.x) {
+        const uint4 rec = pieces[r];  // the same for every thread
+        double4_ acc[C];
+        coop_sum<G, C>(acc, dup, rec.x, rec.y, D, grp, lane, s_part);
+        if (grp == 0) {
+            if (rec.w == 0u)
                 apply_row<G, C>(t, rec.z, acc, lr, lane);
-            } else {
-                double* part = rec.w == 1u ? partB : partA;
-                PartIO<G, C>::store(part, w, D, lane, acc);
-            }
-        }
-        if (!(wc & kHasLong)) continue;
-        // long pieces: the whole workgroup (rec is the same for every thread)
-        for (uint32_t p = 0; p < cnt; ++p) {
-            const uint4 rec = work[w * kChunk + p];
-            if (rec.y <= kLongPiece) continue;
-            const uint32_t part_len = (rec.y + PPB - 1) / PPB;
-            const uint32_t b0 = grp * part_len;
-            const uint32_t b1 = b0 + part_len < rec.y ? b0 + part_len : rec.y;
-            double4_ acc[C];
-            sum_rows<G, C>(acc, dup, (int64_t)rec.x + b0, b1 > b0 ? (int64_t)(b1 - b0) : 0, D,
-                           lane);
-            coop_store<G, C>(s_part, grp, lane, D, acc);
-            __syncthreads();
-            if (grp == 0) {
-                coop_total<G, C>(acc, s_part, lane, D);
-                if (rec.w == 0u) {
-                    apply_row<G, C>(t, rec.z, acc, lr, lane);
-                } else {
-                    double* part = rec.w == 1u ? partB : partA;
-                    PartIO<G, C>::store(part, w, D, lane, acc);
-                }
-            }
-            __syncthreads();
+            else
+                PartIO<G, C>::store(part, (int64_t)rec.w - 1, D, lane, acc);
         }
     }
 }
 
-// A run that spans windows w0 .. wl: its first piece's partial sum (partB of
-// w0) plus the pieces of windows w0+1 .. wl (partA), then one update of the
-// row.  The windows of the run are found 256 at a time; the groups of the
-// workgroup sum fixed interleaved subsets of them, combined in group order.
+// Runs longer than kPiece ({key, first partial, partials}): the partial sums
+// of their pieces, added in piece order, update the row once.
 template <int G, int C>
-__global__ __launch_bounds__(kBlock) void k_long_combine(TableArgs t, const Control* __restrict__ ctl,
-                                                         const uint32_t* __restrict__ longhead,
-                                                         const uint32_t* __restrict__ keys,
-                                                         int64_t m, const double* __restrict__ partA,
-                                                         const double* __restrict__ partB,
-                                                         float lr, int64_t windows) {
-    using IO = PartIO<G, C>;
-    constexpr int PPB = kBlock / G;
+__global__ __launch_bounds__(kBlock) void k_combine(TableArgs t, const Control* __restrict__ ctl,
+                                                    const uint4* __restrict__ combs,
+                                                    const double* __restrict__ part, float lr,
+                                                    ListCaps caps) {
     __shared__ double s_part[1024 * C];
-    __shared__ int64_t s_end;
     if (ctl->step_bad) return;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
-    const int32_t D = t.D;
-    for (int64_t w0 = blockIdx.x; w0 < windows; w0 += gridDim.x) {
-        const uint32_t head = longhead[w0];
-        if (head == kNoHead) continue;  // uniform over the workgroup
-        const uint32_t key = keys[head];
-        // last window of the run: the first window from w0+1 whose first key
-        // differs (or that starts past the end), minus one
-        int64_t base = w0 + 1;
-        while (true) {
-            if (threadIdx.x == 0) s_end = INT64_MAX;
-            __syncthreads();
-            const int64_t w = base + threadIdx.x;
-            const bool cont = w * kChunk < m && keys[w * kChunk] == key;
-            if (!cont) atomicMin((unsigned long long*)&s_end, (unsigned long long)w);
-            __syncthreads();
-            const int64_t e = s_end;
-            __syncthreads();
-            if (e != INT64_MAX) {
-                base = e;
-                break;
-            }
-            base += kBlock;
-        }
-        const int64_t wl = base - 1;  // >= w0 + 1: the head piece reached its window's end
+    const uint32_t nc = ctl->n_comb < caps.combs ? ctl->n_comb : caps.combs;
+    for (uint32_t r = blockIdx.x; r < nc; r += gridDim.x) {
+        const uint4 rec = combs[r];
         double4_ acc[C];
-#pragma unroll
-        for (int q = 0; q < C; ++q) acc[q] = double4_{0.0, 0.0, 0.0, 0.0};
-        for (int64_t w = w0 + 1 + grp; w <= wl; w += PPB) {
-            double4_ b[C];
-            IO::load(b, partA, w, D, lane);
-#pragma unroll
-            for (int q = 0; q < C; ++q) {
-                acc[q].x += b[q].x;
-                acc[q].y += b[q].y;
-                acc[q].z += b[q].z;
-                acc[q].w += b[q].w;
-            }
-        }
-        coop_store<G, C>(s_part, grp, lane, D, acc);
-        __syncthreads();
-        if (grp == 0) {
-            double4_ tot[C], hb[C];
-            coop_total<G, C>(tot, s_part, lane, D);
-            IO::load(hb, partB, w0, D, lane);
-#pragma unroll
-            for (int q = 0; q < C; ++q) {
-                hb[q].x += tot[q].x;
-                hb[q].y += tot[q].y;
-                hb[q].z += tot[q].z;
-                hb[q].w += tot[q].w;
-            }
-            apply_row<G, C>(t, key, hb, lr, lane);
-        }
-        __syncthreads();
+        coop_sum<G, C>(acc, part, rec.y, rec.z, t.D, grp, lane, s_part);
+        if (grp == 0) apply_row<G, C>(t, rec.x, acc, lr, lane);
     }
 }
 
-hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* work,
-                            const uint32_t* wcount, const float* dup, double* partA,
-                            double* partB, float lr, int64_t m, hipStream_t s) {
+hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* shorts,
+                            const uint4* pieces, const float* dup, double* part, float lr,
+                            ListCaps caps, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
-    const int64_t windows = (m + kChunk - 1) / kChunk;
-    const int64_t blocks = windows < 16384 ? (windows > 0 ? windows : 1) : 16384;
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_dup_apply<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t,
-                           ctl, work, wcount, dup, partA, partB, lr, windows);
+        hipLaunchKernelGGL((k_dup_apply<G_, C_>), dim3(1024), dim3(kBlock), 0, s, t, ctl, shorts,
+                           pieces, dup, part, lr, caps);
     });
     return hipGetLastError();
 }
 
-hipError_t launch_long_combine(const TableArgs& t, Control* ctl, const uint32_t* longhead,
-                               const uint32_t* keys, int64_t m, const double* partA,
-                               const double* partB, float lr, hipStream_t s) {
+hipError_t launch_combine(const TableArgs& t, Control* ctl, const uint4* combs,
+                          const double* part, float lr, ListCaps caps, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
-    const int64_t windows = (m + kChunk - 1) / kChunk;
-    const int64_t blocks = windows < 2048 ? (windows > 0 ? windows : 1) : 2048;
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_long_combine<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
-                           t, ctl, longhead, keys, m, partA, partB, lr, windows);
+        hipLaunchKernelGGL((k_combine<G_, C_>), dim3(256), dim3(kBlock), 0, s, t, ctl, combs,
+                           part, lr, caps);
     });
     return hipGetLastError();
 }

@@ -78,9 +78,9 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 }
 
 // ---------------------------------------------------------------------------
-// Per-call set-up: clear the call's flag, the tile tickets, the sort's
-// overflow flag and queue count, and the digit histograms (a kernel rather
-// than a memset so that the sequence stays valid inside a captured graph).
+// Per-call set-up: clear the call's flag, the tile tickets, the counts of the
+// repeated-row lists and the digit histograms (a kernel rather than a memset
+// so that the sequence stays valid inside a captured graph).
 // ---------------------------------------------------------------------------
 __global__ void k_begin(Control* ctl, uint32_t* hist) {
     const int t = threadIdx.x;
@@ -89,8 +89,7 @@ __global__ void k_begin(Control* ctl, uint32_t* hist) {
     if (t == 0) {
         ctl->step_bad = 0u;
         for (int p = 0; p < kMaxPasses; ++p) ctl->tickets[p] = 0u;
-        ctl->overflow = 0u;
-        ctl->big_count = 0u;
+        ctl->n_short = ctl->n_piece = ctl->n_comb = ctl->n_part = 0u;
     }
 }
 
@@ -128,17 +127,20 @@ hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Validation, negatives and sort keys.  kSamplePer positives per thread
-// (coalesced rounds of one workgroup width); for each positive i:
-//   - checks 0 <= src, dst < N and co_count >= 0 (a failure flags the call);
-//   - draws the K negatives into neg[i K + k];
-//   - if keys != nullptr, writes the (2 + K) occurrence keys of positive i at
-//     o = i (2 + K) + slot: slot 0 the source row (key N + src), slot 1 the
-//     destination row (key dst), slots 2.. the negatives (key m), sets their
-//     info entries to -1 (the run marking overwrites repeated ones) and
-//     counts the digits of every radix pass (digit ps = bits [ps * bits,
-//     (ps + 1) * bits) of the key, counted at hist[ps * kMaxBins + digit]).
-// Without src (src == nullptr) only negatives are drawn.
+// Validation, negatives and sort keys.  A workgroup takes kSamplePos
+// consecutive positives.  Positive i has S = 2 + K occurrences at
+// o = i S + slot: slot 0 the source row (key N + src), slot 1 the destination
+// row (key dst), slot 2 + k negative k (key m).
+//   - one thread per positive checks 0 <= src, dst < N and co_count >= 0 (a
+//     failure flags the call) and, with keys, handles slots 0 and 1;
+//   - one thread per negative, consecutive threads on consecutive (i, k), so
+//     that the stores of a wave are contiguous, draws negative k of positive
+//     i into neg[i K + k] and, with keys, handles slot 2 + k.
+// Handling a slot with keys (keys != nullptr): write keys[o], set info[o] = -1
+// (the grouping overwrites repeated ones) and count the digits of every
+// radix pass (digit ps = bits [ps * bits, (ps + 1) * bits) of the key,
+// counted at hist[ps * kMaxBins + digit]).  Without src only negatives are
+// drawn.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, StepArgs a,
                                                    int32_t* __restrict__ neg,
@@ -153,56 +155,48 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
         for (int j = threadIdx.x; j < passes * kMaxBins; j += kBlock) s_hist[j] = 0u;
         __syncthreads();
     }
-    const int K = t.K;
-    for (int r = 0; r < kSamplePer; ++r) {
-        const int64_t i = ((int64_t)blockIdx.x * kSamplePer + r) * kBlock + threadIdx.x;
-        if (i >= a.n) break;
-        const uint64_t p = a.first_pos + (uint64_t)i;
-        uint32_t key_s = 0, key_d = 0;
-        if (a.src != nullptr) {
+    const int64_t K = t.K, S = 2 + K;
+    const int64_t i0 = (int64_t)blockIdx.x * kSamplePos;
+    const int64_t np = a.n - i0 < kSamplePos ? a.n - i0 : kSamplePos;  // positives here
+    auto put = [&](int64_t o, uint32_t key) {
+        keys[o] = key;
+        info[o] = -1;
+        for (int ps = 0; ps < passes; ++ps)
+            atomicAdd(&s_hist[ps * kMaxBins + ((key >> (ps * bits)) & dmask)], 1u);
+    };
+    if (a.src != nullptr) {
+        for (int64_t j = threadIdx.x; j < np; j += kBlock) {
+            const int64_t i = i0 + j;
             int32_t u = a.src[i], v = a.dst[i];
-            const int32_t c = a.cc[i];
             if (u < 0 || (int64_t)u >= t.N || v < 0 || (int64_t)v >= t.N) {
                 raise_error(ctl, kBadId);
                 u = 0;
                 v = 0;
             }
-            if (c < 0) raise_error(ctl, kBadCount);
-            key_s = (uint32_t)((uint64_t)t.N + (uint64_t)u);
-            key_d = (uint32_t)v;
-        }
-        const int64_t o = i * (int64_t)(2 + K);
-        if (with_keys) {
-            keys[o] = key_s;
-            keys[o + 1] = key_d;
-            for (int sl = 0; sl < 2 + K; ++sl) info[o + sl] = -1;
-            for (int ps = 0; ps < passes; ++ps) {
-                atomicAdd(&s_hist[ps * kMaxBins + ((key_s >> (ps * bits)) & dmask)], 1u);
-                atomicAdd(&s_hist[ps * kMaxBins + ((key_d >> (ps * bits)) & dmask)], 1u);
+            if (a.cc[i] < 0) raise_error(ctl, kBadCount);
+            if (with_keys) {
+                put(i * S, (uint32_t)((uint64_t)t.N + (uint64_t)u));
+                put(i * S + 1, (uint32_t)v);
             }
         }
-        // negatives in chunks of kNegBlock: the alias-table loads of a chunk
-        // are independent and issued together
-        for (int k0 = 0; k0 < K; k0 += kNegBlock) {
-            int32_t mm[kNegBlock];
-#pragma unroll
-            for (int q = 0; q < kNegBlock; ++q)
-                if (k0 + q < K)
-                    mm[q] = draw_negative(t.seed, p, (uint32_t)(k0 + q), (uint64_t)t.N, t.thr,
-                                          t.alias);
-#pragma unroll
-            for (int q = 0; q < kNegBlock; ++q) {
-                if (k0 + q < K) {
-                    const int32_t m = mm[q];
-                    neg[i * K + k0 + q] = m;
-                    if (with_keys) {
-                        keys[o + 2 + k0 + q] = (uint32_t)m;
-                        for (int ps = 0; ps < passes; ++ps)
-                            atomicAdd(&s_hist[ps * kMaxBins + (((uint32_t)m >> (ps * bits)) & dmask)],
-                                      1u);
-                    }
-                }
-            }
+    }
+    // negatives: draw j of this workgroup is negative k of positive i0 + q,
+    // j = q K + k; a round of kBlock draws advances (q, k) by dq K + dr
+    const uint32_t Ku = (uint32_t)K;
+    const uint32_t nd = (uint32_t)(np * K);
+    const uint32_t dq = (uint32_t)kBlock / Ku, dr = (uint32_t)kBlock - dq * Ku;
+    uint32_t q = (uint32_t)threadIdx.x / Ku, k = (uint32_t)threadIdx.x - q * Ku;
+    for (uint32_t j = threadIdx.x; j < nd; j += kBlock) {
+        const int64_t i = i0 + q;
+        const int32_t m = draw_negative(t.seed, a.first_pos + (uint64_t)i, k, (uint64_t)t.N,
+                                        t.thr, t.alias);
+        neg[i * K + k] = m;
+        if (with_keys) put(i * S + 2 + k, (uint32_t)m);
+        k += dr;
+        q += dq;
+        if (k >= Ku) {
+            k -= Ku;
+            ++q;
         }
     }
     if (with_keys) {
@@ -217,9 +211,9 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
                          uint32_t* keys, int32_t* info, uint32_t* hist, SortPlan plan,
                          hipStream_t s) {
-    const int64_t per_block = (int64_t)kBlock * kSamplePer;
-    const int64_t blocks = (a.n + per_block - 1) / per_block;
+    const int64_t blocks = (a.n + kSamplePos - 1) / kSamplePos;
     if (blocks == 0) return hipSuccess;
+    if (t.K < 1 || t.K > kBlock) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
                        info, hist, keys ? plan.passes : 0, plan.bits);
     return hipGetLastError();

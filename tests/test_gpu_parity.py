@@ -94,15 +94,18 @@ STEP_CASES = [
     (2, 8, 5, 50, "two nodes: every row repeats"),
     (1_000, 128, 64, 100, "largest K"),
     (20_000, 128, 5, 9000, "several sort tiles"),
-    (100_000, 16, 5, 20_000, "keys of 18 bits: two 9-bit radix passes"),
-    (300_000, 16, 4, 30_000, "keys of 20 bits: two 10-bit radix passes, 22 tiles"),
+    (100_000, 16, 5, 20_000, "keys of 18 bits: 9-bit digit, 18 radix tiles"),
+    (300_000, 16, 4, 30_000, "keys of 20 bits: 10-bit digit, 22 radix tiles"),
 ]
 
 
 def _one_step(N, D, K, n, scatter, seed=7, weights=None, hub=0.0, cmax=5, lr=0.025,
-              heavy=None):
+              heavy=None, batch=None):
     rng = np.random.default_rng(N * 31 + D * 7 + K)
-    src, dst, cc = _random_batch(rng, N, n, cmax=cmax, hub_frac=hub)
+    if batch is None:
+        src, dst, cc = _random_batch(rng, N, n, cmax=cmax, hub_frac=hub)
+    else:
+        src, dst, cc = batch
     first = 1000
     tr = _trainer(N, D, K, n, seed=seed, weights=weights, scatter=scatter)
     loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), first, lr).item()
@@ -153,18 +156,13 @@ def test_one_step_matches_oracle(scatter, N, D, K, n, note):
     say(f"step {scatter} N={N} D={D} K={K} n={n} ({note})")
     tr, (src, dst, cc, neg) = _one_step(N, D, K, n, scatter)
     if scatter == "sorted":
-        uS, uT, dup = tr.stats()
-        keys = np.concatenate([src.astype(np.int64) + N, dst, neg.reshape(-1)])
-        u, cnt = np.unique(keys, return_counts=True)
-        assert uS == np.unique(src).size
-        assert uT == np.unique(np.concatenate([dst, neg.reshape(-1)])).size
-        assert dup == int(cnt[cnt > 1].sum())
+        _check_counts(tr, N, src, dst, neg)
 
 
 @pytest.mark.parametrize("scatter", ["sorted", "atomic"])
 def test_hub_rows_and_large_counts(scatter):
     """Half the batch shares one source row, a quarter one destination row,
-    co_counts up to 1000: long runs split over several sum windows.  The
+    co_counts up to 1000: long runs summed in pieces and combined.  The
     sorted scatter sums repeated rows in double and meets the element-wise
     bound everywhere; the atomic one is held to it on rows hit <= 64 times."""
     say(f"hub {scatter}")
@@ -172,24 +170,55 @@ def test_hub_rows_and_large_counts(scatter):
               heavy=None if scatter == "sorted" else 64)
 
 
-@pytest.mark.parametrize("N,n,hub,note", [
-    (5_000, 8_000, 0.75, "hub bucket of 6000: large in-LDS sort, output in the other buffer"),
-    (5_000, 16_000, 0.9, "hub bucket of 14400: overflow, later global pass"),
-    (1_100_000, 8_000, 0.75, "three passes: large in-LDS sort in place"),
-    (1_100_000, 16_000, 0.9, "three passes: overflow, two later global passes"),
-])
-def test_bucket_sort_regimes(N, n, hub, note):
-    """Grouping with buckets of every size class; tables and the distinct /
-    repeated counts must match the oracle and numpy."""
-    say(f"bucket regimes N={N} n={n} hub={hub} ({note})")
-    K = 2
-    tr, (src, dst, cc, neg) = _one_step(N, 8, K, n, "sorted", hub=hub)
+def _check_counts(tr, N, src, dst, neg):
     uS, uT, dup = tr.stats()
     keys = np.concatenate([src.astype(np.int64) + N, dst, neg.reshape(-1)])
     u, cnt = np.unique(keys, return_counts=True)
     assert uS == np.unique(src).size
     assert uT == np.unique(np.concatenate([dst, neg.reshape(-1)])).size
     assert dup == int(cnt[cnt > 1].sum())
+
+
+@pytest.mark.parametrize("N,n,hub,note", [
+    (5_000, 8_000, 0.75, "hub rows of 6000 and 1500 occurrences: pieces and combined sums"),
+    (5_000, 16_000, 0.9, "a bucket of > 14400 keys: grouped over several chunks"),
+    (1_100_000, 8_000, 0.75, "hub rows among mostly distinct keys"),
+    (1_100_000, 16_000, 0.9, "several chunks, long runs, distinct tail"),
+])
+@pytest.mark.parametrize("table_bits", [None, 12, 14])
+def test_grouping_regimes(N, n, hub, note, table_bits, monkeypatch):
+    """Grouping with hub rows and buckets of every size; tables and the
+    distinct / repeated counts must match the oracle and numpy.  table_bits
+    forces the hash-table grouping of every key with that table size (by
+    default a bitmap of the bucket's keys lets only repeated keys in)."""
+    if table_bits is not None:
+        monkeypatch.setenv("HUGE_GROUP_TABLE_BITS", str(table_bits))
+    say(f"grouping regimes N={N} n={n} hub={hub} table_bits={table_bits} ({note})")
+    tr, (src, dst, cc, neg) = _one_step(N, 8, 2, n, "sorted", hub=hub)
+    _check_counts(tr, N, src, dst, neg)
+
+
+@pytest.mark.parametrize("table_bits", [None, 12, 13])
+def test_bucket_with_more_distinct_rows_than_one_table(table_bits, monkeypatch):
+    """Every source and destination key has the same lowest 10 bits (the
+    bucket digit for N = 8e6, whose keys have 24 bits), so about 9000
+    distinct keys share one bucket, about 6700 of them repeated: more than
+    one LDS table holds, and the bucket is grouped key range by key range
+    (with the bitmap of repeated keys or, with table_bits, without)."""
+    if table_bits is not None:
+        monkeypatch.setenv("HUGE_GROUP_TABLE_BITS", str(table_bits))
+    N, D, K, n = 8_000_000, 8, 1, 12_000
+    ids = np.arange(N, dtype=np.int64)
+    cand_s = ids[((ids + N) & 1023) == 7][:4500]
+    cand_d = ids[(ids & 1023) == 7][:4500]
+    rng = np.random.default_rng(23)
+    src = rng.choice(cand_s, n).astype(np.int32)   # with replacement: repeats
+    dst = rng.choice(cand_d, n).astype(np.int32)
+    cc = rng.integers(0, 6, n).astype(np.int32)
+    say(f"one crowded bucket: {np.unique(src).size + np.unique(dst).size} distinct keys, "
+        f"table_bits={table_bits}")
+    tr, (src, dst, cc, neg) = _one_step(N, D, K, n, "sorted", batch=(src, dst, cc))
+    _check_counts(tr, N, src, dst, neg)
 
 
 def test_alias_negatives_step():
