@@ -63,7 +63,6 @@ struct huge_handle {
     Layout lay;
     SortPlan plan;  // digit width of the radix pass for keys below 2N
     int key_bits;   // bits of 2N - 1
-    uint32_t epoch;            // tags the look-back words of each radix pass
     int64_t prepared;          // batches sampled
     int64_t applied;           // applies issued
     int last_applied_slot;     // -1 before the first apply
@@ -141,14 +140,15 @@ Layout make_layout(const huge_config* c) {
     for (int s = 0; s < kSlots; ++s) {
         SlotLayout& S = L.slot[s];
         S.ctrl = take(sizeof(Control));
-        S.hist = take(sizeof(uint32_t) * kMaxPasses * kMaxBins);
+        S.hist = take(sizeof(uint32_t) * kMaxBins);
         S.neg = take(sizeof(int32_t) * (size_t)(nb * K));
         if (sorted) {
             S.keys0 = take(sizeof(uint32_t) * (size_t)M);
             S.keys1 = take(sizeof(uint32_t) * (size_t)M);
             S.vals1 = take(sizeof(uint32_t) * (size_t)M);
             S.info = take(sizeof(int32_t) * (size_t)M);
-            S.status = take(sizeof(uint64_t) * (size_t)(L.sort_tiles * kMaxBins));
+            S.tcount = take(sizeof(uint32_t) * (size_t)(L.sort_tiles * kMaxBins));
+            S.tprefix = take(sizeof(uint32_t) * (size_t)(L.sort_tiles * kMaxBins));
             S.bstart = take(sizeof(uint32_t) * kMaxBins);
             S.shorts = take(sizeof(uint4) * (size_t)caps.shorts);
             S.pieces = take(sizeof(uint4) * (size_t)caps.pieces);
@@ -239,7 +239,6 @@ huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* t
     h->lay = L;
     h->key_bits = key_bits(cfg->num_nodes);
     h->plan = sort_plan(h->key_bits);
-    h->epoch = 0;
     if (const char* e = getenv("HUGE_BESIDE_GRID")) {  // tuning experiments
         const int g = atoi(e);
         if (g >= 0 && g <= 65536) h->beside_grid = g;
@@ -265,13 +264,11 @@ huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* t
     return HUGE_OK;
 }
 
-// Zero the control blocks and the look-back words, on the stream.
+// Zero the control blocks and mark every occurrence unrepeated, on the stream.
 huge_status reset_workspace(huge_handle* h, hipStream_t s) {
     for (int k = 0; k < kSlots; ++k) {
         HIP_TRY(hipMemsetAsync(h->ws + h->lay.slot[k].ctrl, 0, sizeof(Control), s));
         if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-            HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
-                                        h->lay.sort_tiles * kMaxBins, s));
             HIP_TRY(launch_fill_i32(at<int32_t>(h, h->lay.slot[k].info), -1, h->lay.max_occ, s));
         }
     }
@@ -300,8 +297,9 @@ hipError_t wait_on(hipStream_t s, hipEvent_t e, hipStream_t from) {
     return hipStreamWaitEvent(s, e, 0);
 }
 
-// Stage 1: validation, negatives, keys and digit counts of a batch, into the
-// next slot, on the grouping stream s (launches only; arguments checked).
+// Stage 1: validation, negatives, keys, per-tile digit counts and their
+// prefixes over tiles, of a batch, into the next slot, on the grouping
+// stream s (launches only; arguments checked).
 huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
                          const int32_t* cc, int64_t n, uint64_t first_pos, hipStream_t s) {
     const int slot = (int)(h->prepared % kSlots);
@@ -321,13 +319,18 @@ huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
     // the slot's previous apply must be complete before its buffers change
     HIP_TRY(wait_on(s, h->done[slot], h->slot_apply_stream[slot]));
     if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
-    HIP_TRY(launch_begin(ctl, hist, s));
+    HIP_TRY(launch_begin(ctl, s));
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
-    // only the digit counts of the one radix pass are needed
-    const SortPlan one{1, h->plan.bits};
     HIP_TRY(launch_sample(t, ctl, a, at<int32_t>(h, SL.neg),
                           sorted ? at<uint32_t>(h, SL.keys0) : nullptr,
-                          sorted ? at<int32_t>(h, SL.info) : nullptr, hist, one, s));
+                          sorted ? at<int32_t>(h, SL.info) : nullptr, s));
+    if (sorted) {
+        const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
+        HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, h->plan.bits,
+                                  at<uint32_t>(h, SL.tcount), s));
+        HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, h->plan.bits,
+                                 at<uint32_t>(h, SL.tprefix), hist, s));
+    }
     if (!prof_mark(h, b, 1, s)) return HUGE_ERR_HIP;
     HIP_TRY(hipEventRecord(h->sampled[slot], s));
     b.stage = sorted ? 0 : 2;  // the atomic scatter needs no grouping
@@ -346,19 +349,10 @@ huge_status stage_radix(huge_handle* h, int slot, hipStream_t s) {
     const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
     HIP_TRY(wait_on(s, h->sampled[slot], b.stage_stream));
     if (!prof_mark(h, b, 2, s)) return HUGE_ERR_HIP;
-    // look-back tags: 8 per radix pass; the words are cleared when the 27-bit
-    // epoch wraps
-    h->epoch += 1;
-    if ((h->epoch & 0x07FFFFFFu) == 0u) {
-        for (int k = 0; k < kSlots; ++k)
-            HIP_TRY(launch_clear_status(at<uint64_t>(h, h->lay.slot[k].status),
-                                        h->lay.sort_tiles * kMaxBins, s));
-        h->epoch += 1;
-    }
-    HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), nullptr, at<uint32_t>(h, SL.keys1),
-                              at<uint32_t>(h, SL.vals1), m, 0, h->plan.bits,
-                              at<uint32_t>(h, SL.hist), at<uint64_t>(h, SL.status),
-                              h->epoch << 3, nullptr, at<uint32_t>(h, SL.bstart), s));
+    HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1),
+                              at<uint32_t>(h, SL.vals1), m, h->plan.bits,
+                              at<uint32_t>(h, SL.hist), at<uint32_t>(h, SL.tprefix),
+                              at<uint32_t>(h, SL.bstart), s));
     if (!prof_mark(h, b, 3, s)) return HUGE_ERR_HIP;
     HIP_TRY(hipEventRecord(h->radixed[slot], s));
     b.stage = 1;
@@ -538,7 +532,7 @@ huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* 
         HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
     double* lossp = at<double>(h, L.lossp);
     StepArgs a{d_src, d_dst, d_cc, n, first_pos_index, 0.0f, d_loss_sum};
-    HIP_TRY(launch_begin(ctl, nullptr, s));
+    HIP_TRY(launch_begin(ctl, s));
     int64_t blocks = 0;
     HIP_TRY(launch_eval(table_args(h), ctl, a, lossp, &blocks, s));
     HIP_TRY(launch_loss_final(ctl, lossp, blocks, d_loss_sum, s));
@@ -578,7 +572,7 @@ huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_
     hipStream_t s = static_cast<hipStream_t>(stream);
     StepArgs a{nullptr, nullptr, nullptr, n, first_pos_index, 0.0f, nullptr};
     HIP_TRY(launch_sample(table_args(h), at<Control>(h, h->lay.eval_ctrl), a, d_neg_out, nullptr,
-                          nullptr, nullptr, h->plan, s));
+                          nullptr, s));
     return HUGE_OK;
 }
 

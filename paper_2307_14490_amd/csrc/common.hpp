@@ -18,7 +18,6 @@ constexpr int kMaxPasses = 4;          // keys < 2^32
 constexpr int kSortThreads = 1024;     // threads of a sort workgroup (16 wave64)
 constexpr int kSortItems = 8;          // keys per thread in a sort tile
 constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 keys per tile
-constexpr int kLookBatch = 8;          // look-back words read together
 // Per-bucket grouping (k_group): chunks of kGroupChunk keys, an LDS hash
 // table of 2^bits slots (bits 12..14, from the mean bucket size); a bucket
 // range with more than 3/4 of the slots in distinct keys is split by further
@@ -53,19 +52,16 @@ constexpr uint32_t kBadInternal = 4u;  // a bounded wait expired or an index che
 struct Control {
     uint32_t step_bad;               // this call's input is invalid: skip all writes
     uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
-    uint32_t tickets[kMaxPasses];    // dynamic tile ids of the radix passes
     uint32_t n_short;                // repeated rows summed by one thread group
     uint32_t n_piece;                // pieces of up to kPiece occurrences summed by a workgroup
     uint32_t n_comb;                 // rows whose pieces' partial sums are combined
     uint32_t n_part;                 // partial sums allocated
     uint32_t site;                   // first failed internal check (a kSite* code)
-    uint32_t pad[5];
+    uint32_t pad[9];
 };
 
 // Internal checks (kBadInternal), recorded in Control::site.
 enum InternalSite : uint32_t {
-    kSiteRadixTicket = 1,
-    kSiteRadixWait = 2,
     kSiteRadixDest = 3,
     kSiteGroupBucket = 4,
     kSiteGroupDepth = 5,
@@ -86,14 +82,15 @@ enum InternalSite : uint32_t {
 // own regions; the apply regions are shared (applies are ordered).
 struct SlotLayout {
     size_t ctrl = 0;     // Control
-    size_t hist = 0;     // u32 [kMaxPasses][kMaxBins] global digit counts
+    size_t hist = 0;     // u32 [kMaxBins] occurrences per bucket (digit)
     size_t neg = 0;      // i32 [max_batch * K]
     // sorted scatter
     size_t keys0 = 0;    // u32 [M] keys in occurrence order
     size_t keys1 = 0;    // u32 [M] keys grouped by their lowest digit
     size_t vals1 = 0;    // u32 [M] their occurrence indices
     size_t info = 0;     // i32 [M]: -1, or the duplicate-buffer slot of an occurrence of a repeated row
-    size_t status = 0;   // u64 [sort_tiles * kMaxBins] look-back words
+    size_t tcount = 0;   // u32 [sort_tiles * kMaxBins] occurrences per tile and digit
+    size_t tprefix = 0;  // u32 [sort_tiles * kMaxBins] the same summed over earlier tiles
     size_t bstart = 0;   // u32 [kMaxBins] first position of each bucket
     size_t shorts = 0;   // uint4 [cap_short] {start, len, key, 0}
     size_t pieces = 0;   // uint4 [cap_piece] {start, len, key, 0 or partial index + 1}
@@ -203,15 +200,19 @@ struct WalkArgs {
 hipError_t launch_init(const TableArgs& t, float half_width, hipStream_t s);
 hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, const int64_t* ids,
                            int64_t n, float* out, hipStream_t s);
-hipError_t launch_begin(Control* ctl, uint32_t* hist, hipStream_t s);
-hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s);
+hipError_t launch_begin(Control* ctl, hipStream_t s);
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, int32_t* info, uint32_t* hist, SortPlan plan,
-                         hipStream_t s);
-hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
-                             uint32_t* keys_out, uint32_t* vals_out, int64_t m, int pass,
-                             int bits, const uint32_t* hist, uint64_t* status, uint32_t tag,
-                             const uint32_t* gate, uint32_t* bstart, hipStream_t s);
+                         uint32_t* keys, int32_t* info, hipStream_t s);
+// Bucketing of m keys by their lowest `bits` bits in tiles of kSortTile:
+// per-tile digit counts, their sums over earlier tiles and the bucket sizes
+// (hist), then the stable scatter into bucket order.
+hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits,
+                             uint32_t* tcount, hipStream_t s);
+hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int bits,
+                            uint32_t* tprefix, uint32_t* hist, hipStream_t s);
+hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
+                             uint32_t* vals_out, int64_t m, int bits, const uint32_t* hist,
+                             const uint32_t* tprefix, uint32_t* bstart, hipStream_t s);
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
                         uint4* shorts, uint4* pieces, uint4* combs, ListCaps caps,

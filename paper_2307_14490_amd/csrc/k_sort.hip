@@ -5,39 +5,23 @@
 //
 // Occurrence o = i (2 + K) + slot of positive i carries key N + src (slot 0,
 // source table) or the context row id (destination, negatives).
-//   1. k_radix_pass: one stable pass of an LSD radix sort on the lowest 8-10
-//      key bits (one kernel, single pass over the data with decoupled
-//      look-back between tiles) puts the occurrences of each bucket (digit)
-//      together, in occurrence order;
-//   2. k_group: one workgroup per bucket counts the bucket's keys in an LDS
-//      hash table, gives every repeated row a contiguous range of
-//      duplicate-buffer slots (inside the bucket's own range of positions),
-//      writes the slot of each of its occurrences, in occurrence order, to
-//      info[o], and lists the repeated rows for the duplicate kernels.
-// The radix pass uses 1024-thread workgroups and runs alone (it is issued just
-// before the previous batch's update); the grouping uses 256-thread
-// workgroups and runs beside that update.
+//   1. k_tile_count, k_tile_scan: the occurrences of each digit (lowest 8-10
+//      key bits) per tile of kSortTile occurrences, their sums over earlier
+//      tiles, and the bucket sizes;
+//   2. k_radix_pass: one stable scatter of the occurrences into bucket
+//      (digit) order, each bucket in occurrence order; no tile waits for
+//      another;
+//   3. k_group: one workgroup per bucket finds the bucket's repeated keys,
+//      gives every repeated row a contiguous range of duplicate-buffer slots
+//      (inside the bucket's own range of positions), writes the slot of each
+//      of its occurrences, in occurrence order, to info[o], and lists the
+//      repeated rows for the duplicate kernels.
+// Steps 1 run with the sampler; the scatter is issued just before the
+// previous batch's update and the grouping runs beside that update.
 #include "common.hpp"
 #include "device.hpp"
 
 namespace huge {
-
-// Look-back word: [tag:30 | flag:2 | count:32].  The tag identifies the
-// (call, pass); words of earlier calls read as "not yet published".
-constexpr uint64_t kFlagAggregate = 1ull;
-constexpr uint64_t kFlagPrefix = 2ull;
-
-__device__ __forceinline__ uint64_t lb_word(uint32_t tag, uint64_t flag, uint32_t count) {
-    return ((uint64_t)(tag & 0x3FFFFFFFu) << 34) | (flag << 32) | (uint64_t)count;
-}
-
-__device__ __forceinline__ void lb_store(uint64_t* p, uint64_t w) {
-    __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ uint64_t lb_load(const uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Inclusive sum over the first kBins threads of the workgroup (one value
 // each): wave shuffles, then the wave totals through LDS.  Every thread of
@@ -59,27 +43,120 @@ __device__ __forceinline__ uint32_t digit_inclusive_sum(uint32_t v, uint32_t* s_
     return mine ? v + add : 0u;
 }
 
-// One pass of BITS bits at shift BITS * pass over a tile of kSortTile
+// ---------------------------------------------------------------------------
+// Digit counts of tile t (kSortTile consecutive occurrences; kBlock threads,
+// coalesced reads): tcount[t * bins + d].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_tile_count(const Control* __restrict__ ctl,
+                                                       const uint32_t* __restrict__ keys,
+                                                       int64_t m, int bits,
+                                                       uint32_t* __restrict__ tcount) {
+    __shared__ uint32_t s_cnt[kMaxBins];
+    const int bins = 1 << bits;
+    for (int d = threadIdx.x; d < bins; d += kBlock) s_cnt[d] = 0u;
+    __syncthreads();
+    const int64_t t = blockIdx.x;
+    if (!ctl->step_bad) {
+        const int64_t base = t * kSortTile;
+        constexpr int kPer = kSortTile / kBlock;
+        uint32_t k[kPer];
+#pragma unroll
+        for (int r = 0; r < kPer; ++r) {
+            const int64_t o = base + (int64_t)r * kBlock + threadIdx.x;
+            k[r] = o < m ? keys[o] : 0xFFFFFFFFu;
+        }
+#pragma unroll
+        for (int r = 0; r < kPer; ++r)
+            if (k[r] != 0xFFFFFFFFu) atomicAdd(&s_cnt[k[r] & (uint32_t)(bins - 1)], 1u);
+    }
+    __syncthreads();
+    for (int d = threadIdx.x; d < bins; d += kBlock) tcount[t * bins + d] = s_cnt[d];
+}
+
+hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits,
+                             uint32_t* tcount, hipStream_t s) {
+    const int64_t tiles = (m + kSortTile - 1) / kSortTile;
+    if (tiles == 0) return hipSuccess;
+    if (bits < kMinDigitBits || bits > kMaxDigitBits) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_tile_count, dim3((unsigned)tiles), dim3(kBlock), 0, s, ctl, keys, m,
+                       bits, tcount);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Per digit d: tprefix[t * bins + d] = sum of tcount[u * bins + d] over tiles
+// u < t, and hist[d] = the sum over all tiles.  A workgroup takes
+// kScanDigits digits; its kSortThreads / kScanDigits thread groups each sum
+// a contiguous range of tiles, and the ranges are combined through LDS.
+// ---------------------------------------------------------------------------
+constexpr int kScanDigits = 16;
+constexpr int kScanGroups = kSortThreads / kScanDigits;  // 64
+
+__global__ __launch_bounds__(kSortThreads) void k_tile_scan(const Control* __restrict__ ctl,
+                                                            const uint32_t* __restrict__ tcount,
+                                                            int64_t tiles, int bits,
+                                                            uint32_t* __restrict__ tprefix,
+                                                            uint32_t* __restrict__ hist) {
+    __shared__ uint32_t s_part[kScanGroups][kScanDigits];
+    if (ctl->step_bad) return;  // uniform
+    const int bins = 1 << bits;
+    const int dl = threadIdx.x % kScanDigits, g = threadIdx.x / kScanDigits;
+    const int d = blockIdx.x * kScanDigits + dl;
+    const int64_t per = (tiles + kScanGroups - 1) / kScanGroups;
+    const int64_t t0 = (int64_t)g * per;
+    const int64_t t1 = t0 + per < tiles ? t0 + per : tiles;
+    uint32_t sum = 0;
+#pragma unroll 8
+    for (int64_t t = t0; t < t1; ++t) sum += tcount[t * bins + d];
+    s_part[g][dl] = sum;
+    __syncthreads();
+    uint32_t run = 0, total = 0;
+    for (int h = 0; h < kScanGroups; ++h) {
+        const uint32_t v = s_part[h][dl];
+        run += h < g ? v : 0u;
+        total += v;
+    }
+    if (g == 0) hist[d] = total;
+#pragma unroll 8
+    for (int64_t t = t0; t < t1; ++t) {
+        const uint32_t v = tcount[t * bins + d];
+        tprefix[t * bins + d] = run;
+        run += v;
+    }
+}
+
+hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int bits,
+                            uint32_t* tprefix, uint32_t* hist, hipStream_t s) {
+    const int64_t tiles = (m + kSortTile - 1) / kSortTile;
+    if (tiles == 0) return hipSuccess;
+    if (bits < kMinDigitBits || bits > kMaxDigitBits) return hipErrorInvalidValue;
+    static_assert((1 << kMinDigitBits) % kScanDigits == 0, "whole digit groups");
+    hipLaunchKernelGGL(k_tile_scan, dim3((unsigned)((1 << bits) / kScanDigits)),
+                       dim3(kSortThreads), 0, s, ctl, tcount, tiles, bits, tprefix, hist);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Stable scatter by the lowest BITS bits over a tile of kSortTile
 // consecutive items, kSortThreads threads; wave w owns items
 // [w * 512, (w + 1) * 512) of the tile in kSortItems rounds of 64.
-//   rank:    lanes of a round holding the same digit are found with BITS
-//            ballots; one lane per digit adds the round's count to the wave's
-//            LDS counter, whose old value places the round after the earlier
-//            ones;
-//   publish: per digit (threads < 2^BITS), the tile's count; the items are
-//            then written to LDS in digit order (stable);
-//   look-back: the counts of earlier tiles, kLookBatch words at a time, up
-//            to the first inclusive prefix;
-//   write:   LDS position p goes to global position p + (digit's global
-//            offset - digit's tile offset): runs of equal digits are
-//            contiguous, so the writes coalesce.
+//   rank:  lanes of a round holding the same digit are found with BITS
+//          ballots; one lane per digit adds the round's count to the wave's
+//          LDS counter, whose old value places the round after the earlier
+//          ones;
+//   order: per digit (threads < 2^BITS) the wave offsets; the items are
+//          written to LDS in digit order (stable);
+//   write: LDS position p goes to global position p + (digit's bucket start
+//          + digit's count in earlier tiles - digit's tile offset): runs of
+//          equal digits are contiguous, so the writes coalesce.
+// vals_out receives the occurrence index of each key.
+// ---------------------------------------------------------------------------
 template <int BITS>
 __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
-    Control* __restrict__ ctl, uint32_t* __restrict__ tickets,
-    const uint32_t* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
-    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m, int pass,
-    const uint32_t* __restrict__ hist, uint64_t* __restrict__ status, uint32_t tag,
-    const uint32_t* __restrict__ gate, uint32_t* __restrict__ bstart) {
+    Control* __restrict__ ctl, const uint32_t* __restrict__ keys_in,
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m,
+    const uint32_t* __restrict__ hist, const uint32_t* __restrict__ tprefix,
+    uint32_t* __restrict__ bstart) {
     constexpr int kBins = 1 << BITS;
     static_assert(kBins <= kSortThreads, "one thread per digit");
     constexpr int kWaves = kSortThreads / 64;
@@ -87,46 +164,30 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     __shared__ uint32_t s_wave[kWaves][kBins];
     __shared__ int32_t s_delta[kBins];
     __shared__ uint32_t s_tmp[2][kBins / 64];
-    __shared__ uint32_t s_tile;
     __shared__ uint32_t s_keys[kSortTile];
     __shared__ uint32_t s_vals[kSortTile];
 
     if (ctl->step_bad) return;  // uniform: the call is a no-op
-    if (gate != nullptr && *gate == 0u) return;  // the bucket sort completed the order
 
     const int tid = threadIdx.x;
     const int wave = tid >> 6;
     const int lane = tid & 63;
-    const int shift = pass * BITS;
     const bool digit_thread = tid < kBins;
     const int d = tid;  // the digit of threads < kBins
+    const int64_t tile = blockIdx.x;
 
     for (int j = tid; j < kWaves * kBins; j += kSortThreads) (&s_wave[0][0])[j] = 0u;
-    if (tid == 0) s_tile = atomicAdd(tickets, 1u);
-    // Tiles are normally handed out in workgroup order: load that tile's
-    // items while the ticket is in flight, reload if it differs.
-    uint32_t key[kSortItems], val[kSortItems];
-    auto load_tile = [&](int64_t t) {
-        const int64_t base = t * kSortTile + (int64_t)wave * kWaveItems;
-#pragma unroll
-        for (int r = 0; r < kSortItems; ++r) {
-            const int64_t idx = base + r * 64 + lane;
-            const bool valid = idx < m;
-            key[r] = valid ? keys_in[idx] : 0u;
-            val[r] = valid ? (vals_in ? vals_in[idx] : (uint32_t)idx) : 0u;
-        }
-    };
-    load_tile(blockIdx.x);
-    const uint32_t hd = digit_thread ? hist[d] : 0u;
-    const uint32_t global_excl = digit_inclusive_sum<kBins>(hd, s_tmp[0]) - hd;  // synchronises
-    const int64_t tile = s_tile;
-    if (tile >= (int64_t)gridDim.x) {  // tickets were not reset: refuse, never wait
-        if (tid == 0) raise_internal(ctl, kSiteRadixTicket);
-        return;
-    }
-    if (bstart != nullptr && tile == 0 && digit_thread) bstart[d] = global_excl;
-    if (tile != (int64_t)blockIdx.x) load_tile(tile);
     const int64_t base_idx = tile * kSortTile + (int64_t)wave * kWaveItems;
+    uint32_t key[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int64_t idx = base_idx + r * 64 + lane;
+        key[r] = idx < m ? keys_in[idx] : 0u;
+    }
+    const uint32_t hd = digit_thread ? hist[d] : 0u;
+    const uint32_t before_tile = digit_thread ? tprefix[tile * kBins + d] : 0u;
+    const uint32_t global_excl = digit_inclusive_sum<kBins>(hd, s_tmp[0]) - hd;  // synchronises
+    if (bstart != nullptr && tile == 0 && digit_thread) bstart[d] = global_excl;
 
     uint32_t rank[kSortItems];
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -136,7 +197,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
 #pragma unroll
         for (int r = 0; r < kSortItems; ++r) {
             const bool valid = base_idx + r * 64 + lane < m;
-            const uint32_t dg = (key[r] >> shift) & (kBins - 1);
+            const uint32_t dg = key[r] & (kBins - 1);
             uint64_t peers = __ballot(valid);
 #pragma unroll
             for (int b = 0; b < BITS; ++b) {
@@ -156,7 +217,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     }
     __syncthreads();
 
-    // Per digit: wave offsets, tile count, publication.
+    // Per digit: wave offsets and the tile's count.
     uint32_t tile_count = 0;
     uint32_t wcnt[kWaves];
     if (digit_thread) {
@@ -165,8 +226,6 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
             wcnt[w] = s_wave[w][d];
             tile_count += wcnt[w];
         }
-        lb_store(status + tile * kBins + d,
-                 lb_word(tag, tile == 0 ? kFlagPrefix : kFlagAggregate, tile_count));
     }
     const uint32_t local_excl = digit_inclusive_sum<kBins>(tile_count, s_tmp[1]) - tile_count;
     if (digit_thread) {
@@ -176,69 +235,19 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
             s_wave[w][d] = run;
             run += wcnt[w];
         }
+        s_delta[d] = (int32_t)(global_excl + before_tile) - (int32_t)local_excl;
     }
     __syncthreads();
 
     // Stable tile-local order in LDS.
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
-        if (base_idx + r * 64 + lane < m) {
-            const uint32_t dg = (key[r] >> shift) & (kBins - 1);
-            const uint32_t p = s_wave[wave][dg] + rank[r];
+        const int64_t idx = base_idx + r * 64 + lane;
+        if (idx < m) {
+            const uint32_t p = s_wave[wave][key[r] & (kBins - 1)] + rank[r];
             s_keys[p] = key[r];
-            s_vals[p] = val[r];
+            s_vals[p] = (uint32_t)idx;
         }
-    }
-
-    // Decoupled look-back over the tiles before this one, for digit d.
-    if (digit_thread) {
-        uint32_t excl = 0;
-        if (tile > 0) {
-            const uint32_t want = tag & 0x3FFFFFFFu;
-            int64_t look = tile - 1;
-            uint32_t spins = 0;
-            bool done = false;
-            while (!done) {
-                uint64_t w[kLookBatch];
-#pragma unroll
-                for (int j = 0; j < kLookBatch; ++j)
-                    w[j] = (look - j >= 0) ? lb_load(status + (look - j) * kBins + d)
-                                           : lb_word(want, kFlagPrefix, 0u);
-                int used = 0;
-                bool stop = false;
-#pragma unroll
-                for (int j = 0; j < kLookBatch; ++j) {
-                    if (!stop) {
-                        const uint64_t flag = (w[j] >> 32) & 3ull;
-                        if ((uint32_t)(w[j] >> 34) != want || flag == 0ull) {
-                            stop = true;
-                        } else {
-                            excl += (uint32_t)w[j];
-                            used = j + 1;
-                            if (flag == kFlagPrefix) {
-                                done = true;
-                                stop = true;
-                            }
-                        }
-                    }
-                }
-                look -= used;
-                if (!done && used < kLookBatch) {
-                    // every earlier tile is resident (it holds a smaller
-                    // ticket) and publishes without waiting; the bound only
-                    // guards against a broken invariant, turning it into a
-                    // reported error
-                    if (++spins > (1u << 22)) {
-                        raise_internal(ctl, kSiteRadixWait);
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                }
-            }
-            lb_store(status + tile * kBins + d,
-                     lb_word(tag, kFlagPrefix, excl + tile_count));
-        }
-        s_delta[d] = (int32_t)(global_excl + excl) - (int32_t)local_excl;
     }
     __syncthreads();
 
@@ -246,7 +255,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     const int64_t valid_n = (m - tile_base) < kSortTile ? (m - tile_base) : kSortTile;
     for (int p = tid; p < valid_n; p += kSortThreads) {
         const uint32_t k = s_keys[p];
-        const int64_t dest = (int64_t)s_delta[(k >> shift) & (kBins - 1)] + p;
+        const int64_t dest = (int64_t)s_delta[k & (kBins - 1)] + p;
         if (dest >= 0 && dest < m) {
             keys_out[dest] = k;
             vals_out[dest] = s_vals[p];
@@ -256,17 +265,14 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     }
 }
 
-hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, const uint32_t* vals_in,
-                             uint32_t* keys_out, uint32_t* vals_out, int64_t m, int pass,
-                             int bits, const uint32_t* hist, uint64_t* status, uint32_t tag,
-                             const uint32_t* gate, uint32_t* bstart, hipStream_t s) {
+hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
+                             uint32_t* vals_out, int64_t m, int bits, const uint32_t* hist,
+                             const uint32_t* tprefix, uint32_t* bstart, hipStream_t s) {
     const int64_t tiles = (m + kSortTile - 1) / kSortTile;
     if (tiles == 0) return hipSuccess;
-    if (pass < 0 || pass >= kMaxPasses) return hipErrorInvalidValue;
 #define HUGE_RADIX_LAUNCH(B)                                                                  \
     hipLaunchKernelGGL(k_radix_pass<B>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ctl, \
-                       &ctl->tickets[pass], keys_in, vals_in, keys_out, vals_out, m, pass,    \
-                       hist + pass * kMaxBins, status, tag, gate, bstart)
+                       keys_in, keys_out, vals_out, m, hist, tprefix, bstart)
     switch (bits) {
         case 8: HUGE_RADIX_LAUNCH(8); break;
         case 9: HUGE_RADIX_LAUNCH(9); break;

@@ -78,30 +78,20 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 }
 
 // ---------------------------------------------------------------------------
-// Per-call set-up: clear the call's flag, the tile tickets, the counts of the
-// repeated-row lists and the digit histograms (a kernel rather than a memset
-// so that the sequence stays valid inside a captured graph).
+// Per-call set-up: clear the call's flag and the counts of the repeated-row
+// lists (a kernel rather than a memset so that the sequence stays valid
+// inside a captured graph).
 // ---------------------------------------------------------------------------
-__global__ void k_begin(Control* ctl, uint32_t* hist) {
-    const int t = threadIdx.x;
-    if (hist != nullptr)
-        for (int i = t; i < kMaxPasses * kMaxBins; i += blockDim.x) hist[i] = 0u;
-    if (t == 0) {
+__global__ void k_begin(Control* ctl) {
+    if (threadIdx.x == 0) {
         ctl->step_bad = 0u;
-        for (int p = 0; p < kMaxPasses; ++p) ctl->tickets[p] = 0u;
         ctl->n_short = ctl->n_piece = ctl->n_comb = ctl->n_part = 0u;
     }
 }
 
-hipError_t launch_begin(Control* ctl, uint32_t* hist, hipStream_t s) {
-    hipLaunchKernelGGL(k_begin, dim3(1), dim3(kBlock), 0, s, ctl, hist);
+hipError_t launch_begin(Control* ctl, hipStream_t s) {
+    hipLaunchKernelGGL(k_begin, dim3(1), dim3(64), 0, s, ctl);
     return hipGetLastError();
-}
-
-__global__ __launch_bounds__(kBlock) void k_clear_u64(uint64_t* p, int64_t words) {
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < words;
-         i += (int64_t)gridDim.x * kBlock)
-        p[i] = 0ull;
 }
 
 __global__ __launch_bounds__(kBlock) void k_fill_i32(int32_t* p, int32_t v, int64_t n) {
@@ -118,13 +108,6 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
-    int64_t blocks = (words + kBlock - 1) / kBlock;
-    if (blocks > 4096) blocks = 4096;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_clear_u64, dim3((unsigned)blocks), dim3(kBlock), 0, s, status, words);
-    return hipGetLastError();
-}
 
 // ---------------------------------------------------------------------------
 // Validation, negatives and sort keys.  A workgroup takes kSamplePos
@@ -136,33 +119,21 @@ hipError_t launch_clear_status(uint64_t* status, int64_t words, hipStream_t s) {
 //   - one thread per negative, consecutive threads on consecutive (i, k), so
 //     that the stores of a wave are contiguous, draws negative k of positive
 //     i into neg[i K + k] and, with keys, handles slot 2 + k.
-// Handling a slot with keys (keys != nullptr): write keys[o], set info[o] = -1
-// (the grouping overwrites repeated ones) and count the digits of every
-// radix pass (digit ps = bits [ps * bits, (ps + 1) * bits) of the key,
-// counted at hist[ps * kMaxBins + digit]).  Without src only negatives are
-// drawn.
+// Handling a slot with keys (keys != nullptr): write keys[o] and set
+// info[o] = -1 (the grouping overwrites repeated ones).  Without src only
+// negatives are drawn.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, StepArgs a,
                                                    int32_t* __restrict__ neg,
                                                    uint32_t* __restrict__ keys,
-                                                   int32_t* __restrict__ info,
-                                                   uint32_t* __restrict__ hist, int passes,
-                                                   int bits) {
-    __shared__ uint32_t s_hist[kMaxPasses * kMaxBins];
+                                                   int32_t* __restrict__ info) {
     const bool with_keys = keys != nullptr;
-    const uint32_t dmask = (1u << bits) - 1u;
-    if (with_keys) {
-        for (int j = threadIdx.x; j < passes * kMaxBins; j += kBlock) s_hist[j] = 0u;
-        __syncthreads();
-    }
     const int64_t K = t.K, S = 2 + K;
     const int64_t i0 = (int64_t)blockIdx.x * kSamplePos;
     const int64_t np = a.n - i0 < kSamplePos ? a.n - i0 : kSamplePos;  // positives here
     auto put = [&](int64_t o, uint32_t key) {
         keys[o] = key;
         info[o] = -1;
-        for (int ps = 0; ps < passes; ++ps)
-            atomicAdd(&s_hist[ps * kMaxBins + ((key >> (ps * bits)) & dmask)], 1u);
     };
     if (a.src != nullptr) {
         for (int64_t j = threadIdx.x; j < np; j += kBlock) {
@@ -199,23 +170,15 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
             ++q;
         }
     }
-    if (with_keys) {
-        __syncthreads();
-        for (int j = threadIdx.x; j < passes * kMaxBins; j += kBlock) {
-            const uint32_t c = s_hist[j];
-            if (c) atomicAdd(&hist[j], c);
-        }
-    }
 }
 
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, int32_t* info, uint32_t* hist, SortPlan plan,
-                         hipStream_t s) {
+                         uint32_t* keys, int32_t* info, hipStream_t s) {
     const int64_t blocks = (a.n + kSamplePos - 1) / kSamplePos;
     if (blocks == 0) return hipSuccess;
     if (t.K < 1 || t.K > kBlock) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
-                       info, hist, keys ? plan.passes : 0, plan.bits);
+                       info);
     return hipGetLastError();
 }
 
