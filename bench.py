@@ -31,6 +31,7 @@ KERNEL = "k_fused_step"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "fused_step_sbm100m_counters.txt")
 KERNEL_SOURCES = ["paper_2307_14490_amd/csrc/device.hpp", "paper_2307_14490_amd/csrc/k_step.hip"]
 KERNEL_END = "int64_t fused_step_blocks("  # the fused kernel's source ends before this line
+PROFILE_EVERY = 4  # timed steps whose fused kernel is bracketed by HIP events
 
 
 def kernel_source_hash() -> str:
@@ -222,8 +223,6 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--sequential", action="store_true",
                     help="one stream, huge_train_step per step (no overlap of grouping)")
-    ap.add_argument("--pipeline", default="side", choices=["alternate", "side"],
-                    help="streams of the overlapped steps (see run_steps)")
     ap.add_argument("--no-phases", action="store_true",
                     help="diagnostic: no per-phase HIP events in the timed steps (no roofline)")
     ap.add_argument("--producer", action="store_true",
@@ -281,34 +280,32 @@ def main():
             pos += n
             per_batch_stats[b] = tr.stats()
 
-    side = torch.cuda.Stream()  # default priority, like the current stream
-    streams = [stream, side]
+    # default priority, like the current stream
+    sides = [torch.cuda.Stream(), torch.cuda.Stream()]
 
     def run_steps(count, first_batch, pos):
         """`count` steps.  Pipelined: batch k+1 is prepared before batch k is
-        applied.  With --pipeline side (default), every batch is prepared on
-        `side` and applied on the current stream: the library issues batch
-        k+1's radix pass on the apply stream just before batch k's update, and
-        its grouping on `side`, beside that update.  With --pipeline
-        alternate, batch k is prepared and applied on streams[k % 2]."""
+        applied on the current stream.  Batches are prepared on two side
+        streams in turn: the library issues batch k+1's radix pass on the
+        apply stream just before batch k's update and its grouping on batch
+        k+1's side stream, beside that update, so batch k+2's sampling (on the
+        other side stream) does not queue behind that grouping."""
         if args.sequential:
             for k in range(count):
                 s, d, c = dev_batches[(first_batch + k) % R]
                 tr.step_no_loss(s, d, c, pos, cfg.lr)
                 pos += n
             return pos
-        alt = args.pipeline == "alternate"
-        gstream = (lambda k: streams[k % 2]) if alt else (lambda k: side)
-        astream = (lambda k: streams[k % 2]) if alt else (lambda k: stream)
         s, d, c = dev_batches[first_batch % R]
-        tr.prepare(s, d, c, pos, stream=gstream(0))
+        tr.prepare(s, d, c, pos, stream=sides[first_batch % 2])
         pos += n
         for k in range(count):
             if k + 1 < count:
-                s, d, c = dev_batches[(first_batch + k + 1) % R]
-                tr.prepare(s, d, c, pos, stream=gstream(k + 1))
+                b = first_batch + k + 1
+                s, d, c = dev_batches[b % R]
+                tr.prepare(s, d, c, pos, stream=sides[b % 2])
                 pos += n
-            tr.train_prepared(cfg.lr, with_loss=False, stream=astream(k))
+            tr.train_prepared(cfg.lr, with_loss=False, stream=stream)
         return pos
 
     pos = run_steps(args.warmup, 0, pos)
@@ -316,16 +313,20 @@ def main():
         raise RuntimeError("device reported an error during warm-up")
     log("[bench] warm-up done")
 
-    # Timed region: exactly K steps; phase events recorded inside the library.
+    # Timed region: exactly K steps; phase events recorded inside the library
+    # around the fused kernel of every PROFILE_EVERY-th step (each event is a
+    # queue packet that costs a few microseconds of its step).
     if not args.no_phases:
-        tr.profile_begin(args.steps)  # events around the fused kernel only
+        tr.profile_begin(-(-args.steps // PROFILE_EVERY), every=PROFILE_EVERY)
     torch.cuda.synchronize()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
-    side.wait_event(ev0)
+    for sd in sides:
+        sd.wait_event(ev0)
     pos = run_steps(args.steps, args.warmup, pos)
-    stream.wait_stream(side)  # the last apply may run on either stream
+    for sd in sides:
+        stream.wait_stream(sd)  # groupings issued for batches past the last one
     ev1.record(stream)
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
@@ -371,7 +372,8 @@ def main():
     n_diag = min(50, args.steps)
     tr.profile_begin(n_diag, all_phases=True)
     pos = run_steps(n_diag, args.warmup + args.steps, pos)
-    stream.wait_stream(side)
+    for sd in sides:
+        stream.wait_stream(sd)
     diag_ms, diag_steps = tr.profile_end()
     phase_avg_us = {p: diag_ms[i] / max(diag_steps, 1) * 1e3 for i, p in enumerate(phases)}
 
@@ -417,7 +419,7 @@ def main():
             "lr": cfg.lr,
             "staged_batches": R,
             "grouping": ("sequential" if args.sequential else
-                         f"overlapped with the previous apply ({args.pipeline} streams)"),
+                         "overlapped with the previous apply (two side streams in turn)"),
         },
         "roofline": {
             "kernel": KERNEL if args.scatter == "sorted" else "k_atomic_gather",
@@ -428,6 +430,8 @@ def main():
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
             "avg_kernel_us": fused_us,
+            "timed_launches": prof_steps,
+            "timing": f"HIP events around the fused kernel of every {PROFILE_EVERY}th timed step",
             "alg_bytes_per_launch": kernel_bytes,
             "probe": {
                 "achieved": probe_gbps,

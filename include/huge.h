@@ -198,21 +198,24 @@ huge_status huge_check(huge_handle* h, void* stream);
 huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
                             int64_t* unique_ctx, int64_t* dup_occurrences);
 
-/* Phase timing.  After huge_profile_begin(h, max_steps, all_phases), each
-   of the next max_steps batches (prepared, or stepped with huge_train_step)
-   records HIP events on the streams its stages run on: around the fused
-   kernel only (all_phases = 0), or at every phase boundary (all_phases = 1;
-   each event is one more packet in a stream, which costs a few
-   microseconds of every step).  huge_profile_end waits for all of them on
-   `stream`, writes the summed durations in milliseconds to
-   phase_ms[HUGE_PHASES] (0 for phases not recorded) and the number of
-   recorded steps to *steps, and releases the events.  Phases: 0 set-up and
-   negative sampling, 1 the radix pass, 2 the per-bucket grouping (1 and 2
-   are empty for the atomic scatter), 3 the fused gather/loss/update kernel
-   (atomic scatter: gather and coefficients), 4 repeated rows (atomic
-   scatter: the atomic adds), 5 loss sum. */
+/* Phase timing.  After huge_profile_begin(h, max_steps, all_phases, every),
+   every every-th one of the next batches (prepared, or stepped with
+   huge_train_step), max_steps of them, records HIP events on the streams
+   its stages run on: around the fused kernel only (all_phases = 0), or at
+   every phase boundary (all_phases = 1).  Each event is one more packet in
+   a stream, which costs a few microseconds of the step it is in; every > 1
+   spreads that cost.  huge_profile_end waits for all of them on `stream`,
+   writes the summed durations in milliseconds to phase_ms[HUGE_PHASES] (0
+   for phases not recorded) and the number of recorded steps to *steps, and
+   releases the events.  Phases: 0 set-up and negative sampling, 1 the radix
+   pass, 2 the per-bucket grouping (1 and 2 are empty for the atomic
+   scatter), 3 the fused gather/loss/update kernel (atomic scatter: gather
+   and coefficients), 4 repeated rows (atomic scatter: the atomic adds), 5
+   loss sum.  Errors: max_steps or every outside [1, 10^6], all_phases not
+   0 or 1. */
 #define HUGE_PHASES 6
-huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases);
+huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases,
+                               int32_t every);
 huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int32_t* steps);
 
 /* ------------------------------------------------------------------------

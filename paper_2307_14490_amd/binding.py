@@ -97,7 +97,7 @@ def load() -> ctypes.CDLL:
     L.huge_check.argtypes = [_vp, _vp]
     L.huge_step_stats.argtypes = [_vp, _vp, ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
-    L.huge_profile_begin.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32]
+    L.huge_profile_begin.argtypes = [_vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
     L.huge_profile_end.argtypes = [_vp, _vp, ctypes.POINTER(ctypes.c_double),
                                    ctypes.POINTER(ctypes.c_int32)]
     wcfgp = ctypes.POINTER(HugeWalkConfig)
@@ -269,8 +269,9 @@ class Trainer:
                                    ctypes.byref(c)), "huge_step_stats")
         return a.value, b.value, c.value
 
-    def profile_begin(self, max_steps, all_phases=False):
-        _ok(load().huge_profile_begin(self._h, int(max_steps), int(bool(all_phases))),
+    def profile_begin(self, max_steps, all_phases=False, every=1):
+        """Events on every `every`-th one of the next batches, max_steps of them."""
+        _ok(load().huge_profile_begin(self._h, int(max_steps), int(bool(all_phases)), int(every)),
             "huge_profile_begin")
 
     def profile_end(self, stream=None):

@@ -74,7 +74,8 @@ struct huge_handle {
     // phase timing
     std::vector<hipEvent_t> prof_ev;
     std::vector<char> prof_applied;
-    int32_t prof_max = 0, prof_next = 0;
+    int32_t prof_max = 0, prof_next = 0;  // batches to profile; profiled so far
+    int32_t prof_every = 1, prof_seen = 0;  // every prof_every-th batch; batches seen
     bool prof_all = false;     // events at every phase boundary, not only the fused kernel
     // the stream each kind of stage last used, so that a wait on an event of
     // the same stream is skipped (the stream orders it already)
@@ -203,7 +204,8 @@ void release_profile(huge_handle* h) {
         if (e) (void)hipEventDestroy(e);
     h->prof_ev.clear();
     h->prof_applied.clear();
-    h->prof_max = h->prof_next = 0;
+    h->prof_max = h->prof_next = h->prof_seen = 0;
+    h->prof_every = 1;
 }
 
 void destroy_handle(huge_handle* h) {
@@ -252,8 +254,11 @@ huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* t
     for (int s = 0; s < kSlots; ++s)
         h->sampled[s] = h->radixed[s] = h->ready[s] = h->done[s] = nullptr;
     for (int s = 0; s < kSlots; ++s) {
+        // the events order streams of this device only: a device-scope
+        // release suffices (the default one is system-scope)
         for (hipEvent_t* e : {&h->sampled[s], &h->radixed[s], &h->ready[s], &h->done[s]}) {
-            if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) {
+            if (hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventReleaseToDevice) !=
+                hipSuccess) {
                 *e = nullptr;
                 destroy_handle(h);
                 return HUGE_ERR_HIP;
@@ -315,7 +320,11 @@ huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
     b.n = n;
     b.first_pos = first_pos;
     b.gstream = s;
-    b.prof = h->prof_next < h->prof_max ? h->prof_next++ : -1;
+    b.prof = -1;
+    if (h->prof_next < h->prof_max) {
+        if (h->prof_seen % h->prof_every == 0) b.prof = h->prof_next++;
+        h->prof_seen += 1;
+    }
     // the slot's previous apply must be complete before its buffers change
     HIP_TRY(wait_on(s, h->done[slot], h->slot_apply_stream[slot]));
     if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
@@ -703,15 +712,18 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
     return HUGE_OK;
 }
 
-huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases) {
+huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases,
+                               int32_t every) {
     if (!h || max_steps < 1 || max_steps > 1000000) return HUGE_ERR_INVALID_ARG;
     if (all_phases != 0 && all_phases != 1) return HUGE_ERR_INVALID_ARG;
+    if (every < 1 || every > 1000000) return HUGE_ERR_INVALID_ARG;
     release_profile(h);
     h->prof_all = all_phases != 0;
+    h->prof_every = every;
     h->prof_ev.assign((size_t)max_steps * kProfEvents, nullptr);
     h->prof_applied.assign((size_t)max_steps, 0);
     for (hipEvent_t& e : h->prof_ev) {
-        if (hipEventCreate(&e) != hipSuccess) {
+        if (hipEventCreateWithFlags(&e, hipEventReleaseToDevice) != hipSuccess) {
             e = nullptr;
             release_profile(h);
             return HUGE_ERR_HIP;
