@@ -530,3 +530,80 @@ int oracle_sample_walks(const int64_t *off, const int32_t *nbr, int64_t num_node
     if (rc != OR_OK) return rc;
     return out > capacity ? OR_ECAP : OR_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Evaluation pairs (Sec. 4's unsupervised metrics: the edge SNR compares    */
+/* distances over edges with distances over a random sub-sample of the       */
+/* non-edges).  Pair j of the edge sample takes Philox counter               */
+/* (lo32 j, hi32 j, 0, 0x80000001): edge index e = floor(x E / 2^64) with     */
+/* x = (r1 << 32) | r0 over the E directed edges of the CSR lists, and the   */
+/* pair is (the row whose list holds e, nbr[e]).  Pair j of the non-edge     */
+/* sample tries a = 0 .. max_tries - 1 with counter (lo32 j, hi32 j, a,      */
+/* 0x80000002): u = floor(x0 N / 2^64), v = floor(x1 N / 2^64) with           */
+/* x0 = (r1 << 32) | r0 and x1 = (r3 << 32) | r2, and keeps the first try     */
+/* with u != v and v not in u's list; with none, the pair is (-1, -1).        */
+/* Output: edge pairs at 0 .. n_edge - 1, non-edge pairs after them.          */
+/* ------------------------------------------------------------------------- */
+static uint64_t mul_hi_u64(uint64_t x, uint64_t n) {
+    return (uint64_t)(((unsigned __int128)x * (unsigned __int128)n) >> 64);
+}
+
+int oracle_eval_pairs(const int64_t *off, const int32_t *nbr, int64_t num_nodes,
+                      int64_t num_edges, uint64_t seed, int64_t n_edge, int64_t n_non,
+                      int32_t max_tries, int32_t *u_out, int32_t *v_out) {
+    if (!off || num_nodes < 1 || num_edges < 0 || n_edge < 0 || n_non < 0 || max_tries < 1 ||
+        (num_edges > 0 && !nbr) || (n_edge + n_non > 0 && (!u_out || !v_out)) ||
+        (n_edge > 0 && num_edges == 0) || off[0] != 0 || off[num_nodes] != num_edges)
+        return OR_EINVAL;
+    uint32_t key[2], ctr[4], r[4];
+    seed_key(seed, key);
+    for (int64_t j = 0; j < n_edge; ++j) {
+        ctr[0] = (uint32_t)((uint64_t)j & 0xFFFFFFFFu);
+        ctr[1] = (uint32_t)((uint64_t)j >> 32);
+        ctr[2] = 0u;
+        ctr[3] = 0x80000001u;
+        oracle_philox4x32_10(ctr, key, r);
+        const uint64_t x = ((uint64_t)r[1] << 32) | (uint64_t)r[0];
+        const int64_t e = (int64_t)mul_hi_u64(x, (uint64_t)num_edges);
+        /* the row whose list holds e: the last row with off[row] <= e, by
+           bisection over the non-decreasing offsets */
+        int64_t lo = 0, hi = num_nodes;  /* off[lo] <= e < off[hi] */
+        while (hi - lo > 1) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            if (off[mid] <= e) lo = mid; else hi = mid;
+        }
+        const int32_t v = nbr[e];
+        if (v < 0 || v >= num_nodes) return OR_ERANGE;
+        u_out[j] = (int32_t)lo;
+        v_out[j] = v;
+    }
+    for (int64_t j = 0; j < n_non; ++j) {
+        int32_t pu = -1, pv = -1;
+        for (int32_t a = 0; a < max_tries; ++a) {
+            ctr[0] = (uint32_t)((uint64_t)j & 0xFFFFFFFFu);
+            ctr[1] = (uint32_t)((uint64_t)j >> 32);
+            ctr[2] = (uint32_t)a;
+            ctr[3] = 0x80000002u;
+            oracle_philox4x32_10(ctr, key, r);
+            const uint64_t x0 = ((uint64_t)r[1] << 32) | (uint64_t)r[0];
+            const uint64_t x1 = ((uint64_t)r[3] << 32) | (uint64_t)r[2];
+            const int64_t u = (int64_t)mul_hi_u64(x0, (uint64_t)num_nodes);
+            const int64_t v = (int64_t)mul_hi_u64(x1, (uint64_t)num_nodes);
+            if (u == v) continue;
+            int is_edge = 0;
+            for (int64_t q = off[u]; q < off[u + 1]; ++q) {
+                if (nbr[q] == v) {
+                    is_edge = 1;
+                    break;
+                }
+            }
+            if (is_edge) continue;
+            pu = (int32_t)u;
+            pv = (int32_t)v;
+            break;
+        }
+        u_out[n_edge + j] = pu;
+        v_out[n_edge + j] = pv;
+    }
+    return OR_OK;
+}

@@ -10,6 +10,10 @@ library) and adds numpy glue:
   by seed (Sec. 3.2, Alg. 1);
 * :func:`lwsgd_lr`     -- the LWSGD learning-rate schedule (Table 2), as the
   piecewise-linear curve through its knots;
+* :func:`eval_pairs`, :func:`pair_distances`, :func:`eval_summary`,
+  :func:`knn`, :func:`recall_at_k` -- the unsupervised embedding metrics of
+  Sec. 4 (edge SNR, edge and non-edge distance percentiles, sampled edge
+  recall) on L2-normalised rows;
 * :func:`step_sparse`  -- the same step on the rows a batch touches only, with
   every other row left at its initial value.  Tables too large for host memory
   (up to 1e8 x 128 floats) are represented by the rows the batch reads; each
@@ -84,8 +88,11 @@ def lib():
                                           ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
                                           ctypes.c_int64, _i32p, _i32p, _i32p, _i32p,
                                           ctypes.c_int64, _i64p]
+        L.oracle_eval_pairs.argtypes = [_i64p, _i32p, ctypes.c_int64, ctypes.c_int64,
+                                        ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64,
+                                        ctypes.c_int32, _i32p, _i32p]
         for name in ("oracle_init_rows", "oracle_build_alias", "oracle_sample_negatives",
-                     "oracle_sample_walks",
+                     "oracle_sample_walks", "oracle_eval_pairs",
                      "oracle_sgns_grad_d", "oracle_sgns_loss_d", "oracle_sgns_step",
                      "oracle_sgns_loss"):
             getattr(L, name).restype = ctypes.c_int
@@ -316,3 +323,114 @@ def sample_walks(off, nbr, num_nodes: int, walks_per_node: int, walk_steps: int,
                                _ptr(hist, _i32p), n, ctypes.byref(count))
     _check(rc, "oracle_sample_walks")
     return src, dst, cc, hist
+
+
+# --------------------------------------------------------------------------- #
+# Embedding evaluation (Sec. 4, unsupervised metrics)
+#
+# Readings: embeddings are L2-normalised and compared by Euclidean distance
+# (values in [0, 2], the range of the paper's distance plots); a row of zeros
+# stays zero.  SNR = mean non-edge distance / mean edge distance over the
+# sampled pairs.  Percentiles interpolate linearly between order statistics.
+# recall@k(u) = |N(u) & S| / k, S = the k rows v != u nearest to u (ties:
+# smaller id first), N(u) = the distinct ids in u's list other than u.
+# --------------------------------------------------------------------------- #
+def eval_pairs(off, nbr, num_nodes: int, seed: int, n_edge: int, n_non: int,
+               max_tries: int = 64):
+    """Edge pairs, then non-edge pairs (see oracle_eval_pairs): (u, v) int32."""
+    off = _c(off, np.int64)
+    nbr = _c(nbr, np.int32)
+    u = np.empty(n_edge + n_non, np.int32)
+    v = np.empty(n_edge + n_non, np.int32)
+    _check(lib().oracle_eval_pairs(_ptr(off, _i64p), _ptr(nbr, _i32p), int(num_nodes),
+                                   int(nbr.size), int(seed), int(n_edge), int(n_non),
+                                   int(max_tries), _ptr(u, _i32p), _ptr(v, _i32p)),
+           "eval_pairs")
+    return u, v
+
+
+def normalize_rows(X) -> np.ndarray:
+    """Rows divided by their Euclidean norm, in double; zero rows stay zero."""
+    X = np.asarray(X, dtype=np.float64)
+    nrm = np.sqrt(np.sum(X * X, axis=1))
+    out = np.zeros_like(X)
+    nz = nrm > 0
+    out[nz] = X[nz] / nrm[nz, None]
+    return out
+
+
+def pair_distances(table, u, v) -> np.ndarray:
+    """|x_u / |x_u| - x_v / |x_v|| in double; NaN where u or v is negative."""
+    u = np.asarray(u, np.int64)
+    v = np.asarray(v, np.int64)
+    out = np.full(u.size, np.nan)
+    ok = (u >= 0) & (v >= 0)
+    a = normalize_rows(np.asarray(table)[u[ok]])
+    b = normalize_rows(np.asarray(table)[v[ok]])
+    out[ok] = np.sqrt(np.sum((a - b) ** 2, axis=1))
+    return out
+
+
+def percentile_linear(values, q: float) -> float:
+    """The q-th percentile (0 <= q <= 100) of the values: sorted, position
+    h = (n - 1) q / 100, linear between the order statistics around h."""
+    x = np.sort(np.asarray(values, dtype=np.float64))
+    n = x.size
+    if n == 0:
+        return float("nan")
+    h = (n - 1) * (q / 100.0)
+    lo = int(np.floor(h))
+    hi = min(lo + 1, n - 1)
+    return float(x[lo] + (h - lo) * (x[hi] - x[lo]))
+
+
+@dataclass
+class EvalSummary:
+    count_edge: int
+    count_non: int
+    mean_edge: float
+    mean_non: float
+    snr: float
+    pct_edge: list
+    pct_non: list
+
+
+def eval_summary(d_edge, d_non, quantiles) -> EvalSummary:
+    """Means over the non-NaN distances, their ratio, and percentiles."""
+    e = np.asarray(d_edge, np.float64)
+    e = e[~np.isnan(e)]
+    m = np.asarray(d_non, np.float64)
+    m = m[~np.isnan(m)]
+    me = float(np.sum(e) / e.size) if e.size else float("nan")
+    mn = float(np.sum(m) / m.size) if m.size else float("nan")
+    return EvalSummary(int(e.size), int(m.size), me, mn, mn / me if e.size and m.size else
+                       float("nan"), [percentile_linear(e, q) for q in quantiles],
+                       [percentile_linear(m, q) for q in quantiles])
+
+
+def knn(table, queries, k: int):
+    """For each query u: the k ids v != u with the smallest distance between
+    the normalised rows (ties: smaller id), and those distances."""
+    Xn = normalize_rows(table)
+    ids = np.arange(Xn.shape[0])
+    out_ids = np.empty((len(queries), k), np.int64)
+    out_d = np.empty((len(queries), k))
+    for qi, u in enumerate(queries):
+        d = np.sqrt(np.sum((Xn - Xn[u]) ** 2, axis=1))
+        keep = ids != u
+        order = np.lexsort((ids[keep], d[keep]))[:k]
+        out_ids[qi] = ids[keep][order]
+        out_d[qi] = d[keep][order]
+    return out_ids, out_d
+
+
+def recall_at_k(off, nbr, queries, nearest, k: int) -> np.ndarray:
+    """|N(u) & S| / k per query, S = the first k ids of its row of `nearest`."""
+    off = np.asarray(off, np.int64)
+    nbr = np.asarray(nbr)
+    out = np.empty(len(queries))
+    for qi, u in enumerate(queries):
+        nb = set(int(x) for x in nbr[off[u]:off[u + 1]]) - {int(u)}
+        S = set(int(x) for x in np.asarray(nearest[qi])[:k])
+        out[qi] = len(nb & S) / k
+    return out
