@@ -276,6 +276,84 @@ huge_status huge_sample_walks(const huge_walk_config* cfg, const int64_t* d_offs
                               int32_t* d_status, void* d_workspace, size_t ws_bytes,
                               void* stream);
 
+/* ------------------------------------------------------------------------
+   Unsupervised evaluation of an embedding table (Sec. 4): rows are
+   L2-normalised (a row of zeros stays zero) and compared by the Euclidean
+   distance d(u, v) = |x_u/|x_u| - x_v/|x_v||, in [0, 2].
+     edge SNR        = mean d over sampled non-edges / mean d over sampled
+                       edges, with percentiles of both distributions;
+     recall@k(u)     = |N(u) & S| / k, S = the k rows v != u nearest to u
+                       (ties: smaller id), N(u) = the ids of u's list other
+                       than u.
+   The calls take no handle and work on any table: N rows of `dim` floats,
+   row-major (dim a multiple of 4, 4 .. 1024).  CSR graphs: N + 1 int64
+   offsets, non-decreasing from 0 to num_edges, and num_edges int32
+   neighbour ids in [0, N); each node's list must be in ascending order (the
+   non-edge test and the recall search it).  d_status (device int32)
+   receives 0, or -2 when a device-side check fails (an id or offset out of
+   range); affected outputs are then NaN or -1.  All calls are asynchronous
+   on `stream`; host-detectable argument errors return before any launch. */
+
+/* Bytes of device workspace huge_eval_summary (up to max_pairs distances)
+   and huge_eval_knn (a table of num_rows x dim, k nearest) need; 0 if the
+   sizes are out of range. */
+size_t huge_eval_workspace_bytes(int64_t max_pairs, int64_t num_rows, int32_t dim, int32_t k);
+
+/* n_edge edge pairs, then n_non non-edge pairs, into d_u[n_edge + n_non],
+   d_v[...] (device int32).  Edge pair j draws the Philox counter
+   (lo32 j, hi32 j, 0, 0x80000001) under key (lo32 seed, hi32 seed): edge
+   index e = floor(x num_edges / 2^64), x = (r1 << 32) | r0, and the pair is
+   (the node whose list holds e, d_neighbors[e]).  Non-edge pair j tries
+   a = 0 .. max_tries - 1 with counter (lo32 j, hi32 j, a, 0x80000002):
+   u = floor(x0 N / 2^64), v = floor(x1 N / 2^64), x0 = (r1 << 32) | r0,
+   x1 = (r3 << 32) | r2, and keeps the first try with u != v and v not in
+   u's list; if none qualifies the pair is (-1, -1).  Errors: n_edge > 0 with
+   num_edges = 0, negative counts, max_tries < 1. */
+huge_status huge_eval_pairs(const int64_t* d_offsets, const int32_t* d_neighbors,
+                            int64_t num_nodes, int64_t num_edges, uint64_t seed, int64_t n_edge,
+                            int64_t n_non, int32_t max_tries, int32_t* d_u, int32_t* d_v,
+                            int32_t* d_status, void* stream);
+
+/* d_dist[i] = d(d_u[i], d_v[i]) (device float), NaN where either id is
+   negative (a failed non-edge draw); an id >= num_rows sets -2. */
+huge_status huge_eval_distances(const float* d_table, int64_t num_rows, int32_t dim,
+                                const int32_t* d_u, const int32_t* d_v, int64_t n,
+                                float* d_dist, int32_t* d_status, void* stream);
+
+/* Summary of n_edge edge distances followed by n_non non-edge distances
+   (device float, NaN = no pair), into d_out (device double):
+     d_out[0], d_out[1]  number of valid edge / non-edge distances
+     d_out[2], d_out[3]  their means (fixed-order double sums)
+     d_out[4]            edge SNR = d_out[3] / d_out[2]
+     d_out[5 .. 5+nq)    percentiles of the edge distances at h_quantiles
+     d_out[5+nq .. 5+2nq) the same for the non-edge distances
+   Percentile q (0 .. 100, host doubles, at most 128 of them) of n values:
+   sorted, position h = (n - 1) q / 100, linear between the order
+   statistics around h.  Means, SNR and percentiles are NaN for an empty
+   set.  Needs huge_eval_workspace_bytes(n_edge + n_non, ...) of workspace. */
+huge_status huge_eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non,
+                              const double* h_quantiles, int32_t n_quantiles, double* d_out,
+                              void* d_workspace, size_t ws_bytes, void* stream);
+
+/* The k rows nearest to each of the n_queries query rows (ids in d_queries),
+   excluding the query itself: d_ids[q k + t] (device int32, ascending
+   (distance, id); -1 if fewer than k other rows exist) and d_dist[...]
+   (device float).  Distances are computed in fp32 on the matrix cores from
+   the expansion d^2 = |q|^2 + |r|^2 - 2 <q, r> of the normalised rows.
+   1 <= k <= 32; dim <= 512.  Queries are processed in passes of up to
+   128 (dim <= 128), 64 (dim <= 256) or 32 over the table. */
+huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
+                          const int32_t* d_queries, int32_t n_queries, int32_t k,
+                          int32_t* d_ids, float* d_dist, void* d_workspace, size_t ws_bytes,
+                          int32_t* d_status, void* stream);
+
+/* d_recall[q] = recall@k of query d_queries[q] (device double) from its k
+   nearest rows d_ids[q k ..] (as huge_eval_knn writes them); 1 <= k <= 64. */
+huge_status huge_eval_recall(const int64_t* d_offsets, const int32_t* d_neighbors,
+                             int64_t num_nodes, int64_t num_edges, const int32_t* d_queries,
+                             int32_t n_queries, const int32_t* d_ids, int32_t k,
+                             double* d_recall, int32_t* d_status, void* stream);
+
 void huge_destroy(huge_handle* h);
 const char* huge_status_string(huge_status s);
 

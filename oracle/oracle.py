@@ -410,17 +410,18 @@ def eval_summary(d_edge, d_non, quantiles) -> EvalSummary:
 
 def knn(table, queries, k: int):
     """For each query u: the k ids v != u with the smallest distance between
-    the normalised rows (ties: smaller id), and those distances."""
+    the normalised rows (ties: smaller id), and those distances; with fewer
+    than k other rows, the missing places hold id -1 and distance NaN."""
     Xn = normalize_rows(table)
     ids = np.arange(Xn.shape[0])
-    out_ids = np.empty((len(queries), k), np.int64)
-    out_d = np.empty((len(queries), k))
+    out_ids = np.full((len(queries), k), -1, np.int64)
+    out_d = np.full((len(queries), k), np.nan)
     for qi, u in enumerate(queries):
         d = np.sqrt(np.sum((Xn - Xn[u]) ** 2, axis=1))
         keep = ids != u
         order = np.lexsort((ids[keep], d[keep]))[:k]
-        out_ids[qi] = ids[keep][order]
-        out_d[qi] = d[keep][order]
+        out_ids[qi, :order.size] = ids[keep][order]
+        out_d[qi, :order.size] = d[keep][order]
     return out_ids, out_d
 
 

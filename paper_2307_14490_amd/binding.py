@@ -32,6 +32,8 @@ EXPORTED = [
     "huge_train_step", "huge_prepare_step", "huge_train_prepared", "huge_eval_loss",
     "huge_get_rows", "huge_sample_negatives", "huge_probe_rows", "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
     "huge_destroy", "huge_status_string", "huge_walk_workspace_bytes", "huge_sample_walks",
+    "huge_eval_workspace_bytes", "huge_eval_pairs", "huge_eval_distances", "huge_eval_summary",
+    "huge_eval_knn", "huge_eval_recall",
 ]
 HUGE_PHASES = 6
 
@@ -107,6 +109,18 @@ def load() -> ctypes.CDLL:
                                     ctypes.c_int64, _vp, _vp, _vp, _vp, ctypes.c_int64, _vp, _vp,
                                     _vp, ctypes.c_size_t, _vp]
     L.huge_sample_walks.restype = ctypes.c_int32
+    i64, i32, u64, szt = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    L.huge_eval_workspace_bytes.argtypes = [i64, i64, i32, i32]
+    L.huge_eval_workspace_bytes.restype = szt
+    L.huge_eval_pairs.argtypes = [_vp, _vp, i64, i64, u64, i64, i64, i32, _vp, _vp, _vp, _vp]
+    L.huge_eval_distances.argtypes = [_vp, i64, i32, _vp, _vp, i64, _vp, _vp, _vp]
+    L.huge_eval_summary.argtypes = [_vp, i64, i64, ctypes.POINTER(ctypes.c_double), i32, _vp,
+                                    _vp, szt, _vp]
+    L.huge_eval_knn.argtypes = [_vp, i64, i32, _vp, i32, i32, _vp, _vp, _vp, szt, _vp, _vp]
+    L.huge_eval_recall.argtypes = [_vp, _vp, i64, i64, _vp, i32, _vp, i32, _vp, _vp, _vp]
+    for name in ("huge_eval_pairs", "huge_eval_distances", "huge_eval_summary", "huge_eval_knn",
+                 "huge_eval_recall"):
+        getattr(L, name).restype = ctypes.c_int32
     L.huge_destroy.argtypes = [_vp]
     L.huge_destroy.restype = None
     L.huge_status_string.argtypes = [ctypes.c_int32]
@@ -347,3 +361,93 @@ def sample_walks(offsets, neighbors, num_nodes, walks_per_node, walk_steps, wind
         raise HugeError(st, "huge_sample_walks (device)")
     got = int(count.item())
     return src[:got], dst[:got], cc[:got], (hist[:got] if hist is not None else None)
+
+
+# --------------------------------------------------------------------------- #
+# Embedding evaluation (argument marshalling for the huge_eval_* calls)
+# --------------------------------------------------------------------------- #
+class Evaluator:
+    """Workspace and status word for the huge_eval_* calls on one table shape.
+    Each method checks the device status word after its call (synchronising
+    the stream) and raises HugeError on a device-detected error."""
+
+    def __init__(self, num_rows, dim, max_pairs, k=10, device="cuda"):
+        import torch
+        L = load()
+        self.num_rows, self.dim, self.k = int(num_rows), int(dim), int(k)
+        self.ws_bytes = L.huge_eval_workspace_bytes(int(max_pairs), self.num_rows, self.dim,
+                                                    self.k)
+        if self.ws_bytes == 0:
+            raise HugeError(HUGE_ERR_INVALID_ARG, "huge_eval_workspace_bytes")
+        self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
+        self._ws_ptr = self._ws.data_ptr() + ((-self._ws.data_ptr()) % 256)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        self.device = device
+
+    def _check(self, what):
+        st = int(self.status.item())
+        if st != 0:
+            raise HugeError(st, what + " (device)")
+
+    def pairs(self, offsets, neighbors, num_nodes, seed, n_edge, n_non, max_tries=64,
+              stream=None):
+        """(u, v) int32 device tensors: n_edge edge pairs, then n_non non-edges."""
+        import torch
+        n = int(n_edge) + int(n_non)
+        u = torch.empty(n, dtype=torch.int32, device=self.device)
+        v = torch.empty(n, dtype=torch.int32, device=self.device)
+        _ok(load().huge_eval_pairs(_dptr(offsets), _dptr(neighbors), int(num_nodes),
+                                   int(neighbors.numel()), int(seed), int(n_edge), int(n_non),
+                                   int(max_tries), _dptr(u), _dptr(v), _dptr(self.status),
+                                   _stream_ptr(stream)), "huge_eval_pairs")
+        self._check("huge_eval_pairs")
+        return u, v
+
+    def distances(self, table, u, v, stream=None):
+        import torch
+        d = torch.empty(u.numel(), dtype=torch.float32, device=self.device)
+        _ok(load().huge_eval_distances(_dptr(table), table.shape[0], table.shape[1], _dptr(u),
+                                       _dptr(v), u.numel(), _dptr(d), _dptr(self.status),
+                                       _stream_ptr(stream)), "huge_eval_distances")
+        self._check("huge_eval_distances")
+        return d
+
+    def summary(self, dist, n_edge, n_non, quantiles=(0, 10, 25, 50, 75, 90, 100), stream=None):
+        """dict: count_edge, count_non, mean_edge, mean_non, snr, pct_edge, pct_non."""
+        import torch
+        q = (ctypes.c_double * len(quantiles))(*[float(x) for x in quantiles])
+        nq = len(quantiles)
+        out = torch.empty(5 + 2 * nq, dtype=torch.float64, device=self.device)
+        _ok(load().huge_eval_summary(_dptr(dist), int(n_edge), int(n_non), q, nq, _dptr(out),
+                                     self._ws_ptr, self.ws_bytes, _stream_ptr(stream)),
+            "huge_eval_summary")
+        o = out.cpu().tolist()
+        return {"count_edge": int(o[0]), "count_non": int(o[1]), "mean_edge": o[2],
+                "mean_non": o[3], "snr": o[4], "pct_edge": o[5:5 + nq],
+                "pct_non": o[5 + nq:5 + 2 * nq]}
+
+    def knn(self, table, queries, k=None, stream=None):
+        """(ids int32 [nq, k], dist float32 [nq, k]) of the nearest rows."""
+        import torch
+        k = self.k if k is None else int(k)
+        if k > self.k:
+            raise HugeError(HUGE_ERR_INVALID_ARG, "Evaluator.knn: k above the workspace's")
+        nq = queries.numel()
+        ids = torch.empty((nq, k), dtype=torch.int32, device=self.device)
+        dist = torch.empty((nq, k), dtype=torch.float32, device=self.device)
+        _ok(load().huge_eval_knn(_dptr(table), table.shape[0], table.shape[1], _dptr(queries),
+                                 nq, k, _dptr(ids), _dptr(dist), self._ws_ptr, self.ws_bytes,
+                                 _dptr(self.status), _stream_ptr(stream)), "huge_eval_knn")
+        self._check("huge_eval_knn")
+        return ids, dist
+
+    def recall(self, offsets, neighbors, num_nodes, queries, ids, stream=None):
+        import torch
+        nq, k = ids.shape
+        out = torch.empty(nq, dtype=torch.float64, device=self.device)
+        _ok(load().huge_eval_recall(_dptr(offsets), _dptr(neighbors), int(num_nodes),
+                                    int(neighbors.numel()), _dptr(queries), int(nq), _dptr(ids),
+                                    int(k), _dptr(out), _dptr(self.status),
+                                    _stream_ptr(stream)), "huge_eval_recall")
+        self._check("huge_eval_recall")
+        return out

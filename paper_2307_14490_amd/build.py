@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libhuge.so")
 BUILD = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.hip", "k_tables.hip", "k_sort.hip", "k_step.hip", "k_atomic.hip", "k_walk.hip",
+SOURCES = ["api.hip", "k_tables.hip", "k_sort.hip", "k_step.hip", "k_atomic.hip", "k_walk.hip", "k_eval.hip",
            "alias.cpp"]
 ARCH = "gfx950"
 

@@ -335,7 +335,7 @@ huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
                           sorted ? at<int32_t>(h, SL.info) : nullptr, s));
     if (sorted) {
         const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-        HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, h->plan.bits,
+        HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, h->plan.bits, 0,
                                   at<uint32_t>(h, SL.tcount), s));
         HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, h->plan.bits,
                                  at<uint32_t>(h, SL.tprefix), hist, s));
@@ -359,7 +359,7 @@ huge_status stage_radix(huge_handle* h, int slot, hipStream_t s) {
     HIP_TRY(wait_on(s, h->sampled[slot], b.stage_stream));
     if (!prof_mark(h, b, 2, s)) return HUGE_ERR_HIP;
     HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1),
-                              at<uint32_t>(h, SL.vals1), m, h->plan.bits,
+                              at<uint32_t>(h, SL.vals1), m, h->plan.bits, 0,
                               at<uint32_t>(h, SL.hist), at<uint32_t>(h, SL.tprefix),
                               at<uint32_t>(h, SL.bstart), s));
     if (!prof_mark(h, b, 3, s)) return HUGE_ERR_HIP;
@@ -767,6 +767,186 @@ huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int
     *steps = counted;
     release_profile(h);
     return st;
+}
+
+// ---------------------------------------------------------------------------
+// Embedding evaluation.  The summary and the nearest-row search each lay out
+// their regions from the start of the caller's workspace (calls on a stream
+// run one after the other).
+// ---------------------------------------------------------------------------
+namespace {
+
+struct SummaryLayout {
+    size_t ctrl, keys_a, keys_b, tcount, tprefix, hist, part, total;
+};
+
+SummaryLayout summary_layout(int64_t max_pairs) {
+    SummaryLayout L;
+    const size_t n = (size_t)(max_pairs > 0 ? max_pairs : 1);
+    const size_t tiles = (n + kSortTile - 1) / kSortTile;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align_up(off + bytes);
+        return at;
+    };
+    L.ctrl = take(sizeof(Control));
+    L.keys_a = take(sizeof(uint32_t) * n);
+    L.keys_b = take(sizeof(uint32_t) * n);
+    L.tcount = take(sizeof(uint32_t) * tiles * kMaxBins);
+    L.tprefix = take(sizeof(uint32_t) * tiles * kMaxBins);
+    L.hist = take(sizeof(uint32_t) * kMaxBins);
+    L.part = take(sizeof(double) * kEvalSumBlocks * 4);
+    L.total = off;
+    return L;
+}
+
+struct KnnLayout {
+    size_t qn, qn2, qid, partial, total;
+};
+
+KnnLayout knn_layout(int64_t num_rows, int32_t dim, int32_t k) {
+    KnnLayout L;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align_up(off + bytes);
+        return at;
+    };
+    L.qn = take(sizeof(float) * kKnnPass * (size_t)dim);
+    L.qn2 = take(sizeof(float) * kKnnPass);
+    L.qid = take(sizeof(int32_t) * kKnnPass);
+    // the most lists: one query block, every wave its own list
+    L.partial = take(sizeof(uint64_t) * (size_t)knn_lists(num_rows, 1) * kKnnPass * (size_t)k);
+    L.total = off;
+    return L;
+}
+
+bool eval_table_ok(int64_t num_rows, int32_t dim) {
+    return num_rows >= 1 && num_rows <= 0x7FFFFFFF && dim >= 4 && dim <= kMaxDim && dim % 4 == 0;
+}
+
+bool eval_graph_ok(int64_t num_nodes, int64_t num_edges) {
+    return num_nodes >= 1 && num_nodes <= 0x7FFFFFFF && num_edges >= 0;
+}
+
+}  // namespace
+
+size_t huge_eval_workspace_bytes(int64_t max_pairs, int64_t num_rows, int32_t dim, int32_t k) {
+    if (max_pairs < 0 || max_pairs > 0x7FFFFFFF || !eval_table_ok(num_rows, dim) || k < 1 ||
+        k > kKnnMaxK)
+        return 0;
+    const size_t a = summary_layout(max_pairs).total;
+    const size_t b = knn_layout(num_rows, dim, k).total;
+    return a > b ? a : b;
+}
+
+huge_status huge_eval_pairs(const int64_t* d_offsets, const int32_t* d_neighbors,
+                            int64_t num_nodes, int64_t num_edges, uint64_t seed, int64_t n_edge,
+                            int64_t n_non, int32_t max_tries, int32_t* d_u, int32_t* d_v,
+                            int32_t* d_status, void* stream) {
+    if (!d_offsets || !d_status || !eval_graph_ok(num_nodes, num_edges) || n_edge < 0 ||
+        n_non < 0 || max_tries < 1 || (n_edge > 0 && num_edges == 0) ||
+        (num_edges > 0 && !d_neighbors) || n_edge + n_non > 0x7FFFFFFF ||
+        (n_edge + n_non > 0 && (!d_u || !d_v)))
+        return HUGE_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(launch_eval_status_clear(d_status, s));
+    HIP_TRY(launch_eval_pairs(d_offsets, d_neighbors, num_nodes, num_edges, seed, n_edge, n_non,
+                              max_tries, d_u, d_v, d_status, s));
+    return HUGE_OK;
+}
+
+huge_status huge_eval_distances(const float* d_table, int64_t num_rows, int32_t dim,
+                                const int32_t* d_u, const int32_t* d_v, int64_t n,
+                                float* d_dist, int32_t* d_status, void* stream) {
+    if (!d_table || !d_status || !eval_table_ok(num_rows, dim) || n < 0 ||
+        (n > 0 && (!d_u || !d_v || !d_dist)))
+        return HUGE_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(launch_eval_status_clear(d_status, s));
+    HIP_TRY(launch_eval_dist(d_table, num_rows, dim, d_u, d_v, n, d_dist, d_status, s));
+    return HUGE_OK;
+}
+
+huge_status huge_eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non,
+                              const double* h_quantiles, int32_t n_quantiles, double* d_out,
+                              void* d_workspace, size_t ws_bytes, void* stream) {
+    if (n_edge < 0 || n_non < 0 || n_edge + n_non > 0x7FFFFFFF || !d_out || !d_workspace ||
+        n_quantiles < 0 || n_quantiles > kEvalMaxQuantiles || (n_quantiles > 0 && !h_quantiles) ||
+        (n_edge + n_non > 0 && !d_dist))
+        return HUGE_ERR_INVALID_ARG;
+    for (int32_t i = 0; i < n_quantiles; ++i)
+        if (!(h_quantiles[i] >= 0.0 && h_quantiles[i] <= 100.0)) return HUGE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(d_workspace) % kAlign != 0) return HUGE_ERR_WORKSPACE;
+    const SummaryLayout L = summary_layout(n_edge + n_non);
+    if (ws_bytes < L.total) return HUGE_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
+    Control* ctl = reinterpret_cast<Control*>(ws + L.ctrl);
+    uint32_t* ka = reinterpret_cast<uint32_t*>(ws + L.keys_a);
+    uint32_t* kb = reinterpret_cast<uint32_t*>(ws + L.keys_b);
+    uint32_t* tcount = reinterpret_cast<uint32_t*>(ws + L.tcount);
+    uint32_t* tprefix = reinterpret_cast<uint32_t*>(ws + L.tprefix);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
+    double* part = reinterpret_cast<double*>(ws + L.part);
+    HIP_TRY(launch_begin(ctl, s));
+    HIP_TRY(launch_eval_sums(d_dist, n_edge, n_edge + n_non, part, d_out, s));
+    // each set sorted by its float bit patterns: four stable passes of 8 bits
+    const int64_t first[2] = {0, n_edge};
+    const int64_t count[2] = {n_edge, n_non};
+    for (int set = 0; set < 2; ++set) {
+        const int64_t m = count[set];
+        HIP_TRY(launch_eval_keys(d_dist + first[set], m, ka, s));
+        for (int pass = 0; pass < 4; ++pass) {
+            uint32_t* src = pass % 2 == 0 ? ka : kb;
+            uint32_t* dst = pass % 2 == 0 ? kb : ka;
+            HIP_TRY(launch_tile_count(ctl, src, m, 8, 8 * pass, tcount, s));
+            HIP_TRY(launch_tile_scan(ctl, tcount, m, 8, tprefix, hist, s));
+            HIP_TRY(launch_radix_pass(ctl, src, dst, nullptr, m, 8, 8 * pass, hist, tprefix,
+                                      nullptr, s));
+        }
+        HIP_TRY(launch_eval_quantiles(ka, d_out + set, h_quantiles, n_quantiles,
+                                      d_out + 5 + set * n_quantiles, s));
+    }
+    return HUGE_OK;
+}
+
+huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
+                          const int32_t* d_queries, int32_t n_queries, int32_t k,
+                          int32_t* d_ids, float* d_dist, void* d_workspace, size_t ws_bytes,
+                          int32_t* d_status, void* stream) {
+    if (!d_table || !d_status || !eval_table_ok(num_rows, dim) || n_queries < 0 || k < 1 ||
+        k > kKnnMaxK || knn_pass_queries(dim) < 32 || !d_workspace ||
+        (n_queries > 0 && (!d_queries || !d_ids || !d_dist)))
+        return HUGE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(d_workspace) % kAlign != 0) return HUGE_ERR_WORKSPACE;
+    const KnnLayout L = knn_layout(num_rows, dim, k);
+    if (ws_bytes < L.total) return HUGE_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(launch_eval_status_clear(d_status, s));
+    if (n_queries == 0) return HUGE_OK;
+    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
+    HIP_TRY(launch_knn(d_table, num_rows, dim, d_queries, n_queries, k, d_ids, d_dist,
+                       reinterpret_cast<float*>(ws + L.qn), reinterpret_cast<float*>(ws + L.qn2),
+                       reinterpret_cast<int32_t*>(ws + L.qid),
+                       reinterpret_cast<uint64_t*>(ws + L.partial), d_status, s));
+    return HUGE_OK;
+}
+
+huge_status huge_eval_recall(const int64_t* d_offsets, const int32_t* d_neighbors,
+                             int64_t num_nodes, int64_t num_edges, const int32_t* d_queries,
+                             int32_t n_queries, const int32_t* d_ids, int32_t k,
+                             double* d_recall, int32_t* d_status, void* stream) {
+    if (!d_offsets || !d_status || !eval_graph_ok(num_nodes, num_edges) || n_queries < 0 ||
+        k < 1 || k > 64 || (num_edges > 0 && !d_neighbors) ||
+        (n_queries > 0 && (!d_queries || !d_ids || !d_recall)))
+        return HUGE_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(launch_eval_status_clear(d_status, s));
+    HIP_TRY(launch_eval_recall(d_offsets, d_neighbors, num_nodes, num_edges, d_queries, n_queries,
+                               d_ids, k, d_recall, d_status, s));
+    return HUGE_OK;
 }
 
 void huge_destroy(huge_handle* h) { destroy_handle(h); }

@@ -29,6 +29,15 @@ constexpr int kGroupChunk = kBlock * kGroupItems;     // 2048 keys per chunk
 constexpr int kTableBitsMin = 12;      // 4096 slots: 36 KB of LDS per workgroup
 constexpr int kTableBitsMax = 14;      // 16384 slots: 144 KB of LDS per workgroup
 constexpr int kBitmapBits = 18;        // two 32 KB bitmaps (seen, repeated)
+// Embedding evaluation
+constexpr int kEvalMaxQuantiles = 128;  // percentiles per summary
+constexpr int kKnnWaves = 4;            // waves of a nearest-row workgroup
+constexpr int kKnnMaxK = 32;            // nearest rows per query, at most
+constexpr int kKnnDimChunk = 128;       // dimensions per MFMA pass over a row tile
+constexpr int kKnnQueryFloats = 16896;  // LDS floats for the queries of a pass (66 KB)
+constexpr int kKnnPass = 128;           // queries per pass over the table, at most
+constexpr int kKnnGrid = 256;           // nearest-row workgroups (one per CU)
+constexpr int kKnnMergeCap = 8192;      // keys sorted together by the merge
 constexpr uint32_t kShortRun = 32;     // repeated rows with at most this many occurrences are
                                        // summed by one thread group
 constexpr uint32_t kPiece = 256;       // occurrences summed by one workgroup task
@@ -203,16 +212,18 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 hipError_t launch_begin(Control* ctl, hipStream_t s);
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
                          uint32_t* keys, int32_t* info, hipStream_t s);
-// Bucketing of m keys by their lowest `bits` bits in tiles of kSortTile:
+// Bucketing of m keys by `bits` bits at `shift` in tiles of kSortTile:
 // per-tile digit counts, their sums over earlier tiles and the bucket sizes
-// (hist), then the stable scatter into bucket order.
-hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits,
+// (hist), then the stable scatter into bucket order (one pass of an LSD
+// radix sort).
+hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits, int shift,
                              uint32_t* tcount, hipStream_t s);
 hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int bits,
                             uint32_t* tprefix, uint32_t* hist, hipStream_t s);
 hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
-                             uint32_t* vals_out, int64_t m, int bits, const uint32_t* hist,
-                             const uint32_t* tprefix, uint32_t* bstart, hipStream_t s);
+                             uint32_t* vals_out, int64_t m, int bits, int shift,
+                             const uint32_t* hist, const uint32_t* tprefix, uint32_t* bstart,
+                             hipStream_t s);
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
                         uint4* shorts, uint4* pieces, uint4* combs, ListCaps caps,
@@ -233,6 +244,28 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_walks(const WalkArgs& A, uint32_t* counts, uint64_t* offsets, int64_t* total,
                         int64_t capacity, int32_t* src, int32_t* dst, int32_t* cc, int32_t* hist,
                         int32_t* status, hipStream_t s);
+// Embedding evaluation (k_eval.hip)
+hipError_t launch_eval_status_clear(int32_t* status, hipStream_t s);
+hipError_t launch_eval_pairs(const int64_t* off, const int32_t* nbr, int64_t N, int64_t E,
+                             uint64_t seed, int64_t n_edge, int64_t n_non, int32_t max_tries,
+                             int32_t* u, int32_t* v, int32_t* status, hipStream_t s);
+hipError_t launch_eval_dist(const float* T, int64_t N, int32_t D, const int32_t* u,
+                            const int32_t* v, int64_t n, float* out, int32_t* status,
+                            hipStream_t s);
+constexpr int kEvalSumBlocks = 256;
+hipError_t launch_eval_sums(const float* d, int64_t n_edge, int64_t n, double* part, double* out,
+                            hipStream_t s);
+hipError_t launch_eval_keys(const float* d, int64_t n, uint32_t* keys, hipStream_t s);
+hipError_t launch_eval_quantiles(const uint32_t* sorted, const double* cnt, const double* q,
+                                 int nq, double* out, hipStream_t s);
+int knn_pass_queries(int D);
+int64_t knn_lists(int64_t N, int QB);
+hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, int32_t nq,
+                      int32_t k, int32_t* ids, float* dist, float* qn, float* qn2, int32_t* qid,
+                      uint64_t* partial, int32_t* status, hipStream_t s);
+hipError_t launch_eval_recall(const int64_t* off, const int32_t* nbr, int64_t N, int64_t E,
+                              const int32_t* q, int32_t nq, const int32_t* ids, int32_t k,
+                              double* out, int32_t* status, hipStream_t s);
 hipError_t launch_loss_final(Control* ctl, const double* lossp, int64_t blocks, double* out,
                              hipStream_t s);
 hipError_t launch_atomic_gather(const TableArgs& t, Control* ctl, const StepArgs& a,

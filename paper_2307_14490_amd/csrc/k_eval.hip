@@ -1,0 +1,629 @@
+// Unsupervised evaluation of an embedding table (HUGE Sec. 4): the rows are
+// L2-normalised and compared by Euclidean distance;
+//   - edge SNR: mean distance over a random sample of non-edges divided by the
+//     mean over a sample of edges, with the distribution of both (percentiles);
+//   - sampled edge recall: for a few query nodes u, the k rows nearest to u
+//     form S, and recall@k(u) = |N(u) & S| / k.
+// Kernels:
+//   k_eval_pairs    edge and non-edge pairs from counter-based Philox draws
+//   k_eval_dist     distances of normalised rows, G lanes per pair
+//   k_eval_sums     per-block double sums and counts of the valid distances;
+//   k_eval_final    their fixed-order totals, the means and the SNR;
+//   k_eval_quantile percentiles of the sorted distances (sorted by the radix
+//                   kernels of k_sort.hip on the float bit patterns);
+//   k_knn_queries   the normalised query rows;
+//   k_knn_tiles     distances of every row to every query by fp32 MFMA
+//                   (32 queries x 32 rows per tile), per-wave top-k lists;
+//   k_knn_merge     the k nearest of each query over all lists (bitonic sort);
+//   k_eval_recall   recall@k from the nearest rows and the sorted CSR lists.
+#include "common.hpp"
+#include "device.hpp"
+#include "dispatch.hpp"
+
+namespace huge {
+
+__device__ __forceinline__ void eval_fail(int32_t* status, int32_t code) {
+    atomicCAS(status, 0, code);
+}
+
+// The row whose list holds edge e: the last row r with off[r] <= e, by
+// bisection over the offsets (off[0] = 0 <= e < off[N] = E).
+__device__ __forceinline__ int64_t edge_row(const int64_t* __restrict__ off, int64_t N,
+                                            int64_t e) {
+    int64_t lo = 0, hi = N;
+    while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (off[mid] <= e)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// Whether v is in the ascending list nbr[b, e).
+__device__ __forceinline__ bool in_sorted_list(const int32_t* __restrict__ nbr, int64_t b,
+                                               int64_t e, int32_t v) {
+    while (b < e) {
+        const int64_t mid = b + (e - b) / 2;
+        const int32_t x = nbr[mid];
+        if (x == v) return true;
+        if (x < v)
+            b = mid + 1;
+        else
+            e = mid;
+    }
+    return false;
+}
+
+// ---------------------------------------------------------------------------
+// Pairs.  Edge pair j: Philox counter (lo32 j, hi32 j, 0, kEdgeWord), edge
+// index floor(x E / 2^64) with x = (r1 << 32) | r0, the pair (its row, its
+// neighbour).  Non-edge pair j: tries a = 0 .. max_tries - 1 with counter
+// (lo32 j, hi32 j, a, kNonEdgeWord), u = floor(x0 N / 2^64), v =
+// floor(x1 N / 2^64) (x0 = (r1 << 32) | r0, x1 = (r3 << 32) | r2); the first
+// try with u != v and v not in u's list, else (-1, -1).
+// ---------------------------------------------------------------------------
+constexpr uint32_t kEdgeWord = 0x80000001u;
+constexpr uint32_t kNonEdgeWord = 0x80000002u;
+
+__global__ __launch_bounds__(kBlock) void k_eval_pairs(
+    const int64_t* __restrict__ off, const int32_t* __restrict__ nbr, int64_t N, int64_t E,
+    uint64_t seed, int64_t n_edge, int64_t n_non, int32_t max_tries, int32_t* __restrict__ u_out,
+    int32_t* __restrict__ v_out, int32_t* __restrict__ status) {
+    const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (j >= n_edge + n_non) return;
+    const uint32_t klo = (uint32_t)seed, khi = (uint32_t)(seed >> 32);
+    int32_t pu = -1, pv = -1;
+    if (j < n_edge) {
+        const uint4 r = philox4x32_10(make_uint4((uint32_t)j, (uint32_t)((uint64_t)j >> 32), 0u,
+                                                 kEdgeWord), klo, khi);
+        const uint64_t x = ((uint64_t)r.y << 32) | r.x;
+        const int64_t e = (int64_t)__umul64hi(x, (uint64_t)E);
+        const int64_t row = edge_row(off, N, e);
+        const int32_t v = nbr[e];
+        if (off[row] <= e && e < off[row + 1] && v >= 0 && (int64_t)v < N) {
+            pu = (int32_t)row;
+            pv = v;
+        } else {
+            eval_fail(status, -2);
+        }
+    } else {
+        const int64_t jj = j - n_edge;
+        for (int32_t a = 0; a < max_tries; ++a) {
+            const uint4 r = philox4x32_10(
+                make_uint4((uint32_t)jj, (uint32_t)((uint64_t)jj >> 32), (uint32_t)a,
+                           kNonEdgeWord), klo, khi);
+            const int64_t u = (int64_t)__umul64hi(((uint64_t)r.y << 32) | r.x, (uint64_t)N);
+            const int64_t v = (int64_t)__umul64hi(((uint64_t)r.w << 32) | r.z, (uint64_t)N);
+            if (u == v) continue;
+            const int64_t b = off[u], e = off[u + 1];
+            if (b < 0 || e < b || e > E) {
+                eval_fail(status, -2);
+                break;
+            }
+            if (in_sorted_list(nbr, b, e, (int32_t)v)) continue;
+            pu = (int32_t)u;
+            pv = (int32_t)v;
+            break;
+        }
+    }
+    u_out[j] = pu;
+    v_out[j] = pv;
+}
+
+hipError_t launch_eval_pairs(const int64_t* off, const int32_t* nbr, int64_t N, int64_t E,
+                             uint64_t seed, int64_t n_edge, int64_t n_non, int32_t max_tries,
+                             int32_t* u, int32_t* v, int32_t* status, hipStream_t s) {
+    const int64_t n = n_edge + n_non;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_eval_pairs, dim3((unsigned)((n + kBlock - 1) / kBlock)), dim3(kBlock),
+                       0, s, off, nbr, N, E, seed, n_edge, n_non, max_tries, u, v, status);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Distances: |x_u / |x_u| - x_v / |x_v||, G lanes per pair and C float4 per
+// lane (a zero row stays zero); NaN for a pair with a negative id.
+// ---------------------------------------------------------------------------
+template <int G, int C>
+__global__ __launch_bounds__(kBlock) void k_eval_dist(const float* __restrict__ T, int64_t N,
+                                                      int32_t D, const int32_t* __restrict__ u,
+                                                      const int32_t* __restrict__ v, int64_t n,
+                                                      float* __restrict__ out,
+                                                      int32_t* __restrict__ status) {
+    const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t p = t / G;  // groups are aligned in the wave and exit together
+    const int g = (int)(t % G);
+    if (p >= n) return;
+    const int32_t a = u[p], b = v[p];
+    if (a < 0 || b < 0) {
+        if (g == 0) out[p] = __builtin_nanf("");
+        return;
+    }
+    if ((int64_t)a >= N || (int64_t)b >= N) {
+        if (g == 0) {
+            out[p] = __builtin_nanf("");
+            eval_fail(status, -2);
+        }
+        return;
+    }
+    const int q4 = D / 4;
+    const float4* xa = reinterpret_cast<const float4*>(T + (int64_t)a * D);
+    const float4* xb = reinterpret_cast<const float4*>(T + (int64_t)b * D);
+    float4 ra[C], rb[C];
+    float na = 0.f, nb = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const int idx = g + G * c;
+        ra[c] = idx < q4 ? xa[idx] : make_float4(0.f, 0.f, 0.f, 0.f);
+        rb[c] = idx < q4 ? xb[idx] : make_float4(0.f, 0.f, 0.f, 0.f);
+        na += ra[c].x * ra[c].x + ra[c].y * ra[c].y + ra[c].z * ra[c].z + ra[c].w * ra[c].w;
+        nb += rb[c].x * rb[c].x + rb[c].y * rb[c].y + rb[c].z * rb[c].z + rb[c].w * rb[c].w;
+    }
+    na = group_sum<G>(na);
+    nb = group_sum<G>(nb);
+    const float ia = na > 0.f ? 1.0f / sqrtf(na) : 0.f;
+    const float ib = nb > 0.f ? 1.0f / sqrtf(nb) : 0.f;
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const float dx = ra[c].x * ia - rb[c].x * ib, dy = ra[c].y * ia - rb[c].y * ib;
+        const float dz = ra[c].z * ia - rb[c].z * ib, dw = ra[c].w * ia - rb[c].w * ib;
+        s += dx * dx + dy * dy + dz * dz + dw * dw;
+    }
+    s = group_sum<G>(s);
+    if (g == 0) out[p] = sqrtf(s);
+}
+
+hipError_t launch_eval_dist(const float* T, int64_t N, int32_t D, const int32_t* u,
+                            const int32_t* v, int64_t n, float* out, int32_t* status,
+                            hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    const RowShape rs = row_shape(D);
+    const int64_t threads = n * rs.G;
+    const dim3 grid((unsigned)((threads + kBlock - 1) / kBlock));
+    HUGE_ROW_DISPATCH(rs, hipLaunchKernelGGL((k_eval_dist<G_, C_>), grid, dim3(kBlock), 0, s, T,
+                                             N, D, u, v, n, out, status));
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Summary of n_edge edge distances followed by n_non non-edge distances:
+// counts and sums of the non-NaN values per block (fixed tree order), then
+// out[0..4] = count_edge, count_non, mean_edge, mean_non, mean_non / mean_edge.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_eval_sums(const float* __restrict__ d, int64_t n_edge,
+                                                      int64_t n, double* __restrict__ part) {
+    __shared__ double s_v[4][kBlock];
+    double se = 0.0, sn = 0.0, ce = 0.0, cn = 0.0;
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kBlock) {
+        const float x = d[i];
+        if (x != x) continue;
+        if (i < n_edge) {
+            se += x;
+            ce += 1.0;
+        } else {
+            sn += x;
+            cn += 1.0;
+        }
+    }
+    s_v[0][threadIdx.x] = se;
+    s_v[1][threadIdx.x] = sn;
+    s_v[2][threadIdx.x] = ce;
+    s_v[3][threadIdx.x] = cn;
+    __syncthreads();
+    for (int w = kBlock / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w)
+            for (int c = 0; c < 4; ++c) s_v[c][threadIdx.x] += s_v[c][threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x < 4) part[blockIdx.x * 4 + threadIdx.x] = s_v[threadIdx.x][0];
+}
+
+__global__ void k_eval_final(const double* __restrict__ part, int blocks, double* __restrict__ out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    double t[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int b = 0; b < blocks; ++b)
+        for (int c = 0; c < 4; ++c) t[c] += part[b * 4 + c];
+    const double nan = __builtin_nan("");
+    const double me = t[2] > 0.0 ? t[0] / t[2] : nan;
+    const double mn = t[3] > 0.0 ? t[1] / t[3] : nan;
+    out[0] = t[2];
+    out[1] = t[3];
+    out[2] = me;
+    out[3] = mn;
+    out[4] = (t[2] > 0.0 && t[3] > 0.0) ? mn / me : nan;
+}
+
+// Percentile q of the `count` smallest values of the ascending keys (the
+// valid distances; NaN bit patterns sort after them): position
+// h = (count - 1) q / 100, linear between the order statistics around h.
+struct Quantiles {
+    double q[kEvalMaxQuantiles];
+};
+
+__global__ void k_eval_quantile(const uint32_t* __restrict__ sorted, const double* __restrict__ cnt,
+                                Quantiles Q, int nq, double* __restrict__ out) {
+    const int i = threadIdx.x;
+    if (i >= nq) return;
+    const int64_t count = (int64_t)*cnt;
+    if (count <= 0) {
+        out[i] = __builtin_nan("");
+        return;
+    }
+    const double h = (double)(count - 1) * (Q.q[i] / 100.0);
+    int64_t lo = (int64_t)floor(h);
+    if (lo < 0) lo = 0;
+    if (lo > count - 1) lo = count - 1;
+    const int64_t hi = lo + 1 < count ? lo + 1 : count - 1;
+    const double a = (double)__uint_as_float(sorted[lo]);
+    const double b = (double)__uint_as_float(sorted[hi]);
+    out[i] = a + (h - (double)lo) * (b - a);
+}
+
+hipError_t launch_eval_sums(const float* d, int64_t n_edge, int64_t n, double* part, double* out,
+                            hipStream_t s) {
+    hipLaunchKernelGGL(k_eval_sums, dim3(kEvalSumBlocks), dim3(kBlock), 0, s, d, n_edge, n, part);
+    hipLaunchKernelGGL(k_eval_final, dim3(1), dim3(64), 0, s, part, kEvalSumBlocks, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_eval_quantiles(const uint32_t* sorted, const double* cnt, const double* q,
+                                 int nq, double* out, hipStream_t s) {
+    if (nq <= 0) return hipSuccess;
+    if (nq > kEvalMaxQuantiles) return hipErrorInvalidValue;
+    Quantiles Q;
+    for (int i = 0; i < nq; ++i) Q.q[i] = q[i];
+    hipLaunchKernelGGL(k_eval_quantile, dim3(1), dim3(kEvalMaxQuantiles), 0, s, sorted, cnt, Q,
+                       nq, out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Nearest rows of up to kKnnPass queries per pass over the table.
+// ---------------------------------------------------------------------------
+// Normalised query rows qn[j * D ..] (zero for a zero row or a padding slot)
+// and qn2[j] = |qn_j|^2 in {0, 1}.
+__global__ __launch_bounds__(kBlock) void k_knn_queries(const float* __restrict__ T, int64_t N,
+                                                        int32_t D, const int32_t* __restrict__ q,
+                                                        int32_t nq, int32_t nqp,
+                                                        float* __restrict__ qn,
+                                                        float* __restrict__ qn2,
+                                                        int32_t* __restrict__ qid,
+                                                        int32_t* __restrict__ status) {
+    __shared__ float s_red[kBlock];
+    const int j = blockIdx.x;
+    if (j >= nqp) return;
+    int32_t id = j < nq ? q[j] : -1;
+    if (id >= 0 && (int64_t)id >= N) {
+        if (threadIdx.x == 0) eval_fail(status, -2);
+        id = -1;
+    }
+    if (j < nq && id < 0 && q[j] < 0 && threadIdx.x == 0) eval_fail(status, -2);
+    float part = 0.f;
+    for (int c = threadIdx.x; c < D; c += kBlock) {
+        const float x = id >= 0 ? T[(int64_t)id * D + c] : 0.f;
+        part += x * x;
+    }
+    s_red[threadIdx.x] = part;
+    __syncthreads();
+    for (int w = kBlock / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) s_red[threadIdx.x] += s_red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const float n2 = s_red[0];
+    const float inv = n2 > 0.f ? 1.0f / sqrtf(n2) : 0.f;
+    for (int c = threadIdx.x; c < D; c += kBlock)
+        qn[(int64_t)j * D + c] = id >= 0 ? T[(int64_t)id * D + c] * inv : 0.f;
+    if (threadIdx.x == 0) {
+        qn2[j] = n2 > 0.f ? 1.f : 0.f;
+        qid[j] = id;
+    }
+}
+
+typedef float knn_acc16 __attribute__((ext_vector_type(16)));
+
+// One workgroup of kKnnWaves waves; wave w serves query block w % QB (32
+// queries) over tiles t = S, S + NS, ... of 32 rows, S = its list slot.  Per
+// tile: the 32 x 32 dot products of the normalised queries with the raw rows
+// by v_mfma_f32_32x32x2f32 (the K dimension runs over the dimensions in
+// chunks of 128: lane (x, h) supplies row x's dimensions c*128 + h*64 + s and
+// query x's same dimension at step s), the rows' norms from the same
+// registers, then d^2 = |q|^2 + [row != 0] - 2 dot / |row| and the key
+// (bits of d^2) << 32 | row.  Keys below the query's current k-th best are
+// staged per query (at most 32 per tile) and inserted by the query's own lane
+// into its sorted list of k.  Lists go to partial[(S * nqp + q) * k + t].
+struct KnnArgs {
+    const float* T;
+    int64_t N;
+    int32_t D;
+    int32_t k;
+    int32_t nqp;   // queries in this pass, padded to 32 * QB
+    int32_t QB;    // query blocks: 1, 2 or 4
+    int32_t stride;  // LDS floats per query row (D + 4)
+    int64_t tiles;
+    const float* qn;
+    const float* qn2;
+    const int32_t* qid;
+    uint64_t* partial;
+};
+
+constexpr uint64_t kNoKey = ~0ull;
+
+__global__ __launch_bounds__(kKnnWaves * 64) void k_knn_tiles(KnnArgs A) {
+    __shared__ __align__(16) float s_q[kKnnQueryFloats];
+    __shared__ uint64_t s_list[kKnnWaves][32][kKnnMaxK];
+    __shared__ uint64_t s_stage[kKnnWaves][32][32];
+    __shared__ uint64_t s_thr[kKnnWaves][32];
+    __shared__ uint32_t s_cnt[kKnnWaves][32];
+    __shared__ uint32_t s_len[kKnnWaves][32];
+    __shared__ float s_qn2[kKnnPass];
+    __shared__ int32_t s_qid[kKnnPass];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int x = lane & 31, h = lane >> 5;
+    const int D = A.D, k = A.k, stride = A.stride;
+    for (int i = tid; i < kKnnQueryFloats; i += kKnnWaves * 64) s_q[i] = 0.f;
+    __syncthreads();
+    for (int64_t i = tid; i < (int64_t)A.nqp * D; i += kKnnWaves * 64)
+        s_q[(i / D) * stride + (i % D)] = A.qn[i];
+    for (int i = tid; i < A.nqp; i += kKnnWaves * 64) {
+        s_qn2[i] = A.qn2[i];
+        s_qid[i] = A.qid[i];
+    }
+    if (lane < 32) {
+        s_thr[w][lane] = kNoKey;
+        s_cnt[w][lane] = 0u;
+        s_len[w][lane] = 0u;
+    }
+    __syncthreads();
+
+    const int qb = w % A.QB;
+    const int wpb = kKnnWaves / A.QB;  // waves per query block
+    const int64_t S = (int64_t)blockIdx.x * wpb + w / A.QB;
+    const int64_t NS = (int64_t)gridDim.x * wpb;
+    const int nch = (D + kKnnDimChunk - 1) / kKnnDimChunk;
+    const float* qrow = s_q + (qb * 32 + x) * stride;
+
+    for (int64_t t = S; t < A.tiles; t += NS) {
+        const int64_t row = t * 32 + x;
+        const bool row_ok = row < A.N;
+        knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
+                         0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        float nr = 0.f;
+        for (int c = 0; c < nch; ++c) {
+            const int d0 = c * kKnnDimChunk + h * (kKnnDimChunk / 2);
+            float4 bv[kKnnDimChunk / 8];
+            const float4* src = reinterpret_cast<const float4*>(A.T + row * (int64_t)D + d0);
+#pragma unroll
+            for (int m = 0; m < kKnnDimChunk / 8; ++m)
+                bv[m] = (row_ok && d0 + 4 * m < D) ? src[m] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int m = 0; m < kKnnDimChunk / 8; ++m) {
+                nr += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z +
+                      bv[m].w * bv[m].w;
+                const int dd = d0 + 4 * m;
+                float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (dd < D) av = *reinterpret_cast<const float4*>(qrow + dd);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv[m].x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv[m].y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv[m].z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv[m].w, acc, 0, 0, 0);
+            }
+        }
+        nr += __shfl_xor(nr, 32, 64);
+        const float inv = nr > 0.f ? 1.0f / sqrtf(nr) : 0.f;
+        const float nx = nr > 0.f ? 1.f : 0.f;
+        // lane (x, h) holds query i = 8 (r / 4) + 4 h + r % 4 against row x
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int i = 8 * (r / 4) + 4 * h + (r % 4);
+            const int q = qb * 32 + i;
+            float d2 = s_qn2[q] + nx - 2.f * acc[r] * inv;
+            d2 = d2 > 0.f ? d2 : 0.f;
+            const bool ok = row_ok && s_qid[q] >= 0 && row != (int64_t)s_qid[q];
+            const uint64_t key =
+                ok ? (((uint64_t)__float_as_uint(d2) << 32) | (uint64_t)row) : kNoKey;
+            if (key < s_thr[w][i]) {
+                const uint32_t pos = atomicAdd(&s_cnt[w][i], 1u);
+                s_stage[w][i][pos] = key;  // pos < 32: one row per lane x
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        if (h == 0) {
+            const uint32_t c = s_cnt[w][x];
+            if (c > 0u) {
+                uint64_t* L = s_list[w][x];
+                uint32_t len = s_len[w][x];
+                for (uint32_t e = 0; e < c; ++e) {
+                    const uint64_t key = s_stage[w][x][e];
+                    if (len == (uint32_t)k && key >= L[k - 1]) continue;
+                    int p = len < (uint32_t)k ? (int)len : k - 1;
+                    while (p > 0 && L[p - 1] > key) {
+                        L[p] = L[p - 1];
+                        --p;
+                    }
+                    L[p] = key;
+                    if (len < (uint32_t)k) ++len;
+                }
+                s_len[w][x] = len;
+                s_cnt[w][x] = 0u;
+                s_thr[w][x] = len == (uint32_t)k ? L[k - 1] : kNoKey;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+    }
+    if (h == 0) {
+        const uint32_t len = s_len[w][x];
+        uint64_t* dst = A.partial + ((size_t)S * A.nqp + qb * 32 + x) * k;
+        for (int t = 0; t < k; ++t) dst[t] = (uint32_t)t < len ? s_list[w][x][t] : kNoKey;
+    }
+}
+
+// The k smallest keys of query q over all NS lists: running best k plus a
+// chunk of candidates, bitonic-sorted together in LDS.
+__global__ __launch_bounds__(kBlock) void k_knn_merge(const uint64_t* __restrict__ partial,
+                                                      int64_t NS, int32_t nqp, int32_t k,
+                                                      int32_t q_first, int32_t* __restrict__ ids,
+                                                      float* __restrict__ dist) {
+    __shared__ uint64_t s_buf[kKnnMergeCap];
+    const int q = blockIdx.x;
+    const int64_t total = NS * k;
+    for (int i = threadIdx.x; i < k; i += kBlock) s_buf[i] = kNoKey;
+    for (int64_t base = 0; base < total; base += kKnnMergeCap - k) {
+        const int64_t chunk =
+            total - base < kKnnMergeCap - k ? total - base : (int64_t)(kKnnMergeCap - k);
+        for (int i = threadIdx.x; i < kKnnMergeCap - k; i += kBlock) {
+            uint64_t v = kNoKey;
+            if (i < chunk) {
+                const int64_t c = base + i;
+                v = partial[((c / k) * nqp + q) * k + (c % k)];
+            }
+            s_buf[k + i] = v;
+        }
+        __syncthreads();
+        for (int size = 2; size <= kKnnMergeCap; size <<= 1) {
+            for (int st = size >> 1; st > 0; st >>= 1) {
+                for (int i = threadIdx.x; i < kKnnMergeCap / 2; i += kBlock) {
+                    const int lo = 2 * i - (i & (st - 1));
+                    const int hi = lo + st;
+                    const bool up = (lo & size) == 0;
+                    const uint64_t a = s_buf[lo], b = s_buf[hi];
+                    if ((a > b) == up) {
+                        s_buf[lo] = b;
+                        s_buf[hi] = a;
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+    for (int t = threadIdx.x; t < k; t += kBlock) {
+        const uint64_t key = s_buf[t];
+        const int64_t o = (int64_t)(q_first + q) * k + t;
+        ids[o] = key == kNoKey ? -1 : (int32_t)(uint32_t)key;
+        dist[o] = key == kNoKey ? __builtin_nanf("") : sqrtf(__uint_as_float((uint32_t)(key >> 32)));
+    }
+}
+
+int knn_pass_queries(int D) {
+    int qp = kKnnQueryFloats / (D + 4);
+    qp = qp > kKnnPass ? kKnnPass : qp;
+    return (qp / 32) * 32;
+}
+
+int64_t knn_lists(int64_t N, int QB) {
+    const int64_t tiles = (N + 31) / 32;
+    const int wpb = kKnnWaves / QB;
+    int64_t grid = (tiles + wpb - 1) / wpb;
+    grid = grid < kKnnGrid ? grid : kKnnGrid;
+    return grid * wpb;
+}
+
+hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, int32_t nq,
+                      int32_t k, int32_t* ids, float* dist, float* qn, float* qn2, int32_t* qid,
+                      uint64_t* partial, int32_t* status, hipStream_t s) {
+    const int qp = knn_pass_queries(D);
+    if (qp < 32 || k < 1 || k > kKnnMaxK || N < 1) return hipErrorInvalidValue;
+    for (int32_t q0 = 0; q0 < nq; q0 += qp) {
+        const int32_t m = nq - q0 < qp ? nq - q0 : qp;
+        int QB = (m + 31) / 32;
+        if (QB == 3) QB = 4;
+        const int32_t nqp = 32 * QB;
+        hipLaunchKernelGGL(k_knn_queries, dim3((unsigned)nqp), dim3(kBlock), 0, s, T, N, D,
+                           q + q0, m, nqp, qn, qn2, qid, status);
+        KnnArgs A;
+        A.T = T;
+        A.N = N;
+        A.D = D;
+        A.k = k;
+        A.nqp = nqp;
+        A.QB = QB;
+        A.stride = D + 4;
+        A.tiles = (N + 31) / 32;
+        A.qn = qn;
+        A.qn2 = qn2;
+        A.qid = qid;
+        A.partial = partial;
+        const int64_t NS = knn_lists(N, QB);
+        const int64_t grid = NS / (kKnnWaves / QB);
+        hipLaunchKernelGGL(k_knn_tiles, dim3((unsigned)grid), dim3(kKnnWaves * 64), 0, s, A);
+        hipLaunchKernelGGL(k_knn_merge, dim3((unsigned)m), dim3(kBlock), 0, s, partial, NS, nqp,
+                           k, q0, ids, dist);
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// recall@k(u) = |N(u) & S| / k, S = the query's k nearest rows (ids[q k ..]),
+// N(u) = the ids of u's ascending list other than u.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_eval_recall(const int64_t* __restrict__ off,
+                                                    const int32_t* __restrict__ nbr, int64_t N,
+                                                    int64_t E, const int32_t* __restrict__ q,
+                                                    const int32_t* __restrict__ ids, int32_t k,
+                                                    double* __restrict__ out,
+                                                    int32_t* __restrict__ status) {
+    const int qi = blockIdx.x;
+    const int t = threadIdx.x;
+    const int32_t u = q[qi];
+    bool found = false;
+    bool bad = u < 0 || (int64_t)u >= N;
+    int64_t b = 0, e = 0;
+    if (!bad) {
+        b = off[u];
+        e = off[u + 1];
+        bad = b < 0 || e < b || e > E;
+    }
+    if (!bad && t < k) {
+        const int32_t id = ids[(int64_t)qi * k + t];
+        found = id >= 0 && id != u && in_sorted_list(nbr, b, e, id);
+    }
+    const uint64_t m = __ballot(found);
+    if (t == 0) {
+        if (bad) eval_fail(status, -2);
+        out[qi] = bad ? __builtin_nan("") : (double)__popcll(m) / (double)k;
+    }
+}
+
+hipError_t launch_eval_recall(const int64_t* off, const int32_t* nbr, int64_t N, int64_t E,
+                              const int32_t* q, int32_t nq, const int32_t* ids, int32_t k,
+                              double* out, int32_t* status, hipStream_t s) {
+    if (nq == 0) return hipSuccess;
+    if (k < 1 || k > 64) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_eval_recall, dim3((unsigned)nq), dim3(64), 0, s, off, nbr, N, E, q, ids,
+                       k, out, status);
+    return hipGetLastError();
+}
+
+__global__ void k_eval_status_clear(int32_t* status) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) *status = 0;
+}
+
+hipError_t launch_eval_status_clear(int32_t* status, hipStream_t s) {
+    hipLaunchKernelGGL(k_eval_status_clear, dim3(1), dim3(64), 0, s, status);
+    return hipGetLastError();
+}
+
+// Keys of the distances: their float bit patterns (non-negative values and
+// NaN order as unsigned integers: every NaN after every value).
+__global__ __launch_bounds__(kBlock) void k_eval_keys(const float* __restrict__ d, int64_t n,
+                                                      uint32_t* __restrict__ keys) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    const float x = d[i];
+    keys[i] = x != x ? 0xFFFFFFFFu : __float_as_uint(x);
+}
+
+hipError_t launch_eval_keys(const float* d, int64_t n, uint32_t* keys, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_eval_keys, dim3((unsigned)((n + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                       s, d, n, keys);
+    return hipGetLastError();
+}
+
+}  // namespace huge

@@ -44,12 +44,13 @@ __device__ __forceinline__ uint32_t digit_inclusive_sum(uint32_t v, uint32_t* s_
 }
 
 // ---------------------------------------------------------------------------
-// Digit counts of tile t (kSortTile consecutive occurrences; kBlock threads,
-// coalesced reads): tcount[t * bins + d].
+// Digit counts of tile t (kSortTile consecutive keys; kBlock threads,
+// coalesced reads): tcount[t * bins + d], digit d = bits [shift, shift + bits)
+// of the key.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_tile_count(const Control* __restrict__ ctl,
                                                        const uint32_t* __restrict__ keys,
-                                                       int64_t m, int bits,
+                                                       int64_t m, int bits, int shift,
                                                        uint32_t* __restrict__ tcount) {
     __shared__ uint32_t s_cnt[kMaxBins];
     const int bins = 1 << bits;
@@ -60,26 +61,29 @@ __global__ __launch_bounds__(kBlock) void k_tile_count(const Control* __restrict
         const int64_t base = t * kSortTile;
         constexpr int kPer = kSortTile / kBlock;
         uint32_t k[kPer];
+        bool ok[kPer];
 #pragma unroll
         for (int r = 0; r < kPer; ++r) {
             const int64_t o = base + (int64_t)r * kBlock + threadIdx.x;
-            k[r] = o < m ? keys[o] : 0xFFFFFFFFu;
+            ok[r] = o < m;
+            k[r] = ok[r] ? keys[o] : 0u;
         }
 #pragma unroll
         for (int r = 0; r < kPer; ++r)
-            if (k[r] != 0xFFFFFFFFu) atomicAdd(&s_cnt[k[r] & (uint32_t)(bins - 1)], 1u);
+            if (ok[r]) atomicAdd(&s_cnt[(k[r] >> shift) & (uint32_t)(bins - 1)], 1u);
     }
     __syncthreads();
     for (int d = threadIdx.x; d < bins; d += kBlock) tcount[t * bins + d] = s_cnt[d];
 }
 
-hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits,
+hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits, int shift,
                              uint32_t* tcount, hipStream_t s) {
     const int64_t tiles = (m + kSortTile - 1) / kSortTile;
     if (tiles == 0) return hipSuccess;
-    if (bits < kMinDigitBits || bits > kMaxDigitBits) return hipErrorInvalidValue;
+    if (bits < kMinDigitBits || bits > kMaxDigitBits || shift < 0 || shift > 31)
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_tile_count, dim3((unsigned)tiles), dim3(kBlock), 0, s, ctl, keys, m,
-                       bits, tcount);
+                       bits, shift, tcount);
     return hipGetLastError();
 }
 
@@ -137,7 +141,7 @@ hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int
 }
 
 // ---------------------------------------------------------------------------
-// Stable scatter by the lowest BITS bits over a tile of kSortTile
+// Stable scatter by BITS bits at `shift` over a tile of kSortTile
 // consecutive items, kSortThreads threads; wave w owns items
 // [w * 512, (w + 1) * 512) of the tile in kSortItems rounds of 64.
 //   rank:  lanes of a round holding the same digit are found with BITS
@@ -149,12 +153,12 @@ hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int
 //   write: LDS position p goes to global position p + (digit's bucket start
 //          + digit's count in earlier tiles - digit's tile offset): runs of
 //          equal digits are contiguous, so the writes coalesce.
-// vals_out receives the occurrence index of each key.
+// vals_out (if not null) receives the position of each key in keys_in.
 // ---------------------------------------------------------------------------
 template <int BITS>
 __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     Control* __restrict__ ctl, const uint32_t* __restrict__ keys_in,
-    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m,
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m, int shift,
     const uint32_t* __restrict__ hist, const uint32_t* __restrict__ tprefix,
     uint32_t* __restrict__ bstart) {
     constexpr int kBins = 1 << BITS;
@@ -197,7 +201,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
 #pragma unroll
         for (int r = 0; r < kSortItems; ++r) {
             const bool valid = base_idx + r * 64 + lane < m;
-            const uint32_t dg = key[r] & (kBins - 1);
+            const uint32_t dg = (key[r] >> shift) & (kBins - 1);
             uint64_t peers = __ballot(valid);
 #pragma unroll
             for (int b = 0; b < BITS; ++b) {
@@ -244,7 +248,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     for (int r = 0; r < kSortItems; ++r) {
         const int64_t idx = base_idx + r * 64 + lane;
         if (idx < m) {
-            const uint32_t p = s_wave[wave][key[r] & (kBins - 1)] + rank[r];
+            const uint32_t p = s_wave[wave][(key[r] >> shift) & (kBins - 1)] + rank[r];
             s_keys[p] = key[r];
             s_vals[p] = (uint32_t)idx;
         }
@@ -255,10 +259,10 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
     const int64_t valid_n = (m - tile_base) < kSortTile ? (m - tile_base) : kSortTile;
     for (int p = tid; p < valid_n; p += kSortThreads) {
         const uint32_t k = s_keys[p];
-        const int64_t dest = (int64_t)s_delta[k & (kBins - 1)] + p;
+        const int64_t dest = (int64_t)s_delta[(k >> shift) & (kBins - 1)] + p;
         if (dest >= 0 && dest < m) {
             keys_out[dest] = k;
-            vals_out[dest] = s_vals[p];
+            if (vals_out != nullptr) vals_out[dest] = s_vals[p];
         } else {
             raise_internal(ctl, kSiteRadixDest);
         }
@@ -266,13 +270,15 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(
 }
 
 hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
-                             uint32_t* vals_out, int64_t m, int bits, const uint32_t* hist,
-                             const uint32_t* tprefix, uint32_t* bstart, hipStream_t s) {
+                             uint32_t* vals_out, int64_t m, int bits, int shift,
+                             const uint32_t* hist, const uint32_t* tprefix, uint32_t* bstart,
+                             hipStream_t s) {
     const int64_t tiles = (m + kSortTile - 1) / kSortTile;
     if (tiles == 0) return hipSuccess;
+    if (shift < 0 || shift > 31) return hipErrorInvalidValue;
 #define HUGE_RADIX_LAUNCH(B)                                                                  \
     hipLaunchKernelGGL(k_radix_pass<B>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, ctl, \
-                       keys_in, keys_out, vals_out, m, hist, tprefix, bstart)
+                       keys_in, keys_out, vals_out, m, shift, hist, tprefix, bstart)
     switch (bits) {
         case 8: HUGE_RADIX_LAUNCH(8); break;
         case 9: HUGE_RADIX_LAUNCH(9); break;

@@ -216,3 +216,10 @@ def test_recall_on_built_graphs():
     # duplicate list entries count once
     off2, nbr2 = _csr(3, [(0, 1), (0, 1), (0, 2)])
     assert orc.recall_at_k(off2, nbr2, [0], np.array([[1, 2]]), 2)[0] == 1.0
+
+
+def test_knn_with_fewer_rows_than_k_pads():
+    T = np.eye(4)[:3]
+    ids, d = orc.knn(T, [0], 5)
+    assert ids[0].tolist()[:2] == [1, 2] and ids[0].tolist()[2:] == [-1, -1, -1]
+    assert np.allclose(d[0][:2], math.sqrt(2)) and np.all(np.isnan(d[0][2:]))
