@@ -817,7 +817,8 @@ KnnLayout knn_layout(int64_t num_rows, int32_t dim, int32_t k) {
     L.qn2 = take(sizeof(float) * kKnnPass);
     L.qid = take(sizeof(int32_t) * kKnnPass);
     // the most lists: one query block, every wave its own list
-    L.partial = take(sizeof(uint64_t) * (size_t)knn_lists(num_rows, 1) * kKnnPass * (size_t)k);
+    L.partial =
+        take(sizeof(uint64_t) * (size_t)knn_lists(num_rows, dim, 1) * kKnnPass * (size_t)k);
     L.total = off;
     return L;
 }

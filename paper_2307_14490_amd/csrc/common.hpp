@@ -31,7 +31,8 @@ constexpr int kTableBitsMax = 14;      // 16384 slots: 144 KB of LDS per workgro
 constexpr int kBitmapBits = 18;        // two 32 KB bitmaps (seen, repeated)
 // Embedding evaluation
 constexpr int kEvalMaxQuantiles = 128;  // percentiles per summary
-constexpr int kKnnWaves = 4;            // waves of a nearest-row workgroup
+constexpr int kKnnWaves = 4;            // waves of a nearest-row workgroup (dim > 128)
+constexpr int kKnnWavesR = 8;           // the same with the queries in registers (dim <= 128)
 constexpr int kKnnMaxK = 32;            // nearest rows per query, at most
 constexpr int kKnnDimChunk = 128;       // dimensions per MFMA pass over a row tile
 constexpr int kKnnQueryFloats = 16896;  // LDS floats for the queries of a pass (66 KB)
@@ -259,7 +260,7 @@ hipError_t launch_eval_keys(const float* d, int64_t n, uint32_t* keys, hipStream
 hipError_t launch_eval_quantiles(const uint32_t* sorted, const double* cnt, const double* q,
                                  int nq, double* out, hipStream_t s);
 int knn_pass_queries(int D);
-int64_t knn_lists(int64_t N, int QB);
+int64_t knn_lists(int64_t N, int D, int QB);
 hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, int32_t nq,
                       int32_t k, int32_t* ids, float* dist, float* qn, float* qn2, int32_t* qid,
                       uint64_t* partial, int32_t* status, hipStream_t s);

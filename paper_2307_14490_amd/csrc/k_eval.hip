@@ -387,32 +387,61 @@ __global__ __launch_bounds__(kKnnWaves * 64) void k_knn_tiles(KnnArgs A) {
     const int nch = (D + kKnnDimChunk - 1) / kKnnDimChunk;
     const float* qrow = s_q + (qb * 32 + x) * stride;
 
+    // one dimension chunk (dim <= 128): the next tile's rows are loaded
+    // while the current tile's products run
+    constexpr int kQ4 = kKnnDimChunk / 8;  // float4 of a lane's half row
+    const int d0h = h * (kKnnDimChunk / 2);
+    auto load_rows = [&](int64_t tt, int c, float4* bv) {
+        const int64_t rr = tt * 32 + x;
+        const int d0 = c * kKnnDimChunk + d0h;
+        const float4* src = reinterpret_cast<const float4*>(A.T + rr * (int64_t)D + d0);
+        const bool ok = tt < A.tiles && rr < A.N;
+#pragma unroll
+        for (int m = 0; m < kQ4; ++m)
+            bv[m] = (ok && d0 + 4 * m < D) ? src[m] : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    float4 nxt[kQ4];
+    if (nch == 1) load_rows(S, 0, nxt);
     for (int64_t t = S; t < A.tiles; t += NS) {
         const int64_t row = t * 32 + x;
         const bool row_ok = row < A.N;
+        // two independent accumulation chains (even and odd float4 of the
+        // lane's half row), added at the end
         knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                          0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        knn_acc16 acc1 = acc;
         float nr = 0.f;
         for (int c = 0; c < nch; ++c) {
-            const int d0 = c * kKnnDimChunk + h * (kKnnDimChunk / 2);
-            float4 bv[kKnnDimChunk / 8];
-            const float4* src = reinterpret_cast<const float4*>(A.T + row * (int64_t)D + d0);
+            const int d0 = c * kKnnDimChunk + d0h;
+            float4 bv[kQ4];
+            if (nch == 1) {
 #pragma unroll
-            for (int m = 0; m < kKnnDimChunk / 8; ++m)
-                bv[m] = (row_ok && d0 + 4 * m < D) ? src[m] : make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int m = 0; m < kQ4; ++m) bv[m] = nxt[m];
+                load_rows(t + NS, 0, nxt);
+            } else {
+                load_rows(t, c, bv);
+            }
 #pragma unroll
-            for (int m = 0; m < kKnnDimChunk / 8; ++m) {
+            for (int m = 0; m < kQ4; ++m) {
                 nr += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z +
                       bv[m].w * bv[m].w;
                 const int dd = d0 + 4 * m;
                 float4 av = make_float4(0.f, 0.f, 0.f, 0.f);
                 if (dd < D) av = *reinterpret_cast<const float4*>(qrow + dd);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv[m].x, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv[m].y, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv[m].z, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv[m].w, acc, 0, 0, 0);
+                if (m % 2 == 0) {
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv[m].x, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv[m].y, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv[m].z, acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv[m].w, acc, 0, 0, 0);
+                } else {
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv[m].x, acc1, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv[m].y, acc1, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv[m].z, acc1, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv[m].w, acc1, 0, 0, 0);
+                }
             }
         }
+        acc += acc1;
         nr += __shfl_xor(nr, 32, 64);
         const float inv = nr > 0.f ? 1.0f / sqrtf(nr) : 0.f;
         const float nx = nr > 0.f ? 1.f : 0.f;
@@ -456,6 +485,137 @@ __global__ __launch_bounds__(kKnnWaves * 64) void k_knn_tiles(KnnArgs A) {
         }
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
         __builtin_amdgcn_wave_barrier();
+    }
+    if (h == 0) {
+        const uint32_t len = s_len[w][x];
+        uint64_t* dst = A.partial + ((size_t)S * A.nqp + qb * 32 + x) * k;
+        for (int t = 0; t < k; ++t) dst[t] = (uint32_t)t < len ? s_list[w][x][t] : kNoKey;
+    }
+}
+
+// The same search for dim <= 128 with the queries' operands in registers:
+// no LDS holds the queries, so kKnnWavesR waves (two per SIMD) fit one CU and
+// the epilogue of one wave overlaps the products of another.  A lane keeps
+// its 16 query slots' thresholds as floats (the d^2 of the query's current
+// k-th key) and builds the exact key only for a score at or below it.
+__global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_r(KnnArgs A) {
+    __shared__ uint64_t s_list[kKnnWavesR][32][kKnnMaxK];
+    __shared__ uint64_t s_stage[kKnnWavesR][32][32];
+    __shared__ uint64_t s_thr[kKnnWavesR][32];
+    __shared__ uint32_t s_cnt[kKnnWavesR][32];
+    __shared__ uint32_t s_len[kKnnWavesR][32];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int x = lane & 31, h = lane >> 5;
+    const int D = A.D, k = A.k;
+    const int qb = w % A.QB;
+    const int wpb = kKnnWavesR / A.QB;
+    const int64_t S = (int64_t)blockIdx.x * wpb + w / A.QB;
+    const int64_t NS = (int64_t)gridDim.x * wpb;
+    constexpr int kQ4 = kKnnDimChunk / 8;
+    const int d0 = h * (kKnnDimChunk / 2);
+
+    // operands of query qb*32 + x, dimensions d0 .. d0 + 63
+    float4 av[kQ4];
+    {
+        const float* qrow = A.qn + (int64_t)(qb * 32 + x) * D;
+#pragma unroll
+        for (int m = 0; m < kQ4; ++m)
+            av[m] = d0 + 4 * m < D ? *reinterpret_cast<const float4*>(qrow + d0 + 4 * m)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    // this lane's 16 score slots: query i = 8 (r / 4) + 4 h + r % 4
+    float qn2[16], thr[16];
+    int32_t qid[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int q = qb * 32 + 8 * (r / 4) + 4 * h + (r % 4);
+        qn2[r] = A.qn2[q];
+        qid[r] = A.qid[q];
+        thr[r] = __builtin_inff();
+    }
+    if (lane < 32) {
+        s_thr[w][lane] = kNoKey;
+        s_cnt[w][lane] = 0u;
+        s_len[w][lane] = 0u;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+
+    auto load_rows = [&](int64_t tt, float4* bv) {
+        const int64_t rr = tt * 32 + x;
+        const float4* src = reinterpret_cast<const float4*>(A.T + rr * (int64_t)D + d0);
+        const bool ok = tt < A.tiles && rr < A.N;
+#pragma unroll
+        for (int m = 0; m < kQ4; ++m)
+            bv[m] = (ok && d0 + 4 * m < D) ? src[m] : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    for (int64_t t = S; t < A.tiles; t += NS) {
+        const int64_t row = t * 32 + x;
+        float4 bv[kQ4];
+        load_rows(t, bv);
+        knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
+                         0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        float nr = 0.f;
+#pragma unroll
+        for (int m = 0; m < kQ4; ++m) {
+            nr += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z + bv[m].w * bv[m].w;
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].x, bv[m].x, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].y, bv[m].y, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].z, bv[m].z, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].w, bv[m].w, acc, 0, 0, 0);
+        }
+        nr += __shfl_xor(nr, 32, 64);
+        const bool row_ok = row < A.N;
+        const float inv = nr > 0.f ? 1.0f / sqrtf(nr) : 0.f;
+        const float nx = nr > 0.f ? 1.f : 0.f;
+        bool staged = false;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float d2 = qn2[r] + nx - 2.f * acc[r] * inv;
+            d2 = d2 > 0.f ? d2 : 0.f;
+            if (d2 <= thr[r] && row_ok && qid[r] >= 0 && row != (int64_t)qid[r]) {
+                const int i = 8 * (r / 4) + 4 * h + (r % 4);
+                const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) | (uint64_t)row;
+                if (key < s_thr[w][i]) {
+                    const uint32_t pos = atomicAdd(&s_cnt[w][i], 1u);
+                    s_stage[w][i][pos] = key;  // pos < 32: one row per lane x
+                    staged = true;
+                }
+            }
+        }
+        if (__ballot(staged) == 0ull) continue;  // wave-uniform: nothing to merge
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        if (h == 0) {
+            const uint32_t c = s_cnt[w][x];
+            if (c > 0u) {
+                uint64_t* L = s_list[w][x];
+                uint32_t len = s_len[w][x];
+                for (uint32_t e = 0; e < c; ++e) {
+                    const uint64_t key = s_stage[w][x][e];
+                    if (len == (uint32_t)k && key >= L[k - 1]) continue;
+                    int p = len < (uint32_t)k ? (int)len : k - 1;
+                    while (p > 0 && L[p - 1] > key) {
+                        L[p] = L[p - 1];
+                        --p;
+                    }
+                    L[p] = key;
+                    if (len < (uint32_t)k) ++len;
+                }
+                s_len[w][x] = len;
+                s_cnt[w][x] = 0u;
+                s_thr[w][x] = len == (uint32_t)k ? L[k - 1] : kNoKey;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int i = 8 * (r / 4) + 4 * h + (r % 4);
+            const uint64_t tk = s_thr[w][i];
+            thr[r] = tk == kNoKey ? __builtin_inff() : __uint_as_float((uint32_t)(tk >> 32));
+        }
     }
     if (h == 0) {
         const uint32_t len = s_len[w][x];
@@ -516,9 +676,11 @@ int knn_pass_queries(int D) {
     return (qp / 32) * 32;
 }
 
-int64_t knn_lists(int64_t N, int QB) {
+// Lists of one pass: (workgroups) x (waves per query block).
+int64_t knn_lists(int64_t N, int D, int QB) {
     const int64_t tiles = (N + 31) / 32;
-    const int wpb = kKnnWaves / QB;
+    const int waves = D <= kKnnDimChunk ? kKnnWavesR : kKnnWaves;
+    const int wpb = waves / QB;
     int64_t grid = (tiles + wpb - 1) / wpb;
     grid = grid < kKnnGrid ? grid : kKnnGrid;
     return grid * wpb;
@@ -549,9 +711,15 @@ hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, in
         A.qn2 = qn2;
         A.qid = qid;
         A.partial = partial;
-        const int64_t NS = knn_lists(N, QB);
-        const int64_t grid = NS / (kKnnWaves / QB);
-        hipLaunchKernelGGL(k_knn_tiles, dim3((unsigned)grid), dim3(kKnnWaves * 64), 0, s, A);
+        const int64_t NS = knn_lists(N, D, QB);
+        if (D <= kKnnDimChunk) {
+            const int64_t grid = NS / (kKnnWavesR / QB);
+            hipLaunchKernelGGL(k_knn_tiles_r, dim3((unsigned)grid), dim3(kKnnWavesR * 64), 0, s,
+                               A);
+        } else {
+            const int64_t grid = NS / (kKnnWaves / QB);
+            hipLaunchKernelGGL(k_knn_tiles, dim3((unsigned)grid), dim3(kKnnWaves * 64), 0, s, A);
+        }
         hipLaunchKernelGGL(k_knn_merge, dim3((unsigned)m), dim3(kBlock), 0, s, partial, NS, nqp,
                            k, q0, ids, dist);
     }

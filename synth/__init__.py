@@ -26,6 +26,7 @@ from .gen import (  # noqa: F401
     chung_lu_weights,
     csr_from_edges,
     make_workload,
+    relabel,
     sbm_edges,
     tuples_from_walks,
     walk_csr,
