@@ -212,7 +212,7 @@ def bench_producer(args):
 
 def bench_eval(args):
     """Unsupervised evaluation of embeddings (Sec. 4): on the medium exact SBM
-    (1M nodes, trained for three epochs of GPU-sampled walk triples) the whole
+    (1M nodes, trained for eight epochs of GPU-sampled walk triples) the whole
     evaluation -- 1M
     edge and 1M non-edge pairs, their distances, SNR and percentiles, the 10
     nearest rows of 100 sampled nodes and recall@10 -- each stage timed with
@@ -261,7 +261,7 @@ def bench_eval(args):
     # epochs of triples from the GPU walk sampler (a walk of the workload's
     # length and window from every node, new walks each epoch), shuffled on
     # the device
-    epochs = 3
+    epochs = 8
     train_steps = 0
     pos = 0
     g = torch.Generator(device="cuda")
