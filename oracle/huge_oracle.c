@@ -234,9 +234,16 @@ int oracle_sample_negatives(uint64_t seed, uint64_t first_pos, int64_t n, int32_
 static double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }
 static double softplus(double z) { return (z > 0.0 ? z : 0.0) + log1p(exp(-fabs(z))); }
 
+/* The weight c_i of positive i: the float weight wf[i] where weights are
+   given (a co-occurrence histogram combined with per-distance weights), else
+   the integer co_count cc[i]. */
+static double weight_of(const int32_t *cc, const float *wf, int64_t i) {
+    return wf ? (double)wf[i] : (double)cc[i];
+}
+
 static int check_batch(int64_t ns, int64_t nt, int64_t n, int32_t num_neg,
                        const int32_t *src, const int32_t *dst, const int32_t *cc,
-                       const int32_t *neg) {
+                       const float *wf, const int32_t *neg) {
     for (int64_t i = 0; i < n; ++i) {
         if (src[i] < 0 || src[i] >= ns || dst[i] < 0 || dst[i] >= nt) return OR_ERANGE;
         for (int32_t k = 0; k < num_neg; ++k) {
@@ -244,8 +251,13 @@ static int check_batch(int64_t ns, int64_t nt, int64_t n, int32_t num_neg,
             if (m < 0 || m >= nt) return OR_ERANGE;
         }
     }
-    for (int64_t i = 0; i < n; ++i)
-        if (cc[i] < 0) return OR_ECOUNT;
+    for (int64_t i = 0; i < n; ++i) {
+        if (wf) {
+            if (!(wf[i] >= 0.0f && wf[i] <= 3.4028234663852886e38f)) return OR_ECOUNT;
+        } else if (cc[i] < 0) {
+            return OR_ECOUNT;
+        }
+    }
     return OR_OK;
 }
 
@@ -260,18 +272,18 @@ static double dot_dd(const double *a, const double *b, int32_t dim) {
  * grad_S and grad_T (same shapes) are overwritten.  Returns 0 and writes the
  * loss, or an error code.
  */
-int oracle_sgns_grad_d(const double *S, const double *T, int64_t ns, int64_t nt, int32_t dim,
+static int sgns_grad_d(const double *S, const double *T, int64_t ns, int64_t nt, int32_t dim,
                        int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
-                       const int32_t *cc, const int32_t *neg, double *grad_S, double *grad_T,
-                       double *loss_out) {
+                       const int32_t *cc, const float *wf, const int32_t *neg, double *grad_S,
+                       double *grad_T, double *loss_out) {
     if (dim <= 0 || n < 0 || num_neg < 1 || !grad_S || !grad_T || !loss_out) return OR_EINVAL;
-    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, neg);
+    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, wf, neg);
     if (rc) return rc;
     memset(grad_S, 0, (size_t)ns * (size_t)dim * sizeof(double));
     memset(grad_T, 0, (size_t)nt * (size_t)dim * sizeof(double));
     double loss = 0.0;
     for (int64_t i = 0; i < n; ++i) {
-        const double c = (double)cc[i];
+        const double c = weight_of(cc, wf, i);
         const double *su = S + (int64_t)src[i] * dim;
         const double *tv = T + (int64_t)dst[i] * dim;
         double *gsu = grad_S + (int64_t)src[i] * dim;
@@ -302,12 +314,21 @@ int oracle_sgns_grad_d(const double *S, const double *T, int64_t ns, int64_t nt,
     return OR_OK;
 }
 
+int oracle_sgns_grad_d(const double *S, const double *T, int64_t ns, int64_t nt, int32_t dim,
+                       int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
+                       const int32_t *cc, const int32_t *neg, double *grad_S, double *grad_T,
+                       double *loss_out) {
+    if (n > 0 && !cc) return OR_EINVAL;
+    return sgns_grad_d(S, T, ns, nt, dim, n, num_neg, src, dst, cc, NULL, neg, grad_S, grad_T,
+                       loss_out);
+}
+
 /* Loss only, on double tables. */
 int oracle_sgns_loss_d(const double *S, const double *T, int64_t ns, int64_t nt, int32_t dim,
                        int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
                        const int32_t *cc, const int32_t *neg, double *loss_out) {
     if (dim <= 0 || n < 0 || num_neg < 1 || !loss_out) return OR_EINVAL;
-    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, neg);
+    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, NULL, neg);
     if (rc) return rc;
     double loss = 0.0;
     for (int64_t i = 0; i < n; ++i) {
@@ -330,12 +351,12 @@ int oracle_sgns_loss_d(const double *S, const double *T, int64_t ns, int64_t nt,
  *   row = (float)((double)row - (double)lr * grad).
  * Rows that no example touches are not written.  On error nothing is written.
  */
-int oracle_sgns_step(float *S, float *T, int64_t ns, int64_t nt, int32_t dim, int64_t n,
+static int sgns_step(float *S, float *T, int64_t ns, int64_t nt, int32_t dim, int64_t n,
                      int32_t num_neg, const int32_t *src, const int32_t *dst, const int32_t *cc,
-                     const int32_t *neg, float lr, double *loss_out) {
+                     const float *wf, const int32_t *neg, float lr, double *loss_out) {
     if (!S || !T || dim <= 0 || n < 0 || num_neg < 1 || !loss_out) return OR_EINVAL;
-    if (n > 0 && (!src || !dst || !cc || !neg)) return OR_EINVAL;
-    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, neg);
+    if (n > 0 && (!src || !dst || (!cc && !wf) || !neg)) return OR_EINVAL;
+    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, wf, neg);
     if (rc) return rc;
     size_t s_elems = (size_t)ns * (size_t)dim, t_elems = (size_t)nt * (size_t)dim;
     double *Sd = (double *)malloc(s_elems * sizeof(double));
@@ -351,7 +372,7 @@ int oracle_sgns_step(float *S, float *T, int64_t ns, int64_t nt, int32_t dim, in
     for (size_t e = 0; e < s_elems; ++e) Sd[e] = (double)S[e];
     for (size_t e = 0; e < t_elems; ++e) Td[e] = (double)T[e];
     double loss = 0.0;
-    rc = oracle_sgns_grad_d(Sd, Td, ns, nt, dim, n, num_neg, src, dst, cc, neg, gS, gT, &loss);
+    rc = sgns_grad_d(Sd, Td, ns, nt, dim, n, num_neg, src, dst, cc, wf, neg, gS, gT, &loss);
     if (rc == OR_OK) {
         for (int64_t i = 0; i < n; ++i) {
             touched_S[src[i]] = 1;
@@ -373,19 +394,36 @@ int oracle_sgns_step(float *S, float *T, int64_t ns, int64_t nt, int32_t dim, in
     return rc;
 }
 
+int oracle_sgns_step(float *S, float *T, int64_t ns, int64_t nt, int32_t dim, int64_t n,
+                     int32_t num_neg, const int32_t *src, const int32_t *dst, const int32_t *cc,
+                     const int32_t *neg, float lr, double *loss_out) {
+    if (n > 0 && !cc) return OR_EINVAL;
+    return sgns_step(S, T, ns, nt, dim, n, num_neg, src, dst, cc, NULL, neg, lr, loss_out);
+}
+
+/* The same step with a float weight per positive in place of the co_count
+   (finite and >= 0, else OR_ECOUNT). */
+int oracle_sgns_step_w(float *S, float *T, int64_t ns, int64_t nt, int32_t dim, int64_t n,
+                       int32_t num_neg, const int32_t *src, const int32_t *dst, const float *w,
+                       const int32_t *neg, float lr, double *loss_out) {
+    if (n > 0 && !w) return OR_EINVAL;
+    return sgns_step(S, T, ns, nt, dim, n, num_neg, src, dst, NULL, w, neg, lr, loss_out);
+}
+
 /* Loss of a batch on float32 tables, evaluated in double. */
-int oracle_sgns_loss(const float *S, const float *T, int64_t ns, int64_t nt, int32_t dim,
+static int sgns_loss(const float *S, const float *T, int64_t ns, int64_t nt, int32_t dim,
                      int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
-                     const int32_t *cc, const int32_t *neg, double *loss_out) {
+                     const int32_t *cc, const float *wf, const int32_t *neg, double *loss_out) {
     if (!S || !T || dim <= 0 || n < 0 || num_neg < 1 || !loss_out) return OR_EINVAL;
-    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, neg);
+    if (n > 0 && !cc && !wf) return OR_EINVAL;
+    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, wf, neg);
     if (rc) return rc;
     double *su = (double *)malloc((size_t)dim * sizeof(double));
     double *tr = (double *)malloc((size_t)dim * sizeof(double));
     if (!su || !tr) { free(su); free(tr); return OR_EINVAL; }
     double loss = 0.0;
     for (int64_t i = 0; i < n; ++i) {
-        const double c = (double)cc[i];
+        const double c = weight_of(cc, wf, i);
         for (int32_t d = 0; d < dim; ++d) su[d] = (double)S[(int64_t)src[i] * dim + d];
         for (int32_t d = 0; d < dim; ++d) tr[d] = (double)T[(int64_t)dst[i] * dim + d];
         loss += c * softplus(-dot_dd(su, tr, dim));
@@ -397,6 +435,44 @@ int oracle_sgns_loss(const float *S, const float *T, int64_t ns, int64_t nt, int
     }
     free(su); free(tr);
     *loss_out = loss;
+    return OR_OK;
+}
+
+int oracle_sgns_loss(const float *S, const float *T, int64_t ns, int64_t nt, int32_t dim,
+                     int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
+                     const int32_t *cc, const int32_t *neg, double *loss_out) {
+    return sgns_loss(S, T, ns, nt, dim, n, num_neg, src, dst, cc, NULL, neg, loss_out);
+}
+
+int oracle_sgns_loss_w(const float *S, const float *T, int64_t ns, int64_t nt, int32_t dim,
+                       int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
+                       const float *w, const int32_t *neg, double *loss_out) {
+    return sgns_loss(S, T, ns, nt, dim, n, num_neg, src, dst, NULL, w, neg, loss_out);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Weights from distance histograms (Sec. 3.2: co_counts is a histogram over  */
+/* the walk distance of a co-occurrence): positive i with histogram           */
+/* hist[i * window + d] (d = distance - 1) gets                               */
+/*   w_i = (float) sum_{d = 0 .. window-1} (double) wd[d] * (double) hist[.]  */
+/* summed in double in ascending d, each product and sum rounded once (no     */
+/* fused multiply-add), then rounded once to float.                           */
+/* ------------------------------------------------------------------------- */
+int oracle_cocount_weights(const int32_t *hist, int64_t n, int32_t window, const float *wd,
+                           float *out) {
+    if (n < 0 || window < 1 || !wd || (n > 0 && (!hist || !out))) return OR_EINVAL;
+    for (int32_t d = 0; d < window; ++d)
+        if (!(wd[d] >= 0.0f && wd[d] <= 3.4028234663852886e38f)) return OR_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        double sum = 0.0;
+        for (int32_t d = 0; d < window; ++d) {
+            const int32_t h = hist[i * window + d];
+            if (h < 0) return OR_ECOUNT;
+            const double prod = (double)wd[d] * (double)h;
+            sum = sum + prod;
+        }
+        out[i] = (float)sum;
+    }
     return OR_OK;
 }
 

@@ -83,6 +83,11 @@ def lib():
                   ctypes.c_int64, ctypes.c_int32, _i32p, _i32p, _i32p, _i32p]
         L.oracle_sgns_step.argtypes = f_args + [ctypes.c_float, _f64p]
         L.oracle_sgns_loss.argtypes = f_args + [_f64p]
+        w_args = [_f32p, _f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                  ctypes.c_int64, ctypes.c_int32, _i32p, _i32p, _f32p, _i32p]
+        L.oracle_sgns_step_w.argtypes = w_args + [ctypes.c_float, _f64p]
+        L.oracle_sgns_loss_w.argtypes = w_args + [_f64p]
+        L.oracle_cocount_weights.argtypes = [_i32p, ctypes.c_int64, ctypes.c_int32, _f32p, _f32p]
         L.oracle_sample_walks.argtypes = [_i64p, _i32p, ctypes.c_int64, ctypes.c_int64,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                           ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
@@ -94,7 +99,8 @@ def lib():
         for name in ("oracle_init_rows", "oracle_build_alias", "oracle_sample_negatives",
                      "oracle_sample_walks", "oracle_eval_pairs",
                      "oracle_sgns_grad_d", "oracle_sgns_loss_d", "oracle_sgns_step",
-                     "oracle_sgns_loss"):
+                     "oracle_sgns_loss", "oracle_sgns_step_w", "oracle_sgns_loss_w",
+                     "oracle_cocount_weights"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -204,13 +210,22 @@ def loss_d(S, T, src, dst, cc, neg) -> float:
 
 
 def step_dense(S: np.ndarray, T: np.ndarray, src, dst, cc, neg, lr: float) -> float:
-    """One step in place on float32 tables S, T (C-contiguous); returns the loss sum."""
+    """One step in place on float32 tables S, T (C-contiguous); returns the loss sum.
+    cc: integer co_counts, or float32 weights (one per positive)."""
     assert S.dtype == np.float32 and T.dtype == np.float32
     assert S.flags.c_contiguous and T.flags.c_contiguous
-    src, dst, cc = _c(src, np.int32), _c(dst, np.int32), _c(cc, np.int32)
+    src, dst = _c(src, np.int32), _c(dst, np.int32)
     neg = _as_neg(neg, len(src))
     n, K = neg.shape
     loss = ctypes.c_double()
+    if np.asarray(cc).dtype.kind == "f":
+        w = _c(cc, np.float32)
+        _check(lib().oracle_sgns_step_w(_ptr(S, _f32p), _ptr(T, _f32p), S.shape[0], T.shape[0],
+                                        S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
+                                        _ptr(w, _f32p), _ptr(neg, _i32p), lr,
+                                        ctypes.byref(loss)), "sgns_step_w")
+        return loss.value
+    cc = _c(cc, np.int32)
     _check(lib().oracle_sgns_step(_ptr(S, _f32p), _ptr(T, _f32p), S.shape[0], T.shape[0],
                                   S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
                                   _ptr(cc, _i32p), _ptr(neg, _i32p), lr, ctypes.byref(loss)),
@@ -219,12 +234,21 @@ def step_dense(S: np.ndarray, T: np.ndarray, src, dst, cc, neg, lr: float) -> fl
 
 
 def loss_dense(S: np.ndarray, T: np.ndarray, src, dst, cc, neg) -> float:
+    """Loss sum in double; cc: integer co_counts or float32 weights."""
     S = _c(S, np.float32)
     T = _c(T, np.float32)
-    src, dst, cc = _c(src, np.int32), _c(dst, np.int32), _c(cc, np.int32)
+    src, dst = _c(src, np.int32), _c(dst, np.int32)
     neg = _as_neg(neg, len(src))
     n, K = neg.shape
     loss = ctypes.c_double()
+    if np.asarray(cc).dtype.kind == "f":
+        w = _c(cc, np.float32)
+        _check(lib().oracle_sgns_loss_w(_ptr(S, _f32p), _ptr(T, _f32p), S.shape[0], T.shape[0],
+                                        S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
+                                        _ptr(w, _f32p), _ptr(neg, _i32p), ctypes.byref(loss)),
+               "sgns_loss_w")
+        return loss.value
+    cc = _c(cc, np.int32)
     _check(lib().oracle_sgns_loss(_ptr(S, _f32p), _ptr(T, _f32p), S.shape[0], T.shape[0],
                                   S.shape[1], n, K, _ptr(src, _i32p), _ptr(dst, _i32p),
                                   _ptr(cc, _i32p), _ptr(neg, _i32p), ctypes.byref(loss)),
@@ -280,6 +304,19 @@ def step_sparse(seed: int, num_nodes: int, dim: int, num_neg: int, half_width: f
     neg_c = np.searchsorted(rows_T, neg.reshape(-1)).astype(np.int32).reshape(n, num_neg)
     loss = step_dense(S, T, src_c, dst_c, cc, neg_c, lr)
     return SparseStep(rows_S, S, rows_T, T, loss, neg)
+
+
+def cocount_weights(hist, dist_weights) -> np.ndarray:
+    """float32 weight per triple from its distance histogram (n x window):
+    sum_d dist_weights[d] * hist[:, d] in double (ascending d), rounded once."""
+    h = _c(hist, np.int32)
+    n, window = h.shape
+    wd = _c(dist_weights, np.float32)
+    assert wd.size == window
+    out = np.empty(n, np.float32)
+    _check(lib().oracle_cocount_weights(_ptr(h, _i32p), n, window, _ptr(wd, _f32p),
+                                        _ptr(out, _f32p)), "cocount_weights")
+    return out
 
 
 def lwsgd_lr(t: int, warmup: int, peak: float, decay: int, final: float) -> float:
