@@ -159,6 +159,32 @@ huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_
                               void* stream);
 huge_status huge_train_prepared(huge_handle* h, float lr, double* d_loss_sum, void* stream);
 
+/* Weighted co-occurrences (Sec. 3.2: co_counts is a histogram over the walk
+   distance of each co-occurrence).  The *_weighted calls are the step, its
+   two halves and the loss with one float weight per positive,
+   c_i = d_weight[i], in place of the integer co_count; a weight that is
+   negative, NaN or infinite makes the call a no-op reported like a negative
+   co_count (HUGE_ERR_BAD_COUNT).  Results with integer-valued weights are
+   bitwise those of the integer calls. */
+huge_status huge_train_step_weighted(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                                     const float* d_weight, int64_t n, uint64_t first_pos_index,
+                                     float lr, double* d_loss_sum, void* stream);
+huge_status huge_prepare_step_weighted(huge_handle* h, const int32_t* d_src,
+                                       const int32_t* d_dst, const float* d_weight, int64_t n,
+                                       uint64_t first_pos_index, void* stream);
+huge_status huge_eval_loss_weighted(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                                    const float* d_weight, int64_t n, uint64_t first_pos_index,
+                                    double* d_loss_sum, void* stream);
+
+/* The weight of each triple from its distance histogram (as
+   huge_sample_walks writes it): d_weight[i] = sum over d of
+   h_dist_weights[d] * d_hist[i * window + d], the products and the sum taken
+   in double (each rounded once, distances in ascending order), then rounded
+   once to float.  h_dist_weights: `window` host floats, finite and >= 0;
+   1 <= window <= 32.  A negative histogram entry gives NaN. */
+huge_status huge_cocount_weights(const int32_t* d_hist, int64_t n, int32_t window,
+                                 const float* h_dist_weights, float* d_weight, void* stream);
+
 /* L of a batch at the current tables, with the negatives huge_train_step
    would draw for the same first_pos_index; writes nothing else. */
 huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,

@@ -18,6 +18,7 @@ from .binding import (  # noqa: F401
     HugeWalkConfig,
     Trainer,
     build_alias,
+    cocount_weights,
     load,
     make_config,
     sample_walks,

@@ -33,7 +33,8 @@ EXPORTED = [
     "huge_get_rows", "huge_sample_negatives", "huge_probe_rows", "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
     "huge_destroy", "huge_status_string", "huge_walk_workspace_bytes", "huge_sample_walks",
     "huge_eval_workspace_bytes", "huge_eval_pairs", "huge_eval_distances", "huge_eval_summary",
-    "huge_eval_knn", "huge_eval_recall",
+    "huge_eval_knn", "huge_eval_recall", "huge_train_step_weighted", "huge_prepare_step_weighted",
+    "huge_eval_loss_weighted", "huge_cocount_weights",
 ]
 HUGE_PHASES = 6
 
@@ -121,6 +122,14 @@ def load() -> ctypes.CDLL:
     for name in ("huge_eval_pairs", "huge_eval_distances", "huge_eval_summary", "huge_eval_knn",
                  "huge_eval_recall"):
         getattr(L, name).restype = ctypes.c_int32
+    L.huge_train_step_weighted.argtypes = [_vp, _vp, _vp, _vp, i64, ctypes.c_uint64,
+                                           ctypes.c_float, _vp, _vp]
+    L.huge_prepare_step_weighted.argtypes = [_vp, _vp, _vp, _vp, i64, ctypes.c_uint64, _vp]
+    L.huge_eval_loss_weighted.argtypes = [_vp, _vp, _vp, _vp, i64, ctypes.c_uint64, _vp, _vp]
+    L.huge_cocount_weights.argtypes = [_vp, i64, i32, ctypes.POINTER(ctypes.c_float), _vp, _vp]
+    for name in ("huge_train_step_weighted", "huge_prepare_step_weighted",
+                 "huge_eval_loss_weighted", "huge_cocount_weights"):
+        getattr(L, name).restype = ctypes.c_int32
     L.huge_destroy.argtypes = [_vp]
     L.huge_destroy.restype = None
     L.huge_status_string.argtypes = [ctypes.c_int32]
@@ -174,6 +183,24 @@ def _dptr(t):
     return None if t is None else t.data_ptr()
 
 
+def _is_float(t):
+    import torch
+    return t is not None and t.dtype == torch.float32
+
+
+def cocount_weights(hist, dist_weights, stream=None):
+    """float32 weight per triple from its distance histogram (device int32,
+    n x window) and per-distance weights (host sequence), by
+    huge_cocount_weights."""
+    import torch
+    n, window = hist.shape
+    wd = (ctypes.c_float * window)(*[float(x) for x in dist_weights])
+    out = torch.empty(n, dtype=torch.float32, device=hist.device)
+    _ok(load().huge_cocount_weights(_dptr(hist), int(n), int(window), wd, _dptr(out),
+                                    _stream_ptr(stream)), "huge_cocount_weights")
+    return out
+
+
 class Trainer:
     """Tables, workspace and a libhuge handle on one GPU.
 
@@ -219,22 +246,24 @@ class Trainer:
         self._h = h
 
     # -- calls ------------------------------------------------------------
+    # cc: int32 co_counts, or float32 weights (the *_weighted calls)
     def step(self, src, dst, cc, first_pos, lr, loss_out=None, stream=None):
         loss = self.loss_buf if loss_out is None else loss_out
-        _ok(load().huge_train_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                   int(first_pos), float(lr), _dptr(loss), _stream_ptr(stream)),
-            "huge_train_step")
+        fn = "huge_train_step_weighted" if _is_float(cc) else "huge_train_step"
+        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                int(first_pos), float(lr), _dptr(loss), _stream_ptr(stream)), fn)
         return loss
 
     def step_no_loss(self, src, dst, cc, first_pos, lr, stream=None):
-        _ok(load().huge_train_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                   int(first_pos), float(lr), None, _stream_ptr(stream)),
-            "huge_train_step")
+        fn = "huge_train_step_weighted" if _is_float(cc) else "huge_train_step"
+        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                int(first_pos), float(lr), None, _stream_ptr(stream)), fn)
 
     def prepare(self, src, dst, cc, first_pos, stream=None):
         """Group a batch (validation, negatives, de-duplication) into a slot."""
-        _ok(load().huge_prepare_step(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                     int(first_pos), _stream_ptr(stream)), "huge_prepare_step")
+        fn = "huge_prepare_step_weighted" if _is_float(cc) else "huge_prepare_step"
+        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                int(first_pos), _stream_ptr(stream)), fn)
 
     def train_prepared(self, lr, loss_out=None, with_loss=True, stream=None):
         """Apply the oldest prepared batch; returns the loss tensor (or None)."""
@@ -245,9 +274,9 @@ class Trainer:
 
     def eval_loss(self, src, dst, cc, first_pos, loss_out=None, stream=None):
         loss = self.loss_buf if loss_out is None else loss_out
-        _ok(load().huge_eval_loss(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                  int(first_pos), _dptr(loss), _stream_ptr(stream)),
-            "huge_eval_loss")
+        fn = "huge_eval_loss_weighted" if _is_float(cc) else "huge_eval_loss"
+        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
+                                int(first_pos), _dptr(loss), _stream_ptr(stream)), fn)
         return loss
 
     def get_rows(self, table, ids, stream=None):

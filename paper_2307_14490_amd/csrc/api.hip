@@ -42,6 +42,7 @@ struct PendingBatch {
     const int32_t* src = nullptr;
     const int32_t* dst = nullptr;
     const int32_t* cc = nullptr;
+    const float* w = nullptr;    // float weights in place of cc
     int64_t n = 0;
     uint64_t first_pos = 0;
     int stage = 0;               // 0 sampled, 1 radix pass issued, 2 grouped
@@ -281,11 +282,12 @@ huge_status reset_workspace(huge_handle* h, hipStream_t s) {
     return HUGE_OK;
 }
 
+// `weights`: the batch's co_counts or float weights.
 huge_status check_batch_args(huge_handle* h, const int32_t* src, const int32_t* dst,
-                             const int32_t* cc, int64_t n) {
+                             const void* weights, int64_t n) {
     if (!h) return HUGE_ERR_INVALID_ARG;
     if (n < 0 || n > h->cfg.max_batch) return HUGE_ERR_INVALID_ARG;
-    if (n > 0 && (!src || !dst || !cc)) return HUGE_ERR_INVALID_ARG;
+    if (n > 0 && (!src || !dst || !weights)) return HUGE_ERR_INVALID_ARG;
     return HUGE_OK;
 }
 
@@ -306,17 +308,20 @@ hipError_t wait_on(hipStream_t s, hipEvent_t e, hipStream_t from) {
 // prefixes over tiles, of a batch, into the next slot, on the grouping
 // stream s (launches only; arguments checked).
 huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
-                         const int32_t* cc, int64_t n, uint64_t first_pos, hipStream_t s) {
+                         const int32_t* cc, const float* w, int64_t n, uint64_t first_pos,
+                         hipStream_t s) {
     const int slot = (int)(h->prepared % kSlots);
     const SlotLayout& SL = h->lay.slot[slot];
     Control* ctl = at<Control>(h, SL.ctrl);
     uint32_t* hist = at<uint32_t>(h, SL.hist);
     const TableArgs t = table_args(h);
-    const StepArgs a{src, dst, cc, n, first_pos, 0.0f, nullptr};
+    StepArgs a{src, dst, cc, n, first_pos, 0.0f, nullptr};
+    a.w = w;
     PendingBatch b;
     b.src = src;
     b.dst = dst;
     b.cc = cc;
+    b.w = w;
     b.n = n;
     b.first_pos = first_pos;
     b.gstream = s;
@@ -414,7 +419,8 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
     const Layout& L = h->lay;
     Control* ctl = at<Control>(h, SL.ctrl);
     const TableArgs t = table_args(h);
-    const StepArgs a{b.src, b.dst, b.cc, b.n, b.first_pos, lr, loss_out};
+    StepArgs a{b.src, b.dst, b.cc, b.n, b.first_pos, lr, loss_out};
+    a.w = b.w;
     const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
     int32_t* neg = at<int32_t>(h, SL.neg);
     double* lossp = at<double>(h, L.lossp);
@@ -498,27 +504,82 @@ huge_status huge_attach_tables(const huge_config* cfg, float* d_S, float* d_T,
     return st;
 }
 
-huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
-                            const int32_t* d_cc, int64_t n, uint64_t first_pos_index, float lr,
-                            double* d_loss_sum, void* stream) {
-    huge_status st = check_batch_args(h, d_src, d_dst, d_cc, n);
+namespace {
+
+huge_status train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                       const int32_t* d_cc, const float* d_w, int64_t n, uint64_t first_pos_index,
+                       float lr, double* d_loss_sum, void* stream) {
+    huge_status st = check_batch_args(h, d_src, d_dst, d_cc ? (const void*)d_cc : d_w, n);
     if (st != HUGE_OK) return st;
     if (!isfinite(lr)) return HUGE_ERR_INVALID_ARG;
     if (h->prepared != h->applied) return HUGE_ERR_INVALID_ARG;  // a prepared batch is pending
     hipStream_t s = static_cast<hipStream_t>(stream);
-    st = stage_sample(h, d_src, d_dst, d_cc, n, first_pos_index, s);
+    st = stage_sample(h, d_src, d_dst, d_cc, d_w, n, first_pos_index, s);
     if (st != HUGE_OK) return st;
     return apply_next(h, lr, d_loss_sum, s);
+}
+
+huge_status prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                         const int32_t* d_cc, const float* d_w, int64_t n,
+                         uint64_t first_pos_index, void* stream) {
+    huge_status st = check_batch_args(h, d_src, d_dst, d_cc ? (const void*)d_cc : d_w, n);
+    if (st != HUGE_OK) return st;
+    if (h->prepared - h->applied >= kMaxPending) return HUGE_ERR_INVALID_ARG;
+    return stage_sample(h, d_src, d_dst, d_cc, d_w, n, first_pos_index,
+                        static_cast<hipStream_t>(stream));
+}
+
+huge_status eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                      const int32_t* d_cc, const float* d_w, int64_t n, uint64_t first_pos_index,
+                      double* d_loss_sum, void* stream) {
+    huge_status st = check_batch_args(h, d_src, d_dst, d_cc ? (const void*)d_cc : d_w, n);
+    if (st != HUGE_OK) return st;
+    if (!d_loss_sum) return HUGE_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Layout& L = h->lay;
+    Control* ctl = at<Control>(h, L.eval_ctrl);
+    // the loss partials are shared with applies: order after the last one
+    if (h->last_applied_slot >= 0)
+        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
+    double* lossp = at<double>(h, L.lossp);
+    StepArgs a{d_src, d_dst, d_cc, n, first_pos_index, 0.0f, d_loss_sum};
+    a.w = d_w;
+    HIP_TRY(launch_begin(ctl, s));
+    int64_t blocks = 0;
+    HIP_TRY(launch_eval(table_args(h), ctl, a, lossp, &blocks, s));
+    HIP_TRY(launch_loss_final(ctl, lossp, blocks, d_loss_sum, s));
+    return HUGE_OK;
+}
+
+}  // namespace
+
+huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                            const int32_t* d_cc, int64_t n, uint64_t first_pos_index, float lr,
+                            double* d_loss_sum, void* stream) {
+    if (n > 0 && !d_cc) return HUGE_ERR_INVALID_ARG;
+    return train_step(h, d_src, d_dst, d_cc, nullptr, n, first_pos_index, lr, d_loss_sum, stream);
+}
+
+huge_status huge_train_step_weighted(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                                     const float* d_weight, int64_t n, uint64_t first_pos_index,
+                                     float lr, double* d_loss_sum, void* stream) {
+    if (n > 0 && !d_weight) return HUGE_ERR_INVALID_ARG;
+    return train_step(h, d_src, d_dst, nullptr, d_weight, n, first_pos_index, lr, d_loss_sum,
+                      stream);
 }
 
 huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
                               const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                               void* stream) {
-    huge_status st = check_batch_args(h, d_src, d_dst, d_cc, n);
-    if (st != HUGE_OK) return st;
-    if (h->prepared - h->applied >= kMaxPending) return HUGE_ERR_INVALID_ARG;
-    return stage_sample(h, d_src, d_dst, d_cc, n, first_pos_index,
-                        static_cast<hipStream_t>(stream));
+    if (n > 0 && !d_cc) return HUGE_ERR_INVALID_ARG;
+    return prepare_step(h, d_src, d_dst, d_cc, nullptr, n, first_pos_index, stream);
+}
+
+huge_status huge_prepare_step_weighted(huge_handle* h, const int32_t* d_src,
+                                       const int32_t* d_dst, const float* d_weight, int64_t n,
+                                       uint64_t first_pos_index, void* stream) {
+    if (n > 0 && !d_weight) return HUGE_ERR_INVALID_ARG;
+    return prepare_step(h, d_src, d_dst, nullptr, d_weight, n, first_pos_index, stream);
 }
 
 huge_status huge_train_prepared(huge_handle* h, float lr, double* d_loss_sum, void* stream) {
@@ -530,21 +591,27 @@ huge_status huge_train_prepared(huge_handle* h, float lr, double* d_loss_sum, vo
 huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
                            const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                            double* d_loss_sum, void* stream) {
-    huge_status st = check_batch_args(h, d_src, d_dst, d_cc, n);
-    if (st != HUGE_OK) return st;
-    if (!d_loss_sum) return HUGE_ERR_INVALID_ARG;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const Layout& L = h->lay;
-    Control* ctl = at<Control>(h, L.eval_ctrl);
-    // the loss partials are shared with applies: order after the last one
-    if (h->last_applied_slot >= 0)
-        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
-    double* lossp = at<double>(h, L.lossp);
-    StepArgs a{d_src, d_dst, d_cc, n, first_pos_index, 0.0f, d_loss_sum};
-    HIP_TRY(launch_begin(ctl, s));
-    int64_t blocks = 0;
-    HIP_TRY(launch_eval(table_args(h), ctl, a, lossp, &blocks, s));
-    HIP_TRY(launch_loss_final(ctl, lossp, blocks, d_loss_sum, s));
+    if (n > 0 && !d_cc) return HUGE_ERR_INVALID_ARG;
+    return eval_loss(h, d_src, d_dst, d_cc, nullptr, n, first_pos_index, d_loss_sum, stream);
+}
+
+huge_status huge_eval_loss_weighted(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
+                                    const float* d_weight, int64_t n, uint64_t first_pos_index,
+                                    double* d_loss_sum, void* stream) {
+    if (n > 0 && !d_weight) return HUGE_ERR_INVALID_ARG;
+    return eval_loss(h, d_src, d_dst, nullptr, d_weight, n, first_pos_index, d_loss_sum, stream);
+}
+
+huge_status huge_cocount_weights(const int32_t* d_hist, int64_t n, int32_t window,
+                                 const float* h_dist_weights, float* d_weight, void* stream) {
+    if (n < 0 || window < 1 || window > kMaxHistWindow || !h_dist_weights ||
+        (n > 0 && (!d_hist || !d_weight)))
+        return HUGE_ERR_INVALID_ARG;
+    for (int32_t d = 0; d < window; ++d)
+        if (!(h_dist_weights[d] >= 0.0f && h_dist_weights[d] <= 3.402823466e38f))
+            return HUGE_ERR_INVALID_ARG;
+    HIP_TRY(launch_cocount_weights(d_hist, n, window, h_dist_weights, d_weight,
+                                   static_cast<hipStream_t>(stream)));
     return HUGE_OK;
 }
 

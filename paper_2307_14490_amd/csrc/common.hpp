@@ -171,11 +171,12 @@ inline RowShape row_shape(int dim) {
 struct StepArgs {
     const int32_t* src;
     const int32_t* dst;
-    const int32_t* cc;
+    const int32_t* cc;         // integer co_counts, or
     int64_t n;
     uint64_t first_pos;
     float lr;
     double* loss_out;
+    const float* w = nullptr;  // a float weight per positive (then cc is unused)
 };
 
 struct TableArgs {
@@ -245,6 +246,10 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_walks(const WalkArgs& A, uint32_t* counts, uint64_t* offsets, int64_t* total,
                         int64_t capacity, int32_t* src, int32_t* dst, int32_t* cc, int32_t* hist,
                         int32_t* status, hipStream_t s);
+// Per-positive weights from distance histograms (k_tables.hip)
+constexpr int kMaxHistWindow = 32;
+hipError_t launch_cocount_weights(const int32_t* hist, int64_t n, int window, const float* wd,
+                                  float* out, hipStream_t s);
 // Embedding evaluation (k_eval.hip)
 hipError_t launch_eval_status_clear(int32_t* status, hipStream_t s);
 hipError_t launch_eval_pairs(const int64_t* off, const int32_t* nbr, int64_t N, int64_t E,

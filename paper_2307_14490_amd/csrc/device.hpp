@@ -117,6 +117,21 @@ struct RowIO {
 };
 
 // Record the first error since the last huge_check and flag this call.
+// Weight c_i of positive i: its float weight where weights are given, else
+// its integer co_count.
+__device__ __forceinline__ float positive_weight(const StepArgs& a, int64_t i) {
+    return a.w != nullptr ? a.w[i] : (float)a.cc[i];
+}
+
+// A usable weight: finite and >= 0 (a co_count >= 0).
+__device__ __forceinline__ bool weight_valid(const StepArgs& a, int64_t i) {
+    if (a.w != nullptr) {
+        const float c = a.w[i];
+        return c >= 0.f && c <= 3.402823466e38f;
+    }
+    return a.cc[i] >= 0;
+}
+
 __device__ __forceinline__ void raise_error(Control* ctl, uint32_t bit) {
     atomicOr(&ctl->step_bad, bit);
     atomicCAS(&ctl->error, 0u, bit);

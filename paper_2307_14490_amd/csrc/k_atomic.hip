@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kBlock) void k_atomic_gather(TableArgs t, Control* 
         // changed before its apply is reported instead of read out of bounds
         const int32_t u = a.src[i], v = a.dst[i];
         if (u >= 0 && (int64_t)u < t.N && v >= 0 && (int64_t)v < t.N) {
-            const float l = forward_positive<G, C, false>(t, a, i, u, v, (float)a.cc[i], neg, lane,
+            const float l = forward_positive<G, C, false>(t, a, i, u, v, positive_weight(a, i), neg, lane,
                                                           coef, gsrc);
             if (lane == 0) loss = l;
         } else if (lane == 0) {
@@ -194,12 +194,13 @@ __global__ __launch_bounds__(kBlock) void k_eval(TableArgs t, Control* __restric
     const int64_t i = (int64_t)blockIdx.x * PPB + threadIdx.x / G;
     float loss = 0.f;
     if (i < a.n) {
-        const int32_t u = a.src[i], v = a.dst[i], c = a.cc[i];
+        const int32_t u = a.src[i], v = a.dst[i];
         const bool ok_id = u >= 0 && (int64_t)u < t.N && v >= 0 && (int64_t)v < t.N;
-        if (!ok_id || c < 0) {
+        const float c = weight_valid(a, i) ? positive_weight(a, i) : -1.f;
+        if (!ok_id || c < 0.f) {
             if (lane == 0) raise_error(ctl, ok_id ? kBadCount : kBadId);
         } else {
-            const float l = forward_positive<G, C, true>(t, a, i, u, v, (float)c, nullptr, lane,
+            const float l = forward_positive<G, C, true>(t, a, i, u, v, c, nullptr, lane,
                                                          nullptr, nullptr);
             if (lane == 0) loss = l;
         }

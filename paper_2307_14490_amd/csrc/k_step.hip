@@ -57,7 +57,8 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     // are checked again so that a batch changed before its apply is reported
     // instead of read out of bounds.
     bool active = i < a.n;
-    int32_t u = 0, v = 0, cnt_i = 0, info_s = -1, info_d = -1;
+    int32_t u = 0, v = 0, info_s = -1, info_d = -1;
+    float c_i = 0.f;
     int32_t mk[NB], ik[NB];
     const int64_t o = i * (int64_t)(2 + K);
     const int32_t* negi = neg + i * (int64_t)K;
@@ -66,7 +67,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     if (active) {
         u = a.src[i];
         v = a.dst[i];
-        cnt_i = a.cc[i];
+        c_i = positive_weight(a, i);
         info_s = info[o];
         info_d = info[o + 1];
 #pragma unroll
@@ -82,7 +83,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
         }
     }
     if (active) {
-        const float c = (float)cnt_i;
+        const float c = c_i;
         float4 s[C], t0[C], dS[C];
         float4 tk[NB][C];
         IO::load(s, S, u, D, lane);

@@ -144,7 +144,7 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
                 u = 0;
                 v = 0;
             }
-            if (a.cc[i] < 0) raise_error(ctl, kBadCount);
+            if (!weight_valid(a, i)) raise_error(ctl, kBadCount);
             if (with_keys) {
                 put(i * S, (uint32_t)((uint64_t)t.N + (uint64_t)u));
                 put(i * S + 1, (uint32_t)v);
@@ -179,6 +179,41 @@ hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, in
     if (t.K < 1 || t.K > kBlock) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
                        info);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Weights from distance histograms: w_i = sum_d wd[d] hist[i window + d],
+// products and sums in double rounded once each (no fused multiply-add), d
+// ascending, then rounded once to float.  A negative count gives NaN.
+// ---------------------------------------------------------------------------
+struct DistWeights {
+    float w[kMaxHistWindow];
+};
+
+__global__ __launch_bounds__(kBlock) void k_cocount_weights(const int32_t* __restrict__ hist,
+                                                            int64_t n, int window, DistWeights wd,
+                                                            float* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= n) return;
+    double sum = 0.0;
+    bool bad = false;
+    for (int d = 0; d < window; ++d) {
+        const int32_t h = hist[i * window + d];
+        bad = bad || h < 0;
+        sum = __dadd_rn(sum, __dmul_rn((double)wd.w[d], (double)h));
+    }
+    out[i] = bad ? __builtin_nanf("") : __double2float_rn(sum);
+}
+
+hipError_t launch_cocount_weights(const int32_t* hist, int64_t n, int window, const float* wd,
+                                  float* out, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    if (window < 1 || window > kMaxHistWindow) return hipErrorInvalidValue;
+    DistWeights W;
+    for (int d = 0; d < kMaxHistWindow; ++d) W.w[d] = d < window ? wd[d] : 0.f;
+    hipLaunchKernelGGL(k_cocount_weights, dim3((unsigned)((n + kBlock - 1) / kBlock)),
+                       dim3(kBlock), 0, s, hist, n, window, W, out);
     return hipGetLastError();
 }
 
