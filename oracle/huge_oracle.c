@@ -683,3 +683,105 @@ int oracle_eval_pairs(const int64_t *off, const int32_t *nbr, int64_t num_nodes,
     }
     return OR_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* bfloat16 tables (the paper's TPUs compute in half precision, Sec. 2.3).    */
+/* A bf16 value is a float32 whose 16 low mantissa bits are zero: 1 sign bit, */
+/* 8 exponent bits, 7 mantissa bits; stored as its 16 high bits.             */
+/* ------------------------------------------------------------------------- */
+/* The bf16 nearest to x (ties to the even mantissa), from x itself: no       */
+/* intermediate rounding to float.  Overflow gives infinity, NaN a quiet NaN. */
+uint16_t oracle_bf16_from_double(double x) {
+    if (x != x) return 0x7FC0u;
+    const uint16_t sign = signbit(x) ? 0x8000u : 0u;
+    const double a = fabs(x);
+    if (a == 0.0) return sign;
+    int e;
+    frexp(a, &e);           /* a in [2^(e-1), 2^e) */
+    int E = e - 1;
+    if (E < -126) E = -126; /* subnormals share the smallest quantum */
+    const double q = ldexp(1.0, E - 7);
+    const double r = a / q; /* exact: q is a power of two */
+    double n = floor(r);
+    const double frac = r - n;
+    if (frac > 0.5 || (frac == 0.5 && fmod(n, 2.0) != 0.0)) n += 1.0;
+    const double v = n * q;
+    if (v >= ldexp(1.0, 128)) return (uint16_t)(sign | 0x7F80u);
+    const float f = (float)v; /* exact: v is a bf16 value */
+    uint32_t bits;
+    memcpy(&bits, &f, 4);
+    return (uint16_t)(sign | (uint16_t)(bits >> 16));
+}
+
+double oracle_bf16_to_double(uint16_t h) {
+    const uint32_t bits = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &bits, 4);
+    return (double)f;
+}
+
+/* Initial rows of bf16 tables: the float initial values rounded to bf16. */
+int oracle_init_rows_bf16(uint64_t seed, int32_t table, const int64_t *rows, int64_t nrows,
+                          int32_t dim, float half_width, uint16_t *out) {
+    if (nrows < 0 || dim <= 0 || (nrows > 0 && (!rows || !out))) return OR_EINVAL;
+    float *tmp = (float *)malloc(sizeof(float) * (size_t)dim);
+    if (!tmp) return OR_EINVAL;
+    for (int64_t r = 0; r < nrows; ++r) {
+        int rc = oracle_init_rows(seed, table, rows + r, 1, dim, half_width, tmp);
+        if (rc) { free(tmp); return rc; }
+        for (int32_t d = 0; d < dim; ++d)
+            out[r * dim + d] = oracle_bf16_from_double((double)tmp[d]);
+    }
+    free(tmp);
+    return OR_OK;
+}
+
+/* One step on bf16 tables: widened to double, the same gradient as the float
+   step, and each touched element rewritten once as
+   bf16_nearest((double)row - (double)lr * grad).  cc or wf as in the float
+   steps (exactly one given). */
+int oracle_sgns_step_bf16(uint16_t *S, uint16_t *T, int64_t ns, int64_t nt, int32_t dim,
+                          int64_t n, int32_t num_neg, const int32_t *src, const int32_t *dst,
+                          const int32_t *cc, const float *wf, const int32_t *neg, float lr,
+                          double *loss_out) {
+    if (!S || !T || dim <= 0 || n < 0 || num_neg < 1 || !loss_out) return OR_EINVAL;
+    if (n > 0 && (!src || !dst || (!cc && !wf) || !neg)) return OR_EINVAL;
+    int rc = check_batch(ns, nt, n, num_neg, src, dst, cc, wf, neg);
+    if (rc) return rc;
+    size_t s_elems = (size_t)ns * (size_t)dim, t_elems = (size_t)nt * (size_t)dim;
+    double *Sd = (double *)malloc(s_elems * sizeof(double));
+    double *Td = (double *)malloc(t_elems * sizeof(double));
+    double *gS = (double *)malloc(s_elems * sizeof(double));
+    double *gT = (double *)malloc(t_elems * sizeof(double));
+    unsigned char *touched_S = (unsigned char *)calloc((size_t)ns, 1);
+    unsigned char *touched_T = (unsigned char *)calloc((size_t)nt, 1);
+    if (!Sd || !Td || !gS || !gT || !touched_S || !touched_T) {
+        free(Sd); free(Td); free(gS); free(gT); free(touched_S); free(touched_T);
+        return OR_EINVAL;
+    }
+    for (size_t e = 0; e < s_elems; ++e) Sd[e] = oracle_bf16_to_double(S[e]);
+    for (size_t e = 0; e < t_elems; ++e) Td[e] = oracle_bf16_to_double(T[e]);
+    double loss = 0.0;
+    rc = sgns_grad_d(Sd, Td, ns, nt, dim, n, num_neg, src, dst, cc, wf, neg, gS, gT, &loss);
+    if (rc == OR_OK) {
+        for (int64_t i = 0; i < n; ++i) {
+            touched_S[src[i]] = 1;
+            touched_T[dst[i]] = 1;
+            for (int32_t k = 0; k < num_neg; ++k) touched_T[neg[i * num_neg + k]] = 1;
+        }
+        const double lr_d = (double)lr;
+        for (int64_t r = 0; r < ns; ++r)
+            if (touched_S[r])
+                for (int32_t d = 0; d < dim; ++d)
+                    S[r * dim + d] =
+                        oracle_bf16_from_double(Sd[r * dim + d] - lr_d * gS[r * dim + d]);
+        for (int64_t r = 0; r < nt; ++r)
+            if (touched_T[r])
+                for (int32_t d = 0; d < dim; ++d)
+                    T[r * dim + d] =
+                        oracle_bf16_from_double(Td[r * dim + d] - lr_d * gT[r * dim + d]);
+        *loss_out = loss;
+    }
+    free(Sd); free(Td); free(gS); free(gT); free(touched_S); free(touched_T);
+    return rc;
+}

@@ -88,6 +88,17 @@ def lib():
         L.oracle_sgns_step_w.argtypes = w_args + [ctypes.c_float, _f64p]
         L.oracle_sgns_loss_w.argtypes = w_args + [_f64p]
         L.oracle_cocount_weights.argtypes = [_i32p, ctypes.c_int64, ctypes.c_int32, _f32p, _f32p]
+        _u16p = ctypes.POINTER(ctypes.c_uint16)
+        L.oracle_bf16_from_double.argtypes = [ctypes.c_double]
+        L.oracle_bf16_from_double.restype = ctypes.c_uint16
+        L.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+        L.oracle_bf16_to_double.restype = ctypes.c_double
+        L.oracle_init_rows_bf16.argtypes = [ctypes.c_uint64, ctypes.c_int32, _i64p,
+                                            ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _u16p]
+        L.oracle_sgns_step_bf16.argtypes = [_u16p, _u16p, ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.c_int32, ctypes.c_int64, ctypes.c_int32,
+                                            _i32p, _i32p, _i32p, _f32p, _i32p, ctypes.c_float,
+                                            _f64p]
         L.oracle_sample_walks.argtypes = [_i64p, _i32p, ctypes.c_int64, ctypes.c_int64,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                           ctypes.c_int32, ctypes.c_uint64, ctypes.c_int64,
@@ -100,7 +111,7 @@ def lib():
                      "oracle_sample_walks", "oracle_eval_pairs",
                      "oracle_sgns_grad_d", "oracle_sgns_loss_d", "oracle_sgns_step",
                      "oracle_sgns_loss", "oracle_sgns_step_w", "oracle_sgns_loss_w",
-                     "oracle_cocount_weights"):
+                     "oracle_cocount_weights", "oracle_init_rows_bf16", "oracle_sgns_step_bf16"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -472,3 +483,48 @@ def recall_at_k(off, nbr, queries, nearest, k: int) -> np.ndarray:
         S = set(int(x) for x in np.asarray(nearest[qi])[:k])
         out[qi] = len(nb & S) / k
     return out
+
+
+# --------------------------------------------------------------------------- #
+# bfloat16 tables (arrays of uint16: the 16 high bits of a float32)
+# --------------------------------------------------------------------------- #
+def bf16_from_double(x: float) -> int:
+    """The bf16 nearest to x (ties to even), rounded once from x."""
+    return int(lib().oracle_bf16_from_double(float(x)))
+
+
+def bf16_to_float(h) -> np.ndarray:
+    """Exact widening of uint16 bf16 values to float32."""
+    h = np.asarray(h, np.uint16)
+    return (h.astype(np.uint32) << 16).view(np.float32)
+
+
+def init_rows_bf16(seed: int, table: int, rows, dim: int, half_width: float) -> np.ndarray:
+    r = _c(rows, np.int64)
+    out = np.empty((r.size, dim), np.uint16)
+    _check(lib().oracle_init_rows_bf16(seed, table, _ptr(r, _i64p), r.size, dim, half_width,
+                                       out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint16))),
+           "init_rows_bf16")
+    return out
+
+
+def step_dense_bf16(S: np.ndarray, T: np.ndarray, src, dst, cc, neg, lr: float) -> float:
+    """One step in place on bf16 tables (uint16, C-contiguous); cc: integer
+    co_counts or float32 weights.  Returns the loss sum (at pre-step values)."""
+    assert S.dtype == np.uint16 and T.dtype == np.uint16
+    assert S.flags.c_contiguous and T.flags.c_contiguous
+    src, dst = _c(src, np.int32), _c(dst, np.int32)
+    neg = _as_neg(neg, len(src))
+    n, K = neg.shape
+    if np.asarray(cc).dtype.kind == "f":
+        ci, wf = None, _c(cc, np.float32)
+    else:
+        ci, wf = _c(cc, np.int32), None
+    u16 = ctypes.POINTER(ctypes.c_uint16)
+    loss = ctypes.c_double()
+    _check(lib().oracle_sgns_step_bf16(S.ctypes.data_as(u16), T.ctypes.data_as(u16), S.shape[0],
+                                       T.shape[0], S.shape[1], n, K, _ptr(src, _i32p),
+                                       _ptr(dst, _i32p), _ptr(ci, _i32p), _ptr(wf, _f32p),
+                                       _ptr(neg, _i32p), lr, ctypes.byref(loss)),
+           "sgns_step_bf16")
+    return loss.value
