@@ -28,7 +28,10 @@ if ROOT not in sys.path:
 METRIC = "positive (src,dst) pairs/sec per train step; achieved HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
 KERNEL = "k_fused_step"
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "fused_step_sbm100m_counters.txt")
+COUNTERS_FILES = {  # committed rocprofv3 HBM counters of the fused kernel, per table type
+    "f32": os.path.join(ROOT, "profiles", "fused_step_sbm100m_counters.txt"),
+    "bf16": os.path.join(ROOT, "profiles", "fused_step_sbm100m_bf16_counters.txt"),
+}
 KERNEL_SOURCES = ["paper_2307_14490_amd/csrc/device.hpp", "paper_2307_14490_amd/csrc/k_step.hip"]
 KERNEL_END = "int64_t fused_step_blocks("  # the fused kernel's source ends before this line
 PROFILE_EVERY = 4  # timed steps whose fused kernel is bracketed by HIP events
@@ -47,13 +50,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload: str, n_launch_units: float):
+def read_traffic(workload: str, dtype: str = "f32"):
     """HBM bytes per launch of the fused kernel from committed rocprofv3
     counters, if they were taken on the current kernel source."""
-    if workload != "sbm100m" or not os.path.exists(COUNTERS_FILE):
+    path = COUNTERS_FILES.get(dtype)
+    if workload != "sbm100m" or path is None or not os.path.exists(path):
         return None
     kv = {}
-    with open(COUNTERS_FILE) as f:
+    with open(path) as f:
         for line in f:
             if "=" in line and not line.startswith("#"):
                 k, v = line.split("=", 1)
@@ -397,6 +401,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="sbm100m")
     ap.add_argument("--scatter", default="sorted", choices=["sorted", "atomic"])
+    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"],
+                    help="element type of the tables (bf16: sorted scatter only)")
     ap.add_argument("--batches", type=int, default=16, help="distinct pre-staged batches")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
@@ -450,9 +456,10 @@ def main():
     dev_batches = [tuple(torch.from_numpy(x).cuda() for x in b) for b in host_batches]
 
     tr = P.Trainer(cfg.num_nodes, cfg.dim, cfg.num_neg, cfg.batch, seed=args.seed,
-                   alias_weights=wl.weights, scatter=args.scatter)
+                   alias_weights=wl.weights, scatter=args.scatter, dtype=args.dtype)
     torch.cuda.synchronize()
-    log(f"[bench] tables initialised: 2 x {cfg.num_nodes} x {cfg.dim} fp32")
+    log(f"[bench] tables initialised: 2 x {cfg.num_nodes} x {cfg.dim} {args.dtype}")
+    eb = 2.0 if args.dtype == "bf16" else 4.0  # bytes per table element
     n = cfg.batch
     K = cfg.num_neg
     D = cfg.dim
@@ -548,7 +555,7 @@ def main():
     probe_us = ev0.elapsed_time(ev1) / n_probe * 1e3
     if tr.check() != 0:
         raise RuntimeError("device reported an error in the probe")
-    probe_bytes = 8.0 * n + 2.0 * 4.0 * D * n * (2 + K)
+    probe_bytes = 8.0 * n + 2.0 * eb * D * n * (2 + K)
     probe_gbps = probe_bytes / (probe_us * 1e-6) / 1e9
     log(f"[bench] probe: {probe_us:.1f} us per launch, {probe_gbps:.0f} GB/s")
 
@@ -566,23 +573,24 @@ def main():
     phase_avg_us = {p: diag_ms[i] / max(diag_steps, 1) * 1e3 for i, p in enumerate(phases)}
 
     # Algorithmic bytes of the fused kernel per launch: the batch (12 B per
-    # positive), each distinct row read once (4 D bytes) and each row that
-    # occurs once written once in place.  Repeated rows are written by the
-    # duplicate kernels, not counted here.
+    # positive), each distinct row read once (eb D bytes, eb = 4 for fp32 and
+    # 2 for bf16 elements) and each row that occurs once written once in
+    # place.  Repeated rows are written by the duplicate kernels, not counted
+    # here.
     if args.scatter == "sorted":
         seq = [(args.warmup + k) % R for k in range(args.steps)]
         uS = np.mean([per_batch_stats[b][0] for b in seq])
         uT = np.mean([per_batch_stats[b][1] for b in seq])
         dup = np.mean([per_batch_stats[b][2] for b in seq])
         occ = n * (2 + K)
-        kernel_bytes = 12.0 * n + 4.0 * D * (uS + uT) + 4.0 * D * (occ - dup)
-        step_bytes = 12.0 * n + 8.0 * D * (uS + uT)
+        kernel_bytes = 12.0 * n + eb * D * (uS + uT) + eb * D * (occ - dup)
+        step_bytes = 12.0 * n + 2.0 * eb * D * (uS + uT)
     else:
         uS = uT = dup = None
         kernel_bytes = 12.0 * n + 4.0 * D * n * (2 + K)  # gather kernel: every row read
         step_bytes = 12.0 * n + 8.0 * D * n * (2 + K)
     achieved = kernel_bytes / (fused_us * 1e-6) / 1e9
-    traffic = read_traffic(cfg.name, n)
+    traffic = read_traffic(cfg.name, args.dtype) if args.scatter == "sorted" else None
     out = {
         "metric": METRIC,
         "value": value,
@@ -604,6 +612,7 @@ def main():
             "batch": n,
             "negatives": cfg.neg_kind,
             "scatter": args.scatter,
+            "tables": args.dtype,
             "lr": cfg.lr,
             "staged_batches": R,
             "grouping": ("sequential" if args.sequential else

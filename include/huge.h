@@ -68,6 +68,17 @@ typedef int32_t huge_status;
 #define HUGE_SCATTER_SORTED 0
 #define HUGE_SCATTER_ATOMIC 1
 
+/* Element type of the two tables.  F32: IEEE binary32.  BF16: bfloat16 (the
+   upper 16 bits of a binary32), half the bytes per row; every step reads the
+   rows widened to fp32, computes in fp32 as for F32 tables, and rounds each
+   written element to the nearest bf16, ties to even (repeated rows: their
+   fp64 sum applied in fp64, rounded to fp32, then to bf16).  The paper keeps
+   fp32 tables; BF16 halves the memory and the traffic of a step (Sec. 3.3.2
+   bounds the step by its row traffic).  BF16 works with the SORTED scatter
+   only. */
+#define HUGE_DTYPE_F32 0
+#define HUGE_DTYPE_BF16 1
+
 typedef struct huge_config {
     int64_t num_nodes;       /* N: rows of each table, 1 .. 2^31-1                       */
     int32_t dim;             /* D: floats per row, multiple of 4, 4 .. 1024              */
@@ -77,6 +88,7 @@ typedef struct huge_config {
     float init_half_width;   /* a: initial values U[-a, a); 0 selects 0.5 / D            */
     int32_t neg_kind;        /* HUGE_NEG_UNIFORM or HUGE_NEG_ALIAS                       */
     int32_t scatter_kind;    /* HUGE_SCATTER_SORTED or HUGE_SCATTER_ATOMIC               */
+    int32_t table_dtype;     /* HUGE_DTYPE_F32 (0) or HUGE_DTYPE_BF16                    */
 } huge_config;
 
 typedef struct huge_handle huge_handle; /* opaque, host-side */
@@ -101,20 +113,22 @@ huge_status huge_build_alias(const double* weights, int64_t n, uint32_t* thr_out
    values: element (r, c) of table t (0 = S, 1 = T) is j * (a 2^-23) with
    j = (word >> 8) - 2^23 and word = word (c mod 4) of Philox4x32-10 on counter
    (lo32 r, hi32 r, c div 4, 2 + t) under key (lo32 seed, hi32 seed): uniform
-   on [-a, a) (the paper does not state an initialisation).
-     d_S, d_T       : N x D fp32 device tables (written)
+   on [-a, a) (the paper does not state an initialisation); a BF16 table holds
+   these values rounded to nearest, ties to even.
+     d_S, d_T       : N x D device tables of cfg->table_dtype elements,
+                      16-byte aligned (written)
      d_alias_thr,
      d_alias        : N entries each on the device (HUGE_NEG_ALIAS), else NULL
      d_workspace    : >= huge_workspace_bytes(cfg) bytes of device memory
      out            : receives the handle; destroy with huge_destroy */
-huge_status huge_init_tables(const huge_config* cfg, float* d_S, float* d_T,
+huge_status huge_init_tables(const huge_config* cfg, void* d_S, void* d_T,
                              const uint32_t* d_alias_thr, const int32_t* d_alias,
                              void* d_workspace, size_t ws_bytes, void* stream,
                              huge_handle** out);
 
 /* Same as huge_init_tables without writing the tables: for tables restored
    from a checkpoint. */
-huge_status huge_attach_tables(const huge_config* cfg, float* d_S, float* d_T,
+huge_status huge_attach_tables(const huge_config* cfg, void* d_S, void* d_T,
                                const uint32_t* d_alias_thr, const int32_t* d_alias,
                                void* d_workspace, size_t ws_bytes, huge_handle** out);
 
@@ -191,7 +205,8 @@ huge_status huge_eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* 
                            const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                            double* d_loss_sum, void* stream);
 
-/* Copy rows of table (0 = S, 1 = T) into d_out (n x D fp32, row-major).
+/* Copy rows of table (0 = S, 1 = T) into d_out (n x D fp32, row-major; rows
+   of a BF16 table are widened exactly).
    d_ids: n int64 device ids; an id outside [0, N) yields a row of NaN and
    makes huge_check report HUGE_ERR_ID_OUT_OF_RANGE. */
 huge_status huge_get_rows(huge_handle* h, int32_t table, const int64_t* d_ids, int64_t n,

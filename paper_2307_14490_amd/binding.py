@@ -26,6 +26,8 @@ HUGE_NEG_UNIFORM = 0
 HUGE_NEG_ALIAS = 1
 HUGE_SCATTER_SORTED = 0
 HUGE_SCATTER_ATOMIC = 1
+HUGE_DTYPE_F32 = 0
+HUGE_DTYPE_BF16 = 1
 
 EXPORTED = [
     "huge_workspace_bytes", "huge_build_alias", "huge_init_tables", "huge_attach_tables",
@@ -49,6 +51,7 @@ class HugeConfig(ctypes.Structure):
         ("init_half_width", ctypes.c_float),
         ("neg_kind", ctypes.c_int32),
         ("scatter_kind", ctypes.c_int32),
+        ("table_dtype", ctypes.c_int32),
     ]
 
 
@@ -154,9 +157,11 @@ def _ok(st: int, what: str):
 
 
 def make_config(num_nodes, dim, num_neg, max_batch, seed=0, init_half_width=0.0,
-                neg_kind=HUGE_NEG_UNIFORM, scatter_kind=HUGE_SCATTER_SORTED) -> HugeConfig:
+                neg_kind=HUGE_NEG_UNIFORM, scatter_kind=HUGE_SCATTER_SORTED,
+                table_dtype=HUGE_DTYPE_F32) -> HugeConfig:
     return HugeConfig(int(num_nodes), int(dim), int(num_neg), int(max_batch), int(seed),
-                      float(init_half_width), int(neg_kind), int(scatter_kind))
+                      float(init_half_width), int(neg_kind), int(scatter_kind),
+                      int(table_dtype))
 
 
 def workspace_bytes(cfg: HugeConfig) -> int:
@@ -204,27 +209,33 @@ def cocount_weights(hist, dist_weights, stream=None):
 class Trainer:
     """Tables, workspace and a libhuge handle on one GPU.
 
-    S and T are float32 torch tensors (N x D) on the device; the workspace is
-    a uint8 torch tensor.  Batches are int32 device tensors.
+    S and T are float32 (or, with dtype="bf16", bfloat16) torch tensors
+    (N x D) on the device; the workspace is a uint8 torch tensor.  Batches are
+    int32 device tensors.
     """
 
     def __init__(self, num_nodes, dim, num_neg, max_batch, seed=0, init_half_width=0.0,
                  alias_weights=None, scatter="sorted", device="cuda", tables=None,
-                 init=True):
+                 init=True, dtype="f32"):
         import torch
         load()
         self.device = torch.device(device)
         kind = HUGE_NEG_ALIAS if alias_weights is not None else HUGE_NEG_UNIFORM
         sk = {"sorted": HUGE_SCATTER_SORTED, "atomic": HUGE_SCATTER_ATOMIC}[scatter]
-        self.cfg = make_config(num_nodes, dim, num_neg, max_batch, seed, init_half_width, kind, sk)
+        td = {"f32": HUGE_DTYPE_F32, "bf16": HUGE_DTYPE_BF16}[dtype]
+        tdt = torch.bfloat16 if td == HUGE_DTYPE_BF16 else torch.float32
+        self.cfg = make_config(num_nodes, dim, num_neg, max_batch, seed, init_half_width, kind, sk,
+                               td)
         ws = workspace_bytes(self.cfg)
         if ws == 0:
             raise HugeError(HUGE_ERR_INVALID_ARG, "huge_workspace_bytes")
         if tables is None:
-            self.S = torch.empty((num_nodes, dim), dtype=torch.float32, device=self.device)
-            self.T = torch.empty((num_nodes, dim), dtype=torch.float32, device=self.device)
+            self.S = torch.empty((num_nodes, dim), dtype=tdt, device=self.device)
+            self.T = torch.empty((num_nodes, dim), dtype=tdt, device=self.device)
         else:
             self.S, self.T = tables
+            if self.S.dtype != tdt or self.T.dtype != tdt:
+                raise ValueError(f"tables must be {tdt}")
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=self.device)
         if kind == HUGE_NEG_ALIAS:
             thr, alias = build_alias(alias_weights)

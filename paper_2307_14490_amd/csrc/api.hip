@@ -55,8 +55,8 @@ struct PendingBatch {
 
 struct huge_handle {
     huge_config cfg;
-    float* S;
-    float* T;
+    void* S;  // rows of cfg.table_dtype
+    void* T;
     const uint32_t* thr;
     const int32_t* alias;
     uint8_t* ws;
@@ -104,6 +104,9 @@ bool config_ok(const huge_config* c) {
     if (c->neg_kind != HUGE_NEG_UNIFORM && c->neg_kind != HUGE_NEG_ALIAS) return false;
     if (c->scatter_kind != HUGE_SCATTER_SORTED && c->scatter_kind != HUGE_SCATTER_ATOMIC)
         return false;
+    if (c->table_dtype != HUGE_DTYPE_F32 && c->table_dtype != HUGE_DTYPE_BF16) return false;
+    // the atomic scatter adds in float
+    if (c->table_dtype == HUGE_DTYPE_BF16 && c->scatter_kind == HUGE_SCATTER_ATOMIC) return false;
     return true;
 }
 
@@ -186,6 +189,7 @@ TableArgs table_args(huge_handle* h) {
     t.seed = h->cfg.seed;
     t.thr = h->cfg.neg_kind == HUGE_NEG_ALIAS ? h->thr : nullptr;
     t.alias = h->cfg.neg_kind == HUGE_NEG_ALIAS ? h->alias : nullptr;
+    t.dtype = h->cfg.table_dtype == HUGE_DTYPE_BF16 ? kDtypeBf16 : kDtypeF32;
     return t;
 }
 
@@ -219,7 +223,7 @@ void destroy_handle(huge_handle* h) {
     delete h;
 }
 
-huge_status create(const huge_config* cfg, float* S, float* T, const uint32_t* thr,
+huge_status create(const huge_config* cfg, void* S, void* T, const uint32_t* thr,
                    const int32_t* alias, void* ws, size_t ws_bytes, huge_handle** out) {
     if (!out) return HUGE_ERR_INVALID_ARG;
     *out = nullptr;
@@ -473,7 +477,7 @@ size_t huge_workspace_bytes(const huge_config* cfg) {
     return make_layout(cfg).total;
 }
 
-huge_status huge_init_tables(const huge_config* cfg, float* d_S, float* d_T,
+huge_status huge_init_tables(const huge_config* cfg, void* d_S, void* d_T,
                              const uint32_t* d_alias_thr, const int32_t* d_alias,
                              void* d_workspace, size_t ws_bytes, void* stream, huge_handle** out) {
     huge_status st = create(cfg, d_S, d_T, d_alias_thr, d_alias, d_workspace, ws_bytes, out);
@@ -490,7 +494,7 @@ huge_status huge_init_tables(const huge_config* cfg, float* d_S, float* d_T,
     return st;
 }
 
-huge_status huge_attach_tables(const huge_config* cfg, float* d_S, float* d_T,
+huge_status huge_attach_tables(const huge_config* cfg, void* d_S, void* d_T,
                                const uint32_t* d_alias_thr, const int32_t* d_alias,
                                void* d_workspace, size_t ws_bytes, huge_handle** out) {
     huge_status st = create(cfg, d_S, d_T, d_alias_thr, d_alias, d_workspace, ws_bytes, out);

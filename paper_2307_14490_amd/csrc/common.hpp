@@ -179,15 +179,22 @@ struct StepArgs {
     const float* w = nullptr;  // a float weight per positive (then cc is unused)
 };
 
+// Element type of the tables (the public HUGE_DTYPE_* values).
+enum : int32_t { kDtypeF32 = 0, kDtypeBf16 = 1 };
+
+// A bfloat16 element: the upper 16 bits of an IEEE binary32.
+typedef uint16_t bf16_t;
+
 struct TableArgs {
-    float* S;
-    float* T;
+    void* S;               // float or bf16_t rows, as dtype says
+    void* T;
     int64_t N;
     int32_t D;
     int32_t K;
     uint64_t seed;
     const uint32_t* thr;   // alias thresholds or nullptr (uniform)
     const int32_t* alias;
+    int32_t dtype;         // kDtypeF32 or kDtypeBf16
 };
 
 struct WalkArgs {

@@ -84,28 +84,64 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) {
 
 __device__ __forceinline__ float4 zero4() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 
-// Row r of a D-float table as float4 chunks; lane l of a group owns chunks
-// l, l + G, ..., l + (C-1) G, those below D/4 are valid.
-template <int G, int C>
+// bfloat16 <-> float.  Widening is exact.  Narrowing rounds to nearest, ties
+// to even, on the bit pattern: adding 0x7FFF plus the lowest kept bit carries
+// into the kept half exactly when the dropped half is above one half, or
+// equal to it with the kept half odd; overflow reaches infinity.  A NaN stays
+// a (quiet) NaN.
+__device__ __forceinline__ float4 bf16x4_to_float4(uint2 w) {
+    return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u),
+                       __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xFFFF0000u));
+}
+
+__device__ __forceinline__ uint32_t float_to_bf16_bits(float f) {
+    const uint32_t b = __float_as_uint(f);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u) return (b >> 16) | 0x0040u;
+    return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ uint2 float4_to_bf16x4(float4 v) {
+    return make_uint2(float_to_bf16_bits(v.x) | (float_to_bf16_bits(v.y) << 16),
+                      float_to_bf16_bits(v.z) | (float_to_bf16_bits(v.w) << 16));
+}
+
+// Chunk j (elements 4j .. 4j + 3) of a row, as float4, for either element type.
+__device__ __forceinline__ float4 load_chunk(const float* __restrict__ row, int j) {
+    return reinterpret_cast<const float4*>(row)[j];
+}
+__device__ __forceinline__ float4 load_chunk(const bf16_t* __restrict__ row, int j) {
+    return bf16x4_to_float4(reinterpret_cast<const uint2*>(row)[j]);
+}
+__device__ __forceinline__ void store_chunk(float* __restrict__ row, int j, float4 v) {
+    reinterpret_cast<float4*>(row)[j] = v;
+}
+__device__ __forceinline__ void store_chunk(bf16_t* __restrict__ row, int j, float4 v) {
+    reinterpret_cast<uint2*>(row)[j] = float4_to_bf16x4(v);
+}
+
+// Row r of a table of D elements (float or bf16_t) as float4 chunks; lane l
+// of a group owns chunks l, l + G, ..., l + (C-1) G, those below D/4 are
+// valid.  bf16 rows are widened on load and rounded on store.
+template <int G, int C, typename E = float>
 struct RowIO {
-    __device__ __forceinline__ static void load(float4 (&x)[C], const float* __restrict__ base,
+    __device__ __forceinline__ static void load(float4 (&x)[C], const E* __restrict__ base,
                                                 int64_t row, int32_t D, int lane) {
-        const float4* p = reinterpret_cast<const float4*>(base + row * (int64_t)D);
+        const E* p = base + row * (int64_t)D;
         const int q = D >> 2;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int j = lane + c * G;
-            x[c] = (j < q) ? p[j] : zero4();
+            x[c] = (j < q) ? load_chunk(p, j) : zero4();
         }
     }
-    __device__ __forceinline__ static void store(float* __restrict__ base, int64_t row,
-                                                 int32_t D, int lane, const float4 (&x)[C]) {
-        float4* p = reinterpret_cast<float4*>(base + row * (int64_t)D);
+    __device__ __forceinline__ static void store(E* __restrict__ base, int64_t row, int32_t D,
+                                                 int lane, const float4 (&x)[C]) {
+        E* p = base + row * (int64_t)D;
         const int q = D >> 2;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             const int j = lane + c * G;
-            if (j < q) p[j] = x[c];
+            if (j < q) store_chunk(p, j, x[c]);
         }
     }
     __device__ __forceinline__ static float dot(const float4 (&a)[C], const float4 (&b)[C]) {

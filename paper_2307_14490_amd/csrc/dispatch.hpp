@@ -52,3 +52,13 @@ inline int neg_block(int K) {
         default:                             \
             return hipErrorInvalidValue;     \
     }
+
+// Element type of the tables: E_ is float or bf16_t.
+#define HUGE_ELEM_DISPATCH(dtype, ...)      \
+    if ((dtype) == kDtypeBf16) {            \
+        using E_ = bf16_t;                  \
+        __VA_ARGS__;                        \
+    } else {                                \
+        using E_ = float;                   \
+        __VA_ARGS__;                        \
+    }

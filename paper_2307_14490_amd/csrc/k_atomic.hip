@@ -5,6 +5,8 @@
 // gradient; (b) adds -lr coef S[u] into the context rows with fp32 atomics
 // (S still holds pre-step values); (c) adds -lr dS into the source rows.
 // The result equals the sorted variant's up to the order of the additions.
+// It works on float tables only (bf16 has no native atomic add of the
+// precision the step needs); the loss evaluation reads either element type.
 #include "common.hpp"
 #include "device.hpp"
 #include "dispatch.hpp"
@@ -28,18 +30,20 @@ __device__ __forceinline__ void block_loss_a(float loss, double* __restrict__ ou
 
 // Forward for one positive: fills the loss sum and, when coef != nullptr,
 // the (1 + K) coefficients and the source gradient.
-template <int G, int C, bool kDrawInline>
+template <int G, int C, bool kDrawInline, typename E>
 __device__ __forceinline__ float forward_positive(const TableArgs& t, const StepArgs& a, int64_t i,
                                                   int32_t u, int32_t v, float c,
                                                   const int32_t* __restrict__ neg, int lane,
                                                   float* __restrict__ coef,
                                                   float* __restrict__ gsrc) {
-    using IO = RowIO<G, C>;
+    using IO = RowIO<G, C, E>;
+    const E* __restrict__ S = static_cast<const E*>(t.S);
+    const E* __restrict__ T = static_cast<const E*>(t.T);
     const int K = t.K;
     const int32_t D = t.D;
     float4 s[C], t0[C], dS[C];
-    IO::load(s, t.S, u, D, lane);
-    IO::load(t0, t.T, v, D, lane);
+    IO::load(s, S, u, D, lane);
+    IO::load(t0, T, v, D, lane);
     const float x = group_sum<G>(IO::dot(s, t0));
     const float g = coef_pos(c, x);
     float lsum = softplus_f(-x);
@@ -64,7 +68,7 @@ __device__ __forceinline__ float forward_positive(const TableArgs& t, const Step
         }
 #pragma unroll
         for (int j = 0; j < kNegBlock; ++j)
-            if (j < cnt) IO::load(tk[j], t.T, mk[j], D, lane);
+            if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
         float y[kNegBlock];
 #pragma unroll
         for (int j = 0; j < kNegBlock; ++j) y[j] = (j < cnt) ? IO::dot(s, tk[j]) : 0.f;
@@ -86,7 +90,7 @@ __device__ __forceinline__ float forward_positive(const TableArgs& t, const Step
             }
         }
     }
-    if (coef) IO::store(gsrc, i, D, lane, dS);
+    if (coef) RowIO<G, C>::store(gsrc, i, D, lane, dS);
     return c * lsum;
 }
 
@@ -107,8 +111,8 @@ __global__ __launch_bounds__(kBlock) void k_atomic_gather(TableArgs t, Control* 
         // changed before its apply is reported instead of read out of bounds
         const int32_t u = a.src[i], v = a.dst[i];
         if (u >= 0 && (int64_t)u < t.N && v >= 0 && (int64_t)v < t.N) {
-            const float l = forward_positive<G, C, false>(t, a, i, u, v, positive_weight(a, i), neg, lane,
-                                                          coef, gsrc);
+            const float l = forward_positive<G, C, false, float>(
+                t, a, i, u, v, positive_weight(a, i), neg, lane, coef, gsrc);
             if (lane == 0) loss = l;
         } else if (lane == 0) {
             raise_internal(ctl, kSiteAtomicIds);
@@ -135,11 +139,11 @@ __global__ __launch_bounds__(kBlock) void k_atomic_scatter_T(TableArgs t,
     const int32_t D = t.D;
     const int q4 = D >> 2;
     float4 s[C];
-    IO::load(s, t.S, u, D, lane);
+    IO::load(s, static_cast<const float*>(t.S), u, D, lane);
     for (int j = 0; j <= K; ++j) {
         const int64_t row = j == 0 ? (int64_t)v : (int64_t)neg[i * (int64_t)K + j - 1];
         const float w = -a.lr * coef[i * (int64_t)(1 + K) + j];
-        float* p = t.T + row * (int64_t)D;
+        float* p = static_cast<float*>(t.T) + row * (int64_t)D;
 #pragma unroll
         for (int q = 0; q < C; ++q) {
             const int jj = lane + q * G;
@@ -170,7 +174,7 @@ __global__ __launch_bounds__(kBlock) void k_atomic_scatter_S(TableArgs t,
     const int q4 = D >> 2;
     float4 g[C];
     IO::load(g, gsrc, i, D, lane);
-    float* p = t.S + (int64_t)u * D;
+    float* p = static_cast<float*>(t.S) + (int64_t)u * D;
     const float w = -a.lr;
 #pragma unroll
     for (int q = 0; q < C; ++q) {
@@ -186,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void k_atomic_scatter_S(TableArgs t,
 
 // Loss of a batch at the current tables; validates ids and counts itself and
 // draws the negatives inline (no workspace for them).
-template <int G, int C>
+template <int G, int C, typename E>
 __global__ __launch_bounds__(kBlock) void k_eval(TableArgs t, Control* __restrict__ ctl, StepArgs a,
                                                  double* __restrict__ lossp) {
     constexpr int PPB = kBlock / G;
@@ -200,8 +204,8 @@ __global__ __launch_bounds__(kBlock) void k_eval(TableArgs t, Control* __restric
         if (!ok_id || c < 0.f) {
             if (lane == 0) raise_error(ctl, ok_id ? kBadCount : kBadId);
         } else {
-            const float l = forward_positive<G, C, true>(t, a, i, u, v, c, nullptr, lane,
-                                                         nullptr, nullptr);
+            const float l = forward_positive<G, C, true, E>(t, a, i, u, v, c, nullptr, lane,
+                                                            nullptr, nullptr);
             if (lane == 0) loss = l;
         }
     }
@@ -259,8 +263,10 @@ hipError_t launch_eval(const TableArgs& t, Control* ctl, const StepArgs& a, doub
     *blocks_out = blocks;
     if (blocks == 0) return hipSuccess;
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_eval<G_, C_>), dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a,
-                           lossp);
+        HUGE_ELEM_DISPATCH(t.dtype, {
+            hipLaunchKernelGGL((k_eval<G_, C_, E_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
+                               t, ctl, a, lossp);
+        });
     });
     return hipGetLastError();
 }

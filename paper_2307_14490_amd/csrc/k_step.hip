@@ -33,13 +33,14 @@ __device__ __forceinline__ void block_loss(float loss, double* __restrict__ out)
 // NB negative rows are in flight at a time (NB = K up to 8, rounded up to
 // a supported block): the block holds NB rows of registers, so a smaller one
 // raises the occupancy, which the kernel needs to hide its memory latency.
-template <int G, int C, int NB>
+template <int G, int C, int NB, typename E>
 __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __restrict__ ctl,
                                                        StepArgs a, const int32_t* __restrict__ neg,
                                                        const int32_t* __restrict__ info,
                                                        float* __restrict__ dup,
                                                        double* __restrict__ lossp) {
-    using IO = RowIO<G, C>;
+    using IO = RowIO<G, C, E>;     // table rows
+    using DIO = RowIO<G, C>;       // contributions of repeated rows (float)
     if (ctl->step_bad) return;
     constexpr int PPB = kBlock / G;
     const int grp = threadIdx.x / G;
@@ -48,8 +49,8 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     const int K = t.K;
     const int32_t D = t.D;
     const float lr = a.lr;
-    float* __restrict__ S = t.S;
-    float* __restrict__ T = t.T;
+    E* __restrict__ S = static_cast<E*>(t.S);
+    E* __restrict__ T = static_cast<E*>(t.T);
     float loss = 0.f;
 
     // Every index of the positive is loaded before any of them is used, so
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
             float4 cv[C];
 #pragma unroll
             for (int q = 0; q < C; ++q) cv[q] = scale4(g, s[q]);
-            IO::store(dup, info_d, D, lane, cv);
+            DIO::store(dup, info_d, D, lane, cv);
         }
 
         // negatives, NB rows in flight at a time
@@ -137,7 +138,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
                         float4 cv[C];
 #pragma unroll
                         for (int q = 0; q < C; ++q) cv[q] = scale4(h, s[q]);
-                        IO::store(dup, ik[j], D, lane, cv);
+                        DIO::store(dup, ik[j], D, lane, cv);
                     }
                 }
             }
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
             for (int q = 0; q < C; ++q) nv[q] = axpy4(-lr, dS[q], s[q]);
             IO::store(S, u, D, lane, nv);
         } else {
-            IO::store(dup, info_s, D, lane, dS);
+            DIO::store(dup, info_s, D, lane, dS);
         }
         if (lane == 0) loss = c * lsum;
     }
@@ -185,8 +186,10 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
     if (blocks == 0) return hipSuccess;
     HUGE_ROW_DISPATCH(rs, {
         HUGE_NEG_DISPATCH(neg_block(t.K), {
-            hipLaunchKernelGGL((k_fused_step<G_, C_, NB_>), dim3((unsigned)blocks), dim3(kBlock),
-                               0, s, t, ctl, a, neg, info, dup, lossp);
+            HUGE_ELEM_DISPATCH(t.dtype, {
+                hipLaunchKernelGGL((k_fused_step<G_, C_, NB_, E_>), dim3((unsigned)blocks),
+                                   dim3(kBlock), 0, s, t, ctl, a, neg, info, dup, lossp);
+            });
         });
     });
     return hipGetLastError();
@@ -201,12 +204,14 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 // stores (x * 1.0f == x for every x).  Its rate is the practical ceiling of
 // the step's random row traffic.
 // ---------------------------------------------------------------------------
-template <int G, int C, int NB>
+template <int G, int C, int NB, typename E>
 __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restrict__ ctl,
                                                   const int32_t* __restrict__ src,
                                                   const int32_t* __restrict__ dst, int64_t n,
                                                   uint64_t first_pos, float one) {
-    using IO = RowIO<G, C>;
+    using IO = RowIO<G, C, E>;
+    E* __restrict__ S = static_cast<E*>(t.S);
+    E* __restrict__ T = static_cast<E*>(t.T);
     constexpr int PPB = kBlock / G;
     const int lane = threadIdx.x % G;
     const int64_t i = (int64_t)blockIdx.x * PPB + threadIdx.x / G;
@@ -232,23 +237,23 @@ __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restri
                 mk[j] = draw_negative(t.seed, first_pos + (uint64_t)i, (uint32_t)(kb + j),
                                       (uint64_t)t.N, t.thr, t.alias);
         if (kb == 0) {
-            IO::load(s, t.S, u, t.D, lane);
-            IO::load(t0, t.T, v, t.D, lane);
+            IO::load(s, S, u, t.D, lane);
+            IO::load(t0, T, v, t.D, lane);
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j)
-            if (j < cnt) IO::load(tk[j], t.T, mk[j], t.D, lane);
+            if (j < cnt) IO::load(tk[j], T, mk[j], t.D, lane);
         if (kb == 0) {
             touch(s);
             touch(t0);
-            IO::store(t.S, u, t.D, lane, s);
-            IO::store(t.T, v, t.D, lane, t0);
+            IO::store(S, u, t.D, lane, s);
+            IO::store(T, v, t.D, lane, t0);
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             if (j < cnt) {
                 touch(tk[j]);
-                IO::store(t.T, mk[j], t.D, lane, tk[j]);
+                IO::store(T, mk[j], t.D, lane, tk[j]);
             }
         }
     }
@@ -261,8 +266,10 @@ hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, co
     if (blocks == 0) return hipSuccess;
     HUGE_ROW_DISPATCH(rs, {
         HUGE_NEG_DISPATCH(neg_block(t.K), {
-            hipLaunchKernelGGL((k_probe<G_, C_, NB_>), dim3((unsigned)blocks), dim3(kBlock), 0, s,
-                               t, ctl, src, dst, n, first_pos, 1.0f);
+            HUGE_ELEM_DISPATCH(t.dtype, {
+                hipLaunchKernelGGL((k_probe<G_, C_, NB_, E_>), dim3((unsigned)blocks),
+                                   dim3(kBlock), 0, s, t, ctl, src, dst, n, first_pos, 1.0f);
+            });
         });
     });
     return hipGetLastError();
@@ -271,8 +278,8 @@ hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, co
 // ---------------------------------------------------------------------------
 // Repeated rows.  The contributions of a row, at duplicate-buffer slots
 // start .. start + len - 1, are added in that order, in double (a hub row can
-// collect tens of thousands of terms), and the row is rounded to fp32 once:
-// row = fp32(row - lr * sum).
+// collect tens of thousands of terms), and the row is rounded once to its
+// element type: row = round(row - lr * sum) (for bf16 tables through fp32).
 // ---------------------------------------------------------------------------
 struct double4_ {
     double x, y, z, w;
@@ -339,11 +346,11 @@ __device__ __forceinline__ void sum_rows(double4_ (&acc)[C], const float* __rest
     }
 }
 
-template <int G, int C>
+template <int G, int C, typename E>
 __device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
                                           const double4_ (&g)[C], float lr, int lane) {
-    using IO = RowIO<G, C>;
-    float* base = (int64_t)key >= t.N ? t.S : t.T;
+    using IO = RowIO<G, C, E>;
+    E* base = static_cast<E*>((int64_t)key >= t.N ? t.S : t.T);
     const int64_t row = (int64_t)key >= t.N ? (int64_t)key - t.N : (int64_t)key;
     const double l = (double)lr;
     float4 r[C];
@@ -434,7 +441,7 @@ __device__ __forceinline__ void coop_sum(double4_ (&acc)[C], const Row* __restri
 // ({start, len <= kPiece, key, part}): the whole workgroup sums them; a whole
 // run (part = 0) updates its row, a piece of a longer run stores its sum as
 // partial part - 1.  The record counts were set by the grouping of this batch.
-template <int G, int C>
+template <int G, int C, typename E>
 __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control* __restrict__ ctl,
                                                       const uint4* __restrict__ shorts,
                                                       const uint4* __restrict__ pieces,
@@ -455,7 +462,7 @@ __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control
         const uint4 rec = shorts[r];
         double4_ acc[C];
         sum_rows<G, C>(acc, dup, rec.x, rec.y, D, lane);
-        apply_row<G, C>(t, rec.z, acc, lr, lane);
+        apply_row<G, C, E>(t, rec.z, acc, lr, lane);
     }
     for (uint32_t r = blockIdx.x; r < np; r += gridDim.x) {
         const uint4 rec = pieces[r];  // the same for every thread
@@ -463,7 +470,7 @@ __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control
         coop_sum<G, C>(acc, dup, rec.x, rec.y, D, grp, lane, s_part);
         if (grp == 0) {
             if (rec.w == 0u)
-                apply_row<G, C>(t, rec.z, acc, lr, lane);
+                apply_row<G, C, E>(t, rec.z, acc, lr, lane);
             else
                 PartIO<G, C>::store(part, (int64_t)rec.w - 1, D, lane, acc);
         }
@@ -472,7 +479,7 @@ __global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control
 
 // Runs longer than kPiece ({key, first partial, partials}): the partial sums
 // of their pieces, added in piece order, update the row once.
-template <int G, int C>
+template <int G, int C, typename E>
 __global__ __launch_bounds__(kBlock) void k_combine(TableArgs t, const Control* __restrict__ ctl,
                                                     const uint4* __restrict__ combs,
                                                     const double* __restrict__ part, float lr,
@@ -486,7 +493,7 @@ __global__ __launch_bounds__(kBlock) void k_combine(TableArgs t, const Control* 
         const uint4 rec = combs[r];
         double4_ acc[C];
         coop_sum<G, C>(acc, part, rec.y, rec.z, t.D, grp, lane, s_part);
-        if (grp == 0) apply_row<G, C>(t, rec.x, acc, lr, lane);
+        if (grp == 0) apply_row<G, C, E>(t, rec.x, acc, lr, lane);
     }
 }
 
@@ -495,8 +502,10 @@ hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* short
                             ListCaps caps, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_dup_apply<G_, C_>), dim3(1024), dim3(kBlock), 0, s, t, ctl, shorts,
-                           pieces, dup, part, lr, caps);
+        HUGE_ELEM_DISPATCH(t.dtype, {
+            hipLaunchKernelGGL((k_dup_apply<G_, C_, E_>), dim3(1024), dim3(kBlock), 0, s, t, ctl,
+                               shorts, pieces, dup, part, lr, caps);
+        });
     });
     return hipGetLastError();
 }
@@ -505,8 +514,10 @@ hipError_t launch_combine(const TableArgs& t, Control* ctl, const uint4* combs,
                           const double* part, float lr, ListCaps caps, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
     HUGE_ROW_DISPATCH(rs, {
-        hipLaunchKernelGGL((k_combine<G_, C_>), dim3(256), dim3(kBlock), 0, s, t, ctl, combs,
-                           part, lr, caps);
+        HUGE_ELEM_DISPATCH(t.dtype, {
+            hipLaunchKernelGGL((k_combine<G_, C_, E_>), dim3(256), dim3(kBlock), 0, s, t, ctl,
+                               combs, part, lr, caps);
+        });
     });
     return hipGetLastError();
 }

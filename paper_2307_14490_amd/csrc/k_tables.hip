@@ -4,13 +4,17 @@
 
 #include "common.hpp"
 #include "device.hpp"
+#include "dispatch.hpp"
 
 namespace huge {
 
 // ---------------------------------------------------------------------------
-// Initial tables: each thread fills one float4 (one Philox block) of one row.
+// Initial tables: each thread fills one chunk of four elements (one Philox
+// block) of one row.  The values are exact in float; a bf16 table holds them
+// rounded to nearest, ties to even.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_init(float* __restrict__ S, float* __restrict__ T,
+template <typename E>
+__global__ __launch_bounds__(kBlock) void k_init(E* __restrict__ S, E* __restrict__ T,
                                                  int64_t N, int32_t D, uint64_t seed,
                                                  float scale) {
     const int64_t q = D >> 2;
@@ -31,8 +35,8 @@ __global__ __launch_bounds__(kBlock) void k_init(float* __restrict__ S, float* _
         v.y = (float)((int32_t)(r.y >> 8) - 8388608) * scale;
         v.z = (float)((int32_t)(r.z >> 8) - 8388608) * scale;
         v.w = (float)((int32_t)(r.w >> 8) - 8388608) * scale;
-        float* base = table ? T : S;
-        reinterpret_cast<float4*>(base + row * (int64_t)D)[blk] = v;
+        E* base = table ? T : S;
+        store_chunk(base + row * (int64_t)D, (int)blk, v);
     }
 }
 
@@ -41,15 +45,19 @@ hipError_t launch_init(const TableArgs& t, float half_width, hipStream_t s) {
     const int64_t total = 2 * t.N * (int64_t)(t.D / 4);
     int64_t blocks = (total + kBlock - 1) / kBlock;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(k_init, dim3((unsigned)blocks), dim3(kBlock), 0, s, t.S, t.T, t.N, t.D,
-                       t.seed, scale);
+    HUGE_ELEM_DISPATCH(t.dtype, {
+        hipLaunchKernelGGL(k_init<E_>, dim3((unsigned)blocks), dim3(kBlock), 0, s,
+                           static_cast<E_*>(t.S), static_cast<E_*>(t.T), t.N, t.D, t.seed, scale);
+    });
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Row gather: one group of 64 lanes per requested row.
+// Row gather: one group of 64 lanes per requested row; rows of a bf16 table
+// are widened to float (exactly).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_get_rows(const float* __restrict__ table, int64_t N,
+template <typename E>
+__global__ __launch_bounds__(kBlock) void k_get_rows(const E* __restrict__ table, int64_t N,
                                                      int32_t D, Control* ctl,
                                                      const int64_t* __restrict__ ids, int64_t n,
                                                      float* __restrict__ out) {
@@ -65,15 +73,17 @@ __global__ __launch_bounds__(kBlock) void k_get_rows(const float* __restrict__ t
         for (int j = lane; j < q; j += 64) o[j] = make_float4(nan, nan, nan, nan);
         return;
     }
-    const float4* p = reinterpret_cast<const float4*>(table + id * (int64_t)D);
-    for (int j = lane; j < q; j += 64) o[j] = p[j];
+    const E* p = table + id * (int64_t)D;
+    for (int j = lane; j < q; j += 64) o[j] = load_chunk(p, j);
 }
 
 hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, const int64_t* ids,
                            int64_t n, float* out, hipStream_t s) {
     const int64_t blocks = (n + 3) / 4;
-    hipLaunchKernelGGL(k_get_rows, dim3((unsigned)blocks), dim3(kBlock), 0, s,
-                       table ? t.T : t.S, t.N, t.D, ctl, ids, n, out);
+    HUGE_ELEM_DISPATCH(t.dtype, {
+        hipLaunchKernelGGL(k_get_rows<E_>, dim3((unsigned)blocks), dim3(kBlock), 0, s,
+                           static_cast<const E_*>(table ? t.T : t.S), t.N, t.D, ctl, ids, n, out);
+    });
     return hipGetLastError();
 }
 

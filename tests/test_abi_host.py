@@ -63,6 +63,18 @@ def test_bad_kind_and_width():
     assert P.workspace_bytes(c) == 0
 
 
+def test_table_dtype_config():
+    f32 = P.workspace_bytes(P.make_config(10**5, 64, 5, 1000))
+    bf16 = P.workspace_bytes(P.make_config(10**5, 64, 5, 1000, table_dtype=P.binding.HUGE_DTYPE_BF16))
+    # the workspace (fp32 contributions of repeated rows) does not depend on it
+    assert bf16 == f32 > 0
+    # bf16 tables take the sorted scatter only
+    assert P.workspace_bytes(P.make_config(10**5, 64, 5, 1000, scatter_kind=1, table_dtype=1)) == 0
+    c = P.make_config(10**5, 64, 5, 1000)
+    c.table_dtype = 2
+    assert P.workspace_bytes(c) == 0
+
+
 def test_workspace_grows_with_batch_and_holds_duplicate_buffer():
     small = P.workspace_bytes(P.make_config(10**6, 128, 5, 1000))
     big = P.workspace_bytes(P.make_config(10**6, 128, 5, 100_000))
