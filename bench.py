@@ -33,7 +33,7 @@ COUNTERS_FILES = {  # committed rocprofv3 HBM counters of the fused kernel, per 
     "bf16": os.path.join(ROOT, "profiles", "fused_step_sbm100m_bf16_counters.txt"),
 }
 KERNEL_SOURCES = ["paper_2307_14490_amd/csrc/device.hpp", "paper_2307_14490_amd/csrc/k_step.hip"]
-KERNEL_END = "int64_t fused_step_blocks("  # the fused kernel's source ends before this line
+KERNEL_END = "// Lanes per row of the fused step and the probe."  # the fused kernel's source ends here
 PROFILE_EVERY = 4  # timed steps whose fused kernel is bracketed by HIP events
 
 

@@ -154,6 +154,12 @@ inline SortPlan sort_plan(int key_bits) {
     return {1, bits};
 }
 
+// Element type of the tables (the public HUGE_DTYPE_* values).
+enum : int32_t { kDtypeF32 = 0, kDtypeBf16 = 1 };
+
+// A bfloat16 element: the upper 16 bits of an IEEE binary32.
+typedef uint16_t bf16_t;
+
 // Rows handled per workgroup: G lanes per row, C float4 per lane.
 struct RowShape {
     int G;
@@ -168,6 +174,23 @@ inline RowShape row_shape(int dim) {
     return {G, C};
 }
 
+// Rows of bf16 tables whose width is a multiple of 8, in 8-element units:
+// G lanes per row (a power of two <= 64), U units per lane.
+struct PairShape {
+    int G;
+    int U;
+};
+
+inline PairShape pair_shape(int dim) {
+    const int nu = dim / 8;
+    int G = 1;
+    while (G < nu && G < 64) G <<= 1;
+    return {G, (nu + G - 1) / G};
+}
+
+// The fused step and the probe take the unit layout for these tables.
+inline bool uses_pairs(int32_t dtype, int dim) { return dtype == kDtypeBf16 && dim % 8 == 0; }
+
 struct StepArgs {
     const int32_t* src;
     const int32_t* dst;
@@ -178,12 +201,6 @@ struct StepArgs {
     double* loss_out;
     const float* w = nullptr;  // a float weight per positive (then cc is unused)
 };
-
-// Element type of the tables (the public HUGE_DTYPE_* values).
-enum : int32_t { kDtypeF32 = 0, kDtypeBf16 = 1 };
-
-// A bfloat16 element: the upper 16 bits of an IEEE binary32.
-typedef uint16_t bf16_t;
 
 struct TableArgs {
     void* S;               // float or bf16_t rows, as dtype says
@@ -294,6 +311,5 @@ hipError_t launch_eval(const TableArgs& t, Control* ctl, const StepArgs& a, doub
 hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, const int32_t* dst,
                         int64_t n, uint64_t first_pos, hipStream_t s);
 
-int64_t fused_step_blocks(int dim, int64_t n);
 
 }  // namespace huge

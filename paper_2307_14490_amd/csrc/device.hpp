@@ -119,11 +119,66 @@ __device__ __forceinline__ void store_chunk(bf16_t* __restrict__ row, int j, flo
     reinterpret_cast<uint2*>(row)[j] = float4_to_bf16x4(v);
 }
 
-// Row r of a table of D elements (float or bf16_t) as float4 chunks; lane l
-// of a group owns chunks l, l + G, ..., l + (C-1) G, those below D/4 are
-// valid.  bf16 rows are widened on load and rounded on store.
-template <int G, int C, typename E = float>
+// Four consecutive elements as a kernel keeps them in registers: a float4
+// for float tables, the packed uint2 for bf16 tables (widened when used).
+template <typename E>
+struct Packed4;
+template <>
+struct Packed4<float> {
+    using T = float4;
+    __device__ __forceinline__ static T load(const float* __restrict__ row, int j) {
+        return reinterpret_cast<const float4*>(row)[j];
+    }
+    __device__ __forceinline__ static float4 widen(T r) { return r; }
+    __device__ __forceinline__ static T zero() { return zero4(); }
+    __device__ __forceinline__ static void refresh(T&) {}
+};
+template <>
+struct Packed4<bf16_t> {
+    using T = uint2;
+    __device__ __forceinline__ static T load(const bf16_t* __restrict__ row, int j) {
+        return reinterpret_cast<const uint2*>(row)[j];
+    }
+    __device__ __forceinline__ static float4 widen(T r) { return bf16x4_to_float4(r); }
+    __device__ __forceinline__ static T zero() { return make_uint2(0u, 0u); }
+    // an empty asm statement that the compiler must assume redefines r
+    __device__ __forceinline__ static void refresh(T& r) { asm volatile("" : "+v"(r.x), "+v"(r.y)); }
+};
+
+// Row access policies.  A policy spreads a row of D elements over the G lanes
+// of a group as C float4 chunks per lane (chunks past the row read as zero
+// and are not stored), and gives the row in two register forms: widened
+// (float4[C]) and packed (Reg[R], widened chunk by chunk with chunk()).
+// refresh() marks packed registers as redefined, so that chunks used again
+// later are widened again from them instead of the widened copies staying
+// live in between: widening costs a shift or a mask, registers cost
+// occupancy, which hides the latency of the random row accesses.
+//
+// RowIO: lane l owns the 4-element chunks l, l + G, ..., l + (C-1) G.
+template <int G, int CC, typename E = float>
 struct RowIO {
+    static constexpr int C = CC;
+    using Elem = E;
+    using P = Packed4<E>;
+    using Reg = typename P::T;
+    static constexpr int R = CC;
+    __device__ __forceinline__ static void load_packed(Reg (&r)[R], const E* __restrict__ base,
+                                                       int64_t row, int32_t D, int lane) {
+        const E* p = base + row * (int64_t)D;
+        const int q = D >> 2;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int j = lane + c * G;
+            r[c] = (j < q) ? P::load(p, j) : P::zero();
+        }
+    }
+    __device__ __forceinline__ static float4 chunk(const Reg (&r)[R], int c) {
+        return P::widen(r[c]);
+    }
+    __device__ __forceinline__ static void refresh(Reg (&r)[R]) {
+#pragma unroll
+        for (int c = 0; c < R; ++c) P::refresh(r[c]);
+    }
     __device__ __forceinline__ static void load(float4 (&x)[C], const E* __restrict__ base,
                                                 int64_t row, int32_t D, int lane) {
         const E* p = base + row * (int64_t)D;
@@ -149,6 +204,115 @@ struct RowIO {
 #pragma unroll
         for (int c = 0; c < C; ++c) s += dot4(a[c], b[c]);
         return s;
+    }
+    __device__ __forceinline__ static float dotp(const float4 (&a)[C], const Reg (&b)[R]) {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) s += dot4(a[c], chunk(b, c));
+        return s;
+    }
+};
+
+// PairIO: rows of a multiple of 8 elements in units of 8 (16 bytes of bf16):
+// lane l owns the units l, l + G, ..., l + (U-1) G, unit u being the chunks
+// 2u and 2u + 1.  With bf16 rows one 16-byte access moves a unit and half
+// as many lanes cover a row as with RowIO, so a wave holds twice as many
+// positives; a packed bf16 unit takes four registers.  The float variant
+// (the contributions of repeated rows) keeps the same element ownership.
+template <int G, int U, typename E>
+struct PairIO;
+
+template <int G, int U>
+struct PairIO<G, U, bf16_t> {
+    static constexpr int C = 2 * U;
+    using Elem = bf16_t;
+    using Reg = uint4;
+    static constexpr int R = U;
+    __device__ __forceinline__ static void load_packed(Reg (&r)[R],
+                                                       const bf16_t* __restrict__ base,
+                                                       int64_t row, int32_t D, int lane) {
+        const uint4* p = reinterpret_cast<const uint4*>(base + row * (int64_t)D);
+        const int nu = D >> 3;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = lane + u * G;
+            r[u] = (k < nu) ? p[k] : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+    __device__ __forceinline__ static float4 chunk(const Reg (&r)[R], int c) {
+        const uint4 w = r[c >> 1];
+        return bf16x4_to_float4((c & 1) ? make_uint2(w.z, w.w) : make_uint2(w.x, w.y));
+    }
+    __device__ __forceinline__ static void refresh(Reg (&r)[R]) {
+#pragma unroll
+        for (int u = 0; u < R; ++u)
+            asm volatile("" : "+v"(r[u].x), "+v"(r[u].y), "+v"(r[u].z), "+v"(r[u].w));
+    }
+    __device__ __forceinline__ static void load(float4 (&x)[C], const bf16_t* __restrict__ base,
+                                                int64_t row, int32_t D, int lane) {
+        Reg r[R];
+        load_packed(r, base, row, D, lane);
+#pragma unroll
+        for (int c = 0; c < C; ++c) x[c] = chunk(r, c);
+    }
+    __device__ __forceinline__ static void store(bf16_t* __restrict__ base, int64_t row,
+                                                 int32_t D, int lane, const float4 (&x)[C]) {
+        uint4* p = reinterpret_cast<uint4*>(base + row * (int64_t)D);
+        const int nu = D >> 3;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = lane + u * G;
+            if (k < nu) {
+                const uint2 a = float4_to_bf16x4(x[2 * u]), b = float4_to_bf16x4(x[2 * u + 1]);
+                p[k] = make_uint4(a.x, a.y, b.x, b.y);
+            }
+        }
+    }
+    __device__ __forceinline__ static float dot(const float4 (&a)[C], const float4 (&b)[C]) {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) s += dot4(a[c], b[c]);
+        return s;
+    }
+    __device__ __forceinline__ static float dotp(const float4 (&a)[C], const Reg (&b)[R]) {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) s += dot4(a[c], chunk(b, c));
+        return s;
+    }
+};
+
+template <int G, int U>
+struct PairIO<G, U, float> {
+    static constexpr int C = 2 * U;
+    using Elem = float;
+    using Reg = float4;
+    static constexpr int R = 2 * U;
+    __device__ __forceinline__ static void load_packed(Reg (&r)[R], const float* __restrict__ base,
+                                                       int64_t row, int32_t D, int lane) {
+        const float4* p = reinterpret_cast<const float4*>(base + row * (int64_t)D);
+        const int nu = D >> 3;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int k = lane + (c >> 1) * G;
+            r[c] = (k < nu) ? p[2 * k + (c & 1)] : zero4();
+        }
+    }
+    __device__ __forceinline__ static float4 chunk(const Reg (&r)[R], int c) { return r[c]; }
+    __device__ __forceinline__ static void refresh(Reg (&)[R]) {}
+    __device__ __forceinline__ static void load(float4 (&x)[C], const float* __restrict__ base,
+                                                int64_t row, int32_t D, int lane) {
+        load_packed(x, base, row, D, lane);
+    }
+    __device__ __forceinline__ static void store(float* __restrict__ base, int64_t row, int32_t D,
+                                                 int lane, const float4 (&x)[C]) {
+        float4* p = reinterpret_cast<float4*>(base + row * (int64_t)D);
+        const int nu = D >> 3;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const int k = lane + (c >> 1) * G;
+            if (k < nu) p[2 * k + (c & 1)] = x[c];
+        }
     }
 };
 

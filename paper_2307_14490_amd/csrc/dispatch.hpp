@@ -62,3 +62,26 @@ inline int neg_block(int K) {
         using E_ = float;                   \
         __VA_ARGS__;                        \
     }
+
+// Unit layouts of bf16 rows (8 elements per unit), D <= 1024: G lanes per
+// row and U units per lane.
+#define HUGE_PAIR_CASE(GG, UU, ...)          \
+    case (GG) * 8 + (UU): {                  \
+        constexpr int G_ = (GG);             \
+        constexpr int U_ = (UU);             \
+        __VA_ARGS__;                         \
+    } break;
+
+#define HUGE_PAIR_DISPATCH(ps, ...)                  \
+    switch ((ps).G * 8 + (ps).U) {                   \
+        HUGE_PAIR_CASE(1, 1, __VA_ARGS__)            \
+        HUGE_PAIR_CASE(2, 1, __VA_ARGS__)            \
+        HUGE_PAIR_CASE(4, 1, __VA_ARGS__)            \
+        HUGE_PAIR_CASE(8, 1, __VA_ARGS__)            \
+        HUGE_PAIR_CASE(16, 1, __VA_ARGS__)           \
+        HUGE_PAIR_CASE(32, 1, __VA_ARGS__)           \
+        HUGE_PAIR_CASE(64, 1, __VA_ARGS__)           \
+        HUGE_PAIR_CASE(64, 2, __VA_ARGS__)           \
+        default:                                     \
+            return hipErrorInvalidValue;             \
+    }

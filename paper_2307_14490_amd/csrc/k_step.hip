@@ -33,14 +33,21 @@ __device__ __forceinline__ void block_loss(float loss, double* __restrict__ out)
 // NB negative rows are in flight at a time (NB = K up to 8, rounded up to
 // a supported block): the block holds NB rows of registers, so a smaller one
 // raises the occupancy, which the kernel needs to hide its memory latency.
-template <int G, int C, int NB, typename E>
+// IO is the row policy of the tables (G lanes per row), DIO the same element
+// ownership over the float contributions of repeated rows.  The context rows
+// stay packed in registers (bf16: half the registers) and are widened where
+// used; the source row and the source gradient are held widened.
+template <int G, int NB, typename IO, typename DIO>
 __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __restrict__ ctl,
                                                        StepArgs a, const int32_t* __restrict__ neg,
                                                        const int32_t* __restrict__ info,
                                                        float* __restrict__ dup,
                                                        double* __restrict__ lossp) {
-    using IO = RowIO<G, C, E>;     // table rows
-    using DIO = RowIO<G, C>;       // contributions of repeated rows (float)
+    using E = typename IO::Elem;
+    using Reg = typename IO::Reg;
+    constexpr int C = IO::C;
+    constexpr int R = IO::R;
+    static_assert(DIO::C == C, "the contribution layout must match the row layout");
     if (ctl->step_bad) return;
     constexpr int PPB = kBlock / G;
     const int grp = threadIdx.x / G;
@@ -85,24 +92,26 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     }
     if (active) {
         const float c = c_i;
-        float4 s[C], t0[C], dS[C];
-        float4 tk[NB][C];
+        float4 s[C], dS[C];
+        Reg t0[R];
+        Reg tk[NB][R];
         IO::load(s, S, u, D, lane);
-        IO::load(t0, T, v, D, lane);
+        IO::load_packed(t0, T, v, D, lane);
 #pragma unroll
         for (int j = 0; j < NB; ++j)
-            if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
+            if (j < cnt) IO::load_packed(tk[j], T, mk[j], D, lane);
 
         // positive pair
-        const float x = group_sum<G>(IO::dot(s, t0));
+        const float x = group_sum<G>(IO::dotp(s, t0));
+        IO::refresh(t0);
         const float g = coef_pos(c, x);
         float lsum = softplus_f(-x);
 #pragma unroll
-        for (int q = 0; q < C; ++q) dS[q] = scale4(g, t0[q]);
+        for (int q = 0; q < C; ++q) dS[q] = scale4(g, IO::chunk(t0, q));
         if (info_d < 0) {
             float4 nv[C];
 #pragma unroll
-            for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * g), s[q], t0[q]);
+            for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * g), s[q], IO::chunk(t0, q));
             IO::store(T, v, D, lane, nv);
         } else {
             float4 cv[C];
@@ -116,23 +125,26 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
         while (true) {
             float y[NB];
 #pragma unroll
-            for (int j = 0; j < NB; ++j) y[j] = (j < cnt) ? IO::dot(s, tk[j]) : 0.f;
+            for (int j = 0; j < NB; ++j) y[j] = (j < cnt) ? IO::dotp(s, tk[j]) : 0.f;
 #pragma unroll
             for (int off = G / 2; off > 0; off >>= 1) {
 #pragma unroll
                 for (int j = 0; j < NB; ++j) y[j] += __shfl_xor(y[j], off, 64);
             }
 #pragma unroll
+            for (int j = 0; j < NB; ++j) IO::refresh(tk[j]);
+#pragma unroll
             for (int j = 0; j < NB; ++j) {
                 if (j < cnt) {
                     const float h = coef_neg(c, y[j]);
                     lsum += softplus_f(y[j]);
 #pragma unroll
-                    for (int q = 0; q < C; ++q) dS[q] = axpy4(h, tk[j][q], dS[q]);
+                    for (int q = 0; q < C; ++q) dS[q] = axpy4(h, IO::chunk(tk[j], q), dS[q]);
                     if (ik[j] < 0) {
                         float4 nv[C];
 #pragma unroll
-                        for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * h), s[q], tk[j][q]);
+                        for (int q = 0; q < C; ++q)
+                            nv[q] = axpy4(-(lr * h), s[q], IO::chunk(tk[j], q));
                         IO::store(T, mk[j], D, lane, nv);
                     } else {
                         float4 cv[C];
@@ -154,7 +166,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
             }
 #pragma unroll
             for (int j = 0; j < NB; ++j)
-                if (j < cnt) IO::load(tk[j], T, mk[j], D, lane);
+                if (j < cnt) IO::load_packed(tk[j], T, mk[j], D, lane);
         }
 
         // source row
@@ -171,27 +183,42 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     block_loss(loss, lossp);
 }
 
-int64_t fused_step_blocks(int dim, int64_t n) {
-    const RowShape rs = row_shape(dim);
-    const int64_t ppb = kBlock / rs.G;
+// Lanes per row of the fused step and the probe.
+static int step_lanes(const TableArgs& t) {
+    return uses_pairs(t.dtype, t.D) ? pair_shape(t.D).G : row_shape(t.D).G;
+}
+
+static int64_t fused_step_blocks(const TableArgs& t, int64_t n) {
+    const int64_t ppb = kBlock / step_lanes(t);
     return (n + ppb - 1) / ppb;
 }
 
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, const int32_t* info, float* dup,
                              double* lossp, int64_t* blocks_out, hipStream_t s) {
-    const RowShape rs = row_shape(t.D);
-    const int64_t blocks = fused_step_blocks(t.D, a.n);
+    const int64_t blocks = fused_step_blocks(t, a.n);
     *blocks_out = blocks;
     if (blocks == 0) return hipSuccess;
-    HUGE_ROW_DISPATCH(rs, {
-        HUGE_NEG_DISPATCH(neg_block(t.K), {
-            HUGE_ELEM_DISPATCH(t.dtype, {
-                hipLaunchKernelGGL((k_fused_step<G_, C_, NB_, E_>), dim3((unsigned)blocks),
-                                   dim3(kBlock), 0, s, t, ctl, a, neg, info, dup, lossp);
+    if (uses_pairs(t.dtype, t.D)) {
+        HUGE_PAIR_DISPATCH(pair_shape(t.D), {
+            HUGE_NEG_DISPATCH(neg_block(t.K), {
+                hipLaunchKernelGGL(
+                    (k_fused_step<G_, NB_, PairIO<G_, U_, bf16_t>, PairIO<G_, U_, float>>),
+                    dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, info, dup, lossp);
             });
         });
-    });
+    } else {
+        HUGE_ROW_DISPATCH(row_shape(t.D), {
+            HUGE_NEG_DISPATCH(neg_block(t.K), {
+                HUGE_ELEM_DISPATCH(t.dtype, {
+                    hipLaunchKernelGGL(
+                        (k_fused_step<G_, NB_, RowIO<G_, C_, E_>, RowIO<G_, C_>>),
+                        dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, info, dup,
+                        lossp);
+                });
+            });
+        });
+    }
     return hipGetLastError();
 }
 
@@ -204,12 +231,13 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 // stores (x * 1.0f == x for every x).  Its rate is the practical ceiling of
 // the step's random row traffic.
 // ---------------------------------------------------------------------------
-template <int G, int C, int NB, typename E>
+template <int G, int NB, typename IO>
 __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restrict__ ctl,
                                                   const int32_t* __restrict__ src,
                                                   const int32_t* __restrict__ dst, int64_t n,
                                                   uint64_t first_pos, float one) {
-    using IO = RowIO<G, C, E>;
+    using E = typename IO::Elem;
+    constexpr int C = IO::C;
     E* __restrict__ S = static_cast<E*>(t.S);
     E* __restrict__ T = static_cast<E*>(t.T);
     constexpr int PPB = kBlock / G;
@@ -261,17 +289,27 @@ __global__ __launch_bounds__(kBlock) void k_probe(TableArgs t, Control* __restri
 
 hipError_t launch_probe(const TableArgs& t, Control* ctl, const int32_t* src, const int32_t* dst,
                         int64_t n, uint64_t first_pos, hipStream_t s) {
-    const RowShape rs = row_shape(t.D);
-    const int64_t blocks = fused_step_blocks(t.D, n);
+    const int64_t blocks = fused_step_blocks(t, n);
     if (blocks == 0) return hipSuccess;
-    HUGE_ROW_DISPATCH(rs, {
-        HUGE_NEG_DISPATCH(neg_block(t.K), {
-            HUGE_ELEM_DISPATCH(t.dtype, {
-                hipLaunchKernelGGL((k_probe<G_, C_, NB_, E_>), dim3((unsigned)blocks),
-                                   dim3(kBlock), 0, s, t, ctl, src, dst, n, first_pos, 1.0f);
+    if (uses_pairs(t.dtype, t.D)) {
+        HUGE_PAIR_DISPATCH(pair_shape(t.D), {
+            HUGE_NEG_DISPATCH(neg_block(t.K), {
+                hipLaunchKernelGGL((k_probe<G_, NB_, PairIO<G_, U_, bf16_t>>),
+                                   dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, src, dst,
+                                   n, first_pos, 1.0f);
             });
         });
-    });
+    } else {
+        HUGE_ROW_DISPATCH(row_shape(t.D), {
+            HUGE_NEG_DISPATCH(neg_block(t.K), {
+                HUGE_ELEM_DISPATCH(t.dtype, {
+                    hipLaunchKernelGGL((k_probe<G_, NB_, RowIO<G_, C_, E_>>),
+                                       dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, src,
+                                       dst, n, first_pos, 1.0f);
+                });
+            });
+        });
+    }
     return hipGetLastError();
 }
 

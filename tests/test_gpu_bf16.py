@@ -89,7 +89,10 @@ STEP_CASES = [
     (200, 32, 3, 3000, 0.0, 5, False, "short runs"),
     (5000, 64, 4, 6000, 0.5, 1000, False, "hub rows: pieces and combined sums"),
     (1000, 8, 10, 2000, 0.2, 5, True, "float weights, narrow rows"),
-    (500, 260, 6, 1500, 0.1, 3, False, "D = 260: several chunks per lane, ragged"),
+    (500, 260, 6, 1500, 0.1, 3, False, "D = 260: 4-element chunks, several per lane, ragged"),
+    (300, 1024, 3, 500, 0.1, 3, False, "D = 1024: two 8-element units per lane"),
+    (400, 520, 4, 800, 0.0, 5, False, "D = 520: 65 units, those past the row masked"),
+    (800, 16, 9, 1200, 0.3, 7, False, "D = 16: two lanes per row, K = 9 in two blocks"),
 ]
 
 
@@ -156,8 +159,9 @@ def test_get_rows_widens_exactly():
         assert torch.equal(got, tab[ids.to(tab.device)].float())
 
 
-def test_probe_rows_leaves_bf16_tables_unchanged():
-    N, D, K, n = 1000, 128, 5, 4000
+@pytest.mark.parametrize("D", [128, 520, 36])
+def test_probe_rows_leaves_bf16_tables_unchanged(D):
+    N, K, n = 1000, 5, 4000
     rng = np.random.default_rng(6)
     src, dst, _ = _batch(rng, N, n, hub=0.3)
     tr = P.Trainer(N, D, K, n, seed=1, dtype="bf16")
