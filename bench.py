@@ -478,7 +478,7 @@ def main():
     # default priority, like the current stream
     sides = [torch.cuda.Stream(), torch.cuda.Stream()]
 
-    def run_steps(count, first_batch, pos):
+    def run_steps(count, first_batch, pos, after_step=None):
         """`count` steps.  Pipelined: batch k+1 is prepared before batch k is
         applied on the current stream.  Batches are prepared on two side
         streams in turn: the library issues batch k+1's radix pass on the
@@ -490,6 +490,8 @@ def main():
                 s, d, c = dev_batches[(first_batch + k) % R]
                 tr.step_no_loss(s, d, c, pos, cfg.lr)
                 pos += n
+                if after_step:
+                    after_step(k)
             return pos
         s, d, c = dev_batches[first_batch % R]
         tr.prepare(s, d, c, pos, stream=sides[first_batch % 2])
@@ -501,6 +503,8 @@ def main():
                 tr.prepare(s, d, c, pos, stream=sides[b % 2])
                 pos += n
             tr.train_prepared(cfg.lr, with_loss=False, stream=stream)
+            if after_step:
+                after_step(k)
         return pos
 
     pos = run_steps(args.warmup, 0, pos)
@@ -571,6 +575,23 @@ def main():
         stream.wait_stream(sd)
     diag_ms, diag_steps = tr.profile_end()
     phase_avg_us = {p: diag_ms[i] / max(diag_steps, 1) * 1e3 for i, p in enumerate(phases)}
+
+    # Distribution of step times from another separate pass: an event on the
+    # apply stream after every step (a queue packet of a few microseconds
+    # each); step k's time (k >= 1) is the interval between the events of
+    # steps k-1 and k.
+    n_dist = min(200, args.steps) + 1
+    dist_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_dist)]
+    pos = run_steps(n_dist, args.warmup + args.steps + n_diag, pos,
+                    after_step=lambda k: dist_ev[k].record(stream))
+    for sd in sides:
+        stream.wait_stream(sd)
+    torch.cuda.synchronize()
+    if tr.check() != 0:
+        raise RuntimeError("device reported an error in the step-time pass")
+    step_ms = np.array([dist_ev[k - 1].elapsed_time(dist_ev[k]) for k in range(1, n_dist)])
+    p10, p50, p90 = (float(np.percentile(step_ms, q)) for q in (10, 50, 90))
+    log(f"[bench] step time p10/p50/p90: {p10:.4f} / {p50:.4f} / {p90:.4f} ms")
 
     # Algorithmic bytes of the fused kernel per launch: the batch (12 B per
     # positive), each distinct row read once (eb D bytes, eb = 4 for fp32 and
@@ -644,6 +665,9 @@ def main():
             "alg_GBps": step_bytes / (ms_per_step * 1e-3) / 1e9,
             "phase_avg_us": phase_avg_us,
             "phase_note": "from a separate 50-step pass with an event at every phase boundary",
+            "ms_percentiles": {"p10": p10, "p50": p50, "p90": p90, "steps": int(step_ms.size),
+                               "positives_per_s_at_p50": n / (p50 * 1e-3),
+                               "note": "a separate pass with one event after every step"},
             "unique_src_rows": uS,
             "unique_ctx_rows": uT,
             "repeated_row_occurrences": dup,
