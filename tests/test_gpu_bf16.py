@@ -21,7 +21,7 @@ torch = pytest.importorskip("torch")
 
 from oracle import oracle as orc  # noqa: E402
 import paper_2307_14490_amd as P  # noqa: E402
-from gpu_common import dev, say  # noqa: E402
+from gpu_common import assert_bf16_close, dev, say  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -40,23 +40,6 @@ def _half(D):
 
 def _bits(t):
     return t.view(torch.int16).cpu().numpy().view(np.uint16)
-
-
-def assert_bf16_close(got, want, what, abs_tol=1e-6, max_mismatch=2e-3):
-    """Each element within one bf16 step (|x| 2^-7 bounds it) plus abs_tol,
-    the float step's absolute tolerance: the kernels' fp32 arithmetic errs
-    by a few fp32 ulps of the operands, which spans more than one bf16 step
-    only where the result is much smaller than the operands (cancellation
-    near zero).  And nearly all elements equal."""
-    g = orc.bf16_to_float(got).astype(np.float64)
-    w = orc.bf16_to_float(want).astype(np.float64)
-    err = np.abs(g - w)
-    bound = np.maximum(np.abs(g), np.abs(w)) * 2.0 ** -7 + abs_tol
-    bad = np.count_nonzero(got != want)
-    say(f"  {what}: {bad} of {got.size} elements differ, max error / bound "
-        f"{(err / bound).max():.3f}")
-    assert np.all(err <= bound), what
-    assert bad <= max_mismatch * got.size, what
 
 
 def _batch(rng, N, n, cmax=5, hub=0.0, weights=False):

@@ -6,7 +6,8 @@ also with the atomic scatter).  The oracle holds only the rows the batch
 touches (its own sampler picks the negatives, its own initialiser the
 pre-step values), so every touched element is checked against it; a random
 sample of untouched rows must still equal the oracle's initial values bit for
-bit, and the step's row counts must equal the oracle's exactly.
+bit, and the step's row counts must equal the oracle's exactly.  SBM-100M
+also runs on bf16 tables against the oracle's bf16 step.
 """
 import time
 
@@ -17,7 +18,7 @@ torch = pytest.importorskip("torch")
 
 from oracle import oracle as orc  # noqa: E402
 import paper_2307_14490_amd as P  # noqa: E402
-from gpu_common import assert_close, dev, say  # noqa: E402
+from gpu_common import assert_bf16_close, assert_close, dev, say  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -85,5 +86,58 @@ def test_full_size_step(name, scatter):
         got = tr.get_rows(table, torch.from_numpy(cand)).cpu().numpy()
         assert np.array_equal(got, orc.init_rows(seed, table, cand, cfg.dim, a))
     say(f"[{name}/{scatter}] checked {time.time() - t0:.1f}s")
+    tr.close()
+    del tr
+
+
+def _bf16_bits(rows_f32):
+    """bf16 bit patterns of float32 rows that hold widened bf16 values."""
+    b = np.ascontiguousarray(rows_f32, np.float32).view(np.uint32)
+    assert not np.any(b & 0xFFFF), "a widened bf16 value has no low half"
+    return (b >> 16).astype(np.uint16)
+
+
+@pytest.mark.timeout(600)
+def test_full_size_step_bf16():
+    """SBM-100M on bf16 tables, one step in the benchmark's launch
+    configuration: the touched rows against the oracle's bf16 step on the
+    compact set of those rows (initial rows rounded to bf16, the step in
+    double, each element rounded once), untouched rows bit-exact."""
+    from synth import make_workload
+    t0 = time.time()
+    wl = make_workload("sbm100m", 0)
+    cfg = wl.cfg
+    src, dst, cc = wl.batch(0)
+    seed, first = 2024, 3 * cfg.batch
+    a = float(np.float32(cfg.init_half_width))
+    tr = P.Trainer(cfg.num_nodes, cfg.dim, cfg.num_neg, cfg.batch, seed=seed, dtype="bf16")
+    loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), first, cfg.lr).item()
+    assert tr.check() == 0
+    say(f"[sbm100m/bf16] gpu step done {time.time() - t0:.1f}s")
+
+    n, K = src.size, cfg.num_neg
+    neg = orc.sample_negatives(seed, first, n, K, cfg.num_nodes)
+    rows_S = np.unique(src.astype(np.int64))
+    rows_T = np.unique(np.concatenate([dst.astype(np.int64), neg.reshape(-1).astype(np.int64)]))
+    S = orc.init_rows_bf16(seed, 0, rows_S, cfg.dim, a)
+    T = orc.init_rows_bf16(seed, 1, rows_T, cfg.dim, a)
+    ref_loss = orc.step_dense_bf16(
+        S, T, np.searchsorted(rows_S, src).astype(np.int32),
+        np.searchsorted(rows_T, dst).astype(np.int32), cc,
+        np.searchsorted(rows_T, neg.reshape(-1)).astype(np.int32).reshape(n, K), cfg.lr)
+    say(f"[sbm100m/bf16] oracle done {time.time() - t0:.1f}s rows S {rows_S.size} T {rows_T.size}")
+    uS, uT, _ = tr.stats()
+    assert (uS, uT) == (rows_S.size, rows_T.size)
+    assert_bf16_close(_bf16_bits(tr.get_rows(0, torch.from_numpy(rows_S)).cpu().numpy()), S,
+                      "sbm100m bf16 S")
+    assert_bf16_close(_bf16_bits(tr.get_rows(1, torch.from_numpy(rows_T)).cpu().numpy()), T,
+                      "sbm100m bf16 T")
+    assert loss == pytest.approx(ref_loss, rel=1e-5)
+    rng = np.random.default_rng(1)
+    for table, rows in ((0, rows_S), (1, rows_T)):
+        cand = np.setdiff1d(rng.integers(0, cfg.num_nodes, 6000), rows)[:4096]
+        got = _bf16_bits(tr.get_rows(table, torch.from_numpy(cand)).cpu().numpy())
+        assert np.array_equal(got, orc.init_rows_bf16(seed, table, cand, cfg.dim, a))
+    say(f"[sbm100m/bf16] checked {time.time() - t0:.1f}s")
     tr.close()
     del tr
