@@ -93,6 +93,7 @@ STEP_CASES = [
     (50, 4, 20, 64, "narrowest row, several negative blocks"),
     (2, 8, 5, 50, "two nodes: every row repeats"),
     (1_000, 128, 64, 100, "largest K"),
+    (3_000, 32, 13, 2_000, "K = 13: two negative blocks, indices staged, ragged last workgroup"),
     (20_000, 128, 5, 9000, "several sort tiles"),
     (100_000, 16, 5, 20_000, "keys of 18 bits: 9-bit digit, 18 radix tiles"),
     (300_000, 16, 4, 30_000, "keys of 20 bits: 10-bit digit, 22 radix tiles"),
