@@ -12,8 +12,10 @@
 //   k_eval_quantile percentiles of the sorted distances (sorted by the radix
 //                   kernels of k_sort.hip on the float bit patterns);
 //   k_knn_queries   the normalised query rows;
-//   k_knn_tiles     distances of every row to every query by fp32 MFMA
-//                   (32 queries x 32 rows per tile), per-wave top-k lists;
+//   k_knn_tiles_h   distances of every row to every query (32 queries x 32 rows
+//                   per tile) for dim <= 128: rows and queries split into two
+//                   fp16 parts on the fp16 matrix cores; per-wave top-k lists;
+//   k_knn_tiles     the same for wider rows: fp32 matrix cores, queries in LDS;
 //   k_knn_merge     the k nearest of each query over all lists (bitonic sort);
 //   k_eval_recall   recall@k from the nearest rows and the sorted CSR lists.
 #include "common.hpp"
@@ -493,12 +495,95 @@ __global__ __launch_bounds__(kKnnWaves * 64) void k_knn_tiles(KnnArgs A) {
     }
 }
 
-// The same search for dim <= 128 with the queries' operands in registers:
-// no LDS holds the queries, so kKnnWavesR waves (two per SIMD) fit one CU and
-// the epilogue of one wave overlaps the products of another.  A lane keeps
-// its 16 query slots' thresholds as floats (the d^2 of the query's current
-// k-th key) and builds the exact key only for a score at or below it.
-__global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_r(KnnArgs A) {
+// The k smallest keys of query q over all NS lists: running best k plus a
+// chunk of candidates, bitonic-sorted together in LDS.
+__global__ __launch_bounds__(kBlock) void k_knn_merge(const uint64_t* __restrict__ partial,
+                                                      int64_t NS, int32_t nqp, int32_t k,
+                                                      int32_t q_first, int32_t* __restrict__ ids,
+                                                      float* __restrict__ dist) {
+    __shared__ uint64_t s_buf[kKnnMergeCap];
+    const int q = blockIdx.x;
+    const int64_t total = NS * k;
+    for (int i = threadIdx.x; i < k; i += kBlock) s_buf[i] = kNoKey;
+    for (int64_t base = 0; base < total; base += kKnnMergeCap - k) {
+        const int64_t chunk =
+            total - base < kKnnMergeCap - k ? total - base : (int64_t)(kKnnMergeCap - k);
+        for (int i = threadIdx.x; i < kKnnMergeCap - k; i += kBlock) {
+            uint64_t v = kNoKey;
+            if (i < chunk) {
+                const int64_t c = base + i;
+                v = partial[((c / k) * nqp + q) * k + (c % k)];
+            }
+            s_buf[k + i] = v;
+        }
+        __syncthreads();
+        for (int size = 2; size <= kKnnMergeCap; size <<= 1) {
+            for (int st = size >> 1; st > 0; st >>= 1) {
+                for (int i = threadIdx.x; i < kKnnMergeCap / 2; i += kBlock) {
+                    const int lo = 2 * i - (i & (st - 1));
+                    const int hi = lo + st;
+                    const bool up = (lo & size) == 0;
+                    const uint64_t a = s_buf[lo], b = s_buf[hi];
+                    if ((a > b) == up) {
+                        s_buf[lo] = b;
+                        s_buf[hi] = a;
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+    for (int t = threadIdx.x; t < k; t += kBlock) {
+        const uint64_t key = s_buf[t];
+        const int64_t o = (int64_t)(q_first + q) * k + t;
+        ids[o] = key == kNoKey ? -1 : (int32_t)(uint32_t)key;
+        dist[o] = key == kNoKey ? __builtin_nanf("") : sqrtf(__uint_as_float((uint32_t)(key >> 32)));
+    }
+}
+
+// The same search for dim <= 128 on the fp16 matrix cores.  Queries and rows
+// are normalised and scaled by 2^10 (|x| <= 1024), and each value is split
+// into two fp16 parts, x = hi + lo + e with |e| <= 2^-22 |x| (hi the nearest
+// fp16 of x, lo that of the exact remainder x - hi); the three products
+// hi.hi + hi.lo + lo.hi (v_mfma_f32_32x32x16_f16, exact fp16 products summed
+// in fp32) leave out lo.lo and e, about 2^-21 of each term, against the 2^-24
+// of fp32 products: well inside the search's distance bound.  A 16-dimension
+// chunk takes three matrix instructions here against eight in fp32.
+// Operand layout (checked on the GPU): A[i][c] comes from element c % 8 of
+// lane i + 32 (c / 8), B[c][j] from element c % 8 of lane j + 32 (c / 8); the
+// accumulators are laid out as for the fp32 instruction.
+typedef _Float16 knn_h8 __attribute__((ext_vector_type(8)));
+constexpr float kKnnSplitScale = 1024.0f;                  // 2^10
+constexpr float kKnnSplitUnscale = 1.0f / (1024.0f * 1024.0f);  // 2^-20, exact
+
+// v rounded to the nearest value with 11 significant bits, ties to even, on
+// the bits of v: a value of the fp16 grid for 2^-14 <= |v| < 65504, so its
+// conversion to fp16 is exact.  Below 2^-14 the whole of v goes to lo.
+__device__ __forceinline__ float knn_f16_grid(float v) {
+    const uint32_t b = __float_as_uint(v);
+    const float r = __uint_as_float((b + 0x0FFFu + ((b >> 13) & 1u)) & ~0x1FFFu);
+    return fabsf(v) >= 6.103515625e-05f ? r : 0.f;
+}
+
+// The split of 8 values scaled by sc.  Every step is an explicit rounding
+// (no contraction of the product into the later operations): hi + lo then
+// equals the scaled value up to the rounding of lo, whichever instructions
+// the conversions become.  With contraction the product could be rounded
+// differently for hi and for lo, and at an exact fp16 tie hi + lo missed
+// the value by one fp16 step.
+__device__ __forceinline__ void knn_split8(float4 a, float4 b, float sc, knn_h8& hi,
+                                           knn_h8& lo) {
+    const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float v = __fmul_rn(x[e], sc);
+        const float g = knn_f16_grid(v);
+        hi[e] = (_Float16)g;                 // exact
+        lo[e] = (_Float16)__fsub_rn(v, g);   // the remainder is exact in fp32
+    }
+}
+
+__global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
     __shared__ uint64_t s_list[kKnnWavesR][32][kKnnMaxK];
     __shared__ uint64_t s_stage[kKnnWavesR][32][32];
     __shared__ uint64_t s_thr[kKnnWavesR][32];
@@ -512,25 +597,33 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_r(KnnArgs A) {
     const int wpb = kKnnWavesR / A.QB;
     const int64_t S = (int64_t)blockIdx.x * wpb + w / A.QB;
     const int64_t NS = (int64_t)gridDim.x * wpb;
-    constexpr int kQ4 = kKnnDimChunk / 8;
-    const int d0 = h * (kKnnDimChunk / 2);
+    constexpr int kCh = kKnnDimChunk / 16;  // 16-dimension chunks
+    // lane (x, h) holds dimensions 16 s + 8 h .. 16 s + 8 h + 7 of chunk s
+    const int d0 = 8 * h;
 
-    // operands of query qb*32 + x, dimensions d0 .. d0 + 63
-    float4 av[kQ4];
+    // operands of query qb * 32 + x (already normalised)
+    knn_h8 qh[kCh], ql[kCh];
     {
         const float* qrow = A.qn + (int64_t)(qb * 32 + x) * D;
 #pragma unroll
-        for (int m = 0; m < kQ4; ++m)
-            av[m] = d0 + 4 * m < D ? *reinterpret_cast<const float4*>(qrow + d0 + 4 * m)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int c = 0; c < kCh; ++c) {
+            const int d = 16 * c + d0;
+            const float4 a = d + 4 <= D ? *reinterpret_cast<const float4*>(qrow + d)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 b = d + 8 <= D ? *reinterpret_cast<const float4*>(qrow + d + 4)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+            knn_split8(a, b, kKnnSplitScale, qh[c], ql[c]);
+        }
     }
-    // this lane's 16 score slots: query i = 8 (r / 4) + 4 h + r % 4
-    float qn2[16], thr[16];
+    // this lane's 16 score slots: query i = 8 (r / 4) + 4 h + r % 4; the
+    // squared norm of a normalised query is 1 (0 for a zero query): one bit
+    float thr[16];
     int32_t qid[16];
+    uint32_t qone = 0u;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int q = qb * 32 + 8 * (r / 4) + 4 * h + (r % 4);
-        qn2[r] = A.qn2[q];
+        qone |= A.qn2[q] > 0.f ? 1u << r : 0u;
         qid[r] = A.qid[q];
         thr[r] = __builtin_inff();
     }
@@ -542,39 +635,43 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_r(KnnArgs A) {
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
     __builtin_amdgcn_wave_barrier();
 
-    auto load_rows = [&](int64_t tt, float4* bv) {
-        const int64_t rr = tt * 32 + x;
-        const float4* src = reinterpret_cast<const float4*>(A.T + rr * (int64_t)D + d0);
-        const bool ok = tt < A.tiles && rr < A.N;
-#pragma unroll
-        for (int m = 0; m < kQ4; ++m)
-            bv[m] = (ok && d0 + 4 * m < D) ? src[m] : make_float4(0.f, 0.f, 0.f, 0.f);
-    };
     for (int64_t t = S; t < A.tiles; t += NS) {
         const int64_t row = t * 32 + x;
-        float4 bv[kQ4];
-        load_rows(t, bv);
-        knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
-                         0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        const bool ok = row < A.N;
+        const float* src = A.T + (ok ? row : 0) * (int64_t)D;
+        float4 bv[2 * kCh];
+#pragma unroll
+        for (int c = 0; c < kCh; ++c) {
+            const int d = 16 * c + d0;
+            bv[2 * c] = (ok && d + 4 <= D) ? *reinterpret_cast<const float4*>(src + d)
+                                           : make_float4(0.f, 0.f, 0.f, 0.f);
+            bv[2 * c + 1] = (ok && d + 8 <= D) ? *reinterpret_cast<const float4*>(src + d + 4)
+                                               : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
         float nr = 0.f;
 #pragma unroll
-        for (int m = 0; m < kQ4; ++m) {
+        for (int m = 0; m < 2 * kCh; ++m)
             nr += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z + bv[m].w * bv[m].w;
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].x, bv[m].x, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].y, bv[m].y, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].z, bv[m].z, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[m].w, bv[m].w, acc, 0, 0, 0);
-        }
         nr += __shfl_xor(nr, 32, 64);
-        const bool row_ok = row < A.N;
-        const float inv = nr > 0.f ? 1.0f / sqrtf(nr) : 0.f;
+        const float sc = nr > 0.f ? kKnnSplitScale / sqrtf(nr) : 0.f;
         const float nx = nr > 0.f ? 1.f : 0.f;
+        knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
+                         0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < kCh; ++c) {
+            knn_h8 bh, bl;
+            knn_split8(bv[2 * c], bv[2 * c + 1], sc, bh, bl);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[c], bh, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[c], bl, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[c], bh, acc, 0, 0, 0);
+        }
         bool staged = false;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            float d2 = qn2[r] + nx - 2.f * acc[r] * inv;
+            const float qn2 = (qone >> r) & 1u ? 1.f : 0.f;
+            float d2 = qn2 + nx - 2.f * kKnnSplitUnscale * acc[r];
             d2 = d2 > 0.f ? d2 : 0.f;
-            if (d2 <= thr[r] && row_ok && qid[r] >= 0 && row != (int64_t)qid[r]) {
+            if (d2 <= thr[r] && ok && qid[r] >= 0 && row != (int64_t)qid[r]) {
                 const int i = 8 * (r / 4) + 4 * h + (r % 4);
                 const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) | (uint64_t)row;
                 if (key < s_thr[w][i]) {
@@ -624,52 +721,6 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_r(KnnArgs A) {
     }
 }
 
-// The k smallest keys of query q over all NS lists: running best k plus a
-// chunk of candidates, bitonic-sorted together in LDS.
-__global__ __launch_bounds__(kBlock) void k_knn_merge(const uint64_t* __restrict__ partial,
-                                                      int64_t NS, int32_t nqp, int32_t k,
-                                                      int32_t q_first, int32_t* __restrict__ ids,
-                                                      float* __restrict__ dist) {
-    __shared__ uint64_t s_buf[kKnnMergeCap];
-    const int q = blockIdx.x;
-    const int64_t total = NS * k;
-    for (int i = threadIdx.x; i < k; i += kBlock) s_buf[i] = kNoKey;
-    for (int64_t base = 0; base < total; base += kKnnMergeCap - k) {
-        const int64_t chunk =
-            total - base < kKnnMergeCap - k ? total - base : (int64_t)(kKnnMergeCap - k);
-        for (int i = threadIdx.x; i < kKnnMergeCap - k; i += kBlock) {
-            uint64_t v = kNoKey;
-            if (i < chunk) {
-                const int64_t c = base + i;
-                v = partial[((c / k) * nqp + q) * k + (c % k)];
-            }
-            s_buf[k + i] = v;
-        }
-        __syncthreads();
-        for (int size = 2; size <= kKnnMergeCap; size <<= 1) {
-            for (int st = size >> 1; st > 0; st >>= 1) {
-                for (int i = threadIdx.x; i < kKnnMergeCap / 2; i += kBlock) {
-                    const int lo = 2 * i - (i & (st - 1));
-                    const int hi = lo + st;
-                    const bool up = (lo & size) == 0;
-                    const uint64_t a = s_buf[lo], b = s_buf[hi];
-                    if ((a > b) == up) {
-                        s_buf[lo] = b;
-                        s_buf[hi] = a;
-                    }
-                }
-                __syncthreads();
-            }
-        }
-    }
-    for (int t = threadIdx.x; t < k; t += kBlock) {
-        const uint64_t key = s_buf[t];
-        const int64_t o = (int64_t)(q_first + q) * k + t;
-        ids[o] = key == kNoKey ? -1 : (int32_t)(uint32_t)key;
-        dist[o] = key == kNoKey ? __builtin_nanf("") : sqrtf(__uint_as_float((uint32_t)(key >> 32)));
-    }
-}
-
 int knn_pass_queries(int D) {
     int qp = kKnnQueryFloats / (D + 4);
     qp = qp > kKnnPass ? kKnnPass : qp;
@@ -714,7 +765,7 @@ hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, in
         const int64_t NS = knn_lists(N, D, QB);
         if (D <= kKnnDimChunk) {
             const int64_t grid = NS / (kKnnWavesR / QB);
-            hipLaunchKernelGGL(k_knn_tiles_r, dim3((unsigned)grid), dim3(kKnnWavesR * 64), 0, s,
+            hipLaunchKernelGGL(k_knn_tiles_h, dim3((unsigned)grid), dim3(kKnnWavesR * 64), 0, s,
                                A);
         } else {
             const int64_t grid = NS / (kKnnWaves / QB);
