@@ -570,7 +570,10 @@ __device__ __forceinline__ float knn_f16_grid(float v) {
 // equals the scaled value up to the rounding of lo, whichever instructions
 // the conversions become.  With contraction the product could be rounded
 // differently for hi and for lo, and at an exact fp16 tie hi + lo missed
-// the value by one fp16 step.
+// the value by one fp16 step.  hi is placed on the fp16 grid with integer
+// operations on the rounded product's bits: a plain conversion, even with
+// __fmul_rn and contraction switched off for the function, still let the
+// compiler form mixed-precision operations that rounded the product twice.
 __device__ __forceinline__ void knn_split8(float4 a, float4 b, float sc, knn_h8& hi,
                                            knn_h8& lo) {
     const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
