@@ -556,33 +556,24 @@ typedef _Float16 knn_h8 __attribute__((ext_vector_type(8)));
 constexpr float kKnnSplitScale = 1024.0f;                  // 2^10
 constexpr float kKnnSplitUnscale = 1.0f / (1024.0f * 1024.0f);  // 2^-20, exact
 
-// v rounded to the nearest value with 11 significant bits, ties to even, on
-// the bits of v: a value of the fp16 grid for 2^-14 <= |v| < 65504, so its
-// conversion to fp16 is exact.  Below 2^-14 the whole of v goes to lo.
-__device__ __forceinline__ float knn_f16_grid(float v) {
-    const uint32_t b = __float_as_uint(v);
-    const float r = __uint_as_float((b + 0x0FFFu + ((b >> 13) & 1u)) & ~0x1FFFu);
-    return fabsf(v) >= 6.103515625e-05f ? r : 0.f;
-}
-
-// The split of 8 values scaled by sc.  Every step is an explicit rounding
-// (no contraction of the product into the later operations): hi + lo then
-// equals the scaled value up to the rounding of lo, whichever instructions
-// the conversions become.  With contraction the product could be rounded
-// differently for hi and for lo, and at an exact fp16 tie hi + lo missed
-// the value by one fp16 step.  hi is placed on the fp16 grid with integer
-// operations on the rounded product's bits: a plain conversion, even with
-// __fmul_rn and contraction switched off for the function, still let the
-// compiler form mixed-precision operations that rounded the product twice.
+// The split of 8 values scaled by sc.  Each product v is pinned as one fp32
+// value (an empty asm statement that the compiler must assume redefines it),
+// so the multiplication cannot be fused into the conversions: hi is the fp16
+// of v and the remainder v - hi is exact, so hi + lo equals v up to the
+// rounding of lo.  Left to the default contraction, the product was rounded
+// once for hi and once, differently, for lo, and at an exact fp16 tie hi + lo
+// missed v by one fp16 step; the pinned form also measured faster than
+// placing hi on the fp16 grid with integer operations on the bits of v.
 __device__ __forceinline__ void knn_split8(float4 a, float4 b, float sc, knn_h8& hi,
                                            knn_h8& lo) {
-    const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    float v[8] = {a.x * sc, a.y * sc, a.z * sc, a.w * sc, b.x * sc, b.y * sc, b.z * sc,
+                  b.w * sc};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const float v = __fmul_rn(x[e], sc);
-        const float g = knn_f16_grid(v);
-        hi[e] = (_Float16)g;                 // exact
-        lo[e] = (_Float16)__fsub_rn(v, g);   // the remainder is exact in fp32
+        asm volatile("" : "+v"(v[e]));
+        const _Float16 h = (_Float16)v[e];
+        hi[e] = h;
+        lo[e] = (_Float16)(v[e] - (float)h);
     }
 }
 
@@ -619,7 +610,8 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
         }
     }
     // this lane's 16 score slots: query i = 8 (r / 4) + 4 h + r % 4; the
-    // squared norm of a normalised query is 1 (0 for a zero query): one bit
+    // squared norm of a normalised query is 1 (0 for a zero query): one bit.
+    // A padding slot (no query) keeps the threshold -inf: nothing passes it.
     float thr[16];
     int32_t qid[16];
     uint32_t qone = 0u;
@@ -628,7 +620,7 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
         const int q = qb * 32 + 8 * (r / 4) + 4 * h + (r % 4);
         qone |= A.qn2[q] > 0.f ? 1u << r : 0u;
         qid[r] = A.qid[q];
-        thr[r] = __builtin_inff();
+        thr[r] = qid[r] >= 0 ? __builtin_inff() : -__builtin_inff();
     }
     if (lane < 32) {
         s_thr[w][lane] = kNoKey;
@@ -669,12 +661,14 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
             acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[c], bh, acc, 0, 0, 0);
         }
         bool staged = false;
+        const float nx1 = nx + 1.f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const float qn2 = (qone >> r) & 1u ? 1.f : 0.f;
-            float d2 = qn2 + nx - 2.f * kKnnSplitUnscale * acc[r];
+            // d^2 = |q|^2 + [r != 0] - 2 <q, r>, clamped at 0
+            const float base = (qone >> r) & 1u ? nx1 : nx;
+            float d2 = fmaf(-2.f * kKnnSplitUnscale, acc[r], base);
             d2 = d2 > 0.f ? d2 : 0.f;
-            if (d2 <= thr[r] && ok && qid[r] >= 0 && row != (int64_t)qid[r]) {
+            if (d2 <= thr[r] && ok && row != (int64_t)qid[r]) {
                 const int i = 8 * (r / 4) + 4 * h + (r % 4);
                 const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) | (uint64_t)row;
                 if (key < s_thr[w][i]) {
@@ -714,7 +708,8 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
         for (int r = 0; r < 16; ++r) {
             const int i = 8 * (r / 4) + 4 * h + (r % 4);
             const uint64_t tk = s_thr[w][i];
-            thr[r] = tk == kNoKey ? __builtin_inff() : __uint_as_float((uint32_t)(tk >> 32));
+            const float tv = tk == kNoKey ? __builtin_inff() : __uint_as_float((uint32_t)(tk >> 32));
+            thr[r] = qid[r] >= 0 ? tv : -__builtin_inff();
         }
     }
     if (h == 0) {
