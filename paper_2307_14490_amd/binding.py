@@ -188,6 +188,29 @@ def _dptr(t):
     return None if t is None else t.data_ptr()
 
 
+def _arg(t, dtypes, what):
+    """Device pointer of `t`, which must be a contiguous GPU tensor of one of
+    `dtypes` (torch dtype names): the C calls take raw pointers, so a tensor
+    of another type would be read as the wrong type."""
+    import torch
+    ok = (isinstance(t, torch.Tensor) and t.is_cuda and t.is_contiguous()
+          and any(t.dtype == getattr(torch, d) for d in dtypes))
+    if not ok:
+        got = (f"{t.dtype} on {t.device}{'' if t.is_contiguous() else ', not contiguous'}"
+               if isinstance(t, torch.Tensor) else type(t).__name__)
+        raise TypeError(f"{what}: expected a contiguous GPU tensor of {' or '.join(dtypes)}, "
+                        f"got {got}")
+    return t.data_ptr()
+
+
+def _batch(src, dst, cc, what):
+    """Pointers of a batch: int32 ids, int32 co_counts or float32 weights."""
+    if src.numel() != dst.numel() or src.numel() != cc.numel():
+        raise ValueError(f"{what}: src, dst and counts differ in length")
+    return (_arg(src, ("int32",), what + " src"), _arg(dst, ("int32",), what + " dst"),
+            _arg(cc, ("int32", "float32"), what + " counts"))
+
+
 def _is_float(t):
     import torch
     return t is not None and t.dtype == torch.float32
@@ -201,7 +224,8 @@ def cocount_weights(hist, dist_weights, stream=None):
     n, window = hist.shape
     wd = (ctypes.c_float * window)(*[float(x) for x in dist_weights])
     out = torch.empty(n, dtype=torch.float32, device=hist.device)
-    _ok(load().huge_cocount_weights(_dptr(hist), int(n), int(window), wd, _dptr(out),
+    _ok(load().huge_cocount_weights(_arg(hist, ("int32",), "cocount_weights hist"), int(n),
+                                    int(window), wd, _dptr(out),
                                     _stream_ptr(stream)), "huge_cocount_weights")
     return out
 
@@ -261,33 +285,38 @@ class Trainer:
     def step(self, src, dst, cc, first_pos, lr, loss_out=None, stream=None):
         loss = self.loss_buf if loss_out is None else loss_out
         fn = "huge_train_step_weighted" if _is_float(cc) else "huge_train_step"
-        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                int(first_pos), float(lr), _dptr(loss), _stream_ptr(stream)), fn)
+        ps, pd, pc = _batch(src, dst, cc, fn)
+        _ok(getattr(load(), fn)(self._h, ps, pd, pc, src.numel(), int(first_pos), float(lr),
+                                _arg(loss, ("float64",), fn + " loss"), _stream_ptr(stream)), fn)
         return loss
 
     def step_no_loss(self, src, dst, cc, first_pos, lr, stream=None):
         fn = "huge_train_step_weighted" if _is_float(cc) else "huge_train_step"
-        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                int(first_pos), float(lr), None, _stream_ptr(stream)), fn)
+        ps, pd, pc = _batch(src, dst, cc, fn)
+        _ok(getattr(load(), fn)(self._h, ps, pd, pc, src.numel(), int(first_pos), float(lr),
+                                None, _stream_ptr(stream)), fn)
 
     def prepare(self, src, dst, cc, first_pos, stream=None):
         """Group a batch (validation, negatives, de-duplication) into a slot."""
         fn = "huge_prepare_step_weighted" if _is_float(cc) else "huge_prepare_step"
-        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                int(first_pos), _stream_ptr(stream)), fn)
+        ps, pd, pc = _batch(src, dst, cc, fn)
+        _ok(getattr(load(), fn)(self._h, ps, pd, pc, src.numel(), int(first_pos),
+                                _stream_ptr(stream)), fn)
 
     def train_prepared(self, lr, loss_out=None, with_loss=True, stream=None):
         """Apply the oldest prepared batch; returns the loss tensor (or None)."""
         loss = (self.loss_buf if loss_out is None else loss_out) if with_loss else None
-        _ok(load().huge_train_prepared(self._h, float(lr), _dptr(loss), _stream_ptr(stream)),
+        pl = None if loss is None else _arg(loss, ("float64",), "huge_train_prepared loss")
+        _ok(load().huge_train_prepared(self._h, float(lr), pl, _stream_ptr(stream)),
             "huge_train_prepared")
         return loss
 
     def eval_loss(self, src, dst, cc, first_pos, loss_out=None, stream=None):
         loss = self.loss_buf if loss_out is None else loss_out
         fn = "huge_eval_loss_weighted" if _is_float(cc) else "huge_eval_loss"
-        _ok(getattr(load(), fn)(self._h, _dptr(src), _dptr(dst), _dptr(cc), src.numel(),
-                                int(first_pos), _dptr(loss), _stream_ptr(stream)), fn)
+        ps, pd, pc = _batch(src, dst, cc, fn)
+        _ok(getattr(load(), fn)(self._h, ps, pd, pc, src.numel(), int(first_pos),
+                                _arg(loss, ("float64",), fn + " loss"), _stream_ptr(stream)), fn)
         return loss
 
     def get_rows(self, table, ids, stream=None):
@@ -311,7 +340,8 @@ class Trainer:
         n = src.numel()
         if dst.numel() != n:
             raise ValueError("src and dst must have the same length")
-        _ok(load().huge_probe_rows(self._h, _dptr(src), _dptr(dst), n, int(first_pos),
+        _ok(load().huge_probe_rows(self._h, _arg(src, ("int32",), "probe_rows src"),
+                                   _arg(dst, ("int32",), "probe_rows dst"), n, int(first_pos),
                                    _stream_ptr(stream)), "huge_probe_rows")
 
     def check(self, stream=None) -> int:
@@ -362,6 +392,8 @@ def sample_walks(offsets, neighbors, num_nodes, walks_per_node, walk_steps, wind
     outputs sized to fit.  Returns (src, dst, cc, hist or None) on the device."""
     import torch
     L = load()
+    p_off = _arg(offsets, ("int64",), "sample_walks offsets")
+    p_nbr = _arg(neighbors, ("int32",), "sample_walks neighbors")
     cfg = walk_config(num_nodes, walks_per_node, walk_steps, window, seed_pairs_only, seed)
     if num_seeds is None:
         num_seeds = int(num_nodes) - int(first_seed)
@@ -376,7 +408,7 @@ def sample_walks(offsets, neighbors, num_nodes, walks_per_node, walk_steps, wind
     empty = torch.empty(0, dtype=torch.int32, device=dev)
 
     def run(cap, src, dst, cc, hist):
-        _ok(L.huge_sample_walks(ctypes.byref(cfg), _dptr(offsets), _dptr(neighbors),
+        _ok(L.huge_sample_walks(ctypes.byref(cfg), p_off, p_nbr,
                                 neighbors.numel(), int(first_seed), int(num_seeds),
                                 _dptr(src) if cap else None, _dptr(dst) if cap else None,
                                 _dptr(cc) if cap else None,
@@ -436,7 +468,9 @@ class Evaluator:
         n = int(n_edge) + int(n_non)
         u = torch.empty(n, dtype=torch.int32, device=self.device)
         v = torch.empty(n, dtype=torch.int32, device=self.device)
-        _ok(load().huge_eval_pairs(_dptr(offsets), _dptr(neighbors), int(num_nodes),
+        _ok(load().huge_eval_pairs(_arg(offsets, ("int64",), "Evaluator.pairs offsets"),
+                                   _arg(neighbors, ("int32",), "Evaluator.pairs neighbors"),
+                                   int(num_nodes),
                                    int(neighbors.numel()), int(seed), int(n_edge), int(n_non),
                                    int(max_tries), _dptr(u), _dptr(v), _dptr(self.status),
                                    _stream_ptr(stream)), "huge_eval_pairs")
@@ -446,8 +480,11 @@ class Evaluator:
     def distances(self, table, u, v, stream=None):
         import torch
         d = torch.empty(u.numel(), dtype=torch.float32, device=self.device)
-        _ok(load().huge_eval_distances(_dptr(table), table.shape[0], table.shape[1], _dptr(u),
-                                       _dptr(v), u.numel(), _dptr(d), _dptr(self.status),
+        _ok(load().huge_eval_distances(_arg(table, ("float32",), "Evaluator.distances table"),
+                                       table.shape[0], table.shape[1],
+                                       _arg(u, ("int32",), "Evaluator.distances u"),
+                                       _arg(v, ("int32",), "Evaluator.distances v"), u.numel(),
+                                       _dptr(d), _dptr(self.status),
                                        _stream_ptr(stream)), "huge_eval_distances")
         self._check("huge_eval_distances")
         return d
@@ -458,7 +495,8 @@ class Evaluator:
         q = (ctypes.c_double * len(quantiles))(*[float(x) for x in quantiles])
         nq = len(quantiles)
         out = torch.empty(5 + 2 * nq, dtype=torch.float64, device=self.device)
-        _ok(load().huge_eval_summary(_dptr(dist), int(n_edge), int(n_non), q, nq, _dptr(out),
+        _ok(load().huge_eval_summary(_arg(dist, ("float32",), "Evaluator.summary dist"),
+                                     int(n_edge), int(n_non), q, nq, _dptr(out),
                                      self._ws_ptr, self.ws_bytes, _stream_ptr(stream)),
             "huge_eval_summary")
         o = out.cpu().tolist()
@@ -475,7 +513,9 @@ class Evaluator:
         nq = queries.numel()
         ids = torch.empty((nq, k), dtype=torch.int32, device=self.device)
         dist = torch.empty((nq, k), dtype=torch.float32, device=self.device)
-        _ok(load().huge_eval_knn(_dptr(table), table.shape[0], table.shape[1], _dptr(queries),
+        _ok(load().huge_eval_knn(_arg(table, ("float32",), "Evaluator.knn table"),
+                                 table.shape[0], table.shape[1],
+                                 _arg(queries, ("int32",), "Evaluator.knn queries"),
                                  nq, k, _dptr(ids), _dptr(dist), self._ws_ptr, self.ws_bytes,
                                  _dptr(self.status), _stream_ptr(stream)), "huge_eval_knn")
         self._check("huge_eval_knn")
@@ -485,8 +525,11 @@ class Evaluator:
         import torch
         nq, k = ids.shape
         out = torch.empty(nq, dtype=torch.float64, device=self.device)
-        _ok(load().huge_eval_recall(_dptr(offsets), _dptr(neighbors), int(num_nodes),
-                                    int(neighbors.numel()), _dptr(queries), int(nq), _dptr(ids),
+        _ok(load().huge_eval_recall(_arg(offsets, ("int64",), "Evaluator.recall offsets"),
+                                    _arg(neighbors, ("int32",), "Evaluator.recall neighbors"),
+                                    int(num_nodes), int(neighbors.numel()),
+                                    _arg(queries, ("int32",), "Evaluator.recall queries"),
+                                    int(nq), _arg(ids, ("int32",), "Evaluator.recall ids"),
                                     int(k), _dptr(out), _dptr(self.status),
                                     _stream_ptr(stream)), "huge_eval_recall")
         self._check("huge_eval_recall")

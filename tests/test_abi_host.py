@@ -140,3 +140,14 @@ def test_calls_reject_bad_arguments_before_any_launch():
     assert L.huge_attach_tables(ctypes.byref(cfg), 4096, 8192, None, None, 1 << 20, need - 1,
                                 ctypes.byref(h)) == -4
     assert not h.value
+
+
+def test_host_tensors_are_refused_before_any_device_work():
+    """The C calls take raw device pointers: the binding refuses tensors of
+    another type or on the host instead of passing their memory on."""
+    torch = pytest.importorskip("torch")
+    with pytest.raises(TypeError, match="GPU tensor of int32"):
+        P.cocount_weights(torch.zeros((3, 2), dtype=torch.int32), [1.0, 0.5])
+    with pytest.raises(TypeError, match="int64"):
+        P.sample_walks(torch.zeros(4, dtype=torch.int64), torch.zeros(3, dtype=torch.int32),
+                       3, 1, 2, 1)

@@ -184,3 +184,16 @@ def test_training_tracks_the_float_tables():
     say(f"  epoch losses f32 {runs['f32']}, bf16 {runs['bf16']}")
     assert runs["f32"][1] < runs["f32"][0] and runs["bf16"][1] < runs["bf16"][0]
     assert runs["bf16"][1] == pytest.approx(runs["f32"][1], rel=0.02)
+
+
+def test_evaluator_refuses_a_bf16_table():
+    """The evaluators read fp32 rows; a bf16 table is refused by the binding
+    (its rows go through get_rows, which widens them)."""
+    tr = P.Trainer(100, 16, 3, 8, seed=1, dtype="bf16")
+    ev = P.Evaluator(100, 16, 8)
+    u = torch.zeros(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(TypeError, match="float32"):
+        ev.distances(tr.S, u, u)
+    ids = torch.arange(100, dtype=torch.int64)
+    d = ev.distances(tr.get_rows(0, ids), u, u)   # a row against itself
+    assert torch.all(d.abs() < 1e-3)

@@ -499,3 +499,17 @@ def test_invalid_prepared_batch_is_a_no_op():
     l2 = tr.train_prepared(0.1, loss_out=torch.zeros(1, dtype=torch.float64, device="cuda"))
     assert np.isfinite(l2.item())
     assert tr.check() == -2
+
+
+def test_batches_of_the_wrong_type_are_refused():
+    tr = _trainer(100, 8, 3, 16)
+    src = torch.zeros(16, dtype=torch.int64, device="cuda")
+    dst = torch.zeros(16, dtype=torch.int32, device="cuda")
+    cc = torch.ones(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(TypeError, match="src"):
+        tr.step(src, dst, cc, 0, 0.1)
+    with pytest.raises(ValueError, match="length"):
+        tr.step(dst, dst[:8], cc, 0, 0.1)
+    with pytest.raises(TypeError, match="counts"):
+        tr.step(dst, dst, cc.double(), 0, 0.1)
+    assert tr.check() == 0
