@@ -197,3 +197,30 @@ def test_evaluator_refuses_a_bf16_table():
     ids = torch.arange(100, dtype=torch.int64)
     d = ev.distances(tr.get_rows(0, ids), u, u)   # a row against itself
     assert torch.all(d.abs() < 1e-3)
+
+
+@pytest.mark.parametrize("bad", ["src", "count"])
+def test_invalid_batch_is_a_no_op_on_bf16_tables(bad):
+    """The same all-or-nothing rule as for fp32 tables: an out-of-range id or
+    a negative count leaves the bf16 tables bit for bit and is reported; an
+    empty batch changes nothing; the next valid batch is applied."""
+    N, D, K, n = 1000, 128, 5, 256
+    tr = P.Trainer(N, D, K, n, seed=2, dtype="bf16")
+    rng = np.random.default_rng(7)
+    src, dst, cc = _batch(rng, N, n)
+    if bad == "src":
+        src[100] = N
+    else:
+        cc[17] = -2
+    S0, T0 = tr.S.clone(), tr.T.clone()
+    loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), 0, 0.1).item()
+    assert np.isnan(loss)
+    assert tr.check() == (-2 if bad == "src" else -3)
+    assert torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+    e = torch.empty(0, dtype=torch.int32, device="cuda")
+    assert tr.step(e, e, e, 0, 0.1).item() == 0.0
+    assert tr.check() == 0 and torch.equal(tr.S, S0) and torch.equal(tr.T, T0)
+    s2, d2, c2 = _batch(rng, N, n)
+    loss = tr.step(dev(s2, torch), dev(d2, torch), dev(c2, torch), n, 0.1).item()
+    assert np.isfinite(loss) and tr.check() == 0
+    assert not torch.equal(tr.S, S0)
