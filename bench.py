@@ -369,7 +369,7 @@ def bench_eval(args):
         "data": "synthetic",
         "config": {"workload": "SBM-100M table (1e8 x 128 fp32, initial values), 100 queries, "
                                "k = 10", "num_rows": NB, "dim": DB, "queries": nq, "k": k},
-        "roofline": {"kernel": "k_knn_tiles_h", "bound": "hbm", "achieved": table_gbps,
+        "roofline": {"kernel": "k_knn_tiles_h4", "bound": "hbm", "achieved": table_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": table_gbps / HBM_PEAK_GBPS,
                      "traffic": None,
                      "note": f"the search reads the {NB * DB * 4 / 1e9:.1f} GB table once: "

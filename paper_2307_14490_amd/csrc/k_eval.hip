@@ -719,6 +719,177 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
     }
 }
 
+// The same search when a pass holds four query blocks (97-128 queries): the
+// four waves of a row tile (one per query block) share its load, norm and
+// split instead of each doing all of it.  Wave qb loads chunks 2 qb and
+// 2 qb + 1 (16-dimension chunks) of the tile's rows and publishes their
+// partial squared norms; after a barrier each wave forms the row scales,
+// splits its two chunks and publishes the fp16 parts; after a second barrier
+// every wave reads all eight chunks' parts from LDS for its products.  Every
+// wave of the workgroup runs the same number of iterations (that of the
+// workgroup's first tile stream; a stream past its last tile loads nothing
+// and offers no candidates), so all of them reach both barriers each time.
+// Candidates are staged as (d^2, row in tile) to leave LDS for the parts.
+__global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h4(KnnArgs A) {
+    constexpr int kQB = 4;
+    constexpr int kStreams = kKnnWavesR / kQB;  // tile streams per workgroup
+    constexpr int kCh = kKnnDimChunk / 16;      // 16-dimension chunks
+    __shared__ uint64_t s_list[kKnnWavesR][32][kKnnMaxK];
+    __shared__ float s_sd[kKnnWavesR][32][32];    // staged d^2
+    __shared__ uint8_t s_sx[kKnnWavesR][32][32];  // staged row within the tile
+    __shared__ uint64_t s_thr[kKnnWavesR][32];
+    __shared__ uint32_t s_cnt[kKnnWavesR][32];
+    __shared__ uint32_t s_len[kKnnWavesR][32];
+    __shared__ float s_nr[kStreams][kQB][32];     // partial squared norms of the rows
+    // fp16 parts of the tile: [stream][chunk][row][h] = {hi, lo} of 8 dimensions
+    __shared__ knn_h8 s_part[kStreams][kCh][32][2][2];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int x = lane & 31, h = lane >> 5;
+    const int D = A.D, k = A.k;
+    const int qb = w % kQB;
+    const int st = w / kQB;
+    const int64_t S0 = (int64_t)blockIdx.x * kStreams;
+    const int64_t S = S0 + st;
+    const int64_t NS = (int64_t)gridDim.x * kStreams;
+    const int d0 = 8 * h;
+    // iterations of every wave: those of the workgroup's first stream
+    const int64_t iters = A.tiles > S0 ? (A.tiles - S0 + NS - 1) / NS : 0;
+
+    // operands of query qb * 32 + x (already normalised)
+    knn_h8 qh[kCh], ql[kCh];
+    {
+        const float* qrow = A.qn + (int64_t)(qb * 32 + x) * D;
+#pragma unroll
+        for (int c = 0; c < kCh; ++c) {
+            const int d = 16 * c + d0;
+            const float4 a = d + 4 <= D ? *reinterpret_cast<const float4*>(qrow + d)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 b = d + 8 <= D ? *reinterpret_cast<const float4*>(qrow + d + 4)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+            knn_split8(a, b, kKnnSplitScale, qh[c], ql[c]);
+        }
+    }
+    float thr[16];
+    int32_t qid[16];
+    uint32_t qone = 0u;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int q = qb * 32 + 8 * (r / 4) + 4 * h + (r % 4);
+        qone |= A.qn2[q] > 0.f ? 1u << r : 0u;
+        qid[r] = A.qid[q];
+        thr[r] = qid[r] >= 0 ? __builtin_inff() : -__builtin_inff();
+    }
+    if (lane < 32) {
+        s_thr[w][lane] = kNoKey;
+        s_cnt[w][lane] = 0u;
+        s_len[w][lane] = 0u;
+    }
+
+    for (int64_t it = 0; it < iters; ++it) {
+        const int64_t t = S + it * NS;
+        const int64_t row = t * 32 + x;
+        const bool ok = t < A.tiles && row < A.N;
+        const float* src = A.T + (ok ? row : 0) * (int64_t)D;
+        // this wave's two chunks of row x
+        float4 bv[4];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int d = 16 * (2 * qb + j) + d0;
+            bv[2 * j] = (ok && d + 4 <= D) ? *reinterpret_cast<const float4*>(src + d)
+                                           : make_float4(0.f, 0.f, 0.f, 0.f);
+            bv[2 * j + 1] = (ok && d + 8 <= D) ? *reinterpret_cast<const float4*>(src + d + 4)
+                                               : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        float pn = 0.f;
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+            pn += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z + bv[m].w * bv[m].w;
+        pn += __shfl_xor(pn, 32, 64);
+        if (h == 0) s_nr[st][qb][x] = pn;
+        __syncthreads();
+        const float nr = (s_nr[st][0][x] + s_nr[st][1][x]) + (s_nr[st][2][x] + s_nr[st][3][x]);
+        const float sc = nr > 0.f ? kKnnSplitScale / sqrtf(nr) : 0.f;
+        const float nx = nr > 0.f ? 1.f : 0.f;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            knn_h8 bh, bl;
+            knn_split8(bv[2 * j], bv[2 * j + 1], sc, bh, bl);
+            s_part[st][2 * qb + j][x][h][0] = bh;
+            s_part[st][2 * qb + j][x][h][1] = bl;
+        }
+        __syncthreads();
+        knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
+                         0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < kCh; ++c) {
+            const knn_h8 bh = s_part[st][c][x][h][0];
+            const knn_h8 bl = s_part[st][c][x][h][1];
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[c], bh, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[c], bl, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[c], bh, acc, 0, 0, 0);
+        }
+        bool staged = false;
+        const float nx1 = nx + 1.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            // d^2 = |q|^2 + [r != 0] - 2 <q, r>, clamped at 0
+            const float base = (qone >> r) & 1u ? nx1 : nx;
+            float d2 = fmaf(-2.f * kKnnSplitUnscale, acc[r], base);
+            d2 = d2 > 0.f ? d2 : 0.f;
+            if (d2 <= thr[r] && ok && row != (int64_t)qid[r]) {
+                const int i = 8 * (r / 4) + 4 * h + (r % 4);
+                const uint64_t key = ((uint64_t)__float_as_uint(d2) << 32) | (uint64_t)row;
+                if (key < s_thr[w][i]) {
+                    const uint32_t pos = atomicAdd(&s_cnt[w][i], 1u);
+                    s_sd[w][i][pos] = d2;  // pos < 32: one row per lane x
+                    s_sx[w][i][pos] = (uint8_t)x;
+                    staged = true;
+                }
+            }
+        }
+        if (__ballot(staged) == 0ull) continue;  // wave-uniform: nothing to merge
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        if (h == 0) {
+            const uint32_t c = s_cnt[w][x];
+            if (c > 0u) {
+                uint64_t* L = s_list[w][x];
+                uint32_t len = s_len[w][x];
+                for (uint32_t e = 0; e < c; ++e) {
+                    const uint64_t key = ((uint64_t)__float_as_uint(s_sd[w][x][e]) << 32) |
+                                         (uint64_t)(t * 32 + s_sx[w][x][e]);
+                    if (len == (uint32_t)k && key >= L[k - 1]) continue;
+                    int p = len < (uint32_t)k ? (int)len : k - 1;
+                    while (p > 0 && L[p - 1] > key) {
+                        L[p] = L[p - 1];
+                        --p;
+                    }
+                    L[p] = key;
+                    if (len < (uint32_t)k) ++len;
+                }
+                s_len[w][x] = len;
+                s_cnt[w][x] = 0u;
+                s_thr[w][x] = len == (uint32_t)k ? L[k - 1] : kNoKey;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int i = 8 * (r / 4) + 4 * h + (r % 4);
+            const uint64_t tk = s_thr[w][i];
+            const float tv = tk == kNoKey ? __builtin_inff() : __uint_as_float((uint32_t)(tk >> 32));
+            thr[r] = qid[r] >= 0 ? tv : -__builtin_inff();
+        }
+    }
+    if (h == 0) {
+        const uint32_t len = s_len[w][x];
+        uint64_t* dst = A.partial + ((size_t)S * A.nqp + qb * 32 + x) * k;
+        for (int t = 0; t < k; ++t) dst[t] = (uint32_t)t < len ? s_list[w][x][t] : kNoKey;
+    }
+}
+
 int knn_pass_queries(int D) {
     int qp = kKnnQueryFloats / (D + 4);
     qp = qp > kKnnPass ? kKnnPass : qp;
@@ -763,8 +934,12 @@ hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, in
         const int64_t NS = knn_lists(N, D, QB);
         if (D <= kKnnDimChunk) {
             const int64_t grid = NS / (kKnnWavesR / QB);
-            hipLaunchKernelGGL(k_knn_tiles_h, dim3((unsigned)grid), dim3(kKnnWavesR * 64), 0, s,
-                               A);
+            if (QB == 4)
+                hipLaunchKernelGGL(k_knn_tiles_h4, dim3((unsigned)grid), dim3(kKnnWavesR * 64), 0,
+                                   s, A);
+            else
+                hipLaunchKernelGGL(k_knn_tiles_h, dim3((unsigned)grid), dim3(kKnnWavesR * 64), 0,
+                                   s, A);
         } else {
             const int64_t grid = NS / (kKnnWaves / QB);
             hipLaunchKernelGGL(k_knn_tiles, dim3((unsigned)grid), dim3(kKnnWaves * 64), 0, s, A);
