@@ -151,3 +151,13 @@ def test_host_tensors_are_refused_before_any_device_work():
     with pytest.raises(TypeError, match="int64"):
         P.sample_walks(torch.zeros(4, dtype=torch.int64), torch.zeros(3, dtype=torch.int32),
                        3, 1, 2, 1)
+
+
+def test_bench_refuses_several_gpus():
+    """The benchmark measures one GPU and says so for --gpus above 1."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120, cwd=root)
+    assert r.returncode == 2 and "one GPU" in r.stderr
