@@ -224,3 +224,27 @@ def test_invalid_batch_is_a_no_op_on_bf16_tables(bad):
     loss = tr.step(dev(s2, torch), dev(d2, torch), dev(c2, torch), n, 0.1).item()
     assert np.isfinite(loss) and tr.check() == 0
     assert not torch.equal(tr.S, S0)
+
+
+def test_alias_negatives_step_on_bf16_tables():
+    """Negatives from an alias table over degree^0.75-like weights (the
+    medium, power-law and hub-stress workloads' sampler), bf16 tables."""
+    N, D, K, n = 2000, 128, 6, 3000
+    rng = np.random.default_rng(12)
+    w = (rng.pareto(1.1, N) + 0.1) ** 0.75
+    w[::9] = 0.0
+    src, dst, cc = _batch(rng, N, n, hub=0.2)
+    seed, first, lr = 4, 99, 0.025
+    tr = P.Trainer(N, D, K, n, seed=seed, alias_weights=w, dtype="bf16")
+    loss = tr.step(dev(src, torch), dev(dst, torch), dev(cc, torch), first, lr).item()
+    assert tr.check() == 0
+    thr, alias = orc.build_alias(w)
+    neg = orc.sample_negatives(seed, first, n, K, N, thr, alias)
+    assert np.array_equal(tr.sample_negatives(n, first).cpu().numpy(), neg)
+    ids = np.arange(N)
+    S = orc.init_rows_bf16(seed, 0, ids, D, _half(D))
+    T = orc.init_rows_bf16(seed, 1, ids, D, _half(D))
+    ref = orc.step_dense_bf16(S, T, src, dst, cc, neg, lr)
+    assert_bf16_close(_bits(tr.S), S, "S")
+    assert_bf16_close(_bits(tr.T), T, "T")
+    assert loss == pytest.approx(ref, rel=1e-5, abs=1e-6)
