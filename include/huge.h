@@ -34,7 +34,9 @@
  *     and never aborts the process.  Argument errors are detected on the
  *     host before any launch and leave every buffer untouched.
  *   - Ids are int32 (N <= 2^31 - 1); row offsets are computed in 64 bits.
- *   - Tables are fp32, row-major, N x D, contiguous.
+ *   - Tables are row-major, N x D, contiguous: fp32, or bf16 with
+ *     huge_config.table_dtype = HUGE_DTYPE_BF16.  The evaluation calls read
+ *     fp32 tables (huge_get_rows widens bf16 rows).
  */
 #ifndef HUGE_H
 #define HUGE_H
@@ -379,9 +381,12 @@ huge_status huge_eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non
 /* The k rows nearest to each of the n_queries query rows (ids in d_queries),
    excluding the query itself: d_ids[q k + t] (device int32, ascending
    (distance, id); -1 if fewer than k other rows exist) and d_dist[...]
-   (device float).  Distances are computed in fp32 on the matrix cores from
-   the expansion d^2 = |q|^2 + |r|^2 - 2 <q, r> of the normalised rows.
-   1 <= k <= 32; dim <= 512.  Queries are processed in passes of up to
+   (device float).  Distances come from the expansion
+   d^2 = |q|^2 + |r|^2 - 2 <q, r> of the normalised rows on the matrix cores:
+   for dim <= 128 each value split into two fp16 parts (hi + lo, within
+   2^-22 of it) and the products hi.hi + hi.lo + lo.hi summed in fp32, which
+   is as accurate as fp32 products; wider rows in fp32.  1 <= k <= 32;
+   dim <= 512.  Queries are processed in passes of up to
    128 (dim <= 128), 64 (dim <= 256) or 32 over the table. */
 huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
                           const int32_t* d_queries, int32_t n_queries, int32_t k,
