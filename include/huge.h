@@ -384,8 +384,9 @@ huge_status huge_eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non
    (device float).  Distances come from the expansion
    d^2 = |q|^2 + |r|^2 - 2 <q, r> of the normalised rows on the matrix cores:
    for dim <= 128 each value split into two fp16 parts (hi + lo, within
-   2^-22 of it) and the products hi.hi + hi.lo + lo.hi summed in fp32, which
-   is as accurate as fp32 products; wider rows in fp32.  1 <= k <= 32;
+   2^-22 of it) and the products hi.hi + hi.lo + lo.hi summed in fp32 (about
+   2^-21 of each term, well inside the search's fp32 distance bound); wider
+   rows in fp32.  1 <= k <= 32;
    dim <= 512.  Queries are processed in passes of up to
    128 (dim <= 128), 64 (dim <= 256) or 32 over the table. */
 huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
