@@ -71,9 +71,35 @@ def read_traffic(workload: str, dtype: str = "f32"):
         return None
 
 
-def cpu_baseline(wl, seed, budget_s=15.0, max_batches=8):
-    """The CPU oracle on a bounded sample: whole batches of the same workload
-    (negatives drawn, touched rows initialised, one step) until budget_s."""
+def cpu_model() -> str:
+    """The host CPU's model name (first "model name" line of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+# Steps of the CPU oracle per workload: a whole epoch of the tiny workload,
+# the first 50 steps of the medium one, the first 3 of the large ones (all
+# within the time budget).
+CPU_STEPS = {"tiny": None, "medium": 50}
+CPU_STEPS_DEFAULT = 3
+
+
+def cpu_baseline(wl, seed, budget_s=30.0):
+    """The CPU oracle on a bounded sample of the same workload, single
+    threaded and pinned to one core of the calling thread's affinity set.
+
+    Each step is the oracle's own work, timed call by call: its negative
+    draws, the initial values of the rows the batch touches, and the double
+    precision step (C code).  The numpy glue between those calls (the
+    distinct row ids and the relabelling to them) is timed apart and not in
+    the rate."""
     import numpy as np
     from oracle import oracle as orc
     cfg = wl.cfg
@@ -81,25 +107,61 @@ def cpu_baseline(wl, seed, budget_s=15.0, max_batches=8):
     if cfg.neg_kind == "alias":
         thr, alias = orc.build_alias(wl.weights)
     a = float(np.float32(cfg.init_half_width))
-    done = 0
-    t_total = 0.0
-    b = 0
-    while b < max_batches and (t_total < budget_s or b == 0):
-        src, dst, cc = wl.batch(b)
-        t0 = time.perf_counter()
-        orc.step_sparse(seed, cfg.num_nodes, cfg.dim, cfg.num_neg, a, src, dst, cc,
-                        b * cfg.batch, cfg.lr, thr, alias)
-        t_total += time.perf_counter() - t0
-        done += src.size
-        b += 1
+    steps = CPU_STEPS.get(cfg.name, CPU_STEPS_DEFAULT)
+    batch = wl.batch
+    if steps is None:  # the epoch's corpus in batches
+        corpus = wl.epoch()
+        steps = -(-corpus[0].size // cfg.batch)
+
+        def batch(b):
+            return tuple(x[b * cfg.batch:(b + 1) * cfg.batch] for x in corpus)
+    allowed = sorted(os.sched_getaffinity(0))
+    core = allowed[0]
+    os.sched_setaffinity(0, {core})
+    t_oracle = t_glue = 0.0
+    done = b = 0
+    try:
+        while b < steps and (t_oracle + t_glue < budget_s or b == 0):
+            src, dst, cc = batch(b)
+            first = b * cfg.batch
+            t0 = time.perf_counter()
+            neg = orc.sample_negatives(seed, first, src.size, cfg.num_neg, cfg.num_nodes, thr,
+                                       alias)
+            t1 = time.perf_counter()
+            rows_S = np.unique(src.astype(np.int64))
+            rows_T = np.unique(np.concatenate([dst.astype(np.int64),
+                                               neg.reshape(-1).astype(np.int64)]))
+            t2 = time.perf_counter()
+            S = orc.init_rows(seed, 0, rows_S, cfg.dim, a)
+            T = orc.init_rows(seed, 1, rows_T, cfg.dim, a)
+            t3 = time.perf_counter()
+            src_c = np.searchsorted(rows_S, src).astype(np.int32)
+            dst_c = np.searchsorted(rows_T, dst).astype(np.int32)
+            neg_c = np.searchsorted(rows_T, neg.reshape(-1)).astype(np.int32).reshape(
+                src.size, cfg.num_neg)
+            t4 = time.perf_counter()
+            orc.step_dense(S, T, src_c, dst_c, cc, neg_c, cfg.lr)
+            t5 = time.perf_counter()
+            t_oracle += (t1 - t0) + (t3 - t2) + (t5 - t4)
+            t_glue += (t2 - t1) + (t4 - t3)
+            done += src.size
+            b += 1
+    finally:
+        os.sched_setaffinity(0, set(allowed))
     return {
-        "value": done / t_total,
+        "value": done / t_oracle,
         "unit": "positives/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"{b} batch(es) of {cfg.batch} positives of the {cfg.name} workload, "
-                  f"one step each from initial values (negative draws, touched-row init, "
-                  f"double-precision step), {t_total:.1f} s single-threaded",
+        "sample": f"the first {b} step(s) of the {cfg.name} workload ({cfg.batch} positives "
+                  f"each), each from initial values: negative draws, initial values of the "
+                  f"touched rows and the double-precision step, {t_oracle:.1f} s; "
+                  f"numpy glue (distinct ids, relabelling) {t_glue:.1f} s more, not in the rate",
+        "pinned_core": core,
+        "cpu_model": cpu_model(),
+        "cores_total": os.cpu_count(),
+        "cores_allowed": len(allowed),
+        "glue_s": t_glue,
     }
 
 
@@ -411,8 +473,8 @@ def main():
     ap.add_argument("--scatter", default="sorted", choices=["sorted", "atomic"])
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"],
                     help="element type of the tables (bf16: sorted scatter only)")
-    ap.add_argument("--batches", type=int, default=16, help="distinct pre-staged batches")
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--batches", type=int, default=64, help="distinct pre-staged batches")
+    ap.add_argument("--cpu-budget", type=float, default=30.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--sequential", action="store_true",
@@ -457,7 +519,7 @@ def main():
     torch.cuda.set_device(0)
     wl = make_workload(args.workload, args.seed)
     cfg = wl.cfg
-    R = max(1, min(args.batches, args.steps + args.warmup))
+    R = max(1, args.batches)
     t0 = time.time()
     host_batches = [wl.batch(b) for b in range(R)]
     log(f"[bench] {cfg.name}: {R} batches of {cfg.batch} generated in {time.time() - t0:.1f}s")
@@ -484,38 +546,46 @@ def main():
             per_batch_stats[b] = tr.stats()
 
     # default priority, like the current stream
-    sides = [torch.cuda.Stream(), torch.cuda.Stream()]
+    side = torch.cuda.Stream()
+    loss_buf = torch.zeros(1, dtype=torch.float64, device="cuda")
+    # A continuous training loop: batch k+1 is prepared (on the preparation
+    # stream, beside batch k's update) before batch k is applied (on the
+    # current stream).  `pending` counts prepared batches not yet applied.
+    state = {"pending": 0, "next_batch": 0, "pos": pos}
 
-    def run_steps(count, first_batch, pos, after_step=None):
-        """`count` steps.  Pipelined: batch k+1 is prepared before batch k is
-        applied on the current stream.  Batches are prepared on two side
-        streams in turn: the library issues batch k+1's radix pass on the
-        apply stream just before batch k's update and its grouping on batch
-        k+1's side stream, beside that update, so batch k+2's sampling (on the
-        other side stream) does not queue behind that grouping."""
+    def prepare_next():
+        b = state["next_batch"]
+        s, d, c = dev_batches[b % R]
+        tr.prepare(s, d, c, state["pos"], stream=side)
+        state["pos"] += n
+        state["next_batch"] = b + 1
+        state["pending"] += 1
+
+    def run_steps(count, after_step=None, drain=False):
+        """`count` steps, each the whole step of one batch (sampling,
+        grouping, gather, loss, update, loss sum).  Pipelined, the loop keeps
+        one batch prepared ahead; with drain the last step prepares none."""
         if args.sequential:
             for k in range(count):
-                s, d, c = dev_batches[(first_batch + k) % R]
-                tr.step_no_loss(s, d, c, pos, cfg.lr)
-                pos += n
+                b = state["next_batch"]
+                s, d, c = dev_batches[b % R]
+                tr.step(s, d, c, state["pos"], cfg.lr, loss_out=loss_buf)
+                state["pos"] += n
+                state["next_batch"] = b + 1
                 if after_step:
                     after_step(k)
-            return pos
-        s, d, c = dev_batches[first_batch % R]
-        tr.prepare(s, d, c, pos, stream=sides[first_batch % 2])
-        pos += n
+            return
+        if state["pending"] == 0:
+            prepare_next()
         for k in range(count):
-            if k + 1 < count:
-                b = first_batch + k + 1
-                s, d, c = dev_batches[b % R]
-                tr.prepare(s, d, c, pos, stream=sides[b % 2])
-                pos += n
-            tr.train_prepared(cfg.lr, with_loss=False, stream=stream)
+            if not (drain and k + 1 == count):
+                prepare_next()
+            tr.train_prepared(cfg.lr, loss_out=loss_buf, stream=stream)
+            state["pending"] -= 1
             if after_step:
                 after_step(k)
-        return pos
 
-    pos = run_steps(args.warmup, 0, pos)
+    run_steps(args.warmup)
     if tr.check() != 0:
         raise RuntimeError("device reported an error during warm-up")
     log("[bench] warm-up done")
@@ -529,11 +599,9 @@ def main():
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
-    for sd in sides:
-        sd.wait_event(ev0)
-    pos = run_steps(args.steps, args.warmup, pos)
-    for sd in sides:
-        stream.wait_stream(sd)  # groupings issued for batches past the last one
+    side.wait_event(ev0)
+    run_steps(args.steps)
+    stream.wait_stream(side)  # the preparation issued for the next batch
     ev1.record(stream)
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
@@ -547,12 +615,19 @@ def main():
         raise RuntimeError("device reported an error in the timed steps")
     ms_per_step = total_ms / args.steps
     value = n * args.steps / (total_ms / 1e3)
-    log(f"[bench] {args.steps} steps in {total_ms:.2f} ms: {ms_per_step:.4f} ms/step")
+    log(f"[bench] {args.steps} steps in {total_ms:.2f} ms: {ms_per_step:.4f} ms/step "
+        f"(last loss {loss_buf.item():.6g})")
 
     # Roofline probe: the rows of the same batches (sources, destinations and
     # the negatives a step would draw) read and written back unchanged, with
     # the fused kernel's launch shape and no arithmetic: the practical ceiling
     # of the step's random row traffic on this device.
+    run_steps(0, drain=True)  # nothing pending: the probe may not run beside a step
+    while state["pending"]:
+        tr.train_prepared(cfg.lr, loss_out=loss_buf, stream=stream)
+        state["pending"] -= 1
+    torch.cuda.synchronize()
+    pos = state["pos"]
     n_probe = min(args.steps, 50)
     for k in range(3):
         s, d, c = dev_batches[k % R]
@@ -571,18 +646,19 @@ def main():
     probe_gbps = probe_bytes / (probe_us * 1e-6) / 1e9
     log(f"[bench] probe: {probe_us:.1f} us per launch, {probe_gbps:.0f} GB/s")
 
-    phases = ["setup_sample", "radix", "group", "fused_step", "repeated_rows", "loss"]
+    phases = ["setup_sample", "radix", "group", "fused_step", "finish", "loss"]
     fused_us = phase_ms[3] / max(prof_steps, 1) * 1e3
+    state["pos"] = pos + 3 * n + n_probe * n
     # Phase breakdown from a separate pass of 50 steps with an event at every
     # phase boundary (those events lengthen each step by tens of microseconds,
     # so the timed steps above record only the two around the fused kernel).
     n_diag = min(50, args.steps)
     tr.profile_begin(n_diag, all_phases=True)
-    pos = run_steps(n_diag, args.warmup + args.steps, pos)
-    for sd in sides:
-        stream.wait_stream(sd)
+    run_steps(n_diag, drain=True)
+    stream.wait_stream(side)
     diag_ms, diag_steps = tr.profile_end()
     phase_avg_us = {p: diag_ms[i] / max(diag_steps, 1) * 1e3 for i, p in enumerate(phases)}
+    del phase_avg_us["loss"]  # folded into the finish kernel
 
     # Distribution of step times from another separate pass: an event on the
     # apply stream after every step (a queue packet of a few microseconds
@@ -590,10 +666,8 @@ def main():
     # steps k-1 and k.
     n_dist = min(200, args.steps) + 1
     dist_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_dist)]
-    pos = run_steps(n_dist, args.warmup + args.steps + n_diag, pos,
-                    after_step=lambda k: dist_ev[k].record(stream))
-    for sd in sides:
-        stream.wait_stream(sd)
+    run_steps(n_dist, after_step=lambda k: dist_ev[k].record(stream), drain=True)
+    stream.wait_stream(side)
     torch.cuda.synchronize()
     if tr.check() != 0:
         raise RuntimeError("device reported an error in the step-time pass")
@@ -608,6 +682,7 @@ def main():
     # here.
     if args.scatter == "sorted":
         seq = [(args.warmup + k) % R for k in range(args.steps)]
+        seq = [b for b in seq if b in per_batch_stats]
         uS = np.mean([per_batch_stats[b][0] for b in seq])
         uT = np.mean([per_batch_stats[b][1] for b in seq])
         dup = np.mean([per_batch_stats[b][2] for b in seq])
@@ -631,7 +706,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32",  # the arithmetic type (bf16 tables compute in fp32)
         "data": "synthetic",
         "config": {
             "workload": cfg.name,
@@ -645,7 +720,7 @@ def main():
             "lr": cfg.lr,
             "staged_batches": R,
             "grouping": ("sequential" if args.sequential else
-                         "overlapped with the previous apply (two side streams in turn)"),
+                         "on a preparation stream, beside the previous batch's update"),
         },
         "roofline": {
             "kernel": KERNEL if args.scatter == "sorted" else "k_atomic_gather",

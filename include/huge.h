@@ -48,6 +48,12 @@
 extern "C" {
 #endif
 
+/* The library is built with hidden symbol visibility: the declarations of
+   this header are its only exports. */
+#if defined(__GNUC__)
+#pragma GCC visibility push(default)
+#endif
+
 typedef int32_t huge_status;
 #define HUGE_OK 0
 #define HUGE_ERR_INVALID_ARG (-1)     /* null pointer, bad size or config          */
@@ -151,25 +157,25 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
                             const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                             float lr, double* d_loss_sum, void* stream);
 
-/* The same step in two halves, so that the next batch is grouped while the
+/* The same step in two halves, so that later batches are grouped while the
    current one is applied (grouping never reads or writes the tables).
-     huge_prepare_step   : validation, negative draws and grouping keys of a
-                           batch, on `stream` (the grouping stream); at most
-                           two prepared batches may be pending
+     huge_prepare_step   : validation, negative draws and the whole grouping
+                           of a batch (keys, radix pass on the lowest digit,
+                           per-bucket grouping), on `stream` (the preparation
+                           stream); at most two prepared batches may be
+                           pending
      huge_train_prepared : the gather, loss and update of the oldest prepared
-                           batch, with the given lr and loss output, on
-                           `stream` (the apply stream)
-   huge_train_prepared also issues the rest of the grouping: on the apply
-   stream, whatever its own batch still lacks and then the radix pass of the
-   next prepared batch (it runs alone, before the update); on the next
-   batch's grouping stream, that batch's per-bucket grouping (it runs beside
-   the update).  So the stream given to huge_prepare_step must stay valid
-   until the batch is applied.  The library orders all of this with HIP
-   events: every stage waits for the previous stage of its batch, an apply
-   for the previous apply, a new batch for the apply that last used its
-   grouping buffers.  The batch arrays must stay valid until the batch is
-   applied.  Results are bitwise those of huge_train_step, which is the two
-   halves on one stream and requires that no batch is pending. */
+                           batch (the fused kernel, then the repeated rows
+                           and the loss sum), with the given lr and loss
+                           output, on `stream` (the apply stream)
+   The grouping kernels run in workgroups of few registers, so that on a
+   preparation stream of their own they run beside the previous batch's
+   update.  The library orders the halves with HIP events: an apply waits for
+   its batch's preparation and for the previous apply, a preparation for the
+   apply that last used its grouping buffers.  The batch arrays must stay
+   valid until the batch is applied.  Results are bitwise those of
+   huge_train_step, which is the two halves on one stream and requires that
+   no batch is pending. */
 huge_status huge_prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
                               const int32_t* d_cc, int64_t n, uint64_t first_pos_index,
                               void* stream);
@@ -250,12 +256,13 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
    spreads that cost.  huge_profile_end waits for all of them on `stream`,
    writes the summed durations in milliseconds to phase_ms[HUGE_PHASES] (0
    for phases not recorded) and the number of recorded steps to *steps, and
-   releases the events.  Phases: 0 set-up and negative sampling, 1 the radix
-   pass, 2 the per-bucket grouping (1 and 2 are empty for the atomic
-   scatter), 3 the fused gather/loss/update kernel (atomic scatter: gather
-   and coefficients), 4 repeated rows (atomic scatter: the atomic adds), 5
-   loss sum.  Errors: max_steps or every outside [1, 10^6], all_phases not
-   0 or 1. */
+   releases the events.  Phases: 0 set-up, negative sampling, tile counts
+   and prefixes, 1 the radix pass, 2 the per-bucket grouping (1 and 2 are
+   empty for the atomic scatter), 3 the fused gather/loss/update kernel
+   (atomic scatter: gather and coefficients), 4 the finish kernel: repeated
+   rows and the loss sum (atomic scatter: the atomic adds and the loss sum),
+   5 always 0 (the loss sum has no kernel of its own).  Errors: max_steps or
+   every outside [1, 10^6], all_phases not 0 or 1. */
 #define HUGE_PHASES 6
 huge_status huge_profile_begin(huge_handle* h, int32_t max_steps, int32_t all_phases,
                                int32_t every);
@@ -403,6 +410,10 @@ huge_status huge_eval_recall(const int64_t* d_offsets, const int32_t* d_neighbor
 
 void huge_destroy(huge_handle* h);
 const char* huge_status_string(huge_status s);
+
+#if defined(__GNUC__)
+#pragma GCC visibility pop
+#endif
 
 #ifdef __cplusplus
 }

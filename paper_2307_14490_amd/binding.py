@@ -230,6 +230,27 @@ def cocount_weights(hist, dist_weights, stream=None):
     return out
 
 
+def _check_tables(tables, num_nodes, dim, dtype, device):
+    """Caller-supplied (S, T): each must be a contiguous (num_nodes, dim)
+    tensor of `dtype` on `device`; every step writes rows of both at offsets
+    computed from num_nodes and dim, so a smaller, strided or host table would
+    be written out of bounds.  Checked before anything is allocated."""
+    import torch
+    if not (isinstance(tables, (tuple, list)) and len(tables) == 2):
+        raise TypeError("tables: expected a pair (S, T) of tensors")
+    for name, t in zip(("S", "T"), tables):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"table {name}: expected a tensor, got {type(t).__name__}")
+        if tuple(t.shape) != (num_nodes, dim):
+            raise ValueError(f"table {name}: shape {tuple(t.shape)}, expected ({num_nodes}, {dim})")
+        if t.dtype != dtype:
+            raise ValueError(f"table {name}: dtype {t.dtype}, expected {dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"table {name}: not contiguous")
+        if t.device.type != "cuda" or (device.index is not None and t.device != device):
+            raise ValueError(f"table {name}: on {t.device}, expected {device}")
+
+
 class Trainer:
     """Tables, workspace and a libhuge handle on one GPU.
 
@@ -253,13 +274,12 @@ class Trainer:
         ws = workspace_bytes(self.cfg)
         if ws == 0:
             raise HugeError(HUGE_ERR_INVALID_ARG, "huge_workspace_bytes")
-        if tables is None:
+        if tables is not None:
+            _check_tables(tables, int(num_nodes), int(dim), tdt, self.device)
+            self.S, self.T = tables
+        else:
             self.S = torch.empty((num_nodes, dim), dtype=tdt, device=self.device)
             self.T = torch.empty((num_nodes, dim), dtype=tdt, device=self.device)
-        else:
-            self.S, self.T = tables
-            if self.S.dtype != tdt or self.T.dtype != tdt:
-                raise ValueError(f"tables must be {tdt}")
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=self.device)
         if kind == HUGE_NEG_ALIAS:
             thr, alias = build_alias(alias_weights)
@@ -438,6 +458,21 @@ def sample_walks(offsets, neighbors, num_nodes, walks_per_node, walk_steps, wind
 # --------------------------------------------------------------------------- #
 # Embedding evaluation (argument marshalling for the huge_eval_* calls)
 # --------------------------------------------------------------------------- #
+def _check_csr(offsets, neighbors, num_nodes, what):
+    """A CSR graph of num_nodes nodes: num_nodes + 1 offsets (the kernels read
+    offsets[u] and offsets[u + 1] for every node u)."""
+    if offsets.dim() != 1 or offsets.numel() != int(num_nodes) + 1:
+        raise ValueError(f"{what}: {offsets.numel()} offsets for {int(num_nodes)} nodes "
+                         f"(expected num_nodes + 1)")
+    if neighbors.dim() != 1:
+        raise ValueError(f"{what}: neighbors must be one-dimensional")
+
+
+def _check_table2d(table, what):
+    if table.dim() != 2:
+        raise ValueError(f"{what}: table must be two-dimensional, got shape {tuple(table.shape)}")
+
+
 class Evaluator:
     """Workspace and status word for the huge_eval_* calls on one table shape.
     Each method checks the device status word after its call (synchronising
@@ -465,6 +500,7 @@ class Evaluator:
               stream=None):
         """(u, v) int32 device tensors: n_edge edge pairs, then n_non non-edges."""
         import torch
+        _check_csr(offsets, neighbors, num_nodes, "Evaluator.pairs")
         n = int(n_edge) + int(n_non)
         u = torch.empty(n, dtype=torch.int32, device=self.device)
         v = torch.empty(n, dtype=torch.int32, device=self.device)
@@ -479,6 +515,9 @@ class Evaluator:
 
     def distances(self, table, u, v, stream=None):
         import torch
+        _check_table2d(table, "Evaluator.distances")
+        if u.numel() != v.numel():
+            raise ValueError("Evaluator.distances: u and v differ in length")
         d = torch.empty(u.numel(), dtype=torch.float32, device=self.device)
         _ok(load().huge_eval_distances(_arg(table, ("float32",), "Evaluator.distances table"),
                                        table.shape[0], table.shape[1],
@@ -492,6 +531,9 @@ class Evaluator:
     def summary(self, dist, n_edge, n_non, quantiles=(0, 10, 25, 50, 75, 90, 100), stream=None):
         """dict: count_edge, count_non, mean_edge, mean_non, snr, pct_edge, pct_non."""
         import torch
+        if int(n_edge) < 0 or int(n_non) < 0 or dist.numel() < int(n_edge) + int(n_non):
+            raise ValueError(f"Evaluator.summary: {dist.numel()} distances for "
+                             f"{int(n_edge)} + {int(n_non)} pairs")
         q = (ctypes.c_double * len(quantiles))(*[float(x) for x in quantiles])
         nq = len(quantiles)
         out = torch.empty(5 + 2 * nq, dtype=torch.float64, device=self.device)
@@ -510,6 +552,7 @@ class Evaluator:
         k = self.k if k is None else int(k)
         if k > self.k:
             raise HugeError(HUGE_ERR_INVALID_ARG, "Evaluator.knn: k above the workspace's")
+        _check_table2d(table, "Evaluator.knn")
         nq = queries.numel()
         ids = torch.empty((nq, k), dtype=torch.int32, device=self.device)
         dist = torch.empty((nq, k), dtype=torch.float32, device=self.device)
@@ -523,6 +566,10 @@ class Evaluator:
 
     def recall(self, offsets, neighbors, num_nodes, queries, ids, stream=None):
         import torch
+        _check_csr(offsets, neighbors, num_nodes, "Evaluator.recall")
+        if ids.dim() != 2 or ids.shape[0] != queries.numel():
+            raise ValueError(f"Evaluator.recall: ids of shape {tuple(ids.shape)} for "
+                             f"{queries.numel()} queries")
         nq, k = ids.shape
         out = torch.empty(nq, dtype=torch.float64, device=self.device)
         _ok(load().huge_eval_recall(_arg(offsets, ("int64",), "Evaluator.recall offsets"),

@@ -25,10 +25,12 @@ ARCH = "gfx950"
 HIP_FLAGS = [
     "-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-fno-gpu-rdc", "-Wall", "-Wno-unused-function",
+    "-fno-gpu-rdc", "-Wall", "-Wno-unused-function", "-fvisibility=hidden",
+    "-fvisibility-inlines-hidden",
     "-I", os.path.join(ROOT, "include"),
 ]
-CXX_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include")]
+CXX_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-fvisibility=hidden",
+             "-fvisibility-inlines-hidden", "-I", os.path.join(ROOT, "include")]
 
 
 def _hipcc() -> str:
@@ -56,7 +58,8 @@ def build(verbose: bool = False) -> str:
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [_hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs]
+    cmd = [_hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}",
+           f"-Wl,--version-script={os.path.join(CSRC, 'libhuge.map')}", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -1,21 +1,19 @@
 // C-ABI host layer of libhuge: argument checks, workspace layout, and the
 // launch sequence of each call on the caller's streams.
 //
-// A batch goes through four stages: sampling (k_begin, k_sample: validation,
-// negatives, keys, digit counts), the radix pass (k_radix_pass: keys grouped
-// by their lowest digit), grouping (k_group: repeated rows and their slots)
-// and the apply (k_fused_step, the repeated-row kernels, the loss).  The
-// first three read only the batch; the apply reads and writes the tables.
-// huge_prepare_step issues the sampling on the caller's grouping stream.
-// huge_train_prepared issues, on the apply stream, whatever its own batch
-// still lacks, then the radix pass of the next prepared batch -- while
-// nothing else runs: its 1024-thread workgroups would find no free CU beside
-// an apply -- then the apply; the next batch's grouping (256-thread
-// workgroups) goes to that batch's grouping stream, where it runs beside the
-// apply.  kSlots grouping slots let two batches be prepared ahead; events
-// order the stages: a stage waits for the previous stage of its batch, an
-// apply for the previous apply, a sampling for the apply that last used its
-// slot.
+// A batch is prepared, then applied.  Preparing (huge_prepare_step, on the
+// caller's preparation stream) validates the batch, draws its negatives and
+// groups its rows: k_begin, k_sample (keys, negatives), k_tile_count and
+// k_tile_scan (digit counts per tile and their prefixes), k_radix_pass
+// (occurrences grouped by the lowest digit of their key) and k_group
+// (repeated rows and their slots).  These read only the batch, and every one
+// of them runs in 256-thread workgroups of few registers, so that they run
+// beside the previous batch's apply without evicting its waves.  Applying
+// (huge_train_prepared, on the apply stream) runs the fused step and the
+// finish kernel (repeated rows, loss).  kSlots grouping slots let two batches
+// be prepared ahead; events order the halves: an apply waits for its batch's
+// preparation and for the previous apply, a preparation for the apply that
+// last used its slot.
 #include <math.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -31,12 +29,13 @@ using namespace huge;
 
 namespace {
 
-// Events recorded per profiled batch: sampling start and end, radix pass
-// start and end, grouping start and end, apply start, after the fused
-// kernel, after the repeated rows, after the loss.
+// Events recorded per profiled batch: sampling start and end (after the
+// tile prefixes), radix pass start and end, grouping start and end, apply
+// start, after the fused kernel, after the finish kernel (repeated rows and
+// the loss), and a last one at the same point (the loss has no kernel of
+// its own).
 constexpr int kProfEvents = 10;
 constexpr int kMaxPending = 2;  // prepared batches not yet applied
-constexpr int kBesideGrid = 0;  // workgroups of a grouping beside an apply (0: one per bucket)
 
 struct PendingBatch {
     const int32_t* src = nullptr;
@@ -45,9 +44,7 @@ struct PendingBatch {
     const float* w = nullptr;    // float weights in place of cc
     int64_t n = 0;
     uint64_t first_pos = 0;
-    int stage = 0;               // 0 sampled, 1 radix pass issued, 2 grouped
     hipStream_t gstream = nullptr;  // the stream of its huge_prepare_step
-    hipStream_t stage_stream = nullptr;  // the stream of its last stage
     int prof = -1;               // index of its profile events, or -1
 };
 
@@ -64,13 +61,11 @@ struct huge_handle {
     Layout lay;
     SortPlan plan;  // digit width of the radix pass for keys below 2N
     int key_bits;   // bits of 2N - 1
-    int64_t prepared;          // batches sampled
+    int64_t prepared;          // batches prepared
     int64_t applied;           // applies issued
     int last_applied_slot;     // -1 before the first apply
     PendingBatch pending[kSlots];
-    hipEvent_t sampled[kSlots];  // sampling of the slot's batch complete
-    hipEvent_t radixed[kSlots];  // its radix pass complete
-    hipEvent_t ready[kSlots];    // its grouping complete
+    hipEvent_t ready[kSlots];    // preparation of the slot's batch complete
     hipEvent_t done[kSlots];     // its apply complete
     // phase timing
     std::vector<hipEvent_t> prof_ev;
@@ -78,12 +73,16 @@ struct huge_handle {
     int32_t prof_max = 0, prof_next = 0;  // batches to profile; profiled so far
     int32_t prof_every = 1, prof_seen = 0;  // every prof_every-th batch; batches seen
     bool prof_all = false;     // events at every phase boundary, not only the fused kernel
-    // the stream each kind of stage last used, so that a wait on an event of
-    // the same stream is skipped (the stream orders it already)
+    // the stream of the last apply and of each slot's last apply, so that a
+    // wait on an event of the same stream is skipped (the stream orders it)
     hipStream_t last_apply_stream = nullptr;
     hipStream_t slot_apply_stream[kSlots] = {};
-    int beside_grid = kBesideGrid;  // workgroups of a grouping beside an apply
-    int group_bits = 0;             // grouping table bits; 0: from the mean bucket size
+    // calls outside the step that read or write the tables or the shared
+    // apply regions (huge_eval_loss, huge_get_rows, huge_probe_rows): the
+    // next apply waits for the last of them
+    hipEvent_t side_done = nullptr;
+    hipStream_t side_stream = nullptr;
+    bool side_pending = false;
 };
 
 namespace {
@@ -146,7 +145,7 @@ Layout make_layout(const huge_config* c) {
         SlotLayout& S = L.slot[s];
         S.ctrl = take(sizeof(Control));
         S.hist = take(sizeof(uint32_t) * kMaxBins);
-        S.neg = take(sizeof(int32_t) * (size_t)(nb * K));
+        if (!sorted) S.neg = take(sizeof(int32_t) * (size_t)(nb * K));
         if (sorted) {
             S.keys0 = take(sizeof(uint32_t) * (size_t)M);
             S.keys1 = take(sizeof(uint32_t) * (size_t)M);
@@ -158,6 +157,7 @@ Layout make_layout(const huge_config* c) {
             S.shorts = take(sizeof(uint4) * (size_t)caps.shorts);
             S.pieces = take(sizeof(uint4) * (size_t)caps.pieces);
             S.combs = take(sizeof(uint4) * (size_t)caps.combs);
+            S.ccount = take(sizeof(uint32_t) * (size_t)caps.combs);
             S.wstats = take(sizeof(uint32_t) * kMaxBins * 3);
         }
     }
@@ -217,9 +217,10 @@ void destroy_handle(huge_handle* h) {
     if (!h) return;
     release_profile(h);
     for (int s = 0; s < kSlots; ++s) {
-        for (hipEvent_t e : {h->sampled[s], h->radixed[s], h->ready[s], h->done[s]})
+        for (hipEvent_t e : {h->ready[s], h->done[s]})
             if (e) (void)hipEventDestroy(e);
     }
+    if (h->side_done) (void)hipEventDestroy(h->side_done);
     delete h;
 }
 
@@ -246,29 +247,25 @@ huge_status create(const huge_config* cfg, void* S, void* T, const uint32_t* thr
     h->lay = L;
     h->key_bits = key_bits(cfg->num_nodes);
     h->plan = sort_plan(h->key_bits);
-    if (const char* e = getenv("HUGE_BESIDE_GRID")) {  // tuning experiments
-        const int g = atoi(e);
-        if (g >= 0 && g <= 65536) h->beside_grid = g;
-    }
-    if (const char* e = getenv("HUGE_GROUP_TABLE_BITS")) {  // tuning experiments
-        const int g = atoi(e);
-        if (g >= kTableBitsMin && g <= kTableBitsMax) h->group_bits = g;
-    }
     h->prepared = h->applied = 0;
     h->last_applied_slot = -1;
-    for (int s = 0; s < kSlots; ++s)
-        h->sampled[s] = h->radixed[s] = h->ready[s] = h->done[s] = nullptr;
+    for (int s = 0; s < kSlots; ++s) h->ready[s] = h->done[s] = nullptr;
+    // the events order streams of this device only: a device-scope release
+    // suffices (the default one is system-scope)
+    const unsigned flags = hipEventDisableTiming | hipEventReleaseToDevice;
     for (int s = 0; s < kSlots; ++s) {
-        // the events order streams of this device only: a device-scope
-        // release suffices (the default one is system-scope)
-        for (hipEvent_t* e : {&h->sampled[s], &h->radixed[s], &h->ready[s], &h->done[s]}) {
-            if (hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventReleaseToDevice) !=
-                hipSuccess) {
+        for (hipEvent_t* e : {&h->ready[s], &h->done[s]}) {
+            if (hipEventCreateWithFlags(e, flags) != hipSuccess) {
                 *e = nullptr;
                 destroy_handle(h);
                 return HUGE_ERR_HIP;
             }
         }
+    }
+    if (hipEventCreateWithFlags(&h->side_done, flags) != hipSuccess) {
+        h->side_done = nullptr;
+        destroy_handle(h);
+        return HUGE_ERR_HIP;
     }
     *out = h;
     return HUGE_OK;
@@ -308,14 +305,36 @@ hipError_t wait_on(hipStream_t s, hipEvent_t e, hipStream_t from) {
     return hipStreamWaitEvent(s, e, 0);
 }
 
-// Stage 1: validation, negatives, keys, per-tile digit counts and their
-// prefixes over tiles, of a batch, into the next slot, on the grouping
-// stream s (launches only; arguments checked).
-huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
-                         const int32_t* cc, const float* w, int64_t n, uint64_t first_pos,
-                         hipStream_t s) {
+// A call outside the step on stream s: ordered after the last apply (it
+// reads the tables or the shared apply regions) ...
+hipError_t side_begin(huge_handle* h, hipStream_t s) {
+    if (h->side_pending) {  // and after the previous such call (shared regions)
+        const hipError_t e = wait_on(s, h->side_done, h->side_stream);
+        if (e != hipSuccess) return e;
+    }
+    if (h->last_applied_slot < 0) return hipSuccess;
+    return wait_on(s, h->done[h->last_applied_slot], h->last_apply_stream);
+}
+
+// ... and the next apply ordered after it.
+hipError_t side_end(huge_handle* h, hipStream_t s) {
+    const hipError_t e = hipEventRecord(h->side_done, s);
+    if (e == hipSuccess) {
+        h->side_stream = s;
+        h->side_pending = true;
+    }
+    return e;
+}
+
+// The preparation of a batch into the next slot, on stream s: validation,
+// negatives and keys, tile counts and prefixes, radix pass, grouping
+// (launches only; arguments checked).
+huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst,
+                          const int32_t* cc, const float* w, int64_t n, uint64_t first_pos,
+                          hipStream_t s) {
     const int slot = (int)(h->prepared % kSlots);
     const SlotLayout& SL = h->lay.slot[slot];
+    const Layout& L = h->lay;
     Control* ctl = at<Control>(h, SL.ctrl);
     uint32_t* hist = at<uint32_t>(h, SL.hist);
     const TableArgs t = table_args(h);
@@ -339,126 +358,93 @@ huge_status stage_sample(huge_handle* h, const int32_t* src, const int32_t* dst,
     if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
     HIP_TRY(launch_begin(ctl, s));
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
-    HIP_TRY(launch_sample(t, ctl, a, at<int32_t>(h, SL.neg),
-                          sorted ? at<uint32_t>(h, SL.keys0) : nullptr,
-                          sorted ? at<int32_t>(h, SL.info) : nullptr, s));
+    HIP_TRY(launch_sample(t, ctl, a, sorted ? nullptr : at<int32_t>(h, SL.neg),
+                          sorted ? at<uint32_t>(h, SL.keys0) : nullptr, s));
     if (sorted) {
         const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-        HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, h->plan.bits, 0,
+        const int bits = h->plan.bits;
+        HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, bits, 0,
                                   at<uint32_t>(h, SL.tcount), s));
-        HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, h->plan.bits,
+        HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, bits,
                                  at<uint32_t>(h, SL.tprefix), hist, s));
+        if (!prof_mark(h, b, 1, s) || !prof_mark(h, b, 2, s)) return HUGE_ERR_HIP;
+        HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1),
+                                  at<uint32_t>(h, SL.vals1), m, bits, 0, hist,
+                                  at<uint32_t>(h, SL.tprefix), at<uint32_t>(h, SL.bstart), s));
+        if (!prof_mark(h, b, 3, s) || !prof_mark(h, b, 4, s)) return HUGE_ERR_HIP;
+        const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
+        HIP_TRY(launch_group(ctl, at<uint32_t>(h, SL.keys1), at<uint32_t>(h, SL.vals1), m,
+                             h->cfg.num_nodes, hist, at<uint32_t>(h, SL.bstart),
+                             at<int32_t>(h, SL.info), at<uint4>(h, SL.shorts),
+                             at<uint4>(h, SL.pieces), at<uint4>(h, SL.combs),
+                             at<uint32_t>(h, SL.ccount), caps, at<uint32_t>(h, SL.wstats),
+                             1 << bits, h->key_bits, s));
+        if (!prof_mark(h, b, 5, s)) return HUGE_ERR_HIP;
+    } else {
+        // the atomic scatter needs no grouping
+        for (int k = 1; k <= 5; ++k)
+            if (!prof_mark(h, b, k, s)) return HUGE_ERR_HIP;
     }
-    if (!prof_mark(h, b, 1, s)) return HUGE_ERR_HIP;
-    HIP_TRY(hipEventRecord(h->sampled[slot], s));
-    b.stage = sorted ? 0 : 2;  // the atomic scatter needs no grouping
-    if (!sorted) HIP_TRY(hipEventRecord(h->ready[slot], s));
-    b.stage_stream = s;
+    HIP_TRY(hipEventRecord(h->ready[slot], s));
     h->pending[slot] = b;
     h->prepared += 1;
     return HUGE_OK;
 }
 
-// Stage 2: the radix pass of the batch in `slot`, on s.
-huge_status stage_radix(huge_handle* h, int slot, hipStream_t s) {
-    PendingBatch& b = h->pending[slot];
-    const SlotLayout& SL = h->lay.slot[slot];
-    Control* ctl = at<Control>(h, SL.ctrl);
-    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-    HIP_TRY(wait_on(s, h->sampled[slot], b.stage_stream));
-    if (!prof_mark(h, b, 2, s)) return HUGE_ERR_HIP;
-    HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1),
-                              at<uint32_t>(h, SL.vals1), m, h->plan.bits, 0,
-                              at<uint32_t>(h, SL.hist), at<uint32_t>(h, SL.tprefix),
-                              at<uint32_t>(h, SL.bstart), s));
-    if (!prof_mark(h, b, 3, s)) return HUGE_ERR_HIP;
-    HIP_TRY(hipEventRecord(h->radixed[slot], s));
-    b.stage = 1;
-    b.stage_stream = s;
-    return HUGE_OK;
-}
-
-// Stage 3: grouping of the batch in `slot`, on s.  Beside an apply
-// (`beside`), its workgroups are few and loop over the buckets, so that they
-// hold a slot of the fused kernel on only a few CUs.
-huge_status stage_group(huge_handle* h, int slot, hipStream_t s, bool beside) {
-    PendingBatch& b = h->pending[slot];
-    const SlotLayout& SL = h->lay.slot[slot];
-    const Layout& L = h->lay;
-    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-    HIP_TRY(wait_on(s, h->radixed[slot], b.stage_stream));
-    if (!prof_mark(h, b, 4, s)) return HUGE_ERR_HIP;
-    const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
-    HIP_TRY(launch_group(at<Control>(h, SL.ctrl), at<uint32_t>(h, SL.keys1),
-                         at<uint32_t>(h, SL.vals1), m, h->cfg.num_nodes, at<uint32_t>(h, SL.hist),
-                         at<uint32_t>(h, SL.bstart), at<int32_t>(h, SL.info),
-                         at<uint4>(h, SL.shorts), at<uint4>(h, SL.pieces), at<uint4>(h, SL.combs),
-                         caps, at<uint32_t>(h, SL.wstats), 1 << h->plan.bits, h->key_bits,
-                         beside ? h->beside_grid : 0, h->group_bits, s));
-    if (!prof_mark(h, b, 5, s)) return HUGE_ERR_HIP;
-    HIP_TRY(hipEventRecord(h->ready[slot], s));
-    b.stage = 2;
-    b.stage_stream = s;
-    return HUGE_OK;
-}
-
-// The oldest prepared batch: its missing stages and the next batch's radix
-// pass on s, the next batch's grouping on its own stream, then the apply
-// (launches only).
+// The apply of the oldest prepared batch on s (launches only).
 huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s) {
     const int slot = (int)(h->applied % kSlots);
     PendingBatch& b = h->pending[slot];
-    if (b.stage == 0) HIP_TRY_ST(stage_radix(h, slot, s));
-    if (b.stage == 1) HIP_TRY_ST(stage_group(h, slot, s, false));
-    if (h->prepared > h->applied + 1) {
-        const int nslot = (int)((h->applied + 1) % kSlots);
-        PendingBatch& nb = h->pending[nslot];
-        if (nb.stage == 0) {
-            HIP_TRY_ST(stage_radix(h, nslot, s));
-            HIP_TRY_ST(stage_group(h, nslot, nb.gstream, true));
-        }
-    }
-
     const SlotLayout& SL = h->lay.slot[slot];
     const Layout& L = h->lay;
     Control* ctl = at<Control>(h, SL.ctrl);
     const TableArgs t = table_args(h);
     StepArgs a{b.src, b.dst, b.cc, b.n, b.first_pos, lr, loss_out};
     a.w = b.w;
-    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-    int32_t* neg = at<int32_t>(h, SL.neg);
     double* lossp = at<double>(h, L.lossp);
 
-    HIP_TRY(wait_on(s, h->ready[slot], b.stage_stream));
+    HIP_TRY(wait_on(s, h->ready[slot], b.gstream));
     // applies write the tables and share the apply regions: one at a time
     if (h->last_applied_slot >= 0)
         HIP_TRY(wait_on(s, h->done[h->last_applied_slot], h->last_apply_stream));
+    // and after the calls outside the step issued since the last apply
+    if (h->side_pending) {
+        HIP_TRY(wait_on(s, h->side_done, h->side_stream));
+        h->side_pending = false;
+    }
     if (!prof_mark(h, b, 6, s)) return HUGE_ERR_HIP;
     int64_t blocks = 0;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-        double* part = at<double>(h, L.part);
-        float* dup = at<float>(h, L.dup);
-        HIP_TRY(launch_fused_step(t, ctl, a, neg, at<int32_t>(h, SL.info), dup, lossp, &blocks,
+        // the negatives are the sort keys of slots 2 .. K + 1
+        const uint32_t stride = 2 + (uint32_t)h->cfg.num_neg_per_pos;
+        HIP_TRY(launch_fused_step(t, ctl, a, at<int32_t>(h, SL.keys0) + 2, stride,
+                                  at<int32_t>(h, SL.info), at<float>(h, L.dup), lossp, &blocks,
                                   s));
         if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
-        if (m > 0) {
-            const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
-            HIP_TRY(launch_dup_apply(t, ctl, at<uint4>(h, SL.shorts), at<uint4>(h, SL.pieces),
-                                     dup, part, lr, caps, s));
-            HIP_TRY(launch_combine(t, ctl, at<uint4>(h, SL.combs), part, lr, caps, s));
-        }
-        if (!prof_mark(h, b, 8, s)) return HUGE_ERR_HIP;
+        FinishArgs f;
+        f.shorts = at<uint4>(h, SL.shorts);
+        f.pieces = at<uint4>(h, SL.pieces);
+        f.combs = at<uint4>(h, SL.combs);
+        f.ccount = at<uint32_t>(h, SL.ccount);
+        f.dup = at<float>(h, L.dup);
+        f.part = at<double>(h, L.part);
+        f.caps = ListCaps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
+        f.lr = lr;
+        f.lossp = lossp;
+        f.loss_blocks = blocks;
+        f.loss_out = loss_out;
+        HIP_TRY(launch_finish(t, ctl, f, s));
     } else {
         float* gsrc = at<float>(h, L.gsrc);
         float* coef = at<float>(h, L.coef);
+        const int32_t* neg = at<int32_t>(h, SL.neg);
         HIP_TRY(launch_atomic_gather(t, ctl, a, neg, gsrc, coef, lossp, &blocks, s));
         if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
         HIP_TRY(launch_atomic_scatter_T(t, ctl, a, neg, coef, s));
         HIP_TRY(launch_atomic_scatter_S(t, ctl, a, gsrc, s));
-        if (!prof_mark(h, b, 8, s)) return HUGE_ERR_HIP;
+        if (loss_out) HIP_TRY(launch_loss_final(ctl, lossp, blocks, loss_out, s));
     }
-    if (loss_out) HIP_TRY(launch_loss_final(ctl, lossp, blocks, loss_out, s));
-    if (!prof_mark(h, b, 9, s)) return HUGE_ERR_HIP;
+    if (!prof_mark(h, b, 8, s) || !prof_mark(h, b, 9, s)) return HUGE_ERR_HIP;
     HIP_TRY(hipEventRecord(h->done[slot], s));
     if (b.prof >= 0) h->prof_applied[(size_t)b.prof] = 1;
     h->slot_apply_stream[slot] = s;
@@ -508,6 +494,8 @@ huge_status huge_attach_tables(const huge_config* cfg, void* d_S, void* d_T,
     return st;
 }
 
+}  // extern "C"
+
 namespace {
 
 huge_status train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
@@ -518,7 +506,7 @@ huge_status train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_ds
     if (!isfinite(lr)) return HUGE_ERR_INVALID_ARG;
     if (h->prepared != h->applied) return HUGE_ERR_INVALID_ARG;  // a prepared batch is pending
     hipStream_t s = static_cast<hipStream_t>(stream);
-    st = stage_sample(h, d_src, d_dst, d_cc, d_w, n, first_pos_index, s);
+    st = stage_prepare(h, d_src, d_dst, d_cc, d_w, n, first_pos_index, s);
     if (st != HUGE_OK) return st;
     return apply_next(h, lr, d_loss_sum, s);
 }
@@ -529,8 +517,8 @@ huge_status prepare_step(huge_handle* h, const int32_t* d_src, const int32_t* d_
     huge_status st = check_batch_args(h, d_src, d_dst, d_cc ? (const void*)d_cc : d_w, n);
     if (st != HUGE_OK) return st;
     if (h->prepared - h->applied >= kMaxPending) return HUGE_ERR_INVALID_ARG;
-    return stage_sample(h, d_src, d_dst, d_cc, d_w, n, first_pos_index,
-                        static_cast<hipStream_t>(stream));
+    return stage_prepare(h, d_src, d_dst, d_cc, d_w, n, first_pos_index,
+                         static_cast<hipStream_t>(stream));
 }
 
 huge_status eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
@@ -542,9 +530,8 @@ huge_status eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst
     hipStream_t s = static_cast<hipStream_t>(stream);
     const Layout& L = h->lay;
     Control* ctl = at<Control>(h, L.eval_ctrl);
-    // the loss partials are shared with applies: order after the last one
-    if (h->last_applied_slot >= 0)
-        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
+    // the loss partials are shared with applies
+    HIP_TRY(side_begin(h, s));
     double* lossp = at<double>(h, L.lossp);
     StepArgs a{d_src, d_dst, d_cc, n, first_pos_index, 0.0f, d_loss_sum};
     a.w = d_w;
@@ -552,10 +539,13 @@ huge_status eval_loss(huge_handle* h, const int32_t* d_src, const int32_t* d_dst
     int64_t blocks = 0;
     HIP_TRY(launch_eval(table_args(h), ctl, a, lossp, &blocks, s));
     HIP_TRY(launch_loss_final(ctl, lossp, blocks, d_loss_sum, s));
+    HIP_TRY(side_end(h, s));
     return HUGE_OK;
 }
 
 }  // namespace
+
+extern "C" {
 
 huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t* d_dst,
                             const int32_t* d_cc, int64_t n, uint64_t first_pos_index, float lr,
@@ -625,8 +615,10 @@ huge_status huge_get_rows(huge_handle* h, int32_t table, const int64_t* d_ids, i
     if (n == 0) return HUGE_OK;
     if (!d_ids || !d_out) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(side_begin(h, s));
     HIP_TRY(launch_get_rows(table_args(h), at<Control>(h, h->lay.eval_ctrl), table, d_ids, n,
                             d_out, s));
+    HIP_TRY(side_end(h, s));
     return HUGE_OK;
 }
 
@@ -636,11 +628,11 @@ huge_status huge_probe_rows(huge_handle* h, const int32_t* d_src, const int32_t*
     if (n == 0) return HUGE_OK;
     if (!d_src || !d_dst) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // the tables are shared with applies: order after the last one
-    if (h->last_applied_slot >= 0)
-        HIP_TRY(hipStreamWaitEvent(s, h->done[h->last_applied_slot], 0));
+    // the probe rewrites table rows: ordered between applies
+    HIP_TRY(side_begin(h, s));
     HIP_TRY(launch_probe(table_args(h), at<Control>(h, h->lay.eval_ctrl), d_src, d_dst, n,
                          first_pos_index, s));
+    HIP_TRY(side_end(h, s));
     return HUGE_OK;
 }
 
@@ -652,9 +644,11 @@ huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_
     hipStream_t s = static_cast<hipStream_t>(stream);
     StepArgs a{nullptr, nullptr, nullptr, n, first_pos_index, 0.0f, nullptr};
     HIP_TRY(launch_sample(table_args(h), at<Control>(h, h->lay.eval_ctrl), a, d_neg_out, nullptr,
-                          nullptr, s));
+                          s));
     return HUGE_OK;
 }
+
+}  // extern "C"
 
 namespace {
 
@@ -678,6 +672,8 @@ bool walk_config_ok(const huge_walk_config* c) {
 }
 
 }  // namespace
+
+extern "C" {
 
 size_t huge_walk_workspace_bytes(const huge_walk_config* cfg, int64_t num_seeds) {
     if (!walk_config_ok(cfg) || num_seeds < 0) return 0;
@@ -725,9 +721,10 @@ huge_status huge_check(huge_handle* h, void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     // every stage issued so far, on any stream
     for (int k = 0; k < kSlots; ++k) {
-        for (hipEvent_t e : {h->sampled[k], h->radixed[k], h->ready[k], h->done[k]})
+        for (hipEvent_t e : {h->ready[k], h->done[k]})
             HIP_TRY(hipStreamWaitEvent(s, e, 0));
     }
+    HIP_TRY(hipStreamWaitEvent(s, h->side_done, 0));
     constexpr int kCtrls = kSlots + 1;
     size_t ctrls[kCtrls];
     for (int k = 0; k < kSlots; ++k) ctrls[k] = h->lay.slot[k].ctrl;
@@ -809,7 +806,7 @@ huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int
     huge_status st = HUGE_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
     for (int k = 0; k < kSlots && st == HUGE_OK; ++k) {
-        for (hipEvent_t e : {h->sampled[k], h->radixed[k], h->ready[k], h->done[k]})
+        for (hipEvent_t e : {h->ready[k], h->done[k]})
             if (hipStreamWaitEvent(s, e, 0) != hipSuccess) st = HUGE_ERR_HIP;
     }
     if (st == HUGE_OK && hipStreamSynchronize(s) != hipSuccess) st = HUGE_ERR_HIP;
@@ -845,6 +842,8 @@ huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int
 // their regions from the start of the caller's workspace (calls on a stream
 // run one after the other).
 // ---------------------------------------------------------------------------
+}  // extern "C"
+
 namespace {
 
 struct SummaryLayout {
@@ -903,6 +902,8 @@ bool eval_graph_ok(int64_t num_nodes, int64_t num_edges) {
 }
 
 }  // namespace
+
+extern "C" {
 
 size_t huge_eval_workspace_bytes(int64_t max_pairs, int64_t num_rows, int32_t dim, int32_t k) {
     if (max_pairs < 0 || max_pairs > 0x7FFFFFFF || !eval_table_ok(num_rows, dim) || k < 1 ||

@@ -15,19 +15,29 @@ constexpr int kMinDigitBits = 8;       // digit widths of the LSD radix sort: 8 
 constexpr int kMaxDigitBits = 10;      // the same in every pass of a sort
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;          // keys < 2^32
-constexpr int kSortThreads = 1024;     // threads of a sort workgroup (16 wave64)
-constexpr int kSortItems = 8;          // keys per thread in a sort tile
-constexpr int kSortTile = kSortThreads * kSortItems;  // 8192 keys per tile
-// Per-bucket grouping (k_group): chunks of kGroupChunk keys, an LDS hash
-// table of 2^bits slots (bits 12..14, from the mean bucket size); a bucket
-// range with more than 3/4 of the slots in distinct keys is split by further
-// hash bits.  Where a bucket's keys differ in at most kBitmapBits bits, an
-// LDS bitmap of them first marks the keys that occur more than once, and
-// only those enter the table (of 2^12 slots).
-constexpr int kGroupItems = 8;         // keys per thread in a grouping chunk
+constexpr int kSortTile = 8192;        // keys per radix-pass tile
+// Every kernel of the grouping (tile counts, their prefixes, the radix pass,
+// the per-bucket grouping) runs in workgroups of kBlock threads within the
+// HUGE_BESIDE register budget, so that it runs beside the fused step without
+// evicting any of the step's waves.
+constexpr int kScanDigits = 4;         // digits per tile-prefix workgroup
+// Register budget of the kernels that run beside the fused step: at most 64
+// VGPRs (the budget of eight waves per SIMD).  With the fused step at five
+// waves of at most 88 VGPRs per SIMD (440 of 512), one such wave per SIMD
+// fits beside them.
+#define HUGE_BESIDE __attribute__((amdgpu_waves_per_eu(8, 8)))
+// Per-bucket grouping (k_group): chunks of kGroupChunk keys (kGroupItems
+// consecutive keys per thread); an LDS hash table of kGroupSlots slots counts
+// the repeated keys of a key range; a range with more than 3/4 of the slots
+// in distinct keys is split by further hash bits.  Where a bucket's keys
+// differ in at most kBitmapBits bits, an LDS bitmap of them first marks the
+// keys that occur more than once, and only those enter the table.  Buckets of
+// up to kGroupCache keys are kept in LDS after the first pass.
+constexpr int kGroupItems = 8;
 constexpr int kGroupChunk = kBlock * kGroupItems;     // 2048 keys per chunk
-constexpr int kTableBitsMin = 12;      // 4096 slots: 36 KB of LDS per workgroup
-constexpr int kTableBitsMax = 14;      // 16384 slots: 144 KB of LDS per workgroup
+constexpr int kGroupTableBits = 12;
+constexpr int kGroupSlots = 1 << kGroupTableBits;     // 4096 slots, 32 KB
+constexpr int kGroupCache = 8192;                     // 32 KB of keys
 constexpr int kBitmapBits = 18;        // two 32 KB bitmaps (seen, repeated)
 // Embedding evaluation
 constexpr int kEvalMaxQuantiles = 128;  // percentiles per summary
@@ -81,30 +91,33 @@ enum InternalSite : uint32_t {
     kSiteStepIds = 9,
     kSiteAtomicIds = 10,
     kSiteGroupBits = 11,
+    kSiteFinishComb = 12,
 };
 
 // Byte offsets of the workspace regions (all 256-byte aligned).
 //
 // A batch is processed in two halves: grouping (validation, negatives, sort,
 // run marking) and applying (gather, loss, updates).  Grouping never touches
-// the tables, so the grouping of the next batch may run on another stream
-// while the current one is applied: each of the two grouping slots has its
-// own regions; the apply regions are shared (applies are ordered).
+// the tables, so the grouping of later batches may run on another stream
+// while the current one is applied: each grouping slot has its own regions;
+// the apply regions are shared (applies are ordered).
 struct SlotLayout {
     size_t ctrl = 0;     // Control
     size_t hist = 0;     // u32 [kMaxBins] occurrences per bucket (digit)
-    size_t neg = 0;      // i32 [max_batch * K]
+    size_t neg = 0;      // i32 [max_batch * K] (atomic scatter; the sorted one reads keys0)
     // sorted scatter
     size_t keys0 = 0;    // u32 [M] keys in occurrence order
     size_t keys1 = 0;    // u32 [M] keys grouped by their lowest digit
     size_t vals1 = 0;    // u32 [M] their occurrence indices
-    size_t info = 0;     // i32 [M]: -1, or the duplicate-buffer slot of an occurrence of a repeated row
+    size_t info = 0;     // i32 [M]: -1, or the duplicate-buffer slot of an occurrence of a
+                         // repeated row (-1 between batches: the fused step resets it)
     size_t tcount = 0;   // u32 [sort_tiles * kMaxBins] occurrences per tile and digit
     size_t tprefix = 0;  // u32 [sort_tiles * kMaxBins] the same summed over earlier tiles
     size_t bstart = 0;   // u32 [kMaxBins] first position of each bucket
     size_t shorts = 0;   // uint4 [cap_short] {start, len, key, 0}
-    size_t pieces = 0;   // uint4 [cap_piece] {start, len, key, 0 or partial index + 1}
-    size_t combs = 0;    // uint4 [cap_comb] {key, first partial, partials, 0}
+    size_t pieces = 0;   // uint4 [cap_piece] {start, len, key, 0 or combine record index + 1}
+    size_t combs = 0;    // uint4 [cap_comb] {key, first partial, partials, first slot}
+    size_t ccount = 0;   // u32 [cap_comb] pieces of the row summed so far
     size_t wstats = 0;   // u32 [kMaxBins * 3] distinct S, distinct T, repeated occurrences
 };
 
@@ -236,12 +249,15 @@ hipError_t launch_init(const TableArgs& t, float half_width, hipStream_t s);
 hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, const int64_t* ids,
                            int64_t n, float* out, hipStream_t s);
 hipError_t launch_begin(Control* ctl, hipStream_t s);
+// Validation, negatives into neg (if not null) and, with keys, the sort key
+// of every occurrence.
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, int32_t* info, hipStream_t s);
+                         uint32_t* keys, hipStream_t s);
 // Bucketing of m keys by `bits` bits at `shift` in tiles of kSortTile:
 // per-tile digit counts, their sums over earlier tiles and the bucket sizes
 // (hist), then the stable scatter into bucket order (one pass of an LSD
-// radix sort).
+// radix sort); bstart (if not null) receives the first position of each
+// bucket.
 hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits, int shift,
                              uint32_t* tcount, hipStream_t s);
 hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int bits,
@@ -252,20 +268,29 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* ke
                              hipStream_t s);
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
-                        uint4* shorts, uint4* pieces, uint4* combs, ListCaps caps,
-                        uint32_t* wstats, int bins, int key_bits, int grid_cap,
-                        int table_bits, hipStream_t s);
-// Table bits for a grouping of m keys over `bins` buckets: the smallest table
-// whose 3/4 load holds a mean bucket of distinct keys.
-int group_table_bits(int64_t m, int bins);
+                        uint4* shorts, uint4* pieces, uint4* combs, uint32_t* ccount,
+                        ListCaps caps, uint32_t* wstats, int bins, int key_bits, hipStream_t s);
+// Negative k of positive i: neg[i * neg_stride + k].
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
-                             const int32_t* neg, const int32_t* info, float* dup,
+                             const int32_t* neg, uint32_t neg_stride, int32_t* info, float* dup,
                              double* lossp, int64_t* blocks_out, hipStream_t s);
-hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* shorts,
-                            const uint4* pieces, const float* dup, double* part, float lr,
-                            ListCaps caps, hipStream_t s);
-hipError_t launch_combine(const TableArgs& t, Control* ctl, const uint4* combs,
-                          const double* part, float lr, ListCaps caps, hipStream_t s);
+// After the fused step: the repeated rows (short runs, pieces, and rows
+// whose pieces are combined by the last piece to finish) and, with a loss
+// output, the loss sum (the fused step's partials in a fixed order).
+struct FinishArgs {
+    const uint4* shorts;
+    const uint4* pieces;
+    const uint4* combs;
+    uint32_t* ccount;
+    const float* dup;
+    double* part;
+    ListCaps caps;
+    float lr;
+    const double* lossp;   // per-workgroup loss partials of the fused step
+    int64_t loss_blocks;   // how many
+    double* loss_out;      // or null: no loss
+};
+hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_walks(const WalkArgs& A, uint32_t* counts, uint64_t* offsets, int64_t* total,
                         int64_t capacity, int32_t* src, int32_t* dst, int32_t* cc, int32_t* hist,

@@ -53,6 +53,16 @@ inline int neg_block(int K) {
             return hipErrorInvalidValue;     \
     }
 
+// Whether the negatives form one block of the block size (K == NB): F_.
+#define HUGE_FULL_DISPATCH(full, ...)      \
+    if (full) {                            \
+        constexpr bool F_ = true;          \
+        __VA_ARGS__;                       \
+    } else {                               \
+        constexpr bool F_ = false;         \
+        __VA_ARGS__;                       \
+    }
+
 // Element type of the tables: E_ is float or bf16_t.
 #define HUGE_ELEM_DISPATCH(dtype, ...)      \
     if ((dtype) == kDtypeBf16) {            \

@@ -6,8 +6,8 @@
 // group that read them -- no other group reads them.  A row that occurs
 // several times is left untouched here: each occurrence stores its
 // contribution in the slot the grouping gave it (a row's slots are
-// consecutive, in occurrence order), and the duplicate kernels sum them in
-// that order and update the row once, so every read sees pre-step values.
+// consecutive, in occurrence order), and the finish kernel sums them in that
+// order and updates the row once, so every read sees pre-step values.
 #include "common.hpp"
 #include "device.hpp"
 #include "dispatch.hpp"
@@ -37,10 +37,18 @@ __device__ __forceinline__ void block_loss(float loss, double* __restrict__ out)
 // ownership over the float contributions of repeated rows.  The context rows
 // stay packed in registers (bf16: half the registers) and are widened where
 // used; the source row and the source gradient are held widened.
-template <int G, int NB, typename IO, typename DIO>
+// FULL: K == NB, the negatives are one block of compile-time size.
+// Negative k of positive i is neg[i * neg_stride + k] (the sort keys in
+// occurrence order, whose slots 2.. are the negatives' row ids).  info[o] is
+// -1 for a row occurring once, else the occurrence's duplicate-buffer slot;
+// the kernel sets every entry it finds >= 0 back to -1 once it has read it,
+// so that the array is all -1 again for the next batch in this slot (the
+// grouping writes only the repeated occurrences).
+template <int G, int NB, bool FULL, typename IO, typename DIO>
 __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __restrict__ ctl,
                                                        StepArgs a, const int32_t* __restrict__ neg,
-                                                       const int32_t* __restrict__ info,
+                                                       uint32_t neg_stride,
+                                                       int32_t* __restrict__ info,
                                                        float* __restrict__ dup,
                                                        double* __restrict__ lossp) {
     using E = typename IO::Elem;
@@ -48,12 +56,24 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     constexpr int C = IO::C;
     constexpr int R = IO::R;
     static_assert(DIO::C == C, "the contribution layout must match the row layout");
-    if (ctl->step_bad) return;
+    // At least 88 VGPRs: five waves per SIMD (440 of 512 registers), not six,
+    // so that one wave of a grouping kernel of the next batch (at most 64
+    // VGPRs) fits beside them on every SIMD.  The empty statement marks v87
+    // as used; it generates no instruction.
+    asm volatile("" ::: "v87");
     constexpr int PPB = kBlock / G;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
     const int64_t i = (int64_t)blockIdx.x * PPB + grp;
-    const int K = t.K;
+    const int K = FULL ? NB : t.K;
+    if (ctl->step_bad) {  // a no-op step: only the slots the grouping may have set
+        if (i < a.n && lane == 0) {
+            const uint32_t o = (uint32_t)i * (uint32_t)(2 + K);
+            for (int q = 0; q < 2 + K; ++q)
+                if (info[o + q] >= 0) info[o + q] = -1;
+        }
+        return;
+    }
     const int32_t D = t.D;
     const float lr = a.lr;
     E* __restrict__ S = static_cast<E*>(t.S);
@@ -64,26 +84,36 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     // the loads overlap; ids were validated when the batch was grouped and
     // are checked again so that a batch changed before its apply is reported
     // instead of read out of bounds.
+    // Batch indices fit in 32 bits (the configuration bounds max_batch (2 + K)
+    // below 2^31), so the batch arrays are addressed as a base plus a 32-bit
+    // offset.
     bool active = i < a.n;
     int32_t u = 0, v = 0, info_s = -1, info_d = -1;
     float c_i = 0.f;
     int32_t mk[NB], ik[NB];
-    const int64_t o = i * (int64_t)(2 + K);
-    const int32_t* negi = neg + i * (int64_t)K;
-    const int32_t* infok = info + o + 2;
+    const uint32_t i32 = (uint32_t)i;
+    const uint32_t o = i32 * (uint32_t)(2 + K);
+    const uint32_t nbase = i32 * neg_stride;
     int cnt = K < NB ? K : NB;
     if (active) {
-        u = a.src[i];
-        v = a.dst[i];
-        c_i = positive_weight(a, i);
+        u = a.src[i32];
+        v = a.dst[i32];
+        c_i = positive_weight(a, i32);
         info_s = info[o];
         info_d = info[o + 1];
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             if (j < cnt) {
-                mk[j] = negi[j];
-                ik[j] = infok[j];
+                mk[j] = neg[nbase + j];
+                ik[j] = info[o + 2 + j];
             }
+        }
+        if (lane == 0) {
+            if (info_s >= 0) info[o] = -1;
+            if (info_d >= 0) info[o + 1] = -1;
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+                if (j < cnt && ik[j] >= 0) info[o + 2 + j] = -1;
         }
         if (u < 0 || (int64_t)u >= t.N || v < 0 || (int64_t)v >= t.N) {
             if (lane == 0) raise_internal(ctl, kSiteStepIds);
@@ -160,9 +190,14 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
 #pragma unroll
             for (int j = 0; j < NB; ++j) {
                 if (j < cnt) {
-                    mk[j] = negi[kb + j];
-                    ik[j] = infok[kb + j];
+                    mk[j] = neg[nbase + (uint32_t)(kb + j)];
+                    ik[j] = info[o + 2 + (uint32_t)(kb + j)];
                 }
+            }
+            if (lane == 0) {
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+                    if (j < cnt && ik[j] >= 0) info[o + 2 + (uint32_t)(kb + j)] = -1;
             }
 #pragma unroll
             for (int j = 0; j < NB; ++j)
@@ -194,7 +229,7 @@ static int64_t fused_step_blocks(const TableArgs& t, int64_t n) {
 }
 
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
-                             const int32_t* neg, const int32_t* info, float* dup,
+                             const int32_t* neg, uint32_t neg_stride, int32_t* info, float* dup,
                              double* lossp, int64_t* blocks_out, hipStream_t s) {
     const int64_t blocks = fused_step_blocks(t, a.n);
     *blocks_out = blocks;
@@ -202,19 +237,24 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
     if (uses_pairs(t.dtype, t.D)) {
         HUGE_PAIR_DISPATCH(pair_shape(t.D), {
             HUGE_NEG_DISPATCH(neg_block(t.K), {
-                hipLaunchKernelGGL(
-                    (k_fused_step<G_, NB_, PairIO<G_, U_, bf16_t>, PairIO<G_, U_, float>>),
-                    dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, info, dup, lossp);
+                HUGE_FULL_DISPATCH(t.K == NB_, {
+                    hipLaunchKernelGGL(
+                        (k_fused_step<G_, NB_, F_, PairIO<G_, U_, bf16_t>, PairIO<G_, U_, float>>),
+                        dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, neg_stride,
+                        info, dup, lossp);
+                });
             });
         });
     } else {
         HUGE_ROW_DISPATCH(row_shape(t.D), {
             HUGE_NEG_DISPATCH(neg_block(t.K), {
                 HUGE_ELEM_DISPATCH(t.dtype, {
-                    hipLaunchKernelGGL(
-                        (k_fused_step<G_, NB_, RowIO<G_, C_, E_>, RowIO<G_, C_>>),
-                        dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, info, dup,
-                        lossp);
+                    HUGE_FULL_DISPATCH(t.K == NB_, {
+                        hipLaunchKernelGGL(
+                            (k_fused_step<G_, NB_, F_, RowIO<G_, C_, E_>, RowIO<G_, C_>>),
+                            dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg,
+                            neg_stride, info, dup, lossp);
+                    });
                 });
             });
         });
@@ -474,87 +514,115 @@ __device__ __forceinline__ void coop_sum(double4_ (&acc)[C], const Row* __restri
     __syncthreads();
 }
 
-// Repeated rows.  Short runs ({start, len <= kShortRun, key}): one group each
-// sums its contributions in occurrence order and updates the row.  Pieces
-// ({start, len <= kPiece, key, part}): the whole workgroup sums them; a whole
-// run (part = 0) updates its row, a piece of a longer run stores its sum as
-// partial part - 1.  The record counts were set by the grouping of this batch.
+// Fixed-order sum of one double per thread over the workgroup (a tree in
+// LDS); every thread receives the sum.  Synchronises.
+__device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
+    s_red[threadIdx.x] = v;
+    __syncthreads();
+#pragma unroll
+    for (int w = kBlock / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) s_red[threadIdx.x] += s_red[threadIdx.x + w];
+        __syncthreads();
+    }
+    const double r = s_red[0];
+    __syncthreads();
+    return r;
+}
+
+// After the fused step, in one launch:
+//   loss:   workgroup 0 sums the fused step's per-workgroup partials in a
+//           fixed order (no cross-workgroup step: a device-scope fence per
+//           workgroup, to pass partial sums between them, measured slower);
+//   short runs ({start, len <= kShortRun, key}): one thread group each sums
+//           its contributions in occurrence order and updates the row;
+//   pieces ({start, len <= kPiece, key, comb}): the whole workgroup sums
+//           them; a whole run (comb = 0) updates its row; a piece of a
+//           longer run stores its sum as partial z of its combine record
+//           {key, first partial, partials, first slot}, and the workgroup
+//           that stores the record's last partial (an arrival counter after
+//           a device-scope fence) adds the partials in piece order and
+//           updates the row once.
+// The record counts were set by the grouping of this batch.
 template <int G, int C, typename E>
-__global__ __launch_bounds__(kBlock) void k_dup_apply(TableArgs t, const Control* __restrict__ ctl,
-                                                      const uint4* __restrict__ shorts,
-                                                      const uint4* __restrict__ pieces,
-                                                      const float* __restrict__ dup,
-                                                      double* __restrict__ part, float lr,
-                                                      ListCaps caps) {
+__global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restrict__ ctl,
+                                                   FinishArgs f) {
     constexpr int PPB = kBlock / G;
     __shared__ double s_part[1024 * C];  // PPB x D doubles: D <= 4 G C
-    if (ctl->step_bad) return;
+    __shared__ double s_red[kBlock];
+    __shared__ uint32_t s_flag;
+    if (ctl->step_bad) {
+        if (blockIdx.x == 0 && threadIdx.x == 0 && f.loss_out != nullptr)
+            *f.loss_out = __builtin_nan("");
+        return;
+    }
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
     const int32_t D = t.D;
+
+    if (blockIdx.x == 0 && f.loss_out != nullptr) {
+        // thread t adds partials t, t + kBlock, ... in that order, then the
+        // threads' sums meet in a fixed tree: the same double on every run;
+        // the loads are issued sixteen at a time
+        double acc = 0.0;
+        int64_t j = threadIdx.x;
+        for (; j + 15 * kBlock < f.loss_blocks; j += 16 * kBlock) {
+            double v[16];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) v[q] = f.lossp[j + q * kBlock];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc += v[q];
+        }
+        for (; j < f.loss_blocks; j += kBlock) acc += f.lossp[j];
+        acc = block_sum_fixed(acc, s_red);
+        if (threadIdx.x == 0) *f.loss_out = acc;
+    }
+
     // the grouping never lists more than the capacities (it flags the call
     // instead); the bounds only keep a broken invariant inside the lists
-    const uint32_t ns = ctl->n_short < caps.shorts ? ctl->n_short : caps.shorts;
-    const uint32_t np = ctl->n_piece < caps.pieces ? ctl->n_piece : caps.pieces;
+    const uint32_t ns = ctl->n_short < f.caps.shorts ? ctl->n_short : f.caps.shorts;
+    const uint32_t np = ctl->n_piece < f.caps.pieces ? ctl->n_piece : f.caps.pieces;
     for (uint32_t r = blockIdx.x * PPB + grp; r < ns; r += gridDim.x * PPB) {
-        const uint4 rec = shorts[r];
+        const uint4 rec = f.shorts[r];
         double4_ acc[C];
-        sum_rows<G, C>(acc, dup, rec.x, rec.y, D, lane);
-        apply_row<G, C, E>(t, rec.z, acc, lr, lane);
+        sum_rows<G, C>(acc, f.dup, rec.x, rec.y, D, lane);
+        apply_row<G, C, E>(t, rec.z, acc, f.lr, lane);
     }
     for (uint32_t r = blockIdx.x; r < np; r += gridDim.x) {
-        const uint4 rec = pieces[r];  // the same for every thread
+        const uint4 rec = f.pieces[r];  // the same for every thread
         double4_ acc[C];
-        coop_sum<G, C>(acc, dup, rec.x, rec.y, D, grp, lane, s_part);
-        if (grp == 0) {
-            if (rec.w == 0u)
-                apply_row<G, C, E>(t, rec.z, acc, lr, lane);
-            else
-                PartIO<G, C>::store(part, (int64_t)rec.w - 1, D, lane, acc);
+        coop_sum<G, C>(acc, f.dup, rec.x, rec.y, D, grp, lane, s_part);
+        if (rec.w == 0u) {
+            if (grp == 0) apply_row<G, C, E>(t, rec.z, acc, f.lr, lane);
+            continue;
+        }
+        const uint32_t ci = rec.w - 1u;
+        const uint4 cb = ci < f.caps.combs ? f.combs[ci] : make_uint4(0u, 0u, 0u, 0u);
+        const uint32_t z = (rec.x - cb.w) / kPiece;
+        if (ci >= f.caps.combs || z >= cb.z || (uint64_t)cb.y + cb.z > f.caps.parts) {
+            if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
+            continue;  // uniform
+        }
+        if (grp == 0) PartIO<G, C>::store(f.part, (int64_t)cb.y + z, D, lane, acc);
+        __threadfence();
+        __syncthreads();
+        if (threadIdx.x == 0) s_flag = atomicAdd(&f.ccount[ci], 1u) == cb.z - 1u ? 1u : 0u;
+        __syncthreads();
+        if (s_flag) {  // uniform: the last piece of the row
+            __threadfence();
+            coop_sum<G, C>(acc, static_cast<const double*>(f.part), cb.y, cb.z, D, grp, lane,
+                           s_part);
+            if (grp == 0) apply_row<G, C, E>(t, cb.x, acc, f.lr, lane);
         }
     }
 }
 
-// Runs longer than kPiece ({key, first partial, partials}): the partial sums
-// of their pieces, added in piece order, update the row once.
-template <int G, int C, typename E>
-__global__ __launch_bounds__(kBlock) void k_combine(TableArgs t, const Control* __restrict__ ctl,
-                                                    const uint4* __restrict__ combs,
-                                                    const double* __restrict__ part, float lr,
-                                                    ListCaps caps) {
-    __shared__ double s_part[1024 * C];
-    if (ctl->step_bad) return;
-    const int grp = threadIdx.x / G;
-    const int lane = threadIdx.x % G;
-    const uint32_t nc = ctl->n_comb < caps.combs ? ctl->n_comb : caps.combs;
-    for (uint32_t r = blockIdx.x; r < nc; r += gridDim.x) {
-        const uint4 rec = combs[r];
-        double4_ acc[C];
-        coop_sum<G, C>(acc, part, rec.y, rec.z, t.D, grp, lane, s_part);
-        if (grp == 0) apply_row<G, C, E>(t, rec.x, acc, lr, lane);
-    }
-}
-
-hipError_t launch_dup_apply(const TableArgs& t, Control* ctl, const uint4* shorts,
-                            const uint4* pieces, const float* dup, double* part, float lr,
-                            ListCaps caps, hipStream_t s) {
+hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipStream_t s) {
     const RowShape rs = row_shape(t.D);
+    const int64_t grid = 1024;
     HUGE_ROW_DISPATCH(rs, {
         HUGE_ELEM_DISPATCH(t.dtype, {
-            hipLaunchKernelGGL((k_dup_apply<G_, C_, E_>), dim3(1024), dim3(kBlock), 0, s, t, ctl,
-                               shorts, pieces, dup, part, lr, caps);
-        });
-    });
-    return hipGetLastError();
-}
-
-hipError_t launch_combine(const TableArgs& t, Control* ctl, const uint4* combs,
-                          const double* part, float lr, ListCaps caps, hipStream_t s) {
-    const RowShape rs = row_shape(t.D);
-    HUGE_ROW_DISPATCH(rs, {
-        HUGE_ELEM_DISPATCH(t.dtype, {
-            hipLaunchKernelGGL((k_combine<G_, C_, E_>), dim3(256), dim3(kBlock), 0, s, t, ctl,
-                               combs, part, lr, caps);
+            hipLaunchKernelGGL((k_finish<G_, C_, E_>), dim3((unsigned)grid), dim3(kBlock), 0, s, t,
+                               ctl, f);
         });
     });
     return hipGetLastError();

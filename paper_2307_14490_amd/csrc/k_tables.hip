@@ -92,7 +92,7 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 // lists (a kernel rather than a memset so that the sequence stays valid
 // inside a captured graph).
 // ---------------------------------------------------------------------------
-__global__ void k_begin(Control* ctl) {
+__global__ HUGE_BESIDE void k_begin(Control* ctl) {
     if (threadIdx.x == 0) {
         ctl->step_bad = 0u;
         ctl->n_short = ctl->n_piece = ctl->n_comb = ctl->n_part = 0u;
@@ -125,26 +125,21 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s) {
 // o = i S + slot: slot 0 the source row (key N + src), slot 1 the destination
 // row (key dst), slot 2 + k negative k (key m).
 //   - one thread per positive checks 0 <= src, dst < N and co_count >= 0 (a
-//     failure flags the call) and, with keys, handles slots 0 and 1;
+//     failure flags the call) and, with keys, writes keys of slots 0 and 1;
 //   - one thread per negative, consecutive threads on consecutive (i, k), so
 //     that the stores of a wave are contiguous, draws negative k of positive
-//     i into neg[i K + k] and, with keys, handles slot 2 + k.
-// Handling a slot with keys (keys != nullptr): write keys[o] and set
-// info[o] = -1 (the grouping overwrites repeated ones).  Without src only
-// negatives are drawn.
+//     i into neg[i K + k] (if neg is not null) and, with keys, keys[o] of
+//     slot 2 + k.
+// Without src only negatives are drawn.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, StepArgs a,
-                                                   int32_t* __restrict__ neg,
-                                                   uint32_t* __restrict__ keys,
-                                                   int32_t* __restrict__ info) {
+__global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_sample(TableArgs t, Control* ctl,
+                                                               StepArgs a,
+                                                               int32_t* __restrict__ neg,
+                                                               uint32_t* __restrict__ keys) {
     const bool with_keys = keys != nullptr;
     const int64_t K = t.K, S = 2 + K;
     const int64_t i0 = (int64_t)blockIdx.x * kSamplePos;
     const int64_t np = a.n - i0 < kSamplePos ? a.n - i0 : kSamplePos;  // positives here
-    auto put = [&](int64_t o, uint32_t key) {
-        keys[o] = key;
-        info[o] = -1;
-    };
     if (a.src != nullptr) {
         for (int64_t j = threadIdx.x; j < np; j += kBlock) {
             const int64_t i = i0 + j;
@@ -156,8 +151,8 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
             }
             if (!weight_valid(a, i)) raise_error(ctl, kBadCount);
             if (with_keys) {
-                put(i * S, (uint32_t)((uint64_t)t.N + (uint64_t)u));
-                put(i * S + 1, (uint32_t)v);
+                keys[i * S] = (uint32_t)((uint64_t)t.N + (uint64_t)u);
+                keys[i * S + 1] = (uint32_t)v;
             }
         }
     }
@@ -171,8 +166,8 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
         const int64_t i = i0 + q;
         const int32_t m = draw_negative(t.seed, a.first_pos + (uint64_t)i, k, (uint64_t)t.N,
                                         t.thr, t.alias);
-        neg[i * K + k] = m;
-        if (with_keys) put(i * S + 2 + k, (uint32_t)m);
+        if (neg != nullptr) neg[i * K + k] = m;
+        if (with_keys) keys[i * S + 2 + k] = (uint32_t)m;
         k += dr;
         q += dq;
         if (k >= Ku) {
@@ -183,12 +178,11 @@ __global__ __launch_bounds__(kBlock) void k_sample(TableArgs t, Control* ctl, St
 }
 
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, int32_t* info, hipStream_t s) {
+                         uint32_t* keys, hipStream_t s) {
     const int64_t blocks = (a.n + kSamplePos - 1) / kSamplePos;
     if (blocks == 0) return hipSuccess;
     if (t.K < 1 || t.K > kBlock) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
-                       info);
+    hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys);
     return hipGetLastError();
 }
 

@@ -30,6 +30,74 @@ def test_library_exports_every_declared_symbol():
     assert sorted(B.EXPORTED) == names
 
 
+def test_library_exports_only_declared_symbols():
+    """The dynamic symbol table of libhuge.so holds exactly the functions of
+    include/huge.h: no helper, kernel stub or template instantiation that
+    another library in the process could collide with."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm is not installed")
+    out = subprocess.run([nm, "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = sorted(line.split()[-1] for line in out.splitlines() if line.strip())
+    assert exported == _declared()
+
+
+def _bad_tables():
+    import torch
+    N, D = 64, 8
+    f32 = torch.float32
+    good = torch.zeros((N, D), dtype=f32)
+    yield "shape", (torch.zeros((N - 1, D), dtype=f32), good)
+    yield "shape", (good, torch.zeros((N, D + 4), dtype=f32))
+    yield "dtype", (torch.zeros((N, D), dtype=torch.float64), good)
+    yield "dtype", (good, torch.zeros((N, D), dtype=torch.bfloat16))
+    yield "contiguous", (torch.zeros((D, N), dtype=f32).t(), good)
+    yield "on cpu", (good, good)
+    yield "pair", (good,)
+
+
+@pytest.mark.parametrize("case", list(range(7)))
+def test_trainer_rejects_bad_tables_before_any_launch(case):
+    """Caller tables are checked for shape, dtype, contiguity and device
+    before any pointer reaches the library: every step writes rows at offsets
+    computed from (num_nodes, dim)."""
+    what, tables = list(_bad_tables())[case]
+    with pytest.raises((ValueError, TypeError)):
+        B.Trainer(64, 8, 2, 16, tables=tables, device="cuda:0")
+
+
+def test_evaluator_rejects_mismatched_lengths():
+    """Lengths the kernels index by are checked on the host (no GPU: the
+    checks run before any device allocation or launch)."""
+    import torch
+    ev = B.Evaluator.__new__(B.Evaluator)  # no workspace: the checks come first
+    ev.device = "cpu"
+    ev.k = 10
+    off = torch.zeros(11, dtype=torch.int64)
+    nbr = torch.zeros(5, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        ev.pairs(off, nbr, 12, 0, 4, 4)           # offsets must be num_nodes + 1
+    with pytest.raises(ValueError):
+        ev.recall(off, nbr, 12, torch.zeros(3, dtype=torch.int32),
+                  torch.zeros((3, 2), dtype=torch.int32))
+    with pytest.raises(ValueError):
+        ev.recall(off, nbr, 10, torch.zeros(3, dtype=torch.int32),
+                  torch.zeros((4, 2), dtype=torch.int32))  # one id row per query
+    tab = torch.zeros((10, 8), dtype=torch.float32)
+    with pytest.raises(ValueError):
+        ev.distances(tab, torch.zeros(3, dtype=torch.int32), torch.zeros(4, dtype=torch.int32))
+    with pytest.raises(ValueError):
+        ev.distances(tab.view(-1), torch.zeros(3, dtype=torch.int32),
+                     torch.zeros(3, dtype=torch.int32))
+    with pytest.raises(ValueError):
+        ev.summary(torch.zeros(5, dtype=torch.float32), 3, 3)  # 6 pairs, 5 distances
+    with pytest.raises(ValueError):
+        ev.knn(tab.view(-1), torch.zeros(2, dtype=torch.int32), 1)
+
+
 def test_status_strings_cover_every_code():
     seen = set()
     for code in (0, -1, -2, -3, -4, -5):
