@@ -158,6 +158,7 @@ Layout make_layout(const huge_config* c) {
             S.pieces = take(sizeof(uint4) * (size_t)caps.pieces);
             S.combs = take(sizeof(uint4) * (size_t)caps.combs);
             S.ccount = take(sizeof(uint32_t) * (size_t)caps.combs);
+            S.bcount = take(sizeof(uint4) * kMaxBins);
             S.wstats = take(sizeof(uint32_t) * kMaxBins * 3);
         }
     }
@@ -377,8 +378,8 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
                              h->cfg.num_nodes, hist, at<uint32_t>(h, SL.bstart),
                              at<int32_t>(h, SL.info), at<uint4>(h, SL.shorts),
                              at<uint4>(h, SL.pieces), at<uint4>(h, SL.combs),
-                             at<uint32_t>(h, SL.ccount), caps, at<uint32_t>(h, SL.wstats),
-                             1 << bits, h->key_bits, s));
+                             at<uint32_t>(h, SL.ccount), at<uint4>(h, SL.bcount), caps,
+                             at<uint32_t>(h, SL.wstats), 1 << bits, h->key_bits, s));
         if (!prof_mark(h, b, 5, s)) return HUGE_ERR_HIP;
     } else {
         // the atomic scatter needs no grouping
@@ -402,6 +403,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
     StepArgs a{b.src, b.dst, b.cc, b.n, b.first_pos, lr, loss_out};
     a.w = b.w;
     double* lossp = at<double>(h, L.lossp);
+    const int64_t m = b.n * (2 + (int64_t)h->cfg.num_neg_per_pos);
 
     HIP_TRY(wait_on(s, h->ready[slot], b.gstream));
     // applies write the tables and share the apply regions: one at a time
@@ -422,6 +424,12 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
                                   s));
         if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
         FinishArgs f;
+        f.bstart = at<uint32_t>(h, SL.bstart);
+        f.bcount = at<uint4>(h, SL.bcount);
+        // an empty batch is not grouped: its slot's bucket counts are not
+        // this batch's, so no bucket is read
+        f.bins = m > 0 ? 1 << h->plan.bits : 0;
+        f.m = m;
         f.shorts = at<uint4>(h, SL.shorts);
         f.pieces = at<uint4>(h, SL.pieces);
         f.combs = at<uint4>(h, SL.combs);

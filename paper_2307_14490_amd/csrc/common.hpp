@@ -23,21 +23,26 @@ constexpr int kSortTile = 8192;        // keys per radix-pass tile
 constexpr int kScanDigits = 4;         // digits per tile-prefix workgroup
 // Register budget of the kernels that run beside the fused step: at most 64
 // VGPRs (the budget of eight waves per SIMD).  With the fused step at five
-// waves of at most 88 VGPRs per SIMD (440 of 512), one such wave per SIMD
-// fits beside them.
+// waves of 88 VGPRs per SIMD (440 of 512), one such wave per SIMD fits beside
+// them.
 #define HUGE_BESIDE __attribute__((amdgpu_waves_per_eu(8, 8)))
+// The same at 72 VGPRs (seven waves per SIMD), the most that fits beside the
+// fused step's five waves, for the per-bucket grouping, which needs them.
+#define HUGE_BESIDE_72 __attribute__((amdgpu_waves_per_eu(7, 7)))
 // Per-bucket grouping (k_group): chunks of kGroupChunk keys (kGroupItems
 // consecutive keys per thread); an LDS hash table of kGroupSlots slots counts
 // the repeated keys of a key range; a range with more than 3/4 of the slots
 // in distinct keys is split by further hash bits.  Where a bucket's keys
 // differ in at most kBitmapBits bits, an LDS bitmap of them first marks the
-// keys that occur more than once, and only those enter the table.  Buckets of
-// up to kGroupCache keys are kept in LDS after the first pass.
-constexpr int kGroupItems = 8;
-constexpr int kGroupChunk = kBlock * kGroupItems;     // 2048 keys per chunk
+// keys that occur more than once, and only those enter the table.  The first
+// pass copies up to kGroupCacheKeys keys and kGroupCacheVals occurrence
+// indices of a bucket to LDS; later passes read them there.
+constexpr int kGroupItems = 4;
+constexpr int kGroupChunk = kBlock * kGroupItems;     // 1024 keys per chunk
 constexpr int kGroupTableBits = 12;
 constexpr int kGroupSlots = 1 << kGroupTableBits;     // 4096 slots, 32 KB
-constexpr int kGroupCache = 8192;                     // 32 KB of keys
+constexpr int kGroupCacheKeys = 8192;                 // 32 KB
+constexpr int kGroupCacheVals = 4096;                 // 16 KB
 constexpr int kBitmapBits = 18;        // two 32 KB bitmaps (seen, repeated)
 // Embedding evaluation
 constexpr int kEvalMaxQuantiles = 128;  // percentiles per summary
@@ -72,12 +77,8 @@ constexpr uint32_t kBadInternal = 4u;  // a bounded wait expired or an index che
 struct Control {
     uint32_t step_bad;               // this call's input is invalid: skip all writes
     uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
-    uint32_t n_short;                // repeated rows summed by one thread group
-    uint32_t n_piece;                // pieces of up to kPiece occurrences summed by a workgroup
-    uint32_t n_comb;                 // rows whose pieces' partial sums are combined
-    uint32_t n_part;                 // partial sums allocated
     uint32_t site;                   // first failed internal check (a kSite* code)
-    uint32_t pad[9];
+    uint32_t pad[13];
 };
 
 // Internal checks (kBadInternal), recorded in Control::site.
@@ -114,10 +115,14 @@ struct SlotLayout {
     size_t tcount = 0;   // u32 [sort_tiles * kMaxBins] occurrences per tile and digit
     size_t tprefix = 0;  // u32 [sort_tiles * kMaxBins] the same summed over earlier tiles
     size_t bstart = 0;   // u32 [kMaxBins] first position of each bucket
+    // repeated-row records; bucket b (first position s0, n items) writes its
+    // records at [s0 / 2, ...), [s0 / 16, ...), [s0 / 256, ...) of these
+    // (ListCaps says why they fit) and their counts to bcount[b]
     size_t shorts = 0;   // uint4 [cap_short] {start, len, key, 0}
     size_t pieces = 0;   // uint4 [cap_piece] {start, len, key, 0 or combine record index + 1}
     size_t combs = 0;    // uint4 [cap_comb] {key, first partial, partials, first slot}
     size_t ccount = 0;   // u32 [cap_comb] pieces of the row summed so far
+    size_t bcount = 0;   // uint4 [kMaxBins] {short runs, pieces, combines, 0} per bucket
     size_t wstats = 0;   // u32 [kMaxBins * 3] distinct S, distinct T, repeated occurrences
 };
 
@@ -140,17 +145,23 @@ struct Layout {
     uint32_t cap_short = 0, cap_piece = 0, cap_comb = 0, cap_part = 0;
 };
 
-// List capacities for M occurrences.  A repeated row has >= 2 occurrences; a
-// piece is either a whole run of kShortRun+1 .. kPiece occurrences or one of
-// the ceil(len / kPiece) pieces of a longer run (fewer than len / (kPiece/2)
-// of them); a combined row has more than kPiece occurrences.
+// Record regions for M occurrences.  Bucket b holds n_b items from position
+// s0_b; it writes at most floor(n_b / 2) short runs (a repeated row has >= 2
+// occurrences), floor(n_b / 16) pieces (a piece is a whole run of
+// kShortRun+1 .. kPiece occurrences, or one of the ceil(c / kPiece) <= c / 16
+// pieces of a run of c > kPiece), floor(n_b / 256) combine records (a
+// combined row has more than kPiece occurrences) and floor(n_b / 128) partial
+// sums (ceil(c / kPiece) <= c / 128 of them per combined row); since
+// floor(x + y) >= floor(x) + floor(y), the region of bucket b starting at
+// floor(s0_b / q) ends before that of bucket b + 1.
+constexpr uint32_t kShortDiv = 2, kPieceDiv = 16, kCombDiv = 256, kPartDiv = 128;
 struct ListCaps {
     uint32_t shorts, pieces, combs, parts;
 };
 
 inline ListCaps list_caps(int64_t M) {
-    return {(uint32_t)(M / 2 + 2), (uint32_t)(M / (kShortRun + 1) + M / (kPiece / 2) + 2),
-            (uint32_t)(M / kPiece + 2), (uint32_t)(M / (kPiece / 2) + 2)};
+    return {(uint32_t)(M / kShortDiv + 1), (uint32_t)(M / kPieceDiv + 1),
+            (uint32_t)(M / kCombDiv + 1), (uint32_t)(M / kPartDiv + 1)};
 }
 
 // Bucketing of keys below 2^key_bits: one radix pass on the lowest digit, as
@@ -269,7 +280,8 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* ke
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
                         uint4* shorts, uint4* pieces, uint4* combs, uint32_t* ccount,
-                        ListCaps caps, uint32_t* wstats, int bins, int key_bits, hipStream_t s);
+                        uint4* bcount, ListCaps caps, uint32_t* wstats, int bins, int key_bits,
+                        hipStream_t s);
 // Negative k of positive i: neg[i * neg_stride + k].
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, uint32_t neg_stride, int32_t* info, float* dup,
@@ -278,6 +290,10 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 // whose pieces are combined by the last piece to finish) and, with a loss
 // output, the loss sum (the fused step's partials in a fixed order).
 struct FinishArgs {
+    const uint32_t* bstart;  // first position of each bucket
+    const uint4* bcount;     // records per bucket
+    int bins;                // buckets of the batch (0: no records)
+    int64_t m;               // occurrences of the batch
     const uint4* shorts;
     const uint4* pieces;
     const uint4* combs;

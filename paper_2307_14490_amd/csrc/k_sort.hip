@@ -340,13 +340,13 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* ke
 // ---------------------------------------------------------------------------
 // Grouping of one bucket (its items are in occurrence order).
 //
+// A first pass copies the bucket's keys (up to kGroupCacheKeys) and
+// occurrence indices (up to kGroupCacheVals) to LDS, in one round of loads.
 // With BM (the bucket's keys differ in at most kBitmapBits bits above the
-// bucket digit), a first pass sets, per item, the key's bit in an LDS bitmap
+// bucket digit) the same pass sets, per item, the key's bit in an LDS bitmap
 // and, where it was set already, the key's bit in a second bitmap of
 // repeated keys; it also counts the bucket's distinct source and destination
-// rows.  Only keys marked repeated take part in what follows.  A bucket of at
-// most kGroupCache items is copied to LDS by that pass and read from there
-// afterwards.
+// rows.  Only keys marked repeated take part in what follows.
 //
 // The (repeated) keys are counted in an LDS hash table of kGroupSlots slots
 // (linear probing).  A bucket with more than 3/4 of the slots in distinct
@@ -360,14 +360,17 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* ke
 //   count:  every item of the range inserts its key and counts it;
 //   emit:   rows counted more than once get consecutive duplicate-buffer
 //           slots (positions of the bucket, after those of earlier ranges),
-//           and a work record: a short run, a piece, or pieces plus a
-//           combine record for a run longer than kPiece;
+//           and a work record in the bucket's own record regions: a short
+//           run, a piece, or pieces plus a combine record for a run longer
+//           than kPiece;
 //   place:  the repeated items, taken in occurrence order (chunk by chunk,
 //           compacted, then ranked by one wave 64 at a time), receive their
 //           row's next slot: info[o] = slot.
-// Where a row's range lands depends on the order of the hash insertions, the
-// order of its occurrences does not: every sum is taken in occurrence order.
-// Items that occur once keep info = -1 (set by the sampler).
+// At the end the bucket's record counts go to bcount[b].  No step waits for
+// another workgroup or uses a device-scope atomic.  Where a row's range lands
+// depends on the order of the hash insertions, the order of its occurrences
+// does not: every sum is taken in occurrence order.  Items that occur once
+// keep info = -1.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;   // keys are below 2N <= 2^32 - 2
 constexpr uint32_t kRepFlag = 0x80000000u;    // table count word: a repeated row, next slot
@@ -381,13 +384,21 @@ __device__ __forceinline__ bool in_range(uint32_t key, int level, uint32_t idx) 
     return level == 0 || ((key * 0xC2B2AE35u) >> (32 - level)) == idx;
 }
 
+// Dynamic LDS words of k_group<BM>.
 template <bool BM>
-__global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
+constexpr size_t group_lds_words() {
+    return 2 * kGroupSlots + kGroupCacheKeys + kGroupCacheVals + kGroupChunk +
+           (BM ? 2 * ((1 << kBitmapBits) / 32) : 0);
+}
+
+template <bool BM>
+__global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     Control* __restrict__ ctl, const uint32_t* __restrict__ keys,
     const uint32_t* __restrict__ vals, int64_t m, int64_t N, const uint32_t* __restrict__ hist,
     const uint32_t* __restrict__ bstart, int32_t* __restrict__ info, uint4* __restrict__ shorts,
     uint4* __restrict__ pieces, uint4* __restrict__ combs, uint32_t* __restrict__ ccount,
-    ListCaps caps, uint32_t* __restrict__ wstats, int bins, int shift, int sub_bits) {
+    uint4* __restrict__ bcount, ListCaps caps, uint32_t* __restrict__ wstats, int bins, int shift,
+    int sub_bits) {
     constexpr uint32_t kMax = (uint32_t)kGroupSlots / 4u * 3u;   // distinct keys a range may hold
     constexpr uint32_t kLoad = (uint32_t)kGroupSlots / 8u * 7u;  // table load a count stays below
     constexpr int kPer = kGroupSlots / kBlock;                   // table slots per thread
@@ -397,17 +408,17 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
     // compiler then keeps to the HUGE_BESIDE register budget, which a static
     // size above a fifth of the LDS would let it exceed.
     extern __shared__ uint32_t s_dyn[];
-    uint32_t* const s_key = s_dyn;                        // [kGroupSlots]
-    uint32_t* const s_cnt = s_key + kGroupSlots;          // count; after emit, kRepFlag | next slot
-    uint32_t* const s_cache = s_cnt + kGroupSlots;        // [kGroupCache]
+    uint32_t* const s_key = s_dyn;                          // [kGroupSlots]
+    uint32_t* const s_cnt = s_key + kGroupSlots;            // count; after emit, kRepFlag | next slot
+    uint32_t* const s_ckey = s_cnt + kGroupSlots;           // [kGroupCacheKeys]
+    uint32_t* const s_cval = s_ckey + kGroupCacheKeys;      // [kGroupCacheVals]
     // repeated items of a chunk in order: their table slot, then their
     // duplicate-buffer slot
-    uint32_t* const s_rep = s_cache + kGroupCache;        // [kGroupChunk]
-    uint32_t* const s_seen = s_rep + kGroupChunk;         // [kBitWords] with BM
-    uint32_t* const s_dup = s_seen + kBitWords;           // [kBitWords] with BM
+    uint32_t* const s_rep = s_cval + kGroupCacheVals;       // [kGroupChunk]
+    uint32_t* const s_seen = s_rep + kGroupChunk;           // [kBitWords] with BM
+    uint32_t* const s_dup = s_seen + kBitWords;             // [kBitWords] with BM
     __shared__ uint32_t s_tmp[6][kBlock / 64];
     __shared__ uint32_t s_distinct, s_fail, s_nrep;
-    __shared__ uint32_t s_base[4];
     __shared__ uint32_t s_stat[3];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -424,16 +435,17 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
     if (n == 0u || s0 + (int64_t)n > m) {
         if (n != 0u && tid == 0) HUGE_FAIL(kSiteGroupBucket);
         if (tid < 3) wstats[b * 3 + tid] = 0u;
+        if (tid == 0) bcount[b] = make_uint4(0u, 0u, 0u, 0u);
         continue;
     }
-    const bool cached = n <= (uint32_t)kGroupCache;
-    // the kGroupItems keys of this thread in chunk c0 (from LDS once cached)
-    auto load_keys = [&](uint32_t c0, uint32_t (&k)[kGroupItems], bool from_global) {
+    const bool keys_cached = n <= (uint32_t)kGroupCacheKeys;
+    const bool vals_cached = n <= (uint32_t)kGroupCacheVals;
+    // the kGroupItems keys of this thread in chunk c0
+    auto load_keys = [&](uint32_t c0, uint32_t (&k)[kGroupItems]) {
         const uint32_t e0 = c0 + (uint32_t)(tid * kGroupItems);
-        if (cached && !from_global) {
+        if (keys_cached) {
 #pragma unroll
-            for (int r = 0; r < kGroupItems; ++r)
-                k[r] = e0 + r < n ? s_cache[e0 + r] : 0u;
+            for (int r = 0; r < kGroupItems; ++r) k[r] = e0 + r < n ? s_ckey[e0 + r] : 0u;
         } else {
             const uint32_t* kp = keys + s0 + e0;
 #pragma unroll
@@ -441,7 +453,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
         }
     };
 
-    // ---- repeated keys (BM), the bucket to LDS ----
+    // ---- copy to LDS; repeated keys (BM) ----
     // the bit of key k is bit (k >> shift) of the bucket's bitmap; a key
     // beyond the bitmap cannot occur (sub_bits <= kBitmapBits)
     const uint32_t bit_words = sub_bits > 5 ? 1u << (sub_bits - 5) : 1u;
@@ -455,19 +467,34 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
             s_seen[j] = 0u;
             s_dup[j] = 0u;
         }
-        __syncthreads();
     }
-    if (BM || cached) {
+    if (keys_cached || vals_cached) {  // coalesced: item j + q kBlock by thread j
+        for (uint32_t e0 = 0; e0 < n; e0 += 4 * kBlock) {
+            uint32_t kk[4], vv[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t e = e0 + (uint32_t)(q * kBlock + tid);
+                kk[q] = e < n && keys_cached ? keys[s0 + e] : 0u;
+                vv[q] = e < n && vals_cached ? vals[s0 + e] : 0u;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t e = e0 + (uint32_t)(q * kBlock + tid);
+                if (e < n && keys_cached) s_ckey[e] = kk[q];
+                if (e < n && vals_cached) s_cval[e] = vv[q];
+            }
+        }
+    }
+    __syncthreads();
+    if (BM) {
         uint32_t nS = 0, nT = 0, nR = 0;
         for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
             uint32_t k[kGroupItems];
-            load_keys(c0, k, true);
+            load_keys(c0, k);
 #pragma unroll 1
             for (int r = 0; r < kGroupItems; ++r) {
                 const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
                 if (e >= n) continue;
-                if (cached) s_cache[e] = k[r];
-                if (!BM) continue;
                 const uint32_t sub = k[r] >> shift, w = sub >> 5, bit = 1u << (sub & 31u);
                 if (w >= bit_words) {
                     HUGE_FAIL(kSiteGroupBits);
@@ -492,6 +519,13 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
     // with the bitmap: nothing repeated, nothing to group
     const bool any = !BM || s_nrep != 0u;
 
+    // the bucket's record regions and how many records it has written
+    const uint32_t r_short = (uint32_t)(s0 / kShortDiv), c_short = (uint32_t)(n / kShortDiv);
+    const uint32_t r_piece = (uint32_t)(s0 / kPieceDiv), c_piece = (uint32_t)(n / kPieceDiv);
+    const uint32_t r_comb = (uint32_t)(s0 / kCombDiv), c_comb = (uint32_t)(n / kCombDiv);
+    const uint32_t r_part = (uint32_t)(s0 / kPartDiv), c_part = (uint32_t)(n / kPartDiv);
+    uint32_t nb_short = 0, nb_piece = 0, nb_comb = 0, nb_part = 0;
+
     uint32_t rep_base = 0;  // slots handed out to earlier ranges
     int level = 0, depth = 0;  // depth: where the next sibling range starts
     uint32_t ridx = 0;
@@ -507,6 +541,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
     };
     while (any) {
         // ---- count ----
+#pragma unroll 1
         for (int j = 0; j < kPer; ++j) {
             s_key[j * kBlock + tid] = kEmptyKey;
             s_cnt[j * kBlock + tid] = 0u;
@@ -525,7 +560,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
                 break;
             }
             uint32_t k[kGroupItems];
-            load_keys(c0, k, false);
+            load_keys(c0, k);
             uint32_t fresh = 0u;
 #pragma unroll 1
             for (int r = 0; r < kGroupItems; ++r) {
@@ -572,11 +607,13 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
             continue;
         }
 
+        {
         // ---- emit ----
         // this thread's table slots (tid, tid + kBlock, ...; conflict-free
         // LDS reads): statistics, slot counts, record counts; slots and
         // records are handed out thread by thread
         uint32_t nS = 0, nT = 0, nrep = 0, nshort = 0, npiece = 0, ncomb = 0, npart = 0;
+#pragma unroll 1
         for (int j = 0; j < kPer; ++j) {
             const int q = j * kBlock + tid;
             const uint32_t k = s_key[q];
@@ -605,28 +642,27 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
         const uint32_t x_piece = block_excl(npiece, s_tmp[2], &t_piece);
         const uint32_t x_comb = block_excl(ncomb, s_tmp[3], &t_comb);
         const uint32_t x_part = block_excl(npart, s_tmp[4], &t_part);
-        if (tid == 0) {
-            s_base[0] = t_short ? atomicAdd(&ctl->n_short, t_short) : 0u;
-            s_base[1] = t_piece ? atomicAdd(&ctl->n_piece, t_piece) : 0u;
-            s_base[2] = t_comb ? atomicAdd(&ctl->n_comb, t_comb) : 0u;
-            s_base[3] = t_part ? atomicAdd(&ctl->n_part, t_part) : 0u;
-        }
         if (nS) atomicAdd(&s_stat[0], nS);
         if (nT) atomicAdd(&s_stat[1], nT);
-        __syncthreads();
-        const bool fits = (uint64_t)s_base[0] + t_short <= caps.shorts &&
-                          (uint64_t)s_base[1] + t_piece <= caps.pieces &&
-                          (uint64_t)s_base[2] + t_comb <= caps.combs &&
-                          (uint64_t)s_base[3] + t_part <= caps.parts &&
-                          (uint64_t)rep_base + t_rep <= n;
-        if (!fits) {  // cannot happen: the capacities bound every batch
+        // uniform: every thread has the same totals and bases
+        const bool fits = (uint64_t)nb_short + t_short <= c_short &&
+                          (uint64_t)nb_piece + t_piece <= c_piece &&
+                          (uint64_t)nb_comb + t_comb <= c_comb &&
+                          (uint64_t)nb_part + t_part <= c_part &&
+                          (uint64_t)rep_base + t_rep <= n &&
+                          (uint64_t)r_short + c_short <= caps.shorts &&
+                          (uint64_t)r_piece + c_piece <= caps.pieces &&
+                          (uint64_t)r_comb + c_comb <= caps.combs &&
+                          (uint64_t)r_part + c_part <= caps.parts;
+        if (!fits) {  // cannot happen: the regions bound every bucket
             HUGE_FAIL(kSiteGroupLists);
             goto finished;
         }
         {
             uint32_t pos = (uint32_t)s0 + rep_base + x_rep;
-            uint32_t is = s_base[0] + x_short, ip = s_base[1] + x_piece;
-            uint32_t ic = s_base[2] + x_comb, ia = s_base[3] + x_part;
+            uint32_t is = r_short + nb_short + x_short, ip = r_piece + nb_piece + x_piece;
+            uint32_t ic = r_comb + nb_comb + x_comb, ia = r_part + nb_part + x_part;
+#pragma unroll 1
             for (int j = 0; j < kPer; ++j) {
                 const int q = j * kBlock + tid;
                 const uint32_t k = s_key[q];
@@ -651,6 +687,10 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
                 pos += c;
             }
         }
+        nb_short += t_short;
+        nb_piece += t_piece;
+        nb_comb += t_comb;
+        nb_part += t_part;
         if (tid == 0) s_stat[2] += t_rep;
         __syncthreads();
 
@@ -658,7 +698,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
         if (t_rep > 0u) {
             for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
                 uint32_t k[kGroupItems];
-                load_keys(c0, k, false);
+                load_keys(c0, k);
                 uint32_t mask = 0u, cnt = 0u;
 #pragma unroll 1
                 for (int r = 0; r < kGroupItems; ++r) {
@@ -708,7 +748,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
                     if (mask & (1u << r)) {
                         const uint32_t pos = s_rep[kk++];
                         const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
-                        const uint32_t o = vals[s0 + e];
+                        const uint32_t o = vals_cached ? s_cval[e] : vals[s0 + e];
                         if ((int64_t)pos >= s0 && (int64_t)pos < s0 + (int64_t)n && (int64_t)o < m)
                             info[o] = (int32_t)pos;
                         else
@@ -719,6 +759,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
             }
         }
         rep_base += t_rep;
+        }
 
         // ---- next range, depth first ----
         while (level > 0 && (ridx & 1u)) {
@@ -735,22 +776,18 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_group(
     }
     __syncthreads();
     if (tid < 3) wstats[b * 3 + tid] = s_stat[tid];
+    if (tid == 0) bcount[b] = make_uint4(nb_short, nb_piece, nb_comb, 0u);
     }
 finished:
     if (bad) raise_internal(ctl, bad);
 #undef HUGE_FAIL
 }
 
-// Dynamic LDS words of k_group<BM>.
-template <bool BM>
-constexpr size_t group_lds_words() {
-    return 2 * kGroupSlots + kGroupCache + kGroupChunk + (BM ? 2 * ((1 << kBitmapBits) / 32) : 0);
-}
-
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
                         uint4* shorts, uint4* pieces, uint4* combs, uint32_t* ccount,
-                        ListCaps caps, uint32_t* wstats, int bins, int key_bits, hipStream_t s) {
+                        uint4* bcount, ListCaps caps, uint32_t* wstats, int bins, int key_bits,
+                        hipStream_t s) {
     if (m == 0) return hipSuccess;
     if (bins < 2 || bins > kMaxBins || (bins & (bins - 1)) != 0) return hipErrorInvalidValue;
     const int shift = __builtin_ctz((unsigned)bins);
@@ -769,13 +806,13 @@ hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals
     }
     if (bm) {
         hipLaunchKernelGGL(k_group<true>, dim3((unsigned)bins), dim3(kBlock),
-                           group_lds_words<true>() * sizeof(uint32_t), s, ctl, keys,
-                           vals, m, N, hist, bstart, info, shorts, pieces, combs, ccount, caps,
+                           group_lds_words<true>() * sizeof(uint32_t), s, ctl, keys, vals, m, N,
+                           hist, bstart, info, shorts, pieces, combs, ccount, bcount, caps,
                            wstats, bins, shift, sub_bits);
     } else {
         hipLaunchKernelGGL(k_group<false>, dim3((unsigned)bins), dim3(kBlock),
-                           group_lds_words<false>() * sizeof(uint32_t), s, ctl, keys,
-                           vals, m, N, hist, bstart, info, shorts, pieces, combs, ccount, caps,
+                           group_lds_words<false>() * sizeof(uint32_t), s, ctl, keys, vals, m, N,
+                           hist, bstart, info, shorts, pieces, combs, ccount, bcount, caps,
                            wstats, bins, shift, sub_bits);
     }
     return hipGetLastError();

@@ -543,12 +543,48 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
 //           a device-scope fence) adds the partials in piece order and
 //           updates the row once.
 // The record counts were set by the grouping of this batch.
+// Exclusive sum of one value per thread over the workgroup; *total receives
+// the sum.  Synchronises; s_tmp (kBlock / 64 words) may be reused after the
+// next barrier.
+__device__ __forceinline__ uint32_t block_excl_sum(uint32_t v, uint32_t* s_tmp, uint32_t* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += t;
+    }
+    if (lane == 63) s_tmp[wave] = incl;
+    __syncthreads();
+    uint32_t add = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kBlock / 64; ++w) {
+        const uint32_t x = s_tmp[w];
+        if (w < wave) add += x;
+        all += x;
+    }
+    *total = all;
+    return add + incl - v;
+}
+
+// The bucket of record r: the largest b < bins with prefix[b] <= r.
+__device__ __forceinline__ int record_bucket(const uint32_t* prefix, int bins, uint32_t r) {
+    int lo = 0, hi = bins - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (prefix[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
 template <int G, int C, typename E>
 __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restrict__ ctl,
                                                    FinishArgs f) {
     constexpr int PPB = kBlock / G;
     __shared__ double s_part[1024 * C];  // PPB x D doubles: D <= 4 G C
     __shared__ double s_red[kBlock];
+    __shared__ uint32_t s_ps[kMaxBins], s_pp[kMaxBins], s_bs[kMaxBins];
+    __shared__ uint32_t s_tmp[2][kBlock / 64];
     __shared__ uint32_t s_flag;
     if (ctl->step_bad) {
         if (blockIdx.x == 0 && threadIdx.x == 0 && f.loss_out != nullptr)
@@ -577,18 +613,70 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
         if (threadIdx.x == 0) *f.loss_out = acc;
     }
 
-    // the grouping never lists more than the capacities (it flags the call
-    // instead); the bounds only keep a broken invariant inside the lists
-    const uint32_t ns = ctl->n_short < f.caps.shorts ? ctl->n_short : f.caps.shorts;
-    const uint32_t np = ctl->n_piece < f.caps.pieces ? ctl->n_piece : f.caps.pieces;
+    // Bucket b wrote its records to its own regions of the lists; record r
+    // of all short runs (pieces) in bucket order is record r - prefix[b] of
+    // bucket b's region.  Every workgroup takes the prefixes of the bucket
+    // counts into LDS (kMaxBins / kBlock buckets per thread).
+    constexpr int kBpt = kMaxBins / kBlock;
+    uint32_t cs = 0, cp = 0;
+#pragma unroll
+    for (int j = 0; j < kBpt; ++j) {
+        const int b = threadIdx.x * kBpt + j;
+        if (b < f.bins) {
+            const uint4 c = f.bcount[b];
+            cs += c.x;
+            cp += c.y;
+        }
+    }
+    uint32_t ns, np;
+    uint32_t xs = block_excl_sum(cs, s_tmp[0], &ns);
+    uint32_t xp = block_excl_sum(cp, s_tmp[1], &np);
+#pragma unroll
+    for (int j = 0; j < kBpt; ++j) {
+        const int b = threadIdx.x * kBpt + j;
+        if (b < f.bins) {
+            const uint4 c = f.bcount[b];
+            s_ps[b] = xs;
+            s_pp[b] = xp;
+            s_bs[b] = f.bstart[b];
+            xs += c.x;
+            xp += c.y;
+        }
+    }
+    __syncthreads();
     for (uint32_t r = blockIdx.x * PPB + grp; r < ns; r += gridDim.x * PPB) {
-        const uint4 rec = f.shorts[r];
+        const int b = record_bucket(s_ps, f.bins, r);
+        const uint32_t idx = s_bs[b] / kShortDiv + (r - s_ps[b]);
+        if (idx >= f.caps.shorts) {  // cannot happen: the regions hold every bucket
+            if (lane == 0) raise_internal(ctl, kSiteFinishComb);
+            continue;
+        }
+        const uint4 rec = f.shorts[idx];
+        // a record is used only if it lies inside this batch (the grouping
+        // writes only such records; the check keeps a broken invariant from
+        // reaching memory outside the buffers)
+        if (rec.y == 0u || rec.y > kShortRun || (int64_t)rec.x + rec.y > f.m ||
+            (int64_t)rec.z >= 2 * t.N) {
+            if (lane == 0) raise_internal(ctl, kSiteFinishComb);
+            continue;
+        }
         double4_ acc[C];
         sum_rows<G, C>(acc, f.dup, rec.x, rec.y, D, lane);
         apply_row<G, C, E>(t, rec.z, acc, f.lr, lane);
     }
     for (uint32_t r = blockIdx.x; r < np; r += gridDim.x) {
-        const uint4 rec = f.pieces[r];  // the same for every thread
+        const int b = record_bucket(s_pp, f.bins, r);
+        const uint32_t idx = s_bs[b] / kPieceDiv + (r - s_pp[b]);
+        if (idx >= f.caps.pieces) {  // uniform; cannot happen
+            if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
+            continue;
+        }
+        const uint4 rec = f.pieces[idx];  // the same for every thread
+        if (rec.y == 0u || rec.y > kPiece || (int64_t)rec.x + rec.y > f.m ||
+            (int64_t)rec.z >= 2 * t.N) {  // uniform; cannot happen
+            if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
+            continue;
+        }
         double4_ acc[C];
         coop_sum<G, C>(acc, f.dup, rec.x, rec.y, D, grp, lane, s_part);
         if (rec.w == 0u) {
@@ -598,7 +686,8 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
         const uint32_t ci = rec.w - 1u;
         const uint4 cb = ci < f.caps.combs ? f.combs[ci] : make_uint4(0u, 0u, 0u, 0u);
         const uint32_t z = (rec.x - cb.w) / kPiece;
-        if (ci >= f.caps.combs || z >= cb.z || (uint64_t)cb.y + cb.z > f.caps.parts) {
+        if (ci >= f.caps.combs || z >= cb.z || (uint64_t)cb.y + cb.z > f.caps.parts ||
+            (int64_t)cb.x >= 2 * t.N) {
             if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
             continue;  // uniform
         }

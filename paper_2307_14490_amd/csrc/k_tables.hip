@@ -88,15 +88,11 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 }
 
 // ---------------------------------------------------------------------------
-// Per-call set-up: clear the call's flag and the counts of the repeated-row
-// lists (a kernel rather than a memset so that the sequence stays valid
-// inside a captured graph).
+// Per-call set-up: clear the call's flag (a kernel rather than a memset so
+// that the sequence stays valid inside a captured graph).
 // ---------------------------------------------------------------------------
 __global__ HUGE_BESIDE void k_begin(Control* ctl) {
-    if (threadIdx.x == 0) {
-        ctl->step_bad = 0u;
-        ctl->n_short = ctl->n_piece = ctl->n_comb = ctl->n_part = 0u;
-    }
+    if (threadIdx.x == 0) ctl->step_bad = 0u;
 }
 
 hipError_t launch_begin(Control* ctl, hipStream_t s) {
