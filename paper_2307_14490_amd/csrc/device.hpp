@@ -48,11 +48,48 @@ __device__ __forceinline__ int32_t draw_negative(uint64_t seed, uint64_t p, uint
     return (int32_t)j;
 }
 
-// Sum over the G lanes of a group (G a power of two <= 64, groups aligned).
+// v plus the value of lane (lane XOR OFF), for a v that is already uniform
+// over aligned runs of OFF lanes (as it is when the steps of a sum are taken
+// in increasing OFF).  Below 16 the partner is read by DPP inside a 16-lane
+// row: swap of lane pairs, swap of pairs of pairs, then -- on such v -- the
+// mirror inside 8 lanes and inside 16 lanes, which read the partner run's
+// value.  At 16 and 32, gfx950's row swaps (v_permlane16_swap: odd rows of
+// one copy with even rows of the other; v_permlane32_swap: the two halves)
+// give every lane its own and its partner's value.  Both partners form the
+// same sum (a + b == b + a), so the result is uniform over 2 OFF lanes.  No
+// step goes through LDS.
+template <int OFF>
+__device__ __forceinline__ float xor_add(float v) {
+    const int x = __float_as_int(v);
+    if constexpr (OFF == 1) {
+        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false));
+    } else if constexpr (OFF == 2) {
+        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false));
+    } else if constexpr (OFF == 4) {
+        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false));
+    } else if constexpr (OFF == 8) {
+        return v + __int_as_float(__builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false));
+    } else if constexpr (OFF == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return __int_as_float(r[0]) + __int_as_float(r[1]);
+    } else {
+        static_assert(OFF == 32, "a power of two below 64");
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return __int_as_float(r[0]) + __int_as_float(r[1]);
+    }
+}
+
+// Sum over the G lanes of a group (G a power of two <= 64, groups aligned),
+// the same value in every lane of the group; every lane of the group is
+// active.
 template <int G>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    if constexpr (G >= 2) v = xor_add<1>(v);
+    if constexpr (G >= 4) v = xor_add<2>(v);
+    if constexpr (G >= 8) v = xor_add<4>(v);
+    if constexpr (G >= 16) v = xor_add<8>(v);
+    if constexpr (G >= 32) v = xor_add<16>(v);
+    if constexpr (G >= 64) v = xor_add<32>(v);
     return v;
 }
 

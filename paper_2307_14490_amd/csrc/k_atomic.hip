@@ -73,10 +73,7 @@ __device__ __forceinline__ float forward_positive(const TableArgs& t, const Step
 #pragma unroll
         for (int j = 0; j < kNegBlock; ++j) y[j] = (j < cnt) ? IO::dot(s, tk[j]) : 0.f;
 #pragma unroll
-        for (int off = G / 2; off > 0; off >>= 1) {
-#pragma unroll
-            for (int j = 0; j < kNegBlock; ++j) y[j] += __shfl_xor(y[j], off, 64);
-        }
+        for (int j = 0; j < kNegBlock; ++j) y[j] = group_sum<G>(y[j]);
 #pragma unroll
         for (int j = 0; j < kNegBlock; ++j) {
             if (j < cnt) {

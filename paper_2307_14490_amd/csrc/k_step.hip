@@ -157,10 +157,7 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
 #pragma unroll
             for (int j = 0; j < NB; ++j) y[j] = (j < cnt) ? IO::dotp(s, tk[j]) : 0.f;
 #pragma unroll
-            for (int off = G / 2; off > 0; off >>= 1) {
-#pragma unroll
-                for (int j = 0; j < NB; ++j) y[j] += __shfl_xor(y[j], off, 64);
-            }
+            for (int j = 0; j < NB; ++j) y[j] = group_sum<G>(y[j]);
 #pragma unroll
             for (int j = 0; j < NB; ++j) IO::refresh(tk[j]);
 #pragma unroll
@@ -424,15 +421,18 @@ __device__ __forceinline__ void sum_rows(double4_ (&acc)[C], const float* __rest
     }
 }
 
-template <int G, int C, typename E>
-__device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
-                                          const double4_ (&g)[C], float lr, int lane) {
-    using IO = RowIO<G, C, E>;
-    E* base = static_cast<E*>((int64_t)key >= t.N ? t.S : t.T);
-    const int64_t row = (int64_t)key >= t.N ? (int64_t)key - t.N : (int64_t)key;
+// The table and row of a key (N + i: source row i, else context row key).
+template <typename E>
+__device__ __forceinline__ E* key_row(const TableArgs& t, uint32_t key, int64_t* row) {
+    const bool src = (int64_t)key >= t.N;
+    *row = src ? (int64_t)key - t.N : (int64_t)key;
+    return static_cast<E*>(src ? t.S : t.T);
+}
+
+// r -= lr g, in double, rounded once to the table's type by the store.
+template <int C>
+__device__ __forceinline__ void sgd_row(float4 (&r)[C], const double4_ (&g)[C], float lr) {
     const double l = (double)lr;
-    float4 r[C];
-    IO::load(r, base, row, t.D, lane);
 #pragma unroll
     for (int q = 0; q < C; ++q) {
         r[q].x = (float)((double)r[q].x - l * g[q].x);
@@ -440,6 +440,17 @@ __device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
         r[q].z = (float)((double)r[q].z - l * g[q].z);
         r[q].w = (float)((double)r[q].w - l * g[q].w);
     }
+}
+
+template <int G, int C, typename E>
+__device__ __forceinline__ void apply_row(const TableArgs& t, uint32_t key,
+                                          const double4_ (&g)[C], float lr, int lane) {
+    using IO = RowIO<G, C, E>;
+    int64_t row;
+    E* base = key_row<E>(t, key, &row);
+    float4 r[C];
+    IO::load(r, base, row, t.D, lane);
+    sgd_row<C>(r, g, lr);
     IO::store(base, row, t.D, lane, r);
 }
 
@@ -530,11 +541,13 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
 }
 
 // After the fused step, in one launch:
-//   loss:   workgroup 0 sums the fused step's per-workgroup partials in a
-//           fixed order (no cross-workgroup step: a device-scope fence per
+//   loss:   the last workgroup sums the fused step's per-workgroup
+//           partials in a fixed order and takes no records, so the sum runs
+//           beside them (no cross-workgroup step: a device-scope fence per
 //           workgroup, to pass partial sums between them, measured slower);
-//   short runs ({start, len <= kShortRun, key}): one thread group each sums
-//           its contributions in occurrence order and updates the row;
+//   short runs ({start, len <= kShortRun, key}): one thread group each
+//           loads the row with its contributions, sums them in occurrence
+//           order and updates the row;
 //   pieces ({start, len <= kPiece, key, comb}): the whole workgroup sums
 //           them; a whole run (comb = 0) updates its row; a piece of a
 //           longer run stores its sum as partial z of its combine record
@@ -595,38 +608,46 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
     const int lane = threadIdx.x % G;
     const int32_t D = t.D;
 
-    if (blockIdx.x == 0 && f.loss_out != nullptr) {
-        // thread t adds partials t, t + kBlock, ... in that order, then the
-        // threads' sums meet in a fixed tree: the same double on every run;
-        // the loads are issued sixteen at a time
+    // The last workgroup sums the loss and nothing else: thread t adds
+    // partials t, t + kBlock, ... in that order (32 loads in flight), then
+    // the threads' sums meet in a fixed tree: the same double on every run.
+    if (blockIdx.x == gridDim.x - 1) {
+        if (f.loss_out == nullptr) return;
         double acc = 0.0;
         int64_t j = threadIdx.x;
-        for (; j + 15 * kBlock < f.loss_blocks; j += 16 * kBlock) {
-            double v[16];
+        for (; j + 31 * kBlock < f.loss_blocks; j += 32 * kBlock) {
+            double v[32];
 #pragma unroll
-            for (int q = 0; q < 16; ++q) v[q] = f.lossp[j + q * kBlock];
+            for (int q = 0; q < 32; ++q) v[q] = f.lossp[j + q * kBlock];
 #pragma unroll
-            for (int q = 0; q < 16; ++q) acc += v[q];
+            for (int q = 0; q < 32; ++q) acc += v[q];
         }
         for (; j < f.loss_blocks; j += kBlock) acc += f.lossp[j];
         acc = block_sum_fixed(acc, s_red);
         if (threadIdx.x == 0) *f.loss_out = acc;
+        return;
     }
+    // the other workgroups take the records
+    const uint32_t rec_groups = gridDim.x - 1u;
 
     // Bucket b wrote its records to its own regions of the lists; record r
     // of all short runs (pieces) in bucket order is record r - prefix[b] of
     // bucket b's region.  Every workgroup takes the prefixes of the bucket
     // counts into LDS (kMaxBins / kBlock buckets per thread).
     constexpr int kBpt = kMaxBins / kBlock;
+    uint4 bc[kBpt];
+    uint32_t bs[kBpt];
     uint32_t cs = 0, cp = 0;
 #pragma unroll
     for (int j = 0; j < kBpt; ++j) {
         const int b = threadIdx.x * kBpt + j;
-        if (b < f.bins) {
-            const uint4 c = f.bcount[b];
-            cs += c.x;
-            cp += c.y;
-        }
+        bc[j] = b < f.bins ? f.bcount[b] : make_uint4(0u, 0u, 0u, 0u);
+        bs[j] = b < f.bins ? f.bstart[b] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kBpt; ++j) {
+        cs += bc[j].x;
+        cp += bc[j].y;
     }
     uint32_t ns, np;
     uint32_t xs = block_excl_sum(cs, s_tmp[0], &ns);
@@ -635,16 +656,15 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
     for (int j = 0; j < kBpt; ++j) {
         const int b = threadIdx.x * kBpt + j;
         if (b < f.bins) {
-            const uint4 c = f.bcount[b];
             s_ps[b] = xs;
             s_pp[b] = xp;
-            s_bs[b] = f.bstart[b];
-            xs += c.x;
-            xp += c.y;
+            s_bs[b] = bs[j];
+            xs += bc[j].x;
+            xp += bc[j].y;
         }
     }
     __syncthreads();
-    for (uint32_t r = blockIdx.x * PPB + grp; r < ns; r += gridDim.x * PPB) {
+    for (uint32_t r = blockIdx.x * PPB + grp; r < ns; r += rec_groups * PPB) {
         const int b = record_bucket(s_ps, f.bins, r);
         const uint32_t idx = s_bs[b] / kShortDiv + (r - s_ps[b]);
         if (idx >= f.caps.shorts) {  // cannot happen: the regions hold every bucket
@@ -660,11 +680,17 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
             if (lane == 0) raise_internal(ctl, kSiteFinishComb);
             continue;
         }
+        // the row's values are loaded with the contributions
+        int64_t row;
+        E* base = key_row<E>(t, rec.z, &row);
+        float4 cur[C];
+        RowIO<G, C, E>::load(cur, base, row, D, lane);
         double4_ acc[C];
         sum_rows<G, C>(acc, f.dup, rec.x, rec.y, D, lane);
-        apply_row<G, C, E>(t, rec.z, acc, f.lr, lane);
+        sgd_row<C>(cur, acc, f.lr);
+        RowIO<G, C, E>::store(base, row, D, lane, cur);
     }
-    for (uint32_t r = blockIdx.x; r < np; r += gridDim.x) {
+    for (uint32_t r = blockIdx.x; r < np; r += rec_groups) {
         const int b = record_bucket(s_pp, f.bins, r);
         const uint32_t idx = s_bs[b] / kPieceDiv + (r - s_pp[b]);
         if (idx >= f.caps.pieces) {  // uniform; cannot happen
