@@ -376,8 +376,9 @@ constexpr uint32_t kEmptyKey = 0xFFFFFFFFu;   // keys are below 2N <= 2^32 - 2
 constexpr uint32_t kRepFlag = 0x80000000u;    // table count word: a repeated row, next slot
 constexpr int kMaxProbe = 512;                // a longer probe also splits the range
 
-__device__ __forceinline__ uint32_t slot_hash(uint32_t key) {
-    return (key * 0x85EBCA6Bu) >> (32 - kGroupTableBits);
+// Slot of a key in a table of 2^tbits slots.
+__device__ __forceinline__ uint32_t slot_hash(uint32_t key, int tbits) {
+    return (key * 0x85EBCA6Bu) >> (32 - tbits);
 }
 
 __device__ __forceinline__ bool in_range(uint32_t key, int level, uint32_t idx) {
@@ -399,11 +400,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     uint4* __restrict__ pieces, uint4* __restrict__ combs, uint32_t* __restrict__ ccount,
     uint4* __restrict__ bcount, ListCaps caps, uint32_t* __restrict__ wstats, int bins, int shift,
     int sub_bits) {
-    constexpr uint32_t kMax = (uint32_t)kGroupSlots / 4u * 3u;   // distinct keys a range may hold
-    constexpr uint32_t kLoad = (uint32_t)kGroupSlots / 8u * 7u;  // table load a count stays below
-    constexpr int kPer = kGroupSlots / kBlock;                   // table slots per thread
     constexpr int kBitWords = (1 << kBitmapBits) / 32;           // words of one bitmap
-    constexpr uint32_t kMask = (uint32_t)kGroupSlots - 1u;
     // The large arrays live in dynamic LDS (group_lds_words<BM>() words): the
     // compiler then keeps to the HUGE_BESIDE register budget, which a static
     // size above a fifth of the LDS would let it exceed.
@@ -441,15 +438,16 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     const bool keys_cached = n <= (uint32_t)kGroupCacheKeys;
     const bool vals_cached = n <= (uint32_t)kGroupCacheVals;
     // the kGroupItems keys of this thread in chunk c0
-    auto load_keys = [&](uint32_t c0, uint32_t (&k)[kGroupItems]) {
+    // (after the compaction: of the first nw items)
+    auto load_keys = [&](uint32_t c0, uint32_t nlim, uint32_t (&k)[kGroupItems]) {
         const uint32_t e0 = c0 + (uint32_t)(tid * kGroupItems);
         if (keys_cached) {
 #pragma unroll
-            for (int r = 0; r < kGroupItems; ++r) k[r] = e0 + r < n ? s_ckey[e0 + r] : 0u;
+            for (int r = 0; r < kGroupItems; ++r) k[r] = e0 + r < nlim ? s_ckey[e0 + r] : 0u;
         } else {
             const uint32_t* kp = keys + s0 + e0;
 #pragma unroll
-            for (int r = 0; r < kGroupItems; ++r) k[r] = e0 + r < n ? kp[r] : 0u;
+            for (int r = 0; r < kGroupItems; ++r) k[r] = e0 + r < nlim ? kp[r] : 0u;
         }
     };
 
@@ -490,7 +488,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
         uint32_t nS = 0, nT = 0, nR = 0;
         for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
             uint32_t k[kGroupItems];
-            load_keys(c0, k);
+            load_keys(c0, n, k);
 #pragma unroll 1
             for (int r = 0; r < kGroupItems; ++r) {
                 const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
@@ -519,6 +517,53 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     // with the bitmap: nothing repeated, nothing to group
     const bool any = !BM || s_nrep != 0u;
 
+    // With the bitmap and the whole bucket in LDS, only the items of
+    // repeated keys are grouped: they are compacted to the front of the LDS
+    // copy, in occurrence order (chunk by chunk; an item moves only to a
+    // lower position, so no item is overwritten before it is read), and
+    // the hash table is sized to them.
+    uint32_t nw = n;  // items the count and the placement go through
+    int tbits = kGroupTableBits;
+    if (BM && any && keys_cached && vals_cached) {
+        uint32_t out = 0;
+        for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
+            uint32_t kk[kGroupItems], vv[kGroupItems];
+            uint32_t mask = 0u, cnt = 0u;
+            const uint32_t e0 = c0 + (uint32_t)(tid * kGroupItems);
+#pragma unroll
+            for (int r = 0; r < kGroupItems; ++r) {
+                kk[r] = e0 + r < n ? s_ckey[e0 + r] : 0u;
+                vv[r] = e0 + r < n ? s_cval[e0 + r] : 0u;
+            }
+#pragma unroll 1
+            for (int r = 0; r < kGroupItems; ++r) {
+                if (e0 + r < n && repeated(kk[r])) {
+                    mask |= 1u << r;
+                    ++cnt;
+                }
+            }
+            uint32_t total;
+            uint32_t p = out + block_excl(cnt, s_tmp[0], &total);  // synchronises
+#pragma unroll 1
+            for (int r = 0; r < kGroupItems; ++r) {
+                if (mask & (1u << r)) {
+                    s_ckey[p] = kk[r];
+                    s_cval[p] = vv[r];
+                    ++p;
+                }
+            }
+            out += total;
+            __syncthreads();  // s_tmp is reused
+        }
+        nw = out;
+        tbits = 6;
+        while (tbits < kGroupTableBits && (1u << tbits) < 2u * nw) ++tbits;
+    }
+    const uint32_t tsize = 1u << tbits;
+    const uint32_t tmask = tsize - 1u;
+    const uint32_t tmax = tsize / 4u * 3u;   // distinct keys a range may hold
+    const uint32_t tload = tsize / 8u * 7u;  // table load a count stays below
+
     // the bucket's record regions and how many records it has written
     const uint32_t r_short = (uint32_t)(s0 / kShortDiv), c_short = (uint32_t)(n / kShortDiv);
     const uint32_t r_piece = (uint32_t)(s0 / kPieceDiv), c_piece = (uint32_t)(n / kPieceDiv);
@@ -530,21 +575,21 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     int level = 0, depth = 0;  // depth: where the next sibling range starts
     uint32_t ridx = 0;
     auto lookup = [&](uint32_t key) -> uint32_t {
-        uint32_t h = slot_hash(key);
+        uint32_t h = slot_hash(key, tbits);
         for (int probe = 0; probe < kMaxProbe; ++probe) {
             const uint32_t kk = s_key[h];
             if (kk == key) return h;
             if (kk == kEmptyKey) return kEmptyKey;
-            h = (h + 1u) & kMask;
+            h = (h + 1u) & tmask;
         }
         return kEmptyKey;
     };
     while (any) {
         // ---- count ----
 #pragma unroll 1
-        for (int j = 0; j < kPer; ++j) {
-            s_key[j * kBlock + tid] = kEmptyKey;
-            s_cnt[j * kBlock + tid] = 0u;
+        for (uint32_t q = tid; q < tsize; q += kBlock) {
+            s_key[q] = kEmptyKey;
+            s_cnt[q] = 0u;
         }
         if (tid == 0) {
             s_distinct = 0u;
@@ -553,20 +598,20 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
         __syncthreads();
         uint32_t seen = 0;  // items the count went through
         bool over = false;
-        for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
-            const uint32_t len = n - c0 < (uint32_t)kGroupChunk ? n - c0 : (uint32_t)kGroupChunk;
-            if (s_distinct + len > kLoad) {  // uniform: the table could fill up
+        for (uint32_t c0 = 0; c0 < nw; c0 += kGroupChunk) {
+            const uint32_t len = nw - c0 < (uint32_t)kGroupChunk ? nw - c0 : (uint32_t)kGroupChunk;
+            if (s_distinct + len > tload) {  // uniform: the table could fill up
                 over = true;
                 break;
             }
             uint32_t k[kGroupItems];
-            load_keys(c0, k);
+            load_keys(c0, nw, k);
             uint32_t fresh = 0u;
 #pragma unroll 1
             for (int r = 0; r < kGroupItems; ++r) {
                 const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
-                if (e >= n || !in_range(k[r], level, ridx) || !repeated(k[r])) continue;
-                uint32_t h = slot_hash(k[r]);
+                if (e >= nw || !in_range(k[r], level, ridx) || !repeated(k[r])) continue;
+                uint32_t h = slot_hash(k[r], tbits);
                 bool found = false;
                 for (int probe = 0; probe < kMaxProbe; ++probe) {
                     const uint32_t old = atomicCAS(&s_key[h], kEmptyKey, k[r]);
@@ -576,14 +621,14 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
                         found = true;
                         break;
                     }
-                    h = (h + 1u) & kMask;
+                    h = (h + 1u) & tmask;
                 }
                 if (!found) s_fail = 1u;
             }
             if (fresh) atomicAdd(&s_distinct, fresh);
             __syncthreads();
             seen = c0 + len;
-            if (s_fail || s_distinct > kMax) {  // uniform
+            if (s_fail || s_distinct > tmax) {  // uniform
                 over = true;
                 break;
             }
@@ -592,8 +637,8 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
             // split the range; its first part next (uniform)
             int add = 1;
             if (!s_fail && seen > 0u) {
-                const uint64_t est = (uint64_t)s_distinct * n / seen;
-                while (add < 8 && est > ((uint64_t)kMax << add) / 4u * 3u) ++add;
+                const uint64_t est = (uint64_t)s_distinct * nw / seen;
+                while (add < 8 && est > ((uint64_t)tmax << add) / 4u * 3u) ++add;
             }
             __syncthreads();
             if (level >= 32) {  // cannot happen: a depth-32 range holds one key value
@@ -614,8 +659,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
         // records are handed out thread by thread
         uint32_t nS = 0, nT = 0, nrep = 0, nshort = 0, npiece = 0, ncomb = 0, npart = 0;
 #pragma unroll 1
-        for (int j = 0; j < kPer; ++j) {
-            const int q = j * kBlock + tid;
+        for (uint32_t q = tid; q < tsize; q += kBlock) {
             const uint32_t k = s_key[q];
             if (k == kEmptyKey) continue;
             if (!BM) {  // with BM the first pass counted the rows
@@ -663,8 +707,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
             uint32_t is = r_short + nb_short + x_short, ip = r_piece + nb_piece + x_piece;
             uint32_t ic = r_comb + nb_comb + x_comb, ia = r_part + nb_part + x_part;
 #pragma unroll 1
-            for (int j = 0; j < kPer; ++j) {
-                const int q = j * kBlock + tid;
+            for (uint32_t q = tid; q < tsize; q += kBlock) {
                 const uint32_t k = s_key[q];
                 const uint32_t c = s_cnt[q];
                 if (k == kEmptyKey || c <= 1u) continue;
@@ -696,14 +739,14 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
 
         // ---- place ----
         if (t_rep > 0u) {
-            for (uint32_t c0 = 0; c0 < n; c0 += kGroupChunk) {
+            for (uint32_t c0 = 0; c0 < nw; c0 += kGroupChunk) {
                 uint32_t k[kGroupItems];
-                load_keys(c0, k);
+                load_keys(c0, nw, k);
                 uint32_t mask = 0u, cnt = 0u;
 #pragma unroll 1
                 for (int r = 0; r < kGroupItems; ++r) {
                     const uint32_t e = c0 + (uint32_t)(tid * kGroupItems + r);
-                    if (e >= n || !in_range(k[r], level, ridx) || !repeated(k[r])) continue;
+                    if (e >= nw || !in_range(k[r], level, ridx) || !repeated(k[r])) continue;
                     const uint32_t h = lookup(k[r]);
                     if (h == kEmptyKey) {
                         HUGE_FAIL(kSiteGroupLookup);
@@ -728,7 +771,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
                         const uint32_t j = j0 + (uint32_t)lane;
                         const bool act = j < chunk_rep;
                         const uint32_t sl = act ? s_rep[j] : 0u;
-                        const uint64_t peers = match_peers(sl, kGroupTableBits, __ballot(act));
+                        const uint64_t peers = match_peers(sl, tbits, __ballot(act));
                         const uint32_t before = (uint32_t)__popcll(peers & lanes_below());
                         const int ld = __ffsll((long long)peers) - 1;
                         const int leader = ld < 0 ? 0 : ld;

@@ -56,12 +56,24 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
     constexpr int C = IO::C;
     constexpr int R = IO::R;
     static_assert(DIO::C == C, "the contribution layout must match the row layout");
-    // At least 88 VGPRs: five waves per SIMD (440 of 512 registers), not six,
-    // so that one wave of a grouping kernel of the next batch (at most 64
-    // VGPRs) fits beside them on every SIMD.  The empty statement marks v87
-    // as used; it generates no instruction.
-    asm volatile("" ::: "v87");
+    // Registers: at least 88 VGPRs for float tables -- five waves per SIMD
+    // (440 of 512 registers), not six -- and at least 104 for bf16 tables,
+    // whose variants need more than 88: four waves, not five -- so that one
+    // wave of a grouping kernel of the next batch (at most 72 VGPRs) fits
+    // beside them on every SIMD.  The empty statement marks the register as
+    // used; it generates no instruction.
+    if constexpr (sizeof(E) == 2)
+        asm volatile("" ::: "v103");
+    else
+        asm volatile("" ::: "v87");
     constexpr int PPB = kBlock / G;
+    // A group of at least 1 + NB lanes evaluates its sigmoids and softplus
+    // terms one value per lane instead of every lane evaluating all of them;
+    // the positive's too where its row takes at most four registers (a wider
+    // row would stay live until the first negatives' coefficients, which
+    // costs more occupancy than the one evaluation saves).
+    constexpr bool kLaneCoefs = G >= NB + 1;
+    constexpr bool kLanePos = kLaneCoefs && sizeof(Reg) * R <= 16;
     const int grp = threadIdx.x / G;
     const int lane = threadIdx.x % G;
     const int64_t i = (int64_t)blockIdx.x * PPB + grp;
@@ -134,20 +146,30 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
         // positive pair
         const float x = group_sum<G>(IO::dotp(s, t0));
         IO::refresh(t0);
-        const float g = coef_pos(c, x);
-        float lsum = softplus_f(-x);
+        // g: the positive's coefficient; dS: the source row's gradient
+        float g = 0.f;
+        float lsum = 0.f;
+        auto positive_update = [&]() {
 #pragma unroll
-        for (int q = 0; q < C; ++q) dS[q] = scale4(g, IO::chunk(t0, q));
-        if (info_d < 0) {
-            float4 nv[C];
+            for (int q = 0; q < C; ++q) dS[q] = scale4(g, IO::chunk(t0, q));
+            if (info_d < 0) {
+                float4 nv[C];
 #pragma unroll
-            for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * g), s[q], IO::chunk(t0, q));
-            IO::store(T, v, D, lane, nv);
-        } else {
-            float4 cv[C];
+                for (int q = 0; q < C; ++q) nv[q] = axpy4(-(lr * g), s[q], IO::chunk(t0, q));
+                IO::store(T, v, D, lane, nv);
+            } else {
+                float4 cv[C];
 #pragma unroll
-            for (int q = 0; q < C; ++q) cv[q] = scale4(g, s[q]);
-            DIO::store(dup, info_d, D, lane, cv);
+                for (int q = 0; q < C; ++q) cv[q] = scale4(g, s[q]);
+                DIO::store(dup, info_d, D, lane, cv);
+            }
+        };
+        if constexpr (!kLanePos) {
+            g = coef_pos(c, x);
+            // with lane coefficients every lane's terms are summed: the
+            // positive's term is lane 0's
+            if (!kLaneCoefs || lane == 0) lsum = softplus_f(-x);
+            positive_update();
         }
 
         // negatives, NB rows in flight at a time
@@ -160,23 +182,57 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
             for (int j = 0; j < NB; ++j) y[j] = group_sum<G>(y[j]);
 #pragma unroll
             for (int j = 0; j < NB; ++j) IO::refresh(tk[j]);
+            float h[NB];
+            if constexpr (kLaneCoefs) {
+                // lane q of the group evaluates value q -- the positive's
+                // -x (q = 0, first block only, with kLanePos) or negative
+                // q - 1's y -- and the group reads the coefficients from
+                // those lanes:
+                //   coefficient sign c sigmoid(z), loss term softplus(z),
+                // both from e = exp(-|z|) (no overflow)
+                float z = lane == 0 ? -x : 0.f;
+                bool has = kLanePos && lane == 0 && kb == 0;
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    if (lane == j + 1) {
+                        z = y[j];
+                        has = j < cnt;
+                    }
+                }
+                const float e = expf(-fabsf(z));
+                const float coef = (lane == 0 ? -c : c) * (z >= 0.f ? 1.0f : e) / (1.0f + e);
+                if (has) lsum += fmaxf(z, 0.f) + log1pf(e);
+                const int first = (int)(threadIdx.x & 63u) - lane;  // the group's first lane
+                if (kLanePos && kb == 0) {
+                    g = __shfl(coef, first, 64);
+                    positive_update();
+                }
+#pragma unroll
+                for (int j = 0; j < NB; ++j) h[j] = __shfl(coef, first + 1 + j, 64);
+            } else {
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    if (j < cnt) {
+                        h[j] = coef_neg(c, y[j]);
+                        lsum += softplus_f(y[j]);
+                    }
+                }
+            }
 #pragma unroll
             for (int j = 0; j < NB; ++j) {
                 if (j < cnt) {
-                    const float h = coef_neg(c, y[j]);
-                    lsum += softplus_f(y[j]);
 #pragma unroll
-                    for (int q = 0; q < C; ++q) dS[q] = axpy4(h, IO::chunk(tk[j], q), dS[q]);
+                    for (int q = 0; q < C; ++q) dS[q] = axpy4(h[j], IO::chunk(tk[j], q), dS[q]);
                     if (ik[j] < 0) {
                         float4 nv[C];
 #pragma unroll
                         for (int q = 0; q < C; ++q)
-                            nv[q] = axpy4(-(lr * h), s[q], IO::chunk(tk[j], q));
+                            nv[q] = axpy4(-(lr * h[j]), s[q], IO::chunk(tk[j], q));
                         IO::store(T, mk[j], D, lane, nv);
                     } else {
                         float4 cv[C];
 #pragma unroll
-                        for (int q = 0; q < C; ++q) cv[q] = scale4(h, s[q]);
+                        for (int q = 0; q < C; ++q) cv[q] = scale4(h[j], s[q]);
                         DIO::store(dup, ik[j], D, lane, cv);
                     }
                 }
@@ -210,7 +266,8 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(TableArgs t, Control* __r
         } else {
             DIO::store(dup, info_s, D, lane, dS);
         }
-        if (lane == 0) loss = c * lsum;
+        // with lane coefficients every lane holds its own loss terms
+        if (kLaneCoefs || lane == 0) loss = c * lsum;
     }
     block_loss(loss, lossp);
 }
