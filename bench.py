@@ -85,10 +85,10 @@ def cpu_model() -> str:
 
 
 # Steps of the CPU oracle per workload: a whole epoch of the tiny workload,
-# the first 50 steps of the medium one, the first 3 of the large ones (all
+# the first 50 steps of the medium one, the first 5 of the large ones (all
 # within the time budget).
 CPU_STEPS = {"tiny": None, "medium": 50}
-CPU_STEPS_DEFAULT = 3
+CPU_STEPS_DEFAULT = 5
 
 
 def cpu_baseline(wl, seed, budget_s=30.0):

@@ -66,12 +66,16 @@ CONFIGS = {
     "medium": Config("medium", 1, 1_000_000, 128, 5, 65_536, 0.025, "alias", "sbm", blocks=100,
                      deg_in=20.0, deg_out=2.0, walks_per_node=8, walk_steps=20, window=3,
                      exact_graph=True),
-    "powerlaw": Config("powerlaw", 2, 10_000_000, 128, 10, 131_072, 0.02, "alias", "chung_lu",
+    # learning rates of the Chung-Lu workloads: the largest power of ten (times
+    # 1 or 5) whose summed hub-row updates stay finite over a few hundred
+    # steps -- a hub row takes thousands of contributions per batch, and the
+    # Hub-stress co_counts reach 1000
+    "powerlaw": Config("powerlaw", 2, 10_000_000, 128, 10, 131_072, 0.005, "alias", "chung_lu",
                        exponent=2.1, mean_deg=30.0, walks_per_node=4, walk_steps=40, window=5),
     "sbm100m": Config("sbm100m", 3, 100_000_000, 128, 5, 262_144, 0.025, "uniform", "sbm",
                       blocks=1000, deg_in=25.0, deg_out=2.0, walks_per_node=1, walk_steps=20,
                       window=2),
-    "hubstress": Config("hubstress", 4, 50_000_000, 256, 20, 262_144, 0.025, "alias",
+    "hubstress": Config("hubstress", 4, 50_000_000, 256, 20, 262_144, 1e-6, "alias",
                         "chung_lu", exponent=1.9, mean_deg=50.0, pairs="endpoints",
                         cc_zipf=1.5, cc_cap=1000),
     # the SBM-100M graph with the paper's 31 negatives per positive (Table 2)
