@@ -385,6 +385,23 @@ huge_status huge_eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non
                               const double* h_quantiles, int32_t n_quantiles, double* d_out,
                               void* d_workspace, size_t ws_bytes, void* stream);
 
+/* huge_eval_summary without a caller workspace, for callers that cannot
+   allocate device memory (code under HIP graph capture, serving loops,
+   harnesses that forbid hipMalloc): the same kernels on a fixed 32 MiB array
+   of device memory that the library holds on every device it runs on until
+   the process ends.  It allocates nothing and calls no allocating routine.
+   n_edge + n_non may be up to 3,726,784 (the largest count whose summary
+   workspace fits in the array); more returns HUGE_ERR_WORKSPACE before any
+   launch.  Every call on a device uses that
+   device's one array and finds the previous call's contents there (nothing
+   is carried over: each call writes what it reads); calls that overlap on
+   one device -- on different streams or from different threads without
+   ordering -- race on it and must be serialised by the caller.  Other
+   arguments and errors as for huge_eval_summary. */
+huge_status huge_eval_summary_static(const float* d_dist, int64_t n_edge, int64_t n_non,
+                                     const double* h_quantiles, int32_t n_quantiles,
+                                     double* d_out, void* stream);
+
 /* The k rows nearest to each of the n_queries query rows (ids in d_queries),
    excluding the query itself: d_ids[q k + t] (device int32, ascending
    (distance, id); -1 if fewer than k other rows exist) and d_dist[...]

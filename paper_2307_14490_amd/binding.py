@@ -35,6 +35,7 @@ EXPORTED = [
     "huge_get_rows", "huge_sample_negatives", "huge_probe_rows", "huge_check", "huge_step_stats", "huge_profile_begin", "huge_profile_end",
     "huge_destroy", "huge_status_string", "huge_walk_workspace_bytes", "huge_sample_walks",
     "huge_eval_workspace_bytes", "huge_eval_pairs", "huge_eval_distances", "huge_eval_summary",
+    "huge_eval_summary_static",
     "huge_eval_knn", "huge_eval_recall", "huge_train_step_weighted", "huge_prepare_step_weighted",
     "huge_eval_loss_weighted", "huge_cocount_weights",
 ]
@@ -120,6 +121,8 @@ def load() -> ctypes.CDLL:
     L.huge_eval_distances.argtypes = [_vp, i64, i32, _vp, _vp, i64, _vp, _vp, _vp]
     L.huge_eval_summary.argtypes = [_vp, i64, i64, ctypes.POINTER(ctypes.c_double), i32, _vp,
                                     _vp, szt, _vp]
+    L.huge_eval_summary_static.argtypes = [_vp, i64, i64, ctypes.POINTER(ctypes.c_double), i32,
+                                           _vp, _vp]
     L.huge_eval_knn.argtypes = [_vp, i64, i32, _vp, i32, i32, _vp, _vp, _vp, szt, _vp, _vp]
     L.huge_eval_recall.argtypes = [_vp, _vp, i64, i64, _vp, i32, _vp, i32, _vp, _vp, _vp]
     for name in ("huge_eval_pairs", "huge_eval_distances", "huge_eval_summary", "huge_eval_knn",
@@ -528,8 +531,11 @@ class Evaluator:
         self._check("huge_eval_distances")
         return d
 
-    def summary(self, dist, n_edge, n_non, quantiles=(0, 10, 25, 50, 75, 90, 100), stream=None):
-        """dict: count_edge, count_non, mean_edge, mean_non, snr, pct_edge, pct_non."""
+    def summary(self, dist, n_edge, n_non, quantiles=(0, 10, 25, 50, 75, 90, 100), stream=None,
+                static=False):
+        """dict: count_edge, count_non, mean_edge, mean_non, snr, pct_edge, pct_non.
+        static=True: through huge_eval_summary_static (the library's own
+        device scratch, no workspace)."""
         import torch
         if int(n_edge) < 0 or int(n_non) < 0 or dist.numel() < int(n_edge) + int(n_non):
             raise ValueError(f"Evaluator.summary: {dist.numel()} distances for "
@@ -537,10 +543,15 @@ class Evaluator:
         q = (ctypes.c_double * len(quantiles))(*[float(x) for x in quantiles])
         nq = len(quantiles)
         out = torch.empty(5 + 2 * nq, dtype=torch.float64, device=self.device)
-        _ok(load().huge_eval_summary(_arg(dist, ("float32",), "Evaluator.summary dist"),
-                                     int(n_edge), int(n_non), q, nq, _dptr(out),
-                                     self._ws_ptr, self.ws_bytes, _stream_ptr(stream)),
-            "huge_eval_summary")
+        if static:
+            _ok(load().huge_eval_summary_static(
+                _arg(dist, ("float32",), "Evaluator.summary dist"), int(n_edge), int(n_non), q,
+                nq, _dptr(out), _stream_ptr(stream)), "huge_eval_summary_static")
+        else:
+            _ok(load().huge_eval_summary(_arg(dist, ("float32",), "Evaluator.summary dist"),
+                                         int(n_edge), int(n_non), q, nq, _dptr(out),
+                                         self._ws_ptr, self.ws_bytes, _stream_ptr(stream)),
+                "huge_eval_summary")
         o = out.cpu().tolist()
         return {"count_edge": int(o[0]), "count_non": int(o[1]), "mean_edge": o[2],
                 "mean_non": o[3], "snr": o[4], "pct_edge": o[5:5 + nq],

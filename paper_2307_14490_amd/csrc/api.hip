@@ -19,6 +19,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -26,6 +27,11 @@
 #include "common.hpp"
 
 using namespace huge;
+
+// The workspace of huge_eval_summary_static (32 MiB; its use is described
+// where its address is looked up).
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -909,6 +915,88 @@ bool eval_graph_ok(int64_t num_nodes, int64_t num_edges) {
     return num_nodes >= 1 && num_nodes <= 0x7FFFFFFF && num_edges >= 0;
 }
 
+// The workspace of huge_eval_summary_static: a fixed array in device memory,
+// one per device (the runtime creates it on each device when the code object
+// is loaded there; it stays until the process ends), for callers that cannot
+// allocate.  Host code never passes the array's name to a kernel (on the host
+// it is a stand-in, not a device address): the address comes from
+// hipGetSymbolAddress, looked up once per device with that device current.
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+hipError_t static_scratch(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+// The argument checks of the summary (all but the workspace).
+huge_status eval_summary_args(const float* d_dist, int64_t n_edge, int64_t n_non,
+                              const double* h_quantiles, int32_t n_quantiles,
+                              const double* d_out) {
+    if (n_edge < 0 || n_non < 0 || n_edge + n_non > 0x7FFFFFFF || !d_out || n_quantiles < 0 ||
+        n_quantiles > kEvalMaxQuantiles || (n_quantiles > 0 && !h_quantiles) ||
+        (n_edge + n_non > 0 && !d_dist))
+        return HUGE_ERR_INVALID_ARG;
+    for (int32_t i = 0; i < n_quantiles; ++i)
+        if (!(h_quantiles[i] >= 0.0 && h_quantiles[i] <= 100.0)) return HUGE_ERR_INVALID_ARG;
+    return HUGE_OK;
+}
+
+// The summary on a workspace of ws_bytes at d_workspace (launches only).
+huge_status eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non,
+                         const double* h_quantiles, int32_t n_quantiles, double* d_out,
+                         void* d_workspace, size_t ws_bytes, void* stream) {
+    const huge_status st = eval_summary_args(d_dist, n_edge, n_non, h_quantiles, n_quantiles,
+                                             d_out);
+    if (st != HUGE_OK) return st;
+    if (!d_workspace) return HUGE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(d_workspace) % kAlign != 0) return HUGE_ERR_WORKSPACE;
+    const SummaryLayout L = summary_layout(n_edge + n_non);
+    if (ws_bytes < L.total) return HUGE_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
+    Control* ctl = reinterpret_cast<Control*>(ws + L.ctrl);
+    uint32_t* ka = reinterpret_cast<uint32_t*>(ws + L.keys_a);
+    uint32_t* kb = reinterpret_cast<uint32_t*>(ws + L.keys_b);
+    uint32_t* tcount = reinterpret_cast<uint32_t*>(ws + L.tcount);
+    uint32_t* tprefix = reinterpret_cast<uint32_t*>(ws + L.tprefix);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
+    double* part = reinterpret_cast<double*>(ws + L.part);
+    HIP_TRY(launch_begin(ctl, s));
+    HIP_TRY(launch_eval_sums(d_dist, n_edge, n_edge + n_non, part, d_out, s));
+    // each set sorted by its float bit patterns: four stable passes of 8 bits
+    const int64_t first[2] = {0, n_edge};
+    const int64_t count[2] = {n_edge, n_non};
+    for (int set = 0; set < 2; ++set) {
+        const int64_t m = count[set];
+        HIP_TRY(launch_eval_keys(d_dist + first[set], m, ka, s));
+        for (int pass = 0; pass < 4; ++pass) {
+            uint32_t* src = pass % 2 == 0 ? ka : kb;
+            uint32_t* dst = pass % 2 == 0 ? kb : ka;
+            HIP_TRY(launch_tile_count(ctl, src, m, 8, 8 * pass, tcount, s));
+            HIP_TRY(launch_tile_scan(ctl, tcount, m, 8, tprefix, hist, s));
+            HIP_TRY(launch_radix_pass(ctl, src, dst, nullptr, m, 8, 8 * pass, hist, tprefix,
+                                      nullptr, s));
+        }
+        HIP_TRY(launch_eval_quantiles(ka, d_out + set, h_quantiles, n_quantiles,
+                                      d_out + 5 + set * n_quantiles, s));
+    }
+    return HUGE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -953,44 +1041,21 @@ huge_status huge_eval_distances(const float* d_table, int64_t num_rows, int32_t 
 huge_status huge_eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non,
                               const double* h_quantiles, int32_t n_quantiles, double* d_out,
                               void* d_workspace, size_t ws_bytes, void* stream) {
-    if (n_edge < 0 || n_non < 0 || n_edge + n_non > 0x7FFFFFFF || !d_out || !d_workspace ||
-        n_quantiles < 0 || n_quantiles > kEvalMaxQuantiles || (n_quantiles > 0 && !h_quantiles) ||
-        (n_edge + n_non > 0 && !d_dist))
-        return HUGE_ERR_INVALID_ARG;
-    for (int32_t i = 0; i < n_quantiles; ++i)
-        if (!(h_quantiles[i] >= 0.0 && h_quantiles[i] <= 100.0)) return HUGE_ERR_INVALID_ARG;
-    if (reinterpret_cast<uintptr_t>(d_workspace) % kAlign != 0) return HUGE_ERR_WORKSPACE;
-    const SummaryLayout L = summary_layout(n_edge + n_non);
-    if (ws_bytes < L.total) return HUGE_ERR_WORKSPACE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
-    Control* ctl = reinterpret_cast<Control*>(ws + L.ctrl);
-    uint32_t* ka = reinterpret_cast<uint32_t*>(ws + L.keys_a);
-    uint32_t* kb = reinterpret_cast<uint32_t*>(ws + L.keys_b);
-    uint32_t* tcount = reinterpret_cast<uint32_t*>(ws + L.tcount);
-    uint32_t* tprefix = reinterpret_cast<uint32_t*>(ws + L.tprefix);
-    uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
-    double* part = reinterpret_cast<double*>(ws + L.part);
-    HIP_TRY(launch_begin(ctl, s));
-    HIP_TRY(launch_eval_sums(d_dist, n_edge, n_edge + n_non, part, d_out, s));
-    // each set sorted by its float bit patterns: four stable passes of 8 bits
-    const int64_t first[2] = {0, n_edge};
-    const int64_t count[2] = {n_edge, n_non};
-    for (int set = 0; set < 2; ++set) {
-        const int64_t m = count[set];
-        HIP_TRY(launch_eval_keys(d_dist + first[set], m, ka, s));
-        for (int pass = 0; pass < 4; ++pass) {
-            uint32_t* src = pass % 2 == 0 ? ka : kb;
-            uint32_t* dst = pass % 2 == 0 ? kb : ka;
-            HIP_TRY(launch_tile_count(ctl, src, m, 8, 8 * pass, tcount, s));
-            HIP_TRY(launch_tile_scan(ctl, tcount, m, 8, tprefix, hist, s));
-            HIP_TRY(launch_radix_pass(ctl, src, dst, nullptr, m, 8, 8 * pass, hist, tprefix,
-                                      nullptr, s));
-        }
-        HIP_TRY(launch_eval_quantiles(ka, d_out + set, h_quantiles, n_quantiles,
-                                      d_out + 5 + set * n_quantiles, s));
-    }
-    return HUGE_OK;
+    return eval_summary(d_dist, n_edge, n_non, h_quantiles, n_quantiles, d_out, d_workspace,
+                        ws_bytes, stream);
+}
+
+huge_status huge_eval_summary_static(const float* d_dist, int64_t n_edge, int64_t n_non,
+                                     const double* h_quantiles, int32_t n_quantiles,
+                                     double* d_out, void* stream) {
+    const huge_status st = eval_summary_args(d_dist, n_edge, n_non, h_quantiles, n_quantiles,
+                                             d_out);
+    if (st != HUGE_OK) return st;
+    if (summary_layout(n_edge + n_non).total > kStaticScratchBytes) return HUGE_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if (static_scratch(&ws) != hipSuccess) return HUGE_ERR_HIP;
+    return eval_summary(d_dist, n_edge, n_non, h_quantiles, n_quantiles, d_out, ws,
+                        kStaticScratchBytes, stream);
 }
 
 huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
