@@ -309,76 +309,84 @@ def bench_eval(args):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
 
-    # ---- medium: the whole evaluation on a trained table
-    wl = make_workload("medium", args.seed)
-    cfg = wl.cfg
-    N, D = cfg.num_nodes, cfg.dim
-    off0, nbr0 = wl.csr
-    a = relabel(np.repeat(np.arange(N), np.diff(off0)), N, wl.perm)
-    b = relabel(np.asarray(nbr0, np.int64), N, wl.perm)
-    order = np.lexsort((b, a))
-    a, b = a[order], b[order]
-    off = np.zeros(N + 1, np.int64)
-    np.add.at(off, a + 1, 1)
-    off = np.cumsum(off)
-    doff = torch.from_numpy(off).cuda()
-    dnbr = torch.from_numpy(b.astype(np.int32)).cuda()
-    tr = P.Trainer(N, D, cfg.num_neg, cfg.batch, seed=args.seed,
-                   alias_weights=wl.weights if cfg.neg_kind == "alias" else None)
-    # epochs of triples from the GPU walk sampler (a walk of the workload's
-    # length and window from every node, new walks each epoch), shuffled on
-    # the device
-    epochs = 8
-    train_steps = 0
-    pos = 0
-    g = torch.Generator(device="cuda")
-    g.manual_seed(args.seed)
-    for ep in range(epochs):
-        ts, td, tc, _ = P.sample_walks(doff, dnbr, N, 1, cfg.walk_steps, cfg.window, False,
-                                       args.seed + ep, with_hist=False)
-        perm = torch.randperm(ts.numel(), device="cuda", generator=g)
-        ts, td, tc = ts[perm].contiguous(), td[perm].contiguous(), tc[perm].contiguous()
-        for i0 in range(0, ts.numel(), cfg.batch):
-            i1 = min(i0 + cfg.batch, ts.numel())
-            tr.step_no_loss(ts[i0:i1], td[i0:i1], tc[i0:i1], pos, cfg.lr)
-            pos += i1 - i0
-            train_steps += 1
-        del ts, td, tc, perm
-    if tr.check() != 0:
-        raise RuntimeError("device reported an error while training")
-    log(f"[bench] medium: {N} nodes, {b.size} directed edges, trained {epochs} epochs of "
-        f"walk triples ({pos} positives, {train_steps} steps)")
-    ne = nn = 1_000_000
+    def medium_evaluation():
+        """The whole evaluation on the medium table, trained from GPU-sampled
+        walks; returns its figures."""
+        wl = make_workload("medium", args.seed)
+        cfg = wl.cfg
+        N, D = cfg.num_nodes, cfg.dim
+        off0, nbr0 = wl.csr
+        a = relabel(np.repeat(np.arange(N), np.diff(off0)), N, wl.perm)
+        b = relabel(np.asarray(nbr0, np.int64), N, wl.perm)
+        order = np.lexsort((b, a))
+        a, b = a[order], b[order]
+        off = np.zeros(N + 1, np.int64)
+        np.add.at(off, a + 1, 1)
+        off = np.cumsum(off)
+        doff = torch.from_numpy(off).cuda()
+        dnbr = torch.from_numpy(b.astype(np.int32)).cuda()
+        tr = P.Trainer(N, D, cfg.num_neg, cfg.batch, seed=args.seed,
+                       alias_weights=wl.weights if cfg.neg_kind == "alias" else None)
+        # epochs of triples from the GPU walk sampler (a walk of the workload's
+        # length and window from every node, new walks each epoch), shuffled on
+        # the device
+        epochs = 8
+        train_steps = 0
+        pos = 0
+        g = torch.Generator(device="cuda")
+        g.manual_seed(args.seed)
+        for ep in range(epochs):
+            ts, td, tc, _ = P.sample_walks(doff, dnbr, N, 1, cfg.walk_steps, cfg.window, False,
+                                           args.seed + ep, with_hist=False)
+            perm = torch.randperm(ts.numel(), device="cuda", generator=g)
+            ts, td, tc = ts[perm].contiguous(), td[perm].contiguous(), tc[perm].contiguous()
+            for i0 in range(0, ts.numel(), cfg.batch):
+                i1 = min(i0 + cfg.batch, ts.numel())
+                tr.step_no_loss(ts[i0:i1], td[i0:i1], tc[i0:i1], pos, cfg.lr)
+                pos += i1 - i0
+                train_steps += 1
+            del ts, td, tc, perm
+        if tr.check() != 0:
+            raise RuntimeError("device reported an error while training")
+        log(f"[bench] medium: {N} nodes, {b.size} directed edges, trained {epochs} epochs of "
+            f"walk triples ({pos} positives, {train_steps} steps)")
+        ne = nn = 1_000_000
+        nq, k = 100, 10
+        ev = P.Evaluator(N, D, ne + nn, k=k)
+        qs = torch.from_numpy(np.random.default_rng(args.seed).choice(N, nq, replace=False)
+                              .astype(np.int32)).cuda()
+        reps = 5
+        t_pairs = timed(lambda: ev.pairs(doff, dnbr, N, args.seed, ne, nn), reps)
+        u, v = ev.pairs(doff, dnbr, N, args.seed, ne, nn)
+        t_dist = timed(lambda: ev.distances(tr.S, u, v), reps)
+        dist = ev.distances(tr.S, u, v)
+        quant = list(range(0, 101, 10))
+        t_sum = timed(lambda: ev.summary(dist, ne, nn, quant), reps)
+        summ = ev.summary(dist, ne, nn, quant)
+        t_knn_m = timed(lambda: ev.knn(tr.S, qs, k), reps)
+        ids, _ = ev.knn(tr.S, qs, k)
+        t_rec = timed(lambda: ev.recall(doff, dnbr, N, qs, ids), reps)
+        rec = ev.recall(doff, dnbr, N, qs, ids)
+        medium = {"num_nodes": N, "dim": D, "edges": int(b.size), "trained_steps": train_steps,
+                  "trained_positives": pos,
+                  "pairs": ne + nn, "queries": nq, "k": k,
+                  "ms": {"pairs": t_pairs, "distances": t_dist, "summary": t_sum, "knn": t_knn_m,
+                         "recall": t_rec},
+                  "snr": summ["snr"], "mean_edge": summ["mean_edge"],
+                  "mean_non": summ["mean_non"], "pct_edge": summ["pct_edge"],
+                  "pct_non": summ["pct_non"], "percentiles": quant,
+                  "recall_at_10_mean": float(rec.mean().item()),
+                  "distances_GBps": (ne + nn) * 2 * 4 * D / (t_dist * 1e-3) / 1e9}
+        log(f"[bench] medium evaluation: SNR {summ['snr']:.3f}, recall@10 "
+            f"{medium['recall_at_10_mean']:.3f}; ms {medium['ms']}")
+        del tr, ev, u, v, dist
+        torch.cuda.empty_cache()
+        return medium
+
+    # ---- medium: the whole evaluation on a trained table (skipped with
+    # --knn-only, which times the large search alone)
     nq, k = 100, 10
-    ev = P.Evaluator(N, D, ne + nn, k=k)
-    qs = torch.from_numpy(np.random.default_rng(args.seed).choice(N, nq, replace=False)
-                          .astype(np.int32)).cuda()
-    reps = 5
-    t_pairs = timed(lambda: ev.pairs(doff, dnbr, N, args.seed, ne, nn), reps)
-    u, v = ev.pairs(doff, dnbr, N, args.seed, ne, nn)
-    t_dist = timed(lambda: ev.distances(tr.S, u, v), reps)
-    dist = ev.distances(tr.S, u, v)
-    quant = list(range(0, 101, 10))
-    t_sum = timed(lambda: ev.summary(dist, ne, nn, quant), reps)
-    summ = ev.summary(dist, ne, nn, quant)
-    t_knn_m = timed(lambda: ev.knn(tr.S, qs, k), reps)
-    ids, _ = ev.knn(tr.S, qs, k)
-    t_rec = timed(lambda: ev.recall(doff, dnbr, N, qs, ids), reps)
-    rec = ev.recall(doff, dnbr, N, qs, ids)
-    medium = {"num_nodes": N, "dim": D, "edges": int(b.size), "trained_steps": train_steps,
-              "trained_positives": pos,
-              "pairs": ne + nn, "queries": nq, "k": k,
-              "ms": {"pairs": t_pairs, "distances": t_dist, "summary": t_sum, "knn": t_knn_m,
-                     "recall": t_rec},
-              "snr": summ["snr"], "mean_edge": summ["mean_edge"],
-              "mean_non": summ["mean_non"], "pct_edge": summ["pct_edge"],
-              "pct_non": summ["pct_non"], "percentiles": quant,
-              "recall_at_10_mean": float(rec.mean().item()),
-              "distances_GBps": (ne + nn) * 2 * 4 * D / (t_dist * 1e-3) / 1e9}
-    log(f"[bench] medium evaluation: SNR {summ['snr']:.3f}, recall@10 "
-        f"{medium['recall_at_10_mean']:.3f}; ms {medium['ms']}")
-    del tr, ev, u, v, dist
-    torch.cuda.empty_cache()
+    medium = None if args.knn_only else medium_evaluation()
 
     # ---- SBM-100M table: the 100-query nearest-row search
     big = make_workload("sbm100m", args.seed).cfg
@@ -487,6 +495,8 @@ def main():
     ap.add_argument("--eval", action="store_true",
                     help="time the embedding evaluation (Sec. 4: SNR, percentiles, recall) "
                          "instead of the training step")
+    ap.add_argument("--knn-only", action="store_true",
+                    help="with --eval: only the 100-query search over the SBM-100M table")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

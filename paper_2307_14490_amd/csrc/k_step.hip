@@ -610,7 +610,8 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
 //           longer run stores its sum as partial z of its combine record
 //           {key, first partial, partials, first slot}, and the workgroup
 //           that stores the record's last partial (an arrival counter after
-//           a device-scope fence) adds the partials in piece order and
+//           a device-scope release by the storing wave; an acquire before
+//           the partials are read) adds the partials in piece order and
 //           updates the row once.
 // The record counts were set by the grouping of this batch.
 // Exclusive sum of one value per thread over the workgroup; *total receives
@@ -775,12 +776,15 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
             continue;  // uniform
         }
         if (grp == 0) PartIO<G, C>::store(f.part, (int64_t)cb.y + z, D, lane, acc);
-        __threadfence();
-        __syncthreads();
-        if (threadIdx.x == 0) s_flag = atomicAdd(&f.ccount[ci], 1u) == cb.z - 1u ? 1u : 0u;
+        // the partial is wave 0's (a group has at most 64 lanes): wave 0
+        // alone releases it before its arrival is counted
+        if (threadIdx.x < 64) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            if (threadIdx.x == 0) s_flag = atomicAdd(&f.ccount[ci], 1u) == cb.z - 1u ? 1u : 0u;
+        }
         __syncthreads();
         if (s_flag) {  // uniform: the last piece of the row
-            __threadfence();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             coop_sum<G, C>(acc, static_cast<const double*>(f.part), cb.y, cb.z, D, grp, lane,
                            s_part);
             if (grp == 0) apply_row<G, C, E>(t, cb.x, acc, f.lr, lane);
