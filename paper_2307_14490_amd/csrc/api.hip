@@ -52,6 +52,7 @@ struct PendingBatch {
     uint64_t first_pos = 0;
     hipStream_t gstream = nullptr;  // the stream of its huge_prepare_step
     int prof = -1;               // index of its profile events, or -1
+    int bits = kMinDigitBits;    // digit width of its radix pass (buckets 2^bits)
 };
 
 }  // namespace
@@ -65,7 +66,6 @@ struct huge_handle {
     uint8_t* ws;
     size_t ws_bytes;
     Layout lay;
-    SortPlan plan;  // digit width of the radix pass for keys below 2N
     int key_bits;   // bits of 2N - 1
     int64_t prepared;          // batches prepared
     int64_t applied;           // applies issued
@@ -253,7 +253,6 @@ huge_status create(const huge_config* cfg, void* S, void* T, const uint32_t* thr
     h->ws_bytes = ws_bytes;
     h->lay = L;
     h->key_bits = key_bits(cfg->num_nodes);
-    h->plan = sort_plan(h->key_bits);
     h->prepared = h->applied = 0;
     h->last_applied_slot = -1;
     for (int s = 0; s < kSlots; ++s) h->ready[s] = h->done[s] = nullptr;
@@ -369,7 +368,8 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
                           sorted ? at<uint32_t>(h, SL.keys0) : nullptr, s));
     if (sorted) {
         const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-        const int bits = h->plan.bits;
+        const int bits = batch_digit_bits(h->key_bits, m);
+        b.bits = bits;
         HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, bits, 0,
                                   at<uint32_t>(h, SL.tcount), s));
         HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, bits,
@@ -434,7 +434,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         f.bcount = at<uint4>(h, SL.bcount);
         // an empty batch is not grouped: its slot's bucket counts are not
         // this batch's, so no bucket is read
-        f.bins = m > 0 ? 1 << h->plan.bits : 0;
+        f.bins = m > 0 ? 1 << b.bits : 0;
         f.m = m;
         f.shorts = at<uint4>(h, SL.shorts);
         f.pieces = at<uint4>(h, SL.pieces);
@@ -775,7 +775,7 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
         HIP_TRY(hipStreamWaitEvent(s, h->done[slot], 0));
         const int64_t m = h->pending[slot].n * (2 + (int64_t)h->cfg.num_neg_per_pos);
         // k_group writes the counts of every bucket when the batch is not empty
-        const int64_t buckets = m > 0 ? ((int64_t)1 << h->plan.bits) : 0;
+        const int64_t buckets = m > 0 ? ((int64_t)1 << h->pending[slot].bits) : 0;
         std::vector<uint32_t> w((size_t)buckets * 3);
         if (buckets > 0)
             HIP_TRY(hipMemcpyAsync(w.data(), h->ws + h->lay.slot[slot].wstats,

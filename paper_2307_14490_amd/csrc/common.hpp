@@ -164,18 +164,21 @@ inline ListCaps list_caps(int64_t M) {
             (uint32_t)(M / kCombDiv + 1), (uint32_t)(M / kPartDiv + 1)};
 }
 
-// Bucketing of keys below 2^key_bits: one radix pass on the lowest digit, as
-// wide as the keys allow within kMinDigitBits..kMaxDigitBits; the grouping of
-// each bucket resolves the remaining key_bits - bits bits.
-struct SortPlan {
-    int passes;
-    int bits;
-};
-
-inline SortPlan sort_plan(int key_bits) {
-    int bits = key_bits < kMaxDigitBits ? key_bits : kMaxDigitBits;
-    if (bits < kMinDigitBits) bits = kMinDigitBits;
-    return {1, bits};
+// Bucketing of keys below 2^key_bits: one radix pass on the lowest digit;
+// the grouping of each bucket resolves the remaining key_bits - bits bits.
+// Digit width of a batch of m keys below 2^key_bits: the narrowest width in
+// kMinDigitBits..kMaxDigitBits whose buckets hold about kBucketTarget keys on
+// average (a grouping workgroup's fixed work per bucket is then spread over
+// as many keys as in a large batch), but no narrower than leaves the bits
+// above the digit within the grouping's bitmap (kBitmapBits) where the key
+// width allows.
+constexpr int64_t kBucketTarget = 2048;
+inline int batch_digit_bits(int key_bits, int64_t m) {
+    int bits = kMinDigitBits;
+    while (bits < kMaxDigitBits && (m >> bits) > kBucketTarget) ++bits;
+    int floor_bits = key_bits - kBitmapBits;
+    if (floor_bits > kMaxDigitBits) floor_bits = kMaxDigitBits;
+    return bits > floor_bits ? bits : floor_bits;
 }
 
 // Element type of the tables (the public HUGE_DTYPE_* values).
