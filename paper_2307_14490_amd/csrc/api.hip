@@ -135,7 +135,11 @@ Layout make_layout(const huge_config* c) {
     const bool sorted = c->scatter_kind == HUGE_SCATTER_SORTED;
     const ListCaps caps = list_caps(M);
     L.max_occ = M;
-    L.sort_tiles = (M + kSortTile - 1) / kSortTile;
+    // radix tiles: the keys of one sampler workgroup each (at most
+    // kSampleTiles of them until a tile reaches kSortTile keys)
+    const int64_t pmax = sample_tile_positives(K, INT64_MAX / 2);
+    L.sort_tiles = (nb + pmax - 1) / pmax;
+    if (L.sort_tiles < kSampleTiles) L.sort_tiles = kSampleTiles;
     L.loss_blocks = nb + 1;  // at most one workgroup per positive
     L.cap_short = caps.shorts;
     L.cap_piece = caps.pieces;
@@ -364,19 +368,21 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
     if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
     HIP_TRY(launch_begin(ctl, s));
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
+    const int64_t S = 2 + (int64_t)h->cfg.num_neg_per_pos;
+    const int64_t m = n * S;
+    // the sampler's workgroups write the radix tiles' digit counts
+    const int bits = batch_digit_bits(h->key_bits, m);
+    const int64_t tile = sample_tile_positives(S - 2, n) * S;
+    b.bits = bits;
     HIP_TRY(launch_sample(t, ctl, a, sorted ? nullptr : at<int32_t>(h, SL.neg),
-                          sorted ? at<uint32_t>(h, SL.keys0) : nullptr, s));
+                          sorted ? at<uint32_t>(h, SL.keys0) : nullptr,
+                          sorted ? at<uint32_t>(h, SL.tcount) : nullptr, bits, s));
     if (sorted) {
-        const int64_t m = n * (2 + (int64_t)h->cfg.num_neg_per_pos);
-        const int bits = batch_digit_bits(h->key_bits, m);
-        b.bits = bits;
-        HIP_TRY(launch_tile_count(ctl, at<uint32_t>(h, SL.keys0), m, bits, 0,
-                                  at<uint32_t>(h, SL.tcount), s));
-        HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, bits,
+        HIP_TRY(launch_tile_scan(ctl, at<uint32_t>(h, SL.tcount), m, tile, bits,
                                  at<uint32_t>(h, SL.tprefix), hist, s));
         if (!prof_mark(h, b, 1, s) || !prof_mark(h, b, 2, s)) return HUGE_ERR_HIP;
         HIP_TRY(launch_radix_pass(ctl, at<uint32_t>(h, SL.keys0), at<uint32_t>(h, SL.keys1),
-                                  at<uint32_t>(h, SL.vals1), m, bits, 0, hist,
+                                  at<uint32_t>(h, SL.vals1), m, tile, bits, 0, hist,
                                   at<uint32_t>(h, SL.tprefix), at<uint32_t>(h, SL.bstart), s));
         if (!prof_mark(h, b, 3, s) || !prof_mark(h, b, 4, s)) return HUGE_ERR_HIP;
         const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
@@ -658,7 +664,7 @@ huge_status huge_sample_negatives(huge_handle* h, int64_t n, uint64_t first_pos_
     hipStream_t s = static_cast<hipStream_t>(stream);
     StepArgs a{nullptr, nullptr, nullptr, n, first_pos_index, 0.0f, nullptr};
     HIP_TRY(launch_sample(table_args(h), at<Control>(h, h->lay.eval_ctrl), a, d_neg_out, nullptr,
-                          s));
+                          nullptr, 0, s));
     return HUGE_OK;
 }
 
@@ -987,9 +993,9 @@ huge_status eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non,
             uint32_t* src = pass % 2 == 0 ? ka : kb;
             uint32_t* dst = pass % 2 == 0 ? kb : ka;
             HIP_TRY(launch_tile_count(ctl, src, m, 8, 8 * pass, tcount, s));
-            HIP_TRY(launch_tile_scan(ctl, tcount, m, 8, tprefix, hist, s));
-            HIP_TRY(launch_radix_pass(ctl, src, dst, nullptr, m, 8, 8 * pass, hist, tprefix,
-                                      nullptr, s));
+            HIP_TRY(launch_tile_scan(ctl, tcount, m, kSortTile, 8, tprefix, hist, s));
+            HIP_TRY(launch_radix_pass(ctl, src, dst, nullptr, m, kSortTile, 8, 8 * pass, hist,
+                                      tprefix, nullptr, s));
         }
         HIP_TRY(launch_eval_quantiles(ka, d_out + set, h_quantiles, n_quantiles,
                                       d_out + 5 + set * n_quantiles, s));

@@ -263,21 +263,34 @@ hipError_t launch_init(const TableArgs& t, float half_width, hipStream_t s);
 hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, const int64_t* ids,
                            int64_t n, float* out, hipStream_t s);
 hipError_t launch_begin(Control* ctl, hipStream_t s);
+// Positives per sampler workgroup when it writes sort keys for a batch of n
+// positives: its keys, (2 + K) per positive, are one radix tile.  A batch
+// gets about kSampleTiles workgroups (one per CU) until a tile reaches
+// kSortTile keys.
+constexpr int64_t kSampleTiles = 256;
+inline int64_t sample_tile_positives(int64_t K, int64_t n) {
+    const int64_t pmax = kSortTile / (2 + K);
+    int64_t p = (n + kSampleTiles - 1) / kSampleTiles;
+    if (p < 1) p = 1;
+    return p < pmax ? p : pmax;
+}
 // Validation, negatives into neg (if not null) and, with keys, the sort key
-// of every occurrence.
+// of every occurrence and the counts of their lowest `bits` bits per
+// workgroup into tcount[workgroup * 2^bits + digit]: a workgroup takes
+// sample_tile_positives(K, n) positives then, else kSamplePos.
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, hipStream_t s);
-// Bucketing of m keys by `bits` bits at `shift` in tiles of kSortTile:
-// per-tile digit counts, their sums over earlier tiles and the bucket sizes
-// (hist), then the stable scatter into bucket order (one pass of an LSD
-// radix sort); bstart (if not null) receives the first position of each
-// bucket.
+                         uint32_t* keys, uint32_t* tcount, int bits, hipStream_t s);
+// Bucketing of m keys by `bits` bits at `shift` in tiles of `tile` keys
+// (at most kSortTile): per-tile digit counts, their sums over earlier tiles
+// and the bucket sizes (hist), then the stable scatter into bucket order (one
+// pass of an LSD radix sort); bstart (if not null) receives the first
+// position of each bucket.
 hipError_t launch_tile_count(Control* ctl, const uint32_t* keys, int64_t m, int bits, int shift,
                              uint32_t* tcount, hipStream_t s);
-hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int bits,
-                            uint32_t* tprefix, uint32_t* hist, hipStream_t s);
+hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int64_t tile,
+                            int bits, uint32_t* tprefix, uint32_t* hist, hipStream_t s);
 hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
-                             uint32_t* vals_out, int64_t m, int bits, int shift,
+                             uint32_t* vals_out, int64_t m, int64_t tile, int bits, int shift,
                              const uint32_t* hist, const uint32_t* tprefix, uint32_t* bstart,
                              hipStream_t s);
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,

@@ -5,9 +5,11 @@
 //
 // Occurrence o = i (2 + K) + slot of positive i carries key N + src (slot 0,
 // source table) or the context row id (destination, negatives).
-//   1. k_tile_count, k_tile_scan: the occurrences of each digit (lowest 8-10
-//      key bits) per tile of kSortTile occurrences, their sums over earlier
-//      tiles, and the bucket sizes;
+//   1. the occurrences of each digit (lowest 8-10 key bits) per tile -- for
+//      the step, counted by the sampler as it writes the keys, a tile being
+//      one sampler workgroup's keys (at most kSortTile); elsewhere by
+//      k_tile_count over tiles of kSortTile -- then k_tile_scan: their sums
+//      over earlier tiles, and the bucket sizes;
 //   2. k_radix_pass: one stable scatter of the occurrences into bucket
 //      (digit) order, each bucket in occurrence order; no tile waits for
 //      another;
@@ -153,9 +155,10 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_tile_scan(const Control*
     }
 }
 
-hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int bits,
-                            uint32_t* tprefix, uint32_t* hist, hipStream_t s) {
-    const int64_t tiles = (m + kSortTile - 1) / kSortTile;
+hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int64_t tile,
+                            int bits, uint32_t* tprefix, uint32_t* hist, hipStream_t s) {
+    if (tile < 1 || tile > kSortTile) return hipErrorInvalidValue;
+    const int64_t tiles = (m + tile - 1) / tile;
     if (tiles == 0) return hipSuccess;
     if (bits < kMinDigitBits || bits > kMaxDigitBits) return hipErrorInvalidValue;
     static_assert((1 << kMinDigitBits) % kScanDigits == 0, "whole digit groups");
@@ -165,9 +168,9 @@ hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int
 }
 
 // ---------------------------------------------------------------------------
-// Stable scatter by BITS bits at `shift` over a tile of kSortTile
-// consecutive items; wave w owns items [w * 2048, (w + 1) * 2048) of the tile
-// in rounds of 64.
+// Stable scatter by BITS bits at `shift` over a tile of tile_keys <=
+// kSortTile consecutive items; wave w owns the w-th quarter of the tile's
+// items, in rounds of 64.
 //   count: lanes of a round holding the same digit are found with BITS
 //          ballots; the lowest of them adds the round's count to the wave's
 //          LDS counter of that digit (one writer per digit and round);
@@ -185,13 +188,11 @@ hipError_t launch_tile_scan(Control* ctl, const uint32_t* tcount, int64_t m, int
 template <int BITS>
 __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_radix_pass(
     Control* __restrict__ ctl, const uint32_t* __restrict__ keys_in,
-    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m, int shift,
-    const uint32_t* __restrict__ hist, const uint32_t* __restrict__ tprefix,
-    uint32_t* __restrict__ bstart) {
+    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t m,
+    int64_t tile_keys, int shift, const uint32_t* __restrict__ hist,
+    const uint32_t* __restrict__ tprefix, uint32_t* __restrict__ bstart) {
     constexpr int kBins = 1 << BITS;
     constexpr int kWaves = kBlock / 64;
-    constexpr int kWaveItems = kSortTile / kWaves;
-    constexpr int kRounds = kWaveItems / 64;
     constexpr int kDpt = kBins / kBlock;  // digits per thread
     static_assert(kDpt >= 1 && kBins % kBlock == 0, "whole digits per thread");
     // dynamic LDS (radix_lds_bytes<BITS>()): with a static size this large
@@ -211,16 +212,19 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_radix_pass(
     const int wave = tid >> 6;
     const int lane = tid & 63;
     const int64_t tile = blockIdx.x;
-    const int64_t tile_base = tile * kSortTile;
-    const int64_t valid_n = (m - tile_base) < kSortTile ? (m - tile_base) : kSortTile;
-    const int wbase = wave * kWaveItems;
+    const int64_t tile_base = tile * tile_keys;  // tile_keys <= kSortTile
+    const int64_t valid_n = (m - tile_base) < tile_keys ? (m - tile_base) : tile_keys;
+    // wave w owns the w-th quarter of the tile (a multiple of 64 items), in
+    // order, so the scatter stays stable
+    const int rounds = (int)((valid_n + kWaves * 64 - 1) / (kWaves * 64));
+    const int wbase = wave * rounds * 64;
 
     for (int j = tid; j < kWaves * kBins; j += kBlock) (&s_wave[0][0])[j] = 0u;
     for (int p = tid; p < valid_n; p += kBlock) s_in[p] = keys_in[tile_base + p];
     __syncthreads();
 
     // count
-    for (int r = 0; r < kRounds; ++r) {
+    for (int r = 0; r < rounds; ++r) {
         const int p = wbase + r * 64 + lane;
         const bool valid = p < valid_n;
         const uint32_t dg = valid ? (s_in[p] >> shift) & (kBins - 1) : 0u;
@@ -260,7 +264,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_radix_pass(
     __syncthreads();
 
     // place
-    for (int r = 0; r < kRounds; ++r) {
+    for (int r = 0; r < rounds; ++r) {
         const int p = wbase + r * 64 + lane;
         const bool valid = p < valid_n;
         const uint32_t key = valid ? s_in[p] : 0u;
@@ -300,9 +304,9 @@ constexpr size_t radix_lds_bytes() {
 
 template <int BITS>
 hipError_t launch_radix_bits(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
-                             uint32_t* vals_out, int64_t m, int shift, const uint32_t* hist,
-                             const uint32_t* tprefix, uint32_t* bstart, int64_t tiles,
-                             hipStream_t s) {
+                             uint32_t* vals_out, int64_t m, int64_t tile, int shift,
+                             const uint32_t* hist, const uint32_t* tprefix, uint32_t* bstart,
+                             int64_t tiles, hipStream_t s) {
     // LDS beyond 64 KB is asked for explicitly, once per variant
     static bool lds_set = false;
     if (!lds_set) {
@@ -313,21 +317,22 @@ hipError_t launch_radix_bits(Control* ctl, const uint32_t* keys_in, uint32_t* ke
         lds_set = true;
     }
     hipLaunchKernelGGL(k_radix_pass<BITS>, dim3((unsigned)tiles), dim3(kBlock),
-                       radix_lds_bytes<BITS>(), s, ctl, keys_in, keys_out, vals_out, m, shift,
-                       hist, tprefix, bstart);
+                       radix_lds_bytes<BITS>(), s, ctl, keys_in, keys_out, vals_out, m, tile,
+                       shift, hist, tprefix, bstart);
     return hipGetLastError();
 }
 
 hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* keys_out,
-                             uint32_t* vals_out, int64_t m, int bits, int shift,
+                             uint32_t* vals_out, int64_t m, int64_t tile, int bits, int shift,
                              const uint32_t* hist, const uint32_t* tprefix, uint32_t* bstart,
                              hipStream_t s) {
-    const int64_t tiles = (m + kSortTile - 1) / kSortTile;
+    if (tile < 1 || tile > kSortTile) return hipErrorInvalidValue;
+    const int64_t tiles = (m + tile - 1) / tile;
     if (tiles == 0) return hipSuccess;
     if (shift < 0 || shift > 31) return hipErrorInvalidValue;
 #define HUGE_RADIX_LAUNCH(B)                                                                  \
-    return launch_radix_bits<B>(ctl, keys_in, keys_out, vals_out, m, shift, hist, tprefix,    \
-                                bstart, tiles, s)
+    return launch_radix_bits<B>(ctl, keys_in, keys_out, vals_out, m, tile, shift, hist,       \
+                                tprefix, bstart, tiles, s)
     switch (bits) {
         case 8: HUGE_RADIX_LAUNCH(8);
         case 9: HUGE_RADIX_LAUNCH(9);

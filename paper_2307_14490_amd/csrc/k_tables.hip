@@ -116,26 +116,38 @@ hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s) {
 
 
 // ---------------------------------------------------------------------------
-// Validation, negatives and sort keys.  A workgroup takes kSamplePos
-// consecutive positives.  Positive i has S = 2 + K occurrences at
-// o = i S + slot: slot 0 the source row (key N + src), slot 1 the destination
-// row (key dst), slot 2 + k negative k (key m).
+// Validation, negatives and sort keys.  A workgroup takes P consecutive
+// positives (P = sample_tile_positives(K, n) with keys, else kSamplePos).
+// Positive i has S = 2 + K occurrences at o = i S + slot: slot 0 the source
+// row (key N + src), slot 1 the destination row (key dst), slot 2 + k
+// negative k (key m).
 //   - one thread per positive checks 0 <= src, dst < N and co_count >= 0 (a
 //     failure flags the call) and, with keys, writes keys of slots 0 and 1;
 //   - one thread per negative, consecutive threads on consecutive (i, k), so
 //     that the stores of a wave are contiguous, draws negative k of positive
 //     i into neg[i K + k] (if neg is not null) and, with keys, keys[o] of
 //     slot 2 + k.
+// With keys, the workgroup's P S keys are one tile of the radix pass: their
+// counts per digit (lowest `bits` bits) go to LDS as they are written and
+// then to tcount[workgroup * 2^bits + digit].
 // Without src only negatives are drawn.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_sample(TableArgs t, Control* ctl,
                                                                StepArgs a,
                                                                int32_t* __restrict__ neg,
-                                                               uint32_t* __restrict__ keys) {
+                                                               uint32_t* __restrict__ keys,
+                                                               uint32_t* __restrict__ tcount,
+                                                               int bits, int64_t per_wg) {
+    __shared__ uint32_t s_cnt[kMaxBins];
     const bool with_keys = keys != nullptr;
+    const uint32_t dmask = (1u << bits) - 1u;
+    if (with_keys) {
+        for (int d = threadIdx.x; d < (1 << bits); d += kBlock) s_cnt[d] = 0u;
+        __syncthreads();
+    }
     const int64_t K = t.K, S = 2 + K;
-    const int64_t i0 = (int64_t)blockIdx.x * kSamplePos;
-    const int64_t np = a.n - i0 < kSamplePos ? a.n - i0 : kSamplePos;  // positives here
+    const int64_t i0 = (int64_t)blockIdx.x * per_wg;
+    const int64_t np = a.n - i0 < per_wg ? a.n - i0 : per_wg;  // positives here
     if (a.src != nullptr) {
         for (int64_t j = threadIdx.x; j < np; j += kBlock) {
             const int64_t i = i0 + j;
@@ -147,8 +159,11 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_sample(TableArgs t, Cont
             }
             if (!weight_valid(a, i)) raise_error(ctl, kBadCount);
             if (with_keys) {
-                keys[i * S] = (uint32_t)((uint64_t)t.N + (uint64_t)u);
+                const uint32_t ks = (uint32_t)((uint64_t)t.N + (uint64_t)u);
+                keys[i * S] = ks;
                 keys[i * S + 1] = (uint32_t)v;
+                atomicAdd(&s_cnt[ks & dmask], 1u);
+                atomicAdd(&s_cnt[(uint32_t)v & dmask], 1u);
             }
         }
     }
@@ -163,7 +178,10 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_sample(TableArgs t, Cont
         const int32_t m = draw_negative(t.seed, a.first_pos + (uint64_t)i, k, (uint64_t)t.N,
                                         t.thr, t.alias);
         if (neg != nullptr) neg[i * K + k] = m;
-        if (with_keys) keys[i * S + 2 + k] = (uint32_t)m;
+        if (with_keys) {
+            keys[i * S + 2 + k] = (uint32_t)m;
+            atomicAdd(&s_cnt[(uint32_t)m & dmask], 1u);
+        }
         k += dr;
         q += dq;
         if (k >= Ku) {
@@ -171,14 +189,24 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_sample(TableArgs t, Cont
             ++q;
         }
     }
+    if (with_keys) {
+        __syncthreads();
+        for (int d = threadIdx.x; d < (1 << bits); d += kBlock)
+            tcount[(int64_t)blockIdx.x * (1 << bits) + d] = s_cnt[d];
+    }
 }
 
 hipError_t launch_sample(const TableArgs& t, Control* ctl, const StepArgs& a, int32_t* neg,
-                         uint32_t* keys, hipStream_t s) {
-    const int64_t blocks = (a.n + kSamplePos - 1) / kSamplePos;
-    if (blocks == 0) return hipSuccess;
+                         uint32_t* keys, uint32_t* tcount, int bits, hipStream_t s) {
     if (t.K < 1 || t.K > kBlock) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys);
+    if (keys != nullptr && (tcount == nullptr || bits < kMinDigitBits || bits > kMaxDigitBits))
+        return hipErrorInvalidValue;
+    const int64_t per_wg = keys != nullptr ? sample_tile_positives(t.K, a.n) : kSamplePos;
+    if (per_wg < 1) return hipErrorInvalidValue;
+    const int64_t blocks = (a.n + per_wg - 1) / per_wg;
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_sample, dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, keys,
+                       tcount, keys != nullptr ? bits : kMinDigitBits, per_wg);
     return hipGetLastError();
 }
 
