@@ -256,8 +256,8 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
    spreads that cost.  huge_profile_end waits for all of them on `stream`,
    writes the summed durations in milliseconds to phase_ms[HUGE_PHASES] (0
    for phases not recorded) and the number of recorded steps to *steps, and
-   releases the events.  Phases: 0 set-up, negative sampling, tile counts
-   and prefixes, 1 the radix pass, 2 the per-bucket grouping (1 and 2 are
+   releases the events.  Phases: 0 set-up, negative sampling with the tile
+   digit counts, tile prefixes, 1 the radix pass, 2 the per-bucket grouping (1 and 2 are
    empty for the atomic scatter), 3 the fused gather/loss/update kernel
    (atomic scatter: gather and coefficients), 4 the finish kernel: repeated
    rows and the loss sum (atomic scatter: the atomic adds and the loss sum),

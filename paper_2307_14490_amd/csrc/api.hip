@@ -3,10 +3,10 @@
 //
 // A batch is prepared, then applied.  Preparing (huge_prepare_step, on the
 // caller's preparation stream) validates the batch, draws its negatives and
-// groups its rows: k_begin, k_sample (keys, negatives), k_tile_count and
-// k_tile_scan (digit counts per tile and their prefixes), k_radix_pass
-// (occurrences grouped by the lowest digit of their key) and k_group
-// (repeated rows and their slots).  These read only the batch, and every one
+// groups its rows: k_begin, k_sample (keys, negatives and the digit counts
+// of each radix tile, a tile being one sampler workgroup's keys), k_tile_scan
+// (the counts' prefixes over tiles), k_radix_pass (occurrences grouped by the
+// lowest digits of their key) and k_group (repeated rows and their slots).  These read only the batch, and every one
 // of them runs in 256-thread workgroups of few registers, so that they run
 // beside the previous batch's apply without evicting its waves.  Applying
 // (huge_train_prepared, on the apply stream) runs the fused step and the
