@@ -368,6 +368,7 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
     if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
     HIP_TRY(launch_begin(ctl, s));
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
+    bool ready_recorded = false;
     const int64_t S = 2 + (int64_t)h->cfg.num_neg_per_pos;
     const int64_t m = n * S;
     // the sampler's workgroups write the radix tiles' digit counts
@@ -391,14 +392,16 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
                              at<int32_t>(h, SL.info), at<uint4>(h, SL.shorts),
                              at<uint4>(h, SL.pieces), at<uint4>(h, SL.combs),
                              at<uint32_t>(h, SL.ccount), at<uint4>(h, SL.bcount), caps,
-                             at<uint32_t>(h, SL.wstats), 1 << bits, h->key_bits, s));
+                             at<uint32_t>(h, SL.wstats), 1 << bits, h->key_bits,
+                             h->ready[slot], &ready_recorded, s));
         if (!prof_mark(h, b, 5, s)) return HUGE_ERR_HIP;
     } else {
         // the atomic scatter needs no grouping
         for (int k = 1; k <= 5; ++k)
             if (!prof_mark(h, b, k, s)) return HUGE_ERR_HIP;
     }
-    HIP_TRY(hipEventRecord(h->ready[slot], s));
+    // the grouping kernel's completion records `ready` (no packet of its own)
+    if (!ready_recorded) HIP_TRY(hipEventRecord(h->ready[slot], s));
     h->pending[slot] = b;
     h->prepared += 1;
     return HUGE_OK;
@@ -428,6 +431,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
     }
     if (!prof_mark(h, b, 6, s)) return HUGE_ERR_HIP;
     int64_t blocks = 0;
+    bool done_recorded = false;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
         // the negatives are the sort keys of slots 2 .. K + 1
         const uint32_t stride = 2 + (uint32_t)h->cfg.num_neg_per_pos;
@@ -453,7 +457,10 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         f.lossp = lossp;
         f.loss_blocks = blocks;
         f.loss_out = loss_out;
-        HIP_TRY(launch_finish(t, ctl, f, s));
+        // the finish kernel's completion records `done` (no packet of its
+        // own between it and the next fused kernel)
+        HIP_TRY(launch_finish(t, ctl, f, h->done[slot], s));
+        done_recorded = true;
     } else {
         float* gsrc = at<float>(h, L.gsrc);
         float* coef = at<float>(h, L.coef);
@@ -465,7 +472,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         if (loss_out) HIP_TRY(launch_loss_final(ctl, lossp, blocks, loss_out, s));
     }
     if (!prof_mark(h, b, 8, s) || !prof_mark(h, b, 9, s)) return HUGE_ERR_HIP;
-    HIP_TRY(hipEventRecord(h->done[slot], s));
+    if (!done_recorded) HIP_TRY(hipEventRecord(h->done[slot], s));
     if (b.prof >= 0) h->prof_applied[(size_t)b.prof] = 1;
     h->slot_apply_stream[slot] = s;
     h->last_apply_stream = s;

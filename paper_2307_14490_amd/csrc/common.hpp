@@ -1,6 +1,7 @@
 // Internal declarations shared by the kernels and the host layer of libhuge.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -293,11 +294,13 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* ke
                              uint32_t* vals_out, int64_t m, int64_t tile, int bits, int shift,
                              const uint32_t* hist, const uint32_t* tprefix, uint32_t* bstart,
                              hipStream_t s);
+// stop (if not null) is recorded by the kernel's completion; *launched says
+// whether a kernel was launched (an empty batch launches none).
 hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals, int64_t m,
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
                         uint4* shorts, uint4* pieces, uint4* combs, uint32_t* ccount,
                         uint4* bcount, ListCaps caps, uint32_t* wstats, int bins, int key_bits,
-                        hipStream_t s);
+                        hipEvent_t stop, bool* launched, hipStream_t s);
 // Negative k of positive i: neg[i * neg_stride + k].
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, uint32_t neg_stride, int32_t* info, float* dup,
@@ -322,7 +325,10 @@ struct FinishArgs {
     int64_t loss_blocks;   // how many
     double* loss_out;      // or null: no loss
 };
-hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipStream_t s);
+// stop (if not null) is recorded by the kernel's own completion, not by a
+// separate queue packet.
+hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipEvent_t stop,
+                         hipStream_t s);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_walks(const WalkArgs& A, uint32_t* counts, uint64_t* offsets, int64_t* total,
                         int64_t capacity, int32_t* src, int32_t* dst, int32_t* cc, int32_t* hist,

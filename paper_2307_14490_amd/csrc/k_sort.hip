@@ -835,7 +835,8 @@ hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals
                         int64_t N, const uint32_t* hist, const uint32_t* bstart, int32_t* info,
                         uint4* shorts, uint4* pieces, uint4* combs, uint32_t* ccount,
                         uint4* bcount, ListCaps caps, uint32_t* wstats, int bins, int key_bits,
-                        hipStream_t s) {
+                        hipEvent_t stop, bool* launched, hipStream_t s) {
+    *launched = false;
     if (m == 0) return hipSuccess;
     if (bins < 2 || bins > kMaxBins || (bins & (bins - 1)) != 0) return hipErrorInvalidValue;
     const int shift = __builtin_ctz((unsigned)bins);
@@ -853,17 +854,19 @@ hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals
         lds_set[bm] = true;
     }
     if (bm) {
-        hipLaunchKernelGGL(k_group<true>, dim3((unsigned)bins), dim3(kBlock),
-                           group_lds_words<true>() * sizeof(uint32_t), s, ctl, keys, vals, m, N,
-                           hist, bstart, info, shorts, pieces, combs, ccount, bcount, caps,
-                           wstats, bins, shift, sub_bits);
+        hipExtLaunchKernelGGL(k_group<true>, dim3((unsigned)bins), dim3(kBlock),
+                              group_lds_words<true>() * sizeof(uint32_t), s, nullptr, stop, 0,
+                              ctl, keys, vals, m, N, hist, bstart, info, shorts, pieces, combs,
+                              ccount, bcount, caps, wstats, bins, shift, sub_bits);
     } else {
-        hipLaunchKernelGGL(k_group<false>, dim3((unsigned)bins), dim3(kBlock),
-                           group_lds_words<false>() * sizeof(uint32_t), s, ctl, keys, vals, m, N,
-                           hist, bstart, info, shorts, pieces, combs, ccount, bcount, caps,
-                           wstats, bins, shift, sub_bits);
+        hipExtLaunchKernelGGL(k_group<false>, dim3((unsigned)bins), dim3(kBlock),
+                              group_lds_words<false>() * sizeof(uint32_t), s, nullptr, stop, 0,
+                              ctl, keys, vals, m, N, hist, bstart, info, shorts, pieces, combs,
+                              ccount, bcount, caps, wstats, bins, shift, sub_bits);
     }
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    *launched = e == hipSuccess;
+    return e;
 }
 
 }  // namespace huge

@@ -792,13 +792,14 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
     }
 }
 
-hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipStream_t s) {
+hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipEvent_t stop,
+                         hipStream_t s) {
     const RowShape rs = row_shape(t.D);
     const int64_t grid = 1024;
     HUGE_ROW_DISPATCH(rs, {
         HUGE_ELEM_DISPATCH(t.dtype, {
-            hipLaunchKernelGGL((k_finish<G_, C_, E_>), dim3((unsigned)grid), dim3(kBlock), 0, s, t,
-                               ctl, f);
+            hipExtLaunchKernelGGL((k_finish<G_, C_, E_>), dim3((unsigned)grid), dim3(kBlock), 0, s,
+                                  nullptr, stop, 0, t, ctl, f);
         });
     });
     return hipGetLastError();

@@ -462,6 +462,34 @@ def test_prepared_steps_on_two_streams_equal_train_step_bitwise():
     assert losses.cpu().tolist() == ref_losses
 
 
+def test_prepared_steps_with_long_groupings_equal_train_step_bitwise():
+    """Batches large enough that the grouping of batch k+1 runs beside the
+    update of batch k for a long while: the events that order the two halves
+    (recorded by the grouping and finish kernels' completion) must hold."""
+    N, D, K, n = 200_000, 128, 10, 60_000
+    rng = np.random.default_rng(23)
+    batches = [_random_batch(rng, N, n, hub_frac=0.3, cmax=20) for _ in range(6)]
+    ref = _trainer(N, D, K, n, seed=8)
+    ref_losses = []
+    for b, (s, d, c) in enumerate(batches):
+        ref_losses.append(ref.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n,
+                                   0.02).item())
+    tr = _trainer(N, D, K, n, seed=8)
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    dbs = [tuple(dev(x, torch) for x in b) for b in batches]
+    losses = torch.zeros(len(batches), dtype=torch.float64, device="cuda")
+    tr.prepare(*dbs[0], 0, stream=side)
+    for k in range(len(batches)):
+        if k + 1 < len(batches):
+            tr.prepare(*dbs[k + 1], (k + 1) * n, stream=side)
+        tr.train_prepared(0.02, loss_out=losses[k:k + 1], stream=main)
+    torch.cuda.synchronize()
+    assert tr.check() == 0
+    assert torch.equal(tr.S, ref.S) and torch.equal(tr.T, ref.T)
+    assert losses.cpu().tolist() == ref_losses
+
+
 def test_prepared_call_order_is_checked_on_host():
     tr = _trainer(100, 16, 3, 64)
     rng = np.random.default_rng(3)
