@@ -429,16 +429,21 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         HIP_TRY(wait_on(s, h->side_done, h->side_stream));
         h->side_pending = false;
     }
-    if (!prof_mark(h, b, 6, s)) return HUGE_ERR_HIP;
     int64_t blocks = 0;
     bool done_recorded = false;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
-        // the negatives are the sort keys of slots 2 .. K + 1
+        // the negatives are the sort keys of slots 2 .. K + 1; a profiled
+        // step's fused-kernel events (6, 7) are the kernel's own start and
+        // completion (no packets of their own)
         const uint32_t stride = 2 + (uint32_t)h->cfg.num_neg_per_pos;
+        hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+        if (b.prof >= 0) {
+            ev_start = h->prof_ev[(size_t)b.prof * kProfEvents + 6];
+            ev_stop = h->prof_ev[(size_t)b.prof * kProfEvents + 7];
+        }
         HIP_TRY(launch_fused_step(t, ctl, a, at<int32_t>(h, SL.keys0) + 2, stride,
                                   at<int32_t>(h, SL.info), at<float>(h, L.dup), lossp, &blocks,
-                                  s));
-        if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
+                                  ev_start, ev_stop, s));
         FinishArgs f;
         f.bstart = at<uint32_t>(h, SL.bstart);
         f.bcount = at<uint4>(h, SL.bcount);
@@ -465,6 +470,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         float* gsrc = at<float>(h, L.gsrc);
         float* coef = at<float>(h, L.coef);
         const int32_t* neg = at<int32_t>(h, SL.neg);
+        if (!prof_mark(h, b, 6, s)) return HUGE_ERR_HIP;
         HIP_TRY(launch_atomic_gather(t, ctl, a, neg, gsrc, coef, lossp, &blocks, s));
         if (!prof_mark(h, b, 7, s)) return HUGE_ERR_HIP;
         HIP_TRY(launch_atomic_scatter_T(t, ctl, a, neg, coef, s));

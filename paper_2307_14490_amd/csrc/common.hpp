@@ -302,9 +302,11 @@ hipError_t launch_group(Control* ctl, const uint32_t* keys, const uint32_t* vals
                         uint4* bcount, ListCaps caps, uint32_t* wstats, int bins, int key_bits,
                         hipEvent_t stop, bool* launched, hipStream_t s);
 // Negative k of positive i: neg[i * neg_stride + k].
+// start, stop (if not null): recorded at the kernel's start and completion.
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, uint32_t neg_stride, int32_t* info, float* dup,
-                             double* lossp, int64_t* blocks_out, hipStream_t s);
+                             double* lossp, int64_t* blocks_out, hipEvent_t start,
+                             hipEvent_t stop, hipStream_t s);
 // After the fused step: the repeated rows (short runs, pieces, and rows
 // whose pieces are combined by the last piece to finish) and, with a loss
 // output, the loss sum (the fused step's partials in a fixed order).

@@ -284,7 +284,8 @@ static int64_t fused_step_blocks(const TableArgs& t, int64_t n) {
 
 hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a,
                              const int32_t* neg, uint32_t neg_stride, int32_t* info, float* dup,
-                             double* lossp, int64_t* blocks_out, hipStream_t s) {
+                             double* lossp, int64_t* blocks_out, hipEvent_t start,
+                             hipEvent_t stop, hipStream_t s) {
     const int64_t blocks = fused_step_blocks(t, a.n);
     *blocks_out = blocks;
     if (blocks == 0) return hipSuccess;
@@ -292,10 +293,10 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
         HUGE_PAIR_DISPATCH(pair_shape(t.D), {
             HUGE_NEG_DISPATCH(neg_block(t.K), {
                 HUGE_FULL_DISPATCH(t.K == NB_, {
-                    hipLaunchKernelGGL(
+                    hipExtLaunchKernelGGL(
                         (k_fused_step<G_, NB_, F_, PairIO<G_, U_, bf16_t>, PairIO<G_, U_, float>>),
-                        dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg, neg_stride,
-                        info, dup, lossp);
+                        dim3((unsigned)blocks), dim3(kBlock), 0, s, start, stop, 0, t, ctl, a,
+                        neg, neg_stride, info, dup, lossp);
                 });
             });
         });
@@ -304,10 +305,10 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
             HUGE_NEG_DISPATCH(neg_block(t.K), {
                 HUGE_ELEM_DISPATCH(t.dtype, {
                     HUGE_FULL_DISPATCH(t.K == NB_, {
-                        hipLaunchKernelGGL(
+                        hipExtLaunchKernelGGL(
                             (k_fused_step<G_, NB_, F_, RowIO<G_, C_, E_>, RowIO<G_, C_>>),
-                            dim3((unsigned)blocks), dim3(kBlock), 0, s, t, ctl, a, neg,
-                            neg_stride, info, dup, lossp);
+                            dim3((unsigned)blocks), dim3(kBlock), 0, s, start, stop, 0, t, ctl,
+                            a, neg, neg_stride, info, dup, lossp);
                     });
                 });
             });
