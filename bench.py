@@ -600,9 +600,9 @@ def main():
         raise RuntimeError("device reported an error during warm-up")
     log("[bench] warm-up done")
 
-    # Timed region: exactly K steps; phase events recorded inside the library
-    # around the fused kernel of every PROFILE_EVERY-th step (each event is a
-    # queue packet that costs a few microseconds of its step).
+    # Timed region: exactly K steps; the library records the fused kernel's
+    # start and completion (its launch's own events, no extra queue packets)
+    # on every PROFILE_EVERY-th step.
     if not args.no_phases:
         tr.profile_begin(-(-args.steps // PROFILE_EVERY), every=PROFILE_EVERY)
     torch.cuda.synchronize()
@@ -661,7 +661,7 @@ def main():
     state["pos"] = pos + 3 * n + n_probe * n
     # Phase breakdown from a separate pass of 50 steps with an event at every
     # phase boundary (those events lengthen each step by tens of microseconds,
-    # so the timed steps above record only the two around the fused kernel).
+    # so the timed steps above record only the fused kernel's two).
     n_diag = min(50, args.steps)
     tr.profile_begin(n_diag, all_phases=True)
     run_steps(n_diag, drain=True)
@@ -742,7 +742,8 @@ def main():
             "traffic": traffic,
             "avg_kernel_us": fused_us,
             "timed_launches": prof_steps,
-            "timing": f"HIP events around the fused kernel of every {PROFILE_EVERY}th timed step",
+            "timing": f"HIP events at the fused kernel's start and completion (its launch's "
+                      f"own events) on every {PROFILE_EVERY}th timed step",
             "alg_bytes_per_launch": kernel_bytes,
             "probe": {
                 "achieved": probe_gbps,
