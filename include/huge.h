@@ -412,11 +412,29 @@ huge_status huge_eval_summary_static(const float* d_dist, int64_t n_edge, int64_
    2^-21 of each term, well inside the search's fp32 distance bound); wider
    rows in fp32.  1 <= k <= 32;
    dim <= 512.  Queries are processed in passes of up to
-   128 (dim <= 128), 64 (dim <= 256) or 32 over the table. */
+   128 (dim <= 128), 64 (dim <= 256) or 32 over the table.  For dim <= 128
+   a pass is a series of threshold scans: strided samples of the row tiles,
+   each 64 times denser than the one before, then every tile; a sample's
+   k-th distance bounds the next scan's candidates per query, which are
+   sorted between scans.  Should more than 8192 rows of the last scan fall
+   within a query's bound (many rows at one distance), the pass is computed
+   again by the per-wave lists of huge_eval_knn_lists; the answer is the
+   same either way, bit for bit.  Sizes (Sec. 4's sampled recall): 100
+   queries over 1e8 x 128 rows. */
 huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
                           const int32_t* d_queries, int32_t n_queries, int32_t k,
                           int32_t* d_ids, float* d_dist, void* d_workspace, size_t ws_bytes,
                           int32_t* d_status, void* stream);
+
+/* huge_eval_knn computed by the search it falls back on: every wave keeps
+   sorted lists of its best k per query over its share of the tiles, merged
+   at the end (no distance bound).  The same distances and the same answer;
+   for comparing the two searches.  Arguments, workspace and errors as for
+   huge_eval_knn. */
+huge_status huge_eval_knn_lists(const float* d_table, int64_t num_rows, int32_t dim,
+                                const int32_t* d_queries, int32_t n_queries, int32_t k,
+                                int32_t* d_ids, float* d_dist, void* d_workspace,
+                                size_t ws_bytes, int32_t* d_status, void* stream);
 
 /* d_recall[q] = recall@k of query d_queries[q] (device double) from its k
    nearest rows d_ids[q k ..] (as huge_eval_knn writes them); 1 <= k <= 64. */

@@ -36,7 +36,7 @@ EXPORTED = [
     "huge_destroy", "huge_status_string", "huge_walk_workspace_bytes", "huge_sample_walks",
     "huge_eval_workspace_bytes", "huge_eval_pairs", "huge_eval_distances", "huge_eval_summary",
     "huge_eval_summary_static",
-    "huge_eval_knn", "huge_eval_recall", "huge_train_step_weighted", "huge_prepare_step_weighted",
+    "huge_eval_knn", "huge_eval_knn_lists", "huge_eval_recall", "huge_train_step_weighted", "huge_prepare_step_weighted",
     "huge_eval_loss_weighted", "huge_cocount_weights",
 ]
 HUGE_PHASES = 6
@@ -124,9 +124,10 @@ def load() -> ctypes.CDLL:
     L.huge_eval_summary_static.argtypes = [_vp, i64, i64, ctypes.POINTER(ctypes.c_double), i32,
                                            _vp, _vp]
     L.huge_eval_knn.argtypes = [_vp, i64, i32, _vp, i32, i32, _vp, _vp, _vp, szt, _vp, _vp]
+    L.huge_eval_knn_lists.argtypes = L.huge_eval_knn.argtypes
     L.huge_eval_recall.argtypes = [_vp, _vp, i64, i64, _vp, i32, _vp, i32, _vp, _vp, _vp]
     for name in ("huge_eval_pairs", "huge_eval_distances", "huge_eval_summary", "huge_eval_knn",
-                 "huge_eval_recall"):
+                 "huge_eval_knn_lists", "huge_eval_recall"):
         getattr(L, name).restype = ctypes.c_int32
     L.huge_train_step_weighted.argtypes = [_vp, _vp, _vp, _vp, i64, ctypes.c_uint64,
                                            ctypes.c_float, _vp, _vp]
@@ -557,8 +558,9 @@ class Evaluator:
                 "mean_non": o[3], "snr": o[4], "pct_edge": o[5:5 + nq],
                 "pct_non": o[5 + nq:5 + 2 * nq]}
 
-    def knn(self, table, queries, k=None, stream=None):
-        """(ids int32 [nq, k], dist float32 [nq, k]) of the nearest rows."""
+    def knn(self, table, queries, k=None, stream=None, lists=False):
+        """(ids int32 [nq, k], dist float32 [nq, k]) of the nearest rows
+        (lists=True: by huge_eval_knn_lists, the per-wave list search)."""
         import torch
         k = self.k if k is None else int(k)
         if k > self.k:
@@ -567,12 +569,13 @@ class Evaluator:
         nq = queries.numel()
         ids = torch.empty((nq, k), dtype=torch.int32, device=self.device)
         dist = torch.empty((nq, k), dtype=torch.float32, device=self.device)
-        _ok(load().huge_eval_knn(_arg(table, ("float32",), "Evaluator.knn table"),
-                                 table.shape[0], table.shape[1],
-                                 _arg(queries, ("int32",), "Evaluator.knn queries"),
-                                 nq, k, _dptr(ids), _dptr(dist), self._ws_ptr, self.ws_bytes,
-                                 _dptr(self.status), _stream_ptr(stream)), "huge_eval_knn")
-        self._check("huge_eval_knn")
+        name = "huge_eval_knn_lists" if lists else "huge_eval_knn"
+        _ok(getattr(load(), name)(_arg(table, ("float32",), "Evaluator.knn table"),
+                                  table.shape[0], table.shape[1],
+                                  _arg(queries, ("int32",), "Evaluator.knn queries"),
+                                  nq, k, _dptr(ids), _dptr(dist), self._ws_ptr, self.ws_bytes,
+                                  _dptr(self.status), _stream_ptr(stream)), name)
+        self._check(name)
         return ids, dist
 
     def recall(self, offsets, neighbors, num_nodes, queries, ids, stream=None):

@@ -905,7 +905,7 @@ SummaryLayout summary_layout(int64_t max_pairs) {
 }
 
 struct KnnLayout {
-    size_t qn, qn2, qid, partial, total;
+    size_t qn, qn2, qid, partial, tau, cnt, gate, cand, total;
 };
 
 KnnLayout knn_layout(int64_t num_rows, int32_t dim, int32_t k) {
@@ -922,6 +922,11 @@ KnnLayout knn_layout(int64_t num_rows, int32_t dim, int32_t k) {
     // the most lists: one query block, every wave its own list
     L.partial =
         take(sizeof(uint64_t) * (size_t)knn_lists(num_rows, dim, 1) * kKnnPass * (size_t)k);
+    // the threshold scans' bounds, counts, gate and candidate lists
+    L.tau = take(sizeof(float) * kKnnPass);
+    L.cnt = take(sizeof(uint32_t) * kKnnPass);
+    L.gate = take(sizeof(int32_t));
+    L.cand = take(sizeof(uint64_t) * kKnnPass * (size_t)kKnnCandCap);
     L.total = off;
     return L;
 }
@@ -1016,6 +1021,35 @@ huge_status eval_summary(const float* d_dist, int64_t n_edge, int64_t n_non,
     return HUGE_OK;
 }
 
+huge_status eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
+                     const int32_t* d_queries, int32_t n_queries, int32_t k, int32_t* d_ids,
+                     float* d_dist, void* d_workspace, size_t ws_bytes, bool lists_only,
+                     int32_t* d_status, void* stream) {
+    if (!d_table || !d_status || !eval_table_ok(num_rows, dim) || n_queries < 0 || k < 1 ||
+        k > kKnnMaxK || knn_pass_queries(dim) < 32 || !d_workspace ||
+        (n_queries > 0 && (!d_queries || !d_ids || !d_dist)))
+        return HUGE_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(d_workspace) % kAlign != 0) return HUGE_ERR_WORKSPACE;
+    const KnnLayout L = knn_layout(num_rows, dim, k);
+    if (ws_bytes < L.total) return HUGE_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    HIP_TRY(launch_eval_status_clear(d_status, s));
+    if (n_queries == 0) return HUGE_OK;
+    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
+    KnnBuffers B;
+    B.qn = reinterpret_cast<float*>(ws + L.qn);
+    B.qn2 = reinterpret_cast<float*>(ws + L.qn2);
+    B.qid = reinterpret_cast<int32_t*>(ws + L.qid);
+    B.partial = reinterpret_cast<uint64_t*>(ws + L.partial);
+    B.tau = reinterpret_cast<float*>(ws + L.tau);
+    B.cnt = reinterpret_cast<uint32_t*>(ws + L.cnt);
+    B.gate = reinterpret_cast<int32_t*>(ws + L.gate);
+    B.cand = reinterpret_cast<uint64_t*>(ws + L.cand);
+    HIP_TRY(launch_knn(d_table, num_rows, dim, d_queries, n_queries, k, d_ids, d_dist, B,
+                       lists_only, d_status, s));
+    return HUGE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1081,22 +1115,16 @@ huge_status huge_eval_knn(const float* d_table, int64_t num_rows, int32_t dim,
                           const int32_t* d_queries, int32_t n_queries, int32_t k,
                           int32_t* d_ids, float* d_dist, void* d_workspace, size_t ws_bytes,
                           int32_t* d_status, void* stream) {
-    if (!d_table || !d_status || !eval_table_ok(num_rows, dim) || n_queries < 0 || k < 1 ||
-        k > kKnnMaxK || knn_pass_queries(dim) < 32 || !d_workspace ||
-        (n_queries > 0 && (!d_queries || !d_ids || !d_dist)))
-        return HUGE_ERR_INVALID_ARG;
-    if (reinterpret_cast<uintptr_t>(d_workspace) % kAlign != 0) return HUGE_ERR_WORKSPACE;
-    const KnnLayout L = knn_layout(num_rows, dim, k);
-    if (ws_bytes < L.total) return HUGE_ERR_WORKSPACE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    HIP_TRY(launch_eval_status_clear(d_status, s));
-    if (n_queries == 0) return HUGE_OK;
-    uint8_t* ws = static_cast<uint8_t*>(d_workspace);
-    HIP_TRY(launch_knn(d_table, num_rows, dim, d_queries, n_queries, k, d_ids, d_dist,
-                       reinterpret_cast<float*>(ws + L.qn), reinterpret_cast<float*>(ws + L.qn2),
-                       reinterpret_cast<int32_t*>(ws + L.qid),
-                       reinterpret_cast<uint64_t*>(ws + L.partial), d_status, s));
-    return HUGE_OK;
+    return eval_knn(d_table, num_rows, dim, d_queries, n_queries, k, d_ids, d_dist, d_workspace,
+                    ws_bytes, false, d_status, stream);
+}
+
+huge_status huge_eval_knn_lists(const float* d_table, int64_t num_rows, int32_t dim,
+                                const int32_t* d_queries, int32_t n_queries, int32_t k,
+                                int32_t* d_ids, float* d_dist, void* d_workspace,
+                                size_t ws_bytes, int32_t* d_status, void* stream) {
+    return eval_knn(d_table, num_rows, dim, d_queries, n_queries, k, d_ids, d_dist, d_workspace,
+                    ws_bytes, true, d_status, stream);
 }
 
 huge_status huge_eval_recall(const int64_t* d_offsets, const int32_t* d_neighbors,

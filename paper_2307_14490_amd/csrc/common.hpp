@@ -55,6 +55,13 @@ constexpr int kKnnQueryFloats = 16896;  // LDS floats for the queries of a pass 
 constexpr int kKnnPass = 128;           // queries per pass over the table, at most
 constexpr int kKnnGrid = 256;           // nearest-row workgroups (one per CU)
 constexpr int kKnnMergeCap = 8192;      // keys sorted together by the merge
+// Threshold scans of the nearest-row search (dim <= 128)
+constexpr int kKnnScanWaves = 4;        // waves of a scan workgroup (two workgroups per CU)
+constexpr int kKnnScanGrid = 512;       // scan workgroups, at most
+constexpr int kKnnCandCap = 8192;       // candidate keys kept per query and scan
+constexpr int kKnnStageTiles = 256;     // row tiles of the first (coarsest) scan, at most
+constexpr int kKnnStageGrowth = 64;     // tile stride of a scan over that of the next
+constexpr int kKnnSelectThreads = 1024; // threads of a candidate selection workgroup
 constexpr uint32_t kShortRun = 32;     // repeated rows with at most this many occurrences are
                                        // summed by one thread group
 constexpr uint32_t kPiece = 256;       // occurrences summed by one workgroup task
@@ -355,9 +362,20 @@ hipError_t launch_eval_quantiles(const uint32_t* sorted, const double* cnt, cons
                                  int nq, double* out, hipStream_t s);
 int knn_pass_queries(int D);
 int64_t knn_lists(int64_t N, int D, int QB);
+// Workspace of a nearest-row search (device memory, one pass of queries).
+struct KnnBuffers {
+    float* qn;        // [kKnnPass][dim] normalised queries
+    float* qn2;       // [kKnnPass] their squared norms (0 or 1)
+    int32_t* qid;     // [kKnnPass] their rows (-1: padding)
+    uint64_t* partial;  // per-wave lists of the list-merging search
+    float* tau;       // [kKnnPass] distance bound of the next threshold scan
+    uint32_t* cnt;    // [kKnnPass] candidates of the current scan
+    uint64_t* cand;   // [kKnnPass][kKnnCandCap] their keys
+    int32_t* gate;    // 1: a final scan overflowed, the list-merging search runs
+};
 hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, int32_t nq,
-                      int32_t k, int32_t* ids, float* dist, float* qn, float* qn2, int32_t* qid,
-                      uint64_t* partial, int32_t* status, hipStream_t s);
+                      int32_t k, int32_t* ids, float* dist, const KnnBuffers& B,
+                      bool lists_only, int32_t* status, hipStream_t s);
 hipError_t launch_eval_recall(const int64_t* off, const int32_t* nbr, int64_t N, int64_t E,
                               const int32_t* q, int32_t nq, const int32_t* ids, int32_t k,
                               double* out, int32_t* status, hipStream_t s);

@@ -287,13 +287,18 @@ hipError_t launch_eval_quantiles(const uint32_t* sorted, const double* cnt, cons
 // Nearest rows of up to kKnnPass queries per pass over the table.
 // ---------------------------------------------------------------------------
 // Normalised query rows qn[j * D ..] (zero for a zero row or a padding slot)
-// and qn2[j] = |qn_j|^2 in {0, 1}.
+// and qn2[j] = |qn_j|^2 in {0, 1}; with the threshold scans, their state: no
+// candidates, the bound +inf (-inf for a padding slot: nothing passes it) and
+// the fallback gate closed.
 __global__ __launch_bounds__(kBlock) void k_knn_queries(const float* __restrict__ T, int64_t N,
                                                         int32_t D, const int32_t* __restrict__ q,
                                                         int32_t nq, int32_t nqp,
                                                         float* __restrict__ qn,
                                                         float* __restrict__ qn2,
                                                         int32_t* __restrict__ qid,
+                                                        float* __restrict__ tau,
+                                                        uint32_t* __restrict__ cnt,
+                                                        int32_t* __restrict__ gate,
                                                         int32_t* __restrict__ status) {
     __shared__ float s_red[kBlock];
     const int j = blockIdx.x;
@@ -322,6 +327,11 @@ __global__ __launch_bounds__(kBlock) void k_knn_queries(const float* __restrict_
     if (threadIdx.x == 0) {
         qn2[j] = n2 > 0.f ? 1.f : 0.f;
         qid[j] = id;
+        if (cnt) {
+            cnt[j] = 0u;
+            tau[j] = id >= 0 ? __builtin_inff() : -__builtin_inff();
+        }
+        if (gate && j == 0) *gate = 0;
     }
 }
 
@@ -350,6 +360,7 @@ struct KnnArgs {
     const float* qn2;
     const int32_t* qid;
     uint64_t* partial;
+    const int32_t* gate;  // null: always run; else run only where *gate != 0
 };
 
 constexpr uint64_t kNoKey = ~0ull;
@@ -364,6 +375,7 @@ __global__ __launch_bounds__(kKnnWaves * 64) void k_knn_tiles(KnnArgs A) {
     __shared__ float s_qn2[kKnnPass];
     __shared__ int32_t s_qid[kKnnPass];
 
+    if (A.gate && *A.gate == 0) return;  // the threshold scans answered every query
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int x = lane & 31, h = lane >> 5;
     const int D = A.D, k = A.k, stride = A.stride;
@@ -500,8 +512,10 @@ __global__ __launch_bounds__(kKnnWaves * 64) void k_knn_tiles(KnnArgs A) {
 __global__ __launch_bounds__(kBlock) void k_knn_merge(const uint64_t* __restrict__ partial,
                                                       int64_t NS, int32_t nqp, int32_t k,
                                                       int32_t q_first, int32_t* __restrict__ ids,
-                                                      float* __restrict__ dist) {
+                                                      float* __restrict__ dist,
+                                                      const int32_t* __restrict__ gate) {
     __shared__ uint64_t s_buf[kKnnMergeCap];
+    if (gate && *gate == 0) return;
     const int q = blockIdx.x;
     const int64_t total = NS * k;
     for (int i = threadIdx.x; i < k; i += kBlock) s_buf[i] = kNoKey;
@@ -577,6 +591,49 @@ __device__ __forceinline__ void knn_split8(float4 a, float4 b, float sc, knn_h8&
     }
 }
 
+// The hi parts alone of knn_split8 (the same pinned products, the same
+// conversions): hi[e] equals knn_split8's hi[e] bit for bit.
+__device__ __forceinline__ knn_h8 knn_hi8(float4 a, float4 b, float sc) {
+    float v[8] = {a.x * sc, a.y * sc, a.z * sc, a.w * sc, b.x * sc, b.y * sc, b.z * sc,
+                  b.w * sc};
+    knn_h8 hi;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        asm volatile("" : "+v"(v[e]));
+        hi[e] = (_Float16)v[e];
+    }
+    return hi;
+}
+
+// Squared norm of the 16 values v[0 .. 3] in a fixed order of explicit fused
+// multiply-adds, and that of a row held by a lane pair (x, 0), (x, 1) as
+// 16 float4 each: four such sums per lane, each added to its partner's, then
+// (P0 + P1) + (P2 + P3).  Every fp16 search forms a row's norm this way (the
+// four-block search from partial sums that its four waves exchange), so all of
+// them compute the same scale and the same distances for a row.
+__device__ __forceinline__ float knn_sq4(const float4* v) {
+    float p = 0.f;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        float t = v[m].x * v[m].x;
+        t = fmaf(v[m].y, v[m].y, t);
+        t = fmaf(v[m].z, v[m].z, t);
+        t = fmaf(v[m].w, v[m].w, t);
+        p += t;
+    }
+    return p;
+}
+
+__device__ __forceinline__ float knn_row_norm(const float4 (&v)[16]) {
+    float P[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        P[i] = knn_sq4(v + 4 * i);
+        P[i] += __shfl_xor(P[i], 32, 64);
+    }
+    return (P[0] + P[1]) + (P[2] + P[3]);
+}
+
 __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
     __shared__ uint64_t s_list[kKnnWavesR][32][kKnnMaxK];
     __shared__ uint64_t s_stage[kKnnWavesR][32][32];
@@ -584,6 +641,7 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
     __shared__ uint32_t s_cnt[kKnnWavesR][32];
     __shared__ uint32_t s_len[kKnnWavesR][32];
 
+    if (A.gate && *A.gate == 0) return;  // the threshold scans answered every query
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int x = lane & 31, h = lane >> 5;
     const int D = A.D, k = A.k;
@@ -643,11 +701,7 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h(KnnArgs A) {
             bv[2 * c + 1] = (ok && d + 8 <= D) ? *reinterpret_cast<const float4*>(src + d + 4)
                                                : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        float nr = 0.f;
-#pragma unroll
-        for (int m = 0; m < 2 * kCh; ++m)
-            nr += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z + bv[m].w * bv[m].w;
-        nr += __shfl_xor(nr, 32, 64);
+        const float nr = knn_row_norm(bv);
         const float sc = nr > 0.f ? kKnnSplitScale / sqrtf(nr) : 0.f;
         const float nx = nr > 0.f ? 1.f : 0.f;
         knn_acc16 acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
@@ -744,6 +798,7 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h4(KnnArgs A) {
     // fp16 parts of the tile: [stream][chunk][row][h] = {hi, lo} of 8 dimensions
     __shared__ knn_h8 s_part[kStreams][kCh][32][2][2];
 
+    if (A.gate && *A.gate == 0) return;  // the threshold scans answered every query
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int x = lane & 31, h = lane >> 5;
     const int D = A.D, k = A.k;
@@ -816,10 +871,7 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h4(KnnArgs A) {
         float4 bv[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) bv[m] = nb[m];
-        float pn = 0.f;
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-            pn += bv[m].x * bv[m].x + bv[m].y * bv[m].y + bv[m].z * bv[m].z + bv[m].w * bv[m].w;
+        float pn = knn_sq4(bv);
         pn += __shfl_xor(pn, 32, 64);
         if (h == 0) s_nr[st][qb][x] = pn;
         __syncthreads();
@@ -906,6 +958,273 @@ __global__ __launch_bounds__(kKnnWavesR * 64) void k_knn_tiles_h4(KnnArgs A) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Threshold scans (dim <= 128): the default search.  A scan visits the row
+// tiles i * step (0 <= i < count); every wave takes whole 32-row tiles, loads
+// the next one while it works on the current one, and forms the distances of
+// its tile to every query of the pass with the fp16 parts of the queries in
+// LDS.  Row x's norm, scale and split, the products and d^2 are those of the
+// list-merging kernels above, bit for bit (the matrix instruction takes the
+// row parts as its first operand here, the same products in the same order).
+// A (row, query) pair whose d^2 is at most the query's bound tau is appended
+// to the query's candidate list; only the count of a list that overflows its
+// capacity keeps growing.  Between scans a selection sorts each list: its
+// k-th key bounds the k-th distance over the whole table (any k rows do), so
+// the next, denser scan keeps every row of the true answer.  The scans are
+// nested (each one's tiles are among the next one's), so each finds at least
+// the k rows that set its bound; the last one visits every tile and its k
+// smallest keys are the answer.
+// A tile is screened first by the hi.hi products alone (one matrix
+// instruction per chunk instead of three, no lo parts): they differ from the
+// full products hi.hi + hi.lo + lo.hi by at most the dropped terms,
+// sum |hi_q lo_r| + |lo_q hi_r| <= 2^-10 (1 + 2^-10) 2^20 with |q|, |r| <= 2^10
+// after scaling, plus the accumulations' roundings (at most 384 of 2^-4
+// each) and fp16 subnormal steps: below 1100 units of the product.  For a
+// present, nonzero row, d^2 <= tau needs acc >= (|q|^2 + 1 - tau) 2^19 - 2
+// (the bound is computed within 2^-3 and d^2's one rounding moves it by at
+// most 2^-21, a quarter of a unit of acc), so a screened product below that
+// less kKnnScreenMargin = 1536 clears the pair.  A query block with any pair
+// left, or a tile with a zero or missing row, gets the full products of the
+// list search (bit for bit) and the exact test.
+// ---------------------------------------------------------------------------
+struct KnnScanArgs {
+    const float* T;
+    int64_t N;
+    int32_t D;
+    int32_t cap;    // keys kept per list
+    int64_t step;   // tiles i * step, 0 <= i < count
+    int64_t count;
+    const float* qn;
+    const float* qn2;
+    const int32_t* qid;
+    const float* tau;
+    uint32_t* cnt;
+    uint64_t* cand;  // [query slot][cap]
+};
+
+constexpr float kKnnAccPerD2 = 524288.0f;  // 2^19: a unit of d^2 in the product's units
+constexpr float kKnnScreenMargin = 1536.0f;  // product units: hi.hi against the full products
+
+// The exact test of a tile's pairs with query block qb and the append of the
+// passing ones (a tile with a candidate, a zero or a missing row).
+template <int QB>
+__device__ __forceinline__ void knn_scan_append(const KnnScanArgs& A, int qb, int x, int h,
+                                                int64_t t, uint64_t live,
+                                                const knn_acc16& acc) {
+    const int q = qb * 32 + x;
+    const float tau = A.tau[q];
+    const int64_t qid = A.qid[q];
+    const bool q1 = A.qn2[q] > 0.f;
+    const int64_t rows = A.N - t * 32;  // rows of the tile present
+    uint32_t pass = 0u;
+    float d2v[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        // d^2 = |q|^2 + [row != 0] - 2 <q, row>, clamped at 0
+        const int m = 8 * (r / 4) + 4 * h + (r % 4);
+        const float nx = (live >> m) & 1ull ? 1.f : 0.f;
+        const float base = q1 ? nx + 1.f : nx;
+        float d2 = fmaf(-2.f * kKnnSplitUnscale, acc[r], base);
+        d2 = d2 > 0.f ? d2 : 0.f;
+        d2v[r] = d2;
+        if (d2 <= tau && m < rows && t * 32 + m != qid) pass |= 1u << r;
+    }
+    if (pass == 0u) return;
+    uint32_t pos = atomicAdd(&A.cnt[q], (uint32_t)__popc(pass));
+    uint64_t* dst = A.cand + (size_t)q * A.cap;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        if (!((pass >> r) & 1u)) continue;
+        const int m = 8 * (r / 4) + 4 * h + (r % 4);
+        if (pos < (uint32_t)A.cap)
+            dst[pos] = ((uint64_t)__float_as_uint(d2v[r]) << 32) | (uint64_t)(t * 32 + m);
+        ++pos;
+    }
+}
+
+// FULL: dim is 128, so no dimension of a chunk lies past the row.
+template <int QB, bool FULL>
+__global__ __launch_bounds__(kKnnScanWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_knn_scan(KnnScanArgs A) {
+    constexpr int kCh = kKnnDimChunk / 16;  // 16-dimension chunks
+    // B operands: lane (x, h) of s_q[qb][c][p] holds the fp16 part p (0 hi,
+    // 1 lo) of query qb * 32 + x's dimensions 16 c + 8 h .. 16 c + 8 h + 7
+    __shared__ knn_h8 s_q[QB][kCh][2][64];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int x = lane & 31, h = lane >> 5;
+    const int D = A.D;
+    const int d0 = 8 * h;
+    for (int j = w; j < QB * kCh; j += kKnnScanWaves) {
+        const int qb = j / kCh, c = j % kCh;
+        const float* qrow = A.qn + (int64_t)(qb * 32 + x) * D;
+        const int d = 16 * c + d0;
+        const float4 a = d + 4 <= D ? *reinterpret_cast<const float4*>(qrow + d)
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 b = d + 8 <= D ? *reinterpret_cast<const float4*>(qrow + d + 4)
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
+        knn_h8 hi, lo;
+        knn_split8(a, b, kKnnSplitScale, hi, lo);
+        s_q[qb][c][0][lane] = hi;
+        s_q[qb][c][1][lane] = lo;
+    }
+    // lane (x, h) holds query qb * 32 + x of every block against rows
+    // 8 (r / 4) + 4 h + r % 4 of the tile (accumulator r); a screened
+    // product below athr[qb] is no candidate for a present, nonzero row
+    float athr[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int q = qb * 32 + x;
+        const float q1 = A.qn2[q] > 0.f ? 1.f : 0.f;
+        athr[qb] = ((q1 + 1.f) - A.tau[q]) * kKnnAccPerD2 - 2.f - kKnnScreenMargin;
+    }
+    __syncthreads();
+
+    const int64_t W = (int64_t)gridDim.x * kKnnScanWaves;
+    const int64_t i0 = (int64_t)blockIdx.x * kKnnScanWaves + w;
+    // Row x of tile i * step: lane (x, h) loads dimensions 16 c + 8 h .. + 7
+    // of every chunk c.  Past the scan's last tile or the table a lane loads
+    // row 0 instead (its rows are marked missing below); past dim, zeros.
+    auto load_tile = [&](int64_t i, float4 (&dst)[2 * kCh]) {
+        const int64_t row = i * A.step * 32 + x;
+        const bool ok = i < A.count && row < A.N;
+        const float* src = A.T + (ok ? row : 0) * (int64_t)D;
+#pragma unroll
+        for (int c = 0; c < kCh; ++c) {
+            const int d = 16 * c + d0;
+            if (FULL) {
+                dst[2 * c] = *reinterpret_cast<const float4*>(src + d);
+                dst[2 * c + 1] = *reinterpret_cast<const float4*>(src + d + 4);
+            } else {
+                dst[2 * c] = d + 4 <= D ? *reinterpret_cast<const float4*>(src + d)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+                dst[2 * c + 1] = d + 8 <= D ? *reinterpret_cast<const float4*>(src + d + 4)
+                                            : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+    };
+    auto scan_tile = [&](int64_t i, const float4 (&bv)[2 * kCh]) {
+        const int64_t t = i * A.step;
+        const float nr = knn_row_norm(bv);
+        const float sc = nr > 0.f ? kKnnSplitScale / sqrtf(nr) : 0.f;
+        // bit m (and m + 32): row m of the tile is present and nonzero
+        const uint64_t live = __ballot(nr > 0.f && t * 32 + x < A.N);
+        // the screen: hi.hi products of every query block
+        knn_acc16 acc[QB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[qb][r] = 0.f;
+#pragma unroll
+        for (int c = 0; c < kCh; ++c) {
+            const knn_h8 bh = knn_hi8(bv[2 * c], bv[2 * c + 1], sc);
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+                acc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(bh, s_q[qb][c][0][lane],
+                                                                 acc[qb], 0, 0, 0);
+        }
+        // bit qb: the block has a pair left (wave-uniform)
+        uint32_t need = 0u;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            bool look = live != ~0ull;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) look |= acc[qb][r] >= athr[qb];
+            need |= __ballot(look) != 0ull ? 1u << qb : 0u;
+        }
+        // the full products of the list search for those blocks, then the exact test
+#pragma unroll 1
+        for (; need != 0u; need &= need - 1u) {
+            const int qb = __builtin_ctz(need);
+            knn_acc16 ex = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
+                            0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < kCh; ++c) {
+                knn_h8 bh, bl;
+                knn_split8(bv[2 * c], bv[2 * c + 1], sc, bh, bl);
+                const knn_h8 qh = s_q[qb][c][0][lane];
+                const knn_h8 ql = s_q[qb][c][1][lane];
+                ex = __builtin_amdgcn_mfma_f32_32x32x16_f16(bh, qh, ex, 0, 0, 0);
+                ex = __builtin_amdgcn_mfma_f32_32x32x16_f16(bl, qh, ex, 0, 0, 0);
+                ex = __builtin_amdgcn_mfma_f32_32x32x16_f16(bh, ql, ex, 0, 0, 0);
+            }
+            knn_scan_append<QB>(A, qb, x, h, t, live, ex);
+        }
+    };
+    // two register buffers in turn: a tile's rows load during the previous
+    // tile's products
+    float4 ba[2 * kCh], bb[2 * kCh];
+    load_tile(i0, ba);
+    for (int64_t i = i0; i < A.count; i += 2 * W) {
+        load_tile(i + W, bb);
+        scan_tile(i, ba);
+        if (i + W >= A.count) break;
+        load_tile(i + 2 * W, ba);
+        scan_tile(i + W, bb);
+    }
+}
+
+// Candidate selection, one workgroup per query slot: the list's kept keys
+// (at most cap, a power of two) sorted in LDS by a bitonic network.  After a
+// sample scan the k-th key's d^2 becomes the query's bound (fewer than k keys
+// leave it); after the last scan the k smallest keys are the answer, written
+// as the list-merging search writes it, and a list that overflowed opens the
+// gate for that search.  The count is reset for the next scan.
+struct KnnSelectArgs {
+    uint32_t* cnt;
+    const uint64_t* cand;
+    int32_t cap;
+    int32_t k;
+    int32_t last;      // 1: the last scan
+    int32_t m;         // queries of the pass (slots beyond are padding)
+    int32_t q_first;   // the pass's first query
+    float* tau;
+    int32_t* ids;
+    float* dist;
+    int32_t* gate;
+};
+
+__global__ __launch_bounds__(kKnnSelectThreads) void k_knn_select(KnnSelectArgs S) {
+    extern __shared__ uint64_t s_key[];
+    const int q = blockIdx.x, tid = threadIdx.x;
+    const uint32_t c = S.cnt[q];
+    const uint32_t n = c < (uint32_t)S.cap ? c : (uint32_t)S.cap;
+    uint32_t P = 2u;
+    while (P < n) P <<= 1;
+    for (uint32_t i = tid; i < P; i += kKnnSelectThreads)
+        s_key[i] = i < n ? S.cand[(size_t)q * S.cap + i] : kNoKey;
+    __syncthreads();
+    for (uint32_t size = 2; size <= P; size <<= 1) {
+        for (uint32_t st = size >> 1; st > 0; st >>= 1) {
+            for (uint32_t i = tid; i < P / 2; i += kKnnSelectThreads) {
+                const uint32_t lo = 2 * i - (i & (st - 1));
+                const uint32_t hi = lo + st;
+                const bool up = (lo & size) == 0;
+                const uint64_t a = s_key[lo], b = s_key[hi];
+                if ((a > b) == up) {
+                    s_key[lo] = b;
+                    s_key[hi] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    if (S.last) {
+        if (q < S.m) {
+            for (int t = tid; t < S.k; t += kKnnSelectThreads) {
+                const uint64_t key = (uint32_t)t < P ? s_key[t] : kNoKey;
+                const int64_t o = (int64_t)(S.q_first + q) * S.k + t;
+                S.ids[o] = key == kNoKey ? -1 : (int32_t)(uint32_t)key;
+                S.dist[o] = key == kNoKey ? __builtin_nanf("")
+                                          : sqrtf(__uint_as_float((uint32_t)(key >> 32)));
+            }
+        }
+        if (tid == 0 && c > (uint32_t)S.cap) *S.gate = 1;
+    } else if (tid == 0 && n >= (uint32_t)S.k) {
+        S.tau[q] = __uint_as_float((uint32_t)(s_key[S.k - 1] >> 32));
+    }
+    if (tid == 0) S.cnt[q] = 0u;
+}
+
 int knn_pass_queries(int D) {
     int qp = kKnnQueryFloats / (D + 4);
     qp = qp > kKnnPass ? kKnnPass : qp;
@@ -922,18 +1241,87 @@ int64_t knn_lists(int64_t N, int D, int QB) {
     return grid * wpb;
 }
 
+template <int QB>
+static void launch_knn_scan(const KnnScanArgs& A, hipStream_t s) {
+    int64_t grid = (A.count + kKnnScanWaves - 1) / kKnnScanWaves;
+    grid = grid < kKnnScanGrid ? grid : kKnnScanGrid;
+    if (A.D == kKnnDimChunk)
+        hipLaunchKernelGGL((k_knn_scan<QB, true>), dim3((unsigned)grid),
+                           dim3(kKnnScanWaves * 64), 0, s, A);
+    else
+        hipLaunchKernelGGL((k_knn_scan<QB, false>), dim3((unsigned)grid),
+                           dim3(kKnnScanWaves * 64), 0, s, A);
+}
+
+// Tile strides of the threshold scans, coarsest first: the first visits at
+// most kKnnStageTiles tiles with no bound (so its lists cannot overflow), each
+// next one a stride kKnnStageGrowth times finer, the last every tile.  Returns
+// the number of scans.
+int knn_scan_steps(int64_t tiles, int64_t* steps) {
+    int64_t s = 1;
+    while ((tiles + s - 1) / s > kKnnStageTiles) s *= kKnnStageGrowth;
+    int n = 0;
+    for (; s >= 1; s /= kKnnStageGrowth) steps[n++] = s;
+    return n;
+}
+
 hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, int32_t nq,
-                      int32_t k, int32_t* ids, float* dist, float* qn, float* qn2, int32_t* qid,
-                      uint64_t* partial, int32_t* status, hipStream_t s) {
+                      int32_t k, int32_t* ids, float* dist, const KnnBuffers& B,
+                      bool lists_only, int32_t* status, hipStream_t s) {
     const int qp = knn_pass_queries(D);
     if (qp < 32 || k < 1 || k > kKnnMaxK || N < 1) return hipErrorInvalidValue;
+    const bool scans = D <= kKnnDimChunk && !lists_only;
+    const int64_t tiles = (N + 31) / 32;
     for (int32_t q0 = 0; q0 < nq; q0 += qp) {
         const int32_t m = nq - q0 < qp ? nq - q0 : qp;
         int QB = (m + 31) / 32;
         if (QB == 3) QB = 4;
         const int32_t nqp = 32 * QB;
         hipLaunchKernelGGL(k_knn_queries, dim3((unsigned)nqp), dim3(kBlock), 0, s, T, N, D,
-                           q + q0, m, nqp, qn, qn2, qid, status);
+                           q + q0, m, nqp, B.qn, B.qn2, B.qid, scans ? B.tau : nullptr,
+                           scans ? B.cnt : nullptr, scans ? B.gate : nullptr, status);
+        if (scans) {
+            KnnScanArgs SA;
+            SA.T = T;
+            SA.N = N;
+            SA.D = D;
+            SA.cap = kKnnCandCap;
+            SA.qn = B.qn;
+            SA.qn2 = B.qn2;
+            SA.qid = B.qid;
+            SA.tau = B.tau;
+            SA.cnt = B.cnt;
+            SA.cand = B.cand;
+            KnnSelectArgs SS;
+            SS.cnt = B.cnt;
+            SS.cand = B.cand;
+            SS.cap = kKnnCandCap;
+            SS.k = k;
+            SS.m = m;
+            SS.q_first = q0;
+            SS.tau = B.tau;
+            SS.ids = ids;
+            SS.dist = dist;
+            SS.gate = B.gate;
+            int64_t steps[16];
+            const int ns = knn_scan_steps(tiles, steps);
+            for (int j = 0; j < ns; ++j) {
+                SA.step = steps[j];
+                SA.count = (tiles + steps[j] - 1) / steps[j];
+                if (QB == 4)
+                    launch_knn_scan<4>(SA, s);
+                else if (QB == 2)
+                    launch_knn_scan<2>(SA, s);
+                else
+                    launch_knn_scan<1>(SA, s);
+                SS.last = j == ns - 1;
+                hipLaunchKernelGGL(k_knn_select, dim3((unsigned)nqp), dim3(kKnnSelectThreads),
+                                   sizeof(uint64_t) * kKnnCandCap, s, SS);
+            }
+        }
+        // the list-merging search: for wider rows always, else only where a
+        // final candidate list overflowed (the gate; otherwise its kernels
+        // return at once)
         KnnArgs A;
         A.T = T;
         A.N = N;
@@ -942,11 +1330,12 @@ hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, in
         A.nqp = nqp;
         A.QB = QB;
         A.stride = D + 4;
-        A.tiles = (N + 31) / 32;
-        A.qn = qn;
-        A.qn2 = qn2;
-        A.qid = qid;
-        A.partial = partial;
+        A.tiles = tiles;
+        A.qn = B.qn;
+        A.qn2 = B.qn2;
+        A.qid = B.qid;
+        A.partial = B.partial;
+        A.gate = scans ? B.gate : nullptr;
         const int64_t NS = knn_lists(N, D, QB);
         if (D <= kKnnDimChunk) {
             const int64_t grid = NS / (kKnnWavesR / QB);
@@ -960,8 +1349,8 @@ hipError_t launch_knn(const float* T, int64_t N, int32_t D, const int32_t* q, in
             const int64_t grid = NS / (kKnnWaves / QB);
             hipLaunchKernelGGL(k_knn_tiles, dim3((unsigned)grid), dim3(kKnnWaves * 64), 0, s, A);
         }
-        hipLaunchKernelGGL(k_knn_merge, dim3((unsigned)m), dim3(kBlock), 0, s, partial, NS, nqp,
-                           k, q0, ids, dist);
+        hipLaunchKernelGGL(k_knn_merge, dim3((unsigned)m), dim3(kBlock), 0, s, B.partial, NS, nqp,
+                           k, q0, ids, dist, A.gate);
     }
     return hipGetLastError();
 }

@@ -221,6 +221,10 @@ def test_knn_and_recall(N, D, nq, k, note):
     ids = ids.cpu().numpy()
     dist = dist.cpu().numpy()
     check_knn(T, queries, k, ids, dist)
+    # the per-wave list search computes the same distances: the same answer, bit for bit
+    ids_l, dist_l = ev.knn(dev(T, torch), dev(queries, torch), k, lists=True)
+    assert np.array_equal(ids, ids_l.cpu().numpy())
+    assert np.array_equal(dist.view(np.int32), dist_l.cpu().numpy().view(np.int32))
     off, nbr = random_graph(N, 6 * N, seed=N)
     rec = ev.recall(dev(off, torch), dev(nbr, torch), N, dev(queries, torch),
                     dev(ids, torch)).cpu().numpy()
@@ -253,6 +257,50 @@ def test_recall_on_an_embedding_that_reconstructs_the_graph():
     ids4, _ = ev.knn(dev(T, torch), dev(q, torch), 4)
     r4 = ev.recall(dev(off, torch), dev(nbr, torch), n, dev(q, torch), ids4).cpu().numpy()
     assert np.all(r4 == 0.5)
+
+
+def test_knn_falls_back_to_the_list_search_when_a_candidate_list_overflows():
+    """18,000 copies of row 5 lie at one distance from query 5, so its last
+    threshold scan keeps more candidates than a list holds (8192): that pass is
+    computed again by the list search.  Its answer for the other queries equals
+    both searches' answer without query 5, bit for bit, and query 5's k nearest
+    are the copies with the smallest ids."""
+    N, D, k = 30000, 128, 10
+    rng = np.random.default_rng(77)
+    T = rng.normal(size=(N, D)).astype(np.float32)
+    T[12000:] = T[5]
+    others = np.setdiff1d(rng.choice(12000, 120, replace=False), [5])[:99].astype(np.int32)
+    with_5 = np.concatenate([[5], others]).astype(np.int32)
+    say(f"knn overflow N={N} D={D} k={k} queries={with_5.size}")
+    ev = P.Evaluator(N, D, 8, k=k)
+    Td = dev(T, torch)
+    ids_a, dist_a = (a.cpu().numpy() for a in ev.knn(Td, dev(with_5, torch), k))
+    ids_b, dist_b = (a.cpu().numpy() for a in ev.knn(Td, dev(others, torch), k))
+    ids_c, dist_c = (a.cpu().numpy() for a in ev.knn(Td, dev(others, torch), k, lists=True))
+    assert ids_a[0].tolist() == list(range(12000, 12000 + k))
+    for ids, dist in ((ids_b, dist_b), (ids_c, dist_c)):
+        assert np.array_equal(ids_a[1:], ids)
+        assert np.array_equal(dist_a[1:].view(np.int32), dist.view(np.int32))
+    check_knn(T, others[:20], k, ids_b[:20], dist_b[:20])
+
+
+def test_knn_threshold_scans_at_a_million_rows():
+    """1e6 x 128 rows, 100 queries, k = 10: three threshold scans (8, 489 and
+    31,250 tiles of 32 rows).  Bit for bit the list search's answer; the
+    first 4 queries against exact double distances."""
+    N, D, k, nq = 1_000_000, 128, 10, 100
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    Td = torch.randn((N, D), generator=g, device="cuda", dtype=torch.float32)
+    rng = np.random.default_rng(12)
+    queries = rng.choice(N, nq, replace=False).astype(np.int32)
+    say(f"knn N={N} D={D} nq={nq} k={k}")
+    ev = P.Evaluator(N, D, 8, k=k)
+    ids, dist = (a.cpu().numpy() for a in ev.knn(Td, dev(queries, torch), k))
+    ids_l, dist_l = (a.cpu().numpy() for a in ev.knn(Td, dev(queries, torch), k, lists=True))
+    assert np.array_equal(ids, ids_l)
+    assert np.array_equal(dist.view(np.int32), dist_l.view(np.int32))
+    check_knn(Td.cpu().numpy(), queries[:4], k, ids[:4], dist[:4])
 
 
 def test_knn_reports_bad_query_ids():
