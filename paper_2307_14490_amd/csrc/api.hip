@@ -13,7 +13,8 @@
 // finish kernel (repeated rows, loss).  kSlots grouping slots let two batches
 // be prepared ahead; events order the halves: an apply waits for its batch's
 // preparation and for the previous apply, a preparation for the apply that
-// last used its slot.
+// last used its slot (an apply's completion is recorded only where such a
+// wait needs it).
 #include <math.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -72,17 +73,24 @@ struct huge_handle {
     int last_applied_slot;     // -1 before the first apply
     PendingBatch pending[kSlots];
     hipEvent_t ready[kSlots];    // preparation of the slot's batch complete
-    hipEvent_t done[kSlots];     // its apply complete
+    // Completion of apply done_idx (0-based), recorded on done_stream: an
+    // apply's completion implies that of every earlier one, so one event,
+    // recorded only where a later wait needs it, serves every such wait.
+    // Each record costs the recording kernel a signalled completion (a
+    // device-wide cache write-back of several microseconds before the next
+    // kernel starts).
+    hipEvent_t done_ev = nullptr;
+    int64_t done_idx = -1;
+    hipStream_t done_stream = nullptr;
     // phase timing
     std::vector<hipEvent_t> prof_ev;
     std::vector<char> prof_applied;
     int32_t prof_max = 0, prof_next = 0;  // batches to profile; profiled so far
     int32_t prof_every = 1, prof_seen = 0;  // every prof_every-th batch; batches seen
     bool prof_all = false;     // events at every phase boundary, not only the fused kernel
-    // the stream of the last apply and of each slot's last apply, so that a
-    // wait on an event of the same stream is skipped (the stream orders it)
+    // the stream of the last apply, so that a wait on it from the same
+    // stream is skipped (the stream orders it)
     hipStream_t last_apply_stream = nullptr;
-    hipStream_t slot_apply_stream[kSlots] = {};
     // calls outside the step that read or write the tables or the shared
     // apply regions (huge_eval_loss, huge_get_rows, huge_probe_rows): the
     // next apply waits for the last of them
@@ -227,10 +235,9 @@ void release_profile(huge_handle* h) {
 void destroy_handle(huge_handle* h) {
     if (!h) return;
     release_profile(h);
-    for (int s = 0; s < kSlots; ++s) {
-        for (hipEvent_t e : {h->ready[s], h->done[s]})
-            if (e) (void)hipEventDestroy(e);
-    }
+    for (int s = 0; s < kSlots; ++s)
+        if (h->ready[s]) (void)hipEventDestroy(h->ready[s]);
+    if (h->done_ev) (void)hipEventDestroy(h->done_ev);
     if (h->side_done) (void)hipEventDestroy(h->side_done);
     delete h;
 }
@@ -259,17 +266,16 @@ huge_status create(const huge_config* cfg, void* S, void* T, const uint32_t* thr
     h->key_bits = key_bits(cfg->num_nodes);
     h->prepared = h->applied = 0;
     h->last_applied_slot = -1;
-    for (int s = 0; s < kSlots; ++s) h->ready[s] = h->done[s] = nullptr;
+    for (int s = 0; s < kSlots; ++s) h->ready[s] = nullptr;
     // the events order streams of this device only: a device-scope release
     // suffices (the default one is system-scope)
     const unsigned flags = hipEventDisableTiming | hipEventReleaseToDevice;
-    for (int s = 0; s < kSlots; ++s) {
-        for (hipEvent_t* e : {&h->ready[s], &h->done[s]}) {
-            if (hipEventCreateWithFlags(e, flags) != hipSuccess) {
-                *e = nullptr;
-                destroy_handle(h);
-                return HUGE_ERR_HIP;
-            }
+    for (int s = 0; s < kSlots + 1; ++s) {
+        hipEvent_t* e = s < kSlots ? &h->ready[s] : &h->done_ev;
+        if (hipEventCreateWithFlags(e, flags) != hipSuccess) {
+            *e = nullptr;
+            destroy_handle(h);
+            return HUGE_ERR_HIP;
         }
     }
     if (hipEventCreateWithFlags(&h->side_done, flags) != hipSuccess) {
@@ -315,6 +321,20 @@ hipError_t wait_on(hipStream_t s, hipEvent_t e, hipStream_t from) {
     return hipStreamWaitEvent(s, e, 0);
 }
 
+// Make s wait until apply i (issued) is complete: nothing on the last apply's
+// stream (it follows every apply), the recorded completion if it covers i,
+// else a completion recorded now after the last apply.
+hipError_t wait_applied(huge_handle* h, hipStream_t s, int64_t i) {
+    if (i < 0 || s == h->last_apply_stream) return hipSuccess;
+    if (h->done_idx < i) {
+        const hipError_t e = hipEventRecord(h->done_ev, h->last_apply_stream);
+        if (e != hipSuccess) return e;
+        h->done_idx = h->applied - 1;
+        h->done_stream = h->last_apply_stream;
+    }
+    return wait_on(s, h->done_ev, h->done_stream);
+}
+
 // A call outside the step on stream s: ordered after the last apply (it
 // reads the tables or the shared apply regions) ...
 hipError_t side_begin(huge_handle* h, hipStream_t s) {
@@ -322,8 +342,7 @@ hipError_t side_begin(huge_handle* h, hipStream_t s) {
         const hipError_t e = wait_on(s, h->side_done, h->side_stream);
         if (e != hipSuccess) return e;
     }
-    if (h->last_applied_slot < 0) return hipSuccess;
-    return wait_on(s, h->done[h->last_applied_slot], h->last_apply_stream);
+    return wait_applied(h, s, h->applied - 1);
 }
 
 // ... and the next apply ordered after it.
@@ -364,7 +383,7 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
         h->prof_seen += 1;
     }
     // the slot's previous apply must be complete before its buffers change
-    HIP_TRY(wait_on(s, h->done[slot], h->slot_apply_stream[slot]));
+    HIP_TRY(wait_applied(h, s, h->prepared - kSlots));
     if (!prof_mark(h, b, 0, s)) return HUGE_ERR_HIP;
     HIP_TRY(launch_begin(ctl, s));
     const bool sorted = h->cfg.scatter_kind == HUGE_SCATTER_SORTED;
@@ -422,15 +441,19 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
 
     HIP_TRY(wait_on(s, h->ready[slot], b.gstream));
     // applies write the tables and share the apply regions: one at a time
-    if (h->last_applied_slot >= 0)
-        HIP_TRY(wait_on(s, h->done[h->last_applied_slot], h->last_apply_stream));
+    HIP_TRY(wait_applied(h, s, h->applied - 1));
     // and after the calls outside the step issued since the last apply
     if (h->side_pending) {
         HIP_TRY(wait_on(s, h->side_done, h->side_stream));
         h->side_pending = false;
     }
     int64_t blocks = 0;
-    bool done_recorded = false;
+    // This apply records its completion only if the next preparation would
+    // otherwise find none recent enough (it needs apply prepared - kSlots;
+    // at most kMaxPending batches wait, so this apply is recent enough):
+    // with one preparation issued ahead of each apply that is every other
+    // apply, and the finish kernel's own completion records it.
+    const bool record_done = h->done_idx < h->prepared - kSlots;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
         // the negatives are the sort keys of slots 2 .. K + 1; a profiled
         // step's fused-kernel events (6, 7) are the kernel's own start and
@@ -462,10 +485,8 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         f.lossp = lossp;
         f.loss_blocks = blocks;
         f.loss_out = loss_out;
-        // the finish kernel's completion records `done` (no packet of its
-        // own between it and the next fused kernel)
-        HIP_TRY(launch_finish(t, ctl, f, h->done[slot], s));
-        done_recorded = true;
+        // the finish kernel's completion records it (no packet of its own)
+        HIP_TRY(launch_finish(t, ctl, f, record_done ? h->done_ev : nullptr, s));
     } else {
         float* gsrc = at<float>(h, L.gsrc);
         float* coef = at<float>(h, L.coef);
@@ -478,9 +499,13 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         if (loss_out) HIP_TRY(launch_loss_final(ctl, lossp, blocks, loss_out, s));
     }
     if (!prof_mark(h, b, 8, s) || !prof_mark(h, b, 9, s)) return HUGE_ERR_HIP;
-    if (!done_recorded) HIP_TRY(hipEventRecord(h->done[slot], s));
+    if (record_done && h->cfg.scatter_kind != HUGE_SCATTER_SORTED)
+        HIP_TRY(hipEventRecord(h->done_ev, s));
+    if (record_done) {
+        h->done_idx = h->applied;
+        h->done_stream = s;
+    }
     if (b.prof >= 0) h->prof_applied[(size_t)b.prof] = 1;
-    h->slot_apply_stream[slot] = s;
     h->last_apply_stream = s;
     h->last_applied_slot = slot;
     h->applied += 1;
@@ -753,10 +778,8 @@ huge_status huge_check(huge_handle* h, void* stream) {
     if (!h) return HUGE_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
     // every stage issued so far, on any stream
-    for (int k = 0; k < kSlots; ++k) {
-        for (hipEvent_t e : {h->ready[k], h->done[k]})
-            HIP_TRY(hipStreamWaitEvent(s, e, 0));
-    }
+    for (int k = 0; k < kSlots; ++k) HIP_TRY(hipStreamWaitEvent(s, h->ready[k], 0));
+    HIP_TRY(wait_applied(h, s, h->applied - 1));
     HIP_TRY(hipStreamWaitEvent(s, h->side_done, 0));
     constexpr int kCtrls = kSlots + 1;
     size_t ctrls[kCtrls];
@@ -791,7 +814,7 @@ huge_status huge_step_stats(huge_handle* h, void* stream, int64_t* unique_src,
     if (sorted && h->last_applied_slot >= 0) {
         const int slot = h->last_applied_slot;
         hipStream_t s = static_cast<hipStream_t>(stream);
-        HIP_TRY(hipStreamWaitEvent(s, h->done[slot], 0));
+        HIP_TRY(wait_applied(h, s, h->applied - 1));
         const int64_t m = h->pending[slot].n * (2 + (int64_t)h->cfg.num_neg_per_pos);
         // k_group writes the counts of every bucket when the batch is not empty
         const int64_t buckets = m > 0 ? ((int64_t)1 << h->pending[slot].bits) : 0;
@@ -838,10 +861,9 @@ huge_status huge_profile_end(huge_handle* h, void* stream, double* phase_ms, int
     if (!h || !phase_ms || !steps) return HUGE_ERR_INVALID_ARG;
     huge_status st = HUGE_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    for (int k = 0; k < kSlots && st == HUGE_OK; ++k) {
-        for (hipEvent_t e : {h->ready[k], h->done[k]})
-            if (hipStreamWaitEvent(s, e, 0) != hipSuccess) st = HUGE_ERR_HIP;
-    }
+    for (int k = 0; k < kSlots && st == HUGE_OK; ++k)
+        if (hipStreamWaitEvent(s, h->ready[k], 0) != hipSuccess) st = HUGE_ERR_HIP;
+    if (st == HUGE_OK && wait_applied(h, s, h->applied - 1) != hipSuccess) st = HUGE_ERR_HIP;
     if (st == HUGE_OK && hipStreamSynchronize(s) != hipSuccess) st = HUGE_ERR_HIP;
     for (int k = 0; k < HUGE_PHASES; ++k) phase_ms[k] = 0.0;
     // phase p lasts from event first[p] to event last[p] of a batch
