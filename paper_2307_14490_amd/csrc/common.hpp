@@ -132,9 +132,16 @@ struct SlotLayout {
     size_t ccount = 0;   // u32 [cap_comb] pieces of the row summed so far
     size_t bcount = 0;   // uint4 [kMaxBins] {short runs, pieces, combines, 0} per bucket
     size_t wstats = 0;   // u32 [kMaxBins * 3] distinct S, distinct T, repeated occurrences
+    // the same records gathered in bucket order (k_records), and their counts
+    size_t cshorts = 0;  // uint4 [cap_short]
+    size_t cpieces = 0;  // uint4 [cap_piece]
+    size_t rcount = 0;   // u32 [2] short runs, pieces
 };
 
-constexpr int kSlots = 3;  // groupings in flight: applied, next, and one more being sampled
+constexpr int kSlots = 3;  // groupings in flight: applied, next, and one more being sampled;
+                           // the wait for a slot's previous apply also paces the preparation
+                           // (six slots let it run ahead onto the finish kernel and the step
+                           // slowed from 0.457 to 0.463 ms)
 
 struct Layout {
     SlotLayout slot[kSlots];
@@ -318,12 +325,10 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 // whose pieces are combined by the last piece to finish) and, with a loss
 // output, the loss sum (the fused step's partials in a fixed order).
 struct FinishArgs {
-    const uint32_t* bstart;  // first position of each bucket
-    const uint4* bcount;     // records per bucket
-    int bins;                // buckets of the batch (0: no records)
-    int64_t m;               // occurrences of the batch
-    const uint4* shorts;
-    const uint4* pieces;
+    int64_t m;               // occurrences of the batch (0: no records)
+    const uint4* cshorts;    // the batch's short-run records, gathered (k_records)
+    const uint4* cpieces;    // its pieces, gathered
+    const uint32_t* rcount;  // how many of each
     const uint4* combs;
     uint32_t* ccount;
     const float* dup;
@@ -334,6 +339,20 @@ struct FinishArgs {
     int64_t loss_blocks;   // how many
     double* loss_out;      // or null: no loss
 };
+// The records of a grouped batch gathered into one list per kind (before its
+// apply, on the preparation stream).
+struct RecordArgs {
+    const uint32_t* bstart;  // first position of each bucket
+    const uint4* bcount;     // records per bucket
+    int bins;                // buckets of the batch
+    const uint4* shorts;     // per-bucket regions, as the grouping left them
+    const uint4* pieces;
+    ListCaps caps;
+    uint4* cshorts;          // out: short runs in bucket order
+    uint4* cpieces;          // out: pieces in bucket order
+    uint32_t* rcount;        // out: their counts
+};
+hipError_t launch_records(Control* ctl, const RecordArgs& r, hipEvent_t stop, hipStream_t s);
 // stop (if not null) is recorded by the kernel's own completion, not by a
 // separate queue packet.
 hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipEvent_t stop,

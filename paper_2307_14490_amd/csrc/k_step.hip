@@ -599,10 +599,10 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
 }
 
 // After the fused step, in one launch:
-//   loss:   the last workgroup sums the fused step's per-workgroup
-//           partials in a fixed order and takes no records, so the sum runs
-//           beside them (no cross-workgroup step: a device-scope fence per
-//           workgroup, to pass partial sums between them, measured slower);
+//   loss:   workgroup 0 sums the fused step's per-workgroup partials in a
+//           fixed order and takes no records, so the sum runs beside them
+//           (no cross-workgroup step: a device-scope fence per workgroup,
+//           to pass partial sums between them, measured slower);
 //   short runs ({start, len <= kShortRun, key}): one thread group each
 //           loads the row with its contributions, sums them in occurrence
 //           order and updates the row;
@@ -614,7 +614,8 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
 //           a device-scope release by the storing wave; an acquire before
 //           the partials are read) adds the partials in piece order and
 //           updates the row once.
-// The record counts were set by the grouping of this batch.
+// The records come gathered into one list per kind, with their counts, by
+// k_records before the step (below).
 // Exclusive sum of one value per thread over the workgroup; *total receives
 // the sum.  Synchronises; s_tmp (kBlock / 64 words) may be reused after the
 // next barrier.
@@ -649,14 +650,92 @@ __device__ __forceinline__ int record_bucket(const uint32_t* prefix, int bins, u
     return lo;
 }
 
+// The grouping leaves bucket b's short runs at [bstart[b] / kShortDiv, ...)
+// of `shorts` and its pieces at [bstart[b] / kPieceDiv, ...) of `pieces`
+// (counts in bcount[b]); this copies both, in bucket order, into one list
+// each and writes their counts, so that no finish workgroup has a per-bucket
+// step of its own.  It runs on the preparation stream after the grouping
+// (its completion marks the batch prepared).  Every workgroup forms the
+// buckets' prefix sums in LDS (kMaxBins / kBlock buckets per thread), then
+// the grid copies the records.
+__global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_records(Control* __restrict__ ctl,
+                                                                 RecordArgs r) {
+    __shared__ uint32_t s_ps[kMaxBins], s_pp[kMaxBins], s_bs[kMaxBins];
+    __shared__ uint32_t s_tmp[2][kBlock / 64];
+    if (ctl->step_bad) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) r.rcount[0] = r.rcount[1] = 0u;
+        return;
+    }
+    constexpr int kBpt = kMaxBins / kBlock;
+    uint4 bc[kBpt];
+    uint32_t bs[kBpt];
+    uint32_t cs = 0, cp = 0;
+#pragma unroll
+    for (int j = 0; j < kBpt; ++j) {
+        const int b = threadIdx.x * kBpt + j;
+        bc[j] = b < r.bins ? r.bcount[b] : make_uint4(0u, 0u, 0u, 0u);
+        bs[j] = b < r.bins ? r.bstart[b] : 0u;
+        cs += bc[j].x;
+        cp += bc[j].y;
+    }
+    uint32_t ns, np;
+    uint32_t xs = block_excl_sum(cs, s_tmp[0], &ns);
+    uint32_t xp = block_excl_sum(cp, s_tmp[1], &np);
+#pragma unroll
+    for (int j = 0; j < kBpt; ++j) {
+        const int b = threadIdx.x * kBpt + j;
+        if (b < r.bins) {
+            s_ps[b] = xs;
+            s_pp[b] = xp;
+            s_bs[b] = bs[j];
+            xs += bc[j].x;
+            xp += bc[j].y;
+        }
+    }
+    __syncthreads();
+    // the regions of all buckets lie inside the lists, so the totals fit
+    // them; the clamp keeps a broken invariant from writing past them
+    if (ns > r.caps.shorts || np > r.caps.pieces) {
+        if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
+        ns = ns < r.caps.shorts ? ns : r.caps.shorts;
+        np = np < r.caps.pieces ? np : r.caps.pieces;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        r.rcount[0] = ns;
+        r.rcount[1] = np;
+    }
+    const uint32_t step = gridDim.x * kBlock;
+    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ns; i += step) {
+        const int b = record_bucket(s_ps, r.bins, i);
+        const uint32_t idx = s_bs[b] / kShortDiv + (i - s_ps[b]);
+        // cannot happen (the regions hold every bucket); a zero record is
+        // one the finish kernel rejects
+        if (idx >= r.caps.shorts) raise_internal(ctl, kSiteFinishComb);
+        r.cshorts[i] = idx < r.caps.shorts ? r.shorts[idx] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < np; i += step) {
+        const int b = record_bucket(s_pp, r.bins, i);
+        const uint32_t idx = s_bs[b] / kPieceDiv + (i - s_pp[b]);
+        if (idx >= r.caps.pieces) raise_internal(ctl, kSiteFinishComb);
+        r.cpieces[i] = idx < r.caps.pieces ? r.pieces[idx] : make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+constexpr int kRecordBlocks = 64;  // workgroups of k_records
+
+hipError_t launch_records(Control* ctl, const RecordArgs& r, hipEvent_t stop, hipStream_t s) {
+    if (r.bins < 1 || r.bins > kMaxBins) return hipErrorInvalidValue;
+    hipExtLaunchKernelGGL(k_records, dim3(kRecordBlocks), dim3(kBlock), 0, s, nullptr, stop, 0,
+                          ctl, r);
+    return hipGetLastError();
+}
+
 template <int G, int C, typename E>
 __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restrict__ ctl,
                                                    FinishArgs f) {
     constexpr int PPB = kBlock / G;
     __shared__ double s_part[1024 * C];  // PPB x D doubles: D <= 4 G C
     __shared__ double s_red[kBlock];
-    __shared__ uint32_t s_ps[kMaxBins], s_pp[kMaxBins], s_bs[kMaxBins];
-    __shared__ uint32_t s_tmp[2][kBlock / 64];
     __shared__ uint32_t s_flag;
     if (ctl->step_bad) {
         if (blockIdx.x == 0 && threadIdx.x == 0 && f.loss_out != nullptr)
@@ -667,70 +746,43 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
     const int lane = threadIdx.x % G;
     const int32_t D = t.D;
 
-    // The last workgroup sums the loss and nothing else: thread t adds
-    // partials t, t + kBlock, ... in that order (32 loads in flight), then
-    // the threads' sums meet in a fixed tree: the same double on every run.
-    if (blockIdx.x == gridDim.x - 1) {
+    // Workgroup 0 (dispatched first) sums the loss and nothing else: thread t
+    // adds partial pairs t, t + kBlock, ... in that order (16-byte loads, 32
+    // in flight), then the threads' sums meet in a fixed tree: the same
+    // double on every run.
+    if (blockIdx.x == 0) {
         if (f.loss_out == nullptr) return;
+        const double2* p2 = reinterpret_cast<const double2*>(f.lossp);
+        const int64_t n2 = f.loss_blocks / 2;
         double acc = 0.0;
         int64_t j = threadIdx.x;
-        for (; j + 31 * kBlock < f.loss_blocks; j += 32 * kBlock) {
-            double v[32];
+        for (; j + 31 * kBlock < n2; j += 32 * kBlock) {
+            double2 v[32];
 #pragma unroll
-            for (int q = 0; q < 32; ++q) v[q] = f.lossp[j + q * kBlock];
+            for (int q = 0; q < 32; ++q) v[q] = p2[j + q * kBlock];
 #pragma unroll
-            for (int q = 0; q < 32; ++q) acc += v[q];
+            for (int q = 0; q < 32; ++q) {
+                acc += v[q].x;
+                acc += v[q].y;
+            }
         }
-        for (; j < f.loss_blocks; j += kBlock) acc += f.lossp[j];
+        for (; j < n2; j += kBlock) {
+            const double2 v = p2[j];
+            acc += v.x;
+            acc += v.y;
+        }
+        if (threadIdx.x == 0 && (f.loss_blocks & 1)) acc += f.lossp[f.loss_blocks - 1];
         acc = block_sum_fixed(acc, s_red);
         if (threadIdx.x == 0) *f.loss_out = acc;
         return;
     }
-    // the other workgroups take the records
+    // the other workgroups take the records, gathered before the step
+    if (f.m == 0) return;
+    const uint32_t ns = f.rcount[0], np = f.rcount[1];
     const uint32_t rec_groups = gridDim.x - 1u;
-
-    // Bucket b wrote its records to its own regions of the lists; record r
-    // of all short runs (pieces) in bucket order is record r - prefix[b] of
-    // bucket b's region.  Every workgroup takes the prefixes of the bucket
-    // counts into LDS (kMaxBins / kBlock buckets per thread).
-    constexpr int kBpt = kMaxBins / kBlock;
-    uint4 bc[kBpt];
-    uint32_t bs[kBpt];
-    uint32_t cs = 0, cp = 0;
-#pragma unroll
-    for (int j = 0; j < kBpt; ++j) {
-        const int b = threadIdx.x * kBpt + j;
-        bc[j] = b < f.bins ? f.bcount[b] : make_uint4(0u, 0u, 0u, 0u);
-        bs[j] = b < f.bins ? f.bstart[b] : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < kBpt; ++j) {
-        cs += bc[j].x;
-        cp += bc[j].y;
-    }
-    uint32_t ns, np;
-    uint32_t xs = block_excl_sum(cs, s_tmp[0], &ns);
-    uint32_t xp = block_excl_sum(cp, s_tmp[1], &np);
-#pragma unroll
-    for (int j = 0; j < kBpt; ++j) {
-        const int b = threadIdx.x * kBpt + j;
-        if (b < f.bins) {
-            s_ps[b] = xs;
-            s_pp[b] = xp;
-            s_bs[b] = bs[j];
-            xs += bc[j].x;
-            xp += bc[j].y;
-        }
-    }
-    __syncthreads();
-    for (uint32_t r = blockIdx.x * PPB + grp; r < ns; r += rec_groups * PPB) {
-        const int b = record_bucket(s_ps, f.bins, r);
-        const uint32_t idx = s_bs[b] / kShortDiv + (r - s_ps[b]);
-        if (idx >= f.caps.shorts) {  // cannot happen: the regions hold every bucket
-            if (lane == 0) raise_internal(ctl, kSiteFinishComb);
-            continue;
-        }
-        const uint4 rec = f.shorts[idx];
+    const uint32_t wg = blockIdx.x - 1u;
+    for (uint32_t r = wg * PPB + grp; r < ns; r += rec_groups * PPB) {
+        const uint4 rec = f.cshorts[r];
         // a record is used only if it lies inside this batch (the grouping
         // writes only such records; the check keeps a broken invariant from
         // reaching memory outside the buffers)
@@ -749,14 +801,8 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
         sgd_row<C>(cur, acc, f.lr);
         RowIO<G, C, E>::store(base, row, D, lane, cur);
     }
-    for (uint32_t r = blockIdx.x; r < np; r += rec_groups) {
-        const int b = record_bucket(s_pp, f.bins, r);
-        const uint32_t idx = s_bs[b] / kPieceDiv + (r - s_pp[b]);
-        if (idx >= f.caps.pieces) {  // uniform; cannot happen
-            if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
-            continue;
-        }
-        const uint4 rec = f.pieces[idx];  // the same for every thread
+    for (uint32_t r = wg; r < np; r += rec_groups) {
+        const uint4 rec = f.cpieces[r];  // the same for every thread
         if (rec.y == 0u || rec.y > kPiece || (int64_t)rec.x + rec.y > f.m ||
             (int64_t)rec.z >= 2 * t.N) {  // uniform; cannot happen
             if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
@@ -796,7 +842,9 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
 hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipEvent_t stop,
                          hipStream_t s) {
     const RowShape rs = row_shape(t.D);
-    const int64_t grid = 1024;
+    // workgroup 0 sums the loss; the other 2047 take the gathered records
+    // (1024 workgroups measured 1 us slower per step at SBM-100M)
+    const int64_t grid = 2048;
     HUGE_ROW_DISPATCH(rs, {
         HUGE_ELEM_DISPATCH(t.dtype, {
             hipExtLaunchKernelGGL((k_finish<G_, C_, E_>), dim3((unsigned)grid), dim3(kBlock), 0, s,
