@@ -178,9 +178,6 @@ Layout make_layout(const huge_config* c) {
             S.ccount = take(sizeof(uint32_t) * (size_t)caps.combs);
             S.bcount = take(sizeof(uint4) * kMaxBins);
             S.wstats = take(sizeof(uint32_t) * kMaxBins * 3);
-            S.cshorts = take(sizeof(uint4) * (size_t)caps.shorts);
-            S.cpieces = take(sizeof(uint4) * (size_t)caps.pieces);
-            S.rcount = take(sizeof(uint32_t) * 2);
         }
     }
     L.eval_ctrl = take(sizeof(Control));
@@ -409,37 +406,20 @@ huge_status stage_prepare(huge_handle* h, const int32_t* src, const int32_t* dst
                                   at<uint32_t>(h, SL.tprefix), at<uint32_t>(h, SL.bstart), s));
         if (!prof_mark(h, b, 3, s) || !prof_mark(h, b, 4, s)) return HUGE_ERR_HIP;
         const ListCaps caps{L.cap_short, L.cap_piece, L.cap_comb, L.cap_part};
-        bool grouped = false;
         HIP_TRY(launch_group(ctl, at<uint32_t>(h, SL.keys1), at<uint32_t>(h, SL.vals1), m,
                              h->cfg.num_nodes, hist, at<uint32_t>(h, SL.bstart),
                              at<int32_t>(h, SL.info), at<uint4>(h, SL.shorts),
                              at<uint4>(h, SL.pieces), at<uint4>(h, SL.combs),
                              at<uint32_t>(h, SL.ccount), at<uint4>(h, SL.bcount), caps,
-                             at<uint32_t>(h, SL.wstats), 1 << bits, h->key_bits, nullptr,
-                             &grouped, s));
-        if (grouped) {
-            // the records gathered for the finish kernel; its completion
-            // records `ready` (no packet of its own)
-            RecordArgs R;
-            R.bstart = at<uint32_t>(h, SL.bstart);
-            R.bcount = at<uint4>(h, SL.bcount);
-            R.bins = 1 << bits;
-            R.shorts = at<uint4>(h, SL.shorts);
-            R.pieces = at<uint4>(h, SL.pieces);
-            R.caps = caps;
-            R.cshorts = at<uint4>(h, SL.cshorts);
-            R.cpieces = at<uint4>(h, SL.cpieces);
-            R.rcount = at<uint32_t>(h, SL.rcount);
-            HIP_TRY(launch_records(ctl, R, h->ready[slot], s));
-            ready_recorded = true;
-        }
+                             at<uint32_t>(h, SL.wstats), 1 << bits, h->key_bits,
+                             h->ready[slot], &ready_recorded, s));
         if (!prof_mark(h, b, 5, s)) return HUGE_ERR_HIP;
     } else {
         // the atomic scatter needs no grouping
         for (int k = 1; k <= 5; ++k)
             if (!prof_mark(h, b, k, s)) return HUGE_ERR_HIP;
     }
-    // the records kernel's completion records `ready` (no packet of its own)
+    // the grouping kernel's completion records `ready` (no packet of its own)
     if (!ready_recorded) HIP_TRY(hipEventRecord(h->ready[slot], s));
     h->pending[slot] = b;
     h->prepared += 1;
@@ -488,12 +468,10 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
                                   at<int32_t>(h, SL.info), at<float>(h, L.dup), lossp, &blocks,
                                   ev_start, ev_stop, s));
         FinishArgs f;
-        // an empty batch is not grouped: its slot's record counts are not
-        // this batch's, so none is read (f.m = 0)
+        // an empty batch is not grouped: no record is read (f.m = 0)
         f.m = m;
-        f.cshorts = at<uint4>(h, SL.cshorts);
-        f.cpieces = at<uint4>(h, SL.cpieces);
-        f.rcount = at<uint32_t>(h, SL.rcount);
+        f.shorts = at<uint4>(h, SL.shorts);
+        f.pieces = at<uint4>(h, SL.pieces);
         f.combs = at<uint4>(h, SL.combs);
         f.ccount = at<uint32_t>(h, SL.ccount);
         f.dup = at<float>(h, L.dup);

@@ -86,7 +86,9 @@ struct Control {
     uint32_t step_bad;               // this call's input is invalid: skip all writes
     uint32_t error;                  // first error since huge_check (kBadId/kBadCount)
     uint32_t site;                   // first failed internal check (a kSite* code)
-    uint32_t pad[13];
+    uint32_t nshort;                 // short-run records of the batch (its grouping's)
+    uint32_t npiece;                 // its pieces
+    uint32_t pad[11];
 };
 
 // Internal checks (kBadInternal), recorded in Control::site.
@@ -123,19 +125,17 @@ struct SlotLayout {
     size_t tcount = 0;   // u32 [sort_tiles * kMaxBins] occurrences per tile and digit
     size_t tprefix = 0;  // u32 [sort_tiles * kMaxBins] the same summed over earlier tiles
     size_t bstart = 0;   // u32 [kMaxBins] first position of each bucket
-    // repeated-row records; bucket b (first position s0, n items) writes its
-    // records at [s0 / 2, ...), [s0 / 16, ...), [s0 / 256, ...) of these
-    // (ListCaps says why they fit) and their counts to bcount[b]
+    // repeated-row records: short runs and pieces in one list each (a range
+    // of the grouping appends at positions reserved from Control::nshort,
+    // ::npiece); bucket b (first position s0, n items) writes its combine
+    // records at [s0 / 256, ...) and partial slots from s0 / 128 (ListCaps
+    // says why they fit) and its counts to bcount[b]
     size_t shorts = 0;   // uint4 [cap_short] {start, len, key, 0}
     size_t pieces = 0;   // uint4 [cap_piece] {start, len, key, 0 or combine record index + 1}
     size_t combs = 0;    // uint4 [cap_comb] {key, first partial, partials, first slot}
     size_t ccount = 0;   // u32 [cap_comb] pieces of the row summed so far
     size_t bcount = 0;   // uint4 [kMaxBins] {short runs, pieces, combines, 0} per bucket
     size_t wstats = 0;   // u32 [kMaxBins * 3] distinct S, distinct T, repeated occurrences
-    // the same records gathered in bucket order (k_records), and their counts
-    size_t cshorts = 0;  // uint4 [cap_short]
-    size_t cpieces = 0;  // uint4 [cap_piece]
-    size_t rcount = 0;   // u32 [2] short runs, pieces
 };
 
 constexpr int kSlots = 3;  // groupings in flight: applied, next, and one more being sampled;
@@ -326,9 +326,8 @@ hipError_t launch_fused_step(const TableArgs& t, Control* ctl, const StepArgs& a
 // output, the loss sum (the fused step's partials in a fixed order).
 struct FinishArgs {
     int64_t m;               // occurrences of the batch (0: no records)
-    const uint4* cshorts;    // the batch's short-run records, gathered (k_records)
-    const uint4* cpieces;    // its pieces, gathered
-    const uint32_t* rcount;  // how many of each
+    const uint4* shorts;     // its short-run records (Control::nshort of them)
+    const uint4* pieces;     // its pieces (Control::npiece)
     const uint4* combs;
     uint32_t* ccount;
     const float* dup;
@@ -339,20 +338,6 @@ struct FinishArgs {
     int64_t loss_blocks;   // how many
     double* loss_out;      // or null: no loss
 };
-// The records of a grouped batch gathered into one list per kind (before its
-// apply, on the preparation stream).
-struct RecordArgs {
-    const uint32_t* bstart;  // first position of each bucket
-    const uint4* bcount;     // records per bucket
-    int bins;                // buckets of the batch
-    const uint4* shorts;     // per-bucket regions, as the grouping left them
-    const uint4* pieces;
-    ListCaps caps;
-    uint4* cshorts;          // out: short runs in bucket order
-    uint4* cpieces;          // out: pieces in bucket order
-    uint32_t* rcount;        // out: their counts
-};
-hipError_t launch_records(Control* ctl, const RecordArgs& r, hipEvent_t stop, hipStream_t s);
 // stop (if not null) is recorded by the kernel's own completion, not by a
 // separate queue packet.
 hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipEvent_t stop,

@@ -365,14 +365,15 @@ hipError_t launch_radix_pass(Control* ctl, const uint32_t* keys_in, uint32_t* ke
 //   count:  every item of the range inserts its key and counts it;
 //   emit:   rows counted more than once get consecutive duplicate-buffer
 //           slots (positions of the bucket, after those of earlier ranges),
-//           and a work record in the bucket's own record regions: a short
-//           run, a piece, or pieces plus a combine record for a run longer
-//           than kPiece;
+//           and a work record: a short run or a piece appended to the
+//           batch's lists, or pieces plus a combine record (in the bucket's
+//           own region) for a run longer than kPiece;
 //   place:  the repeated items, taken in occurrence order (chunk by chunk,
 //           compacted, then ranked by one wave 64 at a time), receive their
 //           row's next slot: info[o] = slot.
 // At the end the bucket's record counts go to bcount[b].  No step waits for
-// another workgroup or uses a device-scope atomic.  Where a row's range lands
+// another workgroup; the only device-scope atomics reserve a range's places
+// in the batch's record lists.  Where a row's range lands
 // depends on the order of the hash insertions, the order of its occurrences
 // does not: every sum is taken in occurrence order.  Items that occur once
 // keep info = -1.
@@ -422,6 +423,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     __shared__ uint32_t s_tmp[6][kBlock / 64];
     __shared__ uint32_t s_distinct, s_fail, s_nrep;
     __shared__ uint32_t s_stat[3];
+    __shared__ uint32_t s_rbase[2];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // the first failed internal check of this thread, raised once at the end
@@ -569,9 +571,8 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
     const uint32_t tmax = tsize / 4u * 3u;   // distinct keys a range may hold
     const uint32_t tload = tsize / 8u * 7u;  // table load a count stays below
 
-    // the bucket's record regions and how many records it has written
-    const uint32_t r_short = (uint32_t)(s0 / kShortDiv), c_short = (uint32_t)(n / kShortDiv);
-    const uint32_t r_piece = (uint32_t)(s0 / kPieceDiv), c_piece = (uint32_t)(n / kPieceDiv);
+    // the bucket's record bounds and regions, and how many records it has written
+    const uint32_t c_short = (uint32_t)(n / kShortDiv), c_piece = (uint32_t)(n / kPieceDiv);
     const uint32_t r_comb = (uint32_t)(s0 / kCombDiv), c_comb = (uint32_t)(n / kCombDiv);
     const uint32_t r_part = (uint32_t)(s0 / kPartDiv), c_part = (uint32_t)(n / kPartDiv);
     uint32_t nb_short = 0, nb_piece = 0, nb_comb = 0, nb_part = 0;
@@ -693,14 +694,23 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
         const uint32_t x_part = block_excl(npart, s_tmp[4], &t_part);
         if (nS) atomicAdd(&s_stat[0], nS);
         if (nT) atomicAdd(&s_stat[1], nT);
+        // the range's short runs and pieces are appended to the batch's lists
+        // at positions reserved by one device-scope atomic each (the finish
+        // kernel takes each record alone, so their order is free)
+        if (tid == 0) {
+            s_rbase[0] = t_short ? atomicAdd(&ctl->nshort, t_short) : 0u;
+            s_rbase[1] = t_piece ? atomicAdd(&ctl->npiece, t_piece) : 0u;
+        }
+        __syncthreads();
+        const uint32_t b_short = s_rbase[0], b_piece = s_rbase[1];
         // uniform: every thread has the same totals and bases
         const bool fits = (uint64_t)nb_short + t_short <= c_short &&
                           (uint64_t)nb_piece + t_piece <= c_piece &&
                           (uint64_t)nb_comb + t_comb <= c_comb &&
                           (uint64_t)nb_part + t_part <= c_part &&
                           (uint64_t)rep_base + t_rep <= n &&
-                          (uint64_t)r_short + c_short <= caps.shorts &&
-                          (uint64_t)r_piece + c_piece <= caps.pieces &&
+                          (uint64_t)b_short + t_short <= caps.shorts &&
+                          (uint64_t)b_piece + t_piece <= caps.pieces &&
                           (uint64_t)r_comb + c_comb <= caps.combs &&
                           (uint64_t)r_part + c_part <= caps.parts;
         if (!fits) {  // cannot happen: the regions bound every bucket
@@ -709,7 +719,7 @@ __global__ __launch_bounds__(kBlock) HUGE_BESIDE_72 void k_group(
         }
         {
             uint32_t pos = (uint32_t)s0 + rep_base + x_rep;
-            uint32_t is = r_short + nb_short + x_short, ip = r_piece + nb_piece + x_piece;
+            uint32_t is = b_short + x_short, ip = b_piece + x_piece;
             uint32_t ic = r_comb + nb_comb + x_comb, ia = r_part + nb_part + x_part;
 #pragma unroll 1
             for (uint32_t q = tid; q < tsize; q += kBlock) {

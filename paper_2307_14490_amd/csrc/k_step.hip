@@ -614,8 +614,8 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* s_red) {
 //           a device-scope release by the storing wave; an acquire before
 //           the partials are read) adds the partials in piece order and
 //           updates the row once.
-// The records come gathered into one list per kind, with their counts, by
-// k_records before the step (below).
+// The records come in one list per kind, their counts in Control (the
+// grouping of the batch appended them).
 // Exclusive sum of one value per thread over the workgroup; *total receives
 // the sum.  Synchronises; s_tmp (kBlock / 64 words) may be reused after the
 // next barrier.
@@ -650,85 +650,6 @@ __device__ __forceinline__ int record_bucket(const uint32_t* prefix, int bins, u
     return lo;
 }
 
-// The grouping leaves bucket b's short runs at [bstart[b] / kShortDiv, ...)
-// of `shorts` and its pieces at [bstart[b] / kPieceDiv, ...) of `pieces`
-// (counts in bcount[b]); this copies both, in bucket order, into one list
-// each and writes their counts, so that no finish workgroup has a per-bucket
-// step of its own.  It runs on the preparation stream after the grouping
-// (its completion marks the batch prepared).  Every workgroup forms the
-// buckets' prefix sums in LDS (kMaxBins / kBlock buckets per thread), then
-// the grid copies the records.
-__global__ __launch_bounds__(kBlock) HUGE_BESIDE void k_records(Control* __restrict__ ctl,
-                                                                 RecordArgs r) {
-    __shared__ uint32_t s_ps[kMaxBins], s_pp[kMaxBins], s_bs[kMaxBins];
-    __shared__ uint32_t s_tmp[2][kBlock / 64];
-    if (ctl->step_bad) {
-        if (blockIdx.x == 0 && threadIdx.x == 0) r.rcount[0] = r.rcount[1] = 0u;
-        return;
-    }
-    constexpr int kBpt = kMaxBins / kBlock;
-    uint4 bc[kBpt];
-    uint32_t bs[kBpt];
-    uint32_t cs = 0, cp = 0;
-#pragma unroll
-    for (int j = 0; j < kBpt; ++j) {
-        const int b = threadIdx.x * kBpt + j;
-        bc[j] = b < r.bins ? r.bcount[b] : make_uint4(0u, 0u, 0u, 0u);
-        bs[j] = b < r.bins ? r.bstart[b] : 0u;
-        cs += bc[j].x;
-        cp += bc[j].y;
-    }
-    uint32_t ns, np;
-    uint32_t xs = block_excl_sum(cs, s_tmp[0], &ns);
-    uint32_t xp = block_excl_sum(cp, s_tmp[1], &np);
-#pragma unroll
-    for (int j = 0; j < kBpt; ++j) {
-        const int b = threadIdx.x * kBpt + j;
-        if (b < r.bins) {
-            s_ps[b] = xs;
-            s_pp[b] = xp;
-            s_bs[b] = bs[j];
-            xs += bc[j].x;
-            xp += bc[j].y;
-        }
-    }
-    __syncthreads();
-    // the regions of all buckets lie inside the lists, so the totals fit
-    // them; the clamp keeps a broken invariant from writing past them
-    if (ns > r.caps.shorts || np > r.caps.pieces) {
-        if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
-        ns = ns < r.caps.shorts ? ns : r.caps.shorts;
-        np = np < r.caps.pieces ? np : r.caps.pieces;
-    }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        r.rcount[0] = ns;
-        r.rcount[1] = np;
-    }
-    const uint32_t step = gridDim.x * kBlock;
-    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ns; i += step) {
-        const int b = record_bucket(s_ps, r.bins, i);
-        const uint32_t idx = s_bs[b] / kShortDiv + (i - s_ps[b]);
-        // cannot happen (the regions hold every bucket); a zero record is
-        // one the finish kernel rejects
-        if (idx >= r.caps.shorts) raise_internal(ctl, kSiteFinishComb);
-        r.cshorts[i] = idx < r.caps.shorts ? r.shorts[idx] : make_uint4(0u, 0u, 0u, 0u);
-    }
-    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < np; i += step) {
-        const int b = record_bucket(s_pp, r.bins, i);
-        const uint32_t idx = s_bs[b] / kPieceDiv + (i - s_pp[b]);
-        if (idx >= r.caps.pieces) raise_internal(ctl, kSiteFinishComb);
-        r.cpieces[i] = idx < r.caps.pieces ? r.pieces[idx] : make_uint4(0u, 0u, 0u, 0u);
-    }
-}
-
-constexpr int kRecordBlocks = 64;  // workgroups of k_records
-
-hipError_t launch_records(Control* ctl, const RecordArgs& r, hipEvent_t stop, hipStream_t s) {
-    if (r.bins < 1 || r.bins > kMaxBins) return hipErrorInvalidValue;
-    hipExtLaunchKernelGGL(k_records, dim3(kRecordBlocks), dim3(kBlock), 0, s, nullptr, stop, 0,
-                          ctl, r);
-    return hipGetLastError();
-}
 
 template <int G, int C, typename E>
 __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restrict__ ctl,
@@ -776,13 +697,18 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
         if (threadIdx.x == 0) *f.loss_out = acc;
         return;
     }
-    // the other workgroups take the records, gathered before the step
+    // the other workgroups take the records
     if (f.m == 0) return;
-    const uint32_t ns = f.rcount[0], np = f.rcount[1];
+    uint32_t ns = ctl->nshort, np = ctl->npiece;
+    if (ns > f.caps.shorts || np > f.caps.pieces) {  // cannot happen: the grouping checks
+        if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);
+        ns = ns < f.caps.shorts ? ns : f.caps.shorts;
+        np = np < f.caps.pieces ? np : f.caps.pieces;
+    }
     const uint32_t rec_groups = gridDim.x - 1u;
     const uint32_t wg = blockIdx.x - 1u;
     for (uint32_t r = wg * PPB + grp; r < ns; r += rec_groups * PPB) {
-        const uint4 rec = f.cshorts[r];
+        const uint4 rec = f.shorts[r];
         // a record is used only if it lies inside this batch (the grouping
         // writes only such records; the check keeps a broken invariant from
         // reaching memory outside the buffers)
@@ -802,7 +728,7 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
         RowIO<G, C, E>::store(base, row, D, lane, cur);
     }
     for (uint32_t r = wg; r < np; r += rec_groups) {
-        const uint4 rec = f.cpieces[r];  // the same for every thread
+        const uint4 rec = f.pieces[r];  // the same for every thread
         if (rec.y == 0u || rec.y > kPiece || (int64_t)rec.x + rec.y > f.m ||
             (int64_t)rec.z >= 2 * t.N) {  // uniform; cannot happen
             if (threadIdx.x == 0) raise_internal(ctl, kSiteFinishComb);

@@ -92,7 +92,11 @@ hipError_t launch_get_rows(const TableArgs& t, Control* ctl, int32_t table, cons
 // that the sequence stays valid inside a captured graph).
 // ---------------------------------------------------------------------------
 __global__ HUGE_BESIDE void k_begin(Control* ctl) {
-    if (threadIdx.x == 0) ctl->step_bad = 0u;
+    if (threadIdx.x == 0) {
+        ctl->step_bad = 0u;
+        ctl->nshort = 0u;
+        ctl->npiece = 0u;
+    }
 }
 
 hipError_t launch_begin(Control* ctl, hipStream_t s) {
