@@ -205,6 +205,8 @@ def check_knn(T, queries, k, ids, dist):
     (700, 512, 40, 16, "four dimension chunks"),
     (20, 16, 20, 32, "fewer rows than k: trailing -1"),
     (33, 8, 1, 1, "one query, one neighbour"),
+    (9000, 128, 40, 7, "two query blocks of full-width rows, two threshold scans"),
+    (12000, 128, 20, 12, "one query block of full-width rows, two threshold scans"),
 ])
 def test_knn_and_recall(N, D, nq, k, note):
     rng = np.random.default_rng(N + D + nq)
