@@ -73,15 +73,16 @@ struct huge_handle {
     int last_applied_slot;     // -1 before the first apply
     PendingBatch pending[kSlots];
     hipEvent_t ready[kSlots];    // preparation of the slot's batch complete
-    // Completion of apply done_idx (0-based), recorded on done_stream: an
-    // apply's completion implies that of every earlier one, so one event,
-    // recorded only where a later wait needs it, serves every such wait.
+    // The completions of applies done_idx and done_idx2 (0-based), recorded
+    // on done_stream and done_stream2: an apply's completion implies that of
+    // every earlier one, so two events, recorded only where a later wait
+    // needs one, serve every such wait, each taking the oldest that suffices.
     // Each record costs the recording kernel a signalled completion (a
     // device-wide cache write-back of several microseconds before the next
     // kernel starts).
-    hipEvent_t done_ev = nullptr;
-    int64_t done_idx = -1;
-    hipStream_t done_stream = nullptr;
+    hipEvent_t done_ev = nullptr, done_ev2 = nullptr;
+    int64_t done_idx = -1, done_idx2 = -1;
+    hipStream_t done_stream = nullptr, done_stream2 = nullptr;
     // phase timing
     std::vector<hipEvent_t> prof_ev;
     std::vector<char> prof_applied;
@@ -238,6 +239,7 @@ void destroy_handle(huge_handle* h) {
     for (int s = 0; s < kSlots; ++s)
         if (h->ready[s]) (void)hipEventDestroy(h->ready[s]);
     if (h->done_ev) (void)hipEventDestroy(h->done_ev);
+    if (h->done_ev2) (void)hipEventDestroy(h->done_ev2);
     if (h->side_done) (void)hipEventDestroy(h->side_done);
     delete h;
 }
@@ -270,8 +272,8 @@ huge_status create(const huge_config* cfg, void* S, void* T, const uint32_t* thr
     // the events order streams of this device only: a device-scope release
     // suffices (the default one is system-scope)
     const unsigned flags = hipEventDisableTiming | hipEventReleaseToDevice;
-    for (int s = 0; s < kSlots + 1; ++s) {
-        hipEvent_t* e = s < kSlots ? &h->ready[s] : &h->done_ev;
+    for (int s = 0; s < kSlots + 2; ++s) {
+        hipEvent_t* e = s < kSlots ? &h->ready[s] : s == kSlots ? &h->done_ev : &h->done_ev2;
         if (hipEventCreateWithFlags(e, flags) != hipSuccess) {
             *e = nullptr;
             destroy_handle(h);
@@ -324,15 +326,28 @@ hipError_t wait_on(hipStream_t s, hipEvent_t e, hipStream_t from) {
 // Make s wait until apply i (issued) is complete: nothing on the last apply's
 // stream (it follows every apply), the recorded completion if it covers i,
 // else a completion recorded now after the last apply.
+// Overwrite the older of the two recorded completions with apply idx's.
+hipEvent_t take_done(huge_handle* h, int64_t idx, hipStream_t s) {
+    if (h->done_idx <= h->done_idx2) {
+        h->done_idx = idx;
+        h->done_stream = s;
+        return h->done_ev;
+    }
+    h->done_idx2 = idx;
+    h->done_stream2 = s;
+    return h->done_ev2;
+}
+
 hipError_t wait_applied(huge_handle* h, hipStream_t s, int64_t i) {
     if (i < 0 || s == h->last_apply_stream) return hipSuccess;
-    if (h->done_idx < i) {
-        const hipError_t e = hipEventRecord(h->done_ev, h->last_apply_stream);
-        if (e != hipSuccess) return e;
-        h->done_idx = h->applied - 1;
-        h->done_stream = h->last_apply_stream;
-    }
-    return wait_on(s, h->done_ev, h->done_stream);
+    // the oldest recorded completion that covers i (a later one would hold s back)
+    const bool ok1 = h->done_idx >= i, ok2 = h->done_idx2 >= i;
+    if (ok1 && (!ok2 || h->done_idx <= h->done_idx2)) return wait_on(s, h->done_ev, h->done_stream);
+    if (ok2) return wait_on(s, h->done_ev2, h->done_stream2);
+    hipEvent_t e = take_done(h, h->applied - 1, h->last_apply_stream);
+    const hipError_t r = hipEventRecord(e, h->last_apply_stream);
+    if (r != hipSuccess) return r;
+    return wait_on(s, e, h->last_apply_stream);
 }
 
 // A call outside the step on stream s: ordered after the last apply (it
@@ -448,12 +463,15 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         h->side_pending = false;
     }
     int64_t blocks = 0;
-    // This apply records its completion only if the next preparation would
-    // otherwise find none recent enough (it needs apply prepared - kSlots;
-    // at most kMaxPending batches wait, so this apply is recent enough):
-    // with one preparation issued ahead of each apply that is every other
-    // apply, and the finish kernel's own completion records it.
-    const bool record_done = h->done_idx < h->prepared - kSlots;
+    // This apply records its completion only if the newest recorded one is
+    // older than apply prepared - (kSlots - 1), one later than what the next
+    // preparation needs: with one preparation issued ahead of each apply that
+    // is every other apply, and a preparation then waits for the apply it
+    // needs or the one after it, never a later one.  The finish kernel's own
+    // completion records it.
+    const int64_t newest = h->done_idx > h->done_idx2 ? h->done_idx : h->done_idx2;
+    const bool record_done = newest < h->prepared - (kSlots - 1);
+    hipEvent_t done_e = record_done ? take_done(h, h->applied, s) : nullptr;
     if (h->cfg.scatter_kind == HUGE_SCATTER_SORTED) {
         // the negatives are the sort keys of slots 2 .. K + 1; a profiled
         // step's fused-kernel events (6, 7) are the kernel's own start and
@@ -482,7 +500,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
         f.loss_blocks = blocks;
         f.loss_out = loss_out;
         // the finish kernel's completion records it (no packet of its own)
-        HIP_TRY(launch_finish(t, ctl, f, record_done ? h->done_ev : nullptr, s));
+        HIP_TRY(launch_finish(t, ctl, f, done_e, s));
     } else {
         float* gsrc = at<float>(h, L.gsrc);
         float* coef = at<float>(h, L.coef);
@@ -496,11 +514,7 @@ huge_status apply_next(huge_handle* h, float lr, double* loss_out, hipStream_t s
     }
     if (!prof_mark(h, b, 8, s) || !prof_mark(h, b, 9, s)) return HUGE_ERR_HIP;
     if (record_done && h->cfg.scatter_kind != HUGE_SCATTER_SORTED)
-        HIP_TRY(hipEventRecord(h->done_ev, s));
-    if (record_done) {
-        h->done_idx = h->applied;
-        h->done_stream = s;
-    }
+        HIP_TRY(hipEventRecord(done_e, s));
     if (b.prof >= 0) h->prof_applied[(size_t)b.prof] = 1;
     h->last_apply_stream = s;
     h->last_applied_slot = slot;

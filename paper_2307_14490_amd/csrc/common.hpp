@@ -138,10 +138,12 @@ struct SlotLayout {
     size_t wstats = 0;   // u32 [kMaxBins * 3] distinct S, distinct T, repeated occurrences
 };
 
-constexpr int kSlots = 3;  // groupings in flight: applied, next, and one more being sampled;
-                           // the wait for a slot's previous apply also paces the preparation
-                           // (six slots let it run ahead onto the finish kernel and the step
-                           // slowed from 0.457 to 0.463 ms)
+constexpr int kSlots = 4;  // grouping slots: the applied batch, the next, one being prepared
+                           // and one more, so that a preparation can wait for an apply one
+                           // earlier than the last while completions are recorded every
+                           // other step (the wait paces the preparation: with six slots and
+                           // one completion in five it ran onto the finish kernel and the
+                           // step slowed from 0.457 to 0.463 ms)
 
 struct Layout {
     SlotLayout slot[kSlots];
