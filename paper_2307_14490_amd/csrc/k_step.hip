@@ -768,7 +768,7 @@ __global__ __launch_bounds__(kBlock) void k_finish(TableArgs t, Control* __restr
 hipError_t launch_finish(const TableArgs& t, Control* ctl, const FinishArgs& f, hipEvent_t stop,
                          hipStream_t s) {
     const RowShape rs = row_shape(t.D);
-    // workgroup 0 sums the loss; the other 2047 take the gathered records
+    // workgroup 0 sums the loss; the other 2047 take the repeated-row records
     // (1024 workgroups measured 1 us slower per step at SBM-100M)
     const int64_t grid = 2048;
     HUGE_ROW_DISPATCH(rs, {
