@@ -490,6 +490,52 @@ def test_prepared_steps_with_long_groupings_equal_train_step_bitwise():
     assert losses.cpu().tolist() == ref_losses
 
 
+def test_prepared_steps_in_irregular_orders_equal_train_step_bitwise():
+    """Applies alternate between two streams, preparations run two batches
+    ahead on a third, and side calls (a loss evaluation, a row read) on a
+    fourth come between them.  An apply's completion is recorded only where a
+    wait needs it (by a finish kernel, or on demand): every such wait must
+    hold, so tables, losses and the side calls' results equal those of
+    sequential steps bit for bit."""
+    N, D, K, n, nb = 50_000, 64, 5, 20_000, 9
+    rng = np.random.default_rng(31)
+    batches = [_random_batch(rng, N, n, hub_frac=0.05, cmax=5) for _ in range(nb)]
+    deb = tuple(dev(x, torch) for x in _random_batch(rng, N, 4000))
+    ids = torch.from_numpy(rng.integers(0, N, 500)).to("cuda")  # int64: read as given
+    ref = _trainer(N, D, K, n, seed=6)
+    ref_losses, ref_eval, ref_rows = [], {}, {}
+    for b, (s, d, c) in enumerate(batches):
+        ref_losses.append(ref.step(dev(s, torch), dev(d, torch), dev(c, torch), b * n,
+                                   0.005).item())
+        if b % 3 == 1:
+            ref_eval[b] = ref.eval_loss(*deb, 7).item()
+            ref_rows[b] = ref.get_rows(b % 2, ids).cpu()
+    tr = _trainer(N, D, K, n, seed=6)
+    applies = [torch.cuda.current_stream(), torch.cuda.Stream()]
+    prep, side = torch.cuda.Stream(), torch.cuda.Stream()
+    dbs = [tuple(dev(x, torch) for x in b) for b in batches]
+    losses = torch.zeros(nb, dtype=torch.float64, device="cuda")
+    evals = torch.zeros(nb, dtype=torch.float64, device="cuda")
+    rows = {}
+    tr.prepare(*dbs[0], 0, stream=prep)
+    tr.prepare(*dbs[1], n, stream=prep)
+    for k in range(nb):
+        tr.train_prepared(0.005, loss_out=losses[k:k + 1], stream=applies[k % 2])
+        if k % 3 == 1:
+            tr.eval_loss(*deb, 7, loss_out=evals[k:k + 1], stream=side)
+            rows[k] = tr.get_rows(k % 2, ids, stream=side)
+        if k + 2 < nb:
+            tr.prepare(*dbs[k + 2], (k + 2) * n, stream=prep)
+    torch.cuda.synchronize()
+    assert tr.check() == 0
+    assert bool(torch.isfinite(tr.S).all()) and bool(torch.isfinite(tr.T).all())
+    assert torch.equal(tr.S, ref.S) and torch.equal(tr.T, ref.T)
+    assert losses.cpu().tolist() == ref_losses
+    for k in ref_eval:
+        assert evals[k].item() == ref_eval[k]
+        assert torch.equal(rows[k].cpu(), ref_rows[k])
+
+
 def test_prepared_call_order_is_checked_on_host():
     tr = _trainer(100, 16, 3, 64)
     rng = np.random.default_rng(3)
