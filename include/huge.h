@@ -172,7 +172,8 @@ huge_status huge_train_step(huge_handle* h, const int32_t* d_src, const int32_t*
    preparation stream of their own they run beside the previous batch's
    update.  The library orders the halves with HIP events: an apply waits for
    its batch's preparation and for the previous apply, a preparation for the
-   apply that last used its grouping buffers.  The batch arrays must stay
+   apply that last used its grouping buffers (or the one after it: apply
+   completions are recorded only every other step).  The batch arrays must stay
    valid until the batch is applied.  Results are bitwise those of
    huge_train_step, which is the two halves on one stream and requires that
    no batch is pending. */
