@@ -448,7 +448,7 @@ def bench_eval(args):
         "roofline": {"kernel": "k_knn_scan<4, true>", "bound": "hbm", "achieved": table_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": table_gbps / HBM_PEAK_GBPS,
                      "traffic": None,
-                     "note": f"the whole search (three sample scans over 1.6% of the tiles, the "
+                     "note": f"the whole search (three sample scans over 3.2% of the tiles, the "
                              f"full scan, four selections) against one read of the "
                              f"{NB * DB * 4 / 1e9:.1f} GB table: "
                              f"{NB * DB * 4 / HBM_PEAK_GBPS / 1e6:.1f} ms at the HBM peak; the "

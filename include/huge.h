@@ -415,7 +415,7 @@ huge_status huge_eval_summary_static(const float* d_dist, int64_t n_edge, int64_
    dim <= 512.  Queries are processed in passes of up to
    128 (dim <= 128), 64 (dim <= 256) or 32 over the table.  For dim <= 128
    a pass is a series of threshold scans: strided samples of the row tiles,
-   each 64 times denser than the one before, then every tile; a sample's
+   each 32 times denser than the one before, then every tile; a sample's
    k-th distance bounds the next scan's candidates per query, which are
    sorted between scans.  Should more than 8192 rows of the last scan fall
    within a query's bound (many rows at one distance), the pass is computed

@@ -60,7 +60,7 @@ constexpr int kKnnScanWaves = 4;        // waves of a scan workgroup (two workgr
 constexpr int kKnnScanGrid = 512;       // scan workgroups, at most
 constexpr int kKnnCandCap = 8192;       // candidate keys kept per query and scan
 constexpr int kKnnStageTiles = 256;     // row tiles of the first (coarsest) scan, at most
-constexpr int kKnnStageGrowth = 64;     // tile stride of a scan over that of the next
+constexpr int kKnnStageGrowth = 32;     // tile stride of a scan over that of the next
 constexpr int kKnnSelectThreads = 1024; // threads of a candidate selection workgroup
 constexpr uint32_t kShortRun = 32;     // repeated rows with at most this many occurrences are
                                        // summed by one thread group

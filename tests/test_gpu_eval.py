@@ -287,7 +287,7 @@ def test_knn_falls_back_to_the_list_search_when_a_candidate_list_overflows():
 
 
 def test_knn_threshold_scans_at_a_million_rows():
-    """1e6 x 128 rows, 100 queries, k = 10: three threshold scans (8, 489 and
+    """1e6 x 128 rows, 100 queries, k = 10: three threshold scans (31, 977 and
     31,250 tiles of 32 rows).  Bit for bit the list search's answer; the
     first 4 queries against exact double distances."""
     N, D, k, nq = 1_000_000, 128, 10, 100
