@@ -207,6 +207,7 @@ def check_knn(T, queries, k, ids, dist):
     (33, 8, 1, 1, "one query, one neighbour"),
     (9000, 128, 40, 7, "two query blocks of full-width rows, two threshold scans"),
     (12000, 128, 20, 12, "one query block of full-width rows, two threshold scans"),
+    (300000, 64, 33, 32, "k = 32 over three threshold scans, half-width rows, two blocks"),
 ])
 def test_knn_and_recall(N, D, nq, k, note):
     rng = np.random.default_rng(N + D + nq)
@@ -261,17 +262,20 @@ def test_recall_on_an_embedding_that_reconstructs_the_graph():
     assert np.all(r4 == 0.5)
 
 
-def test_knn_falls_back_to_the_list_search_when_a_candidate_list_overflows():
+@pytest.mark.parametrize("n_others", [99, 20])
+def test_knn_falls_back_to_the_list_search_when_a_candidate_list_overflows(n_others):
     """18,000 copies of row 5 lie at one distance from query 5, so its last
     threshold scan keeps more candidates than a list holds (8192): that pass is
-    computed again by the list search.  Its answer for the other queries equals
-    both searches' answer without query 5, bit for bit, and query 5's k nearest
-    are the copies with the smallest ids."""
+    computed again by the list search (four query blocks with 99 other
+    queries, one with 20).  Its answer for the other queries equals both
+    searches' answer without query 5, bit for bit, and query 5's k nearest are
+    the copies with the smallest ids."""
     N, D, k = 30000, 128, 10
     rng = np.random.default_rng(77)
     T = rng.normal(size=(N, D)).astype(np.float32)
     T[12000:] = T[5]
-    others = np.setdiff1d(rng.choice(12000, 120, replace=False), [5])[:99].astype(np.int32)
+    others = np.setdiff1d(rng.choice(12000, 120, replace=False), [5])[:n_others]
+    others = others.astype(np.int32)
     with_5 = np.concatenate([[5], others]).astype(np.int32)
     say(f"knn overflow N={N} D={D} k={k} queries={with_5.size}")
     ev = P.Evaluator(N, D, 8, k=k)
